@@ -1,0 +1,385 @@
+/*
+ * conduit.h -- C ABI of the MI355X experience-path library (libconduit.so).
+ *
+ * The experience path is the per-iteration work between actors and learners
+ * that the Conduit paper calls experience ingestion and experience delivery
+ * (Sec. 2.2, "Experience Path Responsibilities"; Sec. 4, "Experience Data
+ * Plane"):
+ *   - off-policy ingestion inserts transitions into a persistent replay dataset
+ *     and maintains the indices and metadata used for sampling and eviction;
+ *   - off-policy delivery samples from that dataset, materialises the chosen
+ *     transitions and applies batch/layout transforms (stacking, reshaping);
+ *   - on-policy ingestion computes returns/advantages over trajectories;
+ *   - on-policy delivery partitions a rollout into shuffled minibatches;
+ *   - replay priorities are updated through algorithm callbacks (App. C,
+ *     Invariant 2), and staging never changes contents (App. C, Invariant 1).
+ * The mathematics of these operations is the one of the works the paper cites
+ * for them: proportional prioritised replay (Schaul et al.), generalised
+ * advantage estimation as used by PPO (Schulman et al.), the DQN frame stack
+ * (Mnih et al.).  Where those leave a choice open, the choice made here is
+ * stated at the entry point.
+ *
+ * Conventions for every entry point:
+ *   - Pointers documented as "device" point to HIP device memory of the GPU
+ *     that is current when the call is made (e.g. torch CUDA tensors);
+ *     "host" pointers point to ordinary host memory.  The caller owns every
+ *     input and output buffer; the library owns only what a buffer allocates
+ *     (or the arena the caller hands it, see conduit_buffer_create).
+ *   - `stream` is a hipStream_t (NULL: the default stream).  Calls enqueue their
+ *     kernels and return; outputs are valid in stream order.  A buffer is not
+ *     thread-safe: serialise calls on one stream or order streams with events.
+ *   - Every call returns a conduit_status.  Argument errors are detected on the
+ *     host before anything is enqueued and leave all state unchanged.  Errors a
+ *     kernel finds in device-resident arguments (an index out of range, an empty
+ *     priority tree, a sequence longer than the slot) are recorded in a sticky
+ *     flag: the kernel never touches memory out of bounds (the offending element
+ *     is skipped or written as zeros), and the first call that starts after the
+ *     kernel has finished returns CONDUIT_ESTATE until the flag is cleared.
+ *     conduit_sync_check() waits for a stream and reports the flag.
+ *   - conduit_last_error() returns a thread-local message for the last failure.
+ */
+#ifndef CONDUIT_H
+#define CONDUIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t conduit_status;
+#define CONDUIT_OK 0
+#define CONDUIT_EINVAL (-1)  /* bad argument (detected on the host) */
+#define CONDUIT_ENOMEM (-2)  /* device or pinned-host allocation failed */
+#define CONDUIT_EEMPTY (-3)  /* sample from a buffer holding no transitions */
+#define CONDUIT_EDEVICE (-4) /* a HIP runtime call failed (text in conduit_last_error) */
+#define CONDUIT_ESTATE (-5)  /* a kernel flagged bad device-side input earlier */
+
+typedef enum {
+    CONDUIT_U8 = 0,
+    CONDUIT_I32 = 1,
+    CONDUIT_F32 = 2,
+    CONDUIT_BF16 = 3,
+} conduit_dtype;
+
+typedef struct conduit_buffer conduit_buffer;
+
+/* ---------------------------------------------------------------------------
+ * Buffer options.  Fill with conduit_buffer_opts_default() and override.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    /* 1: keep per-slot priorities and the sum tree (prioritised replay).
+     * 0: no priorities (on-policy rollouts, uniform replay by caller indices). */
+    int32_t prioritized;
+    /* alpha = alpha_num / alpha_den, 0 <= alpha_num <= alpha_den <= 8.
+     * Default 3/5 (alpha = 0.6). */
+    int32_t alpha_num;
+    int32_t alpha_den;
+    /* importance-sampling exponent beta >= 0.  Default 0.4. */
+    double beta;
+    /* observations per sample returned by gather (frame stacking), 1..16.
+     * K > 1 needs episode_id and step on every ingest.  Default 1. */
+    int32_t frame_stack;
+    /* bytes of one action (any layout; copied verbatim), 0..256.  Default 4. */
+    int32_t action_bytes;
+    /* 1: observations are variable-length sequences: obs_shape = {max_len},
+     * obs_dtype a 4-byte type, and each slot may also hold aux_elem_bytes per
+     * element (e.g. a float log-probability).  Default 0. */
+    int32_t ragged;
+    /* ragged: bytes of the auxiliary per-element value, 0 or 4.  Default 0. */
+    int32_t aux_elem_bytes;
+} conduit_buffer_opts;
+
+void conduit_buffer_opts_default(conduit_buffer_opts* opts);
+
+/* ---------------------------------------------------------------------------
+ * Buffer lifecycle
+ * ------------------------------------------------------------------------- */
+/*
+ * Bytes of device memory a buffer with these parameters needs (all columns,
+ * the priority tree and small state), rounded to 256-byte alignment.
+ * Returns 0 for invalid parameters.  Host-only; allocates nothing.
+ */
+size_t conduit_buffer_required_bytes(int64_t capacity, const int64_t* obs_shape, int32_t ndim,
+                                     conduit_dtype obs_dtype, const conduit_buffer_opts* opts);
+
+/*
+ * Create the persistent replay dataset of Sec. 2.2 ("inserts transitions into a
+ * persistent replay dataset and maintains indices and metadata"): an HBM ring
+ * of `capacity` slots, each holding one observation of shape obs_shape[0..ndim)
+ * and type obs_dtype (row-major), an action, a reward, a done flag, an episode
+ * id and a step index, and (prioritized) a quantised priority leaf of a 64-ary
+ * sum tree.
+ *   capacity   1 .. 2^31-1 slots.
+ *   obs_shape  host array of ndim >= 1 positive sizes.
+ *   opts       host pointer or NULL (defaults).
+ *   arena      NULL: the library allocates the memory (hipMalloc) and frees it in
+ *              conduit_buffer_destroy.  Otherwise device memory of at least
+ *              conduit_buffer_required_bytes() bytes, 256-byte aligned, owned by
+ *              the caller and kept alive until destroy.
+ *   out        host pointer receiving the handle.
+ * The buffer is bound to the device current at creation.  Slots start empty;
+ * every tree node and leaf starts at 0; the running maximum priority starts at 1.
+ * Errors: EINVAL (bad sizes/options, arena too small or misaligned), ENOMEM,
+ * EDEVICE.  Synchronous.
+ */
+conduit_status conduit_buffer_create(int64_t capacity, const int64_t* obs_shape, int32_t ndim,
+                                     conduit_dtype obs_dtype, const conduit_buffer_opts* opts,
+                                     void* arena, size_t arena_bytes, conduit_buffer** out);
+
+/* Wait for the device and free what the buffer allocated.  NULL is a no-op. */
+void conduit_buffer_destroy(conduit_buffer* buf);
+
+/* ---------------------------------------------------------------------------
+ * Ingestion (Sec. 2.2 off-policy ingestion; Sec. 4.1)
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    int64_t n;                   /* transitions in this call, 0 .. capacity */
+    /* dense: device [n, row] observations, row = prod(obs_shape) * dtype size.
+     * ragged: device concatenated elements of the n sequences. */
+    const void* obs;
+    const int64_t* offsets;      /* ragged: device [n+1] element offsets, offsets[0] = 0 */
+    const void* aux;             /* ragged, aux_elem_bytes > 0: device concatenated aux elements */
+    const void* action;          /* device [n, action_bytes] or NULL (zeros) */
+    const float* reward;         /* device [n] or NULL (zeros) */
+    const uint8_t* done;         /* device [n] or NULL (zeros) */
+    const uint32_t* episode_id;  /* device [n] or NULL; required when frame_stack > 1 */
+    const int32_t* step;         /* device [n] step index within the episode (>= 0) or NULL;
+                                    required when frame_stack > 1 */
+    const uint32_t* prio;        /* device [n] priorities or NULL: the running maximum */
+} conduit_transitions;
+
+/*
+ * Insert transitions j = 0..n-1 into slots (head + j) mod capacity, evicting the
+ * oldest transitions once the ring is full.  Then head = (head + n) mod capacity,
+ * size = min(size + n, capacity).  With priorities, slot j's leaf becomes
+ * L(prio[j]) and the running maximum absorbs prio[j]; without them, every new
+ * transition gets L(running maximum) ("new transitions at maximal priority",
+ * Schaul et al.).  L(p) = floor(2^F * p^alpha) computed exactly in integers,
+ * F = min(31, floor(32 (1 - alpha))) (see conduit_update_priorities).  The sum
+ * tree is brought up to date before any later call in stream order.
+ * Ragged rows longer than max_len are flagged (CONDUIT_ESTATE later) and stored
+ * truncated.  Observation pointers must be 4-byte aligned.
+ * Errors: EINVAL (n < 0 or n > capacity, missing required pointer), ESTATE.
+ */
+conduit_status conduit_ingest(conduit_buffer* buf, const conduit_transitions* t, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Priority callback (App. C, Invariant 2: priorities updated by algorithm
+ * callbacks; proportional prioritisation of Schaul et al.)
+ * ------------------------------------------------------------------------- */
+/*
+ * Set the priority of slots idx[k] to prio[k] for k = 0..n-1 (device int64 and
+ * uint32 arrays).  A repeated index takes its LAST occurrence (array order), as
+ * if the updates ran one after another.  The stored leaf is the exact integer
+ *     L(p) = floor(2^F * p^(alpha_num/alpha_den)),  F = min(31, floor(32(1-alpha)))
+ * (F = 12 for alpha = 0.6), so every leaf is below 2^32, the tree root below
+ * 2^63, and the sampling probability of a slot is its leaf over the root.
+ * L(0) = 0: a zero priority is never sampled.  The running maximum priority
+ * absorbs every applied prio[k].  Indices outside [0, size) are skipped and
+ * flagged.  Deterministic: integer tree arithmetic, no float atomics.
+ * Errors: EINVAL (n < 0, NULL arrays with n > 0, buffer not prioritized), ESTATE.
+ */
+conduit_status conduit_update_priorities(conduit_buffer* buf, const int64_t* idx, const uint32_t* prio,
+                                         int64_t n, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Sampling (Sec. 2.2 off-policy delivery: "samples from a persistent replay
+ * dataset"; proportional prioritised replay)
+ * ------------------------------------------------------------------------- */
+/*
+ * Draw `batch` slots by stratified inverse-CDF sampling over the sum tree.
+ * With Q the root (sum of leaves) and u_k = uniforms[k] (device uint64, caller
+ * supplied, uniform on [0, 2^64)), stratum k's target is
+ *     t_k = floor((k + u_k / 2^64) * Q / batch)
+ * evaluated exactly in integers, and idx_out[k] is the first slot whose
+ * inclusive prefix sum of leaves exceeds t_k.  is_w_out[k] is the importance
+ * weight (N P(i))^-beta normalised by the largest weight in the batch, i.e.
+ * (q_min / q_i)^beta with q_min the smallest sampled leaf, computed in fp64 and
+ * rounded to fp32 (the largest weight is exactly 1).
+ *   uniforms  device uint64 [batch]
+ *   idx_out   device int64 [batch]
+ *   is_w_out  device float [batch] or NULL
+ * A tree whose root is 0 (all priorities 0) is flagged, and idx_out = -1,
+ * is_w_out = 0 are written.
+ * Errors: EINVAL (batch < 1 or > 2^20, NULL pointers, not prioritized),
+ * EEMPTY (size == 0), ESTATE.
+ */
+conduit_status conduit_sample(conduit_buffer* buf, int64_t batch, const uint64_t* uniforms, int64_t* idx_out,
+                              float* is_w_out, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Gather / transform (Sec. 2.2 off-policy delivery: "materializes the selected
+ * transitions, and performs batch/layout transformations"; processing
+ * operators concat/stack, reshape, batching, padding/packing)
+ * ------------------------------------------------------------------------- */
+typedef enum {
+    CONDUIT_XF_NONE = 0,        /* copy observation bytes unchanged */
+    CONDUIT_XF_U8_F32 = 1,      /* uint8 x -> float x/255 (the float nearest to x/255) */
+    CONDUIT_XF_U8_BF16_NORM = 2,/* uint8 x -> bf16(((x/255) - mean_c) / std_c), c = plane */
+    CONDUIT_XF_TOKENS_PAD = 3,  /* ragged: right-pad sequences to max_len with pad_id */
+} conduit_xform_kind;
+
+typedef struct {
+    conduit_xform_kind kind;
+    int32_t channels;  /* U8_BF16_NORM: planes per observation (1..4); the row is
+                          split into `channels` equal planes */
+    float mean[4];     /* U8_BF16_NORM: per-plane mean */
+    float std[4];      /* U8_BF16_NORM: per-plane std (non-zero) */
+    int32_t pad_id;    /* TOKENS_PAD: value written past the sequence end */
+} conduit_transform;
+
+typedef struct {
+    /* dense: device [n, K, row_elems] of the transform's output type (uint8 /
+     * obs dtype for NONE, float for U8_F32, bf16 bits for U8_BF16_NORM), K =
+     * frame_stack, oldest frame first.  ragged: [n, max_len] sequence elements. */
+    void* obs;
+    void* action;      /* device [n, action_bytes] or NULL */
+    float* reward;     /* device [n] or NULL */
+    uint8_t* done;     /* device [n] or NULL */
+    uint8_t* mask;     /* ragged: device [n, max_len], 1 where t < length, or NULL */
+    void* aux;         /* ragged: device [n, max_len] aux elements (0 past the end) or NULL */
+    int32_t* length;   /* ragged: device [n] sequence lengths or NULL */
+} conduit_learner_batch;
+
+/*
+ * Materialise the learner batch for slots idx[0..n) (device int64), typically the
+ * output of conduit_sample.
+ * Frame stacking (frame_stack K > 1, the DQN input of Mnih et al.): frame k of
+ * sample b is the observation d = K-1-k steps before slot i = idx[b] in the same
+ * episode, read from slot j = (i - d) mod capacity when that slot holds
+ * (episode_id[i], step[i] - d); otherwise the frame is written as zeros (the
+ * stack does not reach across an episode start, into an overwritten slot or an
+ * unwritten one).
+ * Pixel transforms are exact: U8_F32 writes the float nearest to x/255;
+ * U8_BF16_NORM writes bf16_rne(fl(fl(fl(x/255) - mean_c) / std_c)) with every fl
+ * one IEEE single operation rounded to nearest even.
+ * Ragged (TOKENS_PAD): obs[b, t] = sequence element t for t < length, pad_id
+ * after; aux likewise with 0; mask[b, t] = (t < length).
+ * Scalar columns come from slot i.  Indices outside [0, size) are flagged and
+ * their rows written as zeros.  Output pointers must be 16-byte aligned.
+ * Errors: EINVAL (transform not valid for the buffer's dtype/layout, NULL
+ * pointers), ESTATE.
+ */
+conduit_status conduit_gather_transform(conduit_buffer* buf, const int64_t* idx, int64_t n,
+                                        const conduit_transform* xf, const conduit_learner_batch* out,
+                                        void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Returns / advantages (Sec. 2.2 on-policy ingestion "computing
+ * returns/advantages"; GAE as used by PPO, Schulman et al.)
+ * ------------------------------------------------------------------------- */
+/*
+ * Generalised advantage estimation over a time-major rollout of T steps and E
+ * environments (element (t, e) at t*E + e, all device arrays):
+ *     delta_t = r_t + gamma (1 - d_t) V_{t+1} - V_t
+ *     A_t     = delta_t + gamma lambda (1 - d_t) A_{t+1},   A_T = 0
+ *     ret_t   = A_t + V_t
+ * d_t = 1 means transition t ended its episode (nothing is bootstrapped through
+ * it); V_T = bootstrap[e].  rewards float [T,E]; values float [T,E] or NULL (0);
+ * dones uint8 [T,E]; bootstrap float [E] or NULL (0); adv, ret float [T,E]
+ * outputs.  Arithmetic in fp64 inside, fp32 out.
+ * Errors: EINVAL (T, E < 0, NULL required pointers), ESTATE.
+ */
+conduit_status conduit_gae(const float* rewards, const float* values, const uint8_t* dones,
+                           const float* bootstrap, int64_t T, int64_t E, double gamma, double lambda,
+                           float* adv, float* ret, void* stream);
+
+/*
+ * GAE over B right-padded sequences of up to Lmax elements (LLM post-training
+ * shape; the paper's Verl mapping puts advantage computation in ingestion,
+ * App. A / Table "Verl map"): sequence b of length L = lengths[b] receives the
+ * scalar last_reward[b] on element L-1, which also ends it; all other rewards
+ * are 0.  values: device float [B, Lmax] or NULL (0).  adv, ret: device float
+ * [B, Lmax]; positions t >= L are written as 0.  fp64 inside.
+ * Lengths outside [0, Lmax] are flagged and clamped.
+ * Errors: EINVAL, ESTATE.
+ */
+conduit_status conduit_gae_packed(const float* last_reward, const int32_t* lengths, const float* values,
+                                  int64_t B, int64_t Lmax, double gamma, double lambda, float* adv,
+                                  float* ret, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Minibatch shuffle-gather (Sec. 2.2 on-policy delivery: "partitioning
+ * trajectories into mini-batches and ... shuffling"; App. C Invariant 2)
+ * ------------------------------------------------------------------------- */
+/*
+ * out row m = transform(src row perm[m]) for m = 0..n-1, plus up to 8 scalar
+ * float columns: cols_out[c][m] = cols[c][perm[m]].
+ *   src       device [n_src, row_bytes] (e.g. a rollout in flat order t*E + e),
+ *             4-byte aligned, row_bytes a multiple of 4
+ *   perm      device int64 [n]
+ *   xf        NONE, U8_F32 or U8_BF16_NORM (as in conduit_gather_transform)
+ *   out       device [n, row_bytes * out_size], 16-byte aligned
+ *   cols, cols_out  host arrays of ncols device float pointers (may be NULL if
+ *             ncols == 0)
+ * Entries of perm outside [0, n_src) are flagged and their rows zeroed.
+ * Errors: EINVAL, ESTATE.
+ */
+conduit_status conduit_minibatch_gather(const void* src, int64_t row_bytes, int64_t n_src, const int64_t* perm,
+                                        int64_t n, const conduit_transform* xf, void* out,
+                                        const float* const* cols, float* const* cols_out, int32_t ncols,
+                                        void* stream);
+
+/* ---------------------------------------------------------------------------
+ * State, introspection, errors
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    int64_t capacity;
+    int64_t row_bytes;        /* bytes of one stored observation */
+    int64_t head;             /* next slot to write */
+    int64_t size;             /* stored transitions */
+    int64_t total;            /* transitions ever ingested */
+    int32_t tree_depth;       /* root level (leaves are level 0) */
+    int64_t tree_nodes[8];    /* nodes per level 0..tree_depth (level 0 = capacity) */
+    int64_t arena_bytes;
+} conduit_buffer_info;
+
+/* Host-side state of the buffer; no device synchronisation. */
+conduit_status conduit_buffer_get_info(const conduit_buffer* buf, conduit_buffer_info* info);
+
+typedef enum {
+    CONDUIT_COL_OBS = 0,      /* [capacity, row_bytes] bytes */
+    CONDUIT_COL_ACTION = 1,   /* [capacity, action_bytes] */
+    CONDUIT_COL_REWARD = 2,   /* float [capacity] */
+    CONDUIT_COL_DONE = 3,     /* uint8 [capacity] */
+    CONDUIT_COL_EPISODE = 4,  /* uint32 [capacity] */
+    CONDUIT_COL_STEP = 5,     /* int32 [capacity], -1 in unwritten slots */
+    CONDUIT_COL_LENGTH = 6,   /* ragged: int32 [capacity] */
+    CONDUIT_COL_AUX = 7,      /* ragged: [capacity, max_len * aux_elem_bytes] */
+    CONDUIT_COL_LEAVES = 8,   /* uint32 [tree_nodes[0]] quantised priorities */
+    CONDUIT_COL_TREE = 9,     /* uint64 [tree_nodes[level]] sums, level 1..tree_depth */
+    CONDUIT_COL_MAX_PRIO = 10,/* uint32 [1] running maximum priority */
+} conduit_column;
+
+/*
+ * Copy `nbytes` bytes starting `offset` bytes into a column (level selects the
+ * tree level for CONDUIT_COL_TREE) into device memory `dst`, in stream order.
+ * Errors: EINVAL (unknown column, range outside the column).
+ */
+conduit_status conduit_buffer_read(const conduit_buffer* buf, conduit_column col, int32_t level, int64_t offset,
+                                   int64_t nbytes, void* dst, void* stream);
+
+/*
+ * Wait for `stream`, then report the sticky device-side error flag of `buf`
+ * (NULL: the flag shared by the stand-alone calls conduit_gae,
+ * conduit_gae_packed and conduit_minibatch_gather).  Returns OK or ESTATE (with
+ * a description in conduit_last_error), or EDEVICE.
+ */
+conduit_status conduit_sync_check(const conduit_buffer* buf, void* stream);
+
+/* Clear the sticky device-side error flag of `buf` (NULL: the stand-alone flag). */
+void conduit_clear_error(conduit_buffer* buf);
+
+/* Thread-local description of the last failed call ("" if none). */
+const char* conduit_last_error(void);
+
+/* Library version string. */
+const char* conduit_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONDUIT_H */

@@ -1,0 +1,329 @@
+"""Thin Python binding of libconduit's C ABI (include/conduit.h).
+
+Argument marshalling only: every function forwards torch tensor pointers and the
+current HIP stream to the C entry point of the same name; every step of the
+experience path runs in the library's HIP kernels.  There is no CPU fallback:
+if ``libconduit.so`` is missing, loading it raises.
+"""
+import ctypes as C
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libconduit.so")
+_lib = None
+
+# status codes
+OK, EINVAL, ENOMEM, EEMPTY, EDEVICE, ESTATE = 0, -1, -2, -3, -4, -5
+_STATUS_NAMES = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", EEMPTY: "EEMPTY", EDEVICE: "EDEVICE", ESTATE: "ESTATE"}
+
+# dtypes, transforms, columns
+U8, I32, F32, BF16 = 0, 1, 2, 3
+XF_NONE, XF_U8_F32, XF_U8_BF16_NORM, XF_TOKENS_PAD = 0, 1, 2, 3
+(COL_OBS, COL_ACTION, COL_REWARD, COL_DONE, COL_EPISODE, COL_STEP, COL_LENGTH, COL_AUX, COL_LEAVES, COL_TREE,
+ COL_MAX_PRIO) = range(11)
+
+_TORCH_DTYPE = {torch.uint8: U8, torch.int32: I32, torch.float32: F32, torch.bfloat16: BF16}
+
+
+class ConduitError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{_STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+class BufferOpts(C.Structure):
+    _fields_ = [("prioritized", C.c_int32), ("alpha_num", C.c_int32), ("alpha_den", C.c_int32),
+                ("beta", C.c_double), ("frame_stack", C.c_int32), ("action_bytes", C.c_int32),
+                ("ragged", C.c_int32), ("aux_elem_bytes", C.c_int32)]
+
+
+class Transitions(C.Structure):
+    _fields_ = [("n", C.c_int64), ("obs", C.c_void_p), ("offsets", C.c_void_p), ("aux", C.c_void_p),
+                ("action", C.c_void_p), ("reward", C.c_void_p), ("done", C.c_void_p),
+                ("episode_id", C.c_void_p), ("step", C.c_void_p), ("prio", C.c_void_p)]
+
+
+class Transform(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("channels", C.c_int32), ("mean", C.c_float * 4), ("std", C.c_float * 4),
+                ("pad_id", C.c_int32)]
+
+
+class LearnerBatch(C.Structure):
+    _fields_ = [("obs", C.c_void_p), ("action", C.c_void_p), ("reward", C.c_void_p), ("done", C.c_void_p),
+                ("mask", C.c_void_p), ("aux", C.c_void_p), ("length", C.c_void_p)]
+
+
+class BufferInfo(C.Structure):
+    _fields_ = [("capacity", C.c_int64), ("row_bytes", C.c_int64), ("head", C.c_int64), ("size", C.c_int64),
+                ("total", C.c_int64), ("tree_depth", C.c_int32), ("tree_nodes", C.c_int64 * 8),
+                ("arena_bytes", C.c_int64)]
+
+
+# every symbol include/conduit.h declares, with its ctypes signature
+P = C.c_void_p
+I64 = C.c_int64
+I32_ = C.c_int32
+F64 = C.c_double
+ST = C.c_int32
+SIGNATURES = {
+    "conduit_buffer_opts_default": (None, [P]),
+    "conduit_buffer_required_bytes": (C.c_size_t, [I64, P, I32_, I32_, P]),
+    "conduit_buffer_create": (ST, [I64, P, I32_, I32_, P, P, C.c_size_t, P]),
+    "conduit_buffer_destroy": (None, [P]),
+    "conduit_ingest": (ST, [P, P, P]),
+    "conduit_update_priorities": (ST, [P, P, P, I64, P]),
+    "conduit_sample": (ST, [P, I64, P, P, P, P]),
+    "conduit_gather_transform": (ST, [P, P, I64, P, P, P]),
+    "conduit_gae": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
+    "conduit_gae_packed": (ST, [P, P, P, I64, I64, F64, F64, P, P, P]),
+    "conduit_minibatch_gather": (ST, [P, I64, I64, P, I64, P, P, P, P, I32_, P]),
+    "conduit_buffer_get_info": (ST, [P, P]),
+    "conduit_buffer_read": (ST, [P, I32_, I32_, I64, I64, P, P]),
+    "conduit_sync_check": (ST, [P, P]),
+    "conduit_clear_error": (None, [P]),
+    "conduit_last_error": (C.c_char_p, []),
+    "conduit_version": (C.c_char_p, []),
+}
+
+
+def lib():
+    """Load libconduit.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built: run `python -c 'import __graft_entry__ as g; g.build()'`")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def last_error():
+    return lib().conduit_last_error().decode()
+
+
+def _check(status):
+    if status != OK:
+        raise ConduitError(status, last_error())
+
+
+def _stream(stream):
+    if stream is None:
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return C.c_void_p(stream.cuda_stream)
+    return C.c_void_p(int(stream))
+
+
+def _ptr(t, dtype=None, name="tensor"):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a HIP device")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def transform(kind=XF_NONE, mean=None, std=None, pad_id=0):
+    xf = Transform()
+    xf.kind = kind
+    xf.pad_id = int(pad_id)
+    if mean is not None:
+        xf.channels = len(mean)
+        for c in range(len(mean)):
+            xf.mean[c] = float(mean[c])
+            xf.std[c] = float(std[c])
+    else:
+        xf.channels = 1
+        for c in range(4):
+            xf.std[c] = 1.0
+    return xf
+
+
+def default_opts(**kw):
+    o = BufferOpts()
+    lib().conduit_buffer_opts_default(C.byref(o))
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+def conduit_buffer_required_bytes(capacity, obs_shape, obs_dtype, opts=None):
+    shape = (C.c_int64 * len(obs_shape))(*obs_shape)
+    return int(lib().conduit_buffer_required_bytes(capacity, shape, len(obs_shape), obs_dtype,
+                                                   C.byref(opts) if opts is not None else None))
+
+
+def conduit_buffer_create(capacity, obs_shape, obs_dtype, opts=None, arena=None):
+    """Returns an opaque handle (int).  ``arena``: optional uint8 CUDA tensor."""
+    shape = (C.c_int64 * len(obs_shape))(*obs_shape)
+    out = C.c_void_p()
+    ap = _ptr(arena, torch.uint8, "arena") if arena is not None else None
+    ab = arena.numel() if arena is not None else 0
+    _check(lib().conduit_buffer_create(capacity, shape, len(obs_shape), obs_dtype,
+                                       C.byref(opts) if opts is not None else None, ap, ab, C.byref(out)))
+    return out.value
+
+
+def conduit_buffer_destroy(handle):
+    lib().conduit_buffer_destroy(handle)
+
+
+def conduit_ingest(handle, n, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None,
+                   offsets=None, aux=None, stream=None):
+    t = Transitions()
+    t.n = int(n)
+    t.obs = _ptr(obs, None, "obs")
+    t.offsets = _ptr(offsets, torch.int64, "offsets")
+    t.aux = _ptr(aux, None, "aux")
+    t.action = _ptr(action, None, "action")
+    t.reward = _ptr(reward, torch.float32, "reward")
+    t.done = _ptr(done, torch.uint8, "done")
+    t.episode_id = _ptr(episode_id, None, "episode_id")  # uint32 ids (int32 view accepted)
+    t.step = _ptr(step, torch.int32, "step")
+    t.prio = _ptr(prio, None, "prio")
+    _check(lib().conduit_ingest(handle, C.byref(t), _stream(stream)))
+
+
+def conduit_update_priorities(handle, idx, prio, stream=None):
+    n = idx.numel()
+    if prio.numel() != n:
+        raise ValueError("idx and prio must have the same length")
+    _check(lib().conduit_update_priorities(handle, _ptr(idx, torch.int64, "idx"), _ptr(prio, None, "prio"), n,
+                                           _stream(stream)))
+
+
+def conduit_sample(handle, batch, uniforms, idx_out, is_w_out=None, stream=None):
+    if uniforms.numel() < batch or idx_out.numel() < batch or (is_w_out is not None and is_w_out.numel() < batch):
+        raise ValueError("uniforms/outputs smaller than batch")
+    _check(lib().conduit_sample(handle, batch, _ptr(uniforms, None, "uniforms"), _ptr(idx_out, torch.int64, "idx_out"),
+                                _ptr(is_w_out, torch.float32, "is_w_out"), _stream(stream)))
+
+
+def conduit_gather_transform(handle, idx, xf, obs=None, action=None, reward=None, done=None, mask=None, aux=None,
+                             length=None, stream=None):
+    out = LearnerBatch()
+    out.obs = _ptr(obs, None, "obs")
+    out.action = _ptr(action, None, "action")
+    out.reward = _ptr(reward, torch.float32, "reward")
+    out.done = _ptr(done, torch.uint8, "done")
+    out.mask = _ptr(mask, None, "mask")
+    out.aux = _ptr(aux, None, "aux")
+    out.length = _ptr(length, torch.int32, "length")
+    _check(lib().conduit_gather_transform(handle, _ptr(idx, torch.int64, "idx"), idx.numel(), C.byref(xf),
+                                          C.byref(out), _stream(stream)))
+
+
+def conduit_gae(rewards, values, dones, bootstrap, gamma, lam, adv, ret, stream=None):
+    T, E = rewards.shape
+    _check(lib().conduit_gae(_ptr(rewards, torch.float32, "rewards"), _ptr(values, torch.float32, "values"),
+                             _ptr(dones, torch.uint8, "dones"), _ptr(bootstrap, torch.float32, "bootstrap"), T, E,
+                             float(gamma), float(lam), _ptr(adv, torch.float32, "adv"),
+                             _ptr(ret, torch.float32, "ret"), _stream(stream)))
+
+
+def conduit_gae_packed(last_reward, lengths, values, Lmax, gamma, lam, adv, ret, stream=None):
+    B = last_reward.numel()
+    _check(lib().conduit_gae_packed(_ptr(last_reward, torch.float32, "last_reward"),
+                                    _ptr(lengths, torch.int32, "lengths"), _ptr(values, torch.float32, "values"), B,
+                                    int(Lmax), float(gamma), float(lam), _ptr(adv, torch.float32, "adv"),
+                                    _ptr(ret, torch.float32, "ret"), _stream(stream)))
+
+
+def conduit_minibatch_gather(src, row_bytes, n_src, perm, xf, out, cols=(), cols_out=(), stream=None):
+    ncols = len(cols)
+    ca = (C.c_void_p * max(1, ncols))(*[_ptr(c, torch.float32, "col") for c in cols])
+    co = (C.c_void_p * max(1, ncols))(*[_ptr(c, torch.float32, "col_out") for c in cols_out])
+    _check(lib().conduit_minibatch_gather(_ptr(src, None, "src"), int(row_bytes), int(n_src),
+                                          _ptr(perm, torch.int64, "perm"), perm.numel(), C.byref(xf),
+                                          _ptr(out, None, "out"), ca if ncols else None, co if ncols else None,
+                                          ncols, _stream(stream)))
+
+
+def conduit_buffer_get_info(handle):
+    info = BufferInfo()
+    _check(lib().conduit_buffer_get_info(handle, C.byref(info)))
+    return info
+
+
+def conduit_buffer_read(handle, col, dst, offset=0, level=0, stream=None):
+    _check(lib().conduit_buffer_read(handle, col, level, int(offset), dst.numel() * dst.element_size(),
+                                     _ptr(dst, None, "dst"), _stream(stream)))
+
+
+def conduit_sync_check(handle=None, stream=None):
+    return lib().conduit_sync_check(handle, _stream(stream))
+
+
+def conduit_clear_error(handle=None):
+    lib().conduit_clear_error(handle)
+
+
+def conduit_version():
+    return lib().conduit_version().decode()
+
+
+class ReplayBuffer:
+    """Owning wrapper around a conduit_buffer handle."""
+
+    def __init__(self, capacity, obs_shape, obs_dtype=torch.uint8, prioritized=True, alpha=(3, 5), beta=0.4,
+                 frame_stack=1, action_bytes=4, ragged=False, aux_elem_bytes=0, arena=None):
+        self.opts = default_opts(prioritized=int(prioritized), alpha_num=alpha[0], alpha_den=alpha[1], beta=beta,
+                                 frame_stack=frame_stack, action_bytes=action_bytes, ragged=int(ragged),
+                                 aux_elem_bytes=aux_elem_bytes)
+        self.capacity = capacity
+        self.obs_shape = tuple(obs_shape)
+        self.obs_dtype = obs_dtype
+        self._arena = arena
+        self.handle = conduit_buffer_create(capacity, self.obs_shape, _TORCH_DTYPE[obs_dtype], self.opts, arena)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            conduit_buffer_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def info(self):
+        return conduit_buffer_get_info(self.handle)
+
+    def ingest(self, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None, offsets=None,
+               aux=None, n=None, stream=None):
+        n = (offsets.numel() - 1 if offsets is not None else obs.shape[0]) if n is None else n
+        conduit_ingest(self.handle, n, obs, action, reward, done, episode_id, step, prio, offsets, aux, stream)
+
+    def update(self, idx, prio, stream=None):
+        conduit_update_priorities(self.handle, idx, prio, stream)
+
+    def sample(self, uniforms, idx_out=None, w_out=None, stream=None):
+        B = uniforms.numel()
+        dev = uniforms.device
+        idx_out = torch.empty(B, dtype=torch.int64, device=dev) if idx_out is None else idx_out
+        w_out = torch.empty(B, dtype=torch.float32, device=dev) if w_out is None else w_out
+        conduit_sample(self.handle, B, uniforms, idx_out, w_out, stream)
+        return idx_out, w_out
+
+    def gather(self, idx, xf, **outs):
+        conduit_gather_transform(self.handle, idx, xf, stream=outs.pop("stream", None), **outs)
+
+    def read(self, col, dst, offset=0, level=0, stream=None):
+        conduit_buffer_read(self.handle, col, dst, offset, level, stream)
+
+    def sync_check(self, stream=None):
+        return conduit_sync_check(self.handle, stream)
+
+    def clear_error(self):
+        conduit_clear_error(self.handle)

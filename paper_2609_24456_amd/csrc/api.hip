@@ -1,0 +1,714 @@
+// Host side of the C ABI declared in include/conduit.h: argument validation,
+// buffer layout in HBM, host-known ring state, sticky device error flags, and
+// kernel launches on the caller's stream.
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "common.h"
+
+using namespace conduit;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+conduit_status fail(conduit_status s, const std::string& msg) {
+    g_last_error = msg;
+    return s;
+}
+
+conduit_status hip_fail(hipError_t e, const char* what) {
+    return fail(CONDUIT_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------------------
+// Sticky error words.  One page of pinned, device-visible host memory holds
+// kErrKinds words per slot; slot 0 serves the stand-alone calls.  Kernels store
+// a 1 into the word of the error kind they hit.  The page is never freed (a
+// kernel still in flight may write it), so it lives for the process.
+// ---------------------------------------------------------------------------
+constexpr int kErrSlots = 512;
+std::mutex g_err_mu;
+uint32_t* g_err_host = nullptr;  // host view
+uint32_t* g_err_dev = nullptr;   // device view of the same page
+bool g_slot_used[kErrSlots];
+
+conduit_status err_page() {
+    if (g_err_host) return CONDUIT_OK;
+    void* p = nullptr;
+    hipError_t e = hipHostMalloc(&p, sizeof(uint32_t) * kErrKinds * kErrSlots, hipHostMallocMapped);
+    if (e != hipSuccess) return hip_fail(e, "hipHostMalloc(error flags)");
+    void* d = nullptr;
+    e = hipHostGetDevicePointer(&d, p, 0);
+    if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer(error flags)");
+    std::memset(p, 0, sizeof(uint32_t) * kErrKinds * kErrSlots);
+    g_err_host = static_cast<uint32_t*>(p);
+    g_err_dev = static_cast<uint32_t*>(d);
+    g_slot_used[0] = true;
+    return CONDUIT_OK;
+}
+
+conduit_status err_slot_acquire(int* slot) {
+    std::lock_guard<std::mutex> lk(g_err_mu);
+    conduit_status s = err_page();
+    if (s != CONDUIT_OK) return s;
+    for (int i = 1; i < kErrSlots; ++i) {
+        if (!g_slot_used[i]) {
+            g_slot_used[i] = true;
+            std::memset(g_err_host + i * kErrKinds, 0, sizeof(uint32_t) * kErrKinds);
+            *slot = i;
+            return CONDUIT_OK;
+        }
+    }
+    return fail(CONDUIT_ENOMEM, "too many live buffers (error-flag slots exhausted)");
+}
+
+void err_slot_release(int slot) {
+    std::lock_guard<std::mutex> lk(g_err_mu);
+    if (slot > 0 && slot < kErrSlots) g_slot_used[slot] = false;
+}
+
+const char* kErrText[kErrKinds] = {
+    "priority update index outside [0, size)",
+    "gather index outside [0, size)",
+    "sample from a tree whose total priority is 0",
+    "sequence length outside [0, max_len]",
+    "permutation entry outside [0, n_src)",
+    "leaf quantiser exactness check failed",
+    "sum-tree descent found no child",
+    "",
+};
+
+// Returns ESTATE if any flag of `slot` is set (no synchronisation).
+conduit_status check_flags(int slot) {
+    if (!g_err_host) return CONDUIT_OK;
+    volatile uint32_t* w = g_err_host + slot * kErrKinds;
+    std::string msg;
+    for (int k = 0; k < kErrKinds; ++k) {
+        if (w[k]) {
+            if (!msg.empty()) msg += "; ";
+            msg += kErrText[k];
+        }
+    }
+    if (msg.empty()) return CONDUIT_OK;
+    return fail(CONDUIT_ESTATE, "device-side error flagged earlier: " + msg);
+}
+
+uint32_t* err_words(int slot) { return g_err_dev + slot * kErrKinds; }
+
+// Stand-alone calls: make sure the flag page exists, then report slot 0.
+conduit_status standalone_flags() {
+    {
+        std::lock_guard<std::mutex> lk(g_err_mu);
+        conduit_status st = err_page();
+        if (st != CONDUIT_OK) return st;
+    }
+    return check_flags(0);
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+        if (prev != dev) (void)hipSetDevice(dev);
+    }
+    ~DeviceGuard() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int64_t round64(int64_t x) { return (x + 63) / 64 * 64; }
+
+int dtype_size(conduit_dtype d) {
+    switch (d) {
+        case CONDUIT_U8: return 1;
+        case CONDUIT_I32: return 4;
+        case CONDUIT_F32: return 4;
+        case CONDUIT_BF16: return 2;
+    }
+    return 0;
+}
+
+// Everything create() needs, derived from the parameters.
+struct Layout {
+    int64_t row_bytes = 0, max_len = 0;
+    int depth = 0;
+    int64_t nodes[kMaxLevels + 1] = {};
+    size_t off_state = 0, off_obs = 0, off_aux = 0, off_action = 0, off_reward = 0, off_done = 0;
+    size_t off_episode = 0, off_step = 0, off_length = 0, off_leaves = 0, off_level[kMaxLevels + 1] = {};
+    size_t total = 0;
+};
+
+conduit_status make_layout(int64_t capacity, const int64_t* shape, int32_t ndim, conduit_dtype dt,
+                           const conduit_buffer_opts& o, Layout* L) {
+    if (capacity < 1 || capacity > 0x7fffffffLL) return fail(CONDUIT_EINVAL, "capacity must be in [1, 2^31-1]");
+    if (!shape || ndim < 1 || ndim > 8) return fail(CONDUIT_EINVAL, "obs_shape must have 1..8 dimensions");
+    const int es = dtype_size(dt);
+    if (es == 0) return fail(CONDUIT_EINVAL, "unknown obs dtype");
+    int64_t elems = 1;
+    for (int i = 0; i < ndim; ++i) {
+        if (shape[i] < 1 || shape[i] > (1LL << 31)) return fail(CONDUIT_EINVAL, "obs_shape entries must be positive");
+        elems *= shape[i];
+        if (elems > (1LL << 34)) return fail(CONDUIT_EINVAL, "observation too large");
+    }
+    L->row_bytes = elems * es;
+    if (L->row_bytes % 4 != 0) return fail(CONDUIT_EINVAL, "observation size must be a multiple of 4 bytes");
+    if (o.alpha_den < 1 || o.alpha_den > 8 || o.alpha_num < 0 || o.alpha_num > o.alpha_den)
+        return fail(CONDUIT_EINVAL, "alpha must be alpha_num/alpha_den with 0 <= num <= den <= 8");
+    if (!(o.beta >= 0.0) || o.beta > 1e6) return fail(CONDUIT_EINVAL, "beta must be a finite value >= 0");
+    if (o.frame_stack < 1 || o.frame_stack > 16) return fail(CONDUIT_EINVAL, "frame_stack must be in [1, 16]");
+    if (o.frame_stack > capacity) return fail(CONDUIT_EINVAL, "frame_stack larger than capacity");
+    if (o.action_bytes < 0 || o.action_bytes > 256) return fail(CONDUIT_EINVAL, "action_bytes must be in [0, 256]");
+    if (o.prioritized != 0 && o.prioritized != 1) return fail(CONDUIT_EINVAL, "prioritized must be 0 or 1");
+    if (o.ragged) {
+        if (ndim != 1 || es != 4) return fail(CONDUIT_EINVAL, "ragged buffers need obs_shape {max_len} of a 4-byte type");
+        if (shape[0] % 4 != 0) return fail(CONDUIT_EINVAL, "ragged max_len must be a multiple of 4");
+        if (o.aux_elem_bytes != 0 && o.aux_elem_bytes != 4) return fail(CONDUIT_EINVAL, "aux_elem_bytes must be 0 or 4");
+        if (o.frame_stack != 1) return fail(CONDUIT_EINVAL, "ragged buffers do not stack frames");
+        L->max_len = shape[0];
+    } else if (o.aux_elem_bytes != 0) {
+        return fail(CONDUIT_EINVAL, "aux_elem_bytes needs a ragged buffer");
+    }
+    // tree shape
+    L->nodes[0] = capacity;
+    int d = 0;
+    do {
+        ++d;
+        L->nodes[d] = (L->nodes[d - 1] + kFanout - 1) / kFanout;
+    } while (L->nodes[d] > 1);
+    L->depth = d;
+    // arena layout
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t at = off;
+        off += align_up(bytes);
+        return at;
+    };
+    const size_t C = (size_t)capacity;
+    L->off_state = take(sizeof(DeviceState));
+    L->off_obs = take(C * (size_t)L->row_bytes);
+    L->off_aux = o.ragged && o.aux_elem_bytes ? take(C * (size_t)L->max_len * (size_t)o.aux_elem_bytes) : 0;
+    L->off_action = o.action_bytes ? take(C * (size_t)o.action_bytes) : 0;
+    L->off_reward = take(C * 4);
+    L->off_done = take(C);
+    L->off_episode = take(C * 4);
+    L->off_step = take(C * 4);
+    L->off_length = o.ragged ? take(C * 4) : 0;
+    if (o.prioritized) {
+        L->off_leaves = take((size_t)round64(capacity) * 4);
+        for (int l = 1; l <= d; ++l) L->off_level[l] = take((size_t)round64(L->nodes[l]) * 8);
+    }
+    L->total = off;
+    return CONDUIT_OK;
+}
+
+}  // namespace
+
+struct conduit_buffer {
+    int device = 0;
+    int64_t capacity = 0;
+    conduit_dtype obs_dtype = CONDUIT_U8;
+    conduit_buffer_opts opts{};
+    Layout layout;
+    uint8_t* arena = nullptr;
+    bool owns_arena = false;
+    uint8_t* obs = nullptr;
+    uint8_t* aux = nullptr;
+    uint8_t* action = nullptr;
+    float* reward = nullptr;
+    uint8_t* done = nullptr;
+    uint32_t* episode = nullptr;
+    int32_t* step = nullptr;
+    int32_t* length = nullptr;
+    DeviceState* state = nullptr;
+    TreeView tree{};
+    int err_slot = -1;
+    int64_t head = 0, size = 0, total = 0;
+};
+
+extern "C" {
+
+void conduit_buffer_opts_default(conduit_buffer_opts* o) {
+    if (!o) return;
+    o->prioritized = 1;
+    o->alpha_num = 3;
+    o->alpha_den = 5;
+    o->beta = 0.4;
+    o->frame_stack = 1;
+    o->action_bytes = 4;
+    o->ragged = 0;
+    o->aux_elem_bytes = 0;
+}
+
+const char* conduit_last_error(void) { return g_last_error.c_str(); }
+
+const char* conduit_version(void) { return "conduit-mi355x 0.1 (gfx950)"; }
+
+size_t conduit_buffer_required_bytes(int64_t capacity, const int64_t* obs_shape, int32_t ndim, conduit_dtype obs_dtype,
+                                     const conduit_buffer_opts* opts) {
+    conduit_buffer_opts o;
+    conduit_buffer_opts_default(&o);
+    if (opts) o = *opts;
+    Layout L;
+    if (make_layout(capacity, obs_shape, ndim, obs_dtype, o, &L) != CONDUIT_OK) return 0;
+    return L.total;
+}
+
+conduit_status conduit_buffer_create(int64_t capacity, const int64_t* obs_shape, int32_t ndim, conduit_dtype obs_dtype,
+                                     const conduit_buffer_opts* opts, void* arena, size_t arena_bytes,
+                                     conduit_buffer** out) {
+    if (!out) return fail(CONDUIT_EINVAL, "out must not be NULL");
+    *out = nullptr;
+    conduit_buffer_opts o;
+    conduit_buffer_opts_default(&o);
+    if (opts) o = *opts;
+    Layout L;
+    conduit_status st = make_layout(capacity, obs_shape, ndim, obs_dtype, o, &L);
+    if (st != CONDUIT_OK) return st;
+    if (arena) {
+        if (arena_bytes < L.total) return fail(CONDUIT_EINVAL, "arena smaller than conduit_buffer_required_bytes()");
+        if (reinterpret_cast<uintptr_t>(arena) % kAlign) return fail(CONDUIT_EINVAL, "arena must be 256-byte aligned");
+    }
+    int slot = -1;
+    st = err_slot_acquire(&slot);
+    if (st != CONDUIT_OK) return st;
+
+    conduit_buffer* b = new conduit_buffer();
+    (void)hipGetDevice(&b->device);
+    b->capacity = capacity;
+    b->obs_dtype = obs_dtype;
+    b->opts = o;
+    b->layout = L;
+    b->err_slot = slot;
+    if (arena) {
+        b->arena = static_cast<uint8_t*>(arena);
+    } else {
+        void* p = nullptr;
+        hipError_t e = hipMalloc(&p, L.total);
+        if (e != hipSuccess) {
+            err_slot_release(slot);
+            delete b;
+            (void)hipGetLastError();
+            return fail(CONDUIT_ENOMEM, std::string("hipMalloc of ") + std::to_string(L.total) + " bytes failed");
+        }
+        b->arena = static_cast<uint8_t*>(p);
+        b->owns_arena = true;
+    }
+    uint8_t* A = b->arena;
+    b->state = reinterpret_cast<DeviceState*>(A + L.off_state);
+    b->obs = A + L.off_obs;
+    b->aux = (o.ragged && o.aux_elem_bytes) ? A + L.off_aux : nullptr;
+    b->action = o.action_bytes ? A + L.off_action : nullptr;
+    b->reward = reinterpret_cast<float*>(A + L.off_reward);
+    b->done = A + L.off_done;
+    b->episode = reinterpret_cast<uint32_t*>(A + L.off_episode);
+    b->step = reinterpret_cast<int32_t*>(A + L.off_step);
+    b->length = o.ragged ? reinterpret_cast<int32_t*>(A + L.off_length) : nullptr;
+    TreeView& T = b->tree;
+    T.depth = L.depth;
+    T.alpha_num = o.alpha_num;
+    T.alpha_den = o.alpha_den;
+    T.frac_bits = (32 * (o.alpha_den - o.alpha_num)) / o.alpha_den;
+    if (T.frac_bits > 31) T.frac_bits = 31;
+    for (int l = 0; l <= kMaxLevels; ++l) {
+        T.nodes[l] = l <= L.depth ? L.nodes[l] : 0;
+        T.level[l] = nullptr;
+        T.lds_offset[l] = -1;
+    }
+    if (o.prioritized) {
+        T.leaves = reinterpret_cast<uint32_t*>(A + L.off_leaves);
+        for (int l = 1; l <= L.depth; ++l) T.level[l] = reinterpret_cast<uint64_t*>(A + L.off_level[l]);
+        int used = 0;
+        for (int l = L.depth; l >= 1; --l) {  // small levels accumulate in LDS during updates
+            if (L.nodes[l] <= 1024 && used + L.nodes[l] <= 2048) {
+                T.lds_offset[l] = used;
+                used += (int)L.nodes[l];
+            }
+        }
+    }
+    // initial contents: empty tree, unwritten slots (step -1), state words
+    hipError_t e = hipSuccess;
+    if (o.prioritized) {
+        e = launch_fill_u32(T.leaves, 0u, round64(capacity), nullptr);
+        for (int l = 1; l <= L.depth && e == hipSuccess; ++l)
+            e = launch_fill_u64(T.level[l], 0ull, round64(L.nodes[l]), nullptr);
+    }
+    if (e == hipSuccess) e = launch_fill_u32(b->episode, 0u, capacity, nullptr);
+    if (e == hipSuccess) e = launch_fill_u32(reinterpret_cast<uint32_t*>(b->step), 0xffffffffu, capacity, nullptr);
+    if (e == hipSuccess && b->length) e = launch_fill_u32(reinterpret_cast<uint32_t*>(b->length), 0u, capacity, nullptr);
+    DeviceState init{1u, 0xffffffffu, 0u, 0u};
+    if (e == hipSuccess) e = hipMemcpy(b->state, &init, sizeof(init), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        conduit_status r = hip_fail(e, "buffer initialisation");
+        conduit_buffer_destroy(b);
+        return r;
+    }
+    *out = b;
+    return CONDUIT_OK;
+}
+
+void conduit_buffer_destroy(conduit_buffer* b) {
+    if (!b) return;
+    {
+        DeviceGuard g(b->device);
+        (void)hipDeviceSynchronize();
+        if (b->owns_arena && b->arena) (void)hipFree(b->arena);
+    }
+    err_slot_release(b->err_slot);
+    delete b;
+}
+
+conduit_status conduit_buffer_get_info(const conduit_buffer* b, conduit_buffer_info* info) {
+    if (!b || !info) return fail(CONDUIT_EINVAL, "NULL argument");
+    std::memset(info, 0, sizeof(*info));
+    info->capacity = b->capacity;
+    info->row_bytes = b->layout.row_bytes;
+    info->head = b->head;
+    info->size = b->size;
+    info->total = b->total;
+    info->tree_depth = b->opts.prioritized ? b->layout.depth : 0;
+    for (int l = 0; l <= b->layout.depth && l < 8; ++l) info->tree_nodes[l] = b->layout.nodes[l];
+    info->arena_bytes = (int64_t)b->layout.total;
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_ingest(conduit_buffer* b, const conduit_transitions* t, void* stream) {
+    if (!b || !t) return fail(CONDUIT_EINVAL, "NULL buffer or transitions");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (t->n < 0 || t->n > b->capacity) return fail(CONDUIT_EINVAL, "ingest n must be in [0, capacity]");
+    if (t->n == 0) return CONDUIT_OK;
+    const conduit_buffer_opts& o = b->opts;
+    if (!t->obs) return fail(CONDUIT_EINVAL, "obs must not be NULL");
+    if (reinterpret_cast<uintptr_t>(t->obs) % 4) return fail(CONDUIT_EINVAL, "obs must be 4-byte aligned");
+    if (o.ragged && !t->offsets) return fail(CONDUIT_EINVAL, "ragged ingest needs offsets");
+    if (o.ragged && t->aux && reinterpret_cast<uintptr_t>(t->aux) % 4) return fail(CONDUIT_EINVAL, "aux must be 4-byte aligned");
+    if (o.frame_stack > 1 && (!t->episode_id || !t->step))
+        return fail(CONDUIT_EINVAL, "frame-stacking buffers need episode_id and step");
+    DeviceGuard g(b->device);
+    IngestArgs a{};
+    a.obs = b->obs;
+    a.aux = b->aux;
+    a.action = b->action;
+    a.reward = b->reward;
+    a.done = b->done;
+    a.episode = b->episode;
+    a.step = b->step;
+    a.length = b->length;
+    a.capacity = b->capacity;
+    a.row_bytes = b->layout.row_bytes;
+    a.max_len = b->layout.max_len;
+    a.elem_bytes = o.ragged ? 4 : 0;
+    a.aux_elem_bytes = o.aux_elem_bytes;
+    a.action_bytes = o.action_bytes;
+    a.prioritized = o.prioritized;
+    a.src_obs = static_cast<const uint8_t*>(t->obs);
+    a.src_offsets = t->offsets;
+    a.src_aux = static_cast<const uint8_t*>(t->aux);
+    a.src_action = static_cast<const uint8_t*>(t->action);
+    a.src_reward = t->reward;
+    a.src_done = t->done;
+    a.src_episode = t->episode_id;
+    a.src_step = t->step;
+    a.src_prio = o.prioritized ? t->prio : nullptr;
+    a.n = t->n;
+    a.head = b->head;
+    a.tree = b->tree;
+    a.state = b->state;
+    a.err = err_words(b->err_slot);
+    hipError_t e = launch_ingest(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "ingest launch");
+    b->head = (b->head + t->n) % b->capacity;
+    b->size = b->size + t->n < b->capacity ? b->size + t->n : b->capacity;
+    b->total += t->n;
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_update_priorities(conduit_buffer* b, const int64_t* idx, const uint32_t* prio, int64_t n,
+                                         void* stream) {
+    if (!b) return fail(CONDUIT_EINVAL, "NULL buffer");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (!b->opts.prioritized) return fail(CONDUIT_EINVAL, "buffer was created without priorities");
+    if (n < 0) return fail(CONDUIT_EINVAL, "n must be >= 0");
+    if (n == 0) return CONDUIT_OK;
+    if (!idx || !prio) return fail(CONDUIT_EINVAL, "idx and prio must not be NULL");
+    DeviceGuard g(b->device);
+    UpdateArgs a{};
+    a.tree = b->tree;
+    a.idx = idx;
+    a.prio = prio;
+    a.n = n;
+    a.size = b->size;
+    a.state = b->state;
+    a.err = err_words(b->err_slot);
+    hipError_t e = launch_update(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "update launch");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_sample(conduit_buffer* b, int64_t batch, const uint64_t* uniforms, int64_t* idx_out,
+                              float* is_w_out, void* stream) {
+    if (!b) return fail(CONDUIT_EINVAL, "NULL buffer");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (!b->opts.prioritized) return fail(CONDUIT_EINVAL, "buffer was created without priorities");
+    if (batch < 1 || batch > (1LL << 20)) return fail(CONDUIT_EINVAL, "batch must be in [1, 2^20]");
+    if (!uniforms || !idx_out) return fail(CONDUIT_EINVAL, "uniforms and idx_out must not be NULL");
+    if (b->size == 0) return fail(CONDUIT_EEMPTY, "sample from an empty buffer");
+    DeviceGuard g(b->device);
+    SampleArgs a{};
+    a.tree = b->tree;
+    a.uniforms = uniforms;
+    a.idx_out = idx_out;
+    a.w_out = is_w_out;
+    a.batch = batch;
+    a.beta = b->opts.beta;
+    a.state = b->state;
+    a.err = err_words(b->err_slot);
+    hipError_t e = launch_sample(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "sample launch");
+    return CONDUIT_OK;
+}
+
+static conduit_status check_xform(const conduit_transform* xf, int64_t row_bytes, conduit_dtype dt) {
+    switch (xf->kind) {
+        case CONDUIT_XF_NONE:
+            return CONDUIT_OK;
+        case CONDUIT_XF_U8_F32:
+            if (dt != CONDUIT_U8) return fail(CONDUIT_EINVAL, "U8_F32 needs uint8 observations");
+            return CONDUIT_OK;
+        case CONDUIT_XF_U8_BF16_NORM:
+            if (dt != CONDUIT_U8) return fail(CONDUIT_EINVAL, "U8_BF16_NORM needs uint8 observations");
+            if (xf->channels < 1 || xf->channels > 4) return fail(CONDUIT_EINVAL, "channels must be in [1, 4]");
+            if (row_bytes % (4 * xf->channels)) return fail(CONDUIT_EINVAL, "row must split into 4-byte-aligned planes");
+            for (int c = 0; c < xf->channels; ++c)
+                if (!(xf->std[c] != 0.0f)) return fail(CONDUIT_EINVAL, "std must be non-zero");
+            return CONDUIT_OK;
+        default:
+            return fail(CONDUIT_EINVAL, "unknown or unsupported transform");
+    }
+}
+
+static void fill_norm(GatherArgs& a, const conduit_transform* xf, int64_t row_bytes) {
+    if (xf->kind != CONDUIT_XF_U8_BF16_NORM) {
+        a.plane_units = 1;
+        return;
+    }
+    a.plane_units = (int32_t)(row_bytes / 4 / xf->channels);
+    for (int c = 0; c < 4; ++c) {
+        a.mean[c] = c < xf->channels ? xf->mean[c] : 0.0f;
+        a.stdv[c] = c < xf->channels ? xf->std[c] : 1.0f;
+    }
+}
+
+conduit_status conduit_gather_transform(conduit_buffer* b, const int64_t* idx, int64_t n, const conduit_transform* xf,
+                                        const conduit_learner_batch* out, void* stream) {
+    if (!b || !xf || !out) return fail(CONDUIT_EINVAL, "NULL buffer, transform or output");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (n < 0) return fail(CONDUIT_EINVAL, "n must be >= 0");
+    if (n == 0) return CONDUIT_OK;
+    if (!idx) return fail(CONDUIT_EINVAL, "idx must not be NULL");
+    DeviceGuard g(b->device);
+    const conduit_buffer_opts& o = b->opts;
+    if (o.ragged) {
+        if (xf->kind != CONDUIT_XF_TOKENS_PAD) return fail(CONDUIT_EINVAL, "ragged buffers gather with TOKENS_PAD");
+        if (!out->obs) return fail(CONDUIT_EINVAL, "obs output must not be NULL");
+        if ((reinterpret_cast<uintptr_t>(out->obs) | reinterpret_cast<uintptr_t>(out->aux)) % 16)
+            return fail(CONDUIT_EINVAL, "outputs must be 16-byte aligned");
+        if (reinterpret_cast<uintptr_t>(out->mask) % 4) return fail(CONDUIT_EINVAL, "mask must be 4-byte aligned");
+        PackArgs a{};
+        a.idx = idx;
+        a.n = n;
+        a.size = b->size;
+        a.seq = b->obs;
+        a.aux = b->aux;
+        a.length = b->length;
+        a.reward = b->reward;
+        a.max_len = b->layout.max_len;
+        a.pad_id = xf->pad_id;
+        a.out_seq = out->obs;
+        a.out_mask = out->mask;
+        a.out_aux = b->aux ? out->aux : nullptr;
+        a.out_length = out->length;
+        a.out_reward = out->reward;
+        a.action = b->action;
+        a.out_action = b->action ? static_cast<uint8_t*>(out->action) : nullptr;
+        a.action_bytes = o.action_bytes;
+        a.done = b->done;
+        a.out_done = out->done;
+        a.err = err_words(b->err_slot);
+        hipError_t e = launch_pack(a, static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, "pack launch");
+        return CONDUIT_OK;
+    }
+    st = check_xform(xf, b->layout.row_bytes, b->obs_dtype);
+    if (st != CONDUIT_OK) return st;
+    if (reinterpret_cast<uintptr_t>(out->obs) % 16) return fail(CONDUIT_EINVAL, "obs output must be 16-byte aligned");
+    GatherArgs a{};
+    a.idx = idx;
+    a.n = n;
+    a.limit = b->size;
+    a.stack = o.frame_stack;
+    a.capacity = b->capacity;
+    a.src = b->obs;
+    a.row_bytes = b->layout.row_bytes;
+    a.episode = b->episode;
+    a.step = b->step;
+    a.out = out->obs;
+    a.xform = xf->kind;
+    fill_norm(a, xf, b->layout.row_bytes);
+    a.action = b->action;
+    a.out_action = b->action ? static_cast<uint8_t*>(out->action) : nullptr;
+    a.action_bytes = o.action_bytes;
+    a.reward = b->reward;
+    a.out_reward = out->reward;
+    a.done = b->done;
+    a.out_done = out->done;
+    a.ncols = 0;
+    a.err = err_words(b->err_slot);
+    a.err_kind = ERR_GATHER_INDEX;
+    hipError_t e = launch_gather(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gather launch");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_gae(const float* rewards, const float* values, const uint8_t* dones, const float* bootstrap,
+                           int64_t T, int64_t E, double gamma, double lambda, float* adv, float* ret, void* stream) {
+    if (T < 0 || E < 0) return fail(CONDUIT_EINVAL, "T and E must be >= 0");
+    if (T == 0 || E == 0) return CONDUIT_OK;
+    if (!rewards || !dones || !adv || !ret) return fail(CONDUIT_EINVAL, "rewards, dones, adv and ret must not be NULL");
+    if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
+    conduit_status st = standalone_flags();
+    if (st != CONDUIT_OK) return st;
+    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret};
+    hipError_t e = launch_gae(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gae launch");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_gae_packed(const float* last_reward, const int32_t* lengths, const float* values, int64_t B,
+                                  int64_t Lmax, double gamma, double lambda, float* adv, float* ret, void* stream) {
+    if (B < 0 || Lmax < 0) return fail(CONDUIT_EINVAL, "B and Lmax must be >= 0");
+    if (B == 0 || Lmax == 0) return CONDUIT_OK;
+    if (!last_reward || !lengths || !adv || !ret) return fail(CONDUIT_EINVAL, "NULL required pointer");
+    if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
+    conduit_status st = standalone_flags();
+    if (st != CONDUIT_OK) return st;
+    GaePackedArgs a{last_reward, lengths, values, B, Lmax, gamma, lambda, adv, ret, err_words(0)};
+    hipError_t e = launch_gae_packed(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gae_packed launch");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_minibatch_gather(const void* src, int64_t row_bytes, int64_t n_src, const int64_t* perm,
+                                        int64_t n, const conduit_transform* xf, void* out, const float* const* cols,
+                                        float* const* cols_out, int32_t ncols, void* stream) {
+    if (!xf) return fail(CONDUIT_EINVAL, "NULL transform");
+    if (n < 0 || n_src < 0 || row_bytes < 0) return fail(CONDUIT_EINVAL, "sizes must be >= 0");
+    if (ncols < 0 || ncols > kMaxCols) return fail(CONDUIT_EINVAL, "ncols must be in [0, 8]");
+    if (n == 0) return CONDUIT_OK;
+    if (!perm) return fail(CONDUIT_EINVAL, "perm must not be NULL");
+    if (row_bytes % 4) return fail(CONDUIT_EINVAL, "row_bytes must be a multiple of 4");
+    if (out && (!src || reinterpret_cast<uintptr_t>(src) % 4))
+        return fail(CONDUIT_EINVAL, "src must be non-NULL and 4-byte aligned");
+    if (out && reinterpret_cast<uintptr_t>(out) % 16) return fail(CONDUIT_EINVAL, "out must be 16-byte aligned");
+    if (ncols > 0 && (!cols || !cols_out)) return fail(CONDUIT_EINVAL, "column arrays must not be NULL");
+    for (int c = 0; c < ncols; ++c)
+        if (!cols[c] || !cols_out[c]) return fail(CONDUIT_EINVAL, "column pointers must not be NULL");
+    if (xf->kind == CONDUIT_XF_TOKENS_PAD) return fail(CONDUIT_EINVAL, "TOKENS_PAD is for ragged buffers");
+    conduit_status st = check_xform(xf, row_bytes, CONDUIT_U8);
+    if (st != CONDUIT_OK) return st;
+    st = standalone_flags();
+    if (st != CONDUIT_OK) return st;
+    GatherArgs a{};
+    a.idx = perm;
+    a.n = n;
+    a.limit = n_src;
+    a.stack = 1;
+    a.capacity = n_src;
+    a.src = static_cast<const uint8_t*>(src);
+    a.row_bytes = row_bytes;
+    a.out = row_bytes > 0 ? out : nullptr;
+    a.xform = xf->kind;
+    fill_norm(a, xf, row_bytes);
+    a.ncols = ncols;
+    for (int c = 0; c < ncols; ++c) {
+        a.cols[c] = cols[c];
+        a.cols_out[c] = cols_out[c];
+    }
+    a.err = err_words(0);
+    a.err_kind = ERR_PERM_INDEX;
+    hipError_t e = launch_gather(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "minibatch gather launch");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_buffer_read(const conduit_buffer* b, conduit_column col, int32_t level, int64_t offset,
+                                   int64_t nbytes, void* dst, void* stream) {
+    if (!b || !dst) return fail(CONDUIT_EINVAL, "NULL buffer or destination");
+    const Layout& L = b->layout;
+    const int64_t C = b->capacity;
+    const uint8_t* base = nullptr;
+    int64_t bytes = 0;
+    switch (col) {
+        case CONDUIT_COL_OBS: base = b->obs; bytes = C * L.row_bytes; break;
+        case CONDUIT_COL_ACTION: base = b->action; bytes = C * b->opts.action_bytes; break;
+        case CONDUIT_COL_REWARD: base = reinterpret_cast<const uint8_t*>(b->reward); bytes = C * 4; break;
+        case CONDUIT_COL_DONE: base = b->done; bytes = C; break;
+        case CONDUIT_COL_EPISODE: base = reinterpret_cast<const uint8_t*>(b->episode); bytes = C * 4; break;
+        case CONDUIT_COL_STEP: base = reinterpret_cast<const uint8_t*>(b->step); bytes = C * 4; break;
+        case CONDUIT_COL_LENGTH: base = reinterpret_cast<const uint8_t*>(b->length); bytes = b->length ? C * 4 : 0; break;
+        case CONDUIT_COL_AUX: base = b->aux; bytes = b->aux ? C * L.max_len * b->opts.aux_elem_bytes : 0; break;
+        case CONDUIT_COL_LEAVES:
+            base = reinterpret_cast<const uint8_t*>(b->tree.leaves);
+            bytes = b->opts.prioritized ? C * 4 : 0;
+            break;
+        case CONDUIT_COL_TREE:
+            if (!b->opts.prioritized || level < 1 || level > L.depth) return fail(CONDUIT_EINVAL, "no such tree level");
+            base = reinterpret_cast<const uint8_t*>(b->tree.level[level]);
+            bytes = L.nodes[level] * 8;
+            break;
+        case CONDUIT_COL_MAX_PRIO: base = reinterpret_cast<const uint8_t*>(&b->state->max_prio); bytes = 4; break;
+        default: return fail(CONDUIT_EINVAL, "unknown column");
+    }
+    if (!base || offset < 0 || nbytes < 0 || offset + nbytes > bytes) return fail(CONDUIT_EINVAL, "range outside the column");
+    if (nbytes == 0) return CONDUIT_OK;
+    DeviceGuard g(b->device);
+    hipError_t e = hipMemcpyAsync(dst, base + offset, (size_t)nbytes, hipMemcpyDeviceToDevice,
+                                  static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "column copy");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_sync_check(const conduit_buffer* b, void* stream) {
+    int slot = 0;
+    if (b) {
+        slot = b->err_slot;
+        DeviceGuard g(b->device);
+        hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, "stream synchronise");
+    } else {
+        hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+        if (e != hipSuccess) return hip_fail(e, "stream synchronise");
+    }
+    return check_flags(slot);
+}
+
+void conduit_clear_error(conduit_buffer* b) {
+    std::lock_guard<std::mutex> lk(g_err_mu);
+    if (!g_err_host) return;
+    const int slot = b ? b->err_slot : 0;
+    std::memset(g_err_host + slot * kErrKinds, 0, sizeof(uint32_t) * kErrKinds);
+}
+
+}  // extern "C"

@@ -1,0 +1,336 @@
+// Internal declarations shared by the HIP kernels and the host side of
+// libconduit.  Not part of the public ABI (that is include/conduit.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "conduit.h"
+
+namespace conduit {
+
+constexpr int kWave = 64;         // CDNA wavefront width
+constexpr int kFanout = 64;       // sum-tree fanout: one wavefront scans one node's children
+constexpr int kFanoutLog2 = 6;
+constexpr int kMaxLevels = 8;     // levels above the leaves; 64^6 > 2^31 slots
+
+// Sticky device-side error kinds; each has its own word in pinned host memory,
+// so concurrent reporters never need an atomic read-modify-write across PCIe.
+enum ErrKind : int {
+    ERR_UPDATE_INDEX = 0,   // priority update index outside [0, size)
+    ERR_GATHER_INDEX = 1,   // gather index outside [0, size)
+    ERR_EMPTY_TREE = 2,     // sample with a zero root
+    ERR_SEQ_LENGTH = 3,     // ragged sequence longer than the slot / bad GAE length
+    ERR_PERM_INDEX = 4,     // minibatch permutation entry outside [0, n_src)
+    ERR_QUANT = 5,          // leaf quantiser failed its exact check (never expected)
+    ERR_DESCENT = 6,        // tree descent found no child (never expected)
+    kErrKinds = 8,
+};
+
+// Small device-resident state of one buffer.
+struct DeviceState {
+    uint32_t max_prio;   // running maximum priority (starts at 1)
+    uint32_t qmin;       // sampler scratch: batch minimum leaf, UINT32_MAX between calls
+    uint32_t ticket;     // sampler scratch: finished blocks, 0 between calls
+    uint32_t pad;
+};
+
+// The 64-ary sum tree.  Level 0 = uint32 leaves, levels 1..depth = uint64 sums;
+// level l node n covers leaves [n*64^l, (n+1)*64^l).  Every level is padded with
+// zeros to a multiple of 64 entries so a wavefront can always load 64 children.
+struct TreeView {
+    uint32_t* leaves;
+    uint64_t* level[kMaxLevels + 1];  // level[1..depth]
+    int64_t nodes[kMaxLevels + 1];    // nodes per level (unpadded), nodes[0] = capacity
+    int32_t depth;
+    int32_t alpha_num, alpha_den, frac_bits;
+    // update kernel: levels with few nodes are accumulated in LDS first
+    int32_t lds_offset[kMaxLevels + 1];  // -1: direct global atomics
+};
+
+__device__ __forceinline__ void flag_error(uint32_t* err, int kind) {
+    // plain vector store of a non-zero word into pinned host memory
+    __hip_atomic_store(err + kind, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// ---------------------------------------------------------------------------
+// wavefront primitives (64 lanes)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, kWave);
+    return x;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        uint64_t y = __shfl_xor(x, off, kWave);
+        x = y > x ? y : x;
+    }
+    return x;
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        uint32_t y = __shfl_xor(x, off, kWave);
+        x = y < x ? y : x;
+    }
+    return x;
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        uint32_t y = __shfl_xor(x, off, kWave);
+        x = y > x ? y : x;
+    }
+    return x;
+}
+
+// inclusive prefix sum across the wavefront
+__device__ __forceinline__ uint64_t wave_inclusive_scan_u64(uint64_t x) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        uint64_t y = __shfl_up(x, off, kWave);
+        if (lane >= off) x += y;
+    }
+    return x;
+}
+
+// ---------------------------------------------------------------------------
+// exact leaf quantiser  L(p) = floor(2^F p^(a/b))
+// ---------------------------------------------------------------------------
+// q = L(p) is the unique integer with q^b <= 2^(bF) p^a < (q+1)^b.  An fp64
+// candidate (error far below one unit for q < 2^32) is corrected with exact
+// 288-bit integer comparisons, so the result does not depend on the accuracy of
+// the device log2/exp2.
+struct Big288 {
+    uint32_t w[9];
+};
+
+__device__ __forceinline__ void big_one(Big288& x) {
+#pragma unroll
+    for (int i = 0; i < 9; ++i) x.w[i] = 0;
+    x.w[0] = 1;
+}
+
+__device__ __forceinline__ void big_mul32(Big288& x, uint32_t m) {
+    uint64_t carry = 0;
+#pragma unroll
+    for (int i = 0; i < 9; ++i) {
+        uint64_t t = (uint64_t)x.w[i] * m + carry;
+        x.w[i] = (uint32_t)t;
+        carry = t >> 32;
+    }
+}
+
+__device__ __forceinline__ void big_shl(Big288& x, int bits) {
+    const int words = bits >> 5, r = bits & 31;
+    for (int i = 8; i >= 0; --i) {
+        uint32_t hi = i - words >= 0 ? x.w[i - words] : 0u;
+        uint32_t lo = i - words - 1 >= 0 ? x.w[i - words - 1] : 0u;
+        x.w[i] = r ? (hi << r) | (lo >> (32 - r)) : hi;
+    }
+}
+
+// -1, 0, 1 as x <, ==, > y
+__device__ __forceinline__ int big_cmp(const Big288& x, const Big288& y) {
+    for (int i = 8; i >= 0; --i) {
+        if (x.w[i] != y.w[i]) return x.w[i] < y.w[i] ? -1 : 1;
+    }
+    return 0;
+}
+
+__device__ __forceinline__ void big_pow(Big288& x, uint32_t base, int e) {
+    big_one(x);
+    for (int i = 0; i < e; ++i) big_mul32(x, base);
+}
+
+// returns L(p); sets *bad if the exact check could not be satisfied
+__device__ inline uint32_t quantise_leaf(uint32_t p, int a, int b, int F, bool* bad) {
+    if (p == 0u) return 0u;
+    if (a == 0) return 1u << F;
+    if (a == b) return p;  // F = 0
+    double x = exp2((double)F + ((double)a / (double)b) * log2((double)p));
+    uint64_t q = x >= 4294967295.0 ? 4294967295ull : (uint64_t)x;
+    Big288 rhs, lhs;
+    big_pow(rhs, p, a);
+    big_shl(rhs, b * F);
+    for (int it = 0; it < 4; ++it) {  // q too large?
+        big_pow(lhs, (uint32_t)q, b);
+        if (big_cmp(lhs, rhs) > 0 && q > 0) --q; else break;
+    }
+    for (int it = 0; it < 4; ++it) {  // q + 1 still fits?
+        if (q + 1 > 0xffffffffull) break;  // (2^32)^b exceeds every rhs
+        big_pow(lhs, (uint32_t)(q + 1), b);
+        if (big_cmp(lhs, rhs) <= 0) ++q; else break;
+    }
+    big_pow(lhs, (uint32_t)q, b);
+    bool ok = big_cmp(lhs, rhs) <= 0;
+    if (q + 1 <= 0xffffffffull) {
+        big_pow(lhs, (uint32_t)(q + 1), b);
+        ok = ok && big_cmp(lhs, rhs) > 0;
+    }
+    if (!ok) *bad = true;
+    return (uint32_t)q;
+}
+
+// ---------------------------------------------------------------------------
+// kernel launch entry points (host functions defined next to each kernel)
+// ---------------------------------------------------------------------------
+struct IngestArgs {
+    // destination ring
+    uint8_t* obs;
+    uint8_t* aux;
+    uint8_t* action;
+    float* reward;
+    uint8_t* done;
+    uint32_t* episode;
+    int32_t* step;
+    int32_t* length;
+    int64_t capacity;
+    int64_t row_bytes;
+    int64_t max_len;         // ragged: elements per slot
+    int32_t elem_bytes;      // ragged: 4
+    int32_t aux_elem_bytes;  // ragged: 0 or 4
+    int32_t action_bytes;
+    int32_t prioritized;
+    // source
+    const uint8_t* src_obs;
+    const int64_t* src_offsets;
+    const uint8_t* src_aux;
+    const uint8_t* src_action;
+    const float* src_reward;
+    const uint8_t* src_done;
+    const uint32_t* src_episode;
+    const int32_t* src_step;
+    const uint32_t* src_prio;
+    int64_t n;
+    int64_t head;
+    TreeView tree;
+    DeviceState* state;
+    uint32_t* err;
+};
+
+hipError_t launch_ingest(const IngestArgs& a, hipStream_t s);
+
+struct UpdateArgs {
+    TreeView tree;
+    const int64_t* idx;
+    const uint32_t* prio;
+    int64_t n;
+    int64_t size;
+    DeviceState* state;
+    uint32_t* err;
+};
+
+hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
+
+struct SampleArgs {
+    TreeView tree;
+    const uint64_t* uniforms;
+    int64_t* idx_out;
+    float* w_out;
+    int64_t batch;
+    double beta;
+    DeviceState* state;
+    uint32_t* err;
+};
+
+hipError_t launch_sample(const SampleArgs& a, hipStream_t s);
+
+constexpr int kMaxCols = 8;
+
+struct GatherArgs {
+    const int64_t* idx;     // sample indices (or a permutation)
+    int64_t n;              // rows to produce
+    int64_t limit;          // valid index range [0, limit)
+    int32_t stack;          // K
+    int64_t capacity;       // ring size for (i - d) mod capacity
+    const uint8_t* src;     // [*, row_bytes]
+    int64_t row_bytes;
+    const uint32_t* episode;  // frame-stack metadata (NULL if stack == 1)
+    const int32_t* step;
+    void* out;
+    int32_t xform;          // conduit_xform_kind
+    int32_t plane_units;    // U8_BF16_NORM: 4-byte units per plane
+    float mean[4];
+    float stdv[4];
+    // scalar columns taken from the newest slot
+    const uint8_t* action;
+    uint8_t* out_action;
+    int32_t action_bytes;
+    const float* reward;
+    float* out_reward;
+    const uint8_t* done;
+    uint8_t* out_done;
+    // extra float columns (minibatch gather)
+    int32_t ncols;
+    const float* cols[kMaxCols];
+    float* cols_out[kMaxCols];
+    uint32_t* err;
+    int32_t err_kind;
+};
+
+hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
+
+struct PackArgs {
+    const int64_t* idx;
+    int64_t n;
+    int64_t size;
+    const uint8_t* seq;       // [capacity, max_len] 4-byte elements
+    const uint8_t* aux;       // [capacity, max_len] 4-byte elements or NULL
+    const int32_t* length;
+    const float* reward;
+    int64_t max_len;
+    int32_t pad_id;
+    void* out_seq;
+    uint8_t* out_mask;
+    void* out_aux;
+    int32_t* out_length;
+    float* out_reward;
+    const uint8_t* action;
+    uint8_t* out_action;
+    int32_t action_bytes;
+    const uint8_t* done;
+    uint8_t* out_done;
+    uint32_t* err;
+};
+
+hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+
+struct GaeArgs {
+    const float* reward;
+    const float* value;
+    const uint8_t* done;
+    const float* bootstrap;
+    int64_t T, E;
+    double gamma, lambda;
+    float* adv;
+    float* ret;
+};
+
+hipError_t launch_gae(const GaeArgs& a, hipStream_t s);
+
+struct GaePackedArgs {
+    const float* last_reward;
+    const int32_t* length;
+    const float* value;
+    int64_t B, Lmax;
+    double gamma, lambda;
+    float* adv;
+    float* ret;
+    uint32_t* err;
+};
+
+hipError_t launch_gae_packed(const GaePackedArgs& a, hipStream_t s);
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
+hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int64_t n, hipStream_t s);
+
+}  // namespace conduit

@@ -1,0 +1,196 @@
+// Ring-buffer ingest: copy n transitions into slots (head + j) mod capacity and
+// bring the priority sum tree up to date, in one launch.
+//
+// Off-policy ingestion inserts transitions into a persistent replay dataset and
+// keeps the indices and metadata needed for sampling and eviction (paper
+// Sec. 2.2); new transitions enter with the running maximum priority unless the
+// caller gives one (proportional prioritised replay, Schaul et al.).
+//
+// One grid, three block roles:
+//   * copy blocks   -- dense observations as one flat, coalesced vector copy of
+//                      n*row_bytes bytes whose destination wraps once at the
+//                      end of the ring (16-byte vectors when aligned);
+//   * ragged blocks -- one block per variable-length sequence;
+//   * meta blocks   -- one lane per transition: scalar columns, exact leaf
+//                      L(p), and the leaf delta pushed up the 64-ary tree.
+// Tree update: each wavefront covers 64 consecutive slots (the lanes are
+// arranged so that a wavefront never straddles the ring's wrap point), so at any
+// level its slots fall under at most two nodes; the wavefront reduces its deltas
+// per node and issues at most two 64-bit integer atomics per level.  Integer
+// addition modulo 2^64 is exact and order-independent, so the tree is
+// deterministic and equal to the sum of its leaves after the kernel.
+#include "common.h"
+
+namespace conduit {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kCopyUnroll = 4;
+
+template <typename V>
+__device__ void copy_dense(const IngestArgs& a, int64_t block) {
+    const int64_t vec_per_row = a.row_bytes / (int64_t)sizeof(V);
+    const int64_t total = a.n * vec_per_row;
+    const int64_t ring = a.capacity * vec_per_row;
+    const int64_t head_v = a.head * vec_per_row;
+    const V* __restrict__ src = reinterpret_cast<const V*>(a.src_obs);
+    V* __restrict__ dst = reinterpret_cast<V*>(a.obs);
+    const int64_t base = block * (kThreads * kCopyUnroll) + threadIdx.x;
+    V v[kCopyUnroll];
+#pragma unroll
+    for (int r = 0; r < kCopyUnroll; ++r) {
+        const int64_t i = base + (int64_t)r * kThreads;
+        if (i < total) v[r] = src[i];
+    }
+#pragma unroll
+    for (int r = 0; r < kCopyUnroll; ++r) {
+        const int64_t i = base + (int64_t)r * kThreads;
+        if (i < total) {
+            int64_t d = head_v + i;
+            if (d >= ring) d -= ring;
+            dst[d] = v[r];
+        }
+    }
+}
+
+__device__ void copy_ragged(const IngestArgs& a, int64_t j) {
+    int64_t slot = a.head + j;
+    if (slot >= a.capacity) slot -= a.capacity;
+    int64_t len = a.src_offsets[j + 1] - a.src_offsets[j];
+    if (len < 0) len = 0;
+    if (len > a.max_len) len = a.max_len;  // flagged by the meta lane of row j
+    const int64_t off = a.src_offsets[j];
+    const uint32_t* __restrict__ s = reinterpret_cast<const uint32_t*>(a.src_obs) + off;
+    uint32_t* __restrict__ d = reinterpret_cast<uint32_t*>(a.obs + slot * a.row_bytes);
+    for (int64_t t = threadIdx.x; t < len; t += kThreads) d[t] = s[t];
+    if (a.aux && a.src_aux) {
+        const uint32_t* __restrict__ sa = reinterpret_cast<const uint32_t*>(a.src_aux) + off;
+        uint32_t* __restrict__ da = reinterpret_cast<uint32_t*>(a.aux) + slot * a.max_len;
+        for (int64_t t = threadIdx.x; t < len; t += kThreads) da[t] = sa[t];
+    }
+}
+
+__device__ void ingest_meta(const IngestArgs& a, int64_t block) {
+    // rows [0, n1) go to slots head.., rows [n1, n) to slots 0..; each segment
+    // starts on a wavefront boundary
+    const int64_t n1 = a.n < a.capacity - a.head ? a.n : a.capacity - a.head;
+    const int64_t lanes_a = (n1 + kWave - 1) / kWave * kWave;
+    const int64_t t = block * kThreads + threadIdx.x;
+    int64_t j, slot;
+    bool valid;
+    if (t < lanes_a) {
+        j = t;
+        slot = a.head + t;
+        valid = t < n1;
+    } else {
+        j = n1 + (t - lanes_a);
+        slot = t - lanes_a;
+        valid = j < a.n;
+    }
+    const uint64_t any_valid = __ballot(valid);
+    if (any_valid == 0) return;  // whole wavefront past the end (wave-uniform)
+
+    uint64_t delta = 0;
+    uint32_t p_seen = 0;
+    bool bad_q = false;
+    if (valid) {
+        if (a.action_bytes > 0) {
+            uint8_t* dst = a.action + slot * a.action_bytes;
+            if (a.src_action) {
+                const uint8_t* src = a.src_action + j * a.action_bytes;
+                if ((a.action_bytes & 3) == 0) {
+                    for (int c = 0; c < a.action_bytes; c += 4)
+                        *reinterpret_cast<uint32_t*>(dst + c) = *reinterpret_cast<const uint32_t*>(src + c);
+                } else {
+                    for (int c = 0; c < a.action_bytes; ++c) dst[c] = src[c];
+                }
+            } else {
+                for (int c = 0; c < a.action_bytes; ++c) dst[c] = 0;
+            }
+        }
+        a.reward[slot] = a.src_reward ? a.src_reward[j] : 0.0f;
+        a.done[slot] = a.src_done ? a.src_done[j] : (uint8_t)0;
+        a.episode[slot] = a.src_episode ? a.src_episode[j] : 0u;
+        a.step[slot] = a.src_step ? a.src_step[j] : 0;
+        if (a.length) {
+            int64_t len = a.src_offsets[j + 1] - a.src_offsets[j];
+            if (len < 0 || len > a.max_len) {
+                flag_error(a.err, ERR_SEQ_LENGTH);
+                len = len < 0 ? 0 : a.max_len;
+            }
+            a.length[slot] = (int32_t)len;
+        }
+        if (a.prioritized) {
+            const uint32_t p = a.src_prio ? a.src_prio[j] : a.state->max_prio;
+            p_seen = p;
+            const uint32_t q = quantise_leaf(p, a.tree.alpha_num, a.tree.alpha_den, a.tree.frac_bits, &bad_q);
+            const uint32_t old = a.tree.leaves[slot];
+            a.tree.leaves[slot] = q;
+            delta = (uint64_t)q - (uint64_t)old;  // modulo 2^64
+        }
+    }
+    if (!a.prioritized) return;
+    const int lane = lane_id();
+    if (bad_q) flag_error(a.err, ERR_QUANT);
+    if (a.src_prio) {
+        const uint32_t m = wave_max_u32(p_seen);
+        if (lane == 0 && m > 0) atomicMax(&a.state->max_prio, m);
+    }
+    // lane 0 is valid whenever any lane is (segments start on wave boundaries)
+    const int64_t slot0 = __shfl(slot, 0, kWave);
+    const uint64_t my = (uint64_t)(valid ? slot : slot0);
+    for (int l = 1; l <= a.tree.depth; ++l) {
+        const uint64_t key = my >> (kFanoutLog2 * l);
+        const uint64_t k0 = __shfl(key, 0, kWave);
+        const uint64_t k1 = wave_max_u64(key);  // the other node, if the wave spans two
+        const uint64_t sa = wave_sum_u64(key == k0 ? delta : 0ull);
+        const uint64_t sb = wave_sum_u64(key != k0 ? delta : 0ull);
+        if (lane == 0) {
+            if (sa) atomicAdd(reinterpret_cast<unsigned long long*>(a.tree.level[l] + k0), sa);
+            if (k1 != k0 && sb) atomicAdd(reinterpret_cast<unsigned long long*>(a.tree.level[l] + k1), sb);
+        }
+    }
+}
+
+template <typename V, bool RAGGED>
+__global__ __launch_bounds__(kThreads) void k_ingest(IngestArgs a, int64_t data_blocks) {
+    const int64_t b = blockIdx.x;
+    if (b < data_blocks) {
+        if constexpr (RAGGED) copy_ragged(a, b);
+        else copy_dense<V>(a, b);
+    } else {
+        ingest_meta(a, b - data_blocks);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_ingest(const IngestArgs& a, hipStream_t s) {
+    if (a.n <= 0) return hipSuccess;
+    const int64_t n1 = a.n < a.capacity - a.head ? a.n : a.capacity - a.head;
+    const int64_t n2 = a.n - n1;
+    const int64_t lanes = (n1 + kWave - 1) / kWave * kWave + (n2 + kWave - 1) / kWave * kWave;
+    const int64_t meta_blocks = (lanes + kThreads - 1) / kThreads;
+    if (a.length) {  // ragged
+        const int64_t grid = a.n + meta_blocks;
+        hipLaunchKernelGGL((k_ingest<uint32_t, true>), dim3((unsigned)grid), dim3(kThreads), 0, s, a, a.n);
+        return hipGetLastError();
+    }
+    const uintptr_t al = reinterpret_cast<uintptr_t>(a.src_obs) | reinterpret_cast<uintptr_t>(a.obs) |
+                         (uintptr_t)a.row_bytes;
+    int vec = (al & 15) == 0 ? 16 : (al & 7) == 0 ? 8 : (al & 3) == 0 ? 4 : 1;
+    if (a.row_bytes == 0) vec = 16;
+    const int64_t total_vec = a.n * (a.row_bytes / vec);
+    const int64_t copy_blocks = (total_vec + kThreads * kCopyUnroll - 1) / (kThreads * kCopyUnroll);
+    const dim3 grid((unsigned)(copy_blocks + meta_blocks));
+    switch (vec) {
+        case 16: hipLaunchKernelGGL((k_ingest<uint4, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
+        case 8: hipLaunchKernelGGL((k_ingest<uint2, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
+        case 4: hipLaunchKernelGGL((k_ingest<uint32_t, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
+        default: hipLaunchKernelGGL((k_ingest<uint8_t, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace conduit

@@ -1,0 +1,182 @@
+"""GPU parity of the on-policy path: rollout ingest, GAE (time-major and packed)
+and the minibatch shuffle-gather, against the oracle through the C ABI.
+GAE within 1e-5 max(|o|, 1); gathered bytes and u8 transforms bit-exact."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_util import assert_gae_close, dev, host
+
+pytestmark = pytest.mark.gpu
+
+from paper_2609_24456_amd import conduit as cd  # noqa: E402
+
+
+def _gae_gpu(r, v, d, b, gamma, lam):
+    T, E = r.shape
+    adv = torch.full((T, E), np.nan, dtype=torch.float32, device="cuda")
+    ret = torch.full((T, E), np.nan, dtype=torch.float32, device="cuda")
+    cd.conduit_gae(dev(r), dev(v) if v is not None else None, dev(d), dev(b) if b is not None else None,
+                   gamma, lam, adv, ret)
+    assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+    return host(adv), host(ret)
+
+
+@pytest.mark.parametrize("T,E,p_done,with_v,with_b", [
+    (1, 1, 0.0, True, True), (2, 3, 0.5, True, False), (37, 19, 0.05, True, True), (64, 16, 0.0, False, False),
+    (65, 17, 1.0, True, True), (200, 70, 0.01, True, True), (1000, 5, 0.002, True, True)])
+def test_gae_time_major_shapes(T, E, p_done, with_v, with_b):
+    print(f"gae T={T} E={E}", flush=True)
+    rng = np.random.default_rng(T * 131 + E)
+    r = rng.standard_normal((T, E)).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32) if with_v else None
+    d = (rng.random((T, E)) < p_done).astype(np.uint8)
+    b = rng.standard_normal(E).astype(np.float32) if with_b else None
+    for gamma, lam in [(0.99, 0.95), (1.0, 1.0), (0.0, 0.5)]:
+        ga, gr = _gae_gpu(r, v, d, b, gamma, lam)
+        oa, orr = oracle.gae(r, v, d, b, gamma, lam)
+        assert_gae_close(ga, oa)
+        assert_gae_close(gr, orr)
+
+
+def test_gae_ppo_config_full_size():
+    print("gae: PPO rollout 2048 x 256", flush=True)
+    cfg = synth.PPO()
+    ga, gr = _gae_gpu(cfg.reward, cfg.value, cfg.done, cfg.bootstrap, cfg.gamma, cfg.lam)
+    oa, orr = oracle.gae(cfg.reward, cfg.value, cfg.done, cfg.bootstrap, cfg.gamma, cfg.lam)
+    assert_gae_close(ga, oa)
+    assert_gae_close(gr, orr)
+
+
+@pytest.mark.parametrize("B,Lmax,with_v", [(1, 4, False), (5, 8, True), (33, 260, True), (256, 4096, False),
+                                           (64, 4096, True)])
+def test_gae_packed(B, Lmax, with_v):
+    print(f"gae packed B={B} Lmax={Lmax}", flush=True)
+    rng = np.random.default_rng(B * 7 + Lmax)
+    length = rng.integers(0, Lmax + 1, B).astype(np.int32)
+    length[0] = Lmax
+    if B > 2:
+        length[1] = 1
+        length[2] = 0
+    R = rng.standard_normal(B).astype(np.float32)
+    v = rng.standard_normal((B, Lmax)).astype(np.float32) if with_v else None
+    for gamma, lam in [(1.0, 0.95), (0.99, 0.9)]:
+        adv = torch.full((B, Lmax), np.nan, dtype=torch.float32, device="cuda")
+        ret = torch.full((B, Lmax), np.nan, dtype=torch.float32, device="cuda")
+        cd.conduit_gae_packed(dev(R), dev(length), dev(v) if v is not None else None, Lmax, gamma, lam, adv, ret)
+        assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+        oa, orr = oracle.gae_packed(R, length, v, Lmax, gamma, lam)
+        assert_gae_close(host(adv), oa)
+        assert_gae_close(host(ret), orr)
+
+
+def _ppo_rollout_buffer(cfg, steps_per_call):
+    T, E = cfg.T, cfg.E
+    buf = cd.ReplayBuffer(T * E, cfg.obs_shape, torch.uint8, prioritized=False, action_bytes=0)
+    for t0 in range(0, T, steps_per_call):
+        t1 = min(T, t0 + steps_per_call)
+        buf.ingest(cfg.obs_steps(t0, t1, "cuda"), reward=dev(cfg.reward[t0:t1].reshape(-1)),
+                   done=dev(cfg.done[t0:t1].reshape(-1)))
+    return buf
+
+
+def _obs_column_tensor(buf, n_rows, row_bytes):
+    out = torch.empty(n_rows * row_bytes, dtype=torch.uint8, device="cuda")
+    buf.read(cd.COL_OBS, out)
+    return out
+
+
+@pytest.mark.parametrize("T,E,M", [(64, 32, 4), (33, 7, 3)])
+def test_ppo_minibatches_reduced(T, E, M):
+    print(f"ppo minibatches T={T} E={E} M={M}", flush=True)
+    cfg = synth.PPO(T=T, E=E)
+    row = 3 * 84 * 84
+    buf = _ppo_rollout_buffer(cfg, steps_per_call=5)
+    src = _obs_column_tensor(buf, T * E, row)
+    ga, gr = _gae_gpu(cfg.reward, cfg.value, cfg.done, cfg.bootstrap, cfg.gamma, cfg.lam)
+    A, R = dev(ga.reshape(-1)), dev(gr.reshape(-1))
+    oa, orr = oracle.gae(cfg.reward, cfg.value, cfg.done, cfg.bootstrap, cfg.gamma, cfg.lam)
+    obs_host = cfg.obs_steps(0, T).numpy()
+    perm = cfg.perm
+    mb = (T * E) // M
+    seen = []
+    for m in range(M):
+        rows = perm[m * mb:(m + 1) * mb]
+        out = torch.empty((mb, 3, 84, 84), dtype=torch.float32, device="cuda")
+        a_out = torch.empty(mb, dtype=torch.float32, device="cuda")
+        r_out = torch.empty(mb, dtype=torch.float32, device="cuda")
+        cd.conduit_minibatch_gather(src, row, T * E, dev(rows), cd.transform(cd.XF_U8_F32), out, cols=[A, R],
+                                    cols_out=[a_out, r_out])
+        assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+        want = oracle.rows(obs_host, rows, oracle.XF_U8_F32)
+        assert np.array_equal(host(out).view(np.uint32), want.view(np.uint32))
+        assert_gae_close(host(a_out), oa.reshape(-1)[rows])
+        assert_gae_close(host(r_out), orr.reshape(-1)[rows])
+        seen.append(rows)
+    # on-policy freshness: the M minibatches cover the rollout exactly once
+    assert np.array_equal(np.sort(np.concatenate(seen)), np.arange(M * mb))
+    buf.close()
+
+
+def test_minibatch_transforms_and_bad_perm():
+    print("minibatch gather: NONE / BF16 transforms, out-of-range perm", flush=True)
+    rng = np.random.default_rng(3)
+    n_src, shape = 50, (3, 8, 12)
+    row = int(np.prod(shape))
+    src_h = rng.integers(0, 256, size=(n_src,) + shape, dtype=np.uint8)
+    src = dev(src_h)
+    perm = rng.integers(0, n_src, size=40)
+    out = torch.empty((40,) + shape, dtype=torch.uint8, device="cuda")
+    cd.conduit_minibatch_gather(src, row, n_src, dev(perm), cd.transform(cd.XF_NONE), out)
+    assert np.array_equal(host(out), oracle.rows(src_h, perm))
+    mean, std = (0.485, 0.456, 0.406), (0.229, 0.224, 0.225)
+    outb = torch.empty((40,) + shape, dtype=torch.bfloat16, device="cuda")
+    cd.conduit_minibatch_gather(src, row, n_src, dev(perm), cd.transform(cd.XF_U8_BF16_NORM, mean, std), outb)
+    assert np.array_equal(host(outb.view(torch.int16)).view(np.uint16),
+                          oracle.rows(src_h, perm, oracle.XF_U8_BF16_NORM, mean, std))
+    assert cd.conduit_sync_check() == cd.OK
+    bad = perm.copy()
+    bad[5] = n_src
+    bad[6] = -1
+    out.fill_(9)
+    cd.conduit_minibatch_gather(src, row, n_src, dev(bad), cd.transform(cd.XF_NONE), out)
+    assert cd.conduit_sync_check() == cd.ESTATE
+    cd.conduit_clear_error()
+    o = host(out)
+    assert np.all(o[5] == 0) and np.all(o[6] == 0)
+    assert np.array_equal(o[7:], src_h[bad[7:]])
+
+
+@pytest.mark.slow
+def test_ppo_full_size_minibatch_sampled_rows():
+    print("ppo: full rollout 2048 x 256 x 3x84x84 (11.1 GB), GAE, minibatches 0 and 31", flush=True)
+    cfg = synth.PPO()
+    T, E = cfg.T, cfg.E
+    row = 3 * 84 * 84
+    buf = _ppo_rollout_buffer(cfg, steps_per_call=64)
+    src = torch.empty(0, dtype=torch.uint8, device="cuda")
+    # gather straight from the buffer's observation column: one minibatch of 16384 rows
+    ga, gr = _gae_gpu(cfg.reward, cfg.value, cfg.done, cfg.bootstrap, cfg.gamma, cfg.lam)
+    oa, orr = oracle.gae(cfg.reward, cfg.value, cfg.done, cfg.bootstrap, cfg.gamma, cfg.lam)
+    assert_gae_close(ga, oa)
+    A, R = dev(ga.reshape(-1)), dev(gr.reshape(-1))
+    src = _obs_column_tensor(buf, T * E, row)
+    buf.close()
+    mb = 16384
+    check = np.random.default_rng(0).choice(mb, 48, replace=False)
+    for m in [0, 31]:
+        rows = cfg.perm[m * mb:(m + 1) * mb]
+        out = torch.empty((mb, 3, 84, 84), dtype=torch.float32, device="cuda")
+        a_out = torch.empty(mb, dtype=torch.float32, device="cuda")
+        r_out = torch.empty(mb, dtype=torch.float32, device="cuda")
+        cd.conduit_minibatch_gather(src, row, T * E, dev(rows), cd.transform(cd.XF_U8_F32), out, cols=[A, R],
+                                    cols_out=[a_out, r_out])
+        assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+        sel = rows[check]
+        want = oracle.rows(cfg.obs_rows(sel).numpy(), np.arange(len(sel)), oracle.XF_U8_F32)
+        assert np.array_equal(host(out[check]).view(np.uint32), want.view(np.uint32))
+        assert_gae_close(host(a_out), oa.reshape(-1)[rows])
+        assert_gae_close(host(r_out), orr.reshape(-1)[rows])
+        del out
