@@ -1,0 +1,575 @@
+"""Benchmark of the experience path on one MI355X.
+
+Headline workload (the configuration the metric is quoted on): DQN replay of
+1,000,000 single 84x84 uint8 frames, frame stack 4, batch 512, proportional
+prioritisation alpha 0.6 / beta 0.4.  One step = ingest 512 new frames + sample
+512 + gather/transform 512 -> [512, 4, 84, 84] fp32 + priority update 512.
+Inputs (frames of the steps, uniforms, new priorities) are resident in HBM
+before the timed region.
+
+Prints ONE JSON line.  Besides the headline it carries the roofline of the
+dominant kernel, the oracle timed on the host cores (cpu_baseline), per-kernel
+times of the step, and the other workloads' rows (PPO GAE + minibatch gather,
+large-payload bf16 gather, token packing + packed GAE, tiny replay latency).
+"""
+import argparse
+import ctypes as C
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, published
+METRIC = "sampled transitions/sec + gather HBM GB/s (% of peak), DQN 1M-replay config"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-rows", action="store_true", help="only the headline DQN workload")
+    p.add_argument("--only", default="", help="comma list of extra rows to run (ppo,large,tokens,tiny)")
+    p.add_argument("--calibrate-copy", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
+    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    return p.parse_args()
+
+
+def _sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+# ----------------------------------------------------------------------------
+# helpers
+# ----------------------------------------------------------------------------
+def _dev(a):
+    import numpy as np
+    import torch
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint64:
+        a = a.view(np.int64)
+    elif a.dtype == np.uint32:
+        a = a.view(np.int32)
+    return torch.from_numpy(a).cuda()
+
+
+class Timer:
+    """HIP events on the stream the library launches on (torch's current stream)."""
+
+    def __init__(self):
+        import torch
+        self.torch = torch
+
+    def ev(self):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        return e
+
+
+def _kernel_stats(durs_ms):
+    import numpy as np
+    d = np.asarray(durs_ms)
+    return {"mean_us": float(d.mean() * 1e3), "median_us": float(np.median(d) * 1e3)}
+
+
+# ----------------------------------------------------------------------------
+# headline: DQN 1M replay
+# ----------------------------------------------------------------------------
+def bench_dqn(steps, warmup):
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+
+    L = cd.lib()
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    Cap, B, K, prefill, chunk = 1_000_000, 512, 4, 1_050_000, 4096
+    iters = warmup + 2 * steps  # clean timed pass + instrumented pass
+    cfg = synth.DQN(prefill + iters * B)
+    buf = cd.ReplayBuffer(Cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4)
+    t0 = time.time()
+    for a in range(0, prefill, chunk):
+        b = min(prefill, a + chunk)
+        buf.ingest(cfg.frames(a, b - a, "cuda"), action=_dev(cfg.action[a:b]), reward=_dev(cfg.reward[a:b]),
+                   done=_dev(cfg.done[a:b]), episode_id=_dev(cfg.episode[a:b]), step=_dev(cfg.step[a:b]),
+                   prio=_dev(cfg.prio[a:b]))
+    torch.cuda.synchronize()
+    prefill_s = time.time() - t0
+
+    # prefill-style ingest throughput: one 32768-frame chunk, timed alone
+    big = cfg.frames(0, 32768, "cuda")
+    meta = [_dev(x[:32768]) for x in (cfg.action, cfg.reward, cfg.done, cfg.episode, cfg.step)]
+    bigp = _dev(cfg.prio[:32768])
+    tm = Timer()
+    durs = []
+    for _ in range(6):
+        e0 = tm.ev()
+        buf.ingest(big, action=meta[0], reward=meta[1], done=meta[2], episode_id=meta[3], step=meta[4], prio=bigp)
+        e1 = tm.ev()
+        torch.cuda.synchronize()
+        durs.append(e0.elapsed_time(e1))
+    ingest_big_ms = float(np.median(durs[1:]))
+    del big
+
+    # stage every step's inputs in HBM
+    s0 = prefill
+    frames = cfg.frames(s0, iters * B, "cuda")
+    act = _dev(cfg.action[s0:s0 + iters * B])
+    rew = _dev(cfg.reward[s0:s0 + iters * B])
+    done = _dev(cfg.done[s0:s0 + iters * B])
+    epi = _dev(cfg.episode[s0:s0 + iters * B])
+    stp = _dev(cfg.step[s0:s0 + iters * B])
+    u, prio = cfg.draws(iters, B)
+    u_d, prio_d = _dev(u), _dev(prio)
+    idx = torch.empty((iters, B), dtype=torch.int64, device="cuda")
+    w = torch.empty((iters, B), dtype=torch.float32, device="cuda")
+    obs_out = torch.empty((B, K, 84, 84), dtype=torch.float32, device="cuda")
+    act_out = torch.empty(B, dtype=torch.int32, device="cuda")
+    rew_out = torch.empty(B, dtype=torch.float32, device="cuda")
+    done_out = torch.empty(B, dtype=torch.uint8, device="cuda")
+    xf = cd.transform(cd.XF_U8_F32)
+    lb = cd.LearnerBatch()
+    lb.obs, lb.action, lb.reward, lb.done = obs_out.data_ptr(), act_out.data_ptr(), rew_out.data_ptr(), done_out.data_ptr()
+    # every call's arguments prepared up front: the timed loop only enters the C ABI
+    trans = []
+    for i in range(iters):
+        t = cd.Transitions()
+        sl = slice(i * B, (i + 1) * B)
+        t.n = B
+        t.obs = frames[sl].data_ptr()
+        t.action, t.reward, t.done = act[sl].data_ptr(), rew[sl].data_ptr(), done[sl].data_ptr()
+        t.episode_id, t.step = epi[sl].data_ptr(), stp[sl].data_ptr()
+        t.prio = None
+        trans.append(t)
+    h = C.c_void_p(buf.handle)
+    ing, smp, gat, upd = L.conduit_ingest, L.conduit_sample, L.conduit_gather_transform, L.conduit_update_priorities
+    pu = [u_d[i].data_ptr() for i in range(iters)]
+    pp = [prio_d[i].data_ptr() for i in range(iters)]
+    pi = [idx[i].data_ptr() for i in range(iters)]
+    pw = [w[i].data_ptr() for i in range(iters)]
+    xfr, lbr = C.byref(xf), C.byref(lb)
+
+    def step(i):
+        r = ing(h, C.byref(trans[i]), stream)
+        r |= smp(h, B, pu[i], pi[i], pw[i], stream)
+        r |= gat(h, pi[i], B, xfr, lbr, stream)
+        r |= upd(h, pi[i], pp[i], B, stream)
+        return r
+
+    for i in range(warmup):
+        assert step(i) == 0, cd.last_error()
+    torch.cuda.synchronize()
+    # clean timed pass
+    e_start = tm.ev()
+    h0 = time.perf_counter()
+    rc = 0
+    for i in range(warmup, warmup + steps):
+        rc |= step(i)
+    e_end = tm.ev()
+    host_enqueue_s = time.perf_counter() - h0
+    torch.cuda.synchronize()
+    assert rc == 0, cd.last_error()
+    total_ms = e_start.elapsed_time(e_end)
+    # instrumented pass: an event between consecutive calls
+    evs = []
+    for i in range(warmup + steps, warmup + 2 * steps):
+        e = [tm.ev()]
+        ing(h, C.byref(trans[i]), stream)
+        e.append(tm.ev())
+        smp(h, B, pu[i], pi[i], pw[i], stream)
+        e.append(tm.ev())
+        gat(h, pi[i], B, xfr, lbr, stream)
+        e.append(tm.ev())
+        upd(h, pi[i], pp[i], B, stream)
+        e.append(tm.ev())
+        evs.append(e)
+    torch.cuda.synchronize()
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    names = ["ingest_512", "sample_512", "gather_512", "update_512"]
+    per = {n: [e[k].elapsed_time(e[k + 1]) for e in evs] for k, n in enumerate(names)}
+    kern = {n: _kernel_stats(v) for n, v in per.items()}
+
+    # algorithmic bytes of the gather of the last instrumented step: frames the
+    # stack actually reads (zero-filled frames are not read), 4x-wide writes,
+    # plus the index and the three scalar columns
+    last = idx[warmup + 2 * steps - 1].cpu().numpy()
+    ep_col = torch.empty(Cap * 4, dtype=torch.uint8, device="cuda")
+    st_col = torch.empty(Cap * 4, dtype=torch.uint8, device="cuda")
+    buf.read(cd.COL_EPISODE, ep_col)
+    buf.read(cd.COL_STEP, st_col)
+    torch.cuda.synchronize()
+    ep_h = ep_col.cpu().numpy().view(np.uint32)
+    st_h = st_col.cpu().numpy().view(np.int32)
+    valid = 0
+    for i in last:
+        for d in range(K):
+            j = (i - d) % Cap
+            if d == 0 or (d <= st_h[i] and ep_h[j] == ep_h[i] and st_h[j] == st_h[i] - d):
+                valid += 1
+    row = 84 * 84
+    gather_bytes = valid * row + B * (8 + 4 + 4 + 1) + B * K * row * 4 + B * (4 + 4 + 1)
+    ingest_bytes_per_frame = 2 * row + (4 + 4 + 1 + 4 + 4) * 2 + 4 + 4  # obs r+w, scalars r+w, leaf r+w
+    buf.close()
+    return {
+        "B": B, "steps": steps, "warmup": warmup, "total_ms": total_ms, "host_enqueue_s": host_enqueue_s,
+        "kernels": kern, "gather_bytes": gather_bytes, "valid_frames": valid, "prefill_s": prefill_s,
+        "ingest_big": {"frames": 32768, "ms": ingest_big_ms,
+                       "GBps": 32768 * ingest_bytes_per_frame / ingest_big_ms / 1e6},
+        "ingest_bytes_per_frame": ingest_bytes_per_frame,
+    }
+
+
+# ----------------------------------------------------------------------------
+# other rows
+# ----------------------------------------------------------------------------
+def bench_ppo(reps=3):
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+    cfg = synth.PPO()
+    T, E, row = cfg.T, cfg.E, 3 * 84 * 84
+    N = T * E
+    tm = Timer()
+    # rollout ingest into an on-policy buffer (no priorities), 64 steps per call
+    buf = cd.ReplayBuffer(N, cfg.obs_shape, torch.uint8, prioritized=False, action_bytes=0)
+    rew_d, done_d = _dev(cfg.reward.reshape(-1)), _dev(cfg.done.reshape(-1))
+    ing_ms = 0.0
+    for t0 in range(0, T, 64):
+        obs = cfg.obs_steps(t0, t0 + 64, "cuda")
+        sl = slice(t0 * E, (t0 + 64) * E)
+        torch.cuda.synchronize()
+        e0 = tm.ev()
+        buf.ingest(obs, reward=rew_d[sl], done=done_d[sl])
+        e1 = tm.ev()
+        torch.cuda.synchronize()
+        ing_ms += e0.elapsed_time(e1)
+        del obs
+    src = torch.empty(N * row, dtype=torch.uint8, device="cuda")
+    buf.read(cd.COL_OBS, src)
+    torch.cuda.synchronize()
+    buf.close()
+    r, v, d, b = _dev(cfg.reward), _dev(cfg.value), _dev(cfg.done), _dev(cfg.bootstrap)
+    adv = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    ret = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    g = []
+    for _ in range(20):
+        e0 = tm.ev()
+        cd.conduit_gae(r, v, d, b, cfg.gamma, cfg.lam, adv, ret)
+        e1 = tm.ev()
+        torch.cuda.synchronize()
+        g.append(e0.elapsed_time(e1))
+    gae_ms = float(np.median(g[2:]))
+    gae_bytes = N * (4 + 4 + 1 + 4 + 4) + E * 4
+    A, R = adv.view(-1), ret.view(-1)
+    mb = 16384
+    perm = _dev(cfg.perm)
+    out = torch.empty((mb, 3, 84, 84), dtype=torch.float32, device="cuda")
+    a_out = torch.empty(mb, dtype=torch.float32, device="cuda")
+    r_out = torch.empty(mb, dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_U8_F32)
+    times = []
+    for rep in range(reps):
+        for m in range(32):
+            e0 = tm.ev()
+            cd.conduit_minibatch_gather(src, row, N, perm[m * mb:(m + 1) * mb], xf, out, cols=[A, R],
+                                        cols_out=[a_out, r_out])
+            e1 = tm.ev()
+            times.append((e0, e1))
+    torch.cuda.synchronize()
+    assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+    mbt = [a.elapsed_time(b) for a, b in times][32:]  # first epoch is warm-up
+    mb_ms = float(np.mean(mbt))
+    mb_bytes = mb * (row + row * 4 + 8 + 2 * 4 + 2 * 4)
+    ing_bytes = N * (2 * row + 2 * (4 + 1) + 2 * (4 + 4))
+    return {
+        "rollout_ingest": {"bytes": ing_bytes, "ms": ing_ms, "GBps": ing_bytes / ing_ms / 1e6,
+                           "frac": ing_bytes / ing_ms / 1e6 / PEAK_HBM_GBPS},
+        "gae_2048x256": {"bytes": gae_bytes, "us": gae_ms * 1e3, "GBps": gae_bytes / gae_ms / 1e6,
+                         "frac": gae_bytes / gae_ms / 1e6 / PEAK_HBM_GBPS},
+        "minibatch_gather_16384": {"bytes": mb_bytes, "us": mb_ms * 1e3, "GBps": mb_bytes / mb_ms / 1e6,
+                                   "frac": mb_bytes / mb_ms / 1e6 / PEAK_HBM_GBPS},
+        "epoch_32_minibatches_ms": float(np.sum(mbt[-32:])),
+    }
+
+
+def bench_large(iters=10):
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+    Cap, B, row = 200_000, 1024, 3 * 224 * 224
+    cfg = synth.Large(Cap)
+    buf = cd.ReplayBuffer(Cap, cfg.obs_shape, torch.uint8, action_bytes=24)
+    for a in range(0, Cap, 2048):
+        b = min(Cap, a + 2048)
+        buf.ingest(cfg.rows(a, b - a, "cuda"), action=_dev(cfg.action[a:b]), reward=_dev(cfg.reward[a:b]),
+                   done=_dev(cfg.done[a:b]), prio=_dev(cfg.prio[a:b]))
+    u, prio = cfg.draws(iters, B)
+    u_d, p_d = _dev(u), _dev(prio)
+    out = torch.empty((B, 1) + cfg.obs_shape, dtype=torch.bfloat16, device="cuda")
+    act = torch.empty((B, 6), dtype=torch.float32, device="cuda")
+    rew = torch.empty(B, dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_U8_BF16_NORM, cfg.mean, cfg.std)
+    tm = Timer()
+    torch.cuda.synchronize()
+    s_t, g_t, u_t = [], [], []
+    for i in range(iters):
+        e0 = tm.ev()
+        idx, w = buf.sample(u_d[i])
+        e1 = tm.ev()
+        buf.gather(idx, xf, obs=out, action=act, reward=rew)
+        e2 = tm.ev()
+        buf.update(idx, p_d[i])
+        e3 = tm.ev()
+        s_t.append((e0, e1))
+        g_t.append((e1, e2))
+        u_t.append((e2, e3))
+    torch.cuda.synchronize()
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
+    gms = float(np.median([a.elapsed_time(b) for a, b in g_t[2:]]))
+    gbytes = B * (row + 2 * row + 8 + 24 + 4 + 24 + 4)
+    return {
+        "gather_bf16_1024": {"bytes": gbytes, "us": gms * 1e3, "GBps": gbytes / gms / 1e6,
+                             "frac": gbytes / gms / 1e6 / PEAK_HBM_GBPS},
+        "sample_1024_us": float(np.median([a.elapsed_time(b) for a, b in s_t[2:]]) * 1e3),
+        "update_1024_us": float(np.median([a.elapsed_time(b) for a, b in u_t[2:]]) * 1e3),
+    }
+
+
+def bench_tokens(iters=10):
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+    Cap, Lmax, B = 65536, 4096, 256
+    cfg = synth.Tokens(Cap)
+    buf = cd.ReplayBuffer(Cap, (Lmax,), torch.int32, action_bytes=4, ragged=True, aux_elem_bytes=4)
+    for a in range(0, Cap, 4096):
+        b = min(Cap, a + 4096)
+        tok, lp, off = cfg.packed(a, b - a, "cuda")
+        buf.ingest(tok, offsets=off, aux=lp, action=_dev(cfg.action[a:b]), reward=_dev(cfg.reward[a:b]),
+                   done=_dev(cfg.done[a:b]), prio=_dev(cfg.prio[a:b]))
+        del tok, lp
+    u, prio = cfg.draws(iters, B)
+    u_d, p_d = _dev(u), _dev(prio)
+    seq = torch.empty((B, Lmax), dtype=torch.int32, device="cuda")
+    mask = torch.empty((B, Lmax), dtype=torch.uint8, device="cuda")
+    lp_out = torch.empty((B, Lmax), dtype=torch.float32, device="cuda")
+    length = torch.empty(B, dtype=torch.int32, device="cuda")
+    rew = torch.empty(B, dtype=torch.float32, device="cuda")
+    adv = torch.empty((B, Lmax), dtype=torch.float32, device="cuda")
+    ret = torch.empty((B, Lmax), dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_TOKENS_PAD)
+    tm = Timer()
+    torch.cuda.synchronize()
+    pk, ga, it_t = [], [], []
+    lens = []
+    for i in range(iters):
+        e0 = tm.ev()
+        idx, w = buf.sample(u_d[i])
+        e1 = tm.ev()
+        buf.gather(idx, xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
+        e2 = tm.ev()
+        cd.conduit_gae_packed(rew, length, None, Lmax, cfg.gamma, cfg.lam, adv, ret)
+        e3 = tm.ev()
+        buf.update(idx, p_d[i])
+        e4 = tm.ev()
+        pk.append((e1, e2))
+        ga.append((e2, e3))
+        it_t.append((e0, e4))
+        lens.append(length.clone())
+    torch.cuda.synchronize()
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
+    mean_len = float(torch.stack(lens).float().mean())
+    pms = float(np.median([a.elapsed_time(b) for a, b in pk[2:]]))
+    gms = float(np.median([a.elapsed_time(b) for a, b in ga[2:]]))
+    pbytes = int(B * mean_len * 8 + B * Lmax * (4 + 1 + 4) + B * (8 + 4 + 4 + 4 + 4))
+    gbytes = B * (4 + 4) + B * Lmax * 8
+    return {
+        "pack_256x4096": {"bytes": pbytes, "us": pms * 1e3, "GBps": pbytes / pms / 1e6,
+                          "frac": pbytes / pms / 1e6 / PEAK_HBM_GBPS},
+        "gae_packed_256x4096": {"bytes": gbytes, "us": gms * 1e3, "GBps": gbytes / gms / 1e6,
+                                "frac": gbytes / gms / 1e6 / PEAK_HBM_GBPS},
+        "iteration_us": float(np.median([a.elapsed_time(b) for a, b in it_t[2:]]) * 1e3),
+    }
+
+
+def bench_tiny(iters=100):
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+    cfg = synth.Tiny()
+    u, prio = cfg.draws()
+    B, n_in = cfg.batch, cfg.ingest_n
+    buf = cd.ReplayBuffer(cfg.capacity, (8,), torch.float32, action_bytes=4)
+    obs, act, rew, done = _dev(cfg.obs), _dev(cfg.action), _dev(cfg.reward), _dev(cfg.done)
+    epi, stp = _dev(cfg.episode), _dev(cfg.step)
+    u_d, p_d = _dev(u), _dev(prio)
+    out = torch.empty((B, 1, 8), dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_NONE)
+    tm = Timer()
+    torch.cuda.synchronize()
+    e0 = tm.ev()
+    for i in range(iters):
+        sl = slice(i * n_in, (i + 1) * n_in)
+        buf.ingest(obs[sl], action=act[sl], reward=rew[sl], done=done[sl], episode_id=epi[sl], step=stp[sl])
+        idx, w = buf.sample(u_d[i])
+        buf.gather(idx, xf, obs=out)
+        buf.update(idx, p_d[i])
+    e1 = tm.ev()
+    torch.cuda.synchronize()
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
+    ms = e0.elapsed_time(e1)
+    return {"iterations": iters, "us_per_iteration": ms * 1e3 / iters, "launches_per_iteration": 4,
+            "sampled_per_s": iters * B / (ms / 1e3)}
+
+
+# ----------------------------------------------------------------------------
+# CPU baseline: the oracle on the host cores
+# ----------------------------------------------------------------------------
+def cpu_baseline(seconds):
+    import numpy as np
+    import oracle
+    import synth
+    Cap, B, K, prefill = 1_000_000, 512, 4, 1_050_000
+    n_iter_max = 400
+    cfg = synth.DQN(prefill + n_iter_max * B)
+    row = 84 * 84
+    store = np.empty((Cap, row), np.uint8)
+    tile = cfg.frames(0, 4096).reshape(4096, row).numpy()
+    for a in range(0, Cap, 4096):  # every page resident (real DRAM traffic)
+        b = min(Cap, a + 4096)
+        store[a:b] = tile[:b - a]
+    orc = oracle.Replay(Cap, (84, 84), np.uint8, act_bytes=4, frame_stack=K, obs_storage=store)
+    for a in range(0, prefill, 65536):
+        b = min(prefill, a + 65536)
+        orc.ingest(b - a, action=cfg.action[a:b], reward=cfg.reward[a:b], done=cfg.done[a:b],
+                   episode=cfg.episode[a:b], step=cfg.step[a:b], prio=cfg.prio[a:b])
+    u, prio = cfg.draws(n_iter_max, B)
+    frames = cfg.frames(prefill, 8 * B).reshape(8 * B, row).numpy()
+    done_iters = 0
+    t0 = time.perf_counter()
+    while done_iters < n_iter_max:
+        i = done_iters
+        a = prefill + i * B
+        orc.ingest(B, obs=frames[(i % 8) * B:(i % 8 + 1) * B], action=cfg.action[a:a + B],
+                   reward=cfg.reward[a:a + B], done=cfg.done[a:a + B], episode=cfg.episode[a:a + B],
+                   step=cfg.step[a:a + B])
+        idx, w = orc.sample(u[i])
+        orc.gather(idx, oracle.XF_U8_F32)
+        orc.update(idx, prio[i])
+        done_iters += 1
+        if time.perf_counter() - t0 > seconds and done_iters >= 3:
+            break
+    el = time.perf_counter() - t0
+    return {"value": done_iters * B / el, "unit": "sampled transitions/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done_iters} DQN steps (ingest 512 + sample 512 + gather 512 -> fp32 + update 512) on the "
+                      f"1M-slot replay (metadata prefilled with 1.05M transitions), single-threaded C oracle, "
+                      f"{el:.1f} s", "seconds": el}
+
+
+def calibrate_copy():
+    import torch
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": n}), flush=True)
+
+
+def _traffic_from_profile(kernel_src):
+    """HBM bytes per gather launch from the committed counter summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "gather_dqn_counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_sha256_16") != _sha(kernel_src):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              f"(the experience path here is single-GPU; see the sharding notes in DESIGN.md)", flush=True)
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a HIP device"
+    from paper_2609_24456_amd import conduit as cd
+    cd.lib()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+    d = bench_dqn(args.steps, args.warmup)
+    ms_per_step = d["total_ms"] / args.steps
+    value = d["B"] * args.steps / (d["total_ms"] / 1e3)
+    g = d["kernels"]["gather_512"]
+    g_ms = g["mean_us"] / 1e3
+    achieved = d["gather_bytes"] / g_ms / 1e6
+    kernel_src = os.path.join(ROOT, "paper_2609_24456_amd", "csrc", "k_gather.hip")
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "sampled transitions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8->f32",
+        "data": "synthetic",
+        "config": {"workload": "dqn-1M-replay: capacity 1,000,000 single 84x84 u8 frames, frame stack 4, "
+                               "batch 512, PER alpha 0.6 beta 0.4; step = ingest 512 + sample 512 + "
+                               "gather 512 -> [512,4,84,84] fp32 + priority update 512",
+                   "capacity": 1_000_000, "batch": 512, "frame_stack": 4},
+        "gather_GBps": achieved,
+        "gather_frac_of_peak": achieved / PEAK_HBM_GBPS,
+        "roofline": {"bound": "hbm", "kernel": "k_gather<U8_F32> (DQN frame-stack gather)",
+                     "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
+                     "traffic": _traffic_from_profile(kernel_src),
+                     "algorithmic_bytes_per_launch": d["gather_bytes"], "avg_launch_us": g["mean_us"]},
+        "kernels_us": {k: v["mean_us"] for k, v in d["kernels"].items()},
+        "host_enqueue_us_per_step": d["host_enqueue_s"] * 1e6 / args.steps,
+        "rows": {"dqn_ingest_32768": d["ingest_big"]},
+    }
+    if not args.no_rows:
+        only = set(x for x in args.only.split(",") if x) or {"ppo", "large", "tokens", "tiny"}
+        if "tiny" in only:
+            out["rows"]["tiny"] = bench_tiny()
+        if "ppo" in only:
+            out["rows"]["ppo"] = bench_ppo()
+            torch.cuda.empty_cache()
+        if "large" in only:
+            out["rows"]["large"] = bench_large()
+            torch.cuda.empty_cache()
+        if "tokens" in only:
+            out["rows"]["tokens"] = bench_tokens()
+            torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(args.cpu_seconds)
+        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        out["gpu_over_cpu"] = value / cb["value"]
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

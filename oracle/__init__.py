@@ -52,6 +52,8 @@ def _declare(L):
     L.orc_frac_bits.restype = I32
     L.orc_leaf.argtypes = [U32, I32, I32]
     L.orc_leaf.restype = U32
+    L.orc_leaf_many.argtypes = [P, I64, I32, I32, P]
+    L.orc_leaf_many.restype = None
     L.orc_reset.argtypes = [P]
     L.orc_reset.restype = None
     L.orc_total_priority.argtypes = [P]
@@ -102,6 +104,14 @@ def frac_bits(alpha_num, alpha_den):
 def leaf(p, alpha_num=3, alpha_den=5):
     """Exact quantised leaf floor(2^F * p^(a/b)) of a uint32 priority."""
     return int(lib().orc_leaf(int(p), alpha_num, alpha_den))
+
+
+def leaves(p, alpha_num=3, alpha_den=5):
+    """orc_leaf over an array of uint32 priorities."""
+    p = np.ascontiguousarray(p, np.uint32)
+    out = np.zeros(len(p), np.uint32)
+    lib().orc_leaf_many(_ptr(p), len(p), alpha_num, alpha_den, _ptr(out))
+    return out
 
 
 def u8_to_f32(x):

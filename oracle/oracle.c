@@ -108,6 +108,11 @@ uint32_t orc_leaf(uint32_t p, int32_t a, int32_t b) {
     return (uint32_t)lo;
 }
 
+/* L(p) for n priorities (a loop over orc_leaf) */
+void orc_leaf_many(const uint32_t* p, int64_t n, int32_t a, int32_t b, uint32_t* out) {
+    for (int64_t i = 0; i < n; ++i) out[i] = orc_leaf(p[i], a, b);
+}
+
 /* ------------------------------------------------------------------------- */
 /* Replay dataset                                                             */
 /* ------------------------------------------------------------------------- */

@@ -91,6 +91,13 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
     return x;
 }
 
+// value of a 64-bit register in a wave-uniform lane
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)x, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(x >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
+}
+
 // inclusive prefix sum across the wavefront
 __device__ __forceinline__ uint64_t wave_inclusive_scan_u64(uint64_t x) {
     const int lane = lane_id();
@@ -105,10 +112,15 @@ __device__ __forceinline__ uint64_t wave_inclusive_scan_u64(uint64_t x) {
 // ---------------------------------------------------------------------------
 // exact leaf quantiser  L(p) = floor(2^F p^(a/b))
 // ---------------------------------------------------------------------------
-// q = L(p) is the unique integer with q^b <= 2^(bF) p^a < (q+1)^b.  An fp64
-// candidate (error far below one unit for q < 2^32) is corrected with exact
-// 288-bit integer comparisons, so the result does not depend on the accuracy of
-// the device log2/exp2.
+// q = L(p) is the unique integer with q^b <= 2^(bF) p^a < (q+1)^b.
+//
+// Fast path: x = exp2(F + (a/b) log2 p) in fp64.  With the device log2/exp2
+// within a few ulp, the absolute error of x is below x * 2^-45 <= 2^-13 (x is
+// below 2^32), so whenever the fractional part of x lies in [2^-10, 1 - 2^-10]
+// floor(x) is the exact answer.  Otherwise (x within 2^-10 of an integer, about
+// 0.2% of inputs, and every perfect power) the candidate is settled with exact
+// 288-bit integer comparisons.  All limb indices are compile-time constants, so
+// the big integers live in registers.
 struct Big288 {
     uint32_t w[9];
 };
@@ -123,27 +135,34 @@ __device__ __forceinline__ void big_mul32(Big288& x, uint32_t m) {
     uint64_t carry = 0;
 #pragma unroll
     for (int i = 0; i < 9; ++i) {
-        uint64_t t = (uint64_t)x.w[i] * m + carry;
+        const uint64_t t = (uint64_t)x.w[i] * m + carry;
         x.w[i] = (uint32_t)t;
         carry = t >> 32;
     }
 }
 
+// x <<= bits (bits < 256): a multiply by 2^(bits mod 32), then whole-word moves
 __device__ __forceinline__ void big_shl(Big288& x, int bits) {
-    const int words = bits >> 5, r = bits & 31;
-    for (int i = 8; i >= 0; --i) {
-        uint32_t hi = i - words >= 0 ? x.w[i - words] : 0u;
-        uint32_t lo = i - words - 1 >= 0 ? x.w[i - words - 1] : 0u;
-        x.w[i] = r ? (hi << r) | (lo >> (32 - r)) : hi;
+    big_mul32(x, 1u << (bits & 31));
+    const int words = bits >> 5;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+        if (s < words) {
+#pragma unroll
+            for (int i = 8; i > 0; --i) x.w[i] = x.w[i - 1];
+            x.w[0] = 0;
+        }
     }
 }
 
 // -1, 0, 1 as x <, ==, > y
 __device__ __forceinline__ int big_cmp(const Big288& x, const Big288& y) {
-    for (int i = 8; i >= 0; --i) {
-        if (x.w[i] != y.w[i]) return x.w[i] < y.w[i] ? -1 : 1;
+    int r = 0;
+#pragma unroll
+    for (int i = 0; i < 9; ++i) {  // least significant first; higher words override
+        if (x.w[i] != y.w[i]) r = x.w[i] < y.w[i] ? -1 : 1;
     }
-    return 0;
+    return r;
 }
 
 __device__ __forceinline__ void big_pow(Big288& x, uint32_t base, int e) {
@@ -151,33 +170,37 @@ __device__ __forceinline__ void big_pow(Big288& x, uint32_t base, int e) {
     for (int i = 0; i < e; ++i) big_mul32(x, base);
 }
 
-// returns L(p); sets *bad if the exact check could not be satisfied
-__device__ inline uint32_t quantise_leaf(uint32_t p, int a, int b, int F, bool* bad) {
-    if (p == 0u) return 0u;
-    if (a == 0) return 1u << F;
-    if (a == b) return p;  // F = 0
-    double x = exp2((double)F + ((double)a / (double)b) * log2((double)p));
-    uint64_t q = x >= 4294967295.0 ? 4294967295ull : (uint64_t)x;
+// Exact settlement: the largest q with q^b <= 2^(bF) p^a, searched upwards from
+// cand - 2 (the true value is within one of cand).  Bit 32 of the result flags
+// a failed check (never expected).
+__device__ __noinline__ uint64_t quantise_leaf_exact(uint32_t p, int a, int b, int F, uint64_t cand) {
     Big288 rhs, lhs;
     big_pow(rhs, p, a);
     big_shl(rhs, b * F);
-    for (int it = 0; it < 4; ++it) {  // q too large?
-        big_pow(lhs, (uint32_t)q, b);
-        if (big_cmp(lhs, rhs) > 0 && q > 0) --q; else break;
-    }
-    for (int it = 0; it < 4; ++it) {  // q + 1 still fits?
-        if (q + 1 > 0xffffffffull) break;  // (2^32)^b exceeds every rhs
-        big_pow(lhs, (uint32_t)(q + 1), b);
-        if (big_cmp(lhs, rhs) <= 0) ++q; else break;
-    }
+    uint64_t q = cand >= 2 ? cand - 2 : 0;
+    uint64_t bad = 0;
     big_pow(lhs, (uint32_t)q, b);
-    bool ok = big_cmp(lhs, rhs) <= 0;
-    if (q + 1 <= 0xffffffffull) {
+    if (big_cmp(lhs, rhs) > 0) bad = 1ull << 32;  // candidate was not within 2
+    for (int it = 0; it < 4; ++it) {
+        if (q + 1 > 0xffffffffull) return q | bad;  // (2^32)^b exceeds every rhs
         big_pow(lhs, (uint32_t)(q + 1), b);
-        ok = ok && big_cmp(lhs, rhs) > 0;
+        if (big_cmp(lhs, rhs) > 0) return q | bad;
+        ++q;
     }
-    if (!ok) *bad = true;
-    return (uint32_t)q;
+    return q | (1ull << 32);  // ran out of steps
+}
+
+// L(p) in bits 0..31; bit 32 set if the exact check could not be satisfied
+__device__ __forceinline__ uint64_t quantise_leaf(uint32_t p, int a, int b, int F) {
+    if (p == 0u) return 0u;
+    if (a == 0) return 1u << F;
+    if (a == b) return p;  // F = 0
+    const double x = exp2((double)F + ((double)a / (double)b) * log2((double)p));
+    const double fl = floor(x);
+    const double fr = x - fl;
+    const uint64_t cand = fl >= 4294967295.0 ? 4294967295ull : (uint64_t)fl;
+    if (fr >= 0x1p-10 && fr <= 1.0 - 0x1p-10) return cand;
+    return quantise_leaf_exact(p, a, b, F, cand);
 }
 
 // ---------------------------------------------------------------------------

@@ -4,13 +4,14 @@
 // padding/packing are the processing operators it lists).  The same kernel
 // serves the on-policy minibatch shuffle-gather (K = 1, rows of a rollout).
 //
-// Work decomposition: one workgroup of 256 lanes per (sample, frame, part);
-// every lane moves 8 units of 4 source bytes, 256 lanes apart, so each load
-// instruction of a wavefront reads 256 contiguous bytes and each store writes a
-// contiguous run (1 KiB for fp32 output).  All loads of a lane are issued before
-// any store.  Frame-stack validity needs the episode/step of two slots; it is
-// uniform per workgroup and does not gate the pixel loads (which depend only on
-// the sample index), so the metadata round trip overlaps the payload fetch.
+// Work decomposition: a work item is (sample, frame, part) of up to 1792 units
+// of 4 source bytes; a workgroup of 256 lanes moves 7 units per lane, 256 lanes
+// apart, so each load instruction of a wavefront reads 256 contiguous bytes and
+// each store writes a contiguous run (1 KiB for fp32 output).  Four persistent
+// workgroups per compute unit walk the items, double-buffered (see k_gather).
+// Frame-stack validity needs the episode/step of two slots; those loads are
+// unconditional and issued with the payload loads (which depend only on the
+// sample index), so the metadata round trip overlaps the payload fetch.
 //
 // Transforms are exact:
 //   U8_F32:  q0 = x * r (r = fp32(1/255)), e = fma(-q0, 255, x), fma(e, r, q0)
@@ -28,8 +29,10 @@ namespace conduit {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 8;
+constexpr int kUnroll = 7;  // 1792 units per item: one 84x84 frame per item
 constexpr int kUnitsPerBlock = kThreads * kUnroll;
+// outputs up to this size use the persistent pipelined kernel
+constexpr int64_t kPipeMaxOutBytes = 128ll << 20;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -69,61 +72,77 @@ __device__ void gather_scalars(const GatherArgs& a, int64_t block) {
     for (int c = 0; c < a.ncols; ++c) a.cols_out[c][b] = ok ? a.cols[c][i] : 0.0f;
 }
 
-template <int XF>
-__global__ __launch_bounds__(kThreads) void k_gather(GatherArgs a, int32_t blocks_per_frame, int64_t frame_blocks) {
-    __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
-    const int64_t bid = blockIdx.x;
-    if (bid >= frame_blocks) {
-        gather_scalars(a, bid - frame_blocks);
-        return;
+// per-workgroup table of the exact u8 -> bf16 normalisation, 256 entries per plane
+__device__ __forceinline__ void build_lut(const GatherArgs& a, uint16_t* lut) {
+    const int planes = (int)((a.row_bytes >> 2) / a.plane_units);
+    for (int e = threadIdx.x; e < planes * 256; e += kThreads) {
+        const int c = e >> 8;
+        const float v = u8_unit_f32((uint32_t)(e & 255));
+        const float centred = v - a.mean[c];
+        lut[e] = bf16_rne(__fdiv_rn(centred, a.stdv[c]));
     }
-    if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
-        const int planes = (int)((a.row_bytes >> 2) / a.plane_units);
-        for (int e = threadIdx.x; e < planes * 256; e += kThreads) {
-            const int c = e >> 8;
-            const float v = u8_unit_f32((uint32_t)(e & 255));
-            const float centred = v - a.mean[c];
-            lut[e] = bf16_rne(__fdiv_rn(centred, a.stdv[c]));
-        }
-        __syncthreads();
-    }
-    const int64_t frame = bid / blocks_per_frame;
-    const int part = (int)(bid - frame * blocks_per_frame);
-    const int64_t b = frame / a.stack;
-    const int k = (int)(frame - b * a.stack);
-    const int64_t units = a.row_bytes >> 2;
+}
 
-    const int64_t i = a.idx[b];
-    const bool ok = i >= 0 && i < a.limit;
-    if (!ok && threadIdx.x == 0 && part == 0 && k == a.stack - 1) flag_error(a.err, a.err_kind);
-    const int d = a.stack - 1 - k;
-    int64_t j = i - d;
+// One work item = (row b, frame k, part) = up to kUnitsPerBlock 4-byte units.
+struct Item {
+    int64_t b;   // output row
+    int k;       // frame within the stack (0 = oldest)
+    int part;    // chunk of the frame
+    int d;       // frames back from the sampled slot
+    int64_t j;   // source slot
+    bool ok;     // sample index in range
+};
+
+__device__ __forceinline__ Item decode(const GatherArgs& a, int64_t it, int bpf, int64_t i) {
+    Item t;
+    const int64_t frame = it / bpf;
+    t.part = (int)(it - frame * bpf);
+    t.b = frame / a.stack;
+    t.k = (int)(frame - t.b * a.stack);
+    t.ok = i >= 0 && i < a.limit;
+    t.d = a.stack - 1 - t.k;
+    int64_t j = i - t.d;
     if (j < 0) j += a.capacity;
-    if (!ok) j = 0;
+    t.j = t.ok ? j : 0;
+    return t;
+}
 
-    // payload loads first (they depend only on the sample index)
-    const uint32_t* __restrict__ src = reinterpret_cast<const uint32_t*>(a.src + j * a.row_bytes);
-    const int64_t u0 = (int64_t)part * kUnitsPerBlock + threadIdx.x;
-    uint32_t v[kUnroll];
+// issue every load of an item: payload units (clamped, so all are unconditional)
+// and, for stacked frames, the episode/step of the sampled and the source slot
+__device__ __forceinline__ void issue(const GatherArgs& a, const Item& t, int64_t i, uint32_t (&v)[kUnroll],
+                                      int32_t& si, int32_t& sj, uint32_t& ei, uint32_t& ej) {
+    const int64_t units = a.row_bytes >> 2;
+    const uint32_t* __restrict__ src = reinterpret_cast<const uint32_t*>(a.src + t.j * a.row_bytes);
+    const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + threadIdx.x;
 #pragma unroll
     for (int r = 0; r < kUnroll; ++r) {
         const int64_t u = u0 + (int64_t)r * kThreads;
-        v[r] = (ok && u < units) ? src[u] : 0u;
+        v[r] = src[u < units ? u : units - 1];
     }
-    bool valid = ok;
-    if (ok && d > 0) {
-        const int32_t si = a.step[i];
-        valid = d <= si && a.episode[j] == a.episode[i] && a.step[j] == si - d;
+    if (a.stack > 1) {  // kernel argument: uniform
+        const int64_t ii = t.ok ? i : 0;
+        si = a.step[ii];
+        sj = a.step[t.j];
+        ei = a.episode[ii];
+        ej = a.episode[t.j];
     }
+}
 
-    const int64_t out_unit0 = (b * a.stack + k) * units;
+template <int XF, bool NT>
+__device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const uint32_t (&v)[kUnroll], int32_t si,
+                                       int32_t sj, uint32_t ei, uint32_t ej, const uint16_t* lut) {
+    const int64_t units = a.row_bytes >> 2;
+    const bool valid = t.d == 0 ? t.ok : (t.ok & (t.d <= si) & (ei == ej) & (sj == si - t.d));
+    const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + threadIdx.x;
+    const int64_t out_unit0 = (t.b * a.stack + t.k) * units;
 #pragma unroll
     for (int r = 0; r < kUnroll; ++r) {
         const int64_t u = u0 + (int64_t)r * kThreads;
         if (u >= units) continue;
-        const uint32_t x = valid ? v[r] : 0u;
+        const uint32_t x = v[r];
         if constexpr (XF == CONDUIT_XF_NONE) {
-            reinterpret_cast<uint32_t*>(a.out)[out_unit0 + u] = x;
+            uint32_t* p = reinterpret_cast<uint32_t*>(a.out) + out_unit0 + u;
+            if constexpr (NT) __builtin_nontemporal_store(valid ? x : 0u, p); else *p = valid ? x : 0u;
         } else if constexpr (XF == CONDUIT_XF_U8_F32) {
             f32x4 o;
             if (valid) {
@@ -134,19 +153,97 @@ __global__ __launch_bounds__(kThreads) void k_gather(GatherArgs a, int32_t block
             } else {
                 o = (f32x4)(0.0f);
             }
-            __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(a.out) + out_unit0 + u);
+            f32x4* p = reinterpret_cast<f32x4*>(a.out) + out_unit0 + u;
+            if constexpr (NT) __builtin_nontemporal_store(o, p); else *p = o;
         } else {  // U8_BF16_NORM
             u32x2 o;
             if (valid) {
                 const int c = (int)(u / a.plane_units);
-                const uint16_t* t = lut + c * 256;
-                o.x = (uint32_t)t[x & 255u] | ((uint32_t)t[(x >> 8) & 255u] << 16);
-                o.y = (uint32_t)t[(x >> 16) & 255u] | ((uint32_t)t[x >> 24] << 16);
+                const uint16_t* tb = lut + c * 256;
+                o.x = (uint32_t)tb[x & 255u] | ((uint32_t)tb[(x >> 8) & 255u] << 16);
+                o.y = (uint32_t)tb[(x >> 16) & 255u] | ((uint32_t)tb[x >> 24] << 16);
             } else {
                 o = (u32x2)(0u);
             }
-            __builtin_nontemporal_store(o, reinterpret_cast<u32x2*>(a.out) + out_unit0 + u);
+            u32x2* p = reinterpret_cast<u32x2*>(a.out) + out_unit0 + u;
+            if constexpr (NT) __builtin_nontemporal_store(o, p); else *p = o;
         }
+    }
+}
+
+// One work item per workgroup, all of the grid's loads before its stores: the
+// shape for large outputs, where many resident workgroups keep the most bytes
+// in flight.
+template <int XF, bool NT>
+__global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t bpf, int64_t n_items) {
+    __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
+    const int64_t it = blockIdx.x;
+    if (it >= n_items) {
+        gather_scalars(a, it - n_items);
+        return;
+    }
+    if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
+        build_lut(a, lut);
+        __syncthreads();
+    }
+    const int64_t i = a.idx[it / ((int64_t)bpf * a.stack)];
+    const Item t = decode(a, it, bpf, i);
+    if (!t.ok && threadIdx.x == 0 && t.part == 0 && t.k == a.stack - 1) flag_error(a.err, a.err_kind);
+    uint32_t v[kUnroll];
+    int32_t si = 0, sj = 0;
+    uint32_t ei = 0, ej = 0;
+    issue(a, t, i, v, si, sj, ei, ej);
+    finish<XF, NT>(a, t, v, si, sj, ei, ej, lut);
+}
+
+// Persistent workgroups walk the items with a stride of the grid.  Two register
+// sets alternate: the loads of the next item are issued before the stores of
+// the current one, so reads of one item overlap the writes of the previous one
+// instead of the whole GPU reading first and writing afterwards.  The sample
+// index of the item after next is fetched one step ahead as well.
+template <int XF, bool NT>
+__global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t bpf, int64_t n_items, int32_t frame_grid) {
+    __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
+    if ((int32_t)blockIdx.x >= frame_grid) {
+        gather_scalars(a, (int64_t)blockIdx.x - frame_grid);
+        return;
+    }
+    if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
+        build_lut(a, lut);
+        __syncthreads();
+    }
+    const int64_t G = frame_grid;
+    const int64_t per_row = (int64_t)bpf * a.stack;
+    auto clampi = [&](int64_t x) { return x < n_items ? x : n_items - 1; };
+    int64_t it = blockIdx.x;
+    const int64_t i0 = a.idx[it / per_row];
+    int64_t itn = it + G;
+    int64_t i1 = a.idx[clampi(itn) / per_row];
+    uint32_t va[kUnroll], vb[kUnroll];
+    int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
+    uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
+    Item ta = decode(a, it, bpf, i0), tb;
+    if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_error(a.err, a.err_kind);
+    issue(a, ta, i0, va, sia, sja, eia, eja);
+    while (true) {
+        tb = decode(a, clampi(itn), bpf, i1);
+        issue(a, tb, i1, vb, sib, sjb, eib, ejb);
+        int64_t itnn = itn + G;
+        int64_t i2 = a.idx[clampi(itnn) / per_row];
+        finish<XF, NT>(a, ta, va, sia, sja, eia, eja, lut);
+        if (itn >= n_items) break;
+        if (!tb.ok && threadIdx.x == 0 && tb.part == 0 && tb.k == a.stack - 1) flag_error(a.err, a.err_kind);
+        itn = itnn;
+        i1 = i2;
+        ta = decode(a, clampi(itn), bpf, i1);
+        issue(a, ta, i1, va, sia, sja, eia, eja);
+        itnn = itn + G;
+        i2 = a.idx[clampi(itnn) / per_row];
+        finish<XF, NT>(a, tb, vb, sib, sjb, eib, ejb, lut);
+        if (itn >= n_items) break;
+        if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_error(a.err, a.err_kind);
+        itn = itnn;
+        i1 = i2;
     }
 }
 
@@ -204,30 +301,50 @@ __global__ __launch_bounds__(kThreads) void k_pack(PackArgs a) {
 
 }  // namespace
 
+int device_cus() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cached[dev]) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+        cached[dev] = cus;
+    }
+    return cached[dev];
+}
+
+// Both shapes write the learner batch with non-temporal stores: measured in the
+// full ingest/sample/gather/update loop they leave the caches to the next
+// kernels and beat plain stores, even when the batch would fit the 256 MB
+// Infinity Cache.
+template <int XF>
+void launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t bpf, int64_t n_items, int64_t scalar_blocks) {
+    const int64_t out_bytes = n_items * kUnitsPerBlock * 4 * (XF == CONDUIT_XF_U8_F32 ? 4 : XF == CONDUIT_XF_U8_BF16_NORM ? 2 : 1);
+    if (out_bytes <= kPipeMaxOutBytes) {
+        // small batches: persistent pipelined workgroups
+        const int64_t frame_grid = n_items < 4LL * device_cus() ? n_items : 4LL * device_cus();
+        hipLaunchKernelGGL((k_gather_pipe<XF, true>), dim3((unsigned)(frame_grid + scalar_blocks)), dim3(kThreads), 0,
+                           s, a, (int32_t)bpf, n_items, (int32_t)frame_grid);
+    } else {
+        // large batches: one workgroup per item
+        hipLaunchKernelGGL((k_gather_rows<XF, true>), dim3((unsigned)(n_items + scalar_blocks)), dim3(kThreads), 0, s,
+                           a, (int32_t)bpf, n_items);
+    }
+}
+
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;
     const int64_t units = a.row_bytes >> 2;
-    const int64_t bpf = a.out ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
-    const int64_t frame_blocks = a.out ? a.n * a.stack * bpf : 0;
+    const int64_t bpf = a.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
+    const int64_t n_items = a.n * a.stack * bpf;
     const bool scalars = a.out_action || a.out_reward || a.out_done || a.ncols > 0;
     const int64_t scalar_blocks = scalars ? (a.n + kThreads - 1) / kThreads : 0;
-    const int64_t grid = frame_blocks + scalar_blocks;
-    if (grid == 0) return hipSuccess;
+    if (n_items + scalar_blocks == 0) return hipSuccess;
     switch (a.xform) {
-        case CONDUIT_XF_NONE:
-            hipLaunchKernelGGL(k_gather<CONDUIT_XF_NONE>, dim3((unsigned)grid), dim3(kThreads), 0, s, a, (int32_t)bpf,
-                               frame_blocks);
-            break;
-        case CONDUIT_XF_U8_F32:
-            hipLaunchKernelGGL(k_gather<CONDUIT_XF_U8_F32>, dim3((unsigned)grid), dim3(kThreads), 0, s, a,
-                               (int32_t)bpf, frame_blocks);
-            break;
-        case CONDUIT_XF_U8_BF16_NORM:
-            hipLaunchKernelGGL(k_gather<CONDUIT_XF_U8_BF16_NORM>, dim3((unsigned)grid), dim3(kThreads), 0, s, a,
-                               (int32_t)bpf, frame_blocks);
-            break;
-        default:
-            return hipErrorInvalidValue;
+        case CONDUIT_XF_NONE: launch_gather_xf<CONDUIT_XF_NONE>(a, s, bpf, n_items, scalar_blocks); break;
+        case CONDUIT_XF_U8_F32: launch_gather_xf<CONDUIT_XF_U8_F32>(a, s, bpf, n_items, scalar_blocks); break;
+        case CONDUIT_XF_U8_BF16_NORM: launch_gather_xf<CONDUIT_XF_U8_BF16_NORM>(a, s, bpf, n_items, scalar_blocks); break;
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }

@@ -28,6 +28,9 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kCopyUnroll = 4;
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 template <typename V>
 __device__ void copy_dense(const IngestArgs& a, int64_t block) {
     const int64_t vec_per_row = a.row_bytes / (int64_t)sizeof(V);
@@ -37,11 +40,13 @@ __device__ void copy_dense(const IngestArgs& a, int64_t block) {
     const V* __restrict__ src = reinterpret_cast<const V*>(a.src_obs);
     V* __restrict__ dst = reinterpret_cast<V*>(a.obs);
     const int64_t base = block * (kThreads * kCopyUnroll) + threadIdx.x;
+    // every load is unconditional (out-of-range lanes re-read the last vector) so
+    // all kCopyUnroll loads of a lane are in flight at once
     V v[kCopyUnroll];
 #pragma unroll
     for (int r = 0; r < kCopyUnroll; ++r) {
         const int64_t i = base + (int64_t)r * kThreads;
-        if (i < total) v[r] = src[i];
+        v[r] = src[i < total ? i : total - 1];
     }
 #pragma unroll
     for (int r = 0; r < kCopyUnroll; ++r) {
@@ -94,6 +99,7 @@ __device__ void ingest_meta(const IngestArgs& a, int64_t block) {
     uint64_t delta = 0;
     uint32_t p_seen = 0;
     bool bad_q = false;
+    const uint32_t old = (valid && a.prioritized) ? a.tree.leaves[slot] : 0u;  // issued early
     if (valid) {
         if (a.action_bytes > 0) {
             uint8_t* dst = a.action + slot * a.action_bytes;
@@ -124,8 +130,9 @@ __device__ void ingest_meta(const IngestArgs& a, int64_t block) {
         if (a.prioritized) {
             const uint32_t p = a.src_prio ? a.src_prio[j] : a.state->max_prio;
             p_seen = p;
-            const uint32_t q = quantise_leaf(p, a.tree.alpha_num, a.tree.alpha_den, a.tree.frac_bits, &bad_q);
-            const uint32_t old = a.tree.leaves[slot];
+            const uint64_t qf = quantise_leaf(p, a.tree.alpha_num, a.tree.alpha_den, a.tree.frac_bits);
+            bad_q |= (qf >> 32) != 0;
+            const uint32_t q = (uint32_t)qf;
             a.tree.leaves[slot] = q;
             delta = (uint64_t)q - (uint64_t)old;  // modulo 2^64
         }
@@ -137,18 +144,22 @@ __device__ void ingest_meta(const IngestArgs& a, int64_t block) {
         const uint32_t m = wave_max_u32(p_seen);
         if (lane == 0 && m > 0) atomicMax(&a.state->max_prio, m);
     }
-    // lane 0 is valid whenever any lane is (segments start on wave boundaries)
-    const int64_t slot0 = __shfl(slot, 0, kWave);
-    const uint64_t my = (uint64_t)(valid ? slot : slot0);
+    // The wavefront's valid lanes hold consecutive slots slot0, slot0 + 1, ...
+    // (lane 0 is valid whenever any lane is: segments start on wave boundaries),
+    // so at level l the lanes [0, s) fall under node slot0 >> 6l and the rest
+    // under the next node.  One inclusive scan of the deltas gives both sums.
+    const uint64_t incl = wave_inclusive_scan_u64(delta);
+    const uint64_t slot0 = (uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)slot);
+    const uint64_t total = readlane_u64(incl, 63);
     for (int l = 1; l <= a.tree.depth; ++l) {
-        const uint64_t key = my >> (kFanoutLog2 * l);
-        const uint64_t k0 = __shfl(key, 0, kWave);
-        const uint64_t k1 = wave_max_u64(key);  // the other node, if the wave spans two
-        const uint64_t sa = wave_sum_u64(key == k0 ? delta : 0ull);
-        const uint64_t sb = wave_sum_u64(key != k0 ? delta : 0ull);
+        const int shift = kFanoutLog2 * l;
+        const uint64_t k0 = slot0 >> shift;
+        const uint64_t span = ((k0 + 1) << shift) - slot0;  // lanes under node k0
+        const uint64_t sa = span >= 64 ? total : readlane_u64(incl, (int)span - 1);
+        const uint64_t sb = total - sa;
         if (lane == 0) {
             if (sa) atomicAdd(reinterpret_cast<unsigned long long*>(a.tree.level[l] + k0), sa);
-            if (k1 != k0 && sb) atomicAdd(reinterpret_cast<unsigned long long*>(a.tree.level[l] + k1), sb);
+            if (span < 64 && sb) atomicAdd(reinterpret_cast<unsigned long long*>(a.tree.level[l] + k0 + 1), sb);
         }
     }
 }
@@ -185,8 +196,8 @@ hipError_t launch_ingest(const IngestArgs& a, hipStream_t s) {
     const int64_t copy_blocks = (total_vec + kThreads * kCopyUnroll - 1) / (kThreads * kCopyUnroll);
     const dim3 grid((unsigned)(copy_blocks + meta_blocks));
     switch (vec) {
-        case 16: hipLaunchKernelGGL((k_ingest<uint4, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
-        case 8: hipLaunchKernelGGL((k_ingest<uint2, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
+        case 16: hipLaunchKernelGGL((k_ingest<u32x4, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
+        case 8: hipLaunchKernelGGL((k_ingest<u32x2, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
         case 4: hipLaunchKernelGGL((k_ingest<uint32_t, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
         default: hipLaunchKernelGGL((k_ingest<uint8_t, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
     }

@@ -54,6 +54,10 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
             flag_error(a.err, ERR_UPDATE_INDEX);
             valid = false;
         }
+        // the old leaf is needed only by the winner, but its load is issued now so
+        // it overlaps the LDS dedupe and the quantiser (chunks before this one
+        // finished their leaf writes before the barrier above)
+        const uint32_t old = valid ? tr.leaves[slot] : 0u;
         uint32_t h = 0;
         if (valid) {
             pmax = p > pmax ? p : pmax;
@@ -68,8 +72,9 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
         }
         __syncthreads();
         if (valid && owner[h] == tid) {
-            const uint32_t q = quantise_leaf(p, tr.alpha_num, tr.alpha_den, tr.frac_bits, &bad_q);
-            const uint32_t old = tr.leaves[slot];
+            const uint64_t qf = quantise_leaf(p, tr.alpha_num, tr.alpha_den, tr.frac_bits);
+            bad_q |= (qf >> 32) != 0;
+            const uint32_t q = (uint32_t)qf;
             tr.leaves[slot] = q;
             const uint64_t delta = (uint64_t)q - (uint64_t)old;  // modulo 2^64
             if (delta) {

@@ -25,8 +25,8 @@ def _mk(cap, obs_shape, obs_dtype=torch.uint8, **kw):
 def test_leaf_quantiser_matches_oracle(a, b):
     print(f"leaf quantiser alpha={a}/{b}", flush=True)
     rng = np.random.default_rng(100 + 10 * a + b)
-    p = rng.integers(0, 1 << 32, size=8192, dtype=np.uint64).astype(np.uint32)
-    p[:4096] = rng.integers(0, 1 << 16, size=4096).astype(np.uint32)
+    p = rng.integers(0, 1 << 32, size=1 << 20, dtype=np.uint64).astype(np.uint32)
+    p[:1 << 17] = np.arange(1 << 17, dtype=np.uint32)  # every priority below 2^17
     edge = np.array([0, 1, 2, 3, 4095, 4096, (1 << 31) - 1, 1 << 31, (1 << 32) - 2, (1 << 32) - 1], np.uint32)
     p[:len(edge)] = edge
     powers = np.array([k ** b for k in range(1, 300) if k ** b < (1 << 32)], np.uint64).astype(np.uint32)
@@ -36,7 +36,7 @@ def test_leaf_quantiser_matches_oracle(a, b):
     buf.ingest(torch.zeros((n, 4), dtype=torch.uint8, device="cuda"), prio=dev(p))
     assert buf.sync_check() == cd.OK, cd.last_error()
     leaves = read_col(buf, cd.COL_LEAVES, n * 4, np.uint32)
-    want = np.array([oracle.leaf(int(x), a, b) for x in p], np.uint32)
+    want = oracle.leaves(p, a, b)
     assert np.array_equal(leaves, want), np.flatnonzero(leaves != want)[:10]
     tree_consistent(buf, n)
     buf.close()

@@ -40,6 +40,11 @@ def test_leaf_random_full_range(a, b):
         assert oracle.leaf(int(p), a, b) == brute.leaf(int(p), a, b), (a, b, p)
 
 
+def test_leaf_many_matches_scalar():
+    p = np.random.default_rng(2).integers(0, 1 << 32, size=500, dtype=np.uint64).astype(np.uint32)
+    assert list(oracle.leaves(p, 2, 3)) == [oracle.leaf(int(x), 2, 3) for x in p]
+
+
 def test_leaf_closed_forms():
     assert oracle.frac_bits(3, 5) == 12
     for p in [1, 2, 17, 1 << 20, (1 << 32) - 1]:
