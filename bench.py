@@ -3,7 +3,10 @@
 Headline workload (the configuration the metric is quoted on): DQN replay of
 1,000,000 single 84x84 uint8 frames, frame stack 4, batch 512, proportional
 prioritisation alpha 0.6 / beta 0.4.  One step = ingest 512 new frames + sample
-512 + gather/transform 512 -> [512, 4, 84, 84] fp32 + priority update 512.
+512 + gather/transform 512 -> [512, 4, 84, 84] fp32 + priority update 512, with
+sampling and gathering through the fused conduit_sample_gather call (the step
+through separate conduit_sample / conduit_gather_transform calls is reported
+beside it).
 Inputs (frames of the steps, uniforms, new priorities) are resident in HBM
 before the timed region.
 
@@ -90,7 +93,7 @@ def bench_dqn(steps, warmup):
     L = cd.lib()
     stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
     Cap, B, K, prefill, chunk = 1_000_000, 512, 4, 1_050_000, 4096
-    iters = warmup + 2 * steps  # clean timed pass + instrumented pass
+    iters = warmup + 3 * steps  # timed fused pass + timed unfused pass + instrumented pass
     cfg = synth.DQN(prefill + iters * B)
     buf = cd.ReplayBuffer(Cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4)
     t0 = time.time()
@@ -149,13 +152,20 @@ def bench_dqn(steps, warmup):
         trans.append(t)
     h = C.c_void_p(buf.handle)
     ing, smp, gat, upd = L.conduit_ingest, L.conduit_sample, L.conduit_gather_transform, L.conduit_update_priorities
+    sgat = L.conduit_sample_gather
     pu = [u_d[i].data_ptr() for i in range(iters)]
     pp = [prio_d[i].data_ptr() for i in range(iters)]
     pi = [idx[i].data_ptr() for i in range(iters)]
     pw = [w[i].data_ptr() for i in range(iters)]
     xfr, lbr = C.byref(xf), C.byref(lb)
 
-    def step(i):
+    def step(i):  # ingest, fused sample + gather (+ IS weights), priority update
+        r = ing(h, C.byref(trans[i]), stream)
+        r |= sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
+        r |= upd(h, pi[i], pp[i], B, stream)
+        return r
+
+    def step_unfused(i):  # the same step with separate sample and gather calls
         r = ing(h, C.byref(trans[i]), stream)
         r |= smp(h, B, pu[i], pi[i], pw[i], stream)
         r |= gat(h, pi[i], B, xfr, lbr, stream)
@@ -165,7 +175,7 @@ def bench_dqn(steps, warmup):
     for i in range(warmup):
         assert step(i) == 0, cd.last_error()
     torch.cuda.synchronize()
-    # clean timed pass
+    # timed pass
     e_start = tm.ev()
     h0 = time.perf_counter()
     rc = 0
@@ -176,37 +186,48 @@ def bench_dqn(steps, warmup):
     torch.cuda.synchronize()
     assert rc == 0, cd.last_error()
     total_ms = e_start.elapsed_time(e_end)
+    # the same number of steps through the unfused calls
+    u_start = tm.ev()
+    for i in range(warmup + steps, warmup + 2 * steps):
+        rc |= step_unfused(i)
+    u_end = tm.ev()
+    torch.cuda.synchronize()
+    assert rc == 0, cd.last_error()
+    unfused_ms = u_start.elapsed_time(u_end)
     # instrumented pass: an event between consecutive calls
     evs = []
-    for i in range(warmup + steps, warmup + 2 * steps):
+    for i in range(warmup + 2 * steps, warmup + 3 * steps):
         e = [tm.ev()]
         ing(h, C.byref(trans[i]), stream)
         e.append(tm.ev())
-        smp(h, B, pu[i], pi[i], pw[i], stream)
-        e.append(tm.ev())
-        gat(h, pi[i], B, xfr, lbr, stream)
+        sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
         e.append(tm.ev())
         upd(h, pi[i], pp[i], B, stream)
         e.append(tm.ev())
         evs.append(e)
     torch.cuda.synchronize()
     assert buf.sync_check() == cd.OK, cd.last_error()
-    # the dominant kernel alone: the gathers of the timed steps' own batches,
-    # launched back to back between two events on the library's stream
-    gb0 = tm.ev()
+    # kernels alone, back to back between two events on the library's stream,
+    # over the timed steps' own inputs: the fused sample + gather (the dominant
+    # kernel of the step) and the stand-alone gather of the same batches
+    fb0 = tm.ev()
+    for i in range(warmup, warmup + steps):
+        sgat(h, B, pu[i], pi[i], None, xfr, lbr, stream)
+    fb1 = tm.ev()
     for i in range(warmup, warmup + steps):
         gat(h, pi[i], B, xfr, lbr, stream)
     gb1 = tm.ev()
     torch.cuda.synchronize()
-    gather_b2b_ms = gb0.elapsed_time(gb1) / steps
-    names = ["ingest_512", "sample_512", "gather_512", "update_512"]
+    fused_b2b_ms = fb0.elapsed_time(fb1) / steps
+    gather_b2b_ms = fb1.elapsed_time(gb1) / steps
+    names = ["ingest_512", "sample_gather_512", "update_512"]
     per = {n: [e[k].elapsed_time(e[k + 1]) for e in evs] for k, n in enumerate(names)}
     kern = {n: _kernel_stats(v) for n, v in per.items()}
 
     # algorithmic bytes of the gather of the last instrumented step: frames the
     # stack actually reads (zero-filled frames are not read), 4x-wide writes,
     # plus the index and the three scalar columns
-    last = idx[warmup + 2 * steps - 1].cpu().numpy()
+    last = idx[warmup + steps - 1].cpu().numpy()
     ep_col = torch.empty(Cap * 4, dtype=torch.uint8, device="cuda")
     st_col = torch.empty(Cap * 4, dtype=torch.uint8, device="cuda")
     buf.read(cd.COL_EPISODE, ep_col)
@@ -222,11 +243,16 @@ def bench_dqn(steps, warmup):
                 valid += 1
     row = 84 * 84
     gather_bytes = valid * row + B * (8 + 4 + 4 + 1) + B * K * row * 4 + B * (4 + 4 + 1)
+    # the fused kernel also reads each sample's uniform and the 64 children of the
+    # node it visits at each of the tree's levels, and writes the index and leaf
+    depth = buf.info().tree_depth
+    fused_bytes = gather_bytes - B * 8 + B * (8 + depth * 64 * 8 + 8 + 4)
     ingest_bytes_per_frame = 2 * row + (4 + 4 + 1 + 4 + 4) * 2 + 4 + 4  # obs r+w, scalars r+w, leaf r+w
     buf.close()
     return {
         "B": B, "steps": steps, "warmup": warmup, "total_ms": total_ms, "host_enqueue_s": host_enqueue_s,
-        "gather_b2b_ms": gather_b2b_ms,
+        "gather_b2b_ms": gather_b2b_ms, "fused_b2b_ms": fused_b2b_ms, "fused_bytes": fused_bytes,
+        "unfused_ms": unfused_ms,
         "kernels": kern, "gather_bytes": gather_bytes, "valid_frames": valid, "prefill_s": prefill_s,
         "ingest_big": {"frames": 32768, "ms": ingest_big_ms,
                        "GBps": 32768 * ingest_bytes_per_frame / ingest_big_ms / 1e6},
@@ -501,9 +527,9 @@ def calibrate_copy():
 
 
 def _traffic_from_profile(kernel_src):
-    """HBM bytes per gather launch from the committed counter summary, if it was
-    taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "gather_dqn_counters.txt")
+    """HBM bytes per fused sample + gather launch from the committed counter
+    summary, if it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "sample_gather_dqn_counters.txt")
     if not os.path.exists(path):
         return None
     rec = {}
@@ -534,7 +560,9 @@ def main():
     ms_per_step = d["total_ms"] / args.steps
     value = d["B"] * args.steps / (d["total_ms"] / 1e3)
     g_ms = d["gather_b2b_ms"]
-    achieved = d["gather_bytes"] / g_ms / 1e6
+    g_gbps = d["gather_bytes"] / g_ms / 1e6
+    f_ms = d["fused_b2b_ms"]
+    achieved = d["fused_bytes"] / f_ms / 1e6
     kernel_src = os.path.join(ROOT, "paper_2609_24456_amd", "csrc", "k_gather.hip")
     out = {
         "metric": METRIC,
@@ -553,13 +581,16 @@ def main():
                                "batch 512, PER alpha 0.6 beta 0.4; step = ingest 512 + sample 512 + "
                                "gather 512 -> [512,4,84,84] fp32 + priority update 512",
                    "capacity": 1_000_000, "batch": 512, "frame_stack": 4},
-        "gather_GBps": achieved,
-        "gather_frac_of_peak": achieved / PEAK_HBM_GBPS,
-        "roofline": {"bound": "hbm", "kernel": "k_gather_pipe<U8_F32> (DQN frame-stack gather, 512 x 4 frames)",
+        "gather_GBps": g_gbps,
+        "gather_frac_of_peak": g_gbps / PEAK_HBM_GBPS,
+        "gather_kernel": "k_gather_pipe<U8_F32> alone over the timed steps' batches, back to back",
+        "ms_per_step_unfused": d["unfused_ms"] / args.steps,
+        "roofline": {"bound": "hbm", "kernel": "k_sample_gather<U8_F32> (fused sampling + frame-stack gather, "
+                                               "512 samples x 4 frames; the dominant kernel of the step)",
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": _traffic_from_profile(kernel_src),
-                     "algorithmic_bytes_per_launch": d["gather_bytes"], "avg_launch_us": g_ms * 1e3,
-                     "timing": "HIP events around the gathers of the timed steps' batches, launched back to back"},
+                     "algorithmic_bytes_per_launch": d["fused_bytes"], "avg_launch_us": f_ms * 1e3,
+                     "timing": "HIP events around back-to-back launches over the timed steps' uniforms"},
         "kernels_us_in_step": {k: v["mean_us"] for k, v in d["kernels"].items()},
         "host_enqueue_us_per_step": d["host_enqueue_s"] * 1e6 / args.steps,
         "rows": {"dqn_ingest_32768": d["ingest_big"]},

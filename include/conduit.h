@@ -266,6 +266,18 @@ conduit_status conduit_gather_transform(conduit_buffer* buf, const int64_t* idx,
                                         const conduit_transform* xf, const conduit_learner_batch* out,
                                         void* stream);
 
+/*
+ * Fused delivery: exactly conduit_sample(buf, batch, uniforms, idx_out, is_w_out)
+ * followed by conduit_gather_transform(buf, idx_out, batch, xf, out), with the
+ * same outputs, arguments and errors as the two calls, but the gather of each
+ * sample starts in the workgroup that sampled it (one launch fewer and no
+ * round trip of the indices through memory; the IS weights follow in a second
+ * small kernel).  Ragged buffers run the two steps back to back.
+ */
+conduit_status conduit_sample_gather(conduit_buffer* buf, int64_t batch, const uint64_t* uniforms, int64_t* idx_out,
+                                     float* is_w_out, const conduit_transform* xf, const conduit_learner_batch* out,
+                                     void* stream);
+
 /* ---------------------------------------------------------------------------
  * Returns / advantages (Sec. 2.2 on-policy ingestion "computing
  * returns/advantages"; GAE as used by PPO, Schulman et al.)
@@ -280,7 +292,7 @@ conduit_status conduit_gather_transform(conduit_buffer* buf, const int64_t* idx,
  * it); V_T = bootstrap[e].  rewards float [T,E]; values float [T,E] or NULL (0);
  * dones uint8 [T,E]; bootstrap float [E] or NULL (0); adv, ret float [T,E]
  * outputs.  Arithmetic in fp64 inside, fp32 out.
- * Errors: EINVAL (T, E < 0, NULL required pointers), ESTATE.
+ * Errors: EINVAL (T, E < 0, E > 2^19, NULL required pointers), ESTATE.
  */
 conduit_status conduit_gae(const float* rewards, const float* values, const uint8_t* dones,
                            const float* bootstrap, int64_t T, int64_t E, double gamma, double lambda,

@@ -75,6 +75,7 @@ SIGNATURES = {
     "conduit_update_priorities": (ST, [P, P, P, I64, P]),
     "conduit_sample": (ST, [P, I64, P, P, P, P]),
     "conduit_gather_transform": (ST, [P, P, I64, P, P, P]),
+    "conduit_sample_gather": (ST, [P, I64, P, P, P, P, P, P]),
     "conduit_gae": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_gae_packed": (ST, [P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_minibatch_gather": (ST, [P, I64, I64, P, I64, P, P, P, P, I32_, P]),
@@ -223,6 +224,23 @@ def conduit_gather_transform(handle, idx, xf, obs=None, action=None, reward=None
                                           C.byref(out), _stream(stream)))
 
 
+def conduit_sample_gather(handle, batch, uniforms, idx_out, is_w_out, xf, obs=None, action=None, reward=None,
+                          done=None, mask=None, aux=None, length=None, stream=None):
+    if uniforms.numel() < batch or idx_out.numel() < batch or (is_w_out is not None and is_w_out.numel() < batch):
+        raise ValueError("uniforms/outputs smaller than batch")
+    out = LearnerBatch()
+    out.obs = _ptr(obs, None, "obs")
+    out.action = _ptr(action, None, "action")
+    out.reward = _ptr(reward, torch.float32, "reward")
+    out.done = _ptr(done, torch.uint8, "done")
+    out.mask = _ptr(mask, None, "mask")
+    out.aux = _ptr(aux, None, "aux")
+    out.length = _ptr(length, torch.int32, "length")
+    _check(lib().conduit_sample_gather(handle, batch, _ptr(uniforms, None, "uniforms"),
+                                       _ptr(idx_out, torch.int64, "idx_out"), _ptr(is_w_out, torch.float32, "is_w_out"),
+                                       C.byref(xf), C.byref(out), _stream(stream)))
+
+
 def conduit_gae(rewards, values, dones, bootstrap, gamma, lam, adv, ret, stream=None):
     T, E = rewards.shape
     _check(lib().conduit_gae(_ptr(rewards, torch.float32, "rewards"), _ptr(values, torch.float32, "values"),
@@ -314,6 +332,14 @@ class ReplayBuffer:
         idx_out = torch.empty(B, dtype=torch.int64, device=dev) if idx_out is None else idx_out
         w_out = torch.empty(B, dtype=torch.float32, device=dev) if w_out is None else w_out
         conduit_sample(self.handle, B, uniforms, idx_out, w_out, stream)
+        return idx_out, w_out
+
+    def sample_gather(self, uniforms, xf, idx_out=None, w_out=None, **outs):
+        B = uniforms.numel()
+        dev = uniforms.device
+        idx_out = torch.empty(B, dtype=torch.int64, device=dev) if idx_out is None else idx_out
+        w_out = torch.empty(B, dtype=torch.float32, device=dev) if w_out is None else w_out
+        conduit_sample_gather(self.handle, B, uniforms, idx_out, w_out, xf, stream=outs.pop("stream", None), **outs)
         return idx_out, w_out
 
     def gather(self, idx, xf, **outs):

@@ -510,15 +510,10 @@ static void fill_norm(GatherArgs& a, const conduit_transform* xf, int64_t row_by
     }
 }
 
-conduit_status conduit_gather_transform(conduit_buffer* b, const int64_t* idx, int64_t n, const conduit_transform* xf,
-                                        const conduit_learner_batch* out, void* stream) {
-    if (!b || !xf || !out) return fail(CONDUIT_EINVAL, "NULL buffer, transform or output");
-    conduit_status st = check_flags(b->err_slot);
-    if (st != CONDUIT_OK) return st;
-    if (n < 0) return fail(CONDUIT_EINVAL, "n must be >= 0");
-    if (n == 0) return CONDUIT_OK;
-    if (!idx) return fail(CONDUIT_EINVAL, "idx must not be NULL");
-    DeviceGuard g(b->device);
+// Validate a learner-batch request against the buffer and fill the kernel
+// arguments (dense: GatherArgs, ragged: PackArgs).
+static conduit_status prepare_gather(conduit_buffer* b, const int64_t* idx, int64_t n, const conduit_transform* xf,
+                                     const conduit_learner_batch* out, GatherArgs* ga, PackArgs* pa) {
     const conduit_buffer_opts& o = b->opts;
     if (o.ragged) {
         if (xf->kind != CONDUIT_XF_TOKENS_PAD) return fail(CONDUIT_EINVAL, "ragged buffers gather with TOKENS_PAD");
@@ -547,11 +542,10 @@ conduit_status conduit_gather_transform(conduit_buffer* b, const int64_t* idx, i
         a.done = b->done;
         a.out_done = out->done;
         a.err = err_words(b->err_slot);
-        hipError_t e = launch_pack(a, static_cast<hipStream_t>(stream));
-        if (e != hipSuccess) return hip_fail(e, "pack launch");
+        *pa = a;
         return CONDUIT_OK;
     }
-    st = check_xform(xf, b->layout.row_bytes, b->obs_dtype);
+    conduit_status st = check_xform(xf, b->layout.row_bytes, b->obs_dtype);
     if (st != CONDUIT_OK) return st;
     if (reinterpret_cast<uintptr_t>(out->obs) % 16) return fail(CONDUIT_EINVAL, "obs output must be 16-byte aligned");
     GatherArgs a{};
@@ -577,14 +571,69 @@ conduit_status conduit_gather_transform(conduit_buffer* b, const int64_t* idx, i
     a.ncols = 0;
     a.err = err_words(b->err_slot);
     a.err_kind = ERR_GATHER_INDEX;
-    hipError_t e = launch_gather(a, static_cast<hipStream_t>(stream));
+    *ga = a;
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_gather_transform(conduit_buffer* b, const int64_t* idx, int64_t n, const conduit_transform* xf,
+                                        const conduit_learner_batch* out, void* stream) {
+    if (!b || !xf || !out) return fail(CONDUIT_EINVAL, "NULL buffer, transform or output");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (n < 0) return fail(CONDUIT_EINVAL, "n must be >= 0");
+    if (n == 0) return CONDUIT_OK;
+    if (!idx) return fail(CONDUIT_EINVAL, "idx must not be NULL");
+    GatherArgs ga{};
+    PackArgs pa{};
+    st = prepare_gather(b, idx, n, xf, out, &ga, &pa);
+    if (st != CONDUIT_OK) return st;
+    DeviceGuard g(b->device);
+    hipError_t e = b->opts.ragged ? launch_pack(pa, static_cast<hipStream_t>(stream))
+                                  : launch_gather(ga, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "gather launch");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_sample_gather(conduit_buffer* b, int64_t batch, const uint64_t* uniforms, int64_t* idx_out,
+                                     float* is_w_out, const conduit_transform* xf, const conduit_learner_batch* out,
+                                     void* stream) {
+    if (!b || !xf || !out) return fail(CONDUIT_EINVAL, "NULL buffer, transform or output");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (!b->opts.prioritized) return fail(CONDUIT_EINVAL, "buffer was created without priorities");
+    if (batch < 1 || batch > (1LL << 20)) return fail(CONDUIT_EINVAL, "batch must be in [1, 2^20]");
+    if (!uniforms || !idx_out) return fail(CONDUIT_EINVAL, "uniforms and idx_out must not be NULL");
+    if (b->size == 0) return fail(CONDUIT_EEMPTY, "sample from an empty buffer");
+    GatherArgs ga{};
+    PackArgs pa{};
+    st = prepare_gather(b, idx_out, batch, xf, out, &ga, &pa);
+    if (st != CONDUIT_OK) return st;
+    DeviceGuard g(b->device);
+    SampleArgs sa{};
+    sa.tree = b->tree;
+    sa.uniforms = uniforms;
+    sa.idx_out = idx_out;
+    sa.w_out = is_w_out;
+    sa.batch = batch;
+    sa.beta = b->opts.beta;
+    sa.state = b->state;
+    sa.err = err_words(b->err_slot);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (b->opts.ragged) {  // sequences: the sampler, then the packing kernel
+        e = launch_sample(sa, s);
+        if (e == hipSuccess) e = launch_pack(pa, s);
+    } else {
+        e = launch_sample_gather(SampleGatherArgs{sa, ga}, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "sample_gather launch");
     return CONDUIT_OK;
 }
 
 conduit_status conduit_gae(const float* rewards, const float* values, const uint8_t* dones, const float* bootstrap,
                            int64_t T, int64_t E, double gamma, double lambda, float* adv, float* ret, void* stream) {
     if (T < 0 || E < 0) return fail(CONDUIT_EINVAL, "T and E must be >= 0");
+    if (E > kGaeMaxEnvs) return fail(CONDUIT_EINVAL, "E must be at most 2^19 environments");
     if (T == 0 || E == 0) return CONDUIT_OK;
     if (!rewards || !dones || !adv || !ret) return fail(CONDUIT_EINVAL, "rewards, dones, adv and ret must not be NULL");
     if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");

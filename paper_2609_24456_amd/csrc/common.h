@@ -204,6 +204,56 @@ __device__ __forceinline__ uint64_t quantise_leaf(uint32_t p, int a, int b, int 
 }
 
 // ---------------------------------------------------------------------------
+// stratified inverse-CDF descent of the 64-ary tree by one wavefront
+// ---------------------------------------------------------------------------
+struct Descent {
+    int64_t slot;   // sampled slot, -1 if the tree is empty
+    uint32_t leaf;  // its quantised priority
+    bool lost;      // no child exceeded the target (never expected)
+};
+
+// Stratum k of B: target t = floor((k*Q + floor(u*Q / 2^64)) / B), evaluated
+// without 128-bit division by splitting Q and the high product word into
+// quotient and remainder by B (every term fits 64 bits since k < B <= 2^20).
+// At each level the 64 lanes load the 64 children of the current node, take an
+// inclusive wavefront prefix sum, and the first lane whose prefix exceeds the
+// target (ballot + find-first-set) names the child; its exclusive prefix is
+// subtracted from the target.  This is "first slot whose inclusive prefix sum
+// exceeds t" with half-open intervals, so zero leaves are never chosen.  The
+// total, the uniform and the root's children are independent loads, issued
+// together: depth dependent loads in all.  All lanes return the same result.
+__device__ __forceinline__ Descent tree_descend(const TreeView& tr, const uint64_t* uniforms, int64_t k, int64_t batch) {
+    const int lane = lane_id();
+    const int top = tr.depth;
+    const uint64_t Q = tr.level[top][0];
+    const uint64_t u = uniforms[k];
+    uint64_t v = top == 1 ? (uint64_t)tr.leaves[lane] : tr.level[top - 1][lane];
+    Descent r{-1, 0u, false};
+    if (Q == 0ull) return r;
+    const uint64_t B = (uint64_t)batch;
+    const uint64_t h = __umul64hi(u, Q);
+    const uint64_t kk = (uint64_t)k;
+    uint64_t t = kk * (Q / B) + h / B + (kk * (Q % B) + h % B) / B;
+    uint64_t node = 0;
+    for (int l = top; l >= 1; --l) {
+        if (l != top) {
+            const uint64_t child = node * kFanout + (uint64_t)lane;
+            v = l == 1 ? (uint64_t)tr.leaves[child] : tr.level[l - 1][child];
+        }
+        const uint64_t incl = wave_inclusive_scan_u64(v);
+        const uint64_t mask = __ballot(incl > t);
+        int sel = 63;
+        if (mask) sel = __ffsll((unsigned long long)mask) - 1; else r.lost = true;
+        const uint64_t excl = __shfl(incl - v, sel, kWave);
+        t -= excl;
+        node = node * kFanout + (uint64_t)sel;
+        if (l == 1) r.leaf = (uint32_t)__shfl(v, sel, kWave);
+    }
+    r.slot = (int64_t)node;
+    return r;
+}
+
+// ---------------------------------------------------------------------------
 // kernel launch entry points (host functions defined next to each kernel)
 // ---------------------------------------------------------------------------
 struct IngestArgs {
@@ -302,6 +352,16 @@ struct GatherArgs {
 
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 
+// fused sample -> gather: the sampler's arguments plus the gather's (whose idx
+// is the sampler's idx_out and whose limit is the buffer size)
+struct SampleGatherArgs {
+    SampleArgs s;
+    GatherArgs g;
+};
+
+hipError_t launch_sample_gather(const SampleGatherArgs& a, hipStream_t s);
+hipError_t launch_is_weights(const SampleArgs& a, hipStream_t s);
+
 struct PackArgs {
     const int64_t* idx;
     int64_t n;
@@ -326,6 +386,9 @@ struct PackArgs {
 };
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+
+// time-major GAE addresses a slab of the rollout with 32-bit offsets
+constexpr int64_t kGaeMaxEnvs = 1ll << 19;
 
 struct GaeArgs {
     const float* reward;

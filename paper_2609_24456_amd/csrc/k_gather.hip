@@ -72,10 +72,11 @@ __device__ void gather_scalars(const GatherArgs& a, int64_t block) {
     for (int c = 0; c < a.ncols; ++c) a.cols_out[c][b] = ok ? a.cols[c][i] : 0.0f;
 }
 
-// per-workgroup table of the exact u8 -> bf16 normalisation, 256 entries per plane
-__device__ __forceinline__ void build_lut(const GatherArgs& a, uint16_t* lut) {
+// per-workgroup table of the exact u8 -> bf16 normalisation, 256 entries per
+// plane, built by lanes [first, first + count)
+__device__ __forceinline__ void build_lut(const GatherArgs& a, uint16_t* lut, int first = 0, int count = kThreads) {
     const int planes = (int)((a.row_bytes >> 2) / a.plane_units);
-    for (int e = threadIdx.x; e < planes * 256; e += kThreads) {
+    for (int e = (int)threadIdx.x - first; e < planes * 256; e += count) {
         const int c = e >> 8;
         const float v = u8_unit_f32((uint32_t)(e & 255));
         const float centred = v - a.mean[c];
@@ -196,6 +197,71 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
     finish<XF, NT>(a, t, v, si, sj, ei, ej, lut);
 }
 
+// Fused sampler + gather: one workgroup per sample.  Wavefront 0 descends the
+// tree (tree_descend) while the other lanes build the bf16 table if needed; the
+// whole workgroup then gathers the sample's frames, double-buffered across its
+// items, and writes the scalar columns.  Saves the sampler's index round trip
+// and one launch against conduit_sample followed by conduit_gather_transform.
+template <int XF, bool NT>
+__global__ __launch_bounds__(kThreads) void k_sample_gather(SampleGatherArgs sg, int32_t bpf) {
+    __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
+    __shared__ int64_t s_slot;
+    const GatherArgs& a = sg.g;
+    const int64_t b = blockIdx.x;
+    if (threadIdx.x < kWave) {
+        const Descent d = tree_descend(sg.s.tree, sg.s.uniforms, b, sg.s.batch);
+        if (threadIdx.x == 0) {
+            s_slot = d.slot;
+            sg.s.idx_out[b] = d.slot;
+            if (sg.s.w_out) reinterpret_cast<uint32_t*>(sg.s.w_out)[b] = d.leaf;  // for k_is_weights
+            if (d.slot < 0 && b == 0) flag_error(sg.s.err, ERR_EMPTY_TREE);
+            if (d.lost) flag_error(sg.s.err, ERR_DESCENT);
+        }
+    } else if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
+        build_lut(a, lut, kWave, kThreads - kWave);
+    }
+    __syncthreads();
+    const int64_t i = s_slot;
+    const bool ok = i >= 0 && i < a.limit;
+    // scalar columns of the sampled slot
+    if (a.out_action && a.action_bytes > 0) {
+        if ((a.action_bytes & 3) == 0) {
+            for (int c = threadIdx.x; c < a.action_bytes / 4; c += kThreads)
+                reinterpret_cast<uint32_t*>(a.out_action + b * a.action_bytes)[c] =
+                    ok ? reinterpret_cast<const uint32_t*>(a.action + i * a.action_bytes)[c] : 0u;
+        } else {
+            for (int c = threadIdx.x; c < a.action_bytes; c += kThreads)
+                a.out_action[b * a.action_bytes + c] = ok ? a.action[i * a.action_bytes + c] : (uint8_t)0;
+        }
+    }
+    if (threadIdx.x == 0) {
+        if (a.out_reward) a.out_reward[b] = ok ? a.reward[i] : 0.0f;
+        if (a.out_done) a.out_done[b] = ok ? a.done[i] : (uint8_t)0;
+    }
+    const int64_t per_row = (int64_t)bpf * a.stack;
+    if (per_row == 0) return;
+    const int64_t it0 = b * per_row, it_end = it0 + per_row;
+    uint32_t va[kUnroll], vb[kUnroll];
+    int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
+    uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
+    Item ta = decode(a, it0, bpf, i), tb;
+    issue(a, ta, i, va, sia, sja, eia, eja);
+    for (int64_t it = it0; it < it_end; it += 2) {
+        const bool has_b = it + 1 < it_end;  // uniform
+        if (has_b) {
+            tb = decode(a, it + 1, bpf, i);
+            issue(a, tb, i, vb, sib, sjb, eib, ejb);
+        }
+        finish<XF, NT>(a, ta, va, sia, sja, eia, eja, lut);
+        if (!has_b) break;
+        if (it + 2 < it_end) {
+            ta = decode(a, it + 2, bpf, i);
+            issue(a, ta, i, va, sia, sja, eia, eja);
+        }
+        finish<XF, NT>(a, tb, vb, sib, sjb, eib, ejb, lut);
+    }
+}
+
 // Persistent workgroups walk the items with a stride of the grid.  Two register
 // sets alternate: the loads of the next item are issued before the stores of
 // the current one, so reads of one item overlap the writes of the previous one
@@ -247,7 +313,10 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
     }
 }
 
-// ragged token packing: one workgroup per sample, 4 elements per lane step
+// ragged token packing: one workgroup per sample; each lane handles up to 4
+// quads (16 elements) per pass, all loads issued before the stores
+constexpr int kPackQuads = 4;
+
 __global__ __launch_bounds__(kThreads) void k_pack(PackArgs a) {
     const int64_t b = blockIdx.x;
     const int64_t i = a.idx[b];
@@ -259,34 +328,40 @@ __global__ __launch_bounds__(kThreads) void k_pack(PackArgs a) {
     const int32_t* __restrict__ seq = reinterpret_cast<const int32_t*>(a.seq) + (ok ? i : 0) * a.max_len;
     const float* __restrict__ aux = a.aux ? reinterpret_cast<const float*>(a.aux) + (ok ? i : 0) * a.max_len : nullptr;
     const int64_t quads = a.max_len >> 2;
-    for (int64_t q = threadIdx.x; q < quads; q += kThreads) {
-        const int64_t t = q * 4;
-        int4 tok;
-        f32x4 lp;
-        uint32_t m;
-        if (t + 3 < L) {
-            tok = *reinterpret_cast<const int4*>(seq + t);
-            if (aux) lp = *reinterpret_cast<const f32x4*>(aux + t);
-            m = 0x01010101u;
-        } else {
-            tok.x = t + 0 < L ? seq[t + 0] : a.pad_id;
-            tok.y = t + 1 < L ? seq[t + 1] : a.pad_id;
-            tok.z = t + 2 < L ? seq[t + 2] : a.pad_id;
-            tok.w = t + 3 < L ? seq[t + 3] : a.pad_id;
-            if (aux) {
-                lp.x = t + 0 < L ? aux[t + 0] : 0.0f;
-                lp.y = t + 1 < L ? aux[t + 1] : 0.0f;
-                lp.z = t + 2 < L ? aux[t + 2] : 0.0f;
-                lp.w = t + 3 < L ? aux[t + 3] : 0.0f;
+    for (int64_t q0 = threadIdx.x; q0 < quads; q0 += kThreads * kPackQuads) {
+        int4 tok[kPackQuads];
+        f32x4 lp[kPackQuads];
+        uint32_t m[kPackQuads];
+#pragma unroll
+        for (int r = 0; r < kPackQuads; ++r) {
+            const int64_t q = q0 + (int64_t)r * kThreads;
+            const int64_t t = q * 4;
+            if (q < quads && t + 3 < L) {
+                tok[r] = *reinterpret_cast<const int4*>(seq + t);
+                lp[r] = aux ? *reinterpret_cast<const f32x4*>(aux + t) : (f32x4)(0.0f);
+                m[r] = 0x01010101u;
+            } else {
+                tok[r].x = t + 0 < L ? seq[t + 0] : a.pad_id;
+                tok[r].y = t + 1 < L ? seq[t + 1] : a.pad_id;
+                tok[r].z = t + 2 < L ? seq[t + 2] : a.pad_id;
+                tok[r].w = t + 3 < L ? seq[t + 3] : a.pad_id;
+                lp[r].x = (aux && t + 0 < L) ? aux[t + 0] : 0.0f;
+                lp[r].y = (aux && t + 1 < L) ? aux[t + 1] : 0.0f;
+                lp[r].z = (aux && t + 2 < L) ? aux[t + 2] : 0.0f;
+                lp[r].w = (aux && t + 3 < L) ? aux[t + 3] : 0.0f;
+                m[r] = (t + 0 < L ? 0x1u : 0u) | (t + 1 < L ? 0x100u : 0u) | (t + 2 < L ? 0x10000u : 0u) |
+                       (t + 3 < L ? 0x1000000u : 0u);
             }
-            m = (t + 0 < L ? 0x1u : 0u) | (t + 1 < L ? 0x100u : 0u) | (t + 2 < L ? 0x10000u : 0u) |
-                (t + 3 < L ? 0x1000000u : 0u);
         }
-        const int64_t o = b * a.max_len + t;
-        *reinterpret_cast<int4*>(reinterpret_cast<int32_t*>(a.out_seq) + o) = tok;
-        if (a.out_aux && aux) *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out_aux) + o) = lp;
-        else if (a.out_aux) *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out_aux) + o) = (f32x4)(0.0f);
-        if (a.out_mask) *reinterpret_cast<uint32_t*>(a.out_mask + o) = m;
+#pragma unroll
+        for (int r = 0; r < kPackQuads; ++r) {
+            const int64_t q = q0 + (int64_t)r * kThreads;
+            if (q >= quads) continue;
+            const int64_t o = b * a.max_len + q * 4;
+            *reinterpret_cast<int4*>(reinterpret_cast<int32_t*>(a.out_seq) + o) = tok[r];
+            if (a.out_aux) *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out_aux) + o) = lp[r];
+            if (a.out_mask) *reinterpret_cast<uint32_t*>(a.out_mask + o) = m[r];
+        }
     }
     if (threadIdx.x == 0) {
         if (a.out_length) a.out_length[b] = (int32_t)L;
@@ -347,6 +422,30 @@ hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+hipError_t launch_sample_gather(const SampleGatherArgs& a, hipStream_t s) {
+    if (a.s.batch <= 0) return hipSuccess;
+    const GatherArgs& g = a.g;
+    const int64_t units = g.row_bytes >> 2;
+    const int64_t bpf = g.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
+    const dim3 grid((unsigned)a.s.batch), block(kThreads);
+    switch (g.xform) {
+        case CONDUIT_XF_NONE:
+            hipLaunchKernelGGL((k_sample_gather<CONDUIT_XF_NONE, true>), grid, block, 0, s, a, (int32_t)bpf);
+            break;
+        case CONDUIT_XF_U8_F32:
+            hipLaunchKernelGGL((k_sample_gather<CONDUIT_XF_U8_F32, true>), grid, block, 0, s, a, (int32_t)bpf);
+            break;
+        case CONDUIT_XF_U8_BF16_NORM:
+            hipLaunchKernelGGL((k_sample_gather<CONDUIT_XF_U8_BF16_NORM, true>), grid, block, 0, s, a, (int32_t)bpf);
+            break;
+        default:
+            return hipErrorInvalidValue;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_is_weights(a.s, s);
 }
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s) {

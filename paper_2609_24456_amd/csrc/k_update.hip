@@ -36,9 +36,13 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
     const int tid = threadIdx.x;
     const TreeView& tr = a.tree;
 
-    for (int i = tid; i < kBins; i += kThreads) bins[i] = 0ull;
     uint32_t pmax = 0;
     bool bad_q = false;
+    // the first chunk's index and priority loads are issued before the LDS set-up
+    int64_t k = tid;
+    int64_t slot_next = k < a.n ? a.idx[k] : -1;
+    uint32_t p_next = k < a.n ? a.prio[k] : 0u;
+    for (int i = tid; i < kBins; i += kThreads) bins[i] = 0ull;
 
     for (int64_t base = 0; base < a.n; base += kThreads) {
         for (int i = tid; i < kTable; i += kThreads) {
@@ -46,10 +50,10 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
             owner[i] = -1;
         }
         __syncthreads();
-        const int64_t k = base + tid;
+        k = base + tid;
         bool valid = k < a.n;
-        const int64_t slot = valid ? a.idx[k] : -1;
-        const uint32_t p = valid ? a.prio[k] : 0u;
+        const int64_t slot = slot_next;
+        const uint32_t p = p_next;
         if (valid && (slot < 0 || slot >= a.size)) {
             flag_error(a.err, ERR_UPDATE_INDEX);
             valid = false;
@@ -70,6 +74,10 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
             }
             atomicMax(&owner[h], tid);
         }
+        // the next chunk's loads overlap this chunk's dedupe and leaf work
+        const int64_t kn = base + kThreads + tid;
+        slot_next = kn < a.n ? a.idx[kn] : -1;
+        p_next = kn < a.n ? a.prio[kn] : 0u;
         __syncthreads();
         if (valid && owner[h] == tid) {
             const uint64_t qf = quantise_leaf(p, tr.alpha_num, tr.alpha_den, tr.frac_bits);

@@ -26,7 +26,8 @@ def _gae_gpu(r, v, d, b, gamma, lam):
 
 @pytest.mark.parametrize("T,E,p_done,with_v,with_b", [
     (1, 1, 0.0, True, True), (2, 3, 0.5, True, False), (37, 19, 0.05, True, True), (64, 16, 0.0, False, False),
-    (65, 17, 1.0, True, True), (200, 70, 0.01, True, True), (1000, 5, 0.002, True, True)])
+    (65, 17, 1.0, True, True), (200, 70, 0.01, True, True), (1000, 5, 0.002, True, True),
+    (2500, 9, 0.003, True, True), (1024, 8, 0.0, True, False), (3073, 3, 0.01, False, True)])
 def test_gae_time_major_shapes(T, E, p_done, with_v, with_b):
     print(f"gae T={T} E={E}", flush=True)
     rng = np.random.default_rng(T * 131 + E)
@@ -51,7 +52,7 @@ def test_gae_ppo_config_full_size():
 
 
 @pytest.mark.parametrize("B,Lmax,with_v", [(1, 4, False), (5, 8, True), (33, 260, True), (256, 4096, False),
-                                           (64, 4096, True)])
+                                           (64, 4096, True), (7, 4097, True), (5, 9000, True), (3, 12288, False)])
 def test_gae_packed(B, Lmax, with_v):
     print(f"gae packed B={B} Lmax={Lmax}", flush=True)
     rng = np.random.default_rng(B * 7 + Lmax)

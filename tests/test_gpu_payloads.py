@@ -14,7 +14,7 @@ pytestmark = pytest.mark.gpu
 from paper_2609_24456_amd import conduit as cd  # noqa: E402
 
 
-def run_large(cap, prefill, iters, batch, chunk, check_rows):
+def run_large(cap, prefill, iters, batch, chunk, check_rows, fused=False):
     cfg = synth.Large(prefill)
     u, prio = cfg.draws(iters, batch)
     shape = cfg.obs_shape
@@ -33,8 +33,11 @@ def run_large(cap, prefill, iters, batch, chunk, check_rows):
     act = torch.empty((batch, 6), dtype=torch.float32, device="cuda")
     rew = torch.empty(batch, dtype=torch.float32, device="cuda")
     for it in range(iters):
-        idx, w = buf.sample(dev(u[it]))
-        buf.gather(idx, xf, obs=out, action=act, reward=rew)
+        if fused:
+            idx, w = buf.sample_gather(dev(u[it]), xf, obs=out, action=act, reward=rew)
+        else:
+            idx, w = buf.sample(dev(u[it]))
+            buf.gather(idx, xf, obs=out, action=act, reward=rew)
         buf.update(idx, dev(prio[it]))
         o_idx, o_w = orc.sample(u[it])
         assert np.array_equal(host(idx), o_idx), it
@@ -54,9 +57,10 @@ def run_large(cap, prefill, iters, batch, chunk, check_rows):
     buf.close()
 
 
-def test_large_payload_reduced():
-    print("large: cap 600, prefill 700, batch 64 -> bf16", flush=True)
-    run_large(cap=600, prefill=700, iters=3, batch=64, chunk=256, check_rows=np.arange(64))
+@pytest.mark.parametrize("fused", [False, True])
+def test_large_payload_reduced(fused):
+    print(f"large: cap 600, prefill 700, batch 64 -> bf16, fused={fused}", flush=True)
+    run_large(cap=600, prefill=700, iters=3, batch=64, chunk=256, check_rows=np.arange(64), fused=fused)
 
 
 @pytest.mark.slow
@@ -66,7 +70,7 @@ def test_large_payload_full_size():
               check_rows=np.random.default_rng(0).choice(1024, 24, replace=False))
 
 
-def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values):
+def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values, fused=False):
     cfg = synth.Tokens(prefill, max_len=max_len, min_len=min_len)
     u, prio = cfg.draws(iters, batch)
     buf = cd.ReplayBuffer(cap, (max_len,), torch.int32, action_bytes=4, ragged=True, aux_elem_bytes=4)
@@ -94,8 +98,11 @@ def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values)
     ret = torch.empty((batch, max_len), dtype=torch.float32, device="cuda")
     rng = np.random.default_rng(4)
     for it in range(iters):
-        idx, w = buf.sample(dev(u[it]))
-        buf.gather(idx, xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
+        if fused:  # ragged: sampler then packing kernel behind one call
+            idx, w = buf.sample_gather(dev(u[it]), xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
+        else:
+            idx, w = buf.sample(dev(u[it]))
+            buf.gather(idx, xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
         vals = rng.standard_normal((batch, max_len)).astype(np.float32) if with_values else None
         cd.conduit_gae_packed(rew, length, dev(vals) if vals is not None else None, max_len, cfg.gamma, cfg.lam,
                               adv, ret)
@@ -125,9 +132,16 @@ def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values)
     buf.close()
 
 
-def test_tokens_reduced():
-    print("tokens: cap 300, max_len 256, prefill 400 (wraps), batch 64", flush=True)
-    run_tokens(cap=300, max_len=256, min_len=8, prefill=400, iters=3, batch=64, chunk=128, with_values=True)
+@pytest.mark.parametrize("fused", [False, True])
+def test_tokens_reduced(fused):
+    print(f"tokens: cap 300, max_len 256, prefill 400 (wraps), batch 64, fused={fused}", flush=True)
+    run_tokens(cap=300, max_len=256, min_len=8, prefill=400, iters=3, batch=64, chunk=128, with_values=True,
+               fused=fused)
+
+
+def test_tokens_long_rows_segmented_gae():
+    print("tokens: max_len 8192 (two GAE segments), batch 16", flush=True)
+    run_tokens(cap=40, max_len=8192, min_len=3000, prefill=50, iters=2, batch=16, chunk=25, with_values=True)
 
 
 @pytest.mark.slow

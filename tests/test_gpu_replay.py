@@ -45,7 +45,7 @@ def test_leaf_quantiser_matches_oracle(a, b):
 # ----------------------------------------------------------------------------
 # configuration 0: tiny replay, 100 iterations, full parity at every step
 # ----------------------------------------------------------------------------
-def _run_tiny(prefill, iters, seed_shift=0):
+def _run_tiny(prefill, iters, seed_shift=0, fused=False):
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
@@ -69,8 +69,11 @@ def _run_tiny(prefill, iters, seed_shift=0):
     for it in range(iters):
         ingest(pos, pos + n_in)
         pos += n_in
-        idx, w = buf.sample(dev(u[it]))
-        buf.gather(idx, xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
+        if fused:
+            idx, w = buf.sample_gather(dev(u[it]), xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
+        else:
+            idx, w = buf.sample(dev(u[it]))
+            buf.gather(idx, xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
         buf.update(idx, dev(prio[it]))
         o_idx, o_w = orc.sample(u[it])
         o_obs, o_act, o_rew, o_done = orc.gather(o_idx)
@@ -101,10 +104,15 @@ def test_tiny_config_wrapped_ring():
     _run_tiny(prefill=20000, iters=30, seed_shift=7)
 
 
+def test_tiny_config_fused_sample_gather():
+    print("tiny config: 100 iterations through conduit_sample_gather", flush=True)
+    _run_tiny(prefill=0, iters=100, fused=True)
+
+
 # ----------------------------------------------------------------------------
 # configuration 1 (DQN, frame stack 4, u8 -> fp32/255) at reduced capacity
 # ----------------------------------------------------------------------------
-def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None):
+def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False):
     """Drive GPU buffer and oracle through the same DQN stream; the oracle keeps
     metadata only and its observation rows are regenerated for the slots a
     gather reads."""
@@ -141,8 +149,11 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
     for it in range(iters):
         ingest(pos, pos + batch, with_prio=False)
         pos += batch
-        idx, w = buf.sample(dev(u[it]))
-        buf.gather(idx, xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
+        if fused:
+            idx, w = buf.sample_gather(dev(u[it]), xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
+        else:
+            idx, w = buf.sample(dev(u[it]))
+            buf.gather(idx, xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
         buf.update(idx, dev(prio[it]))
         o_idx, o_w = orc.sample(u[it])
         assert np.array_equal(host(idx), o_idx), it
@@ -183,10 +194,17 @@ def test_dqn_short_episodes_zero_fill():
     run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=True)
 
 
+@pytest.mark.parametrize("short", [False, True])
+def test_dqn_fused_sample_gather(short):
+    print(f"dqn: fused sample+gather, cap 3000, short episodes={short}", flush=True)
+    run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused=True)
+
+
 @pytest.mark.slow
-def test_dqn_full_capacity():
-    print("dqn: full size cap 1M, prefill 1.05M in 4096-frame chunks, 3 iterations", flush=True)
-    run_dqn(cap=1_000_000, prefill=1_050_000, iters=3, batch=512, chunk=4096)
+@pytest.mark.parametrize("fused", [False, True])
+def test_dqn_full_capacity(fused):
+    print(f"dqn: full size cap 1M, prefill 1.05M in 4096-frame chunks, 3 iterations, fused={fused}", flush=True)
+    run_dqn(cap=1_000_000, prefill=1_050_000, iters=3, batch=512, chunk=4096, fused=fused)
 
 
 # ----------------------------------------------------------------------------
@@ -272,6 +290,11 @@ def test_error_paths_are_flagged_not_faulting():
     with pytest.raises(cd.ConduitError) as e:
         buf.update(dev(np.array([0], np.int64)), dev(np.array([1], np.uint32)))
     assert e.value.status == cd.ESTATE
+    buf.clear_error()
+    out0 = torch.full((8, 1, 4), 5, dtype=torch.uint8, device="cuda")
+    idx, w = buf.sample_gather(u, cd.transform(cd.XF_NONE), obs=out0)  # fused path, same flags and zeros
+    assert buf.sync_check() == cd.ESTATE
+    assert np.all(host(idx) == -1) and np.all(host(w) == 0) and np.all(host(out0) == 0)
     buf.clear_error()
     assert buf.sync_check() == cd.OK
     # update of a slot >= size is skipped and flagged; the valid ones apply
