@@ -207,20 +207,15 @@ def bench_dqn(steps, warmup):
         evs.append(e)
     torch.cuda.synchronize()
     assert buf.sync_check() == cd.OK, cd.last_error()
-    # kernels alone, back to back between two events on the library's stream,
-    # over the timed steps' own inputs: the fused sample + gather (the dominant
-    # kernel of the step) and the stand-alone gather of the same batches
-    fb0 = tm.ev()
-    for i in range(warmup, warmup + steps):
-        sgat(h, B, pu[i], pi[i], None, xfr, lbr, stream)
-    fb1 = tm.ev()
+    # the dominant kernel alone: the gathers of the timed steps' own batches,
+    # launched back to back between two events on the library's stream
+    gb0 = tm.ev()
     for i in range(warmup, warmup + steps):
         gat(h, pi[i], B, xfr, lbr, stream)
     gb1 = tm.ev()
     torch.cuda.synchronize()
-    fused_b2b_ms = fb0.elapsed_time(fb1) / steps
-    gather_b2b_ms = fb1.elapsed_time(gb1) / steps
-    names = ["ingest_512", "sample_gather_512", "update_512"]
+    gather_b2b_ms = gb0.elapsed_time(gb1) / steps
+    names = ["ingest_512", "sample_gather_512 (sampler + gather launches)", "update_512"]
     per = {n: [e[k].elapsed_time(e[k + 1]) for e in evs] for k, n in enumerate(names)}
     kern = {n: _kernel_stats(v) for n, v in per.items()}
 
@@ -243,16 +238,11 @@ def bench_dqn(steps, warmup):
                 valid += 1
     row = 84 * 84
     gather_bytes = valid * row + B * (8 + 4 + 4 + 1) + B * K * row * 4 + B * (4 + 4 + 1)
-    # the fused kernel also reads each sample's uniform and the 64 children of the
-    # node it visits at each of the tree's levels, and writes the index and leaf
-    depth = buf.info().tree_depth
-    fused_bytes = gather_bytes - B * 8 + B * (8 + depth * 64 * 8 + 8 + 4)
     ingest_bytes_per_frame = 2 * row + (4 + 4 + 1 + 4 + 4) * 2 + 4 + 4  # obs r+w, scalars r+w, leaf r+w
     buf.close()
     return {
         "B": B, "steps": steps, "warmup": warmup, "total_ms": total_ms, "host_enqueue_s": host_enqueue_s,
-        "gather_b2b_ms": gather_b2b_ms, "fused_b2b_ms": fused_b2b_ms, "fused_bytes": fused_bytes,
-        "unfused_ms": unfused_ms,
+        "gather_b2b_ms": gather_b2b_ms, "unfused_ms": unfused_ms,
         "kernels": kern, "gather_bytes": gather_bytes, "valid_frames": valid, "prefill_s": prefill_s,
         "ingest_big": {"frames": 32768, "ms": ingest_big_ms,
                        "GBps": 32768 * ingest_bytes_per_frame / ingest_big_ms / 1e6},
@@ -527,9 +517,9 @@ def calibrate_copy():
 
 
 def _traffic_from_profile(kernel_src):
-    """HBM bytes per fused sample + gather launch from the committed counter
-    summary, if it was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "sample_gather_dqn_counters.txt")
+    """HBM bytes per gather launch from the committed counter summary, if it was
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "gather_dqn_counters.txt")
     if not os.path.exists(path):
         return None
     rec = {}
@@ -560,9 +550,7 @@ def main():
     ms_per_step = d["total_ms"] / args.steps
     value = d["B"] * args.steps / (d["total_ms"] / 1e3)
     g_ms = d["gather_b2b_ms"]
-    g_gbps = d["gather_bytes"] / g_ms / 1e6
-    f_ms = d["fused_b2b_ms"]
-    achieved = d["fused_bytes"] / f_ms / 1e6
+    achieved = d["gather_bytes"] / g_ms / 1e6
     kernel_src = os.path.join(ROOT, "paper_2609_24456_amd", "csrc", "k_gather.hip")
     out = {
         "metric": METRIC,
@@ -581,16 +569,13 @@ def main():
                                "batch 512, PER alpha 0.6 beta 0.4; step = ingest 512 + sample 512 + "
                                "gather 512 -> [512,4,84,84] fp32 + priority update 512",
                    "capacity": 1_000_000, "batch": 512, "frame_stack": 4},
-        "gather_GBps": g_gbps,
-        "gather_frac_of_peak": g_gbps / PEAK_HBM_GBPS,
-        "gather_kernel": "k_gather_pipe<U8_F32> alone over the timed steps' batches, back to back",
         "ms_per_step_unfused": d["unfused_ms"] / args.steps,
-        "roofline": {"bound": "hbm", "kernel": "k_sample_gather<U8_F32> (fused sampling + frame-stack gather, "
+        "roofline": {"bound": "hbm", "kernel": "k_gather_pipe<U8_F32> (frame-stack gather + u8->fp32, "
                                                "512 samples x 4 frames; the dominant kernel of the step)",
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": _traffic_from_profile(kernel_src),
-                     "algorithmic_bytes_per_launch": d["fused_bytes"], "avg_launch_us": f_ms * 1e3,
-                     "timing": "HIP events around back-to-back launches over the timed steps' uniforms"},
+                     "algorithmic_bytes_per_launch": d["gather_bytes"], "avg_launch_us": g_ms * 1e3,
+                     "timing": "HIP events around back-to-back launches over the timed steps' batches"},
         "kernels_us_in_step": {k: v["mean_us"] for k, v in d["kernels"].items()},
         "host_enqueue_us_per_step": d["host_enqueue_s"] * 1e6 / args.steps,
         "rows": {"dqn_ingest_32768": d["ingest_big"]},

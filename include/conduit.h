@@ -269,10 +269,9 @@ conduit_status conduit_gather_transform(conduit_buffer* buf, const int64_t* idx,
 /*
  * Fused delivery: exactly conduit_sample(buf, batch, uniforms, idx_out, is_w_out)
  * followed by conduit_gather_transform(buf, idx_out, batch, xf, out), with the
- * same outputs, arguments and errors as the two calls, but the gather of each
- * sample starts in the workgroup that sampled it (one launch fewer and no
- * round trip of the indices through memory; the IS weights follow in a second
- * small kernel).  Ragged buffers run the two steps back to back.
+ * same outputs, arguments and errors as the two calls, in two launches instead
+ * of three: the importance weights are computed by one extra workgroup of the
+ * gather (or, for ragged buffers, packing) launch.
  */
 conduit_status conduit_sample_gather(conduit_buffer* buf, int64_t batch, const uint64_t* uniforms, int64_t* idx_out,
                                      float* is_w_out, const conduit_transform* xf, const conduit_learner_batch* out,

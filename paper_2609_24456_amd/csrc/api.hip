@@ -76,7 +76,7 @@ const char* kErrText[kErrKinds] = {
     "sample from a tree whose total priority is 0",
     "sequence length outside [0, max_len]",
     "permutation entry outside [0, n_src)",
-    "leaf quantiser exactness check failed",
+    "",
     "sum-tree descent found no child",
     "",
 };
@@ -618,14 +618,14 @@ conduit_status conduit_sample_gather(conduit_buffer* b, int64_t batch, const uin
     sa.beta = b->opts.beta;
     sa.state = b->state;
     sa.err = err_words(b->err_slot);
+    // the sampler parks the sampled leaves in is_w_out; the gather (or packing)
+    // launch carries one more workgroup that turns them into the IS weights
+    const WeightsArgs wa{is_w_out, batch, b->opts.beta};
+    ga.weights = wa;
+    pa.weights = wa;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e;
-    if (b->opts.ragged) {  // sequences: the sampler, then the packing kernel
-        e = launch_sample(sa, s);
-        if (e == hipSuccess) e = launch_pack(pa, s);
-    } else {
-        e = launch_sample_gather(SampleGatherArgs{sa, ga}, s);
-    }
+    hipError_t e = launch_descend(sa, s);
+    if (e == hipSuccess) e = b->opts.ragged ? launch_pack(pa, s) : launch_gather(ga, s);
     if (e != hipSuccess) return hip_fail(e, "sample_gather launch");
     return CONDUIT_OK;
 }

@@ -22,7 +22,7 @@ enum ErrKind : int {
     ERR_EMPTY_TREE = 2,     // sample with a zero root
     ERR_SEQ_LENGTH = 3,     // ragged sequence longer than the slot / bad GAE length
     ERR_PERM_INDEX = 4,     // minibatch permutation entry outside [0, n_src)
-    ERR_QUANT = 5,          // leaf quantiser failed its exact check (never expected)
+    // 5: unused
     ERR_DESCENT = 6,        // tree descent found no child (never expected)
     kErrKinds = 8,
 };
@@ -98,14 +98,27 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int lane) {
     return ((uint64_t)hi << 32) | lo;
 }
 
-// inclusive prefix sum across the wavefront
+// lanes of a 64-bit register moved by one DPP control (lanes with no source, or
+// outside the row/bank masks, read 0)
+template <int CTRL, int ROWS, int BANKS>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, ROWS, BANKS, true);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, ROWS, BANKS, true);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive prefix sum across the wavefront with DPP moves (no LDS traffic):
+// Hillis-Steele shifts by 1, 2, 4 and 8 lanes inside each row of 16, then the
+// last lane of row 0 is broadcast into row 1 and of row 2 into row 3
+// (row_bcast:15), and lane 31 into rows 2 and 3 (row_bcast:31).
 __device__ __forceinline__ uint64_t wave_inclusive_scan_u64(uint64_t x) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        uint64_t y = __shfl_up(x, off, kWave);
-        if (lane >= off) x += y;
-    }
+    constexpr int kRowShr = 0x110, kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+    x += dpp_u64<kRowShr + 1, 0xf, 0xf>(x);
+    x += dpp_u64<kRowShr + 2, 0xf, 0xf>(x);
+    x += dpp_u64<kRowShr + 4, 0xf, 0xf>(x);
+    x += dpp_u64<kRowShr + 8, 0xf, 0xf>(x);
+    x += dpp_u64<kRowBcast15, 0xa, 0xf>(x);
+    x += dpp_u64<kRowBcast31, 0xc, 0xf>(x);
     return x;
 }
 
@@ -116,11 +129,12 @@ __device__ __forceinline__ uint64_t wave_inclusive_scan_u64(uint64_t x) {
 //
 // Fast path: x = exp2(F + (a/b) log2 p) in fp64.  With the device log2/exp2
 // within a few ulp, the absolute error of x is below x * 2^-45 <= 2^-13 (x is
-// below 2^32), so whenever the fractional part of x lies in [2^-10, 1 - 2^-10]
-// floor(x) is the exact answer.  Otherwise (x within 2^-10 of an integer, about
-// 0.2% of inputs, and every perfect power) the candidate is settled with exact
-// 288-bit integer comparisons.  All limb indices are compile-time constants, so
-// the big integers live in registers.
+// below 2^32), so whenever the fractional part of x lies in [2^-12, 1 - 2^-12]
+// floor(x) is the exact answer.  Otherwise x is within 2^-12 of an integer n
+// (about 0.05% of inputs, and every perfect power), the true value lies in
+// (n - 1, n + 1), and one exact 288-bit comparison settles it: L(p) = n if
+// n^b <= 2^(bF) p^a, else n - 1 (b <= 8, so both sides fit 288 bits).  All limb
+// indices are compile-time constants, so the big integers live in registers.
 struct Big288 {
     uint32_t w[9];
 };
@@ -170,87 +184,64 @@ __device__ __forceinline__ void big_pow(Big288& x, uint32_t base, int e) {
     for (int i = 0; i < e; ++i) big_mul32(x, base);
 }
 
-// Exact settlement: the largest q with q^b <= 2^(bF) p^a, searched upwards from
-// cand - 2 (the true value is within one of cand).  Bit 32 of the result flags
-// a failed check (never expected).
-__device__ __noinline__ uint64_t quantise_leaf_exact(uint32_t p, int a, int b, int F, uint64_t cand) {
+// the settlement for x within 2^-12 of the integer n (1 <= n <= 2^32)
+__device__ __noinline__ uint32_t quantise_leaf_exact(uint32_t p, int a, int b, int F, uint64_t n) {
+    if (n > 0xffffffffull) return 0xffffffffu;  // L(p) < 2^32 <= n
     Big288 rhs, lhs;
     big_pow(rhs, p, a);
     big_shl(rhs, b * F);
-    uint64_t q = cand >= 2 ? cand - 2 : 0;
-    uint64_t bad = 0;
-    big_pow(lhs, (uint32_t)q, b);
-    if (big_cmp(lhs, rhs) > 0) bad = 1ull << 32;  // candidate was not within 2
-    for (int it = 0; it < 4; ++it) {
-        if (q + 1 > 0xffffffffull) return q | bad;  // (2^32)^b exceeds every rhs
-        big_pow(lhs, (uint32_t)(q + 1), b);
-        if (big_cmp(lhs, rhs) > 0) return q | bad;
-        ++q;
-    }
-    return q | (1ull << 32);  // ran out of steps
+    big_pow(lhs, (uint32_t)n, b);
+    return big_cmp(lhs, rhs) <= 0 ? (uint32_t)n : (uint32_t)(n - 1);
 }
 
-// L(p) in bits 0..31; bit 32 set if the exact check could not be satisfied
-__device__ __forceinline__ uint64_t quantise_leaf(uint32_t p, int a, int b, int F) {
+__device__ __forceinline__ uint32_t quantise_leaf(uint32_t p, int a, int b, int F) {
     if (p == 0u) return 0u;
     if (a == 0) return 1u << F;
     if (a == b) return p;  // F = 0
     const double x = exp2((double)F + ((double)a / (double)b) * log2((double)p));
     const double fl = floor(x);
     const double fr = x - fl;
-    const uint64_t cand = fl >= 4294967295.0 ? 4294967295ull : (uint64_t)fl;
-    if (fr >= 0x1p-10 && fr <= 1.0 - 0x1p-10) return cand;
-    return quantise_leaf_exact(p, a, b, F, cand);
+    if (fr >= 0x1p-12 && fr <= 1.0 - 0x1p-12) return fl >= 4294967295.0 ? 0xffffffffu : (uint32_t)fl;
+    return quantise_leaf_exact(p, a, b, F, (uint64_t)fl + (fr > 0.5 ? 1u : 0u));
 }
 
 // ---------------------------------------------------------------------------
-// stratified inverse-CDF descent of the 64-ary tree by one wavefront
+// importance-sampling weights of a sampled batch
 // ---------------------------------------------------------------------------
-struct Descent {
-    int64_t slot;   // sampled slot, -1 if the tree is empty
-    uint32_t leaf;  // its quantised priority
-    bool lost;      // no child exceeded the target (never expected)
+// The sampler parks each sample's leaf q_k in the weight array; one whole
+// workgroup of NT lanes then overwrites it in place with
+// w_k = (q_min / q_k)^beta, q_min the smallest non-zero parked leaf, in fp64
+// (0 where nothing was sampled).  Each lane rewrites only the entries it read.
+struct WeightsArgs {
+    float* w;        // parked leaves in, weights out; NULL: no weights
+    int64_t batch;
+    double beta;
 };
 
-// Stratum k of B: target t = floor((k*Q + floor(u*Q / 2^64)) / B), evaluated
-// without 128-bit division by splitting Q and the high product word into
-// quotient and remainder by B (every term fits 64 bits since k < B <= 2^20).
-// At each level the 64 lanes load the 64 children of the current node, take an
-// inclusive wavefront prefix sum, and the first lane whose prefix exceeds the
-// target (ballot + find-first-set) names the child; its exclusive prefix is
-// subtracted from the target.  This is "first slot whose inclusive prefix sum
-// exceeds t" with half-open intervals, so zero leaves are never chosen.  The
-// total, the uniform and the root's children are independent loads, issued
-// together: depth dependent loads in all.  All lanes return the same result.
-__device__ __forceinline__ Descent tree_descend(const TreeView& tr, const uint64_t* uniforms, int64_t k, int64_t batch) {
-    const int lane = lane_id();
-    const int top = tr.depth;
-    const uint64_t Q = tr.level[top][0];
-    const uint64_t u = uniforms[k];
-    uint64_t v = top == 1 ? (uint64_t)tr.leaves[lane] : tr.level[top - 1][lane];
-    Descent r{-1, 0u, false};
-    if (Q == 0ull) return r;
-    const uint64_t B = (uint64_t)batch;
-    const uint64_t h = __umul64hi(u, Q);
-    const uint64_t kk = (uint64_t)k;
-    uint64_t t = kk * (Q / B) + h / B + (kk * (Q % B) + h % B) / B;
-    uint64_t node = 0;
-    for (int l = top; l >= 1; --l) {
-        if (l != top) {
-            const uint64_t child = node * kFanout + (uint64_t)lane;
-            v = l == 1 ? (uint64_t)tr.leaves[child] : tr.level[l - 1][child];
-        }
-        const uint64_t incl = wave_inclusive_scan_u64(v);
-        const uint64_t mask = __ballot(incl > t);
-        int sel = 63;
-        if (mask) sel = __ffsll((unsigned long long)mask) - 1; else r.lost = true;
-        const uint64_t excl = __shfl(incl - v, sel, kWave);
-        t -= excl;
-        node = node * kFanout + (uint64_t)sel;
-        if (l == 1) r.leaf = (uint32_t)__shfl(v, sel, kWave);
+template <int NT>
+__device__ void is_weights_block(const WeightsArgs& a) {
+    __shared__ uint32_t wave_min[NT / kWave];
+    __shared__ uint32_t qmin_s;
+    const uint32_t* q_park = reinterpret_cast<const uint32_t*>(a.w);
+    uint32_t m = 0xffffffffu;
+    for (int64_t k = threadIdx.x; k < a.batch; k += NT) {
+        const uint32_t q = q_park[k];
+        if (q) m = q < m ? q : m;
     }
-    r.slot = (int64_t)node;
-    return r;
+    m = wave_min_u32(m);
+    if (lane_id() == 0) wave_min[threadIdx.x / kWave] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t r = wave_min[0];
+        for (int i = 1; i < NT / kWave; ++i) r = wave_min[i] < r ? wave_min[i] : r;
+        qmin_s = r;
+    }
+    __syncthreads();
+    const double qmin = (double)qmin_s;
+    for (int64_t k = threadIdx.x; k < a.batch; k += NT) {
+        const uint32_t q = q_park[k];
+        a.w[k] = q ? (float)pow(qmin / (double)q, a.beta) : 0.0f;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -315,7 +306,10 @@ struct SampleArgs {
     uint32_t* err;
 };
 
+// sampler, then the weights kernel (if w_out is set)
 hipError_t launch_sample(const SampleArgs& a, hipStream_t s);
+// sampler only: leaves parked in w_out for a later weights block
+hipError_t launch_descend(const SampleArgs& a, hipStream_t s);
 
 constexpr int kMaxCols = 8;
 
@@ -348,19 +342,12 @@ struct GatherArgs {
     float* cols_out[kMaxCols];
     uint32_t* err;
     int32_t err_kind;
+    // the IS weights of the batch the indices were sampled as (one extra
+    // workgroup of the launch); weights.w NULL: none
+    WeightsArgs weights;
 };
 
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
-
-// fused sample -> gather: the sampler's arguments plus the gather's (whose idx
-// is the sampler's idx_out and whose limit is the buffer size)
-struct SampleGatherArgs {
-    SampleArgs s;
-    GatherArgs g;
-};
-
-hipError_t launch_sample_gather(const SampleGatherArgs& a, hipStream_t s);
-hipError_t launch_is_weights(const SampleArgs& a, hipStream_t s);
 
 struct PackArgs {
     const int64_t* idx;
@@ -383,6 +370,7 @@ struct PackArgs {
     const uint8_t* done;
     uint8_t* out_done;
     uint32_t* err;
+    WeightsArgs weights;  // as for GatherArgs
 };
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);

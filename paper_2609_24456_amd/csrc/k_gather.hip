@@ -21,7 +21,10 @@
 //            computed with IEEE single division/subtraction and bf16
 //            round-to-nearest-even.
 // Scalar columns (action, reward, done, extra float columns) are produced by
-// the trailing workgroups of the grid, one lane per output row.
+// the trailing workgroups of the grid, one lane per output row.  When the
+// indices were just sampled, the batch's importance weights are computed by one
+// more workgroup at the very end of the grid (is_weights_block), so sampling and
+// delivery take two launches in all.
 #include "common.h"
 
 namespace conduit {
@@ -180,7 +183,8 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
     __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
     const int64_t it = blockIdx.x;
     if (it >= n_items) {
-        gather_scalars(a, it - n_items);
+        if (a.weights.w && blockIdx.x == gridDim.x - 1) is_weights_block<kThreads>(a.weights);
+        else gather_scalars(a, it - n_items);
         return;
     }
     if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
@@ -197,71 +201,6 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
     finish<XF, NT>(a, t, v, si, sj, ei, ej, lut);
 }
 
-// Fused sampler + gather: one workgroup per sample.  Wavefront 0 descends the
-// tree (tree_descend) while the other lanes build the bf16 table if needed; the
-// whole workgroup then gathers the sample's frames, double-buffered across its
-// items, and writes the scalar columns.  Saves the sampler's index round trip
-// and one launch against conduit_sample followed by conduit_gather_transform.
-template <int XF, bool NT>
-__global__ __launch_bounds__(kThreads) void k_sample_gather(SampleGatherArgs sg, int32_t bpf) {
-    __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
-    __shared__ int64_t s_slot;
-    const GatherArgs& a = sg.g;
-    const int64_t b = blockIdx.x;
-    if (threadIdx.x < kWave) {
-        const Descent d = tree_descend(sg.s.tree, sg.s.uniforms, b, sg.s.batch);
-        if (threadIdx.x == 0) {
-            s_slot = d.slot;
-            sg.s.idx_out[b] = d.slot;
-            if (sg.s.w_out) reinterpret_cast<uint32_t*>(sg.s.w_out)[b] = d.leaf;  // for k_is_weights
-            if (d.slot < 0 && b == 0) flag_error(sg.s.err, ERR_EMPTY_TREE);
-            if (d.lost) flag_error(sg.s.err, ERR_DESCENT);
-        }
-    } else if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
-        build_lut(a, lut, kWave, kThreads - kWave);
-    }
-    __syncthreads();
-    const int64_t i = s_slot;
-    const bool ok = i >= 0 && i < a.limit;
-    // scalar columns of the sampled slot
-    if (a.out_action && a.action_bytes > 0) {
-        if ((a.action_bytes & 3) == 0) {
-            for (int c = threadIdx.x; c < a.action_bytes / 4; c += kThreads)
-                reinterpret_cast<uint32_t*>(a.out_action + b * a.action_bytes)[c] =
-                    ok ? reinterpret_cast<const uint32_t*>(a.action + i * a.action_bytes)[c] : 0u;
-        } else {
-            for (int c = threadIdx.x; c < a.action_bytes; c += kThreads)
-                a.out_action[b * a.action_bytes + c] = ok ? a.action[i * a.action_bytes + c] : (uint8_t)0;
-        }
-    }
-    if (threadIdx.x == 0) {
-        if (a.out_reward) a.out_reward[b] = ok ? a.reward[i] : 0.0f;
-        if (a.out_done) a.out_done[b] = ok ? a.done[i] : (uint8_t)0;
-    }
-    const int64_t per_row = (int64_t)bpf * a.stack;
-    if (per_row == 0) return;
-    const int64_t it0 = b * per_row, it_end = it0 + per_row;
-    uint32_t va[kUnroll], vb[kUnroll];
-    int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
-    uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
-    Item ta = decode(a, it0, bpf, i), tb;
-    issue(a, ta, i, va, sia, sja, eia, eja);
-    for (int64_t it = it0; it < it_end; it += 2) {
-        const bool has_b = it + 1 < it_end;  // uniform
-        if (has_b) {
-            tb = decode(a, it + 1, bpf, i);
-            issue(a, tb, i, vb, sib, sjb, eib, ejb);
-        }
-        finish<XF, NT>(a, ta, va, sia, sja, eia, eja, lut);
-        if (!has_b) break;
-        if (it + 2 < it_end) {
-            ta = decode(a, it + 2, bpf, i);
-            issue(a, ta, i, va, sia, sja, eia, eja);
-        }
-        finish<XF, NT>(a, tb, vb, sib, sjb, eib, ejb, lut);
-    }
-}
-
 // Persistent workgroups walk the items with a stride of the grid.  Two register
 // sets alternate: the loads of the next item are issued before the stores of
 // the current one, so reads of one item overlap the writes of the previous one
@@ -271,7 +210,8 @@ template <int XF, bool NT>
 __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t bpf, int64_t n_items, int32_t frame_grid) {
     __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
     if ((int32_t)blockIdx.x >= frame_grid) {
-        gather_scalars(a, (int64_t)blockIdx.x - frame_grid);
+        if (a.weights.w && blockIdx.x == gridDim.x - 1) is_weights_block<kThreads>(a.weights);
+        else gather_scalars(a, (int64_t)blockIdx.x - frame_grid);
         return;
     }
     if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
@@ -319,6 +259,10 @@ constexpr int kPackQuads = 4;
 
 __global__ __launch_bounds__(kThreads) void k_pack(PackArgs a) {
     const int64_t b = blockIdx.x;
+    if (b >= a.n) {  // the weights workgroup
+        is_weights_block<kThreads>(a.weights);
+        return;
+    }
     const int64_t i = a.idx[b];
     const bool ok = i >= 0 && i < a.size;
     if (!ok && threadIdx.x == 0) flag_error(a.err, ERR_GATHER_INDEX);
@@ -393,16 +337,16 @@ int device_cus() {
 // kernels and beat plain stores, even when the batch would fit the 256 MB
 // Infinity Cache.
 template <int XF>
-void launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t bpf, int64_t n_items, int64_t scalar_blocks) {
+void launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t bpf, int64_t n_items, int64_t tail_blocks) {
     const int64_t out_bytes = n_items * kUnitsPerBlock * 4 * (XF == CONDUIT_XF_U8_F32 ? 4 : XF == CONDUIT_XF_U8_BF16_NORM ? 2 : 1);
     if (out_bytes <= kPipeMaxOutBytes) {
         // small batches: persistent pipelined workgroups
         const int64_t frame_grid = n_items < 4LL * device_cus() ? n_items : 4LL * device_cus();
-        hipLaunchKernelGGL((k_gather_pipe<XF, true>), dim3((unsigned)(frame_grid + scalar_blocks)), dim3(kThreads), 0,
+        hipLaunchKernelGGL((k_gather_pipe<XF, true>), dim3((unsigned)(frame_grid + tail_blocks)), dim3(kThreads), 0,
                            s, a, (int32_t)bpf, n_items, (int32_t)frame_grid);
     } else {
         // large batches: one workgroup per item
-        hipLaunchKernelGGL((k_gather_rows<XF, true>), dim3((unsigned)(n_items + scalar_blocks)), dim3(kThreads), 0, s,
+        hipLaunchKernelGGL((k_gather_rows<XF, true>), dim3((unsigned)(n_items + tail_blocks)), dim3(kThreads), 0, s,
                            a, (int32_t)bpf, n_items);
     }
 }
@@ -413,44 +357,21 @@ hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
     const int64_t bpf = a.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
     const int64_t n_items = a.n * a.stack * bpf;
     const bool scalars = a.out_action || a.out_reward || a.out_done || a.ncols > 0;
-    const int64_t scalar_blocks = scalars ? (a.n + kThreads - 1) / kThreads : 0;
-    if (n_items + scalar_blocks == 0) return hipSuccess;
+    // scalar-column workgroups, then the weights workgroup (last in the grid)
+    const int64_t tail_blocks = (scalars ? (a.n + kThreads - 1) / kThreads : 0) + (a.weights.w ? 1 : 0);
+    if (n_items + tail_blocks == 0) return hipSuccess;
     switch (a.xform) {
-        case CONDUIT_XF_NONE: launch_gather_xf<CONDUIT_XF_NONE>(a, s, bpf, n_items, scalar_blocks); break;
-        case CONDUIT_XF_U8_F32: launch_gather_xf<CONDUIT_XF_U8_F32>(a, s, bpf, n_items, scalar_blocks); break;
-        case CONDUIT_XF_U8_BF16_NORM: launch_gather_xf<CONDUIT_XF_U8_BF16_NORM>(a, s, bpf, n_items, scalar_blocks); break;
+        case CONDUIT_XF_NONE: launch_gather_xf<CONDUIT_XF_NONE>(a, s, bpf, n_items, tail_blocks); break;
+        case CONDUIT_XF_U8_F32: launch_gather_xf<CONDUIT_XF_U8_F32>(a, s, bpf, n_items, tail_blocks); break;
+        case CONDUIT_XF_U8_BF16_NORM: launch_gather_xf<CONDUIT_XF_U8_BF16_NORM>(a, s, bpf, n_items, tail_blocks); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
-hipError_t launch_sample_gather(const SampleGatherArgs& a, hipStream_t s) {
-    if (a.s.batch <= 0) return hipSuccess;
-    const GatherArgs& g = a.g;
-    const int64_t units = g.row_bytes >> 2;
-    const int64_t bpf = g.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
-    const dim3 grid((unsigned)a.s.batch), block(kThreads);
-    switch (g.xform) {
-        case CONDUIT_XF_NONE:
-            hipLaunchKernelGGL((k_sample_gather<CONDUIT_XF_NONE, true>), grid, block, 0, s, a, (int32_t)bpf);
-            break;
-        case CONDUIT_XF_U8_F32:
-            hipLaunchKernelGGL((k_sample_gather<CONDUIT_XF_U8_F32, true>), grid, block, 0, s, a, (int32_t)bpf);
-            break;
-        case CONDUIT_XF_U8_BF16_NORM:
-            hipLaunchKernelGGL((k_sample_gather<CONDUIT_XF_U8_BF16_NORM, true>), grid, block, 0, s, a, (int32_t)bpf);
-            break;
-        default:
-            return hipErrorInvalidValue;
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return launch_is_weights(a.s, s);
-}
-
 hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_pack, dim3((unsigned)a.n), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL(k_pack, dim3((unsigned)(a.n + (a.weights.w ? 1 : 0))), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

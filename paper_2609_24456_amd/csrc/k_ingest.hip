@@ -98,7 +98,6 @@ __device__ void ingest_meta(const IngestArgs& a, int64_t block) {
 
     uint64_t delta = 0;
     uint32_t p_seen = 0;
-    bool bad_q = false;
     const uint32_t old = (valid && a.prioritized) ? a.tree.leaves[slot] : 0u;  // issued early
     if (valid) {
         if (a.action_bytes > 0) {
@@ -130,16 +129,13 @@ __device__ void ingest_meta(const IngestArgs& a, int64_t block) {
         if (a.prioritized) {
             const uint32_t p = a.src_prio ? a.src_prio[j] : a.state->max_prio;
             p_seen = p;
-            const uint64_t qf = quantise_leaf(p, a.tree.alpha_num, a.tree.alpha_den, a.tree.frac_bits);
-            bad_q |= (qf >> 32) != 0;
-            const uint32_t q = (uint32_t)qf;
+            const uint32_t q = quantise_leaf(p, a.tree.alpha_num, a.tree.alpha_den, a.tree.frac_bits);
             a.tree.leaves[slot] = q;
             delta = (uint64_t)q - (uint64_t)old;  // modulo 2^64
         }
     }
     if (!a.prioritized) return;
     const int lane = lane_id();
-    if (bad_q) flag_error(a.err, ERR_QUANT);
     if (a.src_prio) {
         const uint32_t m = wave_max_u32(p_seen);
         if (lane == 0 && m > 0) atomicMax(&a.state->max_prio, m);
@@ -164,14 +160,18 @@ __device__ void ingest_meta(const IngestArgs& a, int64_t block) {
     }
 }
 
+// The metadata/tree workgroups come first in the grid: their chain of
+// dependent memory operations (old leaf, quantiser, tree atomics) is the
+// longest, so they start with the first wave of dispatched workgroups and
+// overlap the payload copy.
 template <typename V, bool RAGGED>
-__global__ __launch_bounds__(kThreads) void k_ingest(IngestArgs a, int64_t data_blocks) {
+__global__ __launch_bounds__(kThreads) void k_ingest(IngestArgs a, int64_t meta_blocks) {
     const int64_t b = blockIdx.x;
-    if (b < data_blocks) {
-        if constexpr (RAGGED) copy_ragged(a, b);
-        else copy_dense<V>(a, b);
+    if (b < meta_blocks) {
+        ingest_meta(a, b);
     } else {
-        ingest_meta(a, b - data_blocks);
+        if constexpr (RAGGED) copy_ragged(a, b - meta_blocks);
+        else copy_dense<V>(a, b - meta_blocks);
     }
 }
 
@@ -185,7 +185,7 @@ hipError_t launch_ingest(const IngestArgs& a, hipStream_t s) {
     const int64_t meta_blocks = (lanes + kThreads - 1) / kThreads;
     if (a.length) {  // ragged
         const int64_t grid = a.n + meta_blocks;
-        hipLaunchKernelGGL((k_ingest<uint32_t, true>), dim3((unsigned)grid), dim3(kThreads), 0, s, a, a.n);
+        hipLaunchKernelGGL((k_ingest<uint32_t, true>), dim3((unsigned)grid), dim3(kThreads), 0, s, a, meta_blocks);
         return hipGetLastError();
     }
     const uintptr_t al = reinterpret_cast<uintptr_t>(a.src_obs) | reinterpret_cast<uintptr_t>(a.obs) |
@@ -196,10 +196,10 @@ hipError_t launch_ingest(const IngestArgs& a, hipStream_t s) {
     const int64_t copy_blocks = (total_vec + kThreads * kCopyUnroll - 1) / (kThreads * kCopyUnroll);
     const dim3 grid((unsigned)(copy_blocks + meta_blocks));
     switch (vec) {
-        case 16: hipLaunchKernelGGL((k_ingest<u32x4, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
-        case 8: hipLaunchKernelGGL((k_ingest<u32x2, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
-        case 4: hipLaunchKernelGGL((k_ingest<uint32_t, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
-        default: hipLaunchKernelGGL((k_ingest<uint8_t, false>), grid, dim3(kThreads), 0, s, a, copy_blocks); break;
+        case 16: hipLaunchKernelGGL((k_ingest<u32x4, false>), grid, dim3(kThreads), 0, s, a, meta_blocks); break;
+        case 8: hipLaunchKernelGGL((k_ingest<u32x2, false>), grid, dim3(kThreads), 0, s, a, meta_blocks); break;
+        case 4: hipLaunchKernelGGL((k_ingest<uint32_t, false>), grid, dim3(kThreads), 0, s, a, meta_blocks); break;
+        default: hipLaunchKernelGGL((k_ingest<uint8_t, false>), grid, dim3(kThreads), 0, s, a, meta_blocks); break;
     }
     return hipGetLastError();
 }

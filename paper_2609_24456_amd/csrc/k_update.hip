@@ -16,6 +16,12 @@
 // All tree arithmetic is integer modulo 2^64: exact and independent of the
 // order in which atomics land.  Sizes of the paper's workloads (256 to 1024
 // updates per call) take a single chunk.
+//
+// Latency: barriers that only order LDS traffic use an LDS-only fence, so the
+// global tree atomics issued by the winners are never waited for inside the
+// kernel (they drain at its end, overlapping the flush); only the barrier that
+// starts a later chunk orders global memory, because that chunk reads leaves
+// the previous one wrote.
 #include "common.h"
 
 namespace conduit {
@@ -28,16 +34,21 @@ constexpr int kBins = 2048;    // u64 LDS bins for small tree levels
 
 __device__ __forceinline__ uint32_t slot_hash(uint32_t key) { return (key * 0x9E3779B1u) >> (32 - 11); }
 
+// workgroup barrier ordering LDS only (no wait for outstanding global memory)
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
     __shared__ uint32_t keys[kTable];
     __shared__ int32_t owner[kTable];
     __shared__ unsigned long long bins[kBins];
-    __shared__ uint32_t wave_pmax[kThreads / kWave];
     const int tid = threadIdx.x;
     const TreeView& tr = a.tree;
 
     uint32_t pmax = 0;
-    bool bad_q = false;
     // the first chunk's index and priority loads are issued before the LDS set-up
     int64_t k = tid;
     int64_t slot_next = k < a.n ? a.idx[k] : -1;
@@ -49,6 +60,8 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
             keys[i] = 0u;
             owner[i] = -1;
         }
+        // orders global memory too: a later chunk reads leaves this one's
+        // predecessors wrote
         __syncthreads();
         k = base + tid;
         bool valid = k < a.n;
@@ -78,11 +91,9 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
         const int64_t kn = base + kThreads + tid;
         slot_next = kn < a.n ? a.idx[kn] : -1;
         p_next = kn < a.n ? a.prio[kn] : 0u;
-        __syncthreads();
+        lds_barrier();
         if (valid && owner[h] == tid) {
-            const uint64_t qf = quantise_leaf(p, tr.alpha_num, tr.alpha_den, tr.frac_bits);
-            bad_q |= (qf >> 32) != 0;
-            const uint32_t q = (uint32_t)qf;
+            const uint32_t q = quantise_leaf(p, tr.alpha_num, tr.alpha_den, tr.frac_bits);
             tr.leaves[slot] = q;
             const uint64_t delta = (uint64_t)q - (uint64_t)old;  // modulo 2^64
             if (delta) {
@@ -94,7 +105,7 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
                 }
             }
         }
-        __syncthreads();
+        lds_barrier();  // bins complete; the table may be cleared again
     }
     // flush the LDS-accumulated levels
     for (int l = 1; l <= tr.depth; ++l) {
@@ -106,16 +117,9 @@ __global__ __launch_bounds__(kThreads) void k_update(UpdateArgs a) {
             if (v) atomicAdd(reinterpret_cast<unsigned long long*>(tr.level[l] + i), v);
         }
     }
-    // running maximum priority
+    // running maximum priority: one atomic per wavefront
     const uint32_t wm = wave_max_u32(pmax);
-    if (lane_id() == 0) wave_pmax[tid / kWave] = wm;
-    if (bad_q) flag_error(a.err, ERR_QUANT);
-    __syncthreads();
-    if (tid == 0) {
-        uint32_t m = 0;
-        for (int w = 0; w < kThreads / kWave; ++w) m = wave_pmax[w] > m ? wave_pmax[w] : m;
-        if (m > 0) atomicMax(&a.state->max_prio, m);
-    }
+    if (lane_id() == 0 && wm > 0) atomicMax(&a.state->max_prio, wm);
 }
 
 }  // namespace

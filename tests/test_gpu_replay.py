@@ -31,6 +31,14 @@ def test_leaf_quantiser_matches_oracle(a, b):
     p[:len(edge)] = edge
     powers = np.array([k ** b for k in range(1, 300) if k ** b < (1 << 32)], np.uint64).astype(np.uint32)
     p[len(edge):len(edge) + len(powers)] = powers
+    if 0 < a < b:
+        # priorities whose unrounded leaf 2^F p^(a/b) lies within about 2^-11 of an
+        # integer: the inputs that take the device's exact big-integer settlement
+        pool = rng.integers(1, 1 << 32, size=1 << 23, dtype=np.uint64)
+        x = np.ldexp(np.power(pool.astype(np.float64), a / b), oracle.frac_bits(a, b))
+        near = pool[np.abs(x - np.rint(x)) < 2.0 ** -11].astype(np.uint32)
+        assert len(near) > 1000
+        p[1 << 17:(1 << 17) + len(near)] = near
     n = len(p)
     buf = _mk(n, (4,), alpha=(a, b))
     buf.ingest(torch.zeros((n, 4), dtype=torch.uint8, device="cuda"), prio=dev(p))
@@ -210,13 +218,16 @@ def test_dqn_full_capacity(fused):
 # ----------------------------------------------------------------------------
 # sum-tree shapes, duplicates, degenerate cases
 # ----------------------------------------------------------------------------
-@pytest.mark.parametrize("cap", [1, 2, 63, 64, 65, 4095, 4097, 262145])
+# capacities span every descent shape: depth 1 to 4, and the level under the
+# root's children prefetched as up to 4 groups (65, 4097, 262145), up to 16
+# groups (16385, 40961) or not at all (4095)
+@pytest.mark.parametrize("cap", [1, 2, 63, 64, 65, 4095, 4097, 16385, 40961, 262145])
 def test_tree_shapes_sample_and_update(cap):
     print(f"tree shape cap={cap}", flush=True)
     rng = np.random.default_rng(cap)
     buf = _mk(cap, (4,), torch.uint8, action_bytes=0)
     orc = oracle.Replay(cap, (4,), np.uint8, act_bytes=0)
-    n = min(cap, 5000)
+    n = cap if cap <= 50000 else 5000
     p = synth.quantise_priority(rng.lognormal(0, 1, n))
     buf.ingest(torch.zeros((n, 4), dtype=torch.uint8, device="cuda"), prio=dev(p))
     orc.ingest(n, obs=np.zeros((n, 4), np.uint8), prio=p)
