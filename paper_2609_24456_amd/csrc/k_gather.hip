@@ -21,10 +21,11 @@
 //            computed with IEEE single division/subtraction and bf16
 //            round-to-nearest-even.
 // Scalar columns (action, reward, done, extra float columns) are produced by
-// the trailing workgroups of the grid, one lane per output row.  When the
-// indices were just sampled, the batch's importance weights are computed by one
-// more workgroup at the very end of the grid (is_weights_block), so sampling and
-// delivery take two launches in all.
+// workgroups at the head of the grid, one lane per output row, so that their
+// dependent loads (index, then the columns) start with the first dispatched
+// workgroups and finish under the frame traffic.  When the indices were just
+// sampled, one more workgroup there computes the batch's importance weights
+// (is_weights_block), so sampling and delivery take two launches in all.
 #include "common.h"
 
 namespace conduit {
@@ -55,24 +56,46 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
     return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
+// One lane per output row.  Every load of the row (clamped to slot 0 when the
+// index is out of range, so all are unconditional) is issued before the first
+// store: one memory round trip after the index instead of one per column.
+constexpr int kScalarWords = 8;  // action words held in registers per pass
+
 __device__ void gather_scalars(const GatherArgs& a, int64_t block) {
     const int64_t b = block * kThreads + threadIdx.x;
     if (b >= a.n) return;
     const int64_t i = a.idx[b];
     const bool ok = i >= 0 && i < a.limit;
-    if (a.out_action && a.action_bytes > 0) {
+    const int64_t s = ok ? i : 0;
+    const bool act = a.out_action && a.action_bytes > 0;
+    const bool act_words = (a.action_bytes & 3) == 0;
+    const int words = act && act_words ? a.action_bytes >> 2 : 0;
+    uint32_t w[kScalarWords];
+#pragma unroll
+    for (int c = 0; c < kScalarWords; ++c)
+        w[c] = c < words ? reinterpret_cast<const uint32_t*>(a.action + s * a.action_bytes)[c] : 0u;
+    const float rew = a.out_reward ? a.reward[s] : 0.0f;
+    const uint8_t dn = a.out_done ? a.done[s] : (uint8_t)0;
+    float col[kMaxCols];
+#pragma unroll
+    for (int c = 0; c < kMaxCols; ++c) col[c] = c < a.ncols ? a.cols[c][s] : 0.0f;
+    if (act) {
         uint8_t* dst = a.out_action + b * a.action_bytes;
-        const uint8_t* src = a.action + (ok ? i : 0) * a.action_bytes;
-        if ((a.action_bytes & 3) == 0) {
-            for (int c = 0; c < a.action_bytes; c += 4)
-                *reinterpret_cast<uint32_t*>(dst + c) = ok ? *reinterpret_cast<const uint32_t*>(src + c) : 0u;
+        if (act_words) {
+#pragma unroll
+            for (int c = 0; c < kScalarWords; ++c)
+                if (c < words) reinterpret_cast<uint32_t*>(dst)[c] = ok ? w[c] : 0u;
+            for (int c = kScalarWords; c < words; ++c)  // long actions: the rest word by word
+                reinterpret_cast<uint32_t*>(dst)[c] = ok ? reinterpret_cast<const uint32_t*>(a.action + s * a.action_bytes)[c] : 0u;
         } else {
-            for (int c = 0; c < a.action_bytes; ++c) dst[c] = ok ? src[c] : (uint8_t)0;
+            for (int c = 0; c < a.action_bytes; ++c) dst[c] = ok ? a.action[s * a.action_bytes + c] : (uint8_t)0;
         }
     }
-    if (a.out_reward) a.out_reward[b] = ok ? a.reward[i] : 0.0f;
-    if (a.out_done) a.out_done[b] = ok ? a.done[i] : (uint8_t)0;
-    for (int c = 0; c < a.ncols; ++c) a.cols_out[c][b] = ok ? a.cols[c][i] : 0.0f;
+    if (a.out_reward) a.out_reward[b] = ok ? rew : 0.0f;
+    if (a.out_done) a.out_done[b] = ok ? dn : (uint8_t)0;
+#pragma unroll
+    for (int c = 0; c < kMaxCols; ++c)
+        if (c < a.ncols) a.cols_out[c][b] = ok ? col[c] : 0.0f;
 }
 
 // per-workgroup table of the exact u8 -> bf16 normalisation, 256 entries per
@@ -178,15 +201,20 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
 // One work item per workgroup, all of the grid's loads before its stores: the
 // shape for large outputs, where many resident workgroups keep the most bytes
 // in flight.
+// Blocks [0, tail): scalar columns, then the weights block (if any).
+__device__ __forceinline__ bool tail_block(const GatherArgs& a, int64_t tail) {
+    const int64_t blk = blockIdx.x;
+    if (blk >= tail) return false;
+    if (a.weights.w && blk == tail - 1) is_weights_block<kThreads>(a.weights);
+    else gather_scalars(a, blk);
+    return true;
+}
+
 template <int XF, bool NT>
-__global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t bpf, int64_t n_items) {
+__global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t bpf, int64_t n_items, int32_t tail) {
     __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
-    const int64_t it = blockIdx.x;
-    if (it >= n_items) {
-        if (a.weights.w && blockIdx.x == gridDim.x - 1) is_weights_block<kThreads>(a.weights);
-        else gather_scalars(a, it - n_items);
-        return;
-    }
+    if (tail_block(a, tail)) return;
+    const int64_t it = (int64_t)blockIdx.x - tail;
     if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
         build_lut(a, lut);
         __syncthreads();
@@ -207,13 +235,10 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
 // instead of the whole GPU reading first and writing afterwards.  The sample
 // index of the item after next is fetched one step ahead as well.
 template <int XF, bool NT>
-__global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t bpf, int64_t n_items, int32_t frame_grid) {
+__global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t bpf, int64_t n_items, int32_t frame_grid,
+                                                          int32_t tail) {
     __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
-    if ((int32_t)blockIdx.x >= frame_grid) {
-        if (a.weights.w && blockIdx.x == gridDim.x - 1) is_weights_block<kThreads>(a.weights);
-        else gather_scalars(a, (int64_t)blockIdx.x - frame_grid);
-        return;
-    }
+    if (tail_block(a, tail)) return;
     if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
         build_lut(a, lut);
         __syncthreads();
@@ -221,7 +246,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
     const int64_t G = frame_grid;
     const int64_t per_row = (int64_t)bpf * a.stack;
     auto clampi = [&](int64_t x) { return x < n_items ? x : n_items - 1; };
-    int64_t it = blockIdx.x;
+    int64_t it = (int64_t)blockIdx.x - tail;
     const int64_t i0 = a.idx[it / per_row];
     int64_t itn = it + G;
     int64_t i1 = a.idx[clampi(itn) / per_row];
@@ -266,6 +291,12 @@ __global__ __launch_bounds__(kThreads) void k_pack(PackArgs a) {
     const int64_t i = a.idx[b];
     const bool ok = i >= 0 && i < a.size;
     if (!ok && threadIdx.x == 0) flag_error(a.err, ERR_GATHER_INDEX);
+    // the row's scalar columns are loaded now, with its length, and stored last
+    const int64_t si = ok ? i : 0;
+    const float rew = a.out_reward ? a.reward[si] : 0.0f;
+    const uint8_t dn = a.out_done ? a.done[si] : (uint8_t)0;
+    const bool act = a.out_action && (int)threadIdx.x < a.action_bytes;
+    const uint8_t ab = act ? a.action[si * a.action_bytes + threadIdx.x] : (uint8_t)0;
     int64_t L = ok ? a.length[i] : 0;
     if (L < 0) L = 0;
     if (L > a.max_len) L = a.max_len;
@@ -309,12 +340,13 @@ __global__ __launch_bounds__(kThreads) void k_pack(PackArgs a) {
     }
     if (threadIdx.x == 0) {
         if (a.out_length) a.out_length[b] = (int32_t)L;
-        if (a.out_reward) a.out_reward[b] = ok ? a.reward[i] : 0.0f;
-        if (a.out_done) a.out_done[b] = ok ? a.done[i] : (uint8_t)0;
+        if (a.out_reward) a.out_reward[b] = ok ? rew : 0.0f;
+        if (a.out_done) a.out_done[b] = ok ? dn : (uint8_t)0;
     }
-    if (a.out_action && a.action_bytes > 0) {
-        for (int c = threadIdx.x; c < a.action_bytes; c += kThreads)
-            a.out_action[b * a.action_bytes + c] = ok ? a.action[i * a.action_bytes + c] : (uint8_t)0;
+    if (act) a.out_action[b * a.action_bytes + threadIdx.x] = ok ? ab : (uint8_t)0;
+    if (a.out_action) {  // actions longer than one byte per lane
+        for (int c = (int)threadIdx.x + kThreads; c < a.action_bytes; c += kThreads)
+            a.out_action[b * a.action_bytes + c] = ok ? a.action[si * a.action_bytes + c] : (uint8_t)0;
     }
 }
 
@@ -343,11 +375,11 @@ void launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t bpf, int64_t n
         // small batches: persistent pipelined workgroups
         const int64_t frame_grid = n_items < 4LL * device_cus() ? n_items : 4LL * device_cus();
         hipLaunchKernelGGL((k_gather_pipe<XF, true>), dim3((unsigned)(frame_grid + tail_blocks)), dim3(kThreads), 0,
-                           s, a, (int32_t)bpf, n_items, (int32_t)frame_grid);
+                           s, a, (int32_t)bpf, n_items, (int32_t)frame_grid, (int32_t)tail_blocks);
     } else {
         // large batches: one workgroup per item
         hipLaunchKernelGGL((k_gather_rows<XF, true>), dim3((unsigned)(n_items + tail_blocks)), dim3(kThreads), 0, s,
-                           a, (int32_t)bpf, n_items);
+                           a, (int32_t)bpf, n_items, (int32_t)tail_blocks);
     }
 }
 
@@ -357,7 +389,7 @@ hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
     const int64_t bpf = a.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
     const int64_t n_items = a.n * a.stack * bpf;
     const bool scalars = a.out_action || a.out_reward || a.out_done || a.ncols > 0;
-    // scalar-column workgroups, then the weights workgroup (last in the grid)
+    // scalar-column workgroups and the weights workgroup, at the head of the grid
     const int64_t tail_blocks = (scalars ? (a.n + kThreads - 1) / kThreads : 0) + (a.weights.w ? 1 : 0);
     if (n_items + tail_blocks == 0) return hipSuccess;
     switch (a.xform) {

@@ -27,6 +27,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kCopyUnroll = 4;
+constexpr int kActWords = 8;  // action words of a row held in registers
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -96,38 +97,52 @@ __device__ void ingest_meta(const IngestArgs& a, int64_t block) {
     const uint64_t any_valid = __ballot(valid);
     if (any_valid == 0) return;  // whole wavefront past the end (wave-uniform)
 
+    // every load of the lane's row is issued before its first store (lanes past
+    // the end read row 0 and store nothing): one memory round trip in all
     uint64_t delta = 0;
     uint32_t p_seen = 0;
-    const uint32_t old = (valid && a.prioritized) ? a.tree.leaves[slot] : 0u;  // issued early
+    const int64_t jj = valid ? j : 0;
+    const uint32_t old = (valid && a.prioritized) ? a.tree.leaves[slot] : 0u;
+    const uint32_t p = !a.prioritized ? 0u : a.src_prio ? a.src_prio[jj] : a.state->max_prio;
+    const float rew = a.src_reward ? a.src_reward[jj] : 0.0f;
+    const uint8_t dn = a.src_done ? a.src_done[jj] : (uint8_t)0;
+    const uint32_t ep = a.src_episode ? a.src_episode[jj] : 0u;
+    const int32_t st = a.src_step ? a.src_step[jj] : 0;
+    const int64_t len = a.length ? a.src_offsets[jj + 1] - a.src_offsets[jj] : 0;
+    const bool act_words = a.src_action && (a.action_bytes & 3) == 0;
+    const int words = act_words ? a.action_bytes >> 2 : 0;
+    uint32_t w[kActWords];
+#pragma unroll
+    for (int c = 0; c < kActWords; ++c)
+        w[c] = c < words ? reinterpret_cast<const uint32_t*>(a.src_action + jj * a.action_bytes)[c] : 0u;
     if (valid) {
         if (a.action_bytes > 0) {
             uint8_t* dst = a.action + slot * a.action_bytes;
-            if (a.src_action) {
-                const uint8_t* src = a.src_action + j * a.action_bytes;
-                if ((a.action_bytes & 3) == 0) {
-                    for (int c = 0; c < a.action_bytes; c += 4)
-                        *reinterpret_cast<uint32_t*>(dst + c) = *reinterpret_cast<const uint32_t*>(src + c);
-                } else {
-                    for (int c = 0; c < a.action_bytes; ++c) dst[c] = src[c];
-                }
+            if (act_words) {
+#pragma unroll
+                for (int c = 0; c < kActWords; ++c)
+                    if (c < words) reinterpret_cast<uint32_t*>(dst)[c] = w[c];
+                for (int c = kActWords; c < words; ++c)  // long actions: the rest word by word
+                    reinterpret_cast<uint32_t*>(dst)[c] = reinterpret_cast<const uint32_t*>(a.src_action + j * a.action_bytes)[c];
+            } else if (a.src_action) {
+                for (int c = 0; c < a.action_bytes; ++c) dst[c] = a.src_action[j * a.action_bytes + c];
             } else {
                 for (int c = 0; c < a.action_bytes; ++c) dst[c] = 0;
             }
         }
-        a.reward[slot] = a.src_reward ? a.src_reward[j] : 0.0f;
-        a.done[slot] = a.src_done ? a.src_done[j] : (uint8_t)0;
-        a.episode[slot] = a.src_episode ? a.src_episode[j] : 0u;
-        a.step[slot] = a.src_step ? a.src_step[j] : 0;
+        a.reward[slot] = rew;
+        a.done[slot] = dn;
+        a.episode[slot] = ep;
+        a.step[slot] = st;
         if (a.length) {
-            int64_t len = a.src_offsets[j + 1] - a.src_offsets[j];
-            if (len < 0 || len > a.max_len) {
+            int64_t l = len;
+            if (l < 0 || l > a.max_len) {
                 flag_error(a.err, ERR_SEQ_LENGTH);
-                len = len < 0 ? 0 : a.max_len;
+                l = l < 0 ? 0 : a.max_len;
             }
-            a.length[slot] = (int32_t)len;
+            a.length[slot] = (int32_t)l;
         }
         if (a.prioritized) {
-            const uint32_t p = a.src_prio ? a.src_prio[j] : a.state->max_prio;
             p_seen = p;
             const uint32_t q = quantise_leaf(p, a.tree.alpha_num, a.tree.alpha_den, a.tree.frac_bits);
             a.tree.leaves[slot] = q;
