@@ -39,13 +39,10 @@ def parse():
     p.add_argument("--no-rows", action="store_true", help="only the headline DQN workload")
     p.add_argument("--only", default="", help="comma list of extra rows to run (ppo,large,tokens,tiny)")
     p.add_argument("--calibrate-copy", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
+    p.add_argument("--sources-sha", action="store_true",
+                   help="print the hash of the fused kernel's sources (for the counter summary)")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     return p.parse_args()
-
-
-def _sha(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
 # ----------------------------------------------------------------------------
@@ -207,14 +204,20 @@ def bench_dqn(steps, warmup):
         evs.append(e)
     torch.cuda.synchronize()
     assert buf.sync_check() == cd.OK, cd.last_error()
-    # the dominant kernel alone: the gathers of the timed steps' own batches,
-    # launched back to back between two events on the library's stream
-    gb0 = tm.ev()
+    # kernels alone, back to back between two events on the library's stream,
+    # over the timed steps' own inputs: the fused sampler + gather (the dominant
+    # kernel of the step, weights included as in the step) and the stand-alone
+    # gather of the same batches
+    fb0 = tm.ev()
+    for i in range(warmup, warmup + steps):
+        sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
+    fb1 = tm.ev()
     for i in range(warmup, warmup + steps):
         gat(h, pi[i], B, xfr, lbr, stream)
     gb1 = tm.ev()
     torch.cuda.synchronize()
-    gather_b2b_ms = gb0.elapsed_time(gb1) / steps
+    fused_b2b_ms = fb0.elapsed_time(fb1) / steps
+    gather_b2b_ms = fb1.elapsed_time(gb1) / steps
     names = ["ingest_512", "sample_gather_512 (sampler + gather launches)", "update_512"]
     per = {n: [e[k].elapsed_time(e[k + 1]) for e in evs] for k, n in enumerate(names)}
     kern = {n: _kernel_stats(v) for n, v in per.items()}
@@ -237,13 +240,22 @@ def bench_dqn(steps, warmup):
             if d == 0 or (d <= st_h[i] and ep_h[j] == ep_h[i] and st_h[j] == st_h[i] - d):
                 valid += 1
     row = 84 * 84
+    # gather: valid source frames, the index, the episode/step of the two slots
+    # each stacked frame compares, action/reward/done in and out, the output
     gather_bytes = valid * row + B * (8 + 4 + 4 + 1) + B * K * row * 4 + B * (4 + 4 + 1)
+    # fused sampler + gather: no index read; per sample one descent (the total,
+    # 64 children at each of depth-1 node levels and 64 leaves), the uniform,
+    # and the index and weight written
+    depth = buf.info().tree_depth
+    descent_bytes = 8 + (depth - 1) * 64 * 8 + 64 * 4
+    fused_bytes = gather_bytes - B * 8 + B * (descent_bytes + 8 + 8 + 4)
     ingest_bytes_per_frame = 2 * row + (4 + 4 + 1 + 4 + 4) * 2 + 4 + 4  # obs r+w, scalars r+w, leaf r+w
     buf.close()
     return {
         "B": B, "steps": steps, "warmup": warmup, "total_ms": total_ms, "host_enqueue_s": host_enqueue_s,
-        "gather_b2b_ms": gather_b2b_ms, "unfused_ms": unfused_ms,
-        "kernels": kern, "gather_bytes": gather_bytes, "valid_frames": valid, "prefill_s": prefill_s,
+        "gather_b2b_ms": gather_b2b_ms, "fused_b2b_ms": fused_b2b_ms, "unfused_ms": unfused_ms,
+        "kernels": kern, "gather_bytes": gather_bytes, "fused_bytes": fused_bytes, "descent_bytes": descent_bytes,
+        "valid_frames": valid, "prefill_s": prefill_s,
         "ingest_big": {"frames": 32768, "ms": ingest_big_ms,
                        "GBps": 32768 * ingest_bytes_per_frame / ingest_big_ms / 1e6},
         "ingest_bytes_per_frame": ingest_bytes_per_frame,
@@ -516,10 +528,23 @@ def calibrate_copy():
     print(json.dumps({"calibrate_copy_bytes": n}), flush=True)
 
 
-def _traffic_from_profile(kernel_src):
-    """HBM bytes per gather launch from the committed counter summary, if it was
-    taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "gather_dqn_counters.txt")
+# the sources the fused sampler + gather is built from: a counter summary taken
+# on other sources no longer describes the kernel
+FUSED_KERNEL_SOURCES = ["k_sample_gather.hip", "gather_dev.h", "descend.h", "common.h"]
+
+
+def kernel_sources_sha():
+    hsh = hashlib.sha256()
+    for name in FUSED_KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_24456_amd", "csrc", name), "rb") as f:
+            hsh.update(f.read())
+    return hsh.hexdigest()[:16]
+
+
+def _traffic_from_profile():
+    """HBM bytes per fused sampler + gather launch from the committed counter
+    summary, if it was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "sample_gather_dqn_counters.txt")
     if not os.path.exists(path):
         return None
     rec = {}
@@ -528,16 +553,18 @@ def _traffic_from_profile(kernel_src):
             if "=" in line and not line.lstrip().startswith("#"):
                 k, v = line.split("=", 1)
                 rec[k.strip()] = v.strip()
-    if rec.get("kernel_source_sha256_16") != _sha(kernel_src):
+    if rec.get("kernel_sources_sha256_16") != kernel_sources_sha():
         return None
     return float(rec["hbm_bytes_per_launch"])
 
 
 def main():
     args = parse()
+    if args.sources_sha:
+        print(kernel_sources_sha())
+        return
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
-              f"(the experience path here is single-GPU; see the sharding notes in DESIGN.md)", flush=True)
+        print(f"bench.py: the experience path runs on one GPU; --gpus {args.gpus} is not supported", flush=True)
         sys.exit(2)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
@@ -550,8 +577,9 @@ def main():
     ms_per_step = d["total_ms"] / args.steps
     value = d["B"] * args.steps / (d["total_ms"] / 1e3)
     g_ms = d["gather_b2b_ms"]
-    achieved = d["gather_bytes"] / g_ms / 1e6
-    kernel_src = os.path.join(ROOT, "paper_2609_24456_amd", "csrc", "k_gather.hip")
+    g_gbps = d["gather_bytes"] / g_ms / 1e6
+    f_ms = d["fused_b2b_ms"]
+    achieved = d["fused_bytes"] / f_ms / 1e6
     out = {
         "metric": METRIC,
         "value": value,
@@ -570,12 +598,18 @@ def main():
                                "gather 512 -> [512,4,84,84] fp32 + priority update 512",
                    "capacity": 1_000_000, "batch": 512, "frame_stack": 4},
         "ms_per_step_unfused": d["unfused_ms"] / args.steps,
-        "roofline": {"bound": "hbm", "kernel": "k_gather_pipe<U8_F32> (frame-stack gather + u8->fp32, "
-                                               "512 samples x 4 frames; the dominant kernel of the step)",
+        "roofline": {"bound": "hbm", "kernel": "k_sample_gather<U8_F32> (one launch: 512 tree descents, "
+                                               "IS weights, frame-stack gather 512 x 4 frames -> fp32; the "
+                                               "dominant kernel of the step)",
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
-                     "traffic": _traffic_from_profile(kernel_src),
-                     "algorithmic_bytes_per_launch": d["gather_bytes"], "avg_launch_us": g_ms * 1e3,
-                     "timing": "HIP events around back-to-back launches over the timed steps' batches"},
+                     "traffic": _traffic_from_profile(),
+                     "algorithmic_bytes_per_launch": d["fused_bytes"], "avg_launch_us": f_ms * 1e3,
+                     "timing": "HIP events around back-to-back launches over the timed steps' uniforms"},
+        "gather_GBps": g_gbps,
+        "gather_frac_of_peak": g_gbps / PEAK_HBM_GBPS,
+        "gather_kernel": "k_gather_pipe<U8_F32>: conduit_gather_transform alone over the timed steps' "
+                         "batches, back to back",
+        "gather_avg_launch_us": g_ms * 1e3,
         "kernels_us_in_step": {k: v["mean_us"] for k, v in d["kernels"].items()},
         "host_enqueue_us_per_step": d["host_enqueue_s"] * 1e6 / args.steps,
         "rows": {"dqn_ingest_32768": d["ingest_big"]},

@@ -618,14 +618,19 @@ conduit_status conduit_sample_gather(conduit_buffer* b, int64_t batch, const uin
     sa.beta = b->opts.beta;
     sa.state = b->state;
     sa.err = err_words(b->err_slot);
-    // the sampler parks the sampled leaves in is_w_out; the gather (or packing)
-    // launch carries one more workgroup that turns them into the IS weights
-    const WeightsArgs wa{is_w_out, batch, b->opts.beta};
-    ga.weights = wa;
-    pa.weights = wa;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = launch_descend(sa, s);
-    if (e == hipSuccess) e = b->opts.ragged ? launch_pack(pa, s) : launch_gather(ga, s);
+    // dense rows of a few work items: one fused launch
+    hipError_t e = b->opts.ragged ? hipErrorNotSupported : launch_sample_gather(sa, ga, s);
+    if (e == hipErrorNotSupported) {
+        // otherwise the sampler parks the sampled leaves in is_w_out, and the
+        // gather (or packing) launch carries one more workgroup that turns them
+        // into the IS weights
+        const WeightsArgs wa{is_w_out, batch, b->opts.beta};
+        ga.weights = wa;
+        pa.weights = wa;
+        e = launch_descend(sa, s);
+        if (e == hipSuccess) e = b->opts.ragged ? launch_pack(pa, s) : launch_gather(ga, s);
+    }
     if (e != hipSuccess) return hip_fail(e, "sample_gather launch");
     return CONDUIT_OK;
 }

@@ -218,14 +218,20 @@ struct WeightsArgs {
     double beta;
 };
 
-template <int NT>
+// COHERENT: the leaves were parked by other workgroups of the same launch with
+// agent-scope atomic stores, and are read back with agent-scope atomic loads.
+template <int NT, bool COHERENT = false>
 __device__ void is_weights_block(const WeightsArgs& a) {
     __shared__ uint32_t wave_min[NT / kWave];
     __shared__ uint32_t qmin_s;
-    const uint32_t* q_park = reinterpret_cast<const uint32_t*>(a.w);
+    uint32_t* q_park = reinterpret_cast<uint32_t*>(a.w);
+    auto parked = [&](int64_t k) -> uint32_t {
+        if constexpr (COHERENT) return __hip_atomic_load(q_park + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        else return q_park[k];
+    };
     uint32_t m = 0xffffffffu;
     for (int64_t k = threadIdx.x; k < a.batch; k += NT) {
-        const uint32_t q = q_park[k];
+        const uint32_t q = parked(k);
         if (q) m = q < m ? q : m;
     }
     m = wave_min_u32(m);
@@ -238,8 +244,8 @@ __device__ void is_weights_block(const WeightsArgs& a) {
     }
     __syncthreads();
     const double qmin = (double)qmin_s;
-    for (int64_t k = threadIdx.x; k < a.batch; k += NT) {
-        const uint32_t q = q_park[k];
+    for (int64_t k = threadIdx.x; k < a.batch; k += NT) {  // the same k per lane as above
+        const uint32_t q = parked(k);
         a.w[k] = q ? (float)pow(qmin / (double)q, a.beta) : 0.0f;
     }
 }
@@ -348,6 +354,11 @@ struct GatherArgs {
 };
 
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
+
+// Fused sampler + gather for dense buffers with short rows (returns
+// hipErrorNotSupported, launching nothing, for shapes it does not take): the
+// sampler's arguments and the gather's, whose idx is the sampler's idx_out.
+hipError_t launch_sample_gather(const SampleArgs& sa, const GatherArgs& ga, hipStream_t s);
 
 struct PackArgs {
     const int64_t* idx;

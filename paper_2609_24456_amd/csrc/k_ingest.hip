@@ -28,9 +28,19 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kCopyUnroll = 4;
 constexpr int kActWords = 8;  // action words of a row held in registers
+constexpr int kRaggedUnroll = 8;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ void pin(u32x4& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void pin(u32x2& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void pin(uint32_t& x) { asm volatile("" : "+v"(x)); }
+__device__ __forceinline__ void pin(uint8_t& x) {
+    uint32_t w = x;
+    asm volatile("" : "+v"(w));
+    x = (uint8_t)w;
+}
 
 template <typename V>
 __device__ void copy_dense(const IngestArgs& a, int64_t block) {
@@ -49,6 +59,11 @@ __device__ void copy_dense(const IngestArgs& a, int64_t block) {
         const int64_t i = base + (int64_t)r * kThreads;
         v[r] = src[i < total ? i : total - 1];
     }
+    // the empty asm statements keep every load ahead of the first store: the
+    // compiler would otherwise sink loads into the stores' range checks and
+    // wait between stores (vmcnt counts both)
+#pragma unroll
+    for (int r = 0; r < kCopyUnroll; ++r) pin(v[r]);
 #pragma unroll
     for (int r = 0; r < kCopyUnroll; ++r) {
         const int64_t i = base + (int64_t)r * kThreads;
@@ -67,13 +82,36 @@ __device__ void copy_ragged(const IngestArgs& a, int64_t j) {
     if (len < 0) len = 0;
     if (len > a.max_len) len = a.max_len;  // flagged by the meta lane of row j
     const int64_t off = a.src_offsets[j];
+    if (len == 0) return;
     const uint32_t* __restrict__ s = reinterpret_cast<const uint32_t*>(a.src_obs) + off;
     uint32_t* __restrict__ d = reinterpret_cast<uint32_t*>(a.obs + slot * a.row_bytes);
-    for (int64_t t = threadIdx.x; t < len; t += kThreads) d[t] = s[t];
-    if (a.aux && a.src_aux) {
-        const uint32_t* __restrict__ sa = reinterpret_cast<const uint32_t*>(a.src_aux) + off;
-        uint32_t* __restrict__ da = reinterpret_cast<uint32_t*>(a.aux) + slot * a.max_len;
-        for (int64_t t = threadIdx.x; t < len; t += kThreads) da[t] = sa[t];
+    const bool aux = a.aux && a.src_aux;
+    const uint32_t* __restrict__ sa = aux ? reinterpret_cast<const uint32_t*>(a.src_aux) + off : s;
+    uint32_t* __restrict__ da = aux ? reinterpret_cast<uint32_t*>(a.aux) + slot * a.max_len : nullptr;
+    // kRaggedUnroll elements per lane per pass, every load (clamped to the last
+    // element) ahead of the stores
+    for (int64_t t0 = threadIdx.x; t0 < len; t0 += (int64_t)kThreads * kRaggedUnroll) {
+        uint32_t v[kRaggedUnroll], w[kRaggedUnroll];
+#pragma unroll
+        for (int r = 0; r < kRaggedUnroll; ++r) {
+            const int64_t t = t0 + (int64_t)r * kThreads;
+            const int64_t tc = t < len ? t : len - 1;
+            v[r] = s[tc];
+            w[r] = sa[tc];
+        }
+#pragma unroll
+        for (int r = 0; r < kRaggedUnroll; ++r) {
+            pin(v[r]);
+            pin(w[r]);
+        }
+#pragma unroll
+        for (int r = 0; r < kRaggedUnroll; ++r) {
+            const int64_t t = t0 + (int64_t)r * kThreads;
+            if (t < len) {
+                d[t] = v[r];
+                if (aux) da[t] = w[r];
+            }
+        }
     }
 }
 

@@ -1,0 +1,185 @@
+// Fused sampler + gather for dense buffers whose rows are a few work items
+// (the frame-stack DQN shape): one launch delivers indices, importance weights
+// and the learner batch (proportional prioritised replay, Schaul et al.; the
+// paper's off-policy delivery samples and then materialises the batch,
+// Sec. 2.2).
+//
+// Two kinds of workgroup share the grid:
+//   * sampler workgroups (the head of the grid, four samples each, one per
+//     wavefront) run tree_descend (descend.h), write the indices and error
+//     flags, and park each sampled leaf in the weight array;
+//   * gather workgroups (W per sample, two work items each; W = 2 for a stack
+//     of four frames) run the same descent for their sample themselves -- a
+//     few KB of redundant tree reads -- so the frame loads never wait for
+//     another workgroup or for the index to make a round trip through memory.
+//     The first of a sample's W writes its scalar columns.
+//
+// Importance weights need the smallest sampled leaf of the whole batch.  Each
+// sampler workgroup parks its leaves with agent-scope atomic stores, waits
+// until they are acknowledged (visible device-wide), and takes a ticket with
+// one agent-scope atomic add on the buffer's device state.  The workgroup that
+// draws the last ticket reads every leaf back with agent-scope atomic loads,
+// writes the weights (is_weights_block) and resets the ticket for the next
+// call.  No workgroup waits for another, no release fence (which would write
+// back the L2 under the frame stores) is needed, and the ticket latency stays
+// off the frame workgroups.
+#include "descend.h"
+#include "gather_dev.h"
+
+namespace conduit {
+
+namespace {
+
+// The row's scalar columns, one column word per lane: every load before any
+// store (the row's slot is known, so this is one memory round trip).
+__device__ __forceinline__ void row_scalars(const GatherArgs& a, int64_t b, int64_t i) {
+    const bool ok = i >= 0 && i < a.limit;
+    const int64_t s = ok ? i : 0;
+    const bool words = (a.action_bytes & 3) == 0;
+    const int na = a.out_action && a.action_bytes > 0 ? (words ? a.action_bytes >> 2 : a.action_bytes) : 0;
+    for (int t = threadIdx.x; t < na + 2; t += kThreads) {
+        if (t < na) {
+            if (words) {
+                const uint32_t v = reinterpret_cast<const uint32_t*>(a.action + s * a.action_bytes)[t];
+                reinterpret_cast<uint32_t*>(a.out_action + b * a.action_bytes)[t] = ok ? v : 0u;
+            } else {
+                const uint8_t v = a.action[s * a.action_bytes + t];
+                a.out_action[b * a.action_bytes + t] = ok ? v : (uint8_t)0;
+            }
+        } else if (t == na) {
+            if (a.out_reward) {
+                const float v = a.reward[s];
+                a.out_reward[b] = ok ? v : 0.0f;
+            }
+        } else {
+            if (a.out_done) {
+                const uint8_t v = a.done[s];
+                a.out_done[b] = ok ? v : (uint8_t)0;
+            }
+        }
+    }
+}
+
+constexpr int kSamplesPerSamplerWg = kThreads / kWave;
+
+template <int PRE>
+__device__ void sampler_wg(const SampleArgs& sa, const DivB& dv, int64_t wg) {
+    __shared__ uint32_t s_last;
+    const int64_t k = wg * kSamplesPerSamplerWg + threadIdx.x / kWave;
+    if (k < sa.batch) {  // wave-uniform
+        const Descent d = tree_descend<PRE>(sa.tree, sa.uniforms, k, dv);
+        if (lane_id() == 0) {
+            sa.idx_out[k] = d.slot;
+            if (d.slot < 0 && k == 0) flag_error(sa.err, ERR_EMPTY_TREE);
+            if (d.lost) flag_error(sa.err, ERR_DESCENT);
+            if (sa.w_out)
+                __hip_atomic_store(reinterpret_cast<uint32_t*>(sa.w_out) + k, d.leaf, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    if (!sa.w_out) return;  // kernel argument: uniform
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's parked leaves are acknowledged
+    __syncthreads();                // ... and every wavefront's
+    if (threadIdx.x == 0) {
+        const uint32_t tickets = (uint32_t)((sa.batch + kSamplesPerSamplerWg - 1) / kSamplesPerSamplerWg);
+        const uint32_t t = __hip_atomic_fetch_add(&sa.state->ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = t == tickets - 1;
+    }
+    __syncthreads();
+    if (s_last) {  // every leaf of the batch is parked and visible
+        is_weights_block<kThreads, true>(WeightsArgs{sa.w_out, sa.batch, sa.beta});
+        if (threadIdx.x == 0) __hip_atomic_store(&sa.state->ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+template <int XF, int PRE>
+__global__ __launch_bounds__(kThreads) void k_sample_gather(SampleArgs sa, GatherArgs a, DivB dv, int32_t bpf,
+                                                            int32_t wgs, int32_t sampler_wgs) {
+    __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
+    __shared__ int64_t s_slot;
+    if ((int32_t)blockIdx.x < sampler_wgs) {
+        sampler_wg<PRE>(sa, dv, blockIdx.x);
+        return;
+    }
+    const int64_t g = (int64_t)blockIdx.x - sampler_wgs;
+    const int64_t b = g / wgs;
+    const int part = (int)(g - b * wgs);
+    if (threadIdx.x < kWave) {
+        const Descent d = tree_descend<PRE>(sa.tree, sa.uniforms, b, dv);
+        if (threadIdx.x == 0) s_slot = d.slot;
+    } else if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
+        build_lut(a, lut, kWave, kThreads - kWave);
+    }
+    __syncthreads();
+    const int64_t i = s_slot;
+    const bool owner = part == 0;
+    // this workgroup's items of the row, double-buffered
+    const int64_t per_row = (int64_t)bpf * a.stack;
+    const int64_t per_wg = (per_row + wgs - 1) / wgs;
+    const int64_t it0 = b * per_row + part * per_wg;
+    int64_t it_end = it0 + per_wg;
+    if (it_end > (b + 1) * per_row) it_end = (b + 1) * per_row;
+    if (it0 >= it_end) {
+        if (owner) row_scalars(a, b, i);
+        return;
+    }
+    uint32_t va[kUnroll], vb[kUnroll];
+    int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
+    uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
+    Item ta = decode(a, it0, bpf, i), tb;
+    issue(a, ta, i, va, sia, sja, eia, eja);
+    if (owner) row_scalars(a, b, i);
+    for (int64_t it = it0; it < it_end; it += 2) {
+        const bool has_b = it + 1 < it_end;  // uniform
+        if (has_b) {
+            tb = decode(a, it + 1, bpf, i);
+            issue(a, tb, i, vb, sib, sjb, eib, ejb);
+        }
+        finish<XF, true, false>(a, ta, va, sia, sja, eia, eja, lut);
+        if (!has_b) break;
+        if (it + 2 < it_end) {
+            ta = decode(a, it + 2, bpf, i);
+            issue(a, ta, i, va, sia, sja, eia, eja);
+        }
+        finish<XF, true, false>(a, tb, vb, sib, sjb, eib, ejb, lut);
+    }
+}
+
+// rows of at most this many work items take the fused kernel
+constexpr int64_t kFusedMaxItemsPerRow = 8;
+
+template <int XF>
+hipError_t launch_xf(const SampleArgs& sa, const GatherArgs& ga, hipStream_t s, int64_t bpf, int64_t wgs,
+                     const DivB& dv, int pre) {
+    const int64_t sampler_wgs = (sa.batch + kSamplesPerSamplerWg - 1) / kSamplesPerSamplerWg;
+    const dim3 grid((unsigned)(sampler_wgs + sa.batch * wgs)), block(kThreads);
+    const int32_t b32 = (int32_t)bpf, w32 = (int32_t)wgs, s32 = (int32_t)sampler_wgs;
+    if (pre == 4)
+        hipLaunchKernelGGL((k_sample_gather<XF, 4>), grid, block, 0, s, sa, ga, dv, b32, w32, s32);
+    else if (pre == 16)
+        hipLaunchKernelGGL((k_sample_gather<XF, 16>), grid, block, 0, s, sa, ga, dv, b32, w32, s32);
+    else
+        hipLaunchKernelGGL((k_sample_gather<XF, 0>), grid, block, 0, s, sa, ga, dv, b32, w32, s32);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_sample_gather(const SampleArgs& sa, const GatherArgs& ga, hipStream_t s) {
+    const int64_t units = ga.row_bytes >> 2;
+    const int64_t bpf = ga.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
+    const int64_t per_row = bpf * ga.stack;
+    if (sa.batch <= 0 || ga.ncols != 0 || per_row > kFusedMaxItemsPerRow) return hipErrorNotSupported;
+    const int64_t wgs = per_row > 2 ? (per_row + 1) / 2 : 1;  // two items per workgroup
+    const DivB dv = make_divb((uint64_t)sa.batch);
+    const int pre = descend_prefetch(sa.tree);
+    switch (ga.xform) {
+        case CONDUIT_XF_NONE: return launch_xf<CONDUIT_XF_NONE>(sa, ga, s, bpf, wgs, dv, pre);
+        case CONDUIT_XF_U8_F32: return launch_xf<CONDUIT_XF_U8_F32>(sa, ga, s, bpf, wgs, dv, pre);
+        case CONDUIT_XF_U8_BF16_NORM: return launch_xf<CONDUIT_XF_U8_BF16_NORM>(sa, ga, s, bpf, wgs, dv, pre);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace conduit

@@ -216,6 +216,58 @@ def test_dqn_full_capacity(fused):
 
 
 # ----------------------------------------------------------------------------
+# fused sample + gather: every transform, stacked and single frames, odd sizes
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("xf_kind,K,shape,B", [
+    (cd.XF_U8_BF16_NORM, 4, (3, 20, 24), 77), (cd.XF_U8_BF16_NORM, 1, (3, 20, 24), 300),
+    (cd.XF_NONE, 4, (5, 8), 1), (cd.XF_U8_F32, 2, (2, 60, 61), 513), (cd.XF_U8_F32, 1, (3, 40, 70), 64)])
+def test_fused_sample_gather_shapes(xf_kind, K, shape, B):
+    print(f"fused sample_gather xf={xf_kind} K={K} shape={shape} B={B}", flush=True)
+    rng = np.random.default_rng(B * 10 + K)
+    cap, n = 700, 900  # wraps
+    row = int(np.prod(shape))
+    done = (rng.random(n) < 0.05).astype(np.uint8)
+    episode, step = synth.episodes_from_done(done)
+    obs = rng.integers(0, 256, size=(n, row), dtype=np.uint8)
+    reward = rng.standard_normal(n).astype(np.float32)
+    action = rng.integers(0, 256, size=(n, 3), dtype=np.uint8)
+    prio = synth.quantise_priority(rng.lognormal(0, 1, n))
+    buf = _mk(cap, shape, torch.uint8, frame_stack=K, action_bytes=3)
+    store = np.zeros((cap, row), np.uint8)
+    orc = oracle.Replay(cap, shape, np.uint8, act_bytes=3, frame_stack=K, obs_storage=store)
+    for a in range(0, n, 250):
+        b = min(n, a + 250)
+        buf.ingest(dev(obs[a:b].reshape((b - a,) + shape)), action=dev(action[a:b]), reward=dev(reward[a:b]),
+                   done=dev(done[a:b]), episode_id=dev(episode[a:b]), step=dev(step[a:b]), prio=dev(prio[a:b]))
+        orc.ingest(b - a, obs=obs[a:b], action=action[a:b], reward=reward[a:b], done=done[a:b],
+                   episode=episode[a:b], step=step[a:b], prio=prio[a:b])
+    mean, std = (0.5, 0.25, 0.125), (0.2, 0.3, 0.7)
+    xf = cd.transform(xf_kind, mean, std) if xf_kind == cd.XF_U8_BF16_NORM else cd.transform(xf_kind)
+    out_dtype = {cd.XF_NONE: torch.uint8, cd.XF_U8_F32: torch.float32, cd.XF_U8_BF16_NORM: torch.bfloat16}[xf_kind]
+    out = torch.empty((B, K) + shape, dtype=out_dtype, device="cuda")
+    act = torch.empty((B, 3), dtype=torch.uint8, device="cuda")
+    rew = torch.empty(B, dtype=torch.float32, device="cuda")
+    dn = torch.empty(B, dtype=torch.uint8, device="cuda")
+    for it in range(3):
+        uu = synth.uniforms(rng, B)
+        idx, w = buf.sample_gather(dev(uu), xf, obs=out, action=act, reward=rew, done=dn)
+        o_idx, o_w = orc.sample(uu)
+        assert np.array_equal(host(idx), o_idx), it
+        assert_weights_close(host(w), o_w)
+        o_obs, o_act, o_rew, o_done = orc.gather(o_idx, xf_kind, mean, std)
+        g = host(out.view(torch.int16)) if xf_kind == cd.XF_U8_BF16_NORM else host(out)
+        assert np.array_equal(g.reshape(-1).view(np.uint8), o_obs.reshape(-1).view(np.uint8)), it
+        assert np.array_equal(host(act).reshape(o_act.shape), o_act), it
+        assert np.array_equal(host(rew), o_rew), it
+        assert np.array_equal(host(dn), o_done), it
+        up = synth.quantise_priority(rng.lognormal(0, 1, B))
+        buf.update(idx, dev(up))
+        orc.update(o_idx, up)
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
+
+
+# ----------------------------------------------------------------------------
 # sum-tree shapes, duplicates, degenerate cases
 # ----------------------------------------------------------------------------
 # capacities span every descent shape: depth 1 to 4, and the level under the
