@@ -267,11 +267,17 @@ conduit_status conduit_gather_transform(conduit_buffer* buf, const int64_t* idx,
                                         void* stream);
 
 /*
- * Fused delivery: exactly conduit_sample(buf, batch, uniforms, idx_out, is_w_out)
- * followed by conduit_gather_transform(buf, idx_out, batch, xf, out), with the
- * same outputs, arguments and errors as the two calls, in two launches instead
- * of three: the importance weights are computed by one extra workgroup of the
- * gather (or, for ragged buffers, packing) launch.
+ * Fused delivery (Sec. 2.2: delivery samples, then materialises the batch):
+ * exactly conduit_sample(buf, batch, uniforms, idx_out, is_w_out) followed by
+ * conduit_gather_transform(buf, idx_out, batch, xf, out), with the same
+ * outputs, arguments and errors as the two calls.  Dense buffers whose rows
+ * are at most 8 gather work items of 7,168 bytes (e.g. a stack of four 84x84
+ * frames) take one launch: the workgroups that gather a sample descend the
+ * tree for it themselves, and the importance weights are computed inside the
+ * same launch.  Other buffers take two launches: the sampler, then the gather
+ * (or packing) launch with one extra workgroup for the weights.  The call uses
+ * a word of the buffer's device state between its launches' workgroups, so
+ * calls on one buffer must not overlap (as for every call on a buffer).
  */
 conduit_status conduit_sample_gather(conduit_buffer* buf, int64_t batch, const uint64_t* uniforms, int64_t* idx_out,
                                      float* is_w_out, const conduit_transform* xf, const conduit_learner_batch* out,
