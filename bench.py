@@ -72,6 +72,23 @@ class Timer:
         return e
 
 
+def _b2b_ms(calls, reps=1):
+    """Milliseconds per call of `calls` (zero-argument callables that enqueue
+    on the library's stream), launched back to back between two events."""
+    import torch
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    rc = 0
+    e0.record()
+    for _ in range(reps):
+        for f in calls:
+            rc |= f()
+    e1.record()
+    torch.cuda.synchronize()
+    assert rc == 0, "a timed call failed"
+    return e0.elapsed_time(e1) / (reps * len(calls))
+
+
 def _kernel_stats(durs_ms):
     import numpy as np
     d = np.asarray(durs_ms)
@@ -266,28 +283,34 @@ def bench_dqn(steps, warmup):
 # other rows
 # ----------------------------------------------------------------------------
 def bench_ppo(reps=3):
+    """PPO rollout [2048 x 256] of 3x84x84 u8: rollout ingest (32 calls of 64
+    steps), GAE over [T, E], and the 32 minibatch gathers of one epoch; each
+    timed as back-to-back launches with prepared arguments."""
     import numpy as np
     import torch
     import synth
     from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
     cfg = synth.PPO()
     T, E, row = cfg.T, cfg.E, 3 * 84 * 84
     N = T * E
-    tm = Timer()
     # rollout ingest into an on-policy buffer (no priorities), 64 steps per call
     buf = cd.ReplayBuffer(N, cfg.obs_shape, torch.uint8, prioritized=False, action_bytes=0)
+    obs_all = cfg.obs_steps(0, T, "cuda")
     rew_d, done_d = _dev(cfg.reward.reshape(-1)), _dev(cfg.done.reshape(-1))
-    ing_ms = 0.0
+    structs = []
     for t0 in range(0, T, 64):
-        obs = cfg.obs_steps(t0, t0 + 64, "cuda")
+        t = cd.Transitions()
         sl = slice(t0 * E, (t0 + 64) * E)
-        torch.cuda.synchronize()
-        e0 = tm.ev()
-        buf.ingest(obs, reward=rew_d[sl], done=done_d[sl])
-        e1 = tm.ev()
-        torch.cuda.synchronize()
-        ing_ms += e0.elapsed_time(e1)
-        del obs
+        t.n = 64 * E
+        t.obs = obs_all[t0:t0 + 64].data_ptr()
+        t.reward, t.done = rew_d[sl].data_ptr(), done_d[sl].data_ptr()
+        structs.append(t)
+    h = C.c_void_p(buf.handle)
+    torch.cuda.synchronize()
+    ing_ms = _b2b_ms([lambda t=t: L.conduit_ingest(h, C.byref(t), stream) for t in structs]) * len(structs)
+    del obs_all
     src = torch.empty(N * row, dtype=torch.uint8, device="cuda")
     buf.read(cd.COL_OBS, src)
     torch.cuda.synchronize()
@@ -295,14 +318,11 @@ def bench_ppo(reps=3):
     r, v, d, b = _dev(cfg.reward), _dev(cfg.value), _dev(cfg.done), _dev(cfg.bootstrap)
     adv = torch.empty((T, E), dtype=torch.float32, device="cuda")
     ret = torch.empty((T, E), dtype=torch.float32, device="cuda")
-    g = []
-    for _ in range(20):
-        e0 = tm.ev()
-        cd.conduit_gae(r, v, d, b, cfg.gamma, cfg.lam, adv, ret)
-        e1 = tm.ev()
-        torch.cuda.synchronize()
-        g.append(e0.elapsed_time(e1))
-    gae_ms = float(np.median(g[2:]))
+    gae_args = (r.data_ptr(), v.data_ptr(), d.data_ptr(), b.data_ptr(), T, E, cfg.gamma, cfg.lam,
+                adv.data_ptr(), ret.data_ptr(), stream)
+    gae = lambda: L.conduit_gae(*gae_args)  # noqa: E731
+    _b2b_ms([gae] * 3)
+    gae_ms = _b2b_ms([gae] * 20)
     gae_bytes = N * (4 + 4 + 1 + 4 + 4) + E * 4
     A, R = adv.view(-1), ret.view(-1)
     mb = 16384
@@ -311,18 +331,14 @@ def bench_ppo(reps=3):
     a_out = torch.empty(mb, dtype=torch.float32, device="cuda")
     r_out = torch.empty(mb, dtype=torch.float32, device="cuda")
     xf = cd.transform(cd.XF_U8_F32)
-    times = []
-    for rep in range(reps):
-        for m in range(32):
-            e0 = tm.ev()
-            cd.conduit_minibatch_gather(src, row, N, perm[m * mb:(m + 1) * mb], xf, out, cols=[A, R],
-                                        cols_out=[a_out, r_out])
-            e1 = tm.ev()
-            times.append((e0, e1))
-    torch.cuda.synchronize()
+    cols = (C.c_void_p * 2)(A.data_ptr(), R.data_ptr())
+    cols_out = (C.c_void_p * 2)(a_out.data_ptr(), r_out.data_ptr())
+    calls = [lambda m=m: L.conduit_minibatch_gather(src.data_ptr(), row, N, perm[m * mb:(m + 1) * mb].data_ptr(), mb,
+                                                    C.byref(xf), out.data_ptr(), cols, cols_out, 2, stream)
+             for m in range(32)]
+    _b2b_ms(calls)  # first epoch: warm-up
+    mb_ms = _b2b_ms(calls, reps=reps - 1 if reps > 1 else 1)
     assert cd.conduit_sync_check() == cd.OK, cd.last_error()
-    mbt = [a.elapsed_time(b) for a, b in times][32:]  # first epoch is warm-up
-    mb_ms = float(np.mean(mbt))
     mb_bytes = mb * (row + row * 4 + 8 + 2 * 4 + 2 * 4)
     ing_bytes = N * (2 * row + 2 * (4 + 1) + 2 * (4 + 4))
     return {
@@ -332,15 +348,22 @@ def bench_ppo(reps=3):
                          "frac": gae_bytes / gae_ms / 1e6 / PEAK_HBM_GBPS},
         "minibatch_gather_16384": {"bytes": mb_bytes, "us": mb_ms * 1e3, "GBps": mb_bytes / mb_ms / 1e6,
                                    "frac": mb_bytes / mb_ms / 1e6 / PEAK_HBM_GBPS},
-        "epoch_32_minibatches_ms": float(np.sum(mbt[-32:])),
+        "epoch_32_minibatches_ms": mb_ms * 32,
+        "timing": "back-to-back launches between two events, arguments prepared up front",
     }
 
 
 def bench_large(iters=10):
+    """Large visual replay (200,000 slots of 3x224x224 u8): sample 1,024 (with
+    IS weights), gather -> normalised bf16 [1024, 3, 224, 224] with action and
+    reward, update 1,024; each call type timed as back-to-back launches with
+    prepared arguments, and whole iterations through the sample + gather call."""
     import numpy as np
     import torch
     import synth
     from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
     Cap, B, row = 200_000, 1024, 3 * 224 * 224
     cfg = synth.Large(Cap)
     buf = cd.ReplayBuffer(Cap, cfg.obs_shape, torch.uint8, action_bytes=24)
@@ -350,42 +373,53 @@ def bench_large(iters=10):
                    done=_dev(cfg.done[a:b]), prio=_dev(cfg.prio[a:b]))
     u, prio = cfg.draws(iters, B)
     u_d, p_d = _dev(u), _dev(prio)
+    idx = torch.empty((iters, B), dtype=torch.int64, device="cuda")
+    w = torch.empty((iters, B), dtype=torch.float32, device="cuda")
     out = torch.empty((B, 1) + cfg.obs_shape, dtype=torch.bfloat16, device="cuda")
     act = torch.empty((B, 6), dtype=torch.float32, device="cuda")
     rew = torch.empty(B, dtype=torch.float32, device="cuda")
     xf = cd.transform(cd.XF_U8_BF16_NORM, cfg.mean, cfg.std)
-    tm = Timer()
+    lb = cd.LearnerBatch()
+    lb.obs, lb.action, lb.reward = out.data_ptr(), act.data_ptr(), rew.data_ptr()
+    h = C.c_void_p(buf.handle)
+    xfr, lbr = C.byref(xf), C.byref(lb)
+    pu = [u_d[i].data_ptr() for i in range(iters)]
+    pp = [p_d[i].data_ptr() for i in range(iters)]
+    pi = [idx[i].data_ptr() for i in range(iters)]
+    pw = [w[i].data_ptr() for i in range(iters)]
     torch.cuda.synchronize()
-    s_t, g_t, u_t = [], [], []
+    it_calls = []
     for i in range(iters):
-        e0 = tm.ev()
-        idx, w = buf.sample(u_d[i])
-        e1 = tm.ev()
-        buf.gather(idx, xf, obs=out, action=act, reward=rew)
-        e2 = tm.ev()
-        buf.update(idx, p_d[i])
-        e3 = tm.ev()
-        s_t.append((e0, e1))
-        g_t.append((e1, e2))
-        u_t.append((e2, e3))
-    torch.cuda.synchronize()
+        it_calls.append(lambda i=i: L.conduit_sample_gather(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream))
+        it_calls.append(lambda i=i: L.conduit_update_priorities(h, pi[i], pp[i], B, stream))
+    iter_ms = _b2b_ms(it_calls) * 2
+    smp_ms = _b2b_ms([lambda i=i: L.conduit_sample(h, B, pu[i], pi[i], pw[i], stream) for i in range(iters)])
+    gat_ms = _b2b_ms([lambda i=i: L.conduit_gather_transform(h, pi[i], B, xfr, lbr, stream) for i in range(iters)])
+    upd_ms = _b2b_ms([lambda i=i: L.conduit_update_priorities(h, pi[i], pp[i], B, stream) for i in range(iters)])
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
-    gms = float(np.median([a.elapsed_time(b) for a, b in g_t[2:]]))
     gbytes = B * (row + 2 * row + 8 + 24 + 4 + 24 + 4)
     return {
-        "gather_bf16_1024": {"bytes": gbytes, "us": gms * 1e3, "GBps": gbytes / gms / 1e6,
-                             "frac": gbytes / gms / 1e6 / PEAK_HBM_GBPS},
-        "sample_1024_us": float(np.median([a.elapsed_time(b) for a, b in s_t[2:]]) * 1e3),
-        "update_1024_us": float(np.median([a.elapsed_time(b) for a, b in u_t[2:]]) * 1e3),
+        "gather_bf16_1024": {"bytes": gbytes, "us": gat_ms * 1e3, "GBps": gbytes / gat_ms / 1e6,
+                             "frac": gbytes / gat_ms / 1e6 / PEAK_HBM_GBPS},
+        "sample_1024_us": smp_ms * 1e3,
+        "update_1024_us": upd_ms * 1e3,
+        "iteration_us": iter_ms * 1e3,
+        "timing": "back-to-back launches between two events, arguments prepared up front",
     }
 
 
 def bench_tokens(iters=10):
+    """Token replay (65,536 ragged sequences of up to 4,096 int32 tokens + fp32
+    log-probs): per iteration sample 256 + pack to [256, 4096] with mask, log-probs
+    and lengths, GAE over the packed rows, update 256; whole iterations and each
+    call type timed as back-to-back launches with prepared arguments."""
     import numpy as np
     import torch
     import synth
     from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
     Cap, Lmax, B = 65536, 4096, 256
     cfg = synth.Tokens(Cap)
     buf = cd.ReplayBuffer(Cap, (Lmax,), torch.int32, action_bytes=4, ragged=True, aux_elem_bytes=4)
@@ -397,6 +431,8 @@ def bench_tokens(iters=10):
         del tok, lp
     u, prio = cfg.draws(iters, B)
     u_d, p_d = _dev(u), _dev(prio)
+    idx = torch.empty((iters, B), dtype=torch.int64, device="cuda")
+    w = torch.empty((iters, B), dtype=torch.float32, device="cuda")
     seq = torch.empty((B, Lmax), dtype=torch.int32, device="cuda")
     mask = torch.empty((B, Lmax), dtype=torch.uint8, device="cuda")
     lp_out = torch.empty((B, Lmax), dtype=torch.float32, device="cuda")
@@ -405,46 +441,52 @@ def bench_tokens(iters=10):
     adv = torch.empty((B, Lmax), dtype=torch.float32, device="cuda")
     ret = torch.empty((B, Lmax), dtype=torch.float32, device="cuda")
     xf = cd.transform(cd.XF_TOKENS_PAD)
-    tm = Timer()
+    lb = cd.LearnerBatch()
+    lb.obs, lb.mask, lb.aux, lb.length, lb.reward = (seq.data_ptr(), mask.data_ptr(), lp_out.data_ptr(),
+                                                     length.data_ptr(), rew.data_ptr())
+    h = C.c_void_p(buf.handle)
+    xfr, lbr = C.byref(xf), C.byref(lb)
+    pu = [u_d[i].data_ptr() for i in range(iters)]
+    pp = [p_d[i].data_ptr() for i in range(iters)]
+    pi = [idx[i].data_ptr() for i in range(iters)]
+    pw = [w[i].data_ptr() for i in range(iters)]
+    gae_args = (rew.data_ptr(), length.data_ptr(), None, B, Lmax, cfg.gamma, cfg.lam, adv.data_ptr(), ret.data_ptr(),
+                stream)
+    gae = lambda: L.conduit_gae_packed(*gae_args)  # noqa: E731
     torch.cuda.synchronize()
-    pk, ga, it_t = [], [], []
-    lens = []
+    it_calls = []
     for i in range(iters):
-        e0 = tm.ev()
-        idx, w = buf.sample(u_d[i])
-        e1 = tm.ev()
-        buf.gather(idx, xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
-        e2 = tm.ev()
-        cd.conduit_gae_packed(rew, length, None, Lmax, cfg.gamma, cfg.lam, adv, ret)
-        e3 = tm.ev()
-        buf.update(idx, p_d[i])
-        e4 = tm.ev()
-        pk.append((e1, e2))
-        ga.append((e2, e3))
-        it_t.append((e0, e4))
-        lens.append(length.clone())
-    torch.cuda.synchronize()
+        it_calls.append(lambda i=i: L.conduit_sample_gather(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream))
+        it_calls.append(gae)
+        it_calls.append(lambda i=i: L.conduit_update_priorities(h, pi[i], pp[i], B, stream))
+    iter_ms = _b2b_ms(it_calls) * 3
+    mean_len = float(length.float().mean())
+    pack_ms = _b2b_ms([lambda i=i: L.conduit_gather_transform(h, pi[i], B, xfr, lbr, stream) for i in range(iters)])
+    gae_ms = _b2b_ms([gae] * iters)
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
-    mean_len = float(torch.stack(lens).float().mean())
-    pms = float(np.median([a.elapsed_time(b) for a, b in pk[2:]]))
-    gms = float(np.median([a.elapsed_time(b) for a, b in ga[2:]]))
     pbytes = int(B * mean_len * 8 + B * Lmax * (4 + 1 + 4) + B * (8 + 4 + 4 + 4 + 4))
     gbytes = B * (4 + 4) + B * Lmax * 8
     return {
-        "pack_256x4096": {"bytes": pbytes, "us": pms * 1e3, "GBps": pbytes / pms / 1e6,
-                          "frac": pbytes / pms / 1e6 / PEAK_HBM_GBPS},
-        "gae_packed_256x4096": {"bytes": gbytes, "us": gms * 1e3, "GBps": gbytes / gms / 1e6,
-                                "frac": gbytes / gms / 1e6 / PEAK_HBM_GBPS},
-        "iteration_us": float(np.median([a.elapsed_time(b) for a, b in it_t[2:]]) * 1e3),
+        "pack_256x4096": {"bytes": pbytes, "us": pack_ms * 1e3, "GBps": pbytes / pack_ms / 1e6,
+                          "frac": pbytes / pack_ms / 1e6 / PEAK_HBM_GBPS},
+        "gae_packed_256x4096": {"bytes": gbytes, "us": gae_ms * 1e3, "GBps": gbytes / gae_ms / 1e6,
+                                "frac": gbytes / gae_ms / 1e6 / PEAK_HBM_GBPS},
+        "iteration_us": iter_ms * 1e3,
+        "timing": "back-to-back launches between two events, arguments prepared up front",
     }
 
 
 def bench_tiny(iters=100):
+    """Tiny replay (16,384 slots of 8 fp32): 100 x [ingest 64, sample + gather 256
+    with IS weights (one launch), update 256], every call's arguments prepared
+    before the timed loop.  Launch-latency bound."""
     import numpy as np
     import torch
     import synth
     from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
     cfg = synth.Tiny()
     u, prio = cfg.draws()
     B, n_in = cfg.batch, cfg.ingest_n
@@ -452,24 +494,51 @@ def bench_tiny(iters=100):
     obs, act, rew, done = _dev(cfg.obs), _dev(cfg.action), _dev(cfg.reward), _dev(cfg.done)
     epi, stp = _dev(cfg.episode), _dev(cfg.step)
     u_d, p_d = _dev(u), _dev(prio)
+    idx = torch.empty((iters, B), dtype=torch.int64, device="cuda")
+    w = torch.empty((iters, B), dtype=torch.float32, device="cuda")
     out = torch.empty((B, 1, 8), dtype=torch.float32, device="cuda")
+    act_out = torch.empty(B, dtype=torch.int32, device="cuda")
+    rew_out = torch.empty(B, dtype=torch.float32, device="cuda")
+    done_out = torch.empty(B, dtype=torch.uint8, device="cuda")
     xf = cd.transform(cd.XF_NONE)
+    lb = cd.LearnerBatch()
+    lb.obs, lb.action, lb.reward, lb.done = out.data_ptr(), act_out.data_ptr(), rew_out.data_ptr(), done_out.data_ptr()
+    structs = []
+    for i in range(iters):
+        t = cd.Transitions()
+        sl = slice(i * n_in, (i + 1) * n_in)
+        t.n = n_in
+        t.obs = obs[sl].data_ptr()
+        t.action, t.reward, t.done = act[sl].data_ptr(), rew[sl].data_ptr(), done[sl].data_ptr()
+        t.episode_id, t.step = epi[sl].data_ptr(), stp[sl].data_ptr()
+        t.prio = None
+        structs.append(t)
+    trans = [C.byref(t) for t in structs]
+    h = C.c_void_p(buf.handle)
+    xfr, lbr = C.byref(xf), C.byref(lb)
+    pu = [u_d[i].data_ptr() for i in range(iters)]
+    pp = [p_d[i].data_ptr() for i in range(iters)]
+    pi = [idx[i].data_ptr() for i in range(iters)]
+    pw = [w[i].data_ptr() for i in range(iters)]
+    ing, sgat, upd = L.conduit_ingest, L.conduit_sample_gather, L.conduit_update_priorities
     tm = Timer()
     torch.cuda.synchronize()
     e0 = tm.ev()
+    h0 = time.perf_counter()
+    rc = 0
     for i in range(iters):
-        sl = slice(i * n_in, (i + 1) * n_in)
-        buf.ingest(obs[sl], action=act[sl], reward=rew[sl], done=done[sl], episode_id=epi[sl], step=stp[sl])
-        idx, w = buf.sample(u_d[i])
-        buf.gather(idx, xf, obs=out)
-        buf.update(idx, p_d[i])
+        rc |= ing(h, trans[i], stream)
+        rc |= sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
+        rc |= upd(h, pi[i], pp[i], B, stream)
     e1 = tm.ev()
+    host_s = time.perf_counter() - h0
     torch.cuda.synchronize()
+    assert rc == 0, cd.last_error()
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
     ms = e0.elapsed_time(e1)
-    return {"iterations": iters, "us_per_iteration": ms * 1e3 / iters, "launches_per_iteration": 4,
-            "sampled_per_s": iters * B / (ms / 1e3)}
+    return {"iterations": iters, "us_per_iteration": ms * 1e3 / iters, "launches_per_iteration": 3,
+            "host_enqueue_us_per_iteration": host_s * 1e6 / iters, "sampled_per_s": iters * B / (ms / 1e3)}
 
 
 # ----------------------------------------------------------------------------
