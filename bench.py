@@ -37,7 +37,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-rows", action="store_true", help="only the headline DQN workload")
-    p.add_argument("--only", default="", help="comma list of extra rows to run (ppo,large,tokens,tiny)")
+    p.add_argument("--only", default="", help="comma list of extra rows to run (ppo,large,tokens,tiny,stress)")
     p.add_argument("--calibrate-copy", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
     p.add_argument("--sources-sha", action="store_true",
                    help="print the hash of the fused kernel's sources (for the counter summary)")
@@ -477,6 +477,84 @@ def bench_tokens(iters=10):
     }
 
 
+def bench_stress(dims=(128, 1000, 5000, 10000, 20000), iters=20):
+    """The paper's synthetic stress sweep at capacity 10^6 and batch 512: for
+    each transition dimension d (obs and next_obs, d fp32 each, 8d bytes per
+    slot) a full buffer (up to 160 GB at d = 20,000), then iterations of
+    ingest 512 + sample + gather 512 (one call, IS weights, no transform) +
+    update 512, timed as back-to-back launches with prepared arguments."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    Cap, B = 1_000_000, 512
+    res = {}
+    for d in dims:
+        torch.cuda.empty_cache()
+        cfg = synth.Stress(d, Cap + iters * B)
+        row = 8 * d
+        buf = cd.ReplayBuffer(Cap, cfg.obs_shape, torch.float32, action_bytes=4)
+        act_d, rew_d, done_d, prio_d = _dev(cfg.action), _dev(cfg.reward), _dev(cfg.done), _dev(cfg.prio)
+        chunk = max(512, min(65536, (1 << 30) // row))
+        t0 = time.time()
+        for a in range(0, Cap, chunk):
+            b = min(Cap, a + chunk)
+            buf.ingest(cfg.rows(a, b - a, "cuda"), action=act_d[a:b], reward=rew_d[a:b], done=done_d[a:b],
+                       prio=prio_d[a:b])
+        torch.cuda.synchronize()
+        prefill_s = time.time() - t0
+        new_rows = cfg.rows(Cap, iters * B, "cuda")
+        u, prio = cfg.draws(iters, B)
+        u_d, p_d = _dev(u), _dev(prio)
+        idx = torch.empty((iters, B), dtype=torch.int64, device="cuda")
+        w = torch.empty((iters, B), dtype=torch.float32, device="cuda")
+        out = torch.empty((B, 1) + cfg.obs_shape, dtype=torch.float32, device="cuda")
+        act = torch.empty(B, dtype=torch.int32, device="cuda")
+        rew = torch.empty(B, dtype=torch.float32, device="cuda")
+        xf = cd.transform(cd.XF_NONE)
+        lb = cd.LearnerBatch()
+        lb.obs, lb.action, lb.reward = out.data_ptr(), act.data_ptr(), rew.data_ptr()
+        structs = []
+        for i in range(iters):
+            t = cd.Transitions()
+            sl = slice(Cap + i * B, Cap + (i + 1) * B)
+            t.n = B
+            t.obs = new_rows[i * B:(i + 1) * B].data_ptr()
+            t.action, t.reward, t.done = act_d[sl].data_ptr(), rew_d[sl].data_ptr(), done_d[sl].data_ptr()
+            t.prio = prio_d[sl].data_ptr()
+            structs.append(t)
+        h = C.c_void_p(buf.handle)
+        xfr, lbr = C.byref(xf), C.byref(lb)
+        pu = [u_d[i].data_ptr() for i in range(iters)]
+        pp = [p_d[i].data_ptr() for i in range(iters)]
+        pi = [idx[i].data_ptr() for i in range(iters)]
+        pw = [w[i].data_ptr() for i in range(iters)]
+        calls = []
+        for i in range(iters):
+            calls.append(lambda i=i: L.conduit_ingest(h, C.byref(structs[i]), stream))
+            calls.append(lambda i=i: L.conduit_sample_gather(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream))
+            calls.append(lambda i=i: L.conduit_update_priorities(h, pi[i], pp[i], B, stream))
+        _b2b_ms(calls[:3])
+        iter_ms = _b2b_ms(calls) * 3
+        ing_ms = _b2b_ms([lambda i=i: L.conduit_ingest(h, C.byref(structs[i]), stream) for i in range(iters)])
+        sg_ms = _b2b_ms([lambda i=i: L.conduit_sample_gather(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
+                         for i in range(iters)])
+        assert buf.sync_check() == cd.OK, cd.last_error()
+        buf.close()
+        del new_rows, out
+        # algorithmic bytes: ingest reads and writes each row and 17 B of scalars
+        # plus the leaf; delivery reads and writes each sampled row and scalars
+        ing_bytes = B * (2 * row + 2 * 17 + 8)
+        sg_bytes = B * (2 * row + 8 + 2 * (4 + 4))
+        res[f"d={d}"] = {"buffer_GB": Cap * row / 1e9, "prefill_s": prefill_s, "iteration_us": iter_ms * 1e3,
+                         "sampled_per_s": B / (iter_ms / 1e3),
+                         "ingest_512_us": ing_ms * 1e3, "ingest_GBps": ing_bytes / ing_ms / 1e6,
+                         "sample_gather_512_us": sg_ms * 1e3, "sample_gather_GBps": sg_bytes / sg_ms / 1e6}
+    return res
+
+
 def bench_tiny(iters=100):
     """Tiny replay (16,384 slots of 8 fp32): 100 x [ingest 64, sample + gather 256
     with IS weights (one launch), update 256], every call's arguments prepared
@@ -684,7 +762,7 @@ def main():
         "rows": {"dqn_ingest_32768": d["ingest_big"]},
     }
     if not args.no_rows:
-        only = set(x for x in args.only.split(",") if x) or {"ppo", "large", "tokens", "tiny"}
+        only = set(x for x in args.only.split(",") if x) or {"ppo", "large", "tokens", "tiny", "stress"}
         if "tiny" in only:
             out["rows"]["tiny"] = bench_tiny()
         if "ppo" in only:
@@ -695,6 +773,9 @@ def main():
             torch.cuda.empty_cache()
         if "tokens" in only:
             out["rows"]["tokens"] = bench_tokens()
+            torch.cuda.empty_cache()
+        if "stress" in only:
+            out["rows"]["stress"] = bench_stress()
             torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         cb = cpu_baseline(args.cpu_seconds)

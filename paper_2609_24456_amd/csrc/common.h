@@ -353,6 +353,12 @@ struct GatherArgs {
     WeightsArgs weights;
 };
 
+// compute units of the current device (cached per device)
+int device_cus();
+// whether a gather moves its rows in 16-byte units (no transform, 16-byte
+// aligned source, output and row size)
+bool copy16(const GatherArgs& a);
+
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s);
 
 // Fused sampler + gather for dense buffers with short rows (returns

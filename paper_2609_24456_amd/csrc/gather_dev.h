@@ -29,6 +29,22 @@ constexpr int kUnitsPerBlock = kThreads * kUnroll;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Internal transform code (not part of the ABI): XF_NONE on rows whose size is
+// a multiple of 16 bytes, moved in 16-byte units, so a wavefront's load or
+// store covers 1 KiB instead of 256 bytes.
+constexpr int kXfCopy16 = 16;
+
+// the unit an item is made of: 4 bytes, or 16 for kXfCopy16
+template <int XF> struct UnitOf {
+    typedef uint32_t T;
+    static constexpr int kShift = 2;
+};
+template <> struct UnitOf<kXfCopy16> {
+    typedef u32x4 T;
+    static constexpr int kShift = 4;
+};
 
 #pragma clang fp contract(off)
 __device__ __forceinline__ float u8_unit_f32(uint32_t x) {
@@ -99,7 +115,8 @@ __device__ __forceinline__ void build_lut(const GatherArgs& a, uint16_t* lut, in
     }
 }
 
-// One work item = (row b, frame k, part) = up to kUnitsPerBlock 4-byte units.
+// One work item = (row b, frame k, part) = up to kUnitsPerBlock units of 4
+// bytes (16 for kXfCopy16).
 struct Item {
     int64_t b;   // output row
     int k;       // frame within the stack (0 = oldest)
@@ -125,10 +142,13 @@ __device__ __forceinline__ Item decode(const GatherArgs& a, int64_t it, int bpf,
 
 // issue every load of an item: payload units (clamped, so all are unconditional)
 // and, for stacked frames, the episode/step of the sampled and the source slot
-__device__ __forceinline__ void issue(const GatherArgs& a, const Item& t, int64_t i, uint32_t (&v)[kUnroll],
-                                      int32_t& si, int32_t& sj, uint32_t& ei, uint32_t& ej) {
-    const int64_t units = a.row_bytes >> 2;
-    const uint32_t* __restrict__ src = reinterpret_cast<const uint32_t*>(a.src + t.j * a.row_bytes);
+template <int XF>
+__device__ __forceinline__ void issue(const GatherArgs& a, const Item& t, int64_t i,
+                                      typename UnitOf<XF>::T (&v)[kUnroll], int32_t& si, int32_t& sj, uint32_t& ei,
+                                      uint32_t& ej) {
+    typedef typename UnitOf<XF>::T U;
+    const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
+    const U* __restrict__ src = reinterpret_cast<const U*>(a.src + t.j * a.row_bytes);
     const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + threadIdx.x;
 #pragma unroll
     for (int r = 0; r < kUnroll; ++r) {
@@ -145,9 +165,9 @@ __device__ __forceinline__ void issue(const GatherArgs& a, const Item& t, int64_
 }
 
 template <int XF, bool NT, bool PIN>
-__device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const uint32_t (&v)[kUnroll], int32_t si,
-                                       int32_t sj, uint32_t ei, uint32_t ej, const uint16_t* lut) {
-    const int64_t units = a.row_bytes >> 2;
+__device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const typename UnitOf<XF>::T (&v)[kUnroll],
+                                       int32_t si, int32_t sj, uint32_t ei, uint32_t ej, const uint16_t* lut) {
+    const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
     const bool valid = t.d == 0 ? t.ok : (t.ok & (t.d <= si) & (ei == ej) & (sj == si - t.d));
     const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + threadIdx.x;
     const int64_t out_unit0 = (t.b * a.stack + t.k) * units;
@@ -160,7 +180,22 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
     // one-item-per-workgroup kernel needs the pin (353 -> 328 us per PPO
     // minibatch); the double-buffered kernels are faster without it (14.9 vs
     // 15.3 us per DQN batch), where waiting per load lets stores start sooner.
-    if constexpr (XF == CONDUIT_XF_NONE) {
+    if constexpr (XF == kXfCopy16) {
+        u32x4 o[kUnroll];
+#pragma unroll
+        for (int r = 0; r < kUnroll; ++r) {
+            o[r] = valid ? v[r] : (u32x4)(0u);
+            if constexpr (PIN) asm volatile("" : "+v"(o[r]));
+        }
+#pragma unroll
+        for (int r = 0; r < kUnroll; ++r) {
+            const int64_t u = u0 + (int64_t)r * kThreads;
+            u32x4* p = reinterpret_cast<u32x4*>(a.out) + out_unit0 + u;
+            if (u < units) {
+                if constexpr (NT) __builtin_nontemporal_store(o[r], p); else *p = o[r];
+            }
+        }
+    } else if constexpr (XF == CONDUIT_XF_NONE) {
         uint32_t o[kUnroll];
 #pragma unroll
         for (int r = 0; r < kUnroll; ++r) {

@@ -47,10 +47,10 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
     const int64_t i = a.idx[it / ((int64_t)bpf * a.stack)];
     const Item t = decode(a, it, bpf, i);
     if (!t.ok && threadIdx.x == 0 && t.part == 0 && t.k == a.stack - 1) flag_error(a.err, a.err_kind);
-    uint32_t v[kUnroll];
+    typename UnitOf<XF>::T v[kUnroll];
     int32_t si = 0, sj = 0;
     uint32_t ei = 0, ej = 0;
-    issue(a, t, i, v, si, sj, ei, ej);
+    issue<XF>(a, t, i, v, si, sj, ei, ej);
     finish<XF, NT, true>(a, t, v, si, sj, ei, ej, lut);
 }
 
@@ -75,15 +75,15 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
     const int64_t i0 = a.idx[it / per_row];
     int64_t itn = it + G;
     int64_t i1 = a.idx[clampi(itn) / per_row];
-    uint32_t va[kUnroll], vb[kUnroll];
+    typename UnitOf<XF>::T va[kUnroll], vb[kUnroll];
     int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
     uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
     Item ta = decode(a, it, bpf, i0), tb;
     if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_error(a.err, a.err_kind);
-    issue(a, ta, i0, va, sia, sja, eia, eja);
+    issue<XF>(a, ta, i0, va, sia, sja, eia, eja);
     while (true) {
         tb = decode(a, clampi(itn), bpf, i1);
-        issue(a, tb, i1, vb, sib, sjb, eib, ejb);
+        issue<XF>(a, tb, i1, vb, sib, sjb, eib, ejb);
         int64_t itnn = itn + G;
         int64_t i2 = a.idx[clampi(itnn) / per_row];
         finish<XF, NT, false>(a, ta, va, sia, sja, eia, eja, lut);
@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
         itn = itnn;
         i1 = i2;
         ta = decode(a, clampi(itn), bpf, i1);
-        issue(a, ta, i1, va, sia, sja, eia, eja);
+        issue<XF>(a, ta, i1, va, sia, sja, eia, eja);
         itnn = itn + G;
         i2 = a.idx[clampi(itnn) / per_row];
         finish<XF, NT, false>(a, tb, vb, sib, sjb, eib, ejb, lut);
@@ -194,8 +194,13 @@ int device_cus() {
 // kernels and beat plain stores, even when the batch would fit the 256 MB
 // Infinity Cache.
 template <int XF>
-void launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t bpf, int64_t n_items, int64_t tail_blocks) {
-    const int64_t out_bytes = n_items * kUnitsPerBlock * 4 * (XF == CONDUIT_XF_U8_F32 ? 4 : XF == CONDUIT_XF_U8_BF16_NORM ? 2 : 1);
+hipError_t launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t tail_blocks) {
+    const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
+    const int64_t bpf = a.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
+    const int64_t n_items = a.n * a.stack * bpf;
+    if (n_items + tail_blocks == 0) return hipSuccess;
+    const int64_t out_bytes = a.n * a.stack * a.row_bytes *
+                              (XF == CONDUIT_XF_U8_F32 ? 4 : XF == CONDUIT_XF_U8_BF16_NORM ? 2 : 1);
     if (out_bytes <= kPipeMaxOutBytes) {
         // small batches: persistent pipelined workgroups
         const int64_t frame_grid = n_items < 4LL * device_cus() ? n_items : 4LL * device_cus();
@@ -206,24 +211,26 @@ void launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t bpf, int64_t n
         hipLaunchKernelGGL((k_gather_rows<XF, true>), dim3((unsigned)(n_items + tail_blocks)), dim3(kThreads), 0, s,
                            a, (int32_t)bpf, n_items, (int32_t)tail_blocks);
     }
+    return hipGetLastError();
+}
+
+bool copy16(const GatherArgs& a) {
+    return a.xform == CONDUIT_XF_NONE &&
+           ((reinterpret_cast<uintptr_t>(a.src) | reinterpret_cast<uintptr_t>(a.out) | (uintptr_t)a.row_bytes) & 15) == 0;
 }
 
 hipError_t launch_gather(const GatherArgs& a, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;
-    const int64_t units = a.row_bytes >> 2;
-    const int64_t bpf = a.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
-    const int64_t n_items = a.n * a.stack * bpf;
     const bool scalars = a.out_action || a.out_reward || a.out_done || a.ncols > 0;
     // scalar-column workgroups and the weights workgroup, at the head of the grid
     const int64_t tail_blocks = (scalars ? (a.n + kThreads - 1) / kThreads : 0) + (a.weights.w ? 1 : 0);
-    if (n_items + tail_blocks == 0) return hipSuccess;
+    if (copy16(a)) return launch_gather_xf<kXfCopy16>(a, s, tail_blocks);
     switch (a.xform) {
-        case CONDUIT_XF_NONE: launch_gather_xf<CONDUIT_XF_NONE>(a, s, bpf, n_items, tail_blocks); break;
-        case CONDUIT_XF_U8_F32: launch_gather_xf<CONDUIT_XF_U8_F32>(a, s, bpf, n_items, tail_blocks); break;
-        case CONDUIT_XF_U8_BF16_NORM: launch_gather_xf<CONDUIT_XF_U8_BF16_NORM>(a, s, bpf, n_items, tail_blocks); break;
+        case CONDUIT_XF_NONE: return launch_gather_xf<CONDUIT_XF_NONE>(a, s, tail_blocks);
+        case CONDUIT_XF_U8_F32: return launch_gather_xf<CONDUIT_XF_U8_F32>(a, s, tail_blocks);
+        case CONDUIT_XF_U8_BF16_NORM: return launch_gather_xf<CONDUIT_XF_U8_BF16_NORM>(a, s, tail_blocks);
         default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s) {

@@ -124,23 +124,23 @@ __global__ __launch_bounds__(kThreads) void k_sample_gather(SampleArgs sa, Gathe
         if (owner) row_scalars(a, b, i);
         return;
     }
-    uint32_t va[kUnroll], vb[kUnroll];
+    typename UnitOf<XF>::T va[kUnroll], vb[kUnroll];
     int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
     uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
     Item ta = decode(a, it0, bpf, i), tb;
-    issue(a, ta, i, va, sia, sja, eia, eja);
+    issue<XF>(a, ta, i, va, sia, sja, eia, eja);
     if (owner) row_scalars(a, b, i);
     for (int64_t it = it0; it < it_end; it += 2) {
         const bool has_b = it + 1 < it_end;  // uniform
         if (has_b) {
             tb = decode(a, it + 1, bpf, i);
-            issue(a, tb, i, vb, sib, sjb, eib, ejb);
+            issue<XF>(a, tb, i, vb, sib, sjb, eib, ejb);
         }
         finish<XF, true, false>(a, ta, va, sia, sja, eia, eja, lut);
         if (!has_b) break;
         if (it + 2 < it_end) {
             ta = decode(a, it + 2, bpf, i);
-            issue(a, ta, i, va, sia, sja, eia, eja);
+            issue<XF>(a, ta, i, va, sia, sja, eia, eja);
         }
         finish<XF, true, false>(a, tb, vb, sib, sjb, eib, ejb, lut);
     }
@@ -167,13 +167,15 @@ hipError_t launch_xf(const SampleArgs& sa, const GatherArgs& ga, hipStream_t s, 
 }  // namespace
 
 hipError_t launch_sample_gather(const SampleArgs& sa, const GatherArgs& ga, hipStream_t s) {
-    const int64_t units = ga.row_bytes >> 2;
+    const bool c16 = copy16(ga);
+    const int64_t units = ga.row_bytes >> (c16 ? 4 : 2);
     const int64_t bpf = ga.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
     const int64_t per_row = bpf * ga.stack;
     if (sa.batch <= 0 || ga.ncols != 0 || per_row > kFusedMaxItemsPerRow) return hipErrorNotSupported;
     const int64_t wgs = per_row > 2 ? (per_row + 1) / 2 : 1;  // two items per workgroup
     const DivB dv = make_divb((uint64_t)sa.batch);
     const int pre = descend_prefetch(sa.tree);
+    if (c16) return launch_xf<kXfCopy16>(sa, ga, s, bpf, wgs, dv, pre);
     switch (ga.xform) {
         case CONDUIT_XF_NONE: return launch_xf<CONDUIT_XF_NONE>(sa, ga, s, bpf, wgs, dv, pre);
         case CONDUIT_XF_U8_F32: return launch_xf<CONDUIT_XF_U8_F32>(sa, ga, s, bpf, wgs, dv, pre);

@@ -16,6 +16,8 @@ Workloads (stand-ins for the paper's environments, which are not available):
   2 ppo     -- on-policy rollout 2048 steps x 256 envs of 3x84x84 frames
   3 large   -- 3x224x224 visual payloads, 200k-transition replay (~30 GB)
   4 tokens  -- variable-length token sequences (LLM post-training shape)
+  5 stress  -- fp32 transitions of dimension d (obs and next_obs, d values each),
+               the paper's synthetic stress test, 1M-transition replay
 Seeds: data 1000 + c, draws (uniforms, permutations, update priorities) 1500 + c.
 """
 import numpy as np
@@ -370,4 +372,52 @@ class Tokens:
     def draws(self, iters, batch=None, seed=None):
         batch = self.batch if batch is None else batch
         rng = np.random.default_rng(draw_seed(4) if seed is None else seed)
+        return uniforms(rng, iters, batch), quantise_priority(rng.lognormal(0.0, 1.0, (iters, batch)))
+
+
+# ----------------------------------------------------------------------------
+# 5: synthetic stress transitions of dimension d
+# ----------------------------------------------------------------------------
+class Stress:
+    """Transitions of dimension d: obs and next_obs, d fp32 values each, stored as
+    one [2, d] row per slot (8d bytes).  Values are exact fp32 numbers in [-1, 1)
+    from an integer hash of (seed, stream position, element): k / 2^23 for a
+    hashed integer k in [-2^23, 2^23).  next_obs of position j is obs of
+    position j + 1 (one endless episode).  action int32 U{0..3}, reward N(0,1),
+    priorities lognormal(0,1) quantised; batch 512, capacity 10^6."""
+
+    capacity = 1_000_000
+    batch = 512
+
+    def __init__(self, d, n, seed=None):
+        self.seed = data_seed(5) if seed is None else seed
+        self.d = d
+        self.obs_shape = (2, d)
+        rng = np.random.default_rng(self.seed)
+        self.n = n
+        self.action = rng.integers(0, 4, n).astype(np.int32)
+        self.reward = rng.standard_normal(n).astype(np.float32)
+        self.done = np.zeros(n, np.uint8)
+        self.prio = quantise_priority(rng.lognormal(0.0, 1.0, n))
+
+    def _obs(self, pos, dev):
+        k = torch.arange(self.d, dtype=torch.int64, device=dev)[None, :]
+        h = hash32(self.seed, 13, pos[:, None], k)
+        return ((h >> 8) - (1 << 23)).to(torch.float32) * (2.0 ** -23)
+
+    def rows(self, start, count, device="cpu"):
+        """fp32 [count, 2, d] transitions of stream positions [start, start+count)."""
+        dev = torch.device(device)
+        pos = torch.arange(start, start + count + 1, dtype=torch.int64, device=dev)
+        o = self._obs(pos, dev)
+        return torch.stack([o[:-1], o[1:]], dim=1)
+
+    def rows_at(self, positions, device="cpu"):
+        dev = torch.device(device)
+        pos = torch.as_tensor(np.asarray(positions, np.int64), device=dev)
+        return torch.stack([self._obs(pos, dev), self._obs(pos + 1, dev)], dim=1)
+
+    def draws(self, iters, batch=None, seed=None):
+        batch = self.batch if batch is None else batch
+        rng = np.random.default_rng(draw_seed(5) if seed is None else seed)
         return uniforms(rng, iters, batch), quantise_priority(rng.lognormal(0.0, 1.0, (iters, batch)))

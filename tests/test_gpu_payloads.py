@@ -149,3 +149,62 @@ def test_tokens_full_size():
     print("tokens: cap 65536 x 4096, batch 256, 2 iterations", flush=True)
     run_tokens(cap=65536, max_len=4096, min_len=512, prefill=65536, iters=2, batch=256, chunk=4096,
                with_values=False)
+
+
+def run_stress(cap, d, prefill, iters, batch, chunk, check_rows):
+    """Synthetic stress transitions (obs and next_obs, d fp32 each) through
+    ingest, the one-call sample + gather and update; indices and weights against
+    the oracle, gathered rows against the rows the stream holds at the sampled
+    slots (no transform: the gather is the stored row)."""
+    cfg = synth.Stress(d, prefill + iters * batch)
+    u, prio = cfg.draws(iters, batch)
+    buf = cd.ReplayBuffer(cap, cfg.obs_shape, torch.float32, action_bytes=4)
+    orc = oracle.Replay(cap, cfg.obs_shape, np.float32, act_bytes=4, keep_obs=False)
+
+    def ingest(a, b):
+        buf.ingest(cfg.rows(a, b - a, "cuda"), action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]),
+                   done=dev(cfg.done[a:b]), prio=dev(cfg.prio[a:b]))
+        orc.ingest(b - a, obs=None, action=cfg.action[a:b], reward=cfg.reward[a:b], done=cfg.done[a:b],
+                   prio=cfg.prio[a:b])
+
+    for a in range(0, prefill, chunk):
+        ingest(a, min(prefill, a + chunk))
+    pos = prefill
+    xf = cd.transform(cd.XF_NONE)
+    out = torch.empty((batch, 1) + cfg.obs_shape, dtype=torch.float32, device="cuda")
+    act = torch.empty(batch, dtype=torch.int32, device="cuda")
+    rew = torch.empty(batch, dtype=torch.float32, device="cuda")
+    for it in range(iters):
+        ingest(pos, pos + batch)
+        pos += batch
+        idx, w = buf.sample_gather(dev(u[it]), xf, obs=out, action=act, reward=rew)
+        o_idx, o_w = orc.sample(u[it])
+        assert np.array_equal(host(idx), o_idx), it
+        assert_weights_close(host(w), o_w)
+        sel = check_rows
+        want = cfg.rows_at(orc.position[o_idx[sel]]).numpy()
+        got = host(out[torch.as_tensor(sel, device="cuda")]).reshape(want.shape)
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), it
+        _, o_act, o_rew, _ = orc.gather(o_idx)
+        assert np.array_equal(host(act).view(np.uint8).reshape(batch, 4), o_act), it
+        assert np.array_equal(host(rew), o_rew), it
+        buf.update(idx, dev(prio[it]))
+        orc.update(o_idx, prio[it])
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    assert np.array_equal(read_col(buf, cd.COL_LEAVES, cap * 4, np.uint32), orc.leaf)
+    assert tree_consistent(buf, cap) == orc.total_priority()
+    buf.close()
+
+
+@pytest.mark.parametrize("d", [128, 1000, 5000, 12000])
+def test_stress_transitions_reduced(d):
+    print(f"stress: d={d}, cap 3000, prefill 3500 (wraps), batch 512", flush=True)
+    run_stress(cap=3000, d=d, prefill=3500, iters=3, batch=512, chunk=1000, check_rows=np.arange(512))
+
+
+@pytest.mark.slow
+def test_stress_transitions_full_size():
+    print("stress: d=20000, cap 10^6 (160 GB), batch 512, 2 iterations", flush=True)
+    torch.cuda.empty_cache()  # the 160 GB arena is the library's own allocation
+    run_stress(cap=1_000_000, d=20000, prefill=1_000_000, iters=2, batch=512, chunk=4096,
+               check_rows=np.random.default_rng(0).choice(512, 24, replace=False))
