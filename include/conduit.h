@@ -395,6 +395,60 @@ const char* conduit_last_error(void);
 /* Library version string. */
 const char* conduit_version(void);
 
+/* ---------------------------------------------------------------------------
+ * Latency-aware scheduling of ingestion and delivery (Sec. 6: timing
+ * `overlap` and granularity `g` of the two operators; iteration-latency model
+ * of Sec. 6.2 with the hidden-latency terms of App. E; cost-based choice of
+ * Eq. (sched_opt), Sec. 6.3).  Host-only, no device work.
+ * ------------------------------------------------------------------------- */
+/*
+ * Profiled costs of one RL configuration, all in the same time unit:
+ *   t_rollout, t_update    one actor rollout / one learner update;
+ *   t_sync_ing, t_sync_del the synchronisation an overlapped operator adds;
+ *   g_ing[n_ing], t_ing[n_ing]  candidate ingestion granularities (rollout
+ *                          units per invocation; > 0, fractions allowed for
+ *                          on-policy pipelining) and the wall time of one
+ *                          invocation at each;
+ *   g_del[n_del], t_del[n_del]  the same for delivery (training batches per
+ *                          invocation).
+ * All arrays are host memory owned by the caller.
+ */
+typedef struct conduit_sched_costs {
+    double t_rollout, t_update;
+    double t_sync_ing, t_sync_del;
+    int32_t n_ing, n_del;
+    const double* g_ing;
+    const double* t_ing;
+    const double* g_del;
+    const double* t_del;
+} conduit_sched_costs;
+
+/* One execution mode and its modelled latencies. */
+typedef struct conduit_sched_mode {
+    int32_t overlap_ing, overlap_del;  /* 0 = sequential, 1 = overlapped */
+    int32_t i_ing, i_del;              /* indices into g_ing / g_del */
+    double g_ing, g_del;
+    double t_ing_path, t_del_path, t_iter;
+} conduit_sched_mode;
+
+/*
+ * Scores every mode -- overlap_ing, overlap_del in {0,1} and every candidate
+ * granularity pair -- with
+ *   Tbar(g)    = T(g) / g                                (per-unit cost)
+ *   gamma(g)   = 1 if g >= 1, else 1 - g
+ *   hide_ing   = gamma(g_ing) * min(t_rollout, Tbar_ing(g_ing))
+ *   T_ing_path = t_rollout + Tbar_ing(g_ing) + overlap_ing * (t_sync_ing - hide_ing)
+ * (delivery alike with t_update), T_iter = T_ing_path + T_del_path, and
+ * returns the mode of least T_iter in *best.  Modes are scored in the order
+ * overlap_ing, overlap_del, i_ing, i_del (each ascending, the last fastest);
+ * the first of equal minima wins.  If `all` is not NULL it receives every
+ * mode in that order (4 * n_ing * n_del entries, caller-owned).
+ * Errors: EINVAL (NULL costs/best, n_ing or n_del < 1, NULL arrays, a
+ * granularity <= 0, a negative or non-finite time).
+ */
+conduit_status conduit_schedule(const conduit_sched_costs* costs, conduit_sched_mode* best,
+                                conduit_sched_mode* all);
+
 #ifdef __cplusplus
 }
 #endif

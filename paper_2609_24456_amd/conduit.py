@@ -54,6 +54,22 @@ class LearnerBatch(C.Structure):
                 ("mask", C.c_void_p), ("aux", C.c_void_p), ("length", C.c_void_p)]
 
 
+class SchedCosts(C.Structure):
+    _fields_ = [("t_rollout", C.c_double), ("t_update", C.c_double), ("t_sync_ing", C.c_double),
+                ("t_sync_del", C.c_double), ("n_ing", C.c_int32), ("n_del", C.c_int32),
+                ("g_ing", C.POINTER(C.c_double)), ("t_ing", C.POINTER(C.c_double)),
+                ("g_del", C.POINTER(C.c_double)), ("t_del", C.POINTER(C.c_double))]
+
+
+class SchedMode(C.Structure):
+    _fields_ = [("overlap_ing", C.c_int32), ("overlap_del", C.c_int32), ("i_ing", C.c_int32), ("i_del", C.c_int32),
+                ("g_ing", C.c_double), ("g_del", C.c_double), ("t_ing_path", C.c_double),
+                ("t_del_path", C.c_double), ("t_iter", C.c_double)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
 class BufferInfo(C.Structure):
     _fields_ = [("capacity", C.c_int64), ("row_bytes", C.c_int64), ("head", C.c_int64), ("size", C.c_int64),
                 ("total", C.c_int64), ("tree_depth", C.c_int32), ("tree_nodes", C.c_int64 * 8),
@@ -85,6 +101,7 @@ SIGNATURES = {
     "conduit_clear_error": (None, [P]),
     "conduit_last_error": (C.c_char_p, []),
     "conduit_version": (C.c_char_p, []),
+    "conduit_schedule": (ST, [P, P, P]),
 }
 
 
@@ -255,6 +272,19 @@ def conduit_gae_packed(last_reward, lengths, values, Lmax, gamma, lam, adv, ret,
                                     _ptr(lengths, torch.int32, "lengths"), _ptr(values, torch.float32, "values"), B,
                                     int(Lmax), float(gamma), float(lam), _ptr(adv, torch.float32, "adv"),
                                     _ptr(ret, torch.float32, "ret"), _stream(stream)))
+
+
+def conduit_schedule(t_rollout, t_update, g_ing, t_ing, g_del, t_del, t_sync_ing=0.0, t_sync_del=0.0):
+    """Sec. 6 cost model: (best mode, every mode) as dicts."""
+    arr = lambda xs: (C.c_double * max(1, len(xs)))(*[float(x) for x in xs])  # noqa: E731
+    gi, ti, gd, td = arr(g_ing), arr(t_ing), arr(g_del), arr(t_del)
+    c = SchedCosts(float(t_rollout), float(t_update), float(t_sync_ing), float(t_sync_del), len(g_ing), len(g_del),
+                   gi, ti, gd, td)
+    best = SchedMode()
+    n = 4 * max(1, len(g_ing)) * max(1, len(g_del))
+    all_ = (SchedMode * n)()
+    _check(lib().conduit_schedule(C.byref(c), C.byref(best), all_))
+    return best.as_dict(), [m.as_dict() for m in all_]
 
 
 def conduit_minibatch_gather(src, row_bytes, n_src, perm, xf, out, cols=(), cols_out=(), stream=None):

@@ -19,6 +19,13 @@ conduit_status fail(conduit_status s, const std::string& msg) {
     return s;
 }
 
+}  // namespace
+
+// the error reporting of the other host sources (common.h)
+conduit_status conduit::report_error(conduit_status s, const char* msg) { return fail(s, msg); }
+
+namespace {
+
 conduit_status hip_fail(hipError_t e, const char* what) {
     return fail(CONDUIT_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }

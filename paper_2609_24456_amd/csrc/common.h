@@ -353,6 +353,9 @@ struct GatherArgs {
     WeightsArgs weights;
 };
 
+// record `msg` as the calling thread's last error and return `s`
+conduit_status report_error(conduit_status s, const char* msg);
+
 // compute units of the current device (cached per device)
 int device_cus();
 // whether a gather moves its rows in 16-byte units (no transform, 16-byte

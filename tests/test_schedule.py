@@ -1,0 +1,129 @@
+"""Scheduling cost model (Sec. 6.2, App. E, Eq. sched_opt): the oracle pinned by
+closed-form cases the text fixes, and the library's conduit_schedule against the
+oracle on random cost sets.  Host-only: no GPU needed."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import schedule as osch
+from paper_2609_24456_amd import conduit as cd
+
+
+# ----------------------------------------------------------------------------
+# pins of the oracle
+# ----------------------------------------------------------------------------
+def test_sequential_mode_is_stage_plus_amortised_cost():
+    # no overlap: nothing is hidden and no synchronisation is paid; an
+    # invocation of g units costing a + b g is a/g + b per unit
+    a, b = 30.0, 2.0
+    gs = [1, 2, 4, 8]
+    ts = [a + b * g for g in gs]
+    ms = osch.modes(100.0, 200.0, gs, ts, [1], [50.0], 1e9, 1e9)
+    seq = [m for m in ms if m["overlap_ing"] == 0 and m["overlap_del"] == 0]
+    for m in seq:
+        assert m["t_iter"] == pytest.approx(100.0 + a / m["g_ing"] + b + 200.0 + 50.0)
+    # larger g amortises the fixed cost: the largest g is the best sequential one
+    assert min(seq, key=lambda m: m["t_iter"])["g_ing"] == 8
+
+
+def test_overlap_hides_an_operator_shorter_than_its_stage():
+    # zero synchronisation, per-unit cost below the neighbouring stage: fully hidden
+    ms = osch.modes(100.0, 200.0, [1, 2], [60.0, 80.0], [1, 4], [150.0, 400.0], 0.0, 0.0)
+    for m in ms:
+        if m["overlap_ing"]:
+            assert m["t_ing_path"] == pytest.approx(100.0)
+        if m["overlap_del"]:
+            assert m["t_del_path"] == pytest.approx(200.0)
+
+
+def test_overlap_of_a_longer_operator_exposes_it_plus_sync():
+    # per-unit cost above the stage: the stage is what gets hidden
+    ms = osch.modes(10.0, 20.0, [1], [70.0], [1], [90.0], 3.0, 4.0)
+    m = next(m for m in ms if m["overlap_ing"] and m["overlap_del"])
+    assert m["t_ing_path"] == pytest.approx(70.0 + 3.0)
+    assert m["t_del_path"] == pytest.approx(90.0 + 4.0)
+
+
+@pytest.mark.parametrize("M", [2, 4, 8])
+def test_fractional_pipelining_hides_only_the_unexposed_fraction(M):
+    # on-policy g = 1/M: T(g) is the cost of one mini-batch slice, so the per-unit
+    # cost is M T(1/M); overlap hides (1 - 1/M) of min(stage, per-unit cost)
+    g = 1.0 / M
+    slice_cost = 5.0
+    ms = osch.modes(100.0, 1.0, [g], [slice_cost], [1], [0.0], 0.0, 0.0)
+    ov = next(m for m in ms if m["overlap_ing"] == 1 and m["overlap_del"] == 0)
+    per_unit = M * slice_cost
+    assert ov["t_ing_path"] == pytest.approx(100.0 + per_unit - (1 - g) * min(100.0, per_unit))
+    assert ov["t_ing_path"] == pytest.approx(100.0 + per_unit / M)  # here per_unit < stage
+
+
+def test_expensive_synchronisation_turns_overlap_off():
+    k, ms = osch.best(100.0, 200.0, [1], [50.0], [1], [50.0], 1000.0, 1000.0)
+    assert ms[k]["overlap_ing"] == 0 and ms[k]["overlap_del"] == 0
+    k, ms = osch.best(100.0, 200.0, [1], [50.0], [1], [50.0], 1.0, 1.0)
+    assert ms[k]["overlap_ing"] == 1 and ms[k]["overlap_del"] == 1
+
+
+def test_superlinear_invocation_cost_gives_an_interior_granularity():
+    # the paper's large-transition case: beyond some g, managing the chunk costs
+    # more than the amortisation saves, so the optimum moves back to a middle g
+    gs = [1, 2, 4, 8, 16]
+    ts = [40.0 + 5.0 * g + 1.2 * g * g for g in gs]  # per unit 40/g + 5 + 1.2 g, least at g ~ 5.8
+    k, ms = osch.best(500.0, 500.0, gs, ts, [1], [10.0], 1e9, 1e9)
+    assert ms[k]["g_ing"] in (4, 8) and ms[k]["g_ing"] not in (1, 16)
+    per = [t / g for g, t in zip(gs, ts)]
+    assert ms[k]["g_ing"] == gs[int(np.argmin(per))]
+
+
+def test_mode_count_order_and_ties():
+    ms = osch.modes(1.0, 1.0, [1, 2, 3], [0.0, 0.0, 0.0], [1, 2], [0.0, 0.0], 0.0, 0.0)
+    assert len(ms) == 4 * 3 * 2
+    assert [(m["overlap_ing"], m["overlap_del"], m["i_ing"], m["i_del"]) for m in ms[:7]] == \
+        [(0, 0, 0, 0), (0, 0, 0, 1), (0, 0, 1, 0), (0, 0, 1, 1), (0, 0, 2, 0), (0, 0, 2, 1), (0, 1, 0, 0)]
+    k, _ = osch.best(1.0, 1.0, [1, 2, 3], [0.0, 0.0, 0.0], [1, 2], [0.0, 0.0], 0.0, 0.0)
+    assert k == 0  # every mode costs 2.0: the first wins
+
+
+# ----------------------------------------------------------------------------
+# the library against the oracle
+# ----------------------------------------------------------------------------
+def _random_case(rng):
+    n_i, n_d = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+    frac = rng.random() < 0.3
+    g_i = sorted(set(rng.choice([0.125, 0.25, 0.5, 1, 2, 3, 4, 8, 16], n_i).tolist())) if frac else \
+        sorted(set(rng.integers(1, 17, n_i).tolist()))
+    g_d = sorted(set(rng.integers(1, 9, n_d).tolist()))
+    t_i = (rng.random(len(g_i)) * 400).tolist()
+    t_d = (rng.random(len(g_d)) * 400).tolist()
+    return (float(rng.random() * 500), float(rng.random() * 500), g_i, t_i, g_d, t_d,
+            float(rng.random() * 50), float(rng.random() * 50))
+
+
+def test_library_matches_oracle_on_random_cost_sets():
+    rng = np.random.default_rng(17)
+    for _ in range(2000):
+        case = _random_case(rng)
+        k, oms = osch.best(*case)
+        best, lms = cd.conduit_schedule(*case)
+        assert len(lms) == len(oms)
+        for lm, om in zip(lms, oms):
+            for f in ("overlap_ing", "overlap_del", "i_ing", "i_del"):
+                assert lm[f] == om[f]
+            for f in ("t_ing_path", "t_del_path", "t_iter"):
+                assert lm[f] == pytest.approx(om[f], rel=1e-12, abs=1e-9)
+        ob = oms[k]
+        assert (best["overlap_ing"], best["overlap_del"], best["i_ing"], best["i_del"]) == \
+            (ob["overlap_ing"], ob["overlap_del"], ob["i_ing"], ob["i_del"])
+
+
+@pytest.mark.parametrize("bad", [
+    dict(g_ing=[], t_ing=[]), dict(g_ing=[0.0], t_ing=[1.0]), dict(g_ing=[-1.0], t_ing=[1.0]),
+    dict(t_ing=[-1.0]), dict(t_ing=[math.nan]), dict(t_rollout=math.inf), dict(t_sync_del=-0.5)])
+def test_schedule_rejects_bad_costs(bad):
+    args = dict(t_rollout=1.0, t_update=1.0, g_ing=[1.0], t_ing=[1.0], g_del=[1.0], t_del=[1.0],
+                t_sync_ing=0.0, t_sync_del=0.0)
+    args.update(bad)
+    with pytest.raises(cd.ConduitError) as e:
+        cd.conduit_schedule(**args)
+    assert e.value.status == cd.EINVAL
