@@ -37,7 +37,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-rows", action="store_true", help="only the headline DQN workload")
-    p.add_argument("--only", default="", help="comma list of extra rows to run (ppo,large,tokens,tiny,stress)")
+    p.add_argument("--only", default="", help="comma list of extra rows to run (ppo,large,tokens,tiny,stress,schedule)")
     p.add_argument("--calibrate-copy", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
     p.add_argument("--sources-sha", action="store_true",
                    help="print the hash of the fused kernel's sources (for the counter summary)")
@@ -555,6 +555,129 @@ def bench_stress(dims=(128, 1000, 5000, 10000, 20000), iters=20):
     return res
 
 
+def bench_schedule(d=10000, t_stage_us=(100.0, 150.0), iters=64, gs=(1, 2, 4, 8)):
+    """Latency-aware scheduling on one GPU (the paper's Sec. 6 knobs): the
+    native off-policy loop (conduit_run_offpolicy) on the synthetic stress
+    workload (dimension d, 10^6 slots, rollout units and learner batches of
+    512) with the library's compute stand-in for the actor's rollout and the
+    learner's update.  The model's inputs are profiled (stage times, one
+    invocation of each operator at each granularity, one cross-stream
+    dependency), conduit_schedule scores every mode, and every mode is then
+    run and timed.  Reports model-predicted vs measured iteration latency per
+    mode, the model's choice against the measured best, and the rank
+    correlation of prediction and measurement."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    Cap, U, B = 1_000_000, 512, 512
+    torch.cuda.empty_cache()
+    cfg = synth.Stress(d, Cap + iters * U)
+    buf = cd.ReplayBuffer(Cap, cfg.obs_shape, torch.float32, action_bytes=4)
+    act_d, rew_d, done_d, prio_d = _dev(cfg.action), _dev(cfg.reward), _dev(cfg.done), _dev(cfg.prio)
+    chunk = max(512, min(65536, (1 << 30) // (8 * d)))
+    for a in range(0, Cap, chunk):
+        b = min(Cap, a + chunk)
+        buf.ingest(cfg.rows(a, b - a, "cuda"), action=act_d[a:b], reward=rew_d[a:b], done=done_d[a:b],
+                   prio=prio_d[a:b])
+    rows = cfg.rows(Cap, iters * U, "cuda")
+    rng = np.random.default_rng(5)
+    u_d = _dev(synth.uniforms(rng, iters * B))
+    p_d = _dev(synth.quantise_priority(rng.lognormal(0, 1, iters * B)))
+    idx = torch.empty(iters * B, dtype=torch.int64, device="cuda")
+    w = torch.empty(iters * B, dtype=torch.float32, device="cuda")
+    out = torch.empty((iters * B, 1) + cfg.obs_shape, dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_NONE)
+    h = C.c_void_p(buf.handle)
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+    def loop_struct(mode, work):
+        lp = cd.OffpolicyLoop()
+        lp.overlap_ing, lp.g_ing, lp.overlap_del, lp.g_del = mode
+        lp.iters, lp.unit, lp.batch = iters, U, B
+        lp.rollout_work, lp.update_work = work
+        lp.rollout.obs, lp.rollout.action = rows.data_ptr(), act_d[Cap:].data_ptr()
+        lp.rollout.reward, lp.rollout.done, lp.rollout.prio = (rew_d[Cap:].data_ptr(), done_d[Cap:].data_ptr(),
+                                                               prio_d[Cap:].data_ptr())
+        lp.uniforms, lp.new_prio = u_d.data_ptr(), p_d.data_ptr()
+        lp.idx_out, lp.is_w_out = idx.data_ptr(), w.data_ptr()
+        lp.xf = C.pointer(xf)
+        lp.out.obs = out.data_ptr()
+        return lp
+
+    # the stand-in's time per unit of work, then the work for each stage
+    base = 20000
+    _b2b_ms([lambda: L.conduit_standin(base, stream)] * 5)
+    us_per_work = _b2b_ms([lambda: L.conduit_standin(base, stream)] * 20) * 1e3 / base
+    work = (int(t_stage_us[0] / us_per_work), int(t_stage_us[1] / us_per_work))
+    t_roll = _b2b_ms([lambda: L.conduit_standin(work[0], stream)] * 20) * 1e3
+    t_upd = _b2b_ms([lambda: L.conduit_standin(work[1], stream)] * 20) * 1e3
+    # operator costs at each granularity: one invocation, back to back
+    t_ing, t_del = [], []
+    for g in gs:
+        tr = cd.Transitions()
+        tr.n = g * U
+        tr.obs, tr.action = rows.data_ptr(), act_d[Cap:].data_ptr()
+        tr.reward, tr.done, tr.prio = rew_d[Cap:].data_ptr(), done_d[Cap:].data_ptr(), prio_d[Cap:].data_ptr()
+        t_ing.append(_b2b_ms([lambda tr=tr: L.conduit_ingest(h, C.byref(tr), stream)] * 10) * 1e3)
+        lb = cd.LearnerBatch()
+        lb.obs = out.data_ptr()
+
+        def one(g=g, lb=lb):
+            r = L.conduit_sample_gather(h, g * B, u_d.data_ptr(), idx.data_ptr(), w.data_ptr(), C.byref(xf),
+                                        C.byref(lb), stream)
+            for j in range(g):
+                r |= L.conduit_update_priorities(h, idx[j * B:].data_ptr(), p_d[j * B:].data_ptr(), B, stream)
+            return r
+        t_del.append(_b2b_ms([one] * 10) * 1e3)
+    comp, exp = torch.cuda.Stream(), torch.cuda.Stream()
+    t_hop, t_sync = cd.conduit_sync_cost_us(comp, exp, 200)
+    best, modes = cd.conduit_schedule(t_roll, t_upd, list(gs), t_ing, list(gs), t_del, t_sync, t_sync)
+    best_hop, _ = cd.conduit_schedule(t_roll, t_upd, list(gs), t_ing, list(gs), t_del, t_hop, t_hop)
+    # every mode, run natively and timed
+    cd.conduit_run_offpolicy(buf.handle, loop_struct((0, 1, 0, 1), work), comp, exp)  # warm-up
+    measured, host_us = [], []
+    for m in modes:
+        lp = loop_struct((m["overlap_ing"], int(m["g_ing"]), m["overlap_del"], int(m["g_del"])), work)
+        h0 = time.perf_counter()
+        ms, _ = cd.conduit_run_offpolicy(buf.handle, lp, comp, exp)
+        host_us.append((time.perf_counter() - h0) * 1e6 / iters)
+        measured.append(ms * 1e3 / iters)
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
+    pred = np.array([m["t_iter"] for m in modes])
+    meas = np.array(measured)
+    k_best = int(np.argmin(meas))
+    k_model = next(i for i, m in enumerate(modes) if all(m[f] == best[f] for f in ("overlap_ing", "overlap_del",
+                                                                                    "i_ing", "i_del")))
+    rank = lambda v: np.argsort(np.argsort(v))  # noqa: E731
+    spearman = float(np.corrcoef(rank(pred), rank(meas))[0, 1])
+    name = lambda m: f"ov_ing={m['overlap_ing']} g_ing={int(m['g_ing'])} ov_del={m['overlap_del']} g_del={int(m['g_del'])}"  # noqa: E731
+    seq = next(i for i, m in enumerate(modes) if m["overlap_ing"] == 0 and m["overlap_del"] == 0 and
+               m["g_ing"] == 1 and m["g_del"] == 1)
+    stages = t_roll + t_upd
+    return {
+        "workload": f"stress d={d}, 10^6 slots, rollout unit = batch = 512, {iters} iterations per mode; "
+                    f"register-only compute stand-in (one workgroup per CU) for rollout and update",
+        "profiled_us": {"t_rollout": t_roll, "t_update": t_upd, "t_sync": t_sync, "t_hop_unmet": t_hop,
+                        "t_ing": dict(zip(map(str, gs), t_ing)), "t_del": dict(zip(map(str, gs), t_del))},
+        "model_choice": {"mode": name(modes[k_model]), "predicted_us": float(pred[k_model]),
+                         "measured_us": float(meas[k_model])},
+        "measured_best": {"mode": name(modes[k_best]), "predicted_us": float(pred[k_best]),
+                          "measured_us": float(meas[k_best])},
+        "sequential_g1": {"predicted_us": float(pred[seq]), "measured_us": float(meas[seq])},
+        "exposed_us": {"sequential_g1": float(meas[seq] - stages), "model_choice": float(meas[k_model] - stages),
+                       "measured_best": float(meas[k_best] - stages)},
+        "model_regret": float(meas[k_model] / meas[k_best] - 1.0),
+        "model_choice_with_unmet_hop_as_t_sync": name(best_hop),
+        "spearman_pred_vs_measured": spearman,
+        "host_us_per_iteration_max": float(max(host_us)),
+        "modes": [{"mode": name(m), "predicted_us": float(p), "measured_us": float(x)}
+                  for m, p, x in zip(modes, pred, meas)],
+    }
+
+
 def bench_tiny(iters=100):
     """Tiny replay (16,384 slots of 8 fp32): 100 x [ingest 64, sample + gather 256
     with IS weights (one launch), update 256], every call's arguments prepared
@@ -705,6 +828,10 @@ def _traffic_from_profile():
     return float(rec["hbm_bytes_per_launch"])
 
 
+ROWS = {"tiny": lambda: bench_tiny(), "ppo": lambda: bench_ppo(), "large": lambda: bench_large(),
+        "tokens": lambda: bench_tokens(), "stress": lambda: bench_stress(), "schedule": lambda: bench_schedule()}
+
+
 def main():
     args = parse()
     if args.sources_sha:
@@ -720,6 +847,7 @@ def main():
     if args.calibrate_copy:
         calibrate_copy()
         return
+    print("bench.py: DQN 1M-replay step ...", file=sys.stderr, flush=True)
     d = bench_dqn(args.steps, args.warmup)
     ms_per_step = d["total_ms"] / args.steps
     value = d["B"] * args.steps / (d["total_ms"] / 1e3)
@@ -762,22 +890,14 @@ def main():
         "rows": {"dqn_ingest_32768": d["ingest_big"]},
     }
     if not args.no_rows:
-        only = set(x for x in args.only.split(",") if x) or {"ppo", "large", "tokens", "tiny", "stress"}
-        if "tiny" in only:
-            out["rows"]["tiny"] = bench_tiny()
-        if "ppo" in only:
-            out["rows"]["ppo"] = bench_ppo()
-            torch.cuda.empty_cache()
-        if "large" in only:
-            out["rows"]["large"] = bench_large()
-            torch.cuda.empty_cache()
-        if "tokens" in only:
-            out["rows"]["tokens"] = bench_tokens()
-            torch.cuda.empty_cache()
-        if "stress" in only:
-            out["rows"]["stress"] = bench_stress()
-            torch.cuda.empty_cache()
+        only = set(x for x in args.only.split(",") if x) or {"ppo", "large", "tokens", "tiny", "stress", "schedule"}
+        for name in ("tiny", "ppo", "large", "tokens", "stress", "schedule"):
+            if name in only:
+                print(f"bench.py: row {name} ...", file=sys.stderr, flush=True)
+                out["rows"][name] = ROWS[name]()
+                torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
+        print("bench.py: CPU baseline (oracle) ...", file=sys.stderr, flush=True)
         cb = cpu_baseline(args.cpu_seconds)
         out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
         out["gpu_over_cpu"] = value / cb["value"]

@@ -449,6 +449,85 @@ typedef struct conduit_sched_mode {
 conduit_status conduit_schedule(const conduit_sched_costs* costs, conduit_sched_mode* best,
                                 conduit_sched_mode* all);
 
+/*
+ * Synthetic compute that stands in for an actor rollout or a learner update in
+ * scheduling experiments: one workgroup of 256 lanes per compute unit, each
+ * lane running `work` dependent fp32 multiply-adds in registers (no memory
+ * traffic, so co-running memory-bound kernels keep their bandwidth).  Duration
+ * grows linearly with `work`.  Errors: EINVAL (work < 0).
+ */
+conduit_status conduit_standin(int64_t work, void* stream);
+
+/*
+ * Profiles the synchronisation cost of overlap (Sec. 6.2 T_sync) between two
+ * streams of one GPU, in microseconds per dependency (each >= 0):
+ *   *hop_us: a dependency the waiting stream reaches before it is met --
+ *            `hops` tiny kernels alternating between s1 and s2, each waiting
+ *            on an event recorded after the previous one, against the same
+ *            kernels on s1 alone;
+ *   *dep_us: what an overlapped operator costs the stream it overlaps -- per
+ *            tiny kernel on s1, one wait on an event of s2 (pending when
+ *            enqueued, met when s1 reaches it) plus one event recorded for
+ *            s2, against the kernels alone (both streams are held by
+ *            stand-ins while the host enqueues, so the GPU's cost is
+ *            measured, not the host's).
+ * Synchronises both streams.  Errors: EINVAL (NULL streams or outputs, hops
+ * outside [1, 1024]), EDEVICE.
+ */
+conduit_status conduit_sync_cost_us(void* s1, void* s2, int32_t hops, double* hop_us, double* dep_us);
+
+/*
+ * An off-policy iteration loop on one GPU with the experience path scheduled
+ * on its own stream (Sec. 4.1-4.2 decoupled ingestion and delivery; Sec. 6
+ * timing and granularity).  Iteration t: the actor's rollout (stand-in compute
+ * of rollout_work) produces rollout unit t; ingestion runs once g_ing units
+ * have accumulated (and after the last iteration's rollout); the learner's
+ * update (stand-in of update_work) consumes batch t, delivered by one
+ * conduit_sample_gather of g_del * batch samples per group of g_del
+ * iterations; the learner's new priorities for batch t are then applied.
+ *   overlap_ing = 0: ingestion runs inline on the compute stream right after
+ *                    the rollout that completes its group (the actor waits);
+ *                    1: it runs on the experience stream after the iteration's
+ *                    priority update, during the next rollout.
+ *   overlap_del = 0: delivery and the priority update run inline on the
+ *                    compute stream before and after the update;
+ *                    1: they run on the experience stream, the next group's
+ *                    delivery issued during the learner's update (prefetch,
+ *                    so it samples before this iteration's new priorities).
+ * Whatever the mode, the experience operators keep one fixed program order
+ * (an operator issued on the other stream than its predecessor waits for the
+ * predecessor's event), so the data produced does not depend on timing
+ * (Sec. 4.3).
+ * Device inputs: the actor's transitions for iteration t are rows
+ * [t*unit, (t+1)*unit) of the columns in `rollout` (its n is ignored);
+ * uniforms of group k are the contiguous run starting at its first
+ * iteration's t*batch; new_prio[t*batch ...] are batch t's priorities.
+ * Outputs: idx_out / is_w_out [iters*batch]; the learner-batch columns in
+ * `out` hold iters*batch rows (group k writes from row first*batch).
+ * `op_log` (host, 3 int64 per entry, NULL allowed; at most 3*iters entries)
+ * receives the experience operators in stream order: (0, first unit, units)
+ * for an ingestion, (1, group, first iteration) for a delivery,
+ * (2, iteration, 0) for a priority update; *n_ops their count.
+ * *elapsed_ms: events around the whole loop on the compute stream.
+ * Errors: EINVAL (granularities < 1, iters/unit/batch < 1, NULL required
+ * pointers, a non-prioritised buffer), plus those of the operators.
+ */
+typedef struct conduit_offpolicy_loop {
+    int32_t overlap_ing, g_ing, overlap_del, g_del;
+    int64_t iters, unit, batch;
+    int64_t rollout_work, update_work;
+    conduit_transitions rollout;
+    const uint64_t* uniforms;
+    const uint32_t* new_prio;
+    int64_t* idx_out;
+    float* is_w_out;
+    const conduit_transform* xf;
+    conduit_learner_batch out;
+} conduit_offpolicy_loop;
+
+conduit_status conduit_run_offpolicy(conduit_buffer* buf, const conduit_offpolicy_loop* loop, void* compute_stream,
+                                     void* experience_stream, double* elapsed_ms, int64_t* op_log, int64_t* n_ops);
+
 #ifdef __cplusplus
 }
 #endif

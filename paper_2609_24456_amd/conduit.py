@@ -70,6 +70,15 @@ class SchedMode(C.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class OffpolicyLoop(C.Structure):
+    _fields_ = [("overlap_ing", C.c_int32), ("g_ing", C.c_int32), ("overlap_del", C.c_int32), ("g_del", C.c_int32),
+                ("iters", C.c_int64), ("unit", C.c_int64), ("batch", C.c_int64),
+                ("rollout_work", C.c_int64), ("update_work", C.c_int64),
+                ("rollout", Transitions), ("uniforms", C.c_void_p), ("new_prio", C.c_void_p),
+                ("idx_out", C.c_void_p), ("is_w_out", C.c_void_p), ("xf", C.POINTER(Transform)),
+                ("out", LearnerBatch)]
+
+
 class BufferInfo(C.Structure):
     _fields_ = [("capacity", C.c_int64), ("row_bytes", C.c_int64), ("head", C.c_int64), ("size", C.c_int64),
                 ("total", C.c_int64), ("tree_depth", C.c_int32), ("tree_nodes", C.c_int64 * 8),
@@ -102,6 +111,9 @@ SIGNATURES = {
     "conduit_last_error": (C.c_char_p, []),
     "conduit_version": (C.c_char_p, []),
     "conduit_schedule": (ST, [P, P, P]),
+    "conduit_standin": (ST, [I64, P]),
+    "conduit_sync_cost_us": (ST, [P, P, I32_, P, P]),
+    "conduit_run_offpolicy": (ST, [P, P, P, P, P, P, P]),
 }
 
 
@@ -285,6 +297,33 @@ def conduit_schedule(t_rollout, t_update, g_ing, t_ing, g_del, t_del, t_sync_ing
     all_ = (SchedMode * n)()
     _check(lib().conduit_schedule(C.byref(c), C.byref(best), all_))
     return best.as_dict(), [m.as_dict() for m in all_]
+
+
+OP_INGEST, OP_DELIVER, OP_PRIO = 0, 1, 2
+
+
+def conduit_run_offpolicy(handle, loop, compute_stream, experience_stream):
+    """Run the native off-policy loop; returns (elapsed ms, op log as a list of
+    (kind, a, b) in experience-stream order)."""
+    cap = 3 * int(loop.iters)
+    log = (C.c_int64 * (3 * cap))()
+    n = C.c_int64(0)
+    ms = C.c_double(0.0)
+    _check(lib().conduit_run_offpolicy(handle, C.byref(loop), _stream(compute_stream), _stream(experience_stream),
+                                       C.byref(ms), log, C.byref(n)))
+    return ms.value, [(log[3 * i], log[3 * i + 1], log[3 * i + 2]) for i in range(min(n.value, cap))]
+
+
+def conduit_standin(work, stream=None):
+    _check(lib().conduit_standin(int(work), _stream(stream)))
+
+
+def conduit_sync_cost_us(s1, s2, hops=200):
+    """(hop_us, dep_us): an unmet cross-stream dependency, and the cost an
+    overlapped operator adds to the stream it overlaps."""
+    hop, dep = C.c_double(0.0), C.c_double(0.0)
+    _check(lib().conduit_sync_cost_us(_stream(s1), _stream(s2), int(hops), C.byref(hop), C.byref(dep)))
+    return hop.value, dep.value
 
 
 def conduit_minibatch_gather(src, row_bytes, n_src, perm, xf, out, cols=(), cols_out=(), stream=None):

@@ -240,6 +240,16 @@ struct conduit_buffer {
     int64_t head = 0, size = 0, total = 0;
 };
 
+BufferGeometry conduit::buffer_geometry(const conduit_buffer* b) {
+    BufferGeometry g;
+    g.row_bytes = b->layout.row_bytes;
+    g.frame_stack = b->opts.frame_stack;
+    g.action_bytes = b->opts.action_bytes;
+    g.ragged = b->opts.ragged != 0;
+    g.prioritized = b->opts.prioritized != 0;
+    return g;
+}
+
 extern "C" {
 
 void conduit_buffer_opts_default(conduit_buffer_opts* o) {

@@ -356,6 +356,16 @@ struct GatherArgs {
 // record `msg` as the calling thread's last error and return `s`
 conduit_status report_error(conduit_status s, const char* msg);
 
+// what the host code outside api.hip needs to know of a buffer's layout
+struct BufferGeometry {
+    int64_t row_bytes;
+    int32_t frame_stack;
+    int32_t action_bytes;
+    bool ragged;
+    bool prioritized;
+};
+BufferGeometry buffer_geometry(const conduit_buffer* b);
+
 // compute units of the current device (cached per device)
 int device_cus();
 // whether a gather moves its rows in 16-byte units (no transform, 16-byte

@@ -1,6 +1,7 @@
 """Scheduling cost model (Sec. 6.2, App. E, Eq. sched_opt): the oracle pinned by
 closed-form cases the text fixes, and the library's conduit_schedule against the
 oracle on random cost sets.  Host-only: no GPU needed."""
+import ctypes as C
 import math
 
 import numpy as np
@@ -127,3 +128,18 @@ def test_schedule_rejects_bad_costs(bad):
     with pytest.raises(cd.ConduitError) as e:
         cd.conduit_schedule(**args)
     assert e.value.status == cd.EINVAL
+
+
+def test_loop_entry_points_reject_bad_arguments_on_the_host():
+    # argument checks return before any device call, so they run without a GPU
+    L = cd.lib()
+    dummy = C.c_void_p(1)
+    hop, dep = C.c_double(), C.c_double()
+    assert L.conduit_standin(-1, None) == cd.EINVAL
+    for hops in (0, 1025):
+        assert L.conduit_sync_cost_us(dummy, dummy, hops, C.byref(hop), C.byref(dep)) == cd.EINVAL
+    assert L.conduit_sync_cost_us(None, dummy, 8, C.byref(hop), C.byref(dep)) == cd.EINVAL
+    assert L.conduit_sync_cost_us(dummy, dummy, 8, None, C.byref(dep)) == cd.EINVAL
+    ms = C.c_double()
+    lp = cd.OffpolicyLoop()
+    assert L.conduit_run_offpolicy(None, C.byref(lp), None, None, C.byref(ms), None, None) == cd.EINVAL
