@@ -646,6 +646,24 @@ def bench_schedule(d=10000, t_stage_us=(100.0, 150.0), iters=64, gs=(1, 2, 4, 8)
         measured.append(ms * 1e3 / iters)
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
+    name = lambda m: f"ov_ing={m['overlap_ing']} g_ing={int(m['g_ing'])} ov_del={m['overlap_del']} g_del={int(m['g_del'])}"  # noqa: E731
+    seq = next(i for i, m in enumerate(modes) if m["overlap_ing"] == 0 and m["overlap_del"] == 0 and
+               m["g_ing"] == 1 and m["g_del"] == 1)
+    out = {
+        "workload": f"stress d={d}, 10^6 slots, rollout unit = batch = 512, {iters} iterations per mode; "
+                    f"register-only compute stand-in (one workgroup per CU) for rollout and update",
+        "profiled_us": {"t_rollout": t_roll, "t_update": t_upd, "t_sync": t_sync, "t_hop_unmet": t_hop,
+                        "t_ing": dict(zip(map(str, gs), t_ing)), "t_del": dict(zip(map(str, gs), t_del))},
+    }
+    out.update(_schedule_report(modes, best, measured, name, seq, t_roll + t_upd, host_us))
+    out["model_choice_with_unmet_hop_as_t_sync"] = name(best_hop)
+    return out
+
+
+def _schedule_report(modes, best, measured, name, seq, stages, host_us):
+    """Model vs measurement over every mode: the model's choice against the
+    measured best, the sequential reference, exposed time, rank correlation."""
+    import numpy as np
     pred = np.array([m["t_iter"] for m in modes])
     meas = np.array(measured)
     k_best = int(np.argmin(meas))
@@ -653,29 +671,146 @@ def bench_schedule(d=10000, t_stage_us=(100.0, 150.0), iters=64, gs=(1, 2, 4, 8)
                                                                                     "i_ing", "i_del")))
     rank = lambda v: np.argsort(np.argsort(v))  # noqa: E731
     spearman = float(np.corrcoef(rank(pred), rank(meas))[0, 1])
-    name = lambda m: f"ov_ing={m['overlap_ing']} g_ing={int(m['g_ing'])} ov_del={m['overlap_del']} g_del={int(m['g_del'])}"  # noqa: E731
-    seq = next(i for i, m in enumerate(modes) if m["overlap_ing"] == 0 and m["overlap_del"] == 0 and
-               m["g_ing"] == 1 and m["g_del"] == 1)
-    stages = t_roll + t_upd
     return {
-        "workload": f"stress d={d}, 10^6 slots, rollout unit = batch = 512, {iters} iterations per mode; "
-                    f"register-only compute stand-in (one workgroup per CU) for rollout and update",
-        "profiled_us": {"t_rollout": t_roll, "t_update": t_upd, "t_sync": t_sync, "t_hop_unmet": t_hop,
-                        "t_ing": dict(zip(map(str, gs), t_ing)), "t_del": dict(zip(map(str, gs), t_del))},
         "model_choice": {"mode": name(modes[k_model]), "predicted_us": float(pred[k_model]),
                          "measured_us": float(meas[k_model])},
         "measured_best": {"mode": name(modes[k_best]), "predicted_us": float(pred[k_best]),
                           "measured_us": float(meas[k_best])},
-        "sequential_g1": {"predicted_us": float(pred[seq]), "measured_us": float(meas[seq])},
-        "exposed_us": {"sequential_g1": float(meas[seq] - stages), "model_choice": float(meas[k_model] - stages),
+        "sequential": {"mode": name(modes[seq]), "predicted_us": float(pred[seq]), "measured_us": float(meas[seq])},
+        "exposed_us": {"sequential": float(meas[seq] - stages), "model_choice": float(meas[k_model] - stages),
                        "measured_best": float(meas[k_best] - stages)},
         "model_regret": float(meas[k_model] / meas[k_best] - 1.0),
-        "model_choice_with_unmet_hop_as_t_sync": name(best_hop),
         "spearman_pred_vs_measured": spearman,
         "host_us_per_iteration_max": float(max(host_us)),
         "modes": [{"mode": name(m), "predicted_us": float(p), "measured_us": float(x)}
                   for m, p, x in zip(modes, pred, meas)],
     }
+
+
+def bench_schedule_onpolicy(T=256, E=64, M=8, iters=8, t_stage_us=(600.0, 800.0)):
+    """On-policy scheduling on one GPU (Sec. 6 knobs, pipelined case): the
+    native on-policy loop (conduit_run_onpolicy) on a PPO-shaped rollout of
+    E x T transitions of 3x84x84 u8, M minibatches gathered with the u8 -> fp32
+    transform plus advantages and returns, GAE gamma 0.99 lambda 0.95.
+    Candidates come from conduit_sched_candidates (ingestion j/M, delivery
+    1/M); the model's inputs are profiled (stage slices, ingestion of j
+    slices plus j/M of the GAE, one minibatch gather, one cross-stream
+    dependency); every mode is then run and timed."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    cfg = synth.PPO(T=T, E=E)
+    U, row = T * E, 3 * 84 * 84
+    torch.cuda.empty_cache()
+    obs = cfg.obs_steps(0, T, "cuda").reshape(1, U, row).expand(iters, U, row).contiguous()
+    tile = lambda a: _dev(np.ascontiguousarray(np.broadcast_to(a.reshape(1, -1), (iters, a.size))))  # noqa: E731
+    rew, val, done, boot = tile(cfg.reward), tile(cfg.value), tile(cfg.done), tile(cfg.bootstrap)
+    perm = _dev(np.stack([np.random.default_rng(7 + i).permutation(U) for i in range(iters)]).astype(np.int64))
+    adv = torch.empty(U, dtype=torch.float32, device="cuda")
+    ret = torch.empty(U, dtype=torch.float32, device="cuda")
+    out = torch.empty((iters, U, row), dtype=torch.float32, device="cuda")
+    out_adv = torch.empty((iters, U), dtype=torch.float32, device="cuda")
+    out_ret = torch.empty((iters, U), dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_U8_F32)
+    buf = cd.ReplayBuffer(U, cfg.obs_shape, torch.uint8, prioritized=False, action_bytes=0)
+    h = C.c_void_p(buf.handle)
+
+    def loop_struct(mode, work):
+        lp = cd.OnpolicyLoop()
+        lp.overlap_ing, lp.ing_slices, lp.overlap_del, lp.minibatches = mode[0], mode[1], mode[2], M
+        lp.iters, lp.steps, lp.envs = iters, T, E
+        lp.rollout_work, lp.update_work = work
+        lp.obs, lp.reward, lp.value, lp.done = obs.data_ptr(), rew.data_ptr(), val.data_ptr(), done.data_ptr()
+        lp.bootstrap, lp.gamma, lp.lam, lp.perm = boot.data_ptr(), cfg.gamma, cfg.lam, perm.data_ptr()
+        lp.xf = C.pointer(xf)
+        lp.adv, lp.ret = adv.data_ptr(), ret.data_ptr()
+        lp.out_obs, lp.out_adv, lp.out_ret = out.data_ptr(), out_adv.data_ptr(), out_ret.data_ptr()
+        return lp
+
+    # stand-ins: each stage runs as M slices
+    base = 20000
+    _b2b_ms([lambda: L.conduit_standin(base, stream)] * 5)
+    us_per_work = _b2b_ms([lambda: L.conduit_standin(base, stream)] * 20) * 1e3 / base
+    work = (int(t_stage_us[0] / us_per_work), int(t_stage_us[1] / us_per_work))
+    t_roll = _b2b_ms([lambda: L.conduit_standin(work[0] // M, stream)] * (10 * M)) * 1e3 * M
+    t_upd = _b2b_ms([lambda: L.conduit_standin(work[1] // M, stream)] * (10 * M)) * 1e3 * M
+    g_ing, g_del = cd.conduit_sched_candidates(True, M)
+    # Operator costs, each call on memory the previous calls did not touch (a
+    # rollout is larger than the 256 MB last-level cache, so repeating one
+    # call on the same data would time cache hits the loop never sees).
+    slice_rows = U // M
+    sweep = torch.empty(1 << 29, dtype=torch.uint8, device="cuda")
+    gae_ms = []
+    for i in range(iters):  # GAE: one call after a 512 MB sweep, timed alone
+        sweep.fill_(i)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        assert L.conduit_gae(rew[i].data_ptr(), val[i].data_ptr(), done[i].data_ptr(), boot[i].data_ptr(), T, E,
+                             cfg.gamma, cfg.lam, adv.data_ptr(), ret.data_ptr(), stream) == 0
+        e1.record()
+        torch.cuda.synchronize()
+        gae_ms.append(e0.elapsed_time(e1))
+    del sweep
+    t_gae = float(np.median(gae_ms[1:])) * 1e3
+    t_ing = []
+    for j in range(1, M + 1):
+        # M calls of j slices walk j whole rollouts of the staged rows (the
+        # head returns to slot 0)
+        structs = []
+        for c in range(M):
+            tr = cd.Transitions()
+            r0 = (c * j * slice_rows) % (iters * U)
+            tr.n = j * slice_rows
+            tr.obs = obs.data_ptr() + r0 * row
+            tr.reward, tr.done = rew.data_ptr() + 4 * r0, done.data_ptr() + r0
+            structs.append(tr)
+        calls = [lambda tr=tr: L.conduit_ingest(h, C.byref(tr), stream) for tr in structs]
+        _b2b_ms(calls)
+        t_ing.append(_b2b_ms(calls) * 1e3 + j / M * t_gae)
+    assert buf.info().head == 0
+    # delivery: the M minibatches of each staged rollout in turn
+    mb = U // M
+    cols = (C.c_void_p * 2)(adv.data_ptr(), ret.data_ptr())
+    calls = []
+    for i in range(iters):
+        for m in range(M):
+            o = i * U + m * mb
+            co = (C.c_void_p * 2)(out_adv.data_ptr() + 4 * o, out_ret.data_ptr() + 4 * o)
+            calls.append(lambda i=i, m=m, o=o, co=co: L.conduit_minibatch_gather(
+                obs.data_ptr() + i * U * row, row, U, perm.data_ptr() + 8 * (i * U + m * mb), mb, C.byref(xf),
+                out.data_ptr() + o * row * 4, cols, co, 2, stream))
+    _b2b_ms(calls)
+    t_del = [_b2b_ms(calls) * 1e3]
+    comp, exp = torch.cuda.Stream(), torch.cuda.Stream()
+    t_hop, t_sync = cd.conduit_sync_cost_us(comp, exp, 200)
+    best, modes = cd.conduit_schedule(t_roll, t_upd, g_ing, t_ing, g_del, t_del, t_sync, t_sync, on_policy=True)
+    cd.conduit_run_onpolicy(buf.handle, loop_struct((0, M, 0), work), comp, exp)  # warm-up
+    measured, host_us = [], []
+    for m in modes:
+        lp = loop_struct((m["overlap_ing"], round(m["g_ing"] * M), m["overlap_del"]), work)
+        h0 = time.perf_counter()
+        ms, _ = cd.conduit_run_onpolicy(buf.handle, lp, comp, exp)
+        host_us.append((time.perf_counter() - h0) * 1e6 / iters)
+        measured.append(ms * 1e3 / iters)
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+    buf.close()
+    name = lambda m: f"ov_ing={m['overlap_ing']} g_ing={round(m['g_ing'] * M)}/{M} ov_del={m['overlap_del']} g_del=1/{M}"  # noqa: E731
+    seq = next(i for i, m in enumerate(modes) if m["overlap_ing"] == 0 and m["overlap_del"] == 0 and
+               m["g_ing"] == 1.0)
+    out_d = {
+        "workload": f"PPO-shaped rollout {E} envs x {T} steps of 3x84x84 u8, {M} minibatches of {mb} -> fp32 "
+                    f"with advantages and returns, GAE over the rollout; {iters} iterations per mode; "
+                    f"register-only compute stand-in for rollout and update, each run as {M} slices",
+        "profiled_us": {"t_rollout": t_roll, "t_update": t_upd, "t_sync": t_sync, "t_hop_unmet": t_hop,
+                        "t_gae": t_gae, "t_ing": {f"{j}/{M}": t for j, t in zip(range(1, M + 1), t_ing)},
+                        "t_del": {f"1/{M}": t_del[0]}},
+    }
+    out_d.update(_schedule_report(modes, best, measured, name, seq, t_roll + t_upd, host_us))
+    return out_d
 
 
 def bench_tiny(iters=100):
@@ -829,7 +964,8 @@ def _traffic_from_profile():
 
 
 ROWS = {"tiny": lambda: bench_tiny(), "ppo": lambda: bench_ppo(), "large": lambda: bench_large(),
-        "tokens": lambda: bench_tokens(), "stress": lambda: bench_stress(), "schedule": lambda: bench_schedule()}
+        "tokens": lambda: bench_tokens(), "stress": lambda: bench_stress(), "schedule": lambda: bench_schedule(),
+        "schedule_onpolicy": lambda: bench_schedule_onpolicy()}
 
 
 def main():
@@ -890,8 +1026,8 @@ def main():
         "rows": {"dqn_ingest_32768": d["ingest_big"]},
     }
     if not args.no_rows:
-        only = set(x for x in args.only.split(",") if x) or {"ppo", "large", "tokens", "tiny", "stress", "schedule"}
-        for name in ("tiny", "ppo", "large", "tokens", "stress", "schedule"):
+        only = set(x for x in args.only.split(",") if x) or set(ROWS)
+        for name in ("tiny", "ppo", "large", "tokens", "stress", "schedule", "schedule_onpolicy"):
             if name in only:
                 print(f"bench.py: row {name} ...", file=sys.stderr, flush=True)
                 out["rows"][name] = ROWS[name]()

@@ -410,7 +410,9 @@ const char* conduit_version(void);
  *                          on-policy pipelining) and the wall time of one
  *                          invocation at each;
  *   g_del[n_del], t_del[n_del]  the same for delivery (training batches per
- *                          invocation).
+ *                          invocation);
+ *   on_policy              0: off-policy batching; 1: on-policy pipelining
+ *                          (every granularity in (0, 1]).
  * All arrays are host memory owned by the caller.
  */
 typedef struct conduit_sched_costs {
@@ -421,6 +423,7 @@ typedef struct conduit_sched_costs {
     const double* t_ing;
     const double* g_del;
     const double* t_del;
+    int32_t on_policy;
 } conduit_sched_costs;
 
 /* One execution mode and its modelled latencies. */
@@ -435,7 +438,8 @@ typedef struct conduit_sched_mode {
  * Scores every mode -- overlap_ing, overlap_del in {0,1} and every candidate
  * granularity pair -- with
  *   Tbar(g)    = T(g) / g                                (per-unit cost)
- *   gamma(g)   = 1 if g >= 1, else 1 - g
+ *   gamma(g)   = 1 if g >= 1, else 1 - g                 (off-policy)
+ *   gamma(g)   = 1 - g                                   (on-policy)
  *   hide_ing   = gamma(g_ing) * min(t_rollout, Tbar_ing(g_ing))
  *   T_ing_path = t_rollout + Tbar_ing(g_ing) + overlap_ing * (t_sync_ing - hide_ing)
  * (delivery alike with t_update), T_iter = T_ing_path + T_del_path, and
@@ -443,11 +447,30 @@ typedef struct conduit_sched_mode {
  * overlap_ing, overlap_del, i_ing, i_del (each ascending, the last fastest);
  * the first of equal minima wins.  If `all` is not NULL it receives every
  * mode in that order (4 * n_ing * n_del entries, caller-owned).
+ * On-policy, App. E's fractional case applies on all of (0, 1]: a rollout
+ * must be ingested, and a batch delivered, within its own iteration, so only
+ * the part of the operator that is not its last invocation can hide; at g = 1
+ * nothing does (the g >= 1 case of App. E describes off-policy batching
+ * across iterations).
  * Errors: EINVAL (NULL costs/best, n_ing or n_del < 1, NULL arrays, a
- * granularity <= 0, a negative or non-finite time).
+ * granularity <= 0, or > 1 on-policy, a negative or non-finite time).
  */
 conduit_status conduit_schedule(const conduit_sched_costs* costs, conduit_sched_mode* best,
                                 conduit_sched_mode* all);
+
+/*
+ * The candidate granularities of an RL configuration (Sec. 4.1-4.3): off-policy
+ * (on_policy = 0) G_ing = {1, ..., g_max_ing} and G_del = {1, ..., g_max_del},
+ * the caps bounding staleness and memory; on-policy with M = minibatches
+ * updates per rollout, G_ing = {1/M, 2/M, ..., 1} and G_del = {1/M} (the caps
+ * are ignored).  Each set is written in ascending order into the caller's
+ * host arrays (cap_ing / cap_del entries available) with its size in *n_ing /
+ * *n_del.  Errors: EINVAL (NULL outputs, minibatches < 1 on-policy, a cap < 1
+ * off-policy, an array too small).
+ */
+conduit_status conduit_sched_candidates(int32_t on_policy, int32_t minibatches, int32_t g_max_ing,
+                                        int32_t g_max_del, double* g_ing, int32_t cap_ing, int32_t* n_ing,
+                                        double* g_del, int32_t cap_del, int32_t* n_del);
 
 /*
  * Synthetic compute that stands in for an actor rollout or a learner update in
@@ -527,6 +550,67 @@ typedef struct conduit_offpolicy_loop {
 
 conduit_status conduit_run_offpolicy(conduit_buffer* buf, const conduit_offpolicy_loop* loop, void* compute_stream,
                                      void* experience_stream, double* elapsed_ms, int64_t* op_log, int64_t* n_ops);
+
+/*
+ * An on-policy iteration loop on one GPU (Sec. 4.1-4.2 decoupled ingestion and
+ * delivery, on-policy case; Sec. 6 timing and granularity; PPO-shaped).  The
+ * rollout unit is `steps` x `envs` transitions, time-major (row t*envs + e).
+ * Iteration i: the actor's rollout runs as M = minibatches slices of
+ * steps/M time steps (stand-in compute of rollout_work/M each); ingestion
+ * copies the rows of ing_slices slices per invocation (g_ing = ing_slices/M;
+ * the last invocation takes what remains) into `buf`; GAE over the whole
+ * rollout follows the last one; delivery then gathers the M minibatches of
+ * steps*envs/M rows through perm (a shuffle of the rollout) with their
+ * advantages and returns, each followed by one update slice (stand-in of
+ * update_work/M).
+ *   overlap_ing = 0: each ingestion runs inline on the compute stream after
+ *                    its slices; 1: on the experience stream as soon as its
+ *                    slices are rolled out, pipelined with the next slices.
+ *   overlap_del = 0: each minibatch gather runs inline before its update
+ *                    slice; 1: minibatch m+1 is gathered on the experience
+ *                    stream during update slice m.
+ * Whatever the mode the experience operators keep one program order (the
+ * ingestions of a rollout, its GAE, its minibatches), so the outputs do not
+ * depend on the mode (App. C: on-policy freshness; Sec. 4.3).
+ * `buf`: a dense, non-prioritised buffer of capacity steps*envs whose head is
+ * at slot 0 (each iteration refills it from slot 0).  Device inputs, per
+ * iteration i at offset i*steps*envs (bootstrap at i*envs): obs [rows of the
+ * buffer's row size], reward float, value float or NULL, done uint8, bootstrap
+ * float [envs] or NULL, perm int64 (a permutation of 0..steps*envs-1).
+ * Scratch: adv, ret float [steps*envs] (the current iteration's GAE).
+ * Outputs at offset i*steps*envs rows: out_obs (rows through xf: NONE,
+ * U8_F32 or U8_BF16_NORM), out_adv, out_ret float.
+ * `op_log` (host, 4 int64 per entry, NULL allowed; at most
+ * iters*(2*minibatches+1) entries) receives the experience operators in
+ * program order: (0, iteration, first slice, slices) for an ingestion,
+ * (1, iteration, minibatch, 0) for a delivery, (3, iteration, 0, 0) for the
+ * GAE; *n_ops their count.  *elapsed_ms: events around the loop on the
+ * compute stream.
+ * Errors: EINVAL (granularities or sizes out of range, steps not a multiple
+ * of minibatches, NULL required pointers, a prioritised or ragged buffer, a
+ * wrong capacity or head), plus those of the operators.
+ */
+typedef struct conduit_onpolicy_loop {
+    int32_t overlap_ing, ing_slices, overlap_del, minibatches;
+    int64_t iters, steps, envs;
+    int64_t rollout_work, update_work;
+    const void* obs;
+    const float* reward;
+    const float* value;
+    const uint8_t* done;
+    const float* bootstrap;
+    double gamma, lam;  /* GAE discount and lambda */
+    const int64_t* perm;
+    const conduit_transform* xf;
+    float* adv;
+    float* ret;
+    void* out_obs;
+    float* out_adv;
+    float* out_ret;
+} conduit_onpolicy_loop;
+
+conduit_status conduit_run_onpolicy(conduit_buffer* buf, const conduit_onpolicy_loop* loop, void* compute_stream,
+                                    void* experience_stream, double* elapsed_ms, int64_t* op_log, int64_t* n_ops);
 
 #ifdef __cplusplus
 }

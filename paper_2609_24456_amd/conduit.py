@@ -58,7 +58,7 @@ class SchedCosts(C.Structure):
     _fields_ = [("t_rollout", C.c_double), ("t_update", C.c_double), ("t_sync_ing", C.c_double),
                 ("t_sync_del", C.c_double), ("n_ing", C.c_int32), ("n_del", C.c_int32),
                 ("g_ing", C.POINTER(C.c_double)), ("t_ing", C.POINTER(C.c_double)),
-                ("g_del", C.POINTER(C.c_double)), ("t_del", C.POINTER(C.c_double))]
+                ("g_del", C.POINTER(C.c_double)), ("t_del", C.POINTER(C.c_double)), ("on_policy", C.c_int32)]
 
 
 class SchedMode(C.Structure):
@@ -77,6 +77,16 @@ class OffpolicyLoop(C.Structure):
                 ("rollout", Transitions), ("uniforms", C.c_void_p), ("new_prio", C.c_void_p),
                 ("idx_out", C.c_void_p), ("is_w_out", C.c_void_p), ("xf", C.POINTER(Transform)),
                 ("out", LearnerBatch)]
+
+
+class OnpolicyLoop(C.Structure):
+    _fields_ = [("overlap_ing", C.c_int32), ("ing_slices", C.c_int32), ("overlap_del", C.c_int32),
+                ("minibatches", C.c_int32), ("iters", C.c_int64), ("steps", C.c_int64), ("envs", C.c_int64),
+                ("rollout_work", C.c_int64), ("update_work", C.c_int64),
+                ("obs", C.c_void_p), ("reward", C.c_void_p), ("value", C.c_void_p), ("done", C.c_void_p),
+                ("bootstrap", C.c_void_p), ("gamma", C.c_double), ("lam", C.c_double), ("perm", C.c_void_p),
+                ("xf", C.POINTER(Transform)), ("adv", C.c_void_p), ("ret", C.c_void_p), ("out_obs", C.c_void_p),
+                ("out_adv", C.c_void_p), ("out_ret", C.c_void_p)]
 
 
 class BufferInfo(C.Structure):
@@ -113,6 +123,8 @@ SIGNATURES = {
     "conduit_schedule": (ST, [P, P, P]),
     "conduit_standin": (ST, [I64, P]),
     "conduit_sync_cost_us": (ST, [P, P, I32_, P, P]),
+    "conduit_sched_candidates": (ST, [I32_, I32_, I32_, I32_, P, I32_, P, P, I32_, P]),
+    "conduit_run_onpolicy": (ST, [P, P, P, P, P, P, P]),
     "conduit_run_offpolicy": (ST, [P, P, P, P, P, P, P]),
 }
 
@@ -286,12 +298,13 @@ def conduit_gae_packed(last_reward, lengths, values, Lmax, gamma, lam, adv, ret,
                                     _ptr(ret, torch.float32, "ret"), _stream(stream)))
 
 
-def conduit_schedule(t_rollout, t_update, g_ing, t_ing, g_del, t_del, t_sync_ing=0.0, t_sync_del=0.0):
+def conduit_schedule(t_rollout, t_update, g_ing, t_ing, g_del, t_del, t_sync_ing=0.0, t_sync_del=0.0,
+                     on_policy=False):
     """Sec. 6 cost model: (best mode, every mode) as dicts."""
     arr = lambda xs: (C.c_double * max(1, len(xs)))(*[float(x) for x in xs])  # noqa: E731
     gi, ti, gd, td = arr(g_ing), arr(t_ing), arr(g_del), arr(t_del)
     c = SchedCosts(float(t_rollout), float(t_update), float(t_sync_ing), float(t_sync_del), len(g_ing), len(g_del),
-                   gi, ti, gd, td)
+                   gi, ti, gd, td, int(bool(on_policy)))
     best = SchedMode()
     n = 4 * max(1, len(g_ing)) * max(1, len(g_del))
     all_ = (SchedMode * n)()
@@ -299,7 +312,17 @@ def conduit_schedule(t_rollout, t_update, g_ing, t_ing, g_del, t_del, t_sync_ing
     return best.as_dict(), [m.as_dict() for m in all_]
 
 
-OP_INGEST, OP_DELIVER, OP_PRIO = 0, 1, 2
+def conduit_sched_candidates(on_policy, minibatches=1, g_max_ing=1, g_max_del=1):
+    """Feasible granularity sets (G_ing, G_del) of an RL configuration."""
+    cap = max(1, int(minibatches), int(g_max_ing), int(g_max_del))
+    gi, gd = (C.c_double * cap)(), (C.c_double * cap)()
+    ni, nd = C.c_int32(0), C.c_int32(0)
+    _check(lib().conduit_sched_candidates(int(bool(on_policy)), int(minibatches), int(g_max_ing), int(g_max_del),
+                                          gi, cap, C.byref(ni), gd, cap, C.byref(nd)))
+    return [gi[i] for i in range(ni.value)], [gd[i] for i in range(nd.value)]
+
+
+OP_INGEST, OP_DELIVER, OP_PRIO, OP_GAE = 0, 1, 2, 3
 
 
 def conduit_run_offpolicy(handle, loop, compute_stream, experience_stream):
@@ -312,6 +335,18 @@ def conduit_run_offpolicy(handle, loop, compute_stream, experience_stream):
     _check(lib().conduit_run_offpolicy(handle, C.byref(loop), _stream(compute_stream), _stream(experience_stream),
                                        C.byref(ms), log, C.byref(n)))
     return ms.value, [(log[3 * i], log[3 * i + 1], log[3 * i + 2]) for i in range(min(n.value, cap))]
+
+
+def conduit_run_onpolicy(handle, loop, compute_stream, experience_stream):
+    """Run the native on-policy loop; returns (elapsed ms, op log as a list of
+    (kind, iteration, a, b) in program order)."""
+    cap = int(loop.iters) * (2 * int(loop.minibatches) + 1)
+    log = (C.c_int64 * (4 * cap))()
+    n = C.c_int64(0)
+    ms = C.c_double(0.0)
+    _check(lib().conduit_run_onpolicy(handle, C.byref(loop), _stream(compute_stream), _stream(experience_stream),
+                                      C.byref(ms), log, C.byref(n)))
+    return ms.value, [tuple(log[4 * i:4 * i + 4]) for i in range(min(n.value, cap))]
 
 
 def conduit_standin(work, stream=None):

@@ -247,6 +247,9 @@ BufferGeometry conduit::buffer_geometry(const conduit_buffer* b) {
     g.action_bytes = b->opts.action_bytes;
     g.ragged = b->opts.ragged != 0;
     g.prioritized = b->opts.prioritized != 0;
+    g.capacity = b->capacity;
+    g.head = b->head;
+    g.obs = b->obs;
     return g;
 }
 

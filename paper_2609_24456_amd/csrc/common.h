@@ -363,6 +363,9 @@ struct BufferGeometry {
     int32_t action_bytes;
     bool ragged;
     bool prioritized;
+    int64_t capacity;
+    int64_t head;              // next slot ingestion writes (host-known)
+    const uint8_t* obs;        // device [capacity, row_bytes]
 };
 BufferGeometry buffer_geometry(const conduit_buffer* b);
 

@@ -66,6 +66,46 @@ struct EventPool {
     }
 };
 
+// One program order over operators issued on two streams C and E: an
+// operator issued on the other stream than its predecessor waits for the
+// predecessor's event.  Events are recorded only where the other stream can
+// wait on them: after every operator on E, and after every operator when
+// operators live on both streams (`both`).  A stream does not wait twice in a
+// row for the same event.
+struct OpOrder {
+    EventPool& pool;
+    hipStream_t C, E;
+    bool both;
+    hipEvent_t last_ev = nullptr;
+    hipStream_t last_s = nullptr;
+    hipEvent_t waited[2] = {nullptr, nullptr};
+    OpOrder(EventPool& p, hipStream_t c, hipStream_t e, bool b) : pool(p), C(c), E(e), both(b) {}
+    void wait(hipStream_t s, hipEvent_t e) {
+        hipEvent_t& w = waited[s == C ? 0 : 1];
+        if (!e || w == e) return;
+        pool.wait(s, e);
+        w = e;
+    }
+    void before(hipStream_t s) {
+        if (last_ev && last_s != s) wait(s, last_ev);
+    }
+    hipEvent_t after(hipStream_t s) {
+        last_ev = (s == E || both) ? pool.mark(s) : nullptr;
+        last_s = s;
+        return last_ev;
+    }
+};
+
+// output bytes per input byte of a row transform usable by the loops
+int xf_out_elem(const conduit_transform* xf) {
+    switch (xf->kind) {
+        case CONDUIT_XF_NONE: return 1;
+        case CONDUIT_XF_U8_F32: return 4;
+        case CONDUIT_XF_U8_BF16_NORM: return 2;
+        default: return 0;
+    }
+}
+
 }  // namespace
 
 }  // namespace conduit
@@ -181,7 +221,8 @@ extern "C" conduit_status conduit_run_offpolicy(conduit_buffer* buf, const condu
     const BufferGeometry G = buffer_geometry(buf);
     if (G.ragged) return report_error(CONDUIT_EINVAL, "the loop takes dense buffers");
     if (!G.prioritized) return report_error(CONDUIT_EINVAL, "the loop needs a prioritised buffer");
-    const int xf_elem = L.xf->kind == CONDUIT_XF_U8_F32 ? 4 : L.xf->kind == CONDUIT_XF_U8_BF16_NORM ? 2 : 1;
+    const int xf_elem = xf_out_elem(L.xf);
+    if (xf_elem == 0) return report_error(CONDUIT_EINVAL, "the loop's transform must be NONE, U8_F32 or U8_BF16_NORM");
     const int64_t out_row = G.frame_stack * G.row_bytes * xf_elem;
     hipStream_t C = static_cast<hipStream_t>(compute_stream);
     hipStream_t E = static_cast<hipStream_t>(experience_stream);
@@ -237,23 +278,11 @@ extern "C" conduit_status conduit_run_offpolicy(conduit_buffer* buf, const condu
         return r;
     };
 
-    // Experience operators keep one total order: an operator issued on the
-    // other stream than its predecessor waits for the predecessor's event.
-    // Events are recorded only where the other stream can wait on them: after
-    // operators on the experience stream, and after every operator when the
-    // two operators live on different streams.
+    // experience operators in one program order across the two streams
     const bool uses_E = S_ing == E || S_del == E;
-    const bool split = S_ing != S_del;
-    hipEvent_t last_ev = nullptr;
-    hipStream_t last_s = nullptr;
-    auto before = [&](hipStream_t s) {
-        if (last_ev && last_s != s) pool.wait(s, last_ev);
-    };
-    auto after = [&](hipStream_t s) {
-        last_ev = (s == E || split) ? pool.mark(s) : nullptr;
-        last_s = s;
-        return last_ev;
-    };
+    OpOrder order(pool, C, E, S_ing != S_del);
+    auto before = [&](hipStream_t s) { order.before(s); };
+    auto after = [&](hipStream_t s) { return order.after(s); };
     int64_t first_pending = 0;
     auto run_ingest = [&](int64_t upto) {  // the units accumulated up to iteration upto
         before(S_ing);
@@ -280,7 +309,7 @@ extern "C" conduit_status conduit_run_offpolicy(conduit_buffer* buf, const condu
             delivered[(size_t)k] = 1;
         }
         if (st != CONDUIT_OK) break;
-        if (S_del != C && t % L.g_del == 0) pool.wait(C, delivered_ev[(size_t)k]);  // once per group
+        if (S_del != C) order.wait(C, delivered_ev[(size_t)k]);
         if (he == hipSuccess) he = launch_standin(L.update_work, C);
         // overlapped delivery: the next group is prepared during the update
         if (L.overlap_del && (t + 1) % L.g_del == 0 && t + 1 < L.iters) {
@@ -292,7 +321,7 @@ extern "C" conduit_status conduit_run_offpolicy(conduit_buffer* buf, const condu
         }
         if (st != CONDUIT_OK) break;
         // the learner's new priorities, after its update
-        if (S_del != C) pool.wait(E, pool.mark(C));
+        if (S_del != C) order.wait(E, pool.mark(C));
         before(S_del);
         st = conduit_update_priorities(buf, L.idx_out + t * B, L.new_prio + t * B, B, S_del);
         log(2, t, 0);
@@ -300,6 +329,142 @@ extern "C" conduit_status conduit_run_offpolicy(conduit_buffer* buf, const condu
         // overlapped ingestion: after this iteration's learner step, so it runs
         // during the next rollout (the next inline operator waits for it)
         if (st == CONDUIT_OK && L.overlap_ing && ing_due) run_ingest(t);
+    }
+    if (uses_E) pool.wait(C, pool.mark(E));
+    if (he == hipSuccess) he = pool.err;
+    if (he == hipSuccess) he = hipEventRecord(t_end, C);
+    if (he == hipSuccess) he = hipEventSynchronize(t_end);
+    float ms = 0.0f;
+    if (he == hipSuccess) he = hipEventElapsedTime(&ms, t_start, t_end);
+    if (t_start) (void)hipEventDestroy(t_start);
+    if (t_end) (void)hipEventDestroy(t_end);
+    if (st != CONDUIT_OK) return st;
+    if (he != hipSuccess) return report_error(CONDUIT_EDEVICE, hipGetErrorString(he));
+    *elapsed_ms = ms;
+    if (n_ops) *n_ops = logged;
+    return CONDUIT_OK;
+}
+
+extern "C" conduit_status conduit_run_onpolicy(conduit_buffer* buf, const conduit_onpolicy_loop* lp,
+                                               void* compute_stream, void* experience_stream, double* elapsed_ms,
+                                               int64_t* op_log, int64_t* n_ops) {
+    if (!buf || !lp || !elapsed_ms) return report_error(CONDUIT_EINVAL, "NULL buffer, loop or elapsed_ms");
+    const conduit_onpolicy_loop& L = *lp;
+    const int64_t M = L.minibatches;
+    if (M < 1 || L.ing_slices < 1 || L.ing_slices > M)
+        return report_error(CONDUIT_EINVAL, "need minibatches >= 1 and 1 <= ing_slices <= minibatches");
+    if (L.iters < 1 || L.steps < 1 || L.envs < 1 || L.steps % M != 0)
+        return report_error(CONDUIT_EINVAL, "iters, steps, envs must be >= 1 and steps a multiple of minibatches");
+    if (L.rollout_work < 0 || L.update_work < 0) return report_error(CONDUIT_EINVAL, "work must be >= 0");
+    if (!L.obs || !L.reward || !L.done || !L.perm || !L.xf || !L.adv || !L.ret || !L.out_obs || !L.out_adv ||
+        !L.out_ret)
+        return report_error(CONDUIT_EINVAL, "NULL required pointer");
+    const int xf_elem = xf_out_elem(L.xf);
+    if (xf_elem == 0) return report_error(CONDUIT_EINVAL, "the loop's transform must be NONE, U8_F32 or U8_BF16_NORM");
+    const BufferGeometry G = buffer_geometry(buf);
+    if (G.ragged || G.prioritized) return report_error(CONDUIT_EINVAL, "the loop takes a dense, non-prioritised buffer");
+    const int64_t U = L.steps * L.envs;  // rows of one rollout
+    if (G.capacity != U || G.head != 0)
+        return report_error(CONDUIT_EINVAL, "buffer capacity must be steps*envs with its head at slot 0");
+    const int64_t out_row = G.row_bytes * xf_elem;
+    const int64_t slice_rows = (L.steps / M) * L.envs;
+    const int64_t mb = U / M;
+    hipStream_t C = static_cast<hipStream_t>(compute_stream);
+    hipStream_t E = static_cast<hipStream_t>(experience_stream);
+    hipStream_t S_ing = L.overlap_ing ? E : C;
+    hipStream_t S_del = L.overlap_del ? E : C;
+    const bool uses_E = S_ing == E || S_del == E;
+
+    EventPool pool((size_t)(L.iters * (4 * M + 4) + 8));
+    OpOrder order(pool, C, E, S_ing != S_del);
+    hipEvent_t t_start = nullptr, t_end = nullptr;
+    hipError_t he = pool.err;
+    if (he == hipSuccess) he = hipEventCreate(&t_start);
+    if (he == hipSuccess) he = hipEventCreate(&t_end);
+    conduit_status st = CONDUIT_OK;
+    const int64_t log_cap = L.iters * (2 * M + 1);
+    int64_t logged = 0;
+    auto log = [&](int64_t a, int64_t b, int64_t c, int64_t d) {
+        if (op_log && logged < log_cap) {
+            int64_t* e = op_log + 4 * logged;
+            e[0] = a;
+            e[1] = b;
+            e[2] = c;
+            e[3] = d;
+        }
+        ++logged;
+    };
+    // ingestion of rollout i's slices [first, first + n): rows copied into
+    // the buffer from slot first * slice_rows on
+    auto ingest = [&](int64_t i, int64_t first, int64_t n) {
+        conduit_transitions tr{};
+        const int64_t r0 = i * U + first * slice_rows;
+        tr.n = n * slice_rows;
+        tr.obs = static_cast<const uint8_t*>(L.obs) + r0 * G.row_bytes;
+        tr.reward = L.reward + r0;
+        tr.done = L.done + r0;
+        return conduit_ingest(buf, &tr, S_ing);
+    };
+    // delivery of rollout i's minibatch m: rows perm[m*mb ...] with their
+    // advantages and returns
+    const float* cols[2] = {L.adv, L.ret};
+    auto deliver = [&](int64_t i, int64_t m, hipStream_t s) {
+        const int64_t o = i * U + m * mb;
+        float* cols_out[2] = {L.out_adv + o, L.out_ret + o};
+        return conduit_minibatch_gather(G.obs, G.row_bytes, U, L.perm + i * U + m * mb, mb, L.xf,
+                                        static_cast<uint8_t*>(L.out_obs) + o * out_row, cols, cols_out, 2, s);
+    };
+    std::vector<hipEvent_t> delivered((size_t)M, nullptr);
+
+    if (he == hipSuccess) he = hipEventRecord(t_start, C);
+    if (uses_E) pool.wait(E, pool.mark(C));
+    for (int64_t i = 0; i < L.iters && st == CONDUIT_OK && he == hipSuccess; ++i) {
+        // rollout slices, each ingestion issued once its slices are rolled out
+        int64_t first = 0;
+        for (int64_t sl = 0; sl < M && st == CONDUIT_OK && he == hipSuccess; ++sl) {
+            he = launch_standin(L.rollout_work / M, C);
+            if (sl + 1 - first == L.ing_slices || sl == M - 1) {
+                if (S_ing != C) order.wait(E, pool.mark(C));
+                order.before(S_ing);
+                st = ingest(i, first, sl + 1 - first);
+                log(0, i, first, sl + 1 - first);
+                order.after(S_ing);
+                first = sl + 1;
+            }
+        }
+        if (st != CONDUIT_OK || he != hipSuccess) break;
+        // GAE over the whole rollout ends the ingestion path
+        order.before(S_ing);
+        st = conduit_gae(L.reward + i * U, L.value ? L.value + i * U : nullptr, L.done + i * U,
+                         L.bootstrap ? L.bootstrap + i * L.envs : nullptr, L.steps, L.envs, L.gamma, L.lam,
+                         L.adv, L.ret, S_ing);
+        log(3, i, 0, 0);
+        order.after(S_ing);
+        if (st != CONDUIT_OK) break;
+        // minibatches, each before its update slice
+        if (S_del == E) {
+            order.before(E);
+            st = deliver(i, 0, E);
+            log(1, i, 0, 0);
+            delivered[0] = order.after(E);
+        }
+        for (int64_t m = 0; m < M && st == CONDUIT_OK && he == hipSuccess; ++m) {
+            if (S_del == C) {
+                order.before(C);
+                st = deliver(i, m, C);
+                log(1, i, m, 0);
+                order.after(C);
+            } else {
+                order.wait(C, delivered[(size_t)m]);
+                if (m + 1 < M) {  // prepared during this update slice
+                    order.before(E);
+                    st = deliver(i, m + 1, E);
+                    log(1, i, m + 1, 0);
+                    delivered[(size_t)m + 1] = order.after(E);
+                }
+            }
+            if (st == CONDUIT_OK) he = launch_standin(L.update_work / M, C);
+        }
     }
     if (uses_E) pool.wait(C, pool.mark(E));
     if (he == hipSuccess) he = pool.err;

@@ -1,8 +1,10 @@
-"""The native off-policy loop (conduit_run_offpolicy) with the experience path
-on its own stream, in several timing/granularity modes: whatever the mode, the
-experience operators run in one program order on their stream, so every
-delivered batch, weight and the final tree must equal the oracle replaying the
-operations of the loop's log in that order."""
+"""The native loops with the experience path on a second stream, in several
+timing/granularity modes.  Off-policy (conduit_run_offpolicy): whatever the
+mode the experience operators keep one program order, so every delivered
+batch, weight and the final tree must equal the oracle replaying the
+operations of the loop's log in that order.  On-policy (conduit_run_onpolicy):
+the outputs do not depend on the mode at all; every minibatch, advantage and
+return must equal the oracle's GAE and shuffle-gather of each rollout."""
 import ctypes as C
 
 import numpy as np
@@ -11,7 +13,7 @@ import torch
 
 import oracle
 import synth
-from gpu_util import assert_weights_close, dev, host, read_col, tree_consistent
+from gpu_util import assert_gae_close, assert_weights_close, dev, host, read_col, tree_consistent
 
 pytestmark = pytest.mark.gpu
 
@@ -120,3 +122,83 @@ def test_standin_scales_with_work_and_sync_costs_are_finite():
     assert 1.6 < times[1] / times[0] < 2.4, times
     hop, dep = cd.conduit_sync_cost_us(s1, s2, 64)
     assert 0.0 <= dep < 1000.0 and 0.0 <= hop < 1000.0, (hop, dep)
+
+
+def _onpolicy(mode, iters=3, T=32, E=16, M=4, shape=(3, 8, 8), work=(4000, 4000)):
+    overlap_ing, ing_slices, overlap_del = mode
+    rng = np.random.default_rng(23)
+    U = T * E
+    obs = rng.integers(0, 256, (iters, U) + shape, dtype=np.uint8)
+    rew = rng.standard_normal((iters, U)).astype(np.float32)
+    val = rng.standard_normal((iters, U)).astype(np.float32)
+    done = (rng.random((iters, U)) < 0.05).astype(np.uint8)
+    boot = rng.standard_normal((iters, E)).astype(np.float32)
+    perm = np.stack([rng.permutation(U) for _ in range(iters)]).astype(np.int64)
+    gamma, lam = 0.99, 0.95
+    buf = cd.ReplayBuffer(U, shape, torch.uint8, prioritized=False, action_bytes=0)
+    d = {k: dev(v) for k, v in dict(obs=obs, rew=rew, val=val, done=done, boot=boot, perm=perm).items()}
+    adv = torch.empty(U, dtype=torch.float32, device="cuda")
+    ret = torch.empty(U, dtype=torch.float32, device="cuda")
+    out = torch.empty((iters, U) + shape, dtype=torch.float32, device="cuda")
+    out_adv = torch.empty((iters, U), dtype=torch.float32, device="cuda")
+    out_ret = torch.empty((iters, U), dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_U8_F32)
+    lp = cd.OnpolicyLoop()
+    lp.overlap_ing, lp.ing_slices, lp.overlap_del, lp.minibatches = overlap_ing, ing_slices, overlap_del, M
+    lp.iters, lp.steps, lp.envs = iters, T, E
+    lp.rollout_work, lp.update_work = work
+    lp.obs, lp.reward, lp.value, lp.done = d["obs"].data_ptr(), d["rew"].data_ptr(), d["val"].data_ptr(), \
+        d["done"].data_ptr()
+    lp.bootstrap, lp.gamma, lp.lam, lp.perm = d["boot"].data_ptr(), gamma, lam, d["perm"].data_ptr()
+    lp.xf = C.pointer(xf)
+    lp.adv, lp.ret = adv.data_ptr(), ret.data_ptr()
+    lp.out_obs, lp.out_adv, lp.out_ret = out.data_ptr(), out_adv.data_ptr(), out_ret.data_ptr()
+    comp, exp = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    ms, log = cd.conduit_run_onpolicy(buf.handle, lp, comp, exp)
+    assert ms > 0
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+    out_h, adv_h, ret_h = host(out), host(out_adv), host(out_ret)
+    for i in range(iters):
+        oa, orr = oracle.gae(rew[i].reshape(T, E), val[i].reshape(T, E), done[i].reshape(T, E), boot[i], gamma, lam)
+        want = oracle.rows(obs[i], perm[i], oracle.XF_U8_F32)
+        assert np.array_equal(out_h[i].view(np.uint32), want.view(np.uint32)), i
+        assert_gae_close(adv_h[i], oa.reshape(-1)[perm[i]])
+        assert_gae_close(ret_h[i], orr.reshape(-1)[perm[i]])
+    # the rollout left in the buffer is the last iteration's
+    assert np.array_equal(read_col(buf, cd.COL_OBS, obs[-1].nbytes, np.uint8), obs[-1].reshape(-1))
+    buf.close()
+    return log
+
+
+@pytest.mark.parametrize("mode", [(0, 4, 0), (1, 1, 1), (1, 3, 0), (0, 2, 1), (1, 4, 1), (0, 1, 0)])
+def test_onpolicy_loop_matches_oracle_in_every_mode(mode):
+    print(f"onpolicy loop mode {mode}", flush=True)
+    M, iters = 4, 3
+    log = _onpolicy(mode, iters=iters, M=M)
+    j = mode[1]
+    want_ing = []
+    first = 0
+    for s in range(M):
+        if s + 1 - first == j or s == M - 1:
+            want_ing.append((first, s + 1 - first))
+            first = s + 1
+    for i in range(iters):
+        ops = [op for op in log if op[1] == i]
+        assert [(op[2], op[3]) for op in ops if op[0] == cd.OP_INGEST] == want_ing
+        kinds = [op[0] for op in ops]
+        # program order: the rollout's ingestions, its GAE, its minibatches in order
+        assert kinds == [cd.OP_INGEST] * len(want_ing) + [cd.OP_GAE] + [cd.OP_DELIVER] * M
+        assert [op[2] for op in ops if op[0] == cd.OP_DELIVER] == list(range(M))
+
+
+def test_onpolicy_loop_rejects_bad_configurations():
+    buf = cd.ReplayBuffer(64, (4,), torch.uint8, prioritized=False, action_bytes=0)
+    lp = cd.OnpolicyLoop()
+    lp.overlap_ing, lp.ing_slices, lp.overlap_del, lp.minibatches = 0, 1, 0, 3
+    lp.iters, lp.steps, lp.envs = 1, 8, 8  # steps not a multiple of minibatches
+    with pytest.raises(cd.ConduitError) as e:
+        cd.conduit_run_onpolicy(buf.handle, lp, None, None)
+    assert e.value.status == cd.EINVAL
+    buf.close()

@@ -86,6 +86,54 @@ def test_mode_count_order_and_ties():
     assert k == 0  # every mode costs 2.0: the first wins
 
 
+def test_on_policy_whole_rollout_overlap_hides_nothing():
+    # on-policy the g = 1 ingestion is the iteration's last invocation: overlap
+    # only adds the synchronisation (off-policy the same g hides fully)
+    on = osch.modes(100.0, 200.0, [1.0], [40.0], [1.0], [30.0], 3.0, 4.0, on_policy=True)
+    off = osch.modes(100.0, 200.0, [1.0], [40.0], [1.0], [30.0], 3.0, 4.0)
+    seq_on = next(m for m in on if m["overlap_ing"] == 0 and m["overlap_del"] == 0)
+    ov_on = next(m for m in on if m["overlap_ing"] == 1 and m["overlap_del"] == 1)
+    assert ov_on["t_ing_path"] == pytest.approx(seq_on["t_ing_path"] + 3.0)
+    assert ov_on["t_del_path"] == pytest.approx(seq_on["t_del_path"] + 4.0)
+    ov_off = next(m for m in off if m["overlap_ing"] == 1 and m["overlap_del"] == 1)
+    assert ov_off["t_ing_path"] == pytest.approx(100.0 + 3.0)
+
+
+@pytest.mark.parametrize("M", [2, 4, 8])
+def test_on_policy_fraction_matches_off_policy_below_one(M):
+    # below g = 1 the two regimes share App. E's fractional case
+    gs = [j / M for j in range(1, M)]
+    ts = [5.0 * j for j in range(1, M)]
+    on = osch.modes(100.0, 150.0, gs, ts, [1 / M], [7.0], 2.0, 2.0, on_policy=True)
+    off = osch.modes(100.0, 150.0, gs, ts, [1 / M], [7.0], 2.0, 2.0)
+    for a, b in zip(on, off):
+        assert a["t_iter"] == pytest.approx(b["t_iter"])
+
+
+def test_candidate_sets():
+    assert osch.candidates(False, g_max_ing=4, g_max_del=3) == ([1, 2, 3, 4], [1, 2, 3])
+    gi, gd = osch.candidates(True, minibatches=4)
+    assert gi == [0.25, 0.5, 0.75, 1.0] and gd == [0.25]
+    for on, kw in [(False, dict(g_max_ing=8, g_max_del=2)), (True, dict(minibatches=32)), (True, dict(minibatches=1))]:
+        lg = cd.conduit_sched_candidates(on, **kw)
+        og = osch.candidates(on, **kw)
+        assert [list(x) for x in lg] == [list(map(float, x)) for x in og]
+
+
+def test_candidate_and_on_policy_errors():
+    L = cd.lib()
+    buf = (C.c_double * 4)()
+    n1, n2 = C.c_int32(), C.c_int32()
+    assert L.conduit_sched_candidates(1, 0, 1, 1, buf, 4, C.byref(n1), buf, 4, C.byref(n2)) == cd.EINVAL
+    assert L.conduit_sched_candidates(1, 5, 1, 1, buf, 4, C.byref(n1), buf, 4, C.byref(n2)) == cd.EINVAL
+    assert L.conduit_sched_candidates(0, 1, 0, 1, buf, 4, C.byref(n1), buf, 4, C.byref(n2)) == cd.EINVAL
+    assert L.conduit_sched_candidates(0, 1, 5, 1, buf, 4, C.byref(n1), buf, 4, C.byref(n2)) == cd.EINVAL
+    assert L.conduit_sched_candidates(0, 1, 1, 1, None, 4, C.byref(n1), buf, 4, C.byref(n2)) == cd.EINVAL
+    with pytest.raises(cd.ConduitError) as e:
+        cd.conduit_schedule(1.0, 1.0, [2.0], [1.0], [0.5], [1.0], on_policy=True)  # g > 1 on-policy
+    assert e.value.status == cd.EINVAL
+
+
 # ----------------------------------------------------------------------------
 # the library against the oracle
 # ----------------------------------------------------------------------------
@@ -101,12 +149,22 @@ def _random_case(rng):
             float(rng.random() * 50), float(rng.random() * 50))
 
 
-def test_library_matches_oracle_on_random_cost_sets():
-    rng = np.random.default_rng(17)
+def _random_on_policy_case(rng):
+    M = int(rng.integers(1, 17))
+    g_i, g_d = osch.candidates(True, minibatches=M)
+    t_i = (rng.random(len(g_i)) * 400).tolist()
+    t_d = (rng.random(len(g_d)) * 400).tolist()
+    return (float(rng.random() * 500), float(rng.random() * 500), g_i, t_i, g_d, t_d,
+            float(rng.random() * 50), float(rng.random() * 50))
+
+
+@pytest.mark.parametrize("on_policy", [False, True])
+def test_library_matches_oracle_on_random_cost_sets(on_policy):
+    rng = np.random.default_rng(17 + on_policy)
     for _ in range(2000):
-        case = _random_case(rng)
-        k, oms = osch.best(*case)
-        best, lms = cd.conduit_schedule(*case)
+        case = _random_on_policy_case(rng) if on_policy else _random_case(rng)
+        k, oms = osch.best(*case, on_policy=on_policy)
+        best, lms = cd.conduit_schedule(*case, on_policy=on_policy)
         assert len(lms) == len(oms)
         for lm, om in zip(lms, oms):
             for f in ("overlap_ing", "overlap_del", "i_ing", "i_del"):
@@ -143,3 +201,5 @@ def test_loop_entry_points_reject_bad_arguments_on_the_host():
     ms = C.c_double()
     lp = cd.OffpolicyLoop()
     assert L.conduit_run_offpolicy(None, C.byref(lp), None, None, C.byref(ms), None, None) == cd.EINVAL
+    op = cd.OnpolicyLoop()
+    assert L.conduit_run_onpolicy(None, C.byref(op), None, None, C.byref(ms), None, None) == cd.EINVAL
