@@ -813,6 +813,106 @@ def bench_schedule_onpolicy(T=256, E=64, M=8, iters=8, t_stage_us=(600.0, 800.0)
     return out_d
 
 
+def bench_placement(cap=200_000, steps=20):
+    """Capacity-constrained, bandwidth-aware placement on one GPU host (Sec. 5):
+    the profiled effective bandwidth of each leg and the memory of each tier
+    (conduit_placement_profile), Alg. 1's choice (conduit_place) for the
+    workload shapes of this repository, and a check of the model's ranking:
+    the DQN step (ingest 512 frames, fused sample + frame-stack gather 512,
+    priority update 512) on a buffer of `cap` frames with the frames in HBM and
+    in pinned host memory, the same kernels in both."""
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    prof = cd.conduit_placement_profile(256 << 20, 3)
+    names = cd.PLACEMENT_NAMES
+    meta = 4 + 4 + 1 + 4 + 4 + 4  # action, reward, done, episode id, step, priority leaf
+    shapes = {
+        "dqn 1M frames 84x84 u8": (1_000_000, 84 * 84 + meta),
+        "ppo rollout 2048x256 of 3x84x84 u8": (2048 * 256, 3 * 84 * 84 + 9),
+        "large 200k of 3x224x224 u8": (200_000, 3 * 224 * 224 + 24 + meta),
+        "tokens 64k of up to 4096 (int32 token + fp32 logprob)": (65536, 4096 * 8 + 4 + meta),
+        "stress d=20000, 10^6": (1_000_000, 2 * 20000 * 4 + meta),
+        "stress d=20000, 1.95x10^6": (1_950_000, 2 * 20000 * 4 + meta),
+        "stress d=20000, 2x10^6": (2_000_000, 2 * 20000 * 4 + meta),
+        "stress d=20000, 10^7": (10_000_000, 2 * 20000 * 4 + meta),
+    }
+    decisions = {}
+    for wl, (c, x) in shapes.items():
+        decisions[wl] = {"bytes": c * x}
+        for actor, who in ((1, "gpu_actor"), (0, "cpu_actor")):
+            choice, t = cd.conduit_place(prof, actor, c, x)
+            decisions[wl][who] = {"choice": names[choice] if choice >= 0 else None,
+                                  "t_transfer_us": {names[i]: t[i] * 1e6 for i in range(3)}}
+    # the DQN step with the frames in each executable tier
+    B, K = 512, 4
+    cfg = synth.DQN(cap + (steps + 2) * B)
+    u, prio = cfg.draws(steps + 2, B)
+    u_d, prio_d = _dev(u), _dev(prio)
+    frames = cfg.frames(cap, (steps + 2) * B, "cuda")
+    sl = slice(cap, cap + (steps + 2) * B)
+    act, rew, done = _dev(cfg.action[sl]), _dev(cfg.reward[sl]), _dev(cfg.done[sl])
+    epi, stp = _dev(cfg.episode[sl]), _dev(cfg.step[sl])
+    idx = torch.empty((steps + 2, B), dtype=torch.int64, device="cuda")
+    w = torch.empty((steps + 2, B), dtype=torch.float32, device="cuda")
+    obs_out = torch.empty((B, K, 84, 84), dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_U8_F32)
+    lb = cd.LearnerBatch()
+    lb.obs = obs_out.data_ptr()
+    measured = {}
+    for pl in (cd.PLACE_HBM, cd.PLACE_HOST_PINNED):
+        buf = cd.ReplayBuffer(cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4, placement=pl)
+        for a in range(0, cap, 8192):
+            b = min(cap, a + 8192)
+            buf.ingest(cfg.frames(a, b - a, "cuda"), action=_dev(cfg.action[a:b]), reward=_dev(cfg.reward[a:b]),
+                       done=_dev(cfg.done[a:b]), episode_id=_dev(cfg.episode[a:b]), step=_dev(cfg.step[a:b]),
+                       prio=_dev(cfg.prio[a:b]))
+        torch.cuda.synchronize()
+        h = C.c_void_p(buf.handle)
+        trans = []
+        for i in range(steps + 2):
+            t = cd.Transitions()
+            r = slice(i * B, (i + 1) * B)
+            t.n, t.obs = B, frames[r].data_ptr()
+            t.action, t.reward, t.done = act[r].data_ptr(), rew[r].data_ptr(), done[r].data_ptr()
+            t.episode_id, t.step = epi[r].data_ptr(), stp[r].data_ptr()
+            trans.append(t)
+        ing = [lambda i=i: L.conduit_ingest(h, C.byref(trans[i]), stream) for i in range(steps + 2)]
+        sg = [lambda i=i: L.conduit_sample_gather(h, B, u_d[i].data_ptr(), idx[i].data_ptr(), w[i].data_ptr(),
+                                                  C.byref(xf), C.byref(lb), stream) for i in range(steps + 2)]
+        up = [lambda i=i: L.conduit_update_priorities(h, idx[i].data_ptr(), prio_d[i].data_ptr(), B, stream)
+              for i in range(steps + 2)]
+        step = [lambda i=i: ing[i]() | sg[i]() | up[i]() for i in range(steps + 2)]
+        step[0]()
+        step[1]()
+        step_ms = _b2b_ms(step[2:])
+        ing_ms = _b2b_ms(ing[2:])
+        sg_ms = _b2b_ms(sg[2:])
+        assert buf.sync_check() == cd.OK, cd.last_error()
+        buf.close()
+        link_in = B * 84 * 84  # frame bytes an ingestion writes into the tier
+        link_out = B * K * 84 * 84  # frame bytes a delivery reads from it
+        # the transfer model's two legs for one step (Sec. 5.1, GPU actor)
+        pred_us = (link_in / prof.bw_in[1][pl] + link_out / prof.bw_out[pl]) * 1e6
+        measured[names[pl]] = {"step_us": step_ms * 1e3, "ingest_us": ing_ms * 1e3, "sample_gather_us": sg_ms * 1e3,
+                               "ingest_tier_GBps": link_in / ing_ms / 1e6,
+                               "delivery_tier_GBps": link_out / sg_ms / 1e6,
+                               "model_transfer_us": pred_us}
+    ranking_holds = measured["hbm"]["step_us"] < measured["host_pinned"]["step_us"]
+    return {
+        "profile_GBps": {"bw_in_gpu_actor": dict(zip(names, (v / 1e9 for v in prof.bw_in[1]))),
+                         "bw_in_cpu_actor": dict(zip(names, (v / 1e9 for v in prof.bw_in[0]))),
+                         "bw_out": dict(zip(names, (v / 1e9 for v in prof.bw_out)))},
+        "mem_GB": dict(zip(names, (v / 1e9 for v in prof.mem))),
+        "alg1": decisions,
+        "dqn_step_by_tier": {"capacity": cap, "batch": B, **measured,
+                             "model_ranking_holds": bool(ranking_holds)},
+    }
+
+
 def bench_tiny(iters=100):
     """Tiny replay (16,384 slots of 8 fp32): 100 x [ingest 64, sample + gather 256
     with IS weights (one launch), update 256], every call's arguments prepared
@@ -965,7 +1065,7 @@ def _traffic_from_profile():
 
 ROWS = {"tiny": lambda: bench_tiny(), "ppo": lambda: bench_ppo(), "large": lambda: bench_large(),
         "tokens": lambda: bench_tokens(), "stress": lambda: bench_stress(), "schedule": lambda: bench_schedule(),
-        "schedule_onpolicy": lambda: bench_schedule_onpolicy()}
+        "schedule_onpolicy": lambda: bench_schedule_onpolicy(), "placement": lambda: bench_placement()}
 
 
 def main():
@@ -1027,7 +1127,7 @@ def main():
     }
     if not args.no_rows:
         only = set(x for x in args.only.split(",") if x) or set(ROWS)
-        for name in ("tiny", "ppo", "large", "tokens", "stress", "schedule", "schedule_onpolicy"):
+        for name in ("tiny", "ppo", "large", "tokens", "stress", "schedule", "schedule_onpolicy", "placement"):
             if name in only:
                 print(f"bench.py: row {name} ...", file=sys.stderr, flush=True)
                 out["rows"][name] = ROWS[name]()

@@ -89,7 +89,22 @@ typedef struct {
     int32_t ragged;
     /* ragged: bytes of the auxiliary per-element value, 0 or 4.  Default 0. */
     int32_t aux_elem_bytes;
+    /* Where the payload (the observation column, and the auxiliary column of
+     * a ragged buffer) lives (Sec. 5 placement): CONDUIT_PLACE_HBM (default)
+     * or CONDUIT_PLACE_HOST_PINNED -- pinned host memory that the same kernels
+     * read and write across the host link.  Metadata, priorities and the tree
+     * stay in HBM either way.  CONDUIT_PLACE_HOST_PAGEABLE is a candidate of
+     * conduit_place only: kernels cannot address pageable memory. */
+    int32_t payload_placement;
 } conduit_buffer_opts;
+
+/* Experience-buffer placements on one GPU host (Sec. 5.1): the memory tier of
+ * the payload.  (The paper's fourth candidate, a buffer sharded over several
+ * GPUs, needs more than one GPU.) */
+#define CONDUIT_PLACE_HBM 0
+#define CONDUIT_PLACE_HOST_PINNED 1
+#define CONDUIT_PLACE_HOST_PAGEABLE 2
+#define CONDUIT_PLACEMENTS 3
 
 void conduit_buffer_opts_default(conduit_buffer_opts* opts);
 
@@ -98,8 +113,9 @@ void conduit_buffer_opts_default(conduit_buffer_opts* opts);
  * ------------------------------------------------------------------------- */
 /*
  * Bytes of device memory a buffer with these parameters needs (all columns,
- * the priority tree and small state), rounded to 256-byte alignment.
- * Returns 0 for invalid parameters.  Host-only; allocates nothing.
+ * the priority tree and small state, without a payload placed in host memory),
+ * rounded to 256-byte alignment.  Returns 0 for invalid parameters.
+ * Host-only; allocates nothing.
  */
 size_t conduit_buffer_required_bytes(int64_t capacity, const int64_t* obs_shape, int32_t ndim,
                                      conduit_dtype obs_dtype, const conduit_buffer_opts* opts);
@@ -117,12 +133,14 @@ size_t conduit_buffer_required_bytes(int64_t capacity, const int64_t* obs_shape,
  *   arena      NULL: the library allocates the memory (hipMalloc) and frees it in
  *              conduit_buffer_destroy.  Otherwise device memory of at least
  *              conduit_buffer_required_bytes() bytes, 256-byte aligned, owned by
- *              the caller and kept alive until destroy.
+ *              the caller and kept alive until destroy.  A payload placed in
+ *              pinned host memory is always allocated by the library
+ *              (hipHostMalloc, coherent) and freed by destroy.
  *   out        host pointer receiving the handle.
  * The buffer is bound to the device current at creation.  Slots start empty;
  * every tree node and leaf starts at 0; the running maximum priority starts at 1.
- * Errors: EINVAL (bad sizes/options, arena too small or misaligned), ENOMEM,
- * EDEVICE.  Synchronous.
+ * Errors: EINVAL (bad sizes/options, a pageable or unknown payload placement,
+ * arena too small or misaligned), ENOMEM, EDEVICE.  Synchronous.
  */
 conduit_status conduit_buffer_create(int64_t capacity, const int64_t* obs_shape, int32_t ndim,
                                      conduit_dtype obs_dtype, const conduit_buffer_opts* opts,
@@ -394,6 +412,59 @@ const char* conduit_last_error(void);
 
 /* Library version string. */
 const char* conduit_version(void);
+
+/* ---------------------------------------------------------------------------
+ * Placement (Sec. 5: capacity-constrained, bandwidth-aware experience data
+ * placement, restricted to the tiers of one GPU host)
+ * ------------------------------------------------------------------------- */
+/*
+ * Profiled transfer model inputs (Sec. 5.1-5.2), indexed by placement
+ * CONDUIT_PLACE_*:
+ *   bw_in[a][p]  effective bytes/s of the ingestion leg, actor -> buffer at p,
+ *                for an actor on the CPU (a = 0, rollouts in pageable memory)
+ *                or on the GPU (a = 1, rollouts in HBM);
+ *   bw_out[p]    effective bytes/s of the delivery leg, buffer at p -> the
+ *                learner's GPU;
+ *   mem[p]       bytes available at p (free HBM; available host memory for
+ *                both host tiers).
+ */
+typedef struct conduit_place_profile {
+    double bw_in[2][CONDUIT_PLACEMENTS];
+    double bw_out[CONDUIT_PLACEMENTS];
+    double mem[CONDUIT_PLACEMENTS];
+} conduit_place_profile;
+
+/*
+ * Measures a conduit_place_profile on the current device with microbenchmarks
+ * of each leg (Sec. 5.1: effective bandwidth from microbenchmarks on the
+ * deployment stack): copies of `bytes` bytes (>= 1 MiB) between HBM, pinned
+ * host memory (hipHostMalloc) and pageable host memory (malloc), device-side
+ * legs with hipMemcpyAsync on a private stream timed by events, host-side legs
+ * (CPU actor into a host tier) with memcpy timed by the host clock, each the
+ * best of `reps` (>= 1) after a warm-up; legs through pageable memory, which
+ * the runtime stages on the host's time, are timed by the host clock.
+ * Allocates and frees 3 x bytes of host and 2 x bytes of device memory.
+ * Synchronous.
+ * Errors: EINVAL (NULL out, bytes < 1 MiB, reps < 1), ENOMEM, EDEVICE.
+ */
+conduit_status conduit_placement_profile(int64_t bytes, int32_t reps, conduit_place_profile* out);
+
+/*
+ * Alg. 1 (bandwidth-aware placement, linear scan) over the candidates
+ * candidates[0..n) (CONDUIT_PLACE_* values, scanned in that order): a
+ * candidate p is feasible if capacity * sample_bytes <= mem[p]; its latency is
+ *   T_transfer(p) = x / bw_in[actor_on_gpu][p] + x / bw_out[p]   (seconds)
+ * with x = sample_bytes; the first feasible candidate of least T_transfer wins.
+ * *choice receives its placement, or -1 if none is feasible.  t_transfer
+ * (host [n] or NULL) receives each candidate's T_transfer (also for
+ * infeasible ones).  Host-only.
+ * Errors: EINVAL (NULL profile/candidates/choice, n < 1, an unknown
+ * placement, actor_on_gpu not 0/1, capacity < 0, sample_bytes not > 0, a
+ * bandwidth not > 0 for a scanned candidate).
+ */
+conduit_status conduit_place(const conduit_place_profile* profile, int32_t actor_on_gpu, int64_t capacity,
+                             double sample_bytes, const int32_t* candidates, int32_t n, int32_t* choice,
+                             double* t_transfer);
 
 /* ---------------------------------------------------------------------------
  * Latency-aware scheduling of ingestion and delivery (Sec. 6: timing

@@ -35,7 +35,7 @@ class ConduitError(RuntimeError):
 class BufferOpts(C.Structure):
     _fields_ = [("prioritized", C.c_int32), ("alpha_num", C.c_int32), ("alpha_den", C.c_int32),
                 ("beta", C.c_double), ("frame_stack", C.c_int32), ("action_bytes", C.c_int32),
-                ("ragged", C.c_int32), ("aux_elem_bytes", C.c_int32)]
+                ("ragged", C.c_int32), ("aux_elem_bytes", C.c_int32), ("payload_placement", C.c_int32)]
 
 
 class Transitions(C.Structure):
@@ -89,6 +89,18 @@ class OnpolicyLoop(C.Structure):
                 ("out_adv", C.c_void_p), ("out_ret", C.c_void_p)]
 
 
+PLACE_HBM, PLACE_HOST_PINNED, PLACE_HOST_PAGEABLE = 0, 1, 2
+PLACEMENT_NAMES = ("hbm", "host_pinned", "host_pageable")
+
+
+class PlaceProfile(C.Structure):
+    _fields_ = [("bw_in", (C.c_double * 3) * 2), ("bw_out", C.c_double * 3), ("mem", C.c_double * 3)]
+
+    def as_dict(self):
+        return {"bw_in_cpu_actor": list(self.bw_in[0]), "bw_in_gpu_actor": list(self.bw_in[1]),
+                "bw_out": list(self.bw_out), "mem": list(self.mem)}
+
+
 class BufferInfo(C.Structure):
     _fields_ = [("capacity", C.c_int64), ("row_bytes", C.c_int64), ("head", C.c_int64), ("size", C.c_int64),
                 ("total", C.c_int64), ("tree_depth", C.c_int32), ("tree_nodes", C.c_int64 * 8),
@@ -125,6 +137,8 @@ SIGNATURES = {
     "conduit_sync_cost_us": (ST, [P, P, I32_, P, P]),
     "conduit_sched_candidates": (ST, [I32_, I32_, I32_, I32_, P, I32_, P, P, I32_, P]),
     "conduit_run_onpolicy": (ST, [P, P, P, P, P, P, P]),
+    "conduit_placement_profile": (ST, [I64, I32_, P]),
+    "conduit_place": (ST, [P, I32_, I64, F64, P, I32_, P, P]),
     "conduit_run_offpolicy": (ST, [P, P, P, P, P, P, P]),
 }
 
@@ -349,6 +363,24 @@ def conduit_run_onpolicy(handle, loop, compute_stream, experience_stream):
     return ms.value, [tuple(log[4 * i:4 * i + 4]) for i in range(min(n.value, cap))]
 
 
+def conduit_placement_profile(nbytes=256 << 20, reps=3):
+    """Sec. 5.1 microbenchmarks: a PlaceProfile of this host and GPU."""
+    prof = PlaceProfile()
+    _check(lib().conduit_placement_profile(int(nbytes), int(reps), C.byref(prof)))
+    return prof
+
+
+def conduit_place(profile, actor_on_gpu, capacity, sample_bytes, candidates=(0, 1, 2)):
+    """Alg. 1: (chosen placement or -1, T_transfer per candidate in seconds)."""
+    n = len(candidates)
+    cand = (C.c_int32 * max(1, n))(*candidates)
+    t = (C.c_double * max(1, n))()
+    choice = C.c_int32(-2)
+    _check(lib().conduit_place(C.byref(profile), int(actor_on_gpu), int(capacity), float(sample_bytes), cand, n,
+                               C.byref(choice), t))
+    return choice.value, [t[i] for i in range(n)]
+
+
 def conduit_standin(work, stream=None):
     _check(lib().conduit_standin(int(work), _stream(stream)))
 
@@ -398,10 +430,10 @@ class ReplayBuffer:
     """Owning wrapper around a conduit_buffer handle."""
 
     def __init__(self, capacity, obs_shape, obs_dtype=torch.uint8, prioritized=True, alpha=(3, 5), beta=0.4,
-                 frame_stack=1, action_bytes=4, ragged=False, aux_elem_bytes=0, arena=None):
+                 frame_stack=1, action_bytes=4, ragged=False, aux_elem_bytes=0, arena=None, placement=PLACE_HBM):
         self.opts = default_opts(prioritized=int(prioritized), alpha_num=alpha[0], alpha_den=alpha[1], beta=beta,
                                  frame_stack=frame_stack, action_bytes=action_bytes, ragged=int(ragged),
-                                 aux_elem_bytes=aux_elem_bytes)
+                                 aux_elem_bytes=aux_elem_bytes, payload_placement=int(placement))
         self.capacity = capacity
         self.obs_shape = tuple(obs_shape)
         self.obs_dtype = obs_dtype

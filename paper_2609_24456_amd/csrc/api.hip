@@ -151,6 +151,9 @@ struct Layout {
     size_t off_state = 0, off_obs = 0, off_aux = 0, off_action = 0, off_reward = 0, off_done = 0;
     size_t off_episode = 0, off_step = 0, off_length = 0, off_leaves = 0, off_level[kMaxLevels + 1] = {};
     size_t total = 0;
+    // payload in pinned host memory: observation then auxiliary column
+    bool host_payload = false;
+    size_t host_obs = 0, host_aux = 0;
 };
 
 conduit_status make_layout(int64_t capacity, const int64_t* shape, int32_t ndim, conduit_dtype dt,
@@ -183,6 +186,10 @@ conduit_status make_layout(int64_t capacity, const int64_t* shape, int32_t ndim,
     } else if (o.aux_elem_bytes != 0) {
         return fail(CONDUIT_EINVAL, "aux_elem_bytes needs a ragged buffer");
     }
+    if (o.payload_placement == CONDUIT_PLACE_HOST_PAGEABLE)
+        return fail(CONDUIT_EINVAL, "kernels cannot address pageable memory: place the payload in HBM or pinned host memory");
+    if (o.payload_placement != CONDUIT_PLACE_HBM && o.payload_placement != CONDUIT_PLACE_HOST_PINNED)
+        return fail(CONDUIT_EINVAL, "unknown payload placement");
     // tree shape
     L->nodes[0] = capacity;
     int d = 0;
@@ -199,9 +206,17 @@ conduit_status make_layout(int64_t capacity, const int64_t* shape, int32_t ndim,
         return at;
     };
     const size_t C = (size_t)capacity;
+    const size_t obs_bytes = C * (size_t)L->row_bytes;
+    const size_t aux_bytes = o.ragged && o.aux_elem_bytes ? C * (size_t)L->max_len * (size_t)o.aux_elem_bytes : 0;
     L->off_state = take(sizeof(DeviceState));
-    L->off_obs = take(C * (size_t)L->row_bytes);
-    L->off_aux = o.ragged && o.aux_elem_bytes ? take(C * (size_t)L->max_len * (size_t)o.aux_elem_bytes) : 0;
+    L->host_payload = o.payload_placement == CONDUIT_PLACE_HOST_PINNED;
+    if (L->host_payload) {
+        L->host_obs = align_up(obs_bytes);
+        L->host_aux = align_up(aux_bytes);
+    } else {
+        L->off_obs = take(obs_bytes);
+        L->off_aux = aux_bytes ? take(aux_bytes) : 0;
+    }
     L->off_action = o.action_bytes ? take(C * (size_t)o.action_bytes) : 0;
     L->off_reward = take(C * 4);
     L->off_done = take(C);
@@ -226,6 +241,7 @@ struct conduit_buffer {
     Layout layout;
     uint8_t* arena = nullptr;
     bool owns_arena = false;
+    uint8_t* host_payload = nullptr;  // pinned host allocation of a host-placed payload
     uint8_t* obs = nullptr;
     uint8_t* aux = nullptr;
     uint8_t* action = nullptr;
@@ -265,6 +281,7 @@ void conduit_buffer_opts_default(conduit_buffer_opts* o) {
     o->action_bytes = 4;
     o->ragged = 0;
     o->aux_elem_bytes = 0;
+    o->payload_placement = CONDUIT_PLACE_HBM;
 }
 
 const char* conduit_last_error(void) { return g_last_error.c_str(); }
@@ -323,8 +340,32 @@ conduit_status conduit_buffer_create(int64_t capacity, const int64_t* obs_shape,
     }
     uint8_t* A = b->arena;
     b->state = reinterpret_cast<DeviceState*>(A + L.off_state);
-    b->obs = A + L.off_obs;
-    b->aux = (o.ragged && o.aux_elem_bytes) ? A + L.off_aux : nullptr;
+    if (L.host_payload) {
+        // coherent pinned host memory mapped into the device's address space:
+        // the kernels reach it across the host link, uncached in the L2s, so
+        // no XCD ever holds a stale line of it
+        void* hp = nullptr;
+        hipError_t e = hipHostMalloc(&hp, L.host_obs + L.host_aux, hipHostMallocMapped | hipHostMallocCoherent);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            conduit_buffer_destroy(b);
+            return fail(CONDUIT_ENOMEM, std::string("hipHostMalloc of ") + std::to_string(L.host_obs + L.host_aux) +
+                                            " bytes failed");
+        }
+        b->host_payload = static_cast<uint8_t*>(hp);
+        void* dp = nullptr;
+        e = hipHostGetDevicePointer(&dp, hp, 0);
+        if (e != hipSuccess) {
+            conduit_status r = hip_fail(e, "hipHostGetDevicePointer");
+            conduit_buffer_destroy(b);
+            return r;
+        }
+        b->obs = static_cast<uint8_t*>(dp);
+        b->aux = (o.ragged && o.aux_elem_bytes) ? b->obs + L.host_obs : nullptr;
+    } else {
+        b->obs = A + L.off_obs;
+        b->aux = (o.ragged && o.aux_elem_bytes) ? A + L.off_aux : nullptr;
+    }
     b->action = o.action_bytes ? A + L.off_action : nullptr;
     b->reward = reinterpret_cast<float*>(A + L.off_reward);
     b->done = A + L.off_done;
@@ -381,6 +422,7 @@ void conduit_buffer_destroy(conduit_buffer* b) {
         DeviceGuard g(b->device);
         (void)hipDeviceSynchronize();
         if (b->owns_arena && b->arena) (void)hipFree(b->arena);
+        if (b->host_payload) (void)hipHostFree(b->host_payload);
     }
     err_slot_release(b->err_slot);
     delete b;
@@ -758,7 +800,7 @@ conduit_status conduit_buffer_read(const conduit_buffer* b, conduit_column col, 
     if (!base || offset < 0 || nbytes < 0 || offset + nbytes > bytes) return fail(CONDUIT_EINVAL, "range outside the column");
     if (nbytes == 0) return CONDUIT_OK;
     DeviceGuard g(b->device);
-    hipError_t e = hipMemcpyAsync(dst, base + offset, (size_t)nbytes, hipMemcpyDeviceToDevice,
+    hipError_t e = hipMemcpyAsync(dst, base + offset, (size_t)nbytes, hipMemcpyDefault,
                                   static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "column copy");
     return CONDUIT_OK;

@@ -117,7 +117,7 @@ def test_struct_layouts_match_header(tmp_path):
                "conduit_transform": cd.Transform, "conduit_learner_batch": cd.LearnerBatch,
                "conduit_buffer_info": cd.BufferInfo, "conduit_sched_costs": cd.SchedCosts,
                "conduit_sched_mode": cd.SchedMode, "conduit_offpolicy_loop": cd.OffpolicyLoop,
-               "conduit_onpolicy_loop": cd.OnpolicyLoop}
+               "conduit_onpolicy_loop": cd.OnpolicyLoop, "conduit_place_profile": cd.PlaceProfile}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "conduit.h"', "int main(void) {"]
     for cname, py in structs.items():
         lines.append(f'printf("{cname} %zu\\n", sizeof({cname}));')

@@ -70,10 +70,11 @@ def test_large_payload_full_size():
               check_rows=np.random.default_rng(0).choice(1024, 24, replace=False))
 
 
-def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values, fused=False):
+def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values, fused=False, placement=cd.PLACE_HBM):
     cfg = synth.Tokens(prefill, max_len=max_len, min_len=min_len)
     u, prio = cfg.draws(iters, batch)
-    buf = cd.ReplayBuffer(cap, (max_len,), torch.int32, action_bytes=4, ragged=True, aux_elem_bytes=4)
+    buf = cd.ReplayBuffer(cap, (max_len,), torch.int32, action_bytes=4, ragged=True, aux_elem_bytes=4,
+                          placement=placement)
     store = np.zeros((cap, max_len * 4), np.uint8)
     aux_store = np.zeros((cap, max_len * 4), np.uint8)
     orc = oracle.Replay(cap, (max_len,), np.int32, act_bytes=4, ragged=True, aux_dtype=np.float32,
@@ -137,6 +138,14 @@ def test_tokens_reduced(fused):
     print(f"tokens: cap 300, max_len 256, prefill 400 (wraps), batch 64, fused={fused}", flush=True)
     run_tokens(cap=300, max_len=256, min_len=8, prefill=400, iters=3, batch=64, chunk=128, with_values=True,
                fused=fused)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_tokens_payload_in_pinned_host_memory(fused):
+    # token and log-probability columns in pinned host memory (Sec. 5 placement)
+    print(f"tokens: payload in pinned host memory, cap 300, fused={fused}", flush=True)
+    run_tokens(cap=300, max_len=256, min_len=8, prefill=400, iters=3, batch=64, chunk=128, with_values=True,
+               fused=fused, placement=cd.PLACE_HOST_PINNED)
 
 
 def test_tokens_long_rows_segmented_gae():

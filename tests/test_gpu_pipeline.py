@@ -124,7 +124,7 @@ def test_standin_scales_with_work_and_sync_costs_are_finite():
     assert 0.0 <= dep < 1000.0 and 0.0 <= hop < 1000.0, (hop, dep)
 
 
-def _onpolicy(mode, iters=3, T=32, E=16, M=4, shape=(3, 8, 8), work=(4000, 4000)):
+def _onpolicy(mode, iters=3, T=32, E=16, M=4, shape=(3, 8, 8), work=(4000, 4000), placement=cd.PLACE_HBM):
     overlap_ing, ing_slices, overlap_del = mode
     rng = np.random.default_rng(23)
     U = T * E
@@ -135,7 +135,7 @@ def _onpolicy(mode, iters=3, T=32, E=16, M=4, shape=(3, 8, 8), work=(4000, 4000)
     boot = rng.standard_normal((iters, E)).astype(np.float32)
     perm = np.stack([rng.permutation(U) for _ in range(iters)]).astype(np.int64)
     gamma, lam = 0.99, 0.95
-    buf = cd.ReplayBuffer(U, shape, torch.uint8, prioritized=False, action_bytes=0)
+    buf = cd.ReplayBuffer(U, shape, torch.uint8, prioritized=False, action_bytes=0, placement=placement)
     d = {k: dev(v) for k, v in dict(obs=obs, rew=rew, val=val, done=done, boot=boot, perm=perm).items()}
     adv = torch.empty(U, dtype=torch.float32, device="cuda")
     ret = torch.empty(U, dtype=torch.float32, device="cuda")
@@ -191,6 +191,22 @@ def test_onpolicy_loop_matches_oracle_in_every_mode(mode):
         # program order: the rollout's ingestions, its GAE, its minibatches in order
         assert kinds == [cd.OP_INGEST] * len(want_ing) + [cd.OP_GAE] + [cd.OP_DELIVER] * M
         assert [op[2] for op in ops if op[0] == cd.OP_DELIVER] == list(range(M))
+
+
+def test_onpolicy_loop_with_the_rollout_in_pinned_host_memory():
+    print("onpolicy loop: rollout buffer in pinned host memory, mode (1, 2, 1)", flush=True)
+    _onpolicy((1, 2, 1), placement=cd.PLACE_HOST_PINNED)
+
+
+def test_placement_profile_is_sane():
+    prof = cd.conduit_placement_profile(64 << 20, 2)
+    d = prof.as_dict()
+    print("placement profile", d, flush=True)
+    assert all(v > 0 for v in d["bw_in_cpu_actor"] + d["bw_in_gpu_actor"] + d["bw_out"] + d["mem"])
+    # HBM to HBM is the fastest leg of all on any sane host
+    assert d["bw_out"][cd.PLACE_HBM] > d["bw_out"][cd.PLACE_HOST_PINNED]
+    choice, t = cd.conduit_place(prof, 1, 1000, 28224.0)
+    assert choice == cd.PLACE_HBM and t[0] == min(t)
 
 
 def test_onpolicy_loop_rejects_bad_configurations():

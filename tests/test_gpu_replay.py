@@ -53,11 +53,11 @@ def test_leaf_quantiser_matches_oracle(a, b):
 # ----------------------------------------------------------------------------
 # configuration 0: tiny replay, 100 iterations, full parity at every step
 # ----------------------------------------------------------------------------
-def _run_tiny(prefill, iters, seed_shift=0, fused=False):
+def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM):
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
-    buf = _mk(C, (8,), torch.float32, action_bytes=4)
+    buf = _mk(C, (8,), torch.float32, action_bytes=4, placement=placement)
     orc = oracle.Replay(C, (8,), np.float32, act_bytes=4)
 
     def ingest(a, b):
@@ -99,6 +99,10 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False):
     assert int(read_col(buf, cd.COL_MAX_PRIO, 4, np.uint32)[0]) == orc.max_prio
     info = buf.info()
     assert (info.head, info.size, info.total) == (orc.head, orc.size, orc.total)
+    # the payload column itself, wherever it is placed (written slots)
+    written = orc.position >= 0
+    got = read_col(buf, cd.COL_OBS, C * 32, np.uint8).reshape(C, 32)
+    assert np.array_equal(got[written], orc.obs[written])
     buf.close()
 
 
@@ -117,10 +121,19 @@ def test_tiny_config_fused_sample_gather():
     _run_tiny(prefill=0, iters=100, fused=True)
 
 
+@pytest.mark.parametrize("fused", [False, True])
+def test_tiny_config_payload_in_pinned_host_memory(fused):
+    # Sec. 5 placement: the observation column in pinned host memory, reached
+    # by the same kernels across the host link; results identical
+    print(f"tiny config: payload in pinned host memory, fused={fused}", flush=True)
+    _run_tiny(prefill=20000, iters=30, seed_shift=3, fused=fused, placement=cd.PLACE_HOST_PINNED)
+
+
 # ----------------------------------------------------------------------------
 # configuration 1 (DQN, frame stack 4, u8 -> fp32/255) at reduced capacity
 # ----------------------------------------------------------------------------
-def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False):
+def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False,
+            placement=cd.PLACE_HBM):
     """Drive GPU buffer and oracle through the same DQN stream; the oracle keeps
     metadata only and its observation rows are regenerated for the slots a
     gather reads."""
@@ -134,7 +147,7 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
         cfg.drift = rng.integers(1, 4, int(cfg.episode.max()) + 1).astype(np.int64)
     u, prio = cfg.draws(iters, batch)
     K = 4
-    buf = _mk(cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4)
+    buf = _mk(cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4, placement=placement)
     obs_store = np.zeros((cap, 84 * 84), np.uint8)  # untouched pages stay unallocated
     orc = oracle.Replay(cap, (84, 84), np.uint8, act_bytes=4, frame_stack=K, obs_storage=obs_store)
 
@@ -206,6 +219,13 @@ def test_dqn_short_episodes_zero_fill():
 def test_dqn_fused_sample_gather(short):
     print(f"dqn: fused sample+gather, cap 3000, short episodes={short}", flush=True)
     run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused=True)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_dqn_payload_in_pinned_host_memory(fused):
+    print(f"dqn: frames in pinned host memory, cap 3000, short episodes, fused={fused}", flush=True)
+    run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=True, fused=fused,
+            placement=cd.PLACE_HOST_PINNED)
 
 
 @pytest.mark.slow
