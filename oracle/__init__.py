@@ -72,6 +72,8 @@ def _declare(L):
     L.orc_rows.restype = I32
     L.orc_gae.argtypes = [I64, I64, P, P, P, P, F64, F64, P, P]
     L.orc_gae.restype = None
+    L.orc_gae_trunc.argtypes = [I64, I64, P, P, P, P, P, P, F64, F64, P, P]
+    L.orc_gae_trunc.restype = None
     L.orc_gae_packed.argtypes = [I64, I64, P, P, P, F64, F64, P, P]
     L.orc_gae_packed.restype = None
     L.orc_u8_to_f32.argtypes = [C.c_uint8]
@@ -297,8 +299,10 @@ def rows(src, perm, xform=XF_NONE, mean=None, std=None):
     return out.view(src.dtype).reshape((len(perm),) + row_shape)
 
 
-def gae(reward, value, done, bootstrap, gamma, lam):
-    """GAE over a time-major [T, E] rollout (fp64 inside, fp32 out)."""
+def gae(reward, value, done, bootstrap, gamma, lam, truncated=None, final_value=None):
+    """GAE over a time-major [T, E] rollout (fp64 inside, fp32 out).  With
+    ``truncated`` (and ``final_value``), truncated steps end the recursion and
+    bootstrap from the value of their true next observation."""
     r = _c(reward, np.float32)
     T, E = r.shape
     v = _c(value, np.float32)
@@ -306,7 +310,13 @@ def gae(reward, value, done, bootstrap, gamma, lam):
     b = _c(bootstrap, np.float32)
     adv = np.zeros((T, E), np.float32)
     ret = np.zeros((T, E), np.float32)
-    lib().orc_gae(T, E, _ptr(r), _ptr(v), _ptr(d), _ptr(b), float(gamma), float(lam), _ptr(adv), _ptr(ret))
+    if truncated is None:
+        lib().orc_gae(T, E, _ptr(r), _ptr(v), _ptr(d), _ptr(b), float(gamma), float(lam), _ptr(adv), _ptr(ret))
+    else:
+        tr = _c(truncated, np.uint8)
+        fv = _c(final_value, np.float32)
+        lib().orc_gae_trunc(T, E, _ptr(r), _ptr(v), _ptr(d), _ptr(tr), _ptr(fv), _ptr(b), float(gamma), float(lam),
+                            _ptr(adv), _ptr(ret))
     return adv, ret
 
 

@@ -446,6 +446,40 @@ void orc_gae(int64_t T, int64_t E, const float* reward, const float* value, cons
 }
 
 /*
+ * GAE with truncation bootstrap over a time-major [T, E] rollout: a step may end
+ * its episode by termination (done = 1: nothing after it is worth anything) or
+ * by truncation (truncated = 1, e.g. a time limit: the episode would have
+ * continued).  Either end cuts the recursion; a truncated step that did not
+ * also terminate bootstraps from final_value (the critic's value of the true
+ * next observation, which the rollout's next row does not hold):
+ *   live_t  = 1 - max(done_t, truncated_t)
+ *   boot_t  = final_value_t if truncated_t and not done_t, else 0
+ *   delta_t = r_t + gamma (live_t V_{t+1} + boot_t) - V_t
+ *   A_t     = delta_t + gamma lambda live_t A_{t+1},   V_T = bootstrap[e]
+ */
+void orc_gae_trunc(int64_t T, int64_t E, const float* reward, const float* value, const uint8_t* done,
+                   const uint8_t* truncated, const float* final_value, const float* bootstrap, double gamma,
+                   double lambda, float* adv, float* ret) {
+    for (int64_t e = 0; e < E; ++e) {
+        double a_next = 0.0;
+        double v_next = bootstrap ? (double)bootstrap[e] : 0.0;
+        for (int64_t t = T - 1; t >= 0; --t) {
+            int64_t at = t * E + e;
+            double v = value ? (double)value[at] : 0.0;
+            int term = done[at] != 0, trunc = truncated[at] != 0;
+            double live = (term || trunc) ? 0.0 : 1.0;
+            double boot = (trunc && !term) ? (double)final_value[at] : 0.0;
+            double delta = (double)reward[at] + gamma * (live * v_next + boot) - v;
+            double a = delta + gamma * lambda * live * a_next;
+            adv[at] = (float)a;
+            ret[at] = (float)(a + v);
+            a_next = a;
+            v_next = v;
+        }
+    }
+}
+
+/*
  * GAE over right-padded sequences [B, Lmax]: a sequence of length L gets its scalar
  * reward on the last element (t = L-1), which also ends the episode; all other
  * rewards are 0.  values NULL means V = 0.  Positions t >= L are written as 0.

@@ -393,6 +393,60 @@ def test_gae_no_value_no_done_is_lambda_gamma_discounting():
         assert adv[t, 0] == pytest.approx(want, rel=1e-6, abs=1e-6)
 
 
+def test_gae_truncation_lambda_one_is_bootstrapped_return_minus_value():
+    # lambda = 1: A_t = G_t - V_t, G_t summing discounted rewards up to the
+    # first end; a truncation (not a termination) adds gamma^(k-t+1) times the
+    # final value of its true next observation
+    rng = np.random.default_rng(67)
+    T, E, gamma = 40, 5, 0.9
+    r, v, d, b = _rollout(rng, T, E, 0.05)
+    tr = (rng.random((T, E)) < 0.08).astype(np.uint8)
+    fv = rng.standard_normal((T, E)).astype(np.float32)
+    adv, ret = oracle.gae(r, v, d, b, gamma, 1.0, truncated=tr, final_value=fv)
+    for e in range(E):
+        for t in range(T):
+            g, disc, end = 0.0, 1.0, False
+            for k in range(t, T):
+                g += disc * float(r[k, e])
+                disc *= gamma
+                if d[k, e] or tr[k, e]:
+                    end = True
+                    if tr[k, e] and not d[k, e]:
+                        g += disc * float(fv[k, e])
+                    break
+            if not end:
+                g += disc * float(b[e])
+            assert adv[t, e] == pytest.approx(g - float(v[t, e]), rel=1e-5, abs=1e-5)
+            assert ret[t, e] == pytest.approx(g, rel=1e-5, abs=1e-5)
+
+
+def test_gae_truncation_splits_the_rollout():
+    # a rollout truncated at step k with final value f is two rollouts: steps
+    # 0..k bootstrapped from f, and the rest with the rollout's own bootstrap
+    rng = np.random.default_rng(71)
+    T, k, gamma, lam = 30, 11, 0.99, 0.95
+    r, v, d, b = _rollout(rng, T, 1, 0.0)
+    tr = np.zeros((T, 1), np.uint8)
+    tr[k] = 1
+    fv = np.zeros((T, 1), np.float32)
+    fv[k] = 2.5
+    adv, ret = oracle.gae(r, v, d, b, gamma, lam, truncated=tr, final_value=fv)
+    a1, r1 = oracle.gae(r[:k + 1], v[:k + 1], d[:k + 1], np.array([2.5], np.float32), gamma, lam)
+    a2, r2 = oracle.gae(r[k + 1:], v[k + 1:], d[k + 1:], b, gamma, lam)
+    assert np.array_equal(adv, np.concatenate([a1, a2])) and np.array_equal(ret, np.concatenate([r1, r2]))
+
+
+def test_gae_termination_wins_over_truncation_and_none_is_plain_gae():
+    rng = np.random.default_rng(73)
+    r, v, d, b = _rollout(rng, 25, 7, 0.2)
+    fv = rng.standard_normal((25, 7)).astype(np.float32)
+    plain = oracle.gae(r, v, d, b, 0.99, 0.95)
+    both = oracle.gae(r, v, d, b, 0.99, 0.95, truncated=d.copy(), final_value=fv)  # every end both
+    none = oracle.gae(r, v, d, b, 0.99, 0.95, truncated=np.zeros_like(d), final_value=fv)
+    for x in (both, none):
+        assert np.array_equal(x[0], plain[0]) and np.array_equal(x[1], plain[1])
+
+
 def test_gae_packed_closed_form_and_padding():
     rng = np.random.default_rng(59)
     B, Lmax, lam = 6, 50, 0.95
