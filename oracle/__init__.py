@@ -62,7 +62,7 @@ def _declare(L):
     L.orc_ingest.restype = I32
     L.orc_update.argtypes = [P, I64, P, P]
     L.orc_update.restype = I64
-    L.orc_sample.argtypes = [P, I64, P, P, P]
+    L.orc_sample.argtypes = [P, I64, P, P, P, I32]
     L.orc_sample.restype = I32
     L.orc_gather.argtypes = [P, I64, P, I32, P, P, I32, P, P, P, P]
     L.orc_gather.restype = I32
@@ -134,8 +134,9 @@ class Replay:
 
     def __init__(self, capacity, obs_shape, obs_dtype=np.uint8, act_bytes=4, alpha=(3, 5),
                  beta=0.4, frame_stack=1, ragged=False, aux_dtype=None, keep_obs=True,
-                 obs_storage=None):
+                 obs_storage=None, buffer_norm=False):
         obs_dtype = np.dtype(obs_dtype)
+        self.buffer_norm = bool(buffer_norm)
         self.capacity = int(capacity)
         self.obs_shape = tuple(int(s) for s in obs_shape)
         self.obs_dtype = obs_dtype
@@ -223,12 +224,16 @@ class Replay:
         prio = _c(prio, np.uint32)
         return int(lib().orc_update(C.byref(self._s), len(idx), _ptr(idx), _ptr(prio)))
 
-    def sample(self, uniforms):
+    def sample(self, uniforms, buffer_norm=None):
+        """Stratified proportional sampling; IS weights normalised by the batch
+        maximum, or with ``buffer_norm`` (default: the replay's own setting)
+        by the largest weight over the whole buffer."""
         u = _c(uniforms, np.uint64)
         B = len(u)
         idx = np.zeros(B, np.int64)
         w = np.zeros(B, np.float32)
-        rc = lib().orc_sample(C.byref(self._s), B, _ptr(u), _ptr(idx), _ptr(w))
+        bn = self.buffer_norm if buffer_norm is None else buffer_norm
+        rc = lib().orc_sample(C.byref(self._s), B, _ptr(u), _ptr(idx), _ptr(w), int(bool(bn)))
         if rc != 0:
             raise ValueError("oracle: nothing to sample")
         return idx, w

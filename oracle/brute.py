@@ -63,6 +63,15 @@ def is_weights(leaves, size, idx, beta):
     return [x / m for x in w]
 
 
+def is_weights_buffer(leaves, size, idx, beta):
+    """The same weights normalised by the largest weight any stored transition
+    could receive: that of the smallest non-zero leaf of the buffer."""
+    Q = sum(int(q) for q in leaves)
+    qmin = min(int(q) for q in leaves if int(q) > 0)
+    m = float(size * Fraction(qmin, Q)) ** (-beta)
+    return [float(size * Fraction(int(leaves[i]), Q)) ** (-beta) / m for i in idx]
+
+
 def stack_from_stream(stream_eps, stream_frames, capacity, total, pos, K):
     """Frame stack for the transition at stream position ``pos``.
 

@@ -246,14 +246,22 @@ int64_t orc_update(orc_replay* r, int64_t n, const int64_t* idx, const uint32_t*
  * leaves exceeds t_k (half-open intervals: zero leaves are never chosen).
  * Importance weights follow Schaul et al.: w_i = (N * P(i))^-beta with
  * P(i) = q_i / Q and N the number of stored transitions, divided by the largest
- * weight in the batch.  Returns 0, or -1 if nothing can be sampled.
+ * weight in the batch, or (buffer_norm) the largest weight any stored
+ * transition could receive: that of the smallest non-zero leaf in the buffer
+ * (zero leaves are never sampled).  Returns 0, or -1 if nothing can be sampled.
  */
 int32_t orc_sample(const orc_replay* r, int64_t B, const uint64_t* uniforms, int64_t* idx_out,
-                   float* w_out) {
+                   float* w_out, int32_t buffer_norm) {
     uint64_t Q = r->tree[1];
     if (r->size == 0 || Q == 0 || B <= 0) return -1;
     double* w = (double*)malloc(sizeof(double) * (size_t)B);
     double wmax = 0.0;
+    if (buffer_norm) {
+        uint32_t qmin = 0;
+        for (int64_t i = 0; i < r->capacity; ++i)
+            if (r->leaf[i] != 0 && (qmin == 0 || r->leaf[i] < qmin)) qmin = r->leaf[i];
+        wmax = pow((double)r->size * ((double)qmin / (double)Q), -r->beta);
+    }
     for (int64_t k = 0; k < B; ++k) {
         u128 h = ((u128)uniforms[k] * Q) >> 64;
         uint64_t t = (uint64_t)(((u128)k * Q + h) / (u128)B);
@@ -271,7 +279,7 @@ int32_t orc_sample(const orc_replay* r, int64_t B, const uint64_t* uniforms, int
         idx_out[k] = slot;
         double P = (double)r->leaf[slot] / (double)Q;
         w[k] = pow((double)r->size * P, -r->beta);
-        if (w[k] > wmax) wmax = w[k];
+        if (!buffer_norm && w[k] > wmax) wmax = w[k];
     }
     for (int64_t k = 0; k < B; ++k) w_out[k] = (float)(w[k] / wmax);
     free(w);

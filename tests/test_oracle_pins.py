@@ -192,6 +192,38 @@ def test_is_weights_closed_form_and_cases():
             assert np.all(w == 1.0)
 
 
+def test_buffer_wide_is_weights():
+    # normalised by the largest weight any stored transition could get: the
+    # smallest non-zero leaf of the buffer, not of the batch
+    rng = np.random.default_rng(37)
+    prio = rng.integers(1, 10 ** 6, size=300)
+    prio[17] = 0  # a zero priority is never sampled and never the minimum
+    for beta in [0.0, 0.4, 1.0]:
+        r = _filled_replay(prio, alpha=(3, 5), beta=beta)
+        u = rng.integers(0, 1 << 64, size=16, dtype=np.uint64)
+        idx, w_batch = r.sample(u)
+        idx2, w_buf = r.sample(u, buffer_norm=True)
+        assert np.array_equal(idx, idx2)
+        q = r.leaf.astype(np.float64)
+        q_buf, q_bat = q[q > 0].min(), q[idx].min()
+        # the two modes differ by one factor per batch
+        np.testing.assert_allclose(w_buf, (w_batch * (q_buf / q_bat) ** beta).astype(np.float32), rtol=1e-6)
+        np.testing.assert_allclose(w_buf, brute.is_weights_buffer(r.leaf, r.size, idx, beta), rtol=1e-6)
+        assert w_buf.max() <= 1.0
+    # a batch that holds the buffer's smallest leaf: the modes agree exactly
+    # (priorities of one magnitude, so that leaf is drawn often)
+    r = _filled_replay(rng.integers(1000, 2000, size=300), alpha=(3, 5), beta=0.4)
+    qmin_slot = int(np.flatnonzero(r.leaf == r.leaf[r.leaf > 0].min())[0])
+    for _ in range(200):
+        u = rng.integers(0, 1 << 64, size=64, dtype=np.uint64)
+        idx, w_batch = r.sample(u)
+        if qmin_slot in idx:
+            assert np.array_equal(r.sample(u, buffer_norm=True)[1], w_batch)
+            break
+    else:
+        pytest.fail("no batch drew the smallest leaf")
+
+
 # ----------------------------------------------------------------------------
 # Ingest, update semantics
 # ----------------------------------------------------------------------------
