@@ -96,7 +96,16 @@ typedef struct {
      * stay in HBM either way.  CONDUIT_PLACE_HOST_PAGEABLE is a candidate of
      * conduit_place only: kernels cannot address pageable memory. */
     int32_t payload_placement;
+    /* Importance-weight normalisation (Schaul et al.'s w_i / max w):
+     * CONDUIT_WNORM_BATCH (default) divides by the largest weight of the
+     * batch; CONDUIT_WNORM_BUFFER by the largest weight any stored transition
+     * could receive, that of the smallest non-zero leaf of the buffer (the
+     * sampler workgroups reduce the leaves in the same launches). */
+    int32_t weight_norm;
 } conduit_buffer_opts;
+
+#define CONDUIT_WNORM_BATCH 0
+#define CONDUIT_WNORM_BUFFER 1
 
 /* Experience-buffer placements on one GPU host (Sec. 5.1): the memory tier of
  * the payload.  (The paper's fourth candidate, a buffer sharded over several
@@ -320,6 +329,25 @@ conduit_status conduit_sample_gather(conduit_buffer* buf, int64_t batch, const u
 conduit_status conduit_gae(const float* rewards, const float* values, const uint8_t* dones,
                            const float* bootstrap, int64_t T, int64_t E, double gamma, double lambda,
                            float* adv, float* ret, void* stream);
+
+/*
+ * GAE with truncation bootstrap (on-policy ingestion's "boundary detection,
+ * padding/truncation ... computing returns/advantages", Sec. 2.2): as
+ * conduit_gae, and a step may also end by truncation (a time limit: the
+ * episode would have continued).  Either end cuts the recursion; a truncated
+ * step that did not also terminate bootstraps from final_values, the critic's
+ * value of its true next observation:
+ *     live_t  = 1 - max(d_t, u_t)
+ *     delta_t = r_t + gamma (live_t V_{t+1} + [u_t and not d_t] F_t) - V_t
+ *     A_t     = delta_t + gamma lambda live_t A_{t+1}
+ * truncated (u) uint8 [T,E] and final_values (F) float [T,E] device arrays,
+ * both required (F is read only where u_t = 1 and d_t = 0); the rest as in
+ * conduit_gae.  Errors: EINVAL, ESTATE.
+ */
+conduit_status conduit_gae_truncated(const float* rewards, const float* values, const uint8_t* dones,
+                                     const uint8_t* truncated, const float* final_values, const float* bootstrap,
+                                     int64_t T, int64_t E, double gamma, double lambda, float* adv, float* ret,
+                                     void* stream);
 
 /*
  * GAE over B right-padded sequences of up to Lmax elements (LLM post-training

@@ -35,7 +35,8 @@ class ConduitError(RuntimeError):
 class BufferOpts(C.Structure):
     _fields_ = [("prioritized", C.c_int32), ("alpha_num", C.c_int32), ("alpha_den", C.c_int32),
                 ("beta", C.c_double), ("frame_stack", C.c_int32), ("action_bytes", C.c_int32),
-                ("ragged", C.c_int32), ("aux_elem_bytes", C.c_int32), ("payload_placement", C.c_int32)]
+                ("ragged", C.c_int32), ("aux_elem_bytes", C.c_int32), ("payload_placement", C.c_int32),
+                ("weight_norm", C.c_int32)]
 
 
 class Transitions(C.Structure):
@@ -90,6 +91,7 @@ class OnpolicyLoop(C.Structure):
 
 
 PLACE_HBM, PLACE_HOST_PINNED, PLACE_HOST_PAGEABLE = 0, 1, 2
+WNORM_BATCH, WNORM_BUFFER = 0, 1
 PLACEMENT_NAMES = ("hbm", "host_pinned", "host_pageable")
 
 
@@ -124,6 +126,7 @@ SIGNATURES = {
     "conduit_gather_transform": (ST, [P, P, I64, P, P, P]),
     "conduit_sample_gather": (ST, [P, I64, P, P, P, P, P, P]),
     "conduit_gae": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
+    "conduit_gae_truncated": (ST, [P, P, P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_gae_packed": (ST, [P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_minibatch_gather": (ST, [P, I64, I64, P, I64, P, P, P, P, I32_, P]),
     "conduit_buffer_get_info": (ST, [P, P]),
@@ -304,6 +307,17 @@ def conduit_gae(rewards, values, dones, bootstrap, gamma, lam, adv, ret, stream=
                              _ptr(ret, torch.float32, "ret"), _stream(stream)))
 
 
+def conduit_gae_truncated(rewards, values, dones, truncated, final_values, bootstrap, gamma, lam, adv, ret,
+                          stream=None):
+    T, E = rewards.shape
+    _check(lib().conduit_gae_truncated(_ptr(rewards, torch.float32, "rewards"), _ptr(values, torch.float32, "values"),
+                                       _ptr(dones, torch.uint8, "dones"), _ptr(truncated, torch.uint8, "truncated"),
+                                       _ptr(final_values, torch.float32, "final_values"),
+                                       _ptr(bootstrap, torch.float32, "bootstrap"), T, E, float(gamma), float(lam),
+                                       _ptr(adv, torch.float32, "adv"), _ptr(ret, torch.float32, "ret"),
+                                       _stream(stream)))
+
+
 def conduit_gae_packed(last_reward, lengths, values, Lmax, gamma, lam, adv, ret, stream=None):
     B = last_reward.numel()
     _check(lib().conduit_gae_packed(_ptr(last_reward, torch.float32, "last_reward"),
@@ -430,10 +444,12 @@ class ReplayBuffer:
     """Owning wrapper around a conduit_buffer handle."""
 
     def __init__(self, capacity, obs_shape, obs_dtype=torch.uint8, prioritized=True, alpha=(3, 5), beta=0.4,
-                 frame_stack=1, action_bytes=4, ragged=False, aux_elem_bytes=0, arena=None, placement=PLACE_HBM):
+                 frame_stack=1, action_bytes=4, ragged=False, aux_elem_bytes=0, arena=None, placement=PLACE_HBM,
+                 weight_norm=0):
         self.opts = default_opts(prioritized=int(prioritized), alpha_num=alpha[0], alpha_den=alpha[1], beta=beta,
                                  frame_stack=frame_stack, action_bytes=action_bytes, ragged=int(ragged),
-                                 aux_elem_bytes=aux_elem_bytes, payload_placement=int(placement))
+                                 aux_elem_bytes=aux_elem_bytes, payload_placement=int(placement),
+                                 weight_norm=int(weight_norm))
         self.capacity = capacity
         self.obs_shape = tuple(obs_shape)
         self.obs_dtype = obs_dtype

@@ -190,6 +190,8 @@ conduit_status make_layout(int64_t capacity, const int64_t* shape, int32_t ndim,
         return fail(CONDUIT_EINVAL, "kernels cannot address pageable memory: place the payload in HBM or pinned host memory");
     if (o.payload_placement != CONDUIT_PLACE_HBM && o.payload_placement != CONDUIT_PLACE_HOST_PINNED)
         return fail(CONDUIT_EINVAL, "unknown payload placement");
+    if (o.weight_norm != CONDUIT_WNORM_BATCH && o.weight_norm != CONDUIT_WNORM_BUFFER)
+        return fail(CONDUIT_EINVAL, "weight_norm must be CONDUIT_WNORM_BATCH or CONDUIT_WNORM_BUFFER");
     // tree shape
     L->nodes[0] = capacity;
     int d = 0;
@@ -282,6 +284,7 @@ void conduit_buffer_opts_default(conduit_buffer_opts* o) {
     o->ragged = 0;
     o->aux_elem_bytes = 0;
     o->payload_placement = CONDUIT_PLACE_HBM;
+    o->weight_norm = CONDUIT_WNORM_BATCH;
 }
 
 const char* conduit_last_error(void) { return g_last_error.c_str(); }
@@ -517,6 +520,15 @@ conduit_status conduit_update_priorities(conduit_buffer* b, const int64_t* idx, 
     return CONDUIT_OK;
 }
 
+// buffer-wide weight normalisation: the sampler folds the leaf minimum
+static void set_leaf_min(const conduit_buffer* b, SampleArgs* a) {
+    if (a->w_out && b->opts.weight_norm == CONDUIT_WNORM_BUFFER) {
+        a->leaf_min = &b->state->leaf_min;
+        a->leaves = b->tree.leaves;
+        a->n_leaves4 = round64(b->capacity) / 4;
+    }
+}
+
 conduit_status conduit_sample(conduit_buffer* b, int64_t batch, const uint64_t* uniforms, int64_t* idx_out,
                               float* is_w_out, void* stream) {
     if (!b) return fail(CONDUIT_EINVAL, "NULL buffer");
@@ -536,6 +548,7 @@ conduit_status conduit_sample(conduit_buffer* b, int64_t batch, const uint64_t* 
     a.beta = b->opts.beta;
     a.state = b->state;
     a.err = err_words(b->err_slot);
+    set_leaf_min(b, &a);
     hipError_t e = launch_sample(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "sample launch");
     return CONDUIT_OK;
@@ -680,6 +693,7 @@ conduit_status conduit_sample_gather(conduit_buffer* b, int64_t batch, const uin
     sa.beta = b->opts.beta;
     sa.state = b->state;
     sa.err = err_words(b->err_slot);
+    set_leaf_min(b, &sa);
     hipStream_t s = static_cast<hipStream_t>(stream);
     // dense rows of a few work items: one fused launch
     hipError_t e = b->opts.ragged ? hipErrorNotSupported : launch_sample_gather(sa, ga, s);
@@ -687,7 +701,7 @@ conduit_status conduit_sample_gather(conduit_buffer* b, int64_t batch, const uin
         // otherwise the sampler parks the sampled leaves in is_w_out, and the
         // gather (or packing) launch carries one more workgroup that turns them
         // into the IS weights
-        const WeightsArgs wa{is_w_out, batch, b->opts.beta};
+        const WeightsArgs wa{is_w_out, batch, b->opts.beta, sa.leaf_min};
         ga.weights = wa;
         pa.weights = wa;
         e = launch_descend(sa, s);
@@ -706,7 +720,25 @@ conduit_status conduit_gae(const float* rewards, const float* values, const uint
     if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
     conduit_status st = standalone_flags();
     if (st != CONDUIT_OK) return st;
-    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret};
+    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, nullptr, nullptr};
+    hipError_t e = launch_gae(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gae launch");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_gae_truncated(const float* rewards, const float* values, const uint8_t* dones,
+                                     const uint8_t* truncated, const float* final_values, const float* bootstrap,
+                                     int64_t T, int64_t E, double gamma, double lambda, float* adv, float* ret,
+                                     void* stream) {
+    if (T < 0 || E < 0) return fail(CONDUIT_EINVAL, "T and E must be >= 0");
+    if (E > kGaeMaxEnvs) return fail(CONDUIT_EINVAL, "E must be at most 2^19 environments");
+    if (T == 0 || E == 0) return CONDUIT_OK;
+    if (!rewards || !dones || !truncated || !final_values || !adv || !ret)
+        return fail(CONDUIT_EINVAL, "rewards, dones, truncated, final_values, adv and ret must not be NULL");
+    if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
+    conduit_status st = standalone_flags();
+    if (st != CONDUIT_OK) return st;
+    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, truncated, final_values};
     hipError_t e = launch_gae(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "gae launch");
     return CONDUIT_OK;

@@ -30,7 +30,8 @@ enum ErrKind : int {
 // Small device-resident state of one buffer.
 struct DeviceState {
     uint32_t max_prio;   // running maximum priority (starts at 1)
-    uint32_t qmin;       // sampler scratch: batch minimum leaf, UINT32_MAX between calls
+    uint32_t leaf_min;   // sampler scratch: smallest non-zero leaf of the buffer (buffer-wide IS
+                         // normalisation), UINT32_MAX between calls
     uint32_t ticket;     // sampler scratch: finished blocks, 0 between calls
     uint32_t pad;
 };
@@ -216,6 +217,8 @@ struct WeightsArgs {
     float* w;        // parked leaves in, weights out; NULL: no weights
     int64_t batch;
     double beta;
+    uint32_t* leaf_min = nullptr;  // non-NULL: normalise by this buffer-wide minimum leaf
+                                   // (folded in by the sampler) and reset it afterwards
 };
 
 // COHERENT: the leaves were parked by other workgroups of the same launch with
@@ -229,18 +232,26 @@ __device__ void is_weights_block(const WeightsArgs& a) {
         if constexpr (COHERENT) return __hip_atomic_load(q_park + k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         else return q_park[k];
     };
-    uint32_t m = 0xffffffffu;
-    for (int64_t k = threadIdx.x; k < a.batch; k += NT) {
-        const uint32_t q = parked(k);
-        if (q) m = q < m ? q : m;
-    }
-    m = wave_min_u32(m);
-    if (lane_id() == 0) wave_min[threadIdx.x / kWave] = m;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t r = wave_min[0];
-        for (int i = 1; i < NT / kWave; ++i) r = wave_min[i] < r ? wave_min[i] : r;
-        qmin_s = r;
+    if (a.leaf_min) {  // buffer-wide: the samplers' fold of every stored leaf
+        if (threadIdx.x == 0) {
+            if constexpr (COHERENT) qmin_s = __hip_atomic_load(a.leaf_min, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            else qmin_s = *a.leaf_min;
+            __hip_atomic_store(a.leaf_min, 0xffffffffu, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    } else {  // the batch's smallest sampled leaf
+        uint32_t m = 0xffffffffu;
+        for (int64_t k = threadIdx.x; k < a.batch; k += NT) {
+            const uint32_t q = parked(k);
+            if (q) m = q < m ? q : m;
+        }
+        m = wave_min_u32(m);
+        if (lane_id() == 0) wave_min[threadIdx.x / kWave] = m;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t r = wave_min[0];
+            for (int i = 1; i < NT / kWave; ++i) r = wave_min[i] < r ? wave_min[i] : r;
+            qmin_s = r;
+        }
     }
     __syncthreads();
     const double qmin = (double)qmin_s;
@@ -310,7 +321,42 @@ struct SampleArgs {
     double beta;
     DeviceState* state;
     uint32_t* err;
+    // buffer-wide IS normalisation: the sampler workgroups fold the smallest
+    // non-zero leaf of leaves4[0, n_leaves4) (uint32 x 4) into *leaf_min
+    uint32_t* leaf_min = nullptr;
+    const uint32_t* leaves = nullptr;
+    int64_t n_leaves4 = 0;
 };
+
+// The smallest non-zero leaf of workgroup wg's share of the buffer's leaves
+// (wgs workgroups split them), folded into *a.leaf_min with one agent-scope
+// atomic per workgroup.  Every thread of the workgroup takes part.
+template <int NT>
+__device__ void fold_leaf_min(const SampleArgs& a, int64_t wg, int64_t wgs) {
+    __shared__ uint32_t wmin[NT / kWave];
+    const int64_t per = (a.n_leaves4 + wgs - 1) / wgs;
+    const int64_t lo = wg * per;
+    const int64_t hi = lo + per < a.n_leaves4 ? lo + per : a.n_leaves4;
+    const uint4* v = reinterpret_cast<const uint4*>(a.leaves);
+    uint32_t m = 0xffffffffu;
+    auto fold = [&](uint32_t q) { m = (q != 0u && q < m) ? q : m; };
+    for (int64_t i = lo + threadIdx.x; i < hi; i += NT) {
+        const uint4 q = v[i];
+        fold(q.x);
+        fold(q.y);
+        fold(q.z);
+        fold(q.w);
+    }
+    m = wave_min_u32(m);
+    if (lane_id() == 0) wmin[threadIdx.x / kWave] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t r = wmin[0];
+        for (int i = 1; i < NT / kWave; ++i) r = wmin[i] < r ? wmin[i] : r;
+        if (r != 0xffffffffu)
+            (void)__hip_atomic_fetch_min(a.leaf_min, r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
 
 // sampler, then the weights kernel (if w_out is set)
 hipError_t launch_sample(const SampleArgs& a, hipStream_t s);
@@ -420,6 +466,8 @@ struct GaeArgs {
     double gamma, lambda;
     float* adv;
     float* ret;
+    const uint8_t* truncated;   // NULL: no truncation bootstrap
+    const float* final_value;   // read where truncated (and not done)
 };
 
 hipError_t launch_gae(const GaeArgs& a, hipStream_t s);

@@ -28,11 +28,30 @@ constexpr int kSuper = kChunks * kChunkLen;   // 1024 steps per pass
 constexpr int kTmThreads = kEnvs * kChunks;   // 512: leaves 256 VGPRs per lane
 static_assert(kGaeMaxEnvs * kSuper * 4 <= (1ll << 32), "byte offsets of a slab fit 32 bits");
 
+// One step of the recursion: delta_t and the coefficient a_t of A_{t+1}.
+// With TRUNC, a truncated step also ends the recursion and, unless it also
+// terminated, bootstraps from the value of its true next observation.
+template <bool TRUNC>
+__device__ __forceinline__ void gae_step(double r, double v, double v_next, uint8_t d, uint8_t tr, float fv,
+                                         double gamma, double gl, double* delta, double* m) {
+    if constexpr (TRUNC) {
+        const double live = (d | tr) ? 0.0 : 1.0;
+        const double boot = (tr && !d) ? (double)fv : 0.0;
+        *delta = r + gamma * (live * v_next + boot) - v;
+        *m = gl * live;
+    } else {
+        const double live = d ? 0.0 : 1.0;
+        *delta = r + gamma * live * v_next - v;
+        *m = gl * live;
+    }
+}
+
 // Time-major GAE.  A workgroup owns 8 environments and walks the rollout in
 // super-chunks of 1024 steps from the end; the carry (A at the start of the
 // later super-chunk) is kept per environment in LDS.  Within a super-chunk every
 // lane loads its 16 steps (reward, value, done) at once into registers, folds
 // them into (P, S), joins the suffix scan and replays from registers.
+template <bool TRUNC>
 __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
     __shared__ double sP[kChunks][kEnvs];
     __shared__ double sS[kChunks][kEnvs];
@@ -57,6 +76,8 @@ __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
         const uint32_t e32 = (uint32_t)e, E32 = (uint32_t)E;
         float r[kChunkLen], v[kChunkLen];
         uint8_t d[kChunkLen];
+        uint8_t tr[TRUNC ? kChunkLen : 1];
+        float fv[TRUNC ? kChunkLen : 1];
 #pragma unroll
         for (int k = 0; k < kChunkLen; ++k) {
             const int lt = c * kChunkLen + k < last_local ? c * kChunkLen + k : last_local;
@@ -64,6 +85,10 @@ __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
             r[k] = rb[off];
             v[k] = vb ? vb[off] : 0.0f;
             d[k] = db[off];
+            if constexpr (TRUNC) {
+                tr[k] = a.truncated[sbase + off];
+                fv[k] = a.final_value[sbase + off];
+            }
         }
         const int64_t t1 = t0 + kChunkLen;  // first step after this chunk
         double v_end;
@@ -74,9 +99,9 @@ __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
 #pragma unroll
         for (int k = kChunkLen - 1; k >= 0; --k) {
             if (t0 + k < T) {
-                const double live = d[k] ? 0.0 : 1.0;
-                const double delta = (double)r[k] + a.gamma * live * v_next - (double)v[k];
-                const double m = gl * live;
+                double delta, m;
+                gae_step<TRUNC>((double)r[k], (double)v[k], v_next, d[k], TRUNC ? tr[TRUNC ? k : 0] : 0,
+                                TRUNC ? fv[TRUNC ? k : 0] : 0.0f, a.gamma, gl, &delta, &m);
                 S = delta + m * S;
                 P = m * P;
                 v_next = (double)v[k];
@@ -112,9 +137,10 @@ __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
 #pragma unroll
         for (int k = kChunkLen - 1; k >= 0; --k) {
             if (t0 + k < T) {
-                const double live = d[k] ? 0.0 : 1.0;
-                const double delta = (double)r[k] + a.gamma * live * v_next - (double)v[k];
-                A = delta + gl * live * A;
+                double delta, m;
+                gae_step<TRUNC>((double)r[k], (double)v[k], v_next, d[k], TRUNC ? tr[TRUNC ? k : 0] : 0,
+                                TRUNC ? fv[TRUNC ? k : 0] : 0.0f, a.gamma, gl, &delta, &m);
+                A = delta + m * A;
                 if (active) {
                     const uint32_t off = (uint32_t)(c * kChunkLen + k) * E32 + e32;
                     ab[off] = (float)A;
@@ -262,7 +288,10 @@ hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
     if (a.T <= 0 || a.E <= 0) return hipSuccess;
     if (a.E > kGaeMaxEnvs) return hipErrorInvalidValue;  // the ABI rejects this first
     const int64_t blocks = (a.E + kEnvs - 1) / kEnvs;
-    hipLaunchKernelGGL(k_gae, dim3((unsigned)blocks), dim3(kTmThreads), 0, s, a);
+    if (a.truncated)
+        hipLaunchKernelGGL(k_gae<true>, dim3((unsigned)blocks), dim3(kTmThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(k_gae<false>, dim3((unsigned)blocks), dim3(kTmThreads), 0, s, a);
     return hipGetLastError();
 }
 

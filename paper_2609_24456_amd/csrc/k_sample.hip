@@ -25,15 +25,18 @@ constexpr int kThreads = kWaves * kWave;
 template <int PRE>
 __global__ __launch_bounds__(kThreads) void k_sample(SampleArgs a, DivB dv) {
     const int64_t k = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
-    if (k >= a.batch) return;  // wave-uniform
-    const Descent d = tree_descend<PRE>(a.tree, a.uniforms, k, dv);
-    if (lane_id() == 0) {
-        a.idx_out[k] = d.slot;
-        // the sampled leaf is parked in the weight slot for the weights block
-        if (a.w_out) reinterpret_cast<uint32_t*>(a.w_out)[k] = d.leaf;
-        if (d.slot < 0 && k == 0) flag_error(a.err, ERR_EMPTY_TREE);
-        if (d.lost) flag_error(a.err, ERR_DESCENT);
+    if (k < a.batch) {  // wave-uniform
+        const Descent d = tree_descend<PRE>(a.tree, a.uniforms, k, dv);
+        if (lane_id() == 0) {
+            a.idx_out[k] = d.slot;
+            // the sampled leaf is parked in the weight slot for the weights block
+            if (a.w_out) reinterpret_cast<uint32_t*>(a.w_out)[k] = d.leaf;
+            if (d.slot < 0 && k == 0) flag_error(a.err, ERR_EMPTY_TREE);
+            if (d.lost) flag_error(a.err, ERR_DESCENT);
+        }
     }
+    // buffer-wide normalisation: this workgroup's share of the leaf minimum
+    if (a.leaf_min) fold_leaf_min<kThreads>(a, blockIdx.x, gridDim.x);
 }
 
 constexpr int kWThreads = 1024;
@@ -58,7 +61,7 @@ hipError_t launch_descend(const SampleArgs& a, hipStream_t s) {
 hipError_t launch_sample(const SampleArgs& a, hipStream_t s) {
     hipError_t e = launch_descend(a, s);
     if (e != hipSuccess || a.w_out == nullptr) return e;
-    hipLaunchKernelGGL(k_is_weights, dim3(1), dim3(kWThreads), 0, s, WeightsArgs{a.w_out, a.batch, a.beta});
+    hipLaunchKernelGGL(k_is_weights, dim3(1), dim3(kWThreads), 0, s, WeightsArgs{a.w_out, a.batch, a.beta, a.leaf_min});
     return hipGetLastError();
 }
 

@@ -14,10 +14,13 @@
 //     another workgroup or for the index to make a round trip through memory.
 //     The first of a sample's W writes its scalar columns.
 //
-// Importance weights need the smallest sampled leaf of the whole batch.  Each
-// sampler workgroup parks its leaves with agent-scope atomic stores, waits
-// until they are acknowledged (visible device-wide), and takes a ticket with
-// one agent-scope atomic add on the buffer's device state.  The workgroup that
+// Importance weights need the smallest sampled leaf of the whole batch (or,
+// normalised buffer-wide, of the whole buffer: then each sampler workgroup
+// also folds the minimum of its share of the leaves into the device state
+// with one agent-scope atomic).  Each sampler workgroup parks its leaves with
+// agent-scope atomic stores, waits until they are acknowledged (visible
+// device-wide), and takes a ticket with one agent-scope atomic add on the
+// buffer's device state.  The workgroup that
 // draws the last ticket reads every leaf back with agent-scope atomic loads,
 // writes the weights (is_weights_block) and resets the ticket for the next
 // call.  No workgroup waits for another, no release fence (which would write
@@ -78,6 +81,9 @@ __device__ void sampler_wg(const SampleArgs& sa, const DivB& dv, int64_t wg) {
         }
     }
     if (!sa.w_out) return;  // kernel argument: uniform
+    // buffer-wide normalisation: this workgroup's share of the leaf minimum,
+    // folded in before the ticket like the parked leaves
+    if (sa.leaf_min) fold_leaf_min<kThreads>(sa, wg, (sa.batch + kSamplesPerSamplerWg - 1) / kSamplesPerSamplerWg);
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_waitcnt(0);  // this wavefront's parked leaves are acknowledged
     __syncthreads();                // ... and every wavefront's
@@ -88,7 +94,7 @@ __device__ void sampler_wg(const SampleArgs& sa, const DivB& dv, int64_t wg) {
     }
     __syncthreads();
     if (s_last) {  // every leaf of the batch is parked and visible
-        is_weights_block<kThreads, true>(WeightsArgs{sa.w_out, sa.batch, sa.beta});
+        is_weights_block<kThreads, true>(WeightsArgs{sa.w_out, sa.batch, sa.beta, sa.leaf_min});
         if (threadIdx.x == 0) __hip_atomic_store(&sa.state->ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }

@@ -42,6 +42,28 @@ def test_gae_time_major_shapes(T, E, p_done, with_v, with_b):
         assert_gae_close(gr, orr)
 
 
+@pytest.mark.parametrize("T,E,p_done,p_trunc", [
+    (1, 1, 0.0, 1.0), (37, 19, 0.05, 0.05), (200, 70, 0.01, 0.02), (1024, 8, 0.0, 0.01), (2500, 9, 0.003, 0.002),
+    (65, 17, 0.5, 0.5), (3073, 3, 0.0, 0.0)])
+def test_gae_truncated_shapes(T, E, p_done, p_trunc):
+    print(f"gae truncated T={T} E={E}", flush=True)
+    rng = np.random.default_rng(T * 137 + E)
+    r = rng.standard_normal((T, E)).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32)
+    d = (rng.random((T, E)) < p_done).astype(np.uint8)
+    tr = (rng.random((T, E)) < p_trunc).astype(np.uint8)
+    fv = rng.standard_normal((T, E)).astype(np.float32)
+    b = rng.standard_normal(E).astype(np.float32)
+    for gamma, lam in [(0.99, 0.95), (1.0, 1.0), (0.0, 0.5)]:
+        adv = torch.full((T, E), np.nan, dtype=torch.float32, device="cuda")
+        ret = torch.full((T, E), np.nan, dtype=torch.float32, device="cuda")
+        cd.conduit_gae_truncated(dev(r), dev(v), dev(d), dev(tr), dev(fv), dev(b), gamma, lam, adv, ret)
+        assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+        oa, orr = oracle.gae(r, v, d, b, gamma, lam, truncated=tr, final_value=fv)
+        assert_gae_close(host(adv), oa)
+        assert_gae_close(host(ret), orr)
+
+
 def test_gae_ppo_config_full_size():
     print("gae: PPO rollout 2048 x 256", flush=True)
     cfg = synth.PPO()

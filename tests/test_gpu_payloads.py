@@ -70,15 +70,16 @@ def test_large_payload_full_size():
               check_rows=np.random.default_rng(0).choice(1024, 24, replace=False))
 
 
-def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values, fused=False, placement=cd.PLACE_HBM):
+def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values, fused=False, placement=cd.PLACE_HBM,
+               weight_norm=cd.WNORM_BATCH):
     cfg = synth.Tokens(prefill, max_len=max_len, min_len=min_len)
     u, prio = cfg.draws(iters, batch)
     buf = cd.ReplayBuffer(cap, (max_len,), torch.int32, action_bytes=4, ragged=True, aux_elem_bytes=4,
-                          placement=placement)
+                          placement=placement, weight_norm=weight_norm)
     store = np.zeros((cap, max_len * 4), np.uint8)
     aux_store = np.zeros((cap, max_len * 4), np.uint8)
     orc = oracle.Replay(cap, (max_len,), np.int32, act_bytes=4, ragged=True, aux_dtype=np.float32,
-                        obs_storage=store)
+                        obs_storage=store, buffer_norm=weight_norm == cd.WNORM_BUFFER)
     orc.aux = aux_store
     orc._s.aux = aux_store.ctypes.data
     for a in range(0, prefill, chunk):
@@ -138,6 +139,13 @@ def test_tokens_reduced(fused):
     print(f"tokens: cap 300, max_len 256, prefill 400 (wraps), batch 64, fused={fused}", flush=True)
     run_tokens(cap=300, max_len=256, min_len=8, prefill=400, iters=3, batch=64, chunk=128, with_values=True,
                fused=fused)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_tokens_buffer_wide_weights(fused):
+    print(f"tokens: buffer-wide IS normalisation, cap 300, fused={fused}", flush=True)
+    run_tokens(cap=300, max_len=256, min_len=8, prefill=400, iters=3, batch=64, chunk=128, with_values=True,
+               fused=fused, weight_norm=cd.WNORM_BUFFER)
 
 
 @pytest.mark.parametrize("fused", [False, True])

@@ -53,12 +53,12 @@ def test_leaf_quantiser_matches_oracle(a, b):
 # ----------------------------------------------------------------------------
 # configuration 0: tiny replay, 100 iterations, full parity at every step
 # ----------------------------------------------------------------------------
-def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM):
+def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH):
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
-    buf = _mk(C, (8,), torch.float32, action_bytes=4, placement=placement)
-    orc = oracle.Replay(C, (8,), np.float32, act_bytes=4)
+    buf = _mk(C, (8,), torch.float32, action_bytes=4, placement=placement, weight_norm=weight_norm)
+    orc = oracle.Replay(C, (8,), np.float32, act_bytes=4, buffer_norm=weight_norm == cd.WNORM_BUFFER)
 
     def ingest(a, b):
         buf.ingest(dev(cfg.obs[a:b]), action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]),
@@ -122,6 +122,14 @@ def test_tiny_config_fused_sample_gather():
 
 
 @pytest.mark.parametrize("fused", [False, True])
+def test_tiny_config_buffer_wide_weights(fused):
+    # IS weights normalised by the smallest non-zero leaf of the whole buffer
+    print(f"tiny config: buffer-wide IS normalisation, fused={fused}", flush=True)
+    _run_tiny(prefill=0, iters=60, seed_shift=5, fused=fused, weight_norm=cd.WNORM_BUFFER)
+    _run_tiny(prefill=20000, iters=20, seed_shift=6, fused=fused, weight_norm=cd.WNORM_BUFFER)
+
+
+@pytest.mark.parametrize("fused", [False, True])
 def test_tiny_config_payload_in_pinned_host_memory(fused):
     # Sec. 5 placement: the observation column in pinned host memory, reached
     # by the same kernels across the host link; results identical
@@ -133,7 +141,7 @@ def test_tiny_config_payload_in_pinned_host_memory(fused):
 # configuration 1 (DQN, frame stack 4, u8 -> fp32/255) at reduced capacity
 # ----------------------------------------------------------------------------
 def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False,
-            placement=cd.PLACE_HBM):
+            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH):
     """Drive GPU buffer and oracle through the same DQN stream; the oracle keeps
     metadata only and its observation rows are regenerated for the slots a
     gather reads."""
@@ -147,9 +155,11 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
         cfg.drift = rng.integers(1, 4, int(cfg.episode.max()) + 1).astype(np.int64)
     u, prio = cfg.draws(iters, batch)
     K = 4
-    buf = _mk(cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4, placement=placement)
+    buf = _mk(cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4, placement=placement,
+              weight_norm=weight_norm)
     obs_store = np.zeros((cap, 84 * 84), np.uint8)  # untouched pages stay unallocated
-    orc = oracle.Replay(cap, (84, 84), np.uint8, act_bytes=4, frame_stack=K, obs_storage=obs_store)
+    orc = oracle.Replay(cap, (84, 84), np.uint8, act_bytes=4, frame_stack=K, obs_storage=obs_store,
+                        buffer_norm=weight_norm == cd.WNORM_BUFFER)
 
     def ingest(a, b, with_prio):
         p = cfg.prio[a:b] if with_prio else None
@@ -219,6 +229,13 @@ def test_dqn_short_episodes_zero_fill():
 def test_dqn_fused_sample_gather(short):
     print(f"dqn: fused sample+gather, cap 3000, short episodes={short}", flush=True)
     run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused=True)
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_dqn_buffer_wide_weights(fused):
+    print(f"dqn: buffer-wide IS normalisation, cap 3000, fused={fused}", flush=True)
+    run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=True, fused=fused,
+            weight_norm=cd.WNORM_BUFFER)
 
 
 @pytest.mark.parametrize("fused", [False, True])
