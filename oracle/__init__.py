@@ -238,6 +238,53 @@ class Replay:
             raise ValueError("oracle: nothing to sample")
         return idx, w
 
+    def nstep(self, idx, n, gamma):
+        """n-step return targets of sampled slots (the n-step Q-learning target
+        of the DQN line the paper cites: sum of gamma^k r over the next n
+        transitions of the episode, then gamma^n times the value of the state
+        n steps ahead).  For slot i holding stream position p, the window is
+        positions p, p+1, ...: it stops after the first done (a terminal: no
+        bootstrap), or after n transitions, where the bootstrap state is the
+        observation at p+n.  A window that reaches a position not yet stored,
+        or another episode without a done, is invalid (every output 0).
+        Returns (bootstrap slot or -1, return, discount, valid) per sample:
+        return = sum_k gamma^k r_{p+k} (fp64, k ascending, fp32 out), discount
+        = gamma^n for a bootstrapped window and 0 otherwise."""
+        idx = np.asarray(idx, np.int64)
+        B = len(idx)
+        C, total = self.capacity, self.total
+        nxt = np.full(B, -1, np.int64)
+        ret = np.zeros(B, np.float32)
+        disc = np.zeros(B, np.float32)
+        valid = np.zeros(B, np.uint8)
+
+        def stored(q, ep):
+            s = q % C
+            return q < total and self.position[s] == q and self.episode[s] == ep
+
+        for b in range(B):
+            i = int(idx[b])
+            p = int(self.position[i])
+            ep = self.episode[i]
+            R, g, ended, ok = 0.0, 1.0, False, True
+            for k in range(n):
+                if not stored(p + k, ep):
+                    ok = False
+                    break
+                s = (p + k) % C
+                R += g * float(self.reward[s])
+                g *= gamma
+                if self.done[s]:
+                    ended = True
+                    break
+            if not ok:
+                continue
+            if ended:
+                ret[b], valid[b] = R, 1
+            elif stored(p + n, ep):
+                nxt[b], ret[b], disc[b], valid[b] = (p + n) % C, R, g, 1
+        return nxt, ret, disc, valid
+
     def gather(self, idx, xform=XF_NONE, mean=None, std=None):
         idx = _c(idx, np.int64)
         B = len(idx)

@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 import oracle
+import synth
 from oracle import brute
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -222,6 +223,75 @@ def test_buffer_wide_is_weights():
             break
     else:
         pytest.fail("no batch drew the smallest leaf")
+
+
+def _stream_replay(rng, cap, total, p_done=0.15, K=1):
+    """A replay fed a known stream of single-float observations (the stream
+    position itself), with episode ids and steps derived from done."""
+    done = (rng.random(total) < p_done).astype(np.uint8)
+    ep, st = synth.episodes_from_done(done)
+    rew = rng.standard_normal(total).astype(np.float32)
+    obs = np.arange(total, dtype=np.float32)[:, None]
+    r = oracle.Replay(cap, (1,), np.float32, act_bytes=0, frame_stack=K)
+    for a in range(0, total, 7):
+        b = min(total, a + 7)
+        r.ingest(b - a, obs=obs[a:b], reward=rew[a:b], done=done[a:b], episode=ep[a:b], step=st[a:b])
+    return r, rew, done, ep
+
+
+def test_nstep_matches_the_stream_definition():
+    # brute force on the stream itself: positions, not ring slots
+    rng = np.random.default_rng(79)
+    for cap, total, n, gamma in [(40, 100, 3, 0.9), (64, 64, 5, 0.99), (33, 1000, 1, 0.5), (50, 77, 8, 1.0)]:
+        r, rew, done, ep = _stream_replay(rng, cap, total)
+        slots = np.arange(cap)
+        nxt, ret, disc, valid = r.nstep(slots, n, gamma)
+        for b, i in enumerate(slots):
+            p = int(r.position[i])
+            want_R, g, m, ended = 0.0, 1.0, None, False
+            for k in range(n):
+                q = p + k
+                if q >= total or ep[q] != ep[p]:
+                    m = None
+                    break
+                want_R += g * float(rew[q])
+                g *= gamma
+                m = k + 1
+                if done[q]:
+                    ended = True
+                    break
+            if m is None or (not ended and (p + n >= total or ep[p + n] != ep[p])):
+                assert valid[b] == 0 and ret[b] == 0 and disc[b] == 0 and nxt[b] == -1, (cap, b)
+                continue
+            assert valid[b] == 1
+            assert ret[b] == pytest.approx(want_R, rel=1e-6, abs=1e-6)
+            if ended:
+                assert disc[b] == 0 and nxt[b] == -1
+            else:
+                assert disc[b] == pytest.approx(gamma ** n, rel=1e-6) and nxt[b] == (p + n) % cap
+                assert r.position[nxt[b]] == p + n
+
+
+def test_nstep_special_cases():
+    rng = np.random.default_rng(83)
+    r, rew, done, ep = _stream_replay(rng, 50, 120, p_done=0.0)
+    slots = np.arange(50)
+    # one step, no dones: the 1-step DQN target
+    nxt, ret, disc, valid = r.nstep(slots, 1, 0.97)
+    newest = (r.head - 1) % 50
+    for b in slots:
+        if b == newest:
+            assert valid[b] == 0  # the newest transition has no successor yet
+        else:
+            assert valid[b] == 1 and ret[b] == rew[r.position[b]] and disc[b] == np.float32(0.97)
+    # gamma = 1 sums the rewards
+    nxt, ret, disc, valid = r.nstep(slots, 4, 1.0)
+    for b in slots:
+        if valid[b]:
+            p = r.position[b]
+            assert ret[b] == pytest.approx(float(rew[p:p + 4].astype(np.float64).sum()), rel=1e-6)
+            assert disc[b] == 1.0
+    assert int(valid.sum()) == 50 - 4  # the newest four cannot look four steps ahead
 
 
 # ----------------------------------------------------------------------------
