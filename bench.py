@@ -267,8 +267,25 @@ def bench_dqn(steps, warmup):
     descent_bytes = 8 + (depth - 1) * 64 * 8 + 64 * 4
     fused_bytes = gather_bytes - B * 8 + B * (descent_bytes + 8 + 8 + 4)
     ingest_bytes_per_frame = 2 * row + (4 + 4 + 1 + 4 + 4) * 2 + 4 + 4  # obs r+w, scalars r+w, leaf r+w
+    # n-step targets (n = 3, gamma 0.99) and bootstrap stacks of the timed
+    # steps' samples, back to back, and the step with them
+    n_step, gam = 3, 0.99
+    nxt = torch.empty(B, dtype=torch.int64, device="cuda")
+    nret = torch.empty(B, dtype=torch.float32, device="cuda")
+    ndisc = torch.empty(B, dtype=torch.float32, device="cuda")
+    nval = torch.empty(B, dtype=torch.uint8, device="cuda")
+    next_out = torch.empty((B, K, 84, 84), dtype=torch.float32, device="cuda")
+    nst = L.conduit_nstep
+    ns_args = (nxt.data_ptr(), nret.data_ptr(), ndisc.data_ptr(), nval.data_ptr(), xfr, next_out.data_ptr(), stream)
+    ns_calls = [lambda i=i: nst(h, pi[i], B, n_step, gam, *ns_args) for i in range(warmup, warmup + steps)]
+    _b2b_ms(ns_calls[:5])
+    nstep_ms = _b2b_ms(ns_calls)
+    boot = int(nval.sum().item())
+    assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
     return {
+        "nstep3": {"us": nstep_ms * 1e3, "n": n_step, "gamma": gam, "valid_in_last_batch": boot,
+                   "call": "conduit_nstep: targets plus the bootstrap frame stacks [512,4,84,84] fp32"},
         "B": B, "steps": steps, "warmup": warmup, "total_ms": total_ms, "host_enqueue_s": host_enqueue_s,
         "gather_b2b_ms": gather_b2b_ms, "fused_b2b_ms": fused_b2b_ms, "unfused_ms": unfused_ms,
         "kernels": kern, "gather_bytes": gather_bytes, "fused_bytes": fused_bytes, "descent_bytes": descent_bytes,
@@ -1123,7 +1140,7 @@ def main():
         "gather_avg_launch_us": g_ms * 1e3,
         "kernels_us_in_step": {k: v["mean_us"] for k, v in d["kernels"].items()},
         "host_enqueue_us_per_step": d["host_enqueue_s"] * 1e6 / args.steps,
-        "rows": {"dqn_ingest_32768": d["ingest_big"]},
+        "rows": {"dqn_ingest_32768": d["ingest_big"], "dqn_nstep3": d["nstep3"]},
     }
     if not args.no_rows:
         only = set(x for x in args.only.split(",") if x) or set(ROWS)

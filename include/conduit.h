@@ -310,6 +310,32 @@ conduit_status conduit_sample_gather(conduit_buffer* buf, int64_t batch, const u
                                      float* is_w_out, const conduit_transform* xf, const conduit_learner_batch* out,
                                      void* stream);
 
+/*
+ * n-step return targets for already-sampled slots (off-policy delivery
+ * materialising training-ready transitions, Sec. 2.2; the n-step Q-learning
+ * target of the DQN line of work): for sample b at slot idx[b], holding stream
+ * position p, the window p, p+1, ... of its episode stops after the first done
+ * (a terminal) or after n transitions; then
+ *   ret[b]      = sum_k gamma^k r_{p+k} over the window (fp64 sum, k ascending)
+ *   discount[b] = gamma^n if the window bootstraps (no done, the state at p+n
+ *                 stored), else 0
+ *   next_idx[b] = the slot holding position p+n if it bootstraps, else -1
+ *   valid[b]    = 0 if the window meets a position not yet stored, or another
+ *                 episode without a done (every output then 0 or -1): the
+ *                 learner drops such samples.
+ * If next_obs is not NULL it receives, for dense buffers, the observation
+ * stack of next_idx through xf (the bootstrap state, laid out as
+ * conduit_gather_transform's obs output; rows of samples without bootstrap are
+ * zero-filled).  idx, next_idx (int64), ret, discount (float), valid (uint8):
+ * device [batch]; 1 <= n <= 63; batch <= 2^20.  The ring state used is the
+ * one at enqueue time (calls on one buffer are stream-ordered).
+ * Errors: EINVAL (n or batch out of range, NULL outputs, a ragged buffer with
+ * next_obs, bad transform), ESTATE (an index outside [0, size), flagged).
+ */
+conduit_status conduit_nstep(conduit_buffer* buf, const int64_t* idx, int64_t batch, int32_t n, double gamma,
+                             int64_t* next_idx, float* ret, float* discount, uint8_t* valid,
+                             const conduit_transform* xf, void* next_obs, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Returns / advantages (Sec. 2.2 on-policy ingestion "computing
  * returns/advantages"; GAE as used by PPO, Schulman et al.)

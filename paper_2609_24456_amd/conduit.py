@@ -126,6 +126,7 @@ SIGNATURES = {
     "conduit_gather_transform": (ST, [P, P, I64, P, P, P]),
     "conduit_sample_gather": (ST, [P, I64, P, P, P, P, P, P]),
     "conduit_gae": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
+    "conduit_nstep": (ST, [P, P, I64, I32_, F64, P, P, P, P, P, P, P]),
     "conduit_gae_truncated": (ST, [P, P, P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_gae_packed": (ST, [P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_minibatch_gather": (ST, [P, I64, I64, P, I64, P, P, P, P, I32_, P]),
@@ -297,6 +298,16 @@ def conduit_sample_gather(handle, batch, uniforms, idx_out, is_w_out, xf, obs=No
     _check(lib().conduit_sample_gather(handle, batch, _ptr(uniforms, None, "uniforms"),
                                        _ptr(idx_out, torch.int64, "idx_out"), _ptr(is_w_out, torch.float32, "is_w_out"),
                                        C.byref(xf), C.byref(out), _stream(stream)))
+
+
+def conduit_nstep(handle, idx, n, gamma, next_idx, ret, discount, valid, xf=None, next_obs=None, stream=None):
+    """n-step return targets (and bootstrap-state stacks) of sampled slots."""
+    B = idx.numel()
+    _check(lib().conduit_nstep(handle, _ptr(idx, torch.int64, "idx"), B, int(n), float(gamma),
+                               _ptr(next_idx, torch.int64, "next_idx"), _ptr(ret, torch.float32, "ret"),
+                               _ptr(discount, torch.float32, "discount"), _ptr(valid, torch.uint8, "valid"),
+                               C.byref(xf) if xf is not None else None,
+                               next_obs.data_ptr() if next_obs is not None else None, _stream(stream)))
 
 
 def conduit_gae(rewards, values, dones, bootstrap, gamma, lam, adv, ret, stream=None):

@@ -711,6 +711,53 @@ conduit_status conduit_sample_gather(conduit_buffer* b, int64_t batch, const uin
     return CONDUIT_OK;
 }
 
+conduit_status conduit_nstep(conduit_buffer* b, const int64_t* idx, int64_t batch, int32_t n, double gamma,
+                             int64_t* next_idx, float* ret, float* discount, uint8_t* valid,
+                             const conduit_transform* xf, void* next_obs, void* stream) {
+    if (!b) return fail(CONDUIT_EINVAL, "NULL buffer");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (batch < 0 || batch > (1LL << 20)) return fail(CONDUIT_EINVAL, "batch must be in [0, 2^20]");
+    if (n < 1 || n > 63) return fail(CONDUIT_EINVAL, "n must be in [1, 63]");
+    if (!(gamma == gamma)) return fail(CONDUIT_EINVAL, "gamma must be a number");
+    if (batch == 0) return CONDUIT_OK;
+    if (!idx || !next_idx || !ret || !discount || !valid) return fail(CONDUIT_EINVAL, "NULL index or output");
+    if (b->size == 0) return fail(CONDUIT_EEMPTY, "n-step targets from an empty buffer");
+    GatherArgs ga{};
+    if (next_obs) {
+        if (b->opts.ragged) return fail(CONDUIT_EINVAL, "next-state stacks need a dense buffer");
+        if (!xf) return fail(CONDUIT_EINVAL, "next_obs needs a transform");
+        conduit_learner_batch nb{};
+        nb.obs = next_obs;
+        PackArgs pa{};
+        st = prepare_gather(b, next_idx, batch, xf, &nb, &ga, &pa);
+        if (st != CONDUIT_OK) return st;
+        ga.err_kind = -1;  // -1 entries are samples without a bootstrap state
+    }
+    DeviceGuard g(b->device);
+    NstepArgs a{};
+    a.idx = idx;
+    a.batch = batch;
+    a.n = n;
+    a.gamma = gamma;
+    a.capacity = b->capacity;
+    a.size = b->size;
+    a.total = b->total;
+    a.reward = b->reward;
+    a.done = b->done;
+    a.episode = b->episode;
+    a.next_idx = next_idx;
+    a.ret = ret;
+    a.discount = discount;
+    a.valid = valid;
+    a.err = err_words(b->err_slot);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = launch_nstep(a, s);
+    if (e == hipSuccess && next_obs) e = launch_gather(ga, s);
+    if (e != hipSuccess) return hip_fail(e, "nstep launch");
+    return CONDUIT_OK;
+}
+
 conduit_status conduit_gae(const float* rewards, const float* values, const uint8_t* dones, const float* bootstrap,
                            int64_t T, int64_t E, double gamma, double lambda, float* adv, float* ret, void* stream) {
     if (T < 0 || E < 0) return fail(CONDUIT_EINVAL, "T and E must be >= 0");

@@ -393,7 +393,7 @@ struct GatherArgs {
     const float* cols[kMaxCols];
     float* cols_out[kMaxCols];
     uint32_t* err;
-    int32_t err_kind;
+    int32_t err_kind;       // flag raised for an index outside [0, limit); < 0: none
     // the IS weights of the batch the indices were sampled as (one extra
     // workgroup of the launch); weights.w NULL: none
     WeightsArgs weights;
@@ -471,6 +471,25 @@ struct GaeArgs {
 };
 
 hipError_t launch_gae(const GaeArgs& a, hipStream_t s);
+
+// n-step return targets of sampled slots (k_nstep.hip)
+struct NstepArgs {
+    const int64_t* idx;
+    int64_t batch;
+    int32_t n;
+    double gamma;
+    int64_t capacity, size, total;  // ring state at enqueue time
+    const float* reward;
+    const uint8_t* done;
+    const uint32_t* episode;
+    int64_t* next_idx;
+    float* ret;
+    float* discount;
+    uint8_t* valid;
+    uint32_t* err;
+};
+
+hipError_t launch_nstep(const NstepArgs& a, hipStream_t s);
 
 struct GaePackedArgs {
     const float* last_reward;

@@ -19,6 +19,12 @@ namespace conduit {
 
 namespace {
 
+// an index outside [0, limit): the row is zero-filled; err_kind < 0 (indices
+// produced by the library, where -1 stands for "no row") raises no flag
+__device__ __forceinline__ void flag_index(const GatherArgs& a) {
+    if (a.err_kind >= 0) flag_error(a.err, a.err_kind);
+}
+
 // outputs up to this size use the persistent pipelined kernel
 constexpr int64_t kPipeMaxOutBytes = 128ll << 20;
 
@@ -46,7 +52,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
     }
     const int64_t i = a.idx[it / ((int64_t)bpf * a.stack)];
     const Item t = decode(a, it, bpf, i);
-    if (!t.ok && threadIdx.x == 0 && t.part == 0 && t.k == a.stack - 1) flag_error(a.err, a.err_kind);
+    if (!t.ok && threadIdx.x == 0 && t.part == 0 && t.k == a.stack - 1) flag_index(a);
     typename UnitOf<XF>::T v[kUnroll];
     int32_t si = 0, sj = 0;
     uint32_t ei = 0, ej = 0;
@@ -79,7 +85,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
     int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
     uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
     Item ta = decode(a, it, bpf, i0), tb;
-    if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_error(a.err, a.err_kind);
+    if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_index(a);
     issue<XF>(a, ta, i0, va, sia, sja, eia, eja);
     while (true) {
         tb = decode(a, clampi(itn), bpf, i1);
@@ -88,7 +94,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
         int64_t i2 = a.idx[clampi(itnn) / per_row];
         finish<XF, NT, false>(a, ta, va, sia, sja, eia, eja, lut);
         if (itn >= n_items) break;
-        if (!tb.ok && threadIdx.x == 0 && tb.part == 0 && tb.k == a.stack - 1) flag_error(a.err, a.err_kind);
+        if (!tb.ok && threadIdx.x == 0 && tb.part == 0 && tb.k == a.stack - 1) flag_index(a);
         itn = itnn;
         i1 = i2;
         ta = decode(a, clampi(itn), bpf, i1);
@@ -97,7 +103,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
         i2 = a.idx[clampi(itnn) / per_row];
         finish<XF, NT, false>(a, tb, vb, sib, sjb, eib, ejb, lut);
         if (itn >= n_items) break;
-        if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_error(a.err, a.err_kind);
+        if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_index(a);
         itn = itnn;
         i1 = i2;
     }

@@ -53,7 +53,35 @@ def test_leaf_quantiser_matches_oracle(a, b):
 # ----------------------------------------------------------------------------
 # configuration 0: tiny replay, 100 iterations, full parity at every step
 # ----------------------------------------------------------------------------
-def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH):
+def _check_nstep(buf, orc, idx_d, o_idx, n, gamma, xf_kind, row_shape, obs_kind=None):
+    """conduit_nstep on the sampled indices against the oracle's n-step
+    targets and bootstrap-state stacks (zero rows where there is none)."""
+    B = idx_d.numel()
+    nxt = torch.empty(B, dtype=torch.int64, device="cuda")
+    ret = torch.empty(B, dtype=torch.float32, device="cuda")
+    disc = torch.empty(B, dtype=torch.float32, device="cuda")
+    val = torch.empty(B, dtype=torch.uint8, device="cuda")
+    out_dtype = torch.float32 if xf_kind == cd.XF_U8_F32 else obs_kind
+    K = orc.frame_stack
+    nobs = torch.full((B, K) + row_shape, 7, dtype=out_dtype, device="cuda")
+    xf = cd.transform(xf_kind)
+    cd.conduit_nstep(buf.handle, idx_d, n, gamma, nxt, ret, disc, val, xf, nobs)
+    o_n, o_r, o_d, o_v = orc.nstep(o_idx, n, gamma)
+    assert np.array_equal(host(nxt), o_n)
+    assert np.array_equal(host(val), o_v)
+    np.testing.assert_allclose(host(ret), o_r, rtol=1e-6, atol=1e-6)
+    assert np.array_equal(host(disc), o_d)
+    g = host(nobs).reshape(B, -1).view(np.uint8)
+    boot = o_n >= 0
+    if boot.any():
+        want, _, _, _ = orc.gather(o_n[boot], oracle.XF_U8_F32 if xf_kind == cd.XF_U8_F32 else oracle.XF_NONE)
+        assert np.array_equal(g[boot], want.reshape(int(boot.sum()), -1).view(np.uint8))
+    assert not g[~boot].any()
+    return o_v
+
+
+def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH,
+              nstep=None):
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
@@ -82,8 +110,10 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
         else:
             idx, w = buf.sample(dev(u[it]))
             buf.gather(idx, xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
-        buf.update(idx, dev(prio[it]))
         o_idx, o_w = orc.sample(u[it])
+        if nstep is not None:
+            _check_nstep(buf, orc, idx, o_idx, nstep[0], nstep[1], cd.XF_NONE, (8,), torch.float32)
+        buf.update(idx, dev(prio[it]))
         o_obs, o_act, o_rew, o_done = orc.gather(o_idx)
         orc.update(o_idx, prio[it])
         assert np.array_equal(host(idx), o_idx), it
@@ -121,6 +151,13 @@ def test_tiny_config_fused_sample_gather():
     _run_tiny(prefill=0, iters=100, fused=True)
 
 
+@pytest.mark.parametrize("n,gamma", [(1, 0.99), (3, 0.99), (63, 0.9)])
+def test_tiny_config_nstep_targets(n, gamma):
+    print(f"tiny config: {n}-step targets", flush=True)
+    _run_tiny(prefill=0, iters=20, seed_shift=9, nstep=(n, gamma))
+    _run_tiny(prefill=20000, iters=10, seed_shift=10, nstep=(n, gamma), fused=True)
+
+
 @pytest.mark.parametrize("fused", [False, True])
 def test_tiny_config_buffer_wide_weights(fused):
     # IS weights normalised by the smallest non-zero leaf of the whole buffer
@@ -141,7 +178,7 @@ def test_tiny_config_payload_in_pinned_host_memory(fused):
 # configuration 1 (DQN, frame stack 4, u8 -> fp32/255) at reduced capacity
 # ----------------------------------------------------------------------------
 def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False,
-            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH):
+            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH, nstep=None):
     """Drive GPU buffer and oracle through the same DQN stream; the oracle keeps
     metadata only and its observation rows are regenerated for the slots a
     gather reads."""
@@ -191,7 +228,12 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
         assert_weights_close(host(w), o_w)
         rows = np.arange(batch) if check_rows is None else check_rows
         sel = o_idx[rows]
-        need = np.unique(np.concatenate([(sel - d) % cap for d in range(K)]))
+        if nstep is not None:  # the bootstrap stacks need their frames too
+            o_next = orc.nstep(o_idx, nstep[0], nstep[1])[0]
+            sel_all = np.concatenate([sel, o_next[o_next >= 0]])
+        else:
+            sel_all = sel
+        need = np.unique(np.concatenate([(sel_all - d) % cap for d in range(K)]))
         need = need[orc.position[need] >= 0]
         if len(need):  # regenerate the observation each needed slot holds
             obs_store[need] = cfg.frames_at(orc.position[need]).reshape(len(need), -1).numpy()
@@ -201,6 +243,8 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
         assert np.array_equal(host(act_out)[rows].view(np.uint8).reshape(-1), o_act.reshape(-1)), it
         assert np.array_equal(host(rew_out)[rows], o_rew), it
         assert np.array_equal(host(done_out)[rows], o_done), it
+        if nstep is not None:
+            _check_nstep(buf, orc, idx, o_idx, nstep[0], nstep[1], cd.XF_U8_F32, (84, 84))
         orc.update(o_idx, prio[it])
     assert buf.sync_check() == cd.OK, cd.last_error()
     leaves = read_col(buf, cd.COL_LEAVES, cap * 4, np.uint32)
@@ -229,6 +273,13 @@ def test_dqn_short_episodes_zero_fill():
 def test_dqn_fused_sample_gather(short):
     print(f"dqn: fused sample+gather, cap 3000, short episodes={short}", flush=True)
     run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused=True)
+
+
+@pytest.mark.parametrize("n,short", [(1, True), (3, True), (5, False)])
+def test_dqn_nstep_targets_and_next_stacks(n, short):
+    print(f"dqn: {n}-step targets and bootstrap stacks, short episodes={short}", flush=True)
+    run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused=True,
+            nstep=(n, 0.99))
 
 
 @pytest.mark.parametrize("fused", [False, True])
@@ -409,6 +460,25 @@ def test_error_paths_are_flagged_not_faulting():
     assert buf.sync_check() == cd.ESTATE
     assert np.all(host(out)[1] == 0)
     buf.clear_error()
+    # n-step targets of an index outside [0, size): invalid outputs and a flag;
+    # a -1 bootstrap slot alone raises nothing
+    nxt = torch.empty(2, dtype=torch.int64, device="cuda")
+    ret = torch.empty(2, dtype=torch.float32, device="cuda")
+    disc = torch.empty(2, dtype=torch.float32, device="cuda")
+    val = torch.empty(2, dtype=torch.uint8, device="cuda")
+    nobs = torch.full((2, 1, 4), 9, dtype=torch.uint8, device="cuda")
+    cd.conduit_nstep(buf.handle, dev(np.array([7, 20], np.int64)), 2, 0.9, nxt, ret, disc, val,
+                     cd.transform(cd.XF_NONE), nobs)
+    assert buf.sync_check() == cd.ESTATE
+    assert host(val)[1] == 0 and host(nxt)[1] == -1 and np.all(host(nobs)[1] == 0)
+    buf.clear_error()
+    cd.conduit_nstep(buf.handle, dev(np.array([7], np.int64)), 2, 0.9, nxt[:1], ret[:1], disc[:1], val[:1],
+                     cd.transform(cd.XF_NONE), nobs[:1])  # slot 7 is the newest: no bootstrap
+    assert buf.sync_check() == cd.OK
+    assert host(val)[0] == 0 and host(nxt)[0] == -1
+    with pytest.raises(cd.ConduitError) as e:
+        cd.conduit_nstep(buf.handle, dev(np.array([1], np.int64)), 64, 0.9, nxt[:1], ret[:1], disc[:1], val[:1])
+    assert e.value.status == cd.EINVAL
     buf.close()
 
 
