@@ -107,7 +107,8 @@ def bench_dqn(steps, warmup):
     L = cd.lib()
     stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
     Cap, B, K, prefill, chunk = 1_000_000, 512, 4, 1_050_000, 4096
-    iters = warmup + 3 * steps  # timed fused pass + timed unfused pass + instrumented pass
+    # passes: timed headline, separate-update, unfused, two instrumented
+    iters = warmup + 5 * steps
     cfg = synth.DQN(prefill + iters * B)
     buf = cd.ReplayBuffer(Cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4)
     t0 = time.time()
@@ -179,6 +180,13 @@ def bench_dqn(steps, warmup):
         r |= upd(h, pi[i], pp[i], B, stream)
         return r
 
+    uing = L.conduit_update_ingest
+
+    def step_ui(i):  # step i-1's priority update with step i's ingest (one call), fused sample + gather
+        r = uing(h, pi[i - 1], pp[i - 1], B, C.byref(trans[i]), stream)
+        r |= sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
+        return r
+
     def step_unfused(i):  # the same step with separate sample and gather calls
         r = ing(h, C.byref(trans[i]), stream)
         r |= smp(h, B, pu[i], pi[i], pw[i], stream)
@@ -186,31 +194,45 @@ def bench_dqn(steps, warmup):
         r |= upd(h, pi[i], pp[i], B, stream)
         return r
 
-    for i in range(warmup):
+    for i in range(warmup - 1):
         assert step(i) == 0, cd.last_error()
+    # the last warm-up step leaves its priority update to the first timed step
+    rc = ing(h, C.byref(trans[warmup - 1]), stream)
+    rc |= sgat(h, B, pu[warmup - 1], pi[warmup - 1], pw[warmup - 1], xfr, lbr, stream)
+    assert rc == 0, cd.last_error()
     torch.cuda.synchronize()
-    # timed pass
+    # timed pass: each step applies the previous step's update with its own
+    # ingest, so K steps hold K ingests, K samples + gathers and K updates
     e_start = tm.ev()
     h0 = time.perf_counter()
     rc = 0
     for i in range(warmup, warmup + steps):
-        rc |= step(i)
+        rc |= step_ui(i)
     e_end = tm.ev()
     host_enqueue_s = time.perf_counter() - h0
+    rc |= upd(h, pi[warmup + steps - 1], pp[warmup + steps - 1], B, stream)  # after the clock
     torch.cuda.synchronize()
     assert rc == 0, cd.last_error()
     total_ms = e_start.elapsed_time(e_end)
-    # the same number of steps through the unfused calls
-    u_start = tm.ev()
+    # the same number of steps with the update as a call of its own
+    s_start = tm.ev()
     for i in range(warmup + steps, warmup + 2 * steps):
+        rc |= step(i)
+    s_end = tm.ev()
+    torch.cuda.synchronize()
+    assert rc == 0, cd.last_error()
+    separate_ms = s_start.elapsed_time(s_end)
+    # and through separate sample and gather calls too
+    u_start = tm.ev()
+    for i in range(warmup + 2 * steps, warmup + 3 * steps):
         rc |= step_unfused(i)
     u_end = tm.ev()
     torch.cuda.synchronize()
     assert rc == 0, cd.last_error()
     unfused_ms = u_start.elapsed_time(u_end)
-    # instrumented pass: an event between consecutive calls
+    # instrumented passes: an event between consecutive calls
     evs = []
-    for i in range(warmup + 2 * steps, warmup + 3 * steps):
+    for i in range(warmup + 3 * steps, warmup + 4 * steps):
         e = [tm.ev()]
         ing(h, C.byref(trans[i]), stream)
         e.append(tm.ev())
@@ -219,7 +241,16 @@ def bench_dqn(steps, warmup):
         upd(h, pi[i], pp[i], B, stream)
         e.append(tm.ev())
         evs.append(e)
+    ui_durs = []
+    for i in range(warmup + 4 * steps, warmup + 5 * steps):
+        e0 = tm.ev()
+        uing(h, pi[i - 1], pp[i - 1], B, C.byref(trans[i]), stream)
+        e1 = tm.ev()
+        sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
+        ui_durs.append((e0, e1))
+    upd(h, pi[warmup + 5 * steps - 1], pp[warmup + 5 * steps - 1], B, stream)
     torch.cuda.synchronize()
+    ui_stats = _kernel_stats([a.elapsed_time(b) for a, b in ui_durs])
     assert buf.sync_check() == cd.OK, cd.last_error()
     # kernels alone, back to back between two events on the library's stream,
     # over the timed steps' own inputs: the fused sampler + gather (the dominant
@@ -288,6 +319,7 @@ def bench_dqn(steps, warmup):
                    "call": "conduit_nstep: targets plus the bootstrap frame stacks [512,4,84,84] fp32"},
         "B": B, "steps": steps, "warmup": warmup, "total_ms": total_ms, "host_enqueue_s": host_enqueue_s,
         "gather_b2b_ms": gather_b2b_ms, "fused_b2b_ms": fused_b2b_ms, "unfused_ms": unfused_ms,
+        "separate_ms": separate_ms, "update_ingest_call": ui_stats,
         "kernels": kern, "gather_bytes": gather_bytes, "fused_bytes": fused_bytes, "descent_bytes": descent_bytes,
         "valid_frames": valid, "prefill_s": prefill_s,
         "ingest_big": {"frames": 32768, "ms": ingest_big_ms,
@@ -1125,7 +1157,11 @@ def main():
                                "batch 512, PER alpha 0.6 beta 0.4; step = ingest 512 + sample 512 + "
                                "gather 512 -> [512,4,84,84] fp32 + priority update 512",
                    "capacity": 1_000_000, "batch": 512, "frame_stack": 4},
+        "step_calls": "conduit_update_ingest (the previous step's priority update, then this step's ingest) "
+                      "+ conduit_sample_gather",
+        "ms_per_step_separate_update": d["separate_ms"] / args.steps,
         "ms_per_step_unfused": d["unfused_ms"] / args.steps,
+        "update_ingest_call_us": d["update_ingest_call"]["mean_us"],
         "roofline": {"bound": "hbm", "kernel": "k_sample_gather<U8_F32> (one launch: 512 tree descents, "
                                                "IS weights, frame-stack gather 512 x 4 frames -> fp32; the "
                                                "dominant kernel of the step)",

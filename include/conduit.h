@@ -211,6 +211,21 @@ conduit_status conduit_ingest(conduit_buffer* buf, const conduit_transitions* t,
 conduit_status conduit_update_priorities(conduit_buffer* buf, const int64_t* idx, const uint32_t* prio,
                                          int64_t n, void* stream);
 
+
+
+/*
+ * The learner's priority update for its last batch followed by the actor's
+ * next transitions (App. C Invariant 2, then Sec. 2.2 off-policy ingestion):
+ * exactly conduit_update_priorities(buf, idx, prio, n_update) followed by
+ * conduit_ingest(buf, t), with the same arguments, effects and errors; either
+ * part may be empty (n_update = 0 or t->n = 0).  A dense buffer with both
+ * parts and at most 4,096 new rows takes one launch: one workgroup applies
+ * the updates and then the new rows' tree leaves, while the rest of the grid
+ * copies the rows and their columns (the update's latency hides behind the
+ * copy).  Otherwise the two operations are launched one after the other.
+ */
+conduit_status conduit_update_ingest(conduit_buffer* buf, const int64_t* idx, const uint32_t* prio, int64_t n_update,
+                                     const conduit_transitions* t, void* stream);
 /* ---------------------------------------------------------------------------
  * Sampling (Sec. 2.2 off-policy delivery: "samples from a persistent replay
  * dataset"; proportional prioritised replay)

@@ -126,6 +126,7 @@ SIGNATURES = {
     "conduit_gather_transform": (ST, [P, P, I64, P, P, P]),
     "conduit_sample_gather": (ST, [P, I64, P, P, P, P, P, P]),
     "conduit_gae": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
+    "conduit_update_ingest": (ST, [P, P, P, I64, P, P]),
     "conduit_nstep": (ST, [P, P, I64, I32_, F64, P, P, P, P, P, P, P]),
     "conduit_gae_truncated": (ST, [P, P, P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_gae_packed": (ST, [P, P, P, I64, I64, F64, F64, P, P, P]),
@@ -238,8 +239,8 @@ def conduit_buffer_destroy(handle):
     lib().conduit_buffer_destroy(handle)
 
 
-def conduit_ingest(handle, n, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None,
-                   offsets=None, aux=None, stream=None):
+def _transitions(n, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None, offsets=None,
+                 aux=None):
     t = Transitions()
     t.n = int(n)
     t.obs = _ptr(obs, None, "obs")
@@ -251,7 +252,22 @@ def conduit_ingest(handle, n, obs, action=None, reward=None, done=None, episode_
     t.episode_id = _ptr(episode_id, None, "episode_id")  # uint32 ids (int32 view accepted)
     t.step = _ptr(step, torch.int32, "step")
     t.prio = _ptr(prio, None, "prio")
+    return t
+
+
+def conduit_ingest(handle, n, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None,
+                   offsets=None, aux=None, stream=None):
+    t = _transitions(n, obs, action, reward, done, episode_id, step, prio, offsets, aux)
     _check(lib().conduit_ingest(handle, C.byref(t), _stream(stream)))
+
+
+def conduit_update_ingest(handle, idx, upd_prio, n, obs, action=None, reward=None, done=None, episode_id=None,
+                          step=None, prio=None, offsets=None, aux=None, stream=None):
+    """The priority update (idx, upd_prio), then the ingest of n rows, in one call."""
+    t = _transitions(n, obs, action, reward, done, episode_id, step, prio, offsets, aux)
+    k = idx.numel() if idx is not None else 0
+    _check(lib().conduit_update_ingest(handle, _ptr(idx, torch.int64, "idx"), _ptr(upd_prio, None, "upd_prio"), k,
+                                       C.byref(t), _stream(stream)))
 
 
 def conduit_update_priorities(handle, idx, prio, stream=None):
@@ -488,6 +504,12 @@ class ReplayBuffer:
 
     def update(self, idx, prio, stream=None):
         conduit_update_priorities(self.handle, idx, prio, stream)
+
+    def update_ingest(self, idx, upd_prio, obs, action=None, reward=None, done=None, episode_id=None, step=None,
+                      prio=None, offsets=None, aux=None, n=None, stream=None):
+        n = (offsets.numel() - 1 if offsets is not None else obs.shape[0]) if n is None else n
+        conduit_update_ingest(self.handle, idx, upd_prio, n, obs, action, reward, done, episode_id, step, prio,
+                              offsets, aux, stream)
 
     def sample(self, uniforms, idx_out=None, w_out=None, stream=None):
         B = uniforms.numel()

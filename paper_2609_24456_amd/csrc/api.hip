@@ -445,12 +445,8 @@ conduit_status conduit_buffer_get_info(const conduit_buffer* b, conduit_buffer_i
     return CONDUIT_OK;
 }
 
-conduit_status conduit_ingest(conduit_buffer* b, const conduit_transitions* t, void* stream) {
-    if (!b || !t) return fail(CONDUIT_EINVAL, "NULL buffer or transitions");
-    conduit_status st = check_flags(b->err_slot);
-    if (st != CONDUIT_OK) return st;
-    if (t->n < 0 || t->n > b->capacity) return fail(CONDUIT_EINVAL, "ingest n must be in [0, capacity]");
-    if (t->n == 0) return CONDUIT_OK;
+// Validated kernel arguments of an ingest (n > 0) at the buffer's current head.
+static conduit_status ingest_args(conduit_buffer* b, const conduit_transitions* t, IngestArgs* out) {
     const conduit_buffer_opts& o = b->opts;
     if (!t->obs) return fail(CONDUIT_EINVAL, "obs must not be NULL");
     if (reinterpret_cast<uintptr_t>(t->obs) % 4) return fail(CONDUIT_EINVAL, "obs must be 4-byte aligned");
@@ -458,7 +454,6 @@ conduit_status conduit_ingest(conduit_buffer* b, const conduit_transitions* t, v
     if (o.ragged && t->aux && reinterpret_cast<uintptr_t>(t->aux) % 4) return fail(CONDUIT_EINVAL, "aux must be 4-byte aligned");
     if (o.frame_stack > 1 && (!t->episode_id || !t->step))
         return fail(CONDUIT_EINVAL, "frame-stacking buffers need episode_id and step");
-    DeviceGuard g(b->device);
     IngestArgs a{};
     a.obs = b->obs;
     a.aux = b->aux;
@@ -489,11 +484,47 @@ conduit_status conduit_ingest(conduit_buffer* b, const conduit_transitions* t, v
     a.tree = b->tree;
     a.state = b->state;
     a.err = err_words(b->err_slot);
+    *out = a;
+    return CONDUIT_OK;
+}
+
+// the host-known ring state after n more transitions
+static void advance_ring(conduit_buffer* b, int64_t n) {
+    b->head = (b->head + n) % b->capacity;
+    b->size = b->size + n < b->capacity ? b->size + n : b->capacity;
+    b->total += n;
+}
+
+// Validated kernel arguments of a priority update (n > 0).
+static conduit_status update_args(conduit_buffer* b, const int64_t* idx, const uint32_t* prio, int64_t n,
+                                  UpdateArgs* out) {
+    if (!b->opts.prioritized) return fail(CONDUIT_EINVAL, "buffer was created without priorities");
+    if (!idx || !prio) return fail(CONDUIT_EINVAL, "idx and prio must not be NULL");
+    UpdateArgs a{};
+    a.tree = b->tree;
+    a.idx = idx;
+    a.prio = prio;
+    a.n = n;
+    a.size = b->size;
+    a.state = b->state;
+    a.err = err_words(b->err_slot);
+    *out = a;
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_ingest(conduit_buffer* b, const conduit_transitions* t, void* stream) {
+    if (!b || !t) return fail(CONDUIT_EINVAL, "NULL buffer or transitions");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (t->n < 0 || t->n > b->capacity) return fail(CONDUIT_EINVAL, "ingest n must be in [0, capacity]");
+    if (t->n == 0) return CONDUIT_OK;
+    IngestArgs a{};
+    st = ingest_args(b, t, &a);
+    if (st != CONDUIT_OK) return st;
+    DeviceGuard g(b->device);
     hipError_t e = launch_ingest(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "ingest launch");
-    b->head = (b->head + t->n) % b->capacity;
-    b->size = b->size + t->n < b->capacity ? b->size + t->n : b->capacity;
-    b->total += t->n;
+    advance_ring(b, t->n);
     return CONDUIT_OK;
 }
 
@@ -505,18 +536,48 @@ conduit_status conduit_update_priorities(conduit_buffer* b, const int64_t* idx, 
     if (!b->opts.prioritized) return fail(CONDUIT_EINVAL, "buffer was created without priorities");
     if (n < 0) return fail(CONDUIT_EINVAL, "n must be >= 0");
     if (n == 0) return CONDUIT_OK;
-    if (!idx || !prio) return fail(CONDUIT_EINVAL, "idx and prio must not be NULL");
-    DeviceGuard g(b->device);
     UpdateArgs a{};
-    a.tree = b->tree;
-    a.idx = idx;
-    a.prio = prio;
-    a.n = n;
-    a.size = b->size;
-    a.state = b->state;
-    a.err = err_words(b->err_slot);
+    st = update_args(b, idx, prio, n, &a);
+    if (st != CONDUIT_OK) return st;
+    DeviceGuard g(b->device);
     hipError_t e = launch_update(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "update launch");
+    return CONDUIT_OK;
+}
+
+// ingests of at most this many rows take the fused launch (its tree pass runs
+// in one workgroup)
+constexpr int64_t kFusedIngestMaxRows = 4096;
+
+conduit_status conduit_update_ingest(conduit_buffer* b, const int64_t* idx, const uint32_t* prio, int64_t n_update,
+                                     const conduit_transitions* t, void* stream) {
+    if (!b || !t) return fail(CONDUIT_EINVAL, "NULL buffer or transitions");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (!b->opts.prioritized) return fail(CONDUIT_EINVAL, "buffer was created without priorities");
+    if (n_update < 0) return fail(CONDUIT_EINVAL, "n_update must be >= 0");
+    if (t->n < 0 || t->n > b->capacity) return fail(CONDUIT_EINVAL, "ingest n must be in [0, capacity]");
+    UpdateArgs u{};
+    if (n_update > 0) {
+        st = update_args(b, idx, prio, n_update, &u);
+        if (st != CONDUIT_OK) return st;
+    }
+    IngestArgs a{};
+    if (t->n > 0) {
+        st = ingest_args(b, t, &a);
+        if (st != CONDUIT_OK) return st;
+    }
+    DeviceGuard g(b->device);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipSuccess;
+    if (n_update > 0 && t->n > 0 && !b->opts.ragged && t->n <= kFusedIngestMaxRows) {
+        e = launch_update_ingest(u, a, s);
+    } else {  // the same two operations, one launch each
+        if (n_update > 0) e = launch_update(u, s);
+        if (e == hipSuccess && t->n > 0) e = launch_ingest(a, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "update + ingest launch");
+    advance_ring(b, t->n);
     return CONDUIT_OK;
 }
 

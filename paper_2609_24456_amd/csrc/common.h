@@ -311,6 +311,8 @@ struct UpdateArgs {
 };
 
 hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
+// the update, then a dense ingest, in one launch (k_update_ingest.hip)
+hipError_t launch_update_ingest(const UpdateArgs& u, const IngestArgs& a, hipStream_t s);
 
 struct SampleArgs {
     TreeView tree;

@@ -81,16 +81,23 @@ def _check_nstep(buf, orc, idx_d, o_idx, n, gamma, xf_kind, row_shape, obs_kind=
 
 
 def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH,
-              nstep=None):
+              nstep=None, update_ingest=False):
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
     buf = _mk(C, (8,), torch.float32, action_bytes=4, placement=placement, weight_norm=weight_norm)
     orc = oracle.Replay(C, (8,), np.float32, act_bytes=4, buffer_norm=weight_norm == cd.WNORM_BUFFER)
 
-    def ingest(a, b):
-        buf.ingest(dev(cfg.obs[a:b]), action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]),
-                   done=dev(cfg.done[a:b]), episode_id=dev(cfg.episode[a:b]), step=dev(cfg.step[a:b]))
+    def ingest(a, b, pending=None):
+        """ingest rows [a, b); `pending` (idx, prio) is a priority update that
+        precedes it, applied through the one-call update + ingest"""
+        cols = dict(action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]), done=dev(cfg.done[a:b]),
+                    episode_id=dev(cfg.episode[a:b]), step=dev(cfg.step[a:b]))
+        if pending is not None:
+            buf.update_ingest(pending[0], dev(pending[1]), dev(cfg.obs[a:b]), **cols)
+            orc.update(pending[2], pending[1])
+        else:
+            buf.ingest(dev(cfg.obs[a:b]), **cols)
         orc.ingest(b - a, obs=cfg.obs[a:b], action=cfg.action[a:b], reward=cfg.reward[a:b], done=cfg.done[a:b],
                    episode=cfg.episode[a:b], step=cfg.step[a:b])
 
@@ -102,8 +109,10 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
     rew_out = torch.empty((B,), dtype=torch.float32, device="cuda")
     done_out = torch.empty((B,), dtype=torch.uint8, device="cuda")
     xf = cd.transform(cd.XF_NONE)
+    pending = None
     for it in range(iters):
-        ingest(pos, pos + n_in)
+        ingest(pos, pos + n_in, pending)
+        pending = None
         pos += n_in
         if fused:
             idx, w = buf.sample_gather(dev(u[it]), xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
@@ -113,9 +122,12 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
         o_idx, o_w = orc.sample(u[it])
         if nstep is not None:
             _check_nstep(buf, orc, idx, o_idx, nstep[0], nstep[1], cd.XF_NONE, (8,), torch.float32)
-        buf.update(idx, dev(prio[it]))
         o_obs, o_act, o_rew, o_done = orc.gather(o_idx)
-        orc.update(o_idx, prio[it])
+        if update_ingest and it + 1 < iters:  # applied with the next ingest
+            pending = (idx.clone(), prio[it], o_idx)
+        else:
+            buf.update(idx, dev(prio[it]))
+            orc.update(o_idx, prio[it])
         assert np.array_equal(host(idx), o_idx), it
         assert_weights_close(host(w), o_w)
         assert np.array_equal(host(obs_out).view(np.uint8).reshape(B, -1), o_obs.reshape(B, -1).view(np.uint8)), it
@@ -151,6 +163,14 @@ def test_tiny_config_fused_sample_gather():
     _run_tiny(prefill=0, iters=100, fused=True)
 
 
+@pytest.mark.parametrize("fused", [False, True])
+def test_tiny_config_update_ingest_one_call(fused):
+    # each iteration's priority update applied together with the next ingest
+    print(f"tiny config: update + ingest in one call, fused sample={fused}", flush=True)
+    _run_tiny(prefill=0, iters=60, seed_shift=11, fused=fused, update_ingest=True)
+    _run_tiny(prefill=20000, iters=30, seed_shift=12, fused=fused, update_ingest=True)
+
+
 @pytest.mark.parametrize("n,gamma", [(1, 0.99), (3, 0.99), (63, 0.9)])
 def test_tiny_config_nstep_targets(n, gamma):
     print(f"tiny config: {n}-step targets", flush=True)
@@ -178,7 +198,7 @@ def test_tiny_config_payload_in_pinned_host_memory(fused):
 # configuration 1 (DQN, frame stack 4, u8 -> fp32/255) at reduced capacity
 # ----------------------------------------------------------------------------
 def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False,
-            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH, nstep=None):
+            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH, nstep=None, update_ingest=False):
     """Drive GPU buffer and oracle through the same DQN stream; the oracle keeps
     metadata only and its observation rows are regenerated for the slots a
     gather reads."""
@@ -198,11 +218,14 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
     orc = oracle.Replay(cap, (84, 84), np.uint8, act_bytes=4, frame_stack=K, obs_storage=obs_store,
                         buffer_norm=weight_norm == cd.WNORM_BUFFER)
 
-    def ingest(a, b, with_prio):
+    def ingest(a, b, with_prio, pending=None):
         p = cfg.prio[a:b] if with_prio else None
-        buf.ingest(cfg.frames(a, b - a, "cuda"), action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]),
-                   done=dev(cfg.done[a:b]), episode_id=dev(cfg.episode[a:b]), step=dev(cfg.step[a:b]),
-                   prio=dev(p) if p is not None else None)
+        cols = dict(action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]), done=dev(cfg.done[a:b]),
+                    episode_id=dev(cfg.episode[a:b]), step=dev(cfg.step[a:b]), prio=dev(p) if p is not None else None)
+        if pending is not None:  # the previous iteration's update, in the same call
+            buf.update_ingest(pending[0], pending[1], cfg.frames(a, b - a, "cuda"), **cols)
+        else:
+            buf.ingest(cfg.frames(a, b - a, "cuda"), **cols)
         orc.ingest(b - a, obs=None, action=cfg.action[a:b], reward=cfg.reward[a:b], done=cfg.done[a:b],
                    episode=cfg.episode[a:b], step=cfg.step[a:b], prio=p)
 
@@ -214,15 +237,20 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
     rew_out = torch.empty((batch,), dtype=torch.float32, device="cuda")
     done_out = torch.empty((batch,), dtype=torch.uint8, device="cuda")
     xf = cd.transform(cd.XF_U8_F32)
+    pending = None
     for it in range(iters):
-        ingest(pos, pos + batch, with_prio=False)
+        ingest(pos, pos + batch, with_prio=False, pending=pending)
+        pending = None
         pos += batch
         if fused:
             idx, w = buf.sample_gather(dev(u[it]), xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
         else:
             idx, w = buf.sample(dev(u[it]))
             buf.gather(idx, xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
-        buf.update(idx, dev(prio[it]))
+        if update_ingest and it + 1 < iters:
+            pending = (idx.clone(), dev(prio[it]))
+        else:
+            buf.update(idx, dev(prio[it]))
         o_idx, o_w = orc.sample(u[it])
         assert np.array_equal(host(idx), o_idx), it
         assert_weights_close(host(w), o_w)
@@ -273,6 +301,13 @@ def test_dqn_short_episodes_zero_fill():
 def test_dqn_fused_sample_gather(short):
     print(f"dqn: fused sample+gather, cap 3000, short episodes={short}", flush=True)
     run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused=True)
+
+
+@pytest.mark.parametrize("short", [False, True])
+def test_dqn_update_ingest_one_call(short):
+    print(f"dqn: update + ingest in one call, cap 3000, short episodes={short}", flush=True)
+    run_dqn(cap=3000, prefill=3500, iters=4, batch=512, chunk=700, short_episodes=short, fused=True,
+            update_ingest=True)
 
 
 @pytest.mark.parametrize("n,short", [(1, True), (3, True), (5, False)])
@@ -420,6 +455,42 @@ def test_zero_priorities_and_batch_larger_than_size():
     assert np.array_equal(host(idx), o_idx)
     assert set(host(idx).tolist()) <= {2, 7}
     assert_weights_close(host(w), o_w)
+    buf.close()
+
+
+@pytest.mark.parametrize("given_prio", [False, True])
+def test_update_ingest_one_call_edge_cases(given_prio):
+    # updates with duplicates and slots the same call's ingest evicts, on a
+    # wrapped ring, with and without caller-given priorities on the new rows
+    print(f"update + ingest edge cases, given priorities={given_prio}", flush=True)
+    rng = np.random.default_rng(91)
+    cap = 300
+    buf = _mk(cap, (4,), torch.uint8, action_bytes=0)
+    orc = oracle.Replay(cap, (4,), np.uint8, act_bytes=0)
+    pos = 0
+    for rnd in range(12):
+        n = int(rng.integers(1, 200))
+        rows = rng.integers(0, 256, (n, 4), dtype=np.uint8)
+        p_new = synth.quantise_priority(rng.lognormal(0, 2, n)) if given_prio else None
+        if orc.size:
+            k = int(rng.integers(1, 400))
+            # half of the updates hit the slots this ingest is about to evict
+            evict = (orc.head + rng.integers(0, n, k)) % cap
+            idx = np.where(rng.random(k) < 0.5, evict, rng.integers(0, orc.size, k)).astype(np.int64)
+            idx = np.minimum(idx, orc.size - 1)
+            up = synth.quantise_priority(rng.lognormal(1, 2, k))
+            buf.update_ingest(dev(idx), dev(up), dev(rows), prio=dev(p_new) if given_prio else None)
+            orc.update(idx, up)
+        else:
+            buf.ingest(dev(rows), prio=dev(p_new) if given_prio else None)
+        orc.ingest(n, obs=rows, prio=p_new)
+        pos += n
+        assert buf.sync_check() == cd.OK, cd.last_error()
+        assert np.array_equal(read_col(buf, cd.COL_LEAVES, cap * 4, np.uint32), orc.leaf), rnd
+        assert tree_consistent(buf, cap) == orc.total_priority(), rnd
+        assert int(read_col(buf, cd.COL_MAX_PRIO, 4, np.uint32)[0]) == orc.max_prio, rnd
+        info = buf.info()
+        assert (info.head, info.size, info.total) == (orc.head, orc.size, orc.total)
     buf.close()
 
 
