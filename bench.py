@@ -107,8 +107,9 @@ def bench_dqn(steps, warmup):
     L = cd.lib()
     stream = C.c_void_p(torch.cuda.current_stream().cuda_stream)
     Cap, B, K, prefill, chunk = 1_000_000, 512, 4, 1_050_000, 4096
-    # passes: timed headline, separate-update, unfused, two instrumented
-    iters = warmup + 5 * steps
+    # passes: timed headline, separate-update and unfused (each after one
+    # untimed step of its own), two instrumented
+    iters = warmup + 5 * steps + 2
     cfg = synth.DQN(prefill + iters * B)
     buf = cd.ReplayBuffer(Cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4)
     t0 = time.time()
@@ -194,11 +195,12 @@ def bench_dqn(steps, warmup):
         r |= upd(h, pi[i], pp[i], B, stream)
         return r
 
-    for i in range(warmup - 1):
-        assert step(i) == 0, cd.last_error()
-    # the last warm-up step leaves its priority update to the first timed step
-    rc = ing(h, C.byref(trans[warmup - 1]), stream)
-    rc |= sgat(h, B, pu[warmup - 1], pi[warmup - 1], pw[warmup - 1], xfr, lbr, stream)
+    # warm-up through the timed step's own calls (every kernel loaded before
+    # the clock starts); its last update is left to the first timed step
+    rc = ing(h, C.byref(trans[0]), stream)
+    rc |= sgat(h, B, pu[0], pi[0], pw[0], xfr, lbr, stream)
+    for i in range(1, warmup):
+        rc |= step_ui(i)
     assert rc == 0, cd.last_error()
     torch.cuda.synchronize()
     # timed pass: each step applies the previous step's update with its own
@@ -215,24 +217,31 @@ def bench_dqn(steps, warmup):
     assert rc == 0, cd.last_error()
     total_ms = e_start.elapsed_time(e_end)
     # the same number of steps with the update as a call of its own
+    p1 = warmup + steps
+    rc |= step(p1)  # one untimed step first
+    torch.cuda.synchronize()
     s_start = tm.ev()
-    for i in range(warmup + steps, warmup + 2 * steps):
+    for i in range(p1 + 1, p1 + 1 + steps):
         rc |= step(i)
     s_end = tm.ev()
     torch.cuda.synchronize()
     assert rc == 0, cd.last_error()
     separate_ms = s_start.elapsed_time(s_end)
     # and through separate sample and gather calls too
+    p2 = p1 + 1 + steps
+    rc |= step_unfused(p2)
+    torch.cuda.synchronize()
     u_start = tm.ev()
-    for i in range(warmup + 2 * steps, warmup + 3 * steps):
+    for i in range(p2 + 1, p2 + 1 + steps):
         rc |= step_unfused(i)
     u_end = tm.ev()
     torch.cuda.synchronize()
     assert rc == 0, cd.last_error()
     unfused_ms = u_start.elapsed_time(u_end)
     # instrumented passes: an event between consecutive calls
+    p3 = p2 + 1 + steps
     evs = []
-    for i in range(warmup + 3 * steps, warmup + 4 * steps):
+    for i in range(p3, p3 + steps):
         e = [tm.ev()]
         ing(h, C.byref(trans[i]), stream)
         e.append(tm.ev())
@@ -242,13 +251,14 @@ def bench_dqn(steps, warmup):
         e.append(tm.ev())
         evs.append(e)
     ui_durs = []
-    for i in range(warmup + 4 * steps, warmup + 5 * steps):
+    p4 = p3 + steps
+    for i in range(p4, p4 + steps):
         e0 = tm.ev()
         uing(h, pi[i - 1], pp[i - 1], B, C.byref(trans[i]), stream)
         e1 = tm.ev()
         sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
         ui_durs.append((e0, e1))
-    upd(h, pi[warmup + 5 * steps - 1], pp[warmup + 5 * steps - 1], B, stream)
+    upd(h, pi[p4 + steps - 1], pp[p4 + steps - 1], B, stream)
     torch.cuda.synchronize()
     ui_stats = _kernel_stats([a.elapsed_time(b) for a, b in ui_durs])
     assert buf.sync_check() == cd.OK, cd.last_error()
@@ -531,7 +541,9 @@ def bench_stress(dims=(128, 1000, 5000, 10000, 20000), iters=20):
     each transition dimension d (obs and next_obs, d fp32 each, 8d bytes per
     slot) a full buffer (up to 160 GB at d = 20,000), then iterations of
     ingest 512 + sample + gather 512 (one call, IS weights, no transform) +
-    update 512, timed as back-to-back launches with prepared arguments."""
+    update 512, timed as back-to-back launches with prepared arguments; each
+    update is applied with the next iteration's ingest in one call
+    (conduit_update_ingest), the separate-call iteration reported beside."""
     import numpy as np
     import torch
     import synth
@@ -586,7 +598,18 @@ def bench_stress(dims=(128, 1000, 5000, 10000, 20000), iters=20):
             calls.append(lambda i=i: L.conduit_sample_gather(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream))
             calls.append(lambda i=i: L.conduit_update_priorities(h, pi[i], pp[i], B, stream))
         _b2b_ms(calls[:3])
-        iter_ms = _b2b_ms(calls) * 3
+        iter_sep_ms = _b2b_ms(calls) * 3
+        # each update applied with the next iteration's ingest in one call
+        calls = []
+        for i in range(iters):
+            if i == 0:
+                calls.append(lambda: L.conduit_ingest(h, C.byref(structs[0]), stream))
+            else:
+                calls.append(lambda i=i: L.conduit_update_ingest(h, pi[i - 1], pp[i - 1], B, C.byref(structs[i]),
+                                                                 stream))
+            calls.append(lambda i=i: L.conduit_sample_gather(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream))
+        calls.append(lambda: L.conduit_update_priorities(h, pi[iters - 1], pp[iters - 1], B, stream))
+        iter_ms = _b2b_ms(calls) * len(calls) / iters
         ing_ms = _b2b_ms([lambda i=i: L.conduit_ingest(h, C.byref(structs[i]), stream) for i in range(iters)])
         sg_ms = _b2b_ms([lambda i=i: L.conduit_sample_gather(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
                          for i in range(iters)])
@@ -598,7 +621,7 @@ def bench_stress(dims=(128, 1000, 5000, 10000, 20000), iters=20):
         ing_bytes = B * (2 * row + 2 * 17 + 8)
         sg_bytes = B * (2 * row + 8 + 2 * (4 + 4))
         res[f"d={d}"] = {"buffer_GB": Cap * row / 1e9, "prefill_s": prefill_s, "iteration_us": iter_ms * 1e3,
-                         "sampled_per_s": B / (iter_ms / 1e3),
+                         "sampled_per_s": B / (iter_ms / 1e3), "iteration_us_separate_update": iter_sep_ms * 1e3,
                          "ingest_512_us": ing_ms * 1e3, "ingest_GBps": ing_bytes / ing_ms / 1e6,
                          "sample_gather_512_us": sg_ms * 1e3, "sample_gather_GBps": sg_bytes / sg_ms / 1e6}
     return res
@@ -1006,8 +1029,10 @@ def bench_tiny(iters=100):
     pi = [idx[i].data_ptr() for i in range(iters)]
     pw = [w[i].data_ptr() for i in range(iters)]
     ing, sgat, upd = L.conduit_ingest, L.conduit_sample_gather, L.conduit_update_priorities
+    uing = L.conduit_update_ingest
     tm = Timer()
     torch.cuda.synchronize()
+    # separate calls: ingest, sample + gather, update
     e0 = tm.ev()
     h0 = time.perf_counter()
     rc = 0
@@ -1021,9 +1046,33 @@ def bench_tiny(iters=100):
     assert rc == 0, cd.last_error()
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
+    ms_sep = e0.elapsed_time(e1)
+    # the same iterations on a fresh buffer, each update applied with the next
+    # ingest in one call (the last one after the loop, inside the clock)
+    buf = cd.ReplayBuffer(cfg.capacity, (8,), torch.float32, action_bytes=4)
+    h = C.c_void_p(buf.handle)
+    torch.cuda.synchronize()
+    e0 = tm.ev()
+    h0 = time.perf_counter()
+    for i in range(iters):
+        if i == 0:
+            rc |= ing(h, trans[i], stream)
+        else:
+            rc |= uing(h, pi[i - 1], pp[i - 1], B, trans[i], stream)
+        rc |= sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
+    rc |= upd(h, pi[iters - 1], pp[iters - 1], B, stream)
+    e1 = tm.ev()
+    host_ui = time.perf_counter() - h0
+    torch.cuda.synchronize()
+    assert rc == 0, cd.last_error()
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
     ms = e0.elapsed_time(e1)
-    return {"iterations": iters, "us_per_iteration": ms * 1e3 / iters, "launches_per_iteration": 3,
-            "host_enqueue_us_per_iteration": host_s * 1e6 / iters, "sampled_per_s": iters * B / (ms / 1e3)}
+    return {"iterations": iters, "us_per_iteration": ms * 1e3 / iters, "launches_per_iteration": 2,
+            "calls": "conduit_update_ingest (previous update + this ingest) + conduit_sample_gather",
+            "host_enqueue_us_per_iteration": host_ui * 1e6 / iters, "sampled_per_s": iters * B / (ms / 1e3),
+            "separate_calls": {"us_per_iteration": ms_sep * 1e3 / iters, "launches_per_iteration": 3,
+                               "host_enqueue_us_per_iteration": host_s * 1e6 / iters}}
 
 
 # ----------------------------------------------------------------------------
