@@ -72,10 +72,14 @@ class Timer:
         return e
 
 
-def _b2b_ms(calls, reps=1):
+def _b2b_ms(calls, reps=1, warm=2):
     """Milliseconds per call of `calls` (zero-argument callables that enqueue
-    on the library's stream), launched back to back between two events."""
+    on the library's stream), launched back to back between two events, after
+    `warm` untimed calls (a kernel's first launch loads its code)."""
     import torch
+    for f in calls[:warm]:
+        f()
+    torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     rc = 0
