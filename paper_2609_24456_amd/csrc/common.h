@@ -59,37 +59,38 @@ __device__ __forceinline__ void flag_error(uint32_t* err, int kind) {
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, kWave);
-    return x;
+// DPP controls: shift right within a row of 16 lanes, and broadcast of lane 15
+// (31) of a row into the next row (rows 1 and 3; rows 2 and 3)
+constexpr int kDppRowShr = 0x110, kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+
+// x moved by one DPP control; lanes with no source, or in rows the row mask
+// leaves out, read `id`
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x, uint32_t id) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)id, (int)x, CTRL, ROWS, 0xf, false);
 }
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t x) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        uint64_t y = __shfl_xor(x, off, kWave);
-        x = y > x ? y : x;
-    }
-    return x;
+// Reduction of a 32-bit value over the whole wavefront (every lane active) with
+// DPP moves instead of LDS permutes: after the row shifts and the two row
+// broadcasts lane 63 holds the combination of all 64 lanes, returned to every
+// lane.  `id` is the identity of `op`.
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t x, uint32_t id, Op op) {
+    x = op(x, dpp_u32<kDppRowShr + 1, 0xf>(x, id));
+    x = op(x, dpp_u32<kDppRowShr + 2, 0xf>(x, id));
+    x = op(x, dpp_u32<kDppRowShr + 4, 0xf>(x, id));
+    x = op(x, dpp_u32<kDppRowShr + 8, 0xf>(x, id));
+    x = op(x, dpp_u32<kDppRowBcast15, 0xa>(x, id));
+    x = op(x, dpp_u32<kDppRowBcast31, 0xc>(x, id));
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
 }
 
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        uint32_t y = __shfl_xor(x, off, kWave);
-        x = y < x ? y : x;
-    }
-    return x;
+    return wave_reduce_u32(x, 0xffffffffu, [](uint32_t p, uint32_t q) { return q < p ? q : p; });
 }
 
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-        uint32_t y = __shfl_xor(x, off, kWave);
-        x = y > x ? y : x;
-    }
-    return x;
+    return wave_reduce_u32(x, 0u, [](uint32_t p, uint32_t q) { return q > p ? q : p; });
 }
 
 // value of a 64-bit register in a wave-uniform lane
@@ -113,13 +114,12 @@ __device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
 // last lane of row 0 is broadcast into row 1 and of row 2 into row 3
 // (row_bcast:15), and lane 31 into rows 2 and 3 (row_bcast:31).
 __device__ __forceinline__ uint64_t wave_inclusive_scan_u64(uint64_t x) {
-    constexpr int kRowShr = 0x110, kRowBcast15 = 0x142, kRowBcast31 = 0x143;
-    x += dpp_u64<kRowShr + 1, 0xf, 0xf>(x);
-    x += dpp_u64<kRowShr + 2, 0xf, 0xf>(x);
-    x += dpp_u64<kRowShr + 4, 0xf, 0xf>(x);
-    x += dpp_u64<kRowShr + 8, 0xf, 0xf>(x);
-    x += dpp_u64<kRowBcast15, 0xa, 0xf>(x);
-    x += dpp_u64<kRowBcast31, 0xc, 0xf>(x);
+    x += dpp_u64<kDppRowShr + 1, 0xf, 0xf>(x);
+    x += dpp_u64<kDppRowShr + 2, 0xf, 0xf>(x);
+    x += dpp_u64<kDppRowShr + 4, 0xf, 0xf>(x);
+    x += dpp_u64<kDppRowShr + 8, 0xf, 0xf>(x);
+    x += dpp_u64<kDppRowBcast15, 0xa, 0xf>(x);
+    x += dpp_u64<kDppRowBcast31, 0xc, 0xf>(x);
     return x;
 }
 

@@ -143,26 +143,64 @@ __device__ __forceinline__ void push_wave_deltas(const TreeView& tr, int64_t slo
     }
 }
 
-// TREE = false: the scalar columns only (the tree part runs elsewhere).
-// running >= 0: the running maximum priority new rows enter with (else read
-// from the device state).
-template <bool TREE = true>
-__device__ void ingest_meta(const IngestArgs& a, int64_t block, int tid, int64_t running = -1) {
+constexpr int kRaiseUnroll = 8;  // update entries per lane per pass, all loads in flight
+
+// An update list whose priorities raise the running maximum (n = 0: none).
+struct RaiseList {
+    const int64_t* idx;
+    const uint32_t* prio;
+    int64_t n;
+    int64_t size;  // valid indices are [0, size)
+};
+
+// max(stored running maximum, every valid priority of u) by one wavefront: the
+// running maximum after the update list has been applied.  A list of up to 512
+// entries is one memory round trip.
+__device__ __forceinline__ uint32_t raised_max(const DeviceState* state, const RaiseList& u) {
+    const uint32_t cur = state->max_prio;
+    uint32_t m = 0;
+    for (int64_t base = 0; base < u.n; base += (int64_t)kWave * kRaiseUnroll) {
+        int64_t s[kRaiseUnroll];
+        uint32_t p[kRaiseUnroll];
+#pragma unroll
+        for (int r = 0; r < kRaiseUnroll; ++r) {
+            const int64_t k = base + (int64_t)r * kWave + lane_id();
+            s[r] = k < u.n ? u.idx[k] : -1;
+            p[r] = k < u.n ? u.prio[k] : 0u;
+        }
+#pragma unroll
+        for (int r = 0; r < kRaiseUnroll; ++r)
+            if (s[r] >= 0 && s[r] < u.size && p[r] > m) m = p[r];
+    }
+    m = wave_max_u32(m);
+    return cur > m ? cur : m;
+}
+
+// The scalar columns, leaf and tree deltas of one lane's row.  Rows without a
+// caller priority enter with the running maximum: the stored one, raised by the
+// priorities of `raise` when it is not empty (an update applied in the same
+// launch); those loads go out together with the row's own.
+__device__ __forceinline__ void ingest_meta(const IngestArgs& a, int64_t block, int tid,
+                                            const RaiseList raise = RaiseList{nullptr, nullptr, 0, 0}) {
     const int64_t t = block * kIngestThreads + tid;
     int64_t j, slot;
     bool valid;
     ingest_row(a, t, &j, &slot, &valid);
-    const bool tree = TREE && a.prioritized;
+    const bool tree = a.prioritized;
     const uint64_t any_valid = __ballot(valid);
     if (any_valid == 0) return;  // whole wavefront past the end (wave-uniform)
 
     // every load of the lane's row is issued before its first store (lanes past
-    // the end read row 0 and store nothing): one memory round trip in all
+    // the end read row 0 and store nothing): one memory round trip in all.  The
+    // old leaf is read unconditionally (slot 0 for lanes past the end) so that
+    // no select of its value waits for it here.
     uint64_t delta = 0;
     uint32_t p_seen = 0;
     const int64_t jj = valid ? j : 0;
-    const uint32_t old = (valid && tree) ? a.tree.leaves[slot] : 0u;
-    const uint32_t p = !tree ? 0u : a.src_prio ? a.src_prio[jj] : running >= 0 ? (uint32_t)running : a.state->max_prio;
+    const uint32_t old = tree ? a.tree.leaves[valid ? slot : 0] : 0u;
+    const uint32_t p_row = tree && a.src_prio ? a.src_prio[jj] : 0u;
+    const bool raised = raise.n > 0;
+    const uint32_t p_state = tree && !a.src_prio && !raised ? a.state->max_prio : 0u;
     const float rew = a.src_reward ? a.src_reward[jj] : 0.0f;
     const uint8_t dn = a.src_done ? a.src_done[jj] : (uint8_t)0;
     const uint32_t ep = a.src_episode ? a.src_episode[jj] : 0u;
@@ -174,6 +212,7 @@ __device__ void ingest_meta(const IngestArgs& a, int64_t block, int tid, int64_t
 #pragma unroll
     for (int c = 0; c < kActWords; ++c)
         w[c] = c < words ? reinterpret_cast<const uint32_t*>(a.src_action + jj * a.action_bytes)[c] : 0u;
+    const uint32_t p = !tree ? 0u : a.src_prio ? p_row : raised ? raised_max(a.state, raise) : p_state;
     if (valid) {
         if (a.action_bytes > 0) {
             uint8_t* dst = a.action + slot * a.action_bytes;

@@ -25,32 +25,6 @@ namespace {
 
 constexpr int kSubs = kUpdateThreads / kIngestThreads;
 
-constexpr int kMaxUnroll = 8;  // update entries per lane per pass, all loads in flight
-
-// max(running maximum, every valid update priority), by one wavefront; a batch
-// of up to 512 updates is one memory round trip
-__device__ uint32_t raised_max(const UpdateArgs& u) {
-    // the update block may already have raised the stored maximum with the
-    // same priorities: max() makes the order irrelevant
-    const uint32_t cur = u.state->max_prio;
-    uint32_t m = 0;
-    for (int64_t base = 0; base < u.n; base += (int64_t)kWave * kMaxUnroll) {
-        int64_t s[kMaxUnroll];
-        uint32_t p[kMaxUnroll];
-#pragma unroll
-        for (int r = 0; r < kMaxUnroll; ++r) {
-            const int64_t k = base + (int64_t)r * kWave + lane_id();
-            s[r] = k < u.n ? u.idx[k] : -1;
-            p[r] = k < u.n ? u.prio[k] : 0u;
-        }
-#pragma unroll
-        for (int r = 0; r < kMaxUnroll; ++r)
-            if (s[r] >= 0 && s[r] < u.size && p[r] > m) m = p[r];
-    }
-    m = wave_max_u32(m);
-    return cur > m ? cur : m;
-}
-
 template <typename V>
 __global__ __launch_bounds__(kUpdateThreads) void k_update_ingest(UpdateArgs u, IngestArgs a, int64_t meta_subs,
                                                                   int64_t copy_subs) {
@@ -67,8 +41,10 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update_ingest(UpdateArgs u, 
     const int64_t sub = (int64_t)(blockIdx.x - 1) * kSubs + threadIdx.x / kIngestThreads;
     const int tid = (int)(threadIdx.x % kIngestThreads);
     if (sub < meta_subs) {
-        const int64_t running = a.src_prio ? -1 : (int64_t)raised_max(u);
-        ingest_meta<true>(a, sub, tid, running);
+        // the update block may already have raised the stored maximum with the
+        // same priorities: raised_max takes max() over both, so the order of
+        // the two parts does not matter
+        ingest_meta(a, sub, tid, RaiseList{u.idx, u.prio, u.n, u.size});
     } else if (sub - meta_subs < copy_subs) {
         copy_dense<V>(a, sub - meta_subs, tid);
     }

@@ -58,8 +58,10 @@ __device__ uint32_t update_pass(const UpdateArgs& a, uint32_t* keys, int32_t* ow
         }
         // the old leaf is needed only by the winner, but its load is issued now so
         // it overlaps the LDS dedupe and the quantiser (chunks before this one
-        // finished their leaf writes before the barrier above)
-        const uint32_t old = valid ? tr.leaves[slot] : 0u;
+        // finished their leaf writes before the barrier above); unconditional,
+        // from slot 0 for an invalid entry, so that no select of its value makes
+        // the lane wait for it here
+        const uint32_t old = tr.leaves[valid ? slot : 0];
         uint32_t h = 0;
         if (valid) {
             pmax = p > pmax ? p : pmax;
@@ -84,7 +86,11 @@ __device__ uint32_t update_pass(const UpdateArgs& a, uint32_t* keys, int32_t* ow
             tr.leaves[slot] = q;
             const uint64_t delta = (uint64_t)q - (uint64_t)old;  // modulo 2^64
             if (delta) {
-                for (int l = 1; l <= tr.depth; ++l) {
+                // unrolled over the largest depth: the per-level arguments are
+                // loaded together rather than one level at a time
+#pragma unroll
+                for (int l = 1; l <= kMaxLevels; ++l) {
+                    if (l > tr.depth) break;
                     const uint64_t node = (uint64_t)slot >> (kFanoutLog2 * l);
                     const int off = tr.lds_offset[l];
                     if (off >= 0) atomicAdd(&bins[off + node], (unsigned long long)delta);
@@ -99,7 +105,9 @@ __device__ uint32_t update_pass(const UpdateArgs& a, uint32_t* keys, int32_t* ow
 
 // Flush the LDS-accumulated levels into the tree (after an LDS barrier).
 __device__ void flush_bins(const TreeView& tr, const unsigned long long* bins) {
-    for (int l = 1; l <= tr.depth; ++l) {
+#pragma unroll
+    for (int l = 1; l <= kMaxLevels; ++l) {
+        if (l > tr.depth) break;
         const int off = tr.lds_offset[l];
         if (off < 0) continue;
         const int nodes = (int)tr.nodes[l];
