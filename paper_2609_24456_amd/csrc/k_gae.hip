@@ -11,9 +11,12 @@
 //      R_t = A_t + V_t.
 // All arithmetic is fp64; outputs are rounded to fp32 once.
 //
-// Time-major rollouts [T, E] (k_gae): a workgroup owns 8 environments x 64
-// chunks of 16 steps (lanes run fastest over environments, so every load
-// instruction of a wavefront reads eight 32-byte runs).  Padded sequences
+// Time-major rollouts [T, E]: a workgroup owns 8 environments and walks the
+// rollout in passes of 2048 steps.  k_gae_v4 (E a multiple of 4, aligned rows)
+// gives each lane 4 environments as 16-byte vectors and 16 steps, 128 chunks
+// per pass; k_gae (any E) gives each lane one environment and 32 steps, 64
+// chunks per pass, lanes fastest over environments so every load instruction of
+// a wavefront reads eight 32-byte runs.  Padded sequences
 // [B, Lmax] (k_gae_packed): one workgroup per sequence, 256 chunks along t.
 #include "common.h"
 
@@ -23,8 +26,8 @@ namespace {
 
 constexpr int kEnvs = 8;                      // environments per workgroup (32-byte runs)
 constexpr int kChunks = 64;                   // chunks per environment and super-chunk
-constexpr int kChunkLen = 16;                 // steps per chunk, held in registers
-constexpr int kSuper = kChunks * kChunkLen;   // 1024 steps per pass
+constexpr int kChunkLen = 32;                 // steps per chunk, held in registers
+constexpr int kSuper = kChunks * kChunkLen;   // 2048 steps per pass: a PPO rollout in one
 constexpr int kTmThreads = kEnvs * kChunks;   // 512: leaves 256 VGPRs per lane
 static_assert(kGaeMaxEnvs * kSuper * 4 <= (1ll << 32), "byte offsets of a slab fit 32 bits");
 
@@ -47,14 +50,15 @@ __device__ __forceinline__ void gae_step(double r, double v, double v_next, uint
 }
 
 // Time-major GAE.  A workgroup owns 8 environments and walks the rollout in
-// super-chunks of 1024 steps from the end; the carry (A at the start of the
+// super-chunks of 2048 steps from the end; the carry (A at the start of the
 // later super-chunk) is kept per environment in LDS.  Within a super-chunk every
-// lane loads its 16 steps (reward, value, done) at once into registers, folds
-// them into (P, S), joins the suffix scan and replays from registers.
+// lane loads its 32 steps (reward, value, done) at once into registers, folds
+// them into (P, S), joins the suffix scan and replays from registers.  The scan
+// ping-pongs between two LDS buffers, so each of its rounds needs one barrier.
 template <bool TRUNC>
 __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
-    __shared__ double sP[kChunks][kEnvs];
-    __shared__ double sS[kChunks][kEnvs];
+    __shared__ double sP[2][kChunks][kEnvs];
+    __shared__ double sS[2][kChunks][kEnvs];
     __shared__ double carry_s[kEnvs];
     const int el = threadIdx.x % kEnvs;
     const int c = threadIdx.x / kEnvs;
@@ -78,16 +82,30 @@ __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
         uint8_t d[kChunkLen];
         uint8_t tr[TRUNC ? kChunkLen : 1];
         float fv[TRUNC ? kChunkLen : 1];
-#pragma unroll
-        for (int k = 0; k < kChunkLen; ++k) {
-            const int lt = c * kChunkLen + k < last_local ? c * kChunkLen + k : last_local;
-            const uint32_t off = (uint32_t)lt * E32 + e32;
-            r[k] = rb[off];
-            v[k] = vb ? vb[off] : 0.0f;
-            d[k] = db[off];
+        // step k of the lane: row `row` (uniform, elements from the slab) plus
+        // the lane's offset `lo` from that row
+        auto load_step = [&](int k, int64_t row, uint32_t lo) {
+            r[k] = (rb + row)[lo];
+            v[k] = vb ? (vb + row)[lo] : 0.0f;
+            d[k] = (db + row)[lo];
             if constexpr (TRUNC) {
-                tr[k] = a.truncated[sbase + off];
-                fv[k] = a.final_value[sbase + off];
+                tr[TRUNC ? k : 0] = (a.truncated + sbase + row)[lo];
+                fv[TRUNC ? k : 0] = (a.final_value + sbase + row)[lo];
+            }
+        };
+        if (sc * kSuper + kSuper <= T) {
+            // a full super-chunk: step k of every lane lies k rows below the
+            // lane's first step, so one lane offset serves all of its loads and
+            // the rows advance in scalar registers
+            const uint32_t lo = (uint32_t)(c * kChunkLen) * E32 + e32;
+#pragma unroll
+            for (int k = 0; k < kChunkLen; ++k) load_step(k, (int64_t)k * E, lo);
+        } else {
+            // the last, partial one: steps past the end re-read the last row
+#pragma unroll
+            for (int k = 0; k < kChunkLen; ++k) {
+                const int lt = c * kChunkLen + k < last_local ? c * kChunkLen + k : last_local;
+                load_step(k, 0, (uint32_t)lt * E32 + e32);
             }
         }
         const int64_t t1 = t0 + kChunkLen;  // first step after this chunk
@@ -108,28 +126,27 @@ __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
             }
         }
         __syncthreads();  // carry_s of the previous pass is final; sP/sS free
-        sP[c][el] = P;
-        sS[c][el] = S;
+        int cur = 0;
+        sP[cur][c][el] = P;
+        sS[cur][c][el] = S;
         __syncthreads();
+        // round r reads the buffer written in round r - 1 and writes the other
+        // one, whose readers all passed the barrier that ended round r - 1
         for (int off = 1; off < kChunks; off <<= 1) {
-            const bool has = c + off < kChunks;
-            double p2 = 1.0, s2 = 0.0;
-            if (has) {
-                p2 = sP[c + off][el];
-                s2 = sS[c + off][el];
-            }
-            __syncthreads();
-            if (has) {
+            if (c + off < kChunks) {
+                const double p2 = sP[cur][c + off][el];
+                const double s2 = sS[cur][c + off][el];
                 S = S + P * s2;
                 P = P * p2;
-                sP[c][el] = P;
-                sS[c][el] = S;
             }
+            sP[cur ^ 1][c][el] = P;
+            sS[cur ^ 1][c][el] = S;
+            cur ^= 1;
             __syncthreads();
         }
         const double cin = carry_s[el];
         // A at the end of this chunk = suffix map of the chunks after it applied to the carry
-        const double A_end = c + 1 < kChunks ? sP[c + 1][el] * cin + sS[c + 1][el] : cin;
+        const double A_end = c + 1 < kChunks ? sP[cur][c + 1][el] * cin + sS[cur][c + 1][el] : cin;
         double A = A_end;
         v_next = v_end;
         float* __restrict__ ab = a.adv + sbase;
@@ -142,15 +159,176 @@ __global__ __launch_bounds__(kTmThreads) void k_gae(GaeArgs a) {
                                 TRUNC ? fv[TRUNC ? k : 0] : 0.0f, a.gamma, gl, &delta, &m);
                 A = delta + m * A;
                 if (active) {
-                    const uint32_t off = (uint32_t)(c * kChunkLen + k) * E32 + e32;
-                    ab[off] = (float)A;
-                    qb[off] = (float)(A + (double)v[k]);
+                    const uint32_t lo = (uint32_t)(c * kChunkLen) * E32 + e32;
+                    (ab + (int64_t)k * E)[lo] = (float)A;
+                    (qb + (int64_t)k * E)[lo] = (float)(A + (double)v[k]);
                 }
                 v_next = (double)v[k];
             }
         }
         __syncthreads();  // every lane has read carry_s
-        if (c == 0) carry_s[el] = sP[0][el] * cin + sS[0][el];
+        if (c == 0) carry_s[el] = sP[cur][0][el] * cin + sS[cur][0][el];
+    }
+}
+
+// Time-major GAE, four environments per lane: the same three phases, with every
+// load and store a 16-byte vector of 4 consecutive environments (a lane pair
+// covers a 32-byte run of a row) and four independent recursions per lane.
+// Compared with one environment per lane this issues a quarter of the memory
+// instructions, which bound the one-environment kernel on the few compute units
+// a rollout of a few hundred environments occupies.  Needs E a multiple of 4,
+// 16-byte aligned float rows and 4-byte aligned flag rows (checked by the
+// launcher).
+#ifndef CONDUIT_GAE_VEC_CHUNK
+#define CONDUIT_GAE_VEC_CHUNK 16
+#endif
+constexpr int kGaeVecChunk = CONDUIT_GAE_VEC_CHUNK;  // steps per chunk
+constexpr int kV = 4;                  // environments per lane
+constexpr int kEnvsV = 8;              // environments per workgroup (32-byte runs)
+constexpr int kQuads = kEnvsV / kV;    // lanes per row
+constexpr int kSuperV = 2048;          // steps per pass
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+static_assert(kGaeMaxEnvs * kSuperV * 4 <= (1ll << 32), "byte offsets of a slab fit 32 bits");
+
+template <bool TRUNC, int L>
+__global__ __launch_bounds__(kQuads * (kSuperV / L)) void k_gae_v4(GaeArgs a) {
+    constexpr int kCh = kSuperV / L;  // chunks per pass
+    __shared__ double sP[2][kCh][kEnvsV];
+    __shared__ double sS[2][kCh][kEnvsV];
+    __shared__ double carry_s[kEnvsV];
+    const int q = threadIdx.x % kQuads;
+    const int c = threadIdx.x / kQuads;
+    const int64_t E = a.E, T = a.T;
+    // workgroups are dealt round-robin to the 8 XCDs: the ones on one XCD take
+    // consecutive environment groups, so the 4 groups that share each 128-byte
+    // line of a row are read through the same L2
+    const int64_t nb = gridDim.x;
+    const int64_t group = nb % 8 == 0 ? (int64_t)(blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : (int64_t)blockIdx.x;
+    const int64_t e_raw = group * kEnvsV + q * kV;
+    const bool active = e_raw < E;                // E % 4 == 0: a quad is wholly in or out
+    const int64_t e0 = active ? e_raw : E - kV;  // inactive lanes read a valid quad
+    const double gl = a.gamma * a.lambda;
+    if (c == 0) {
+#pragma unroll
+        for (int j = 0; j < kV; ++j) carry_s[q * kV + j] = 0.0;
+    }
+    const int64_t supers = (T + kSuperV - 1) / kSuperV;
+    for (int64_t sc = supers - 1; sc >= 0; --sc) {
+        const int64_t row0 = sc * kSuperV;
+        const int last_local = (int)(T - 1 - row0);  // >= 0
+        const bool full = row0 + kSuperV <= T;       // uniform
+        // lane offset of the lane's first step from the row of step k (elements)
+        const uint32_t lo = (uint32_t)(c * L) * (uint32_t)E + (uint32_t)e0;
+        f32x4 r[L], v[L];
+        uint32_t d[L];
+        uint32_t tr[TRUNC ? L : 1];
+        f32x4 fv[TRUNC ? L : 1];
+#pragma unroll
+        for (int k = 0; k < L; ++k) {
+            // full pass: uniform row base + one lane offset; partial pass: steps
+            // past the end re-read the last row
+            const int64_t row = full ? row0 + k : row0 + (c * L + k < last_local ? c * L + k : last_local);
+            const int64_t base = row * E;
+            const uint32_t off = full ? lo : (uint32_t)e0;
+            const int64_t rb = full ? (row0 + k) * E : base;
+            r[k] = *reinterpret_cast<const f32x4*>(a.reward + rb + off);
+            v[k] = a.value ? *reinterpret_cast<const f32x4*>(a.value + rb + off) : (f32x4)(0.0f);
+            d[k] = *reinterpret_cast<const uint32_t*>(a.done + rb + off);
+            if constexpr (TRUNC) {
+                tr[TRUNC ? k : 0] = *reinterpret_cast<const uint32_t*>(a.truncated + rb + off);
+                fv[TRUNC ? k : 0] = *reinterpret_cast<const f32x4*>(a.final_value + rb + off);
+            }
+        }
+        const int64_t t1 = row0 + (int64_t)c * L + L;  // first step after this chunk
+        f32x4 ve;
+        if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4*>(a.bootstrap + e0) : (f32x4)(0.0f);
+        else ve = a.value ? *reinterpret_cast<const f32x4*>(a.value + t1 * E + e0) : (f32x4)(0.0f);
+        // fold the chunk into A_start = P * A_end + S, four environments at once
+        double P[kV], S[kV], vn[kV];
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            P[j] = 1.0;
+            S[j] = 0.0;
+            vn[j] = (double)ve[j];
+        }
+#pragma unroll
+        for (int k = L - 1; k >= 0; --k) {
+            if (c * L + k <= last_local) {
+#pragma unroll
+                for (int j = 0; j < kV; ++j) {
+                    double delta, m;
+                    gae_step<TRUNC>((double)r[k][j], (double)v[k][j], vn[j], (uint8_t)(d[k] >> (8 * j)),
+                                    TRUNC ? (uint8_t)(tr[TRUNC ? k : 0] >> (8 * j)) : 0,
+                                    TRUNC ? fv[TRUNC ? k : 0][j] : 0.0f, a.gamma, gl, &delta, &m);
+                    S[j] = delta + m * S[j];
+                    P[j] = m * P[j];
+                    vn[j] = (double)v[k][j];
+                }
+            }
+        }
+        __syncthreads();  // carry_s of the previous pass is final; sP/sS free
+        int cur = 0;
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            sP[cur][c][q * kV + j] = P[j];
+            sS[cur][c][q * kV + j] = S[j];
+        }
+        __syncthreads();
+        // suffix scan over the chunks, ping-pong buffers: one barrier per round
+        for (int off = 1; off < kCh; off <<= 1) {
+            if (c + off < kCh) {
+#pragma unroll
+                for (int j = 0; j < kV; ++j) {
+                    const double p2 = sP[cur][c + off][q * kV + j];
+                    const double s2 = sS[cur][c + off][q * kV + j];
+                    S[j] = S[j] + P[j] * s2;
+                    P[j] = P[j] * p2;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kV; ++j) {
+                sP[cur ^ 1][c][q * kV + j] = P[j];
+                sS[cur ^ 1][c][q * kV + j] = S[j];
+            }
+            cur ^= 1;
+            __syncthreads();
+        }
+        double cin[kV], A[kV];
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            cin[j] = carry_s[q * kV + j];
+            A[j] = c + 1 < kCh ? sP[cur][c + 1][q * kV + j] * cin[j] + sS[cur][c + 1][q * kV + j] : cin[j];
+            vn[j] = (double)ve[j];
+        }
+#pragma unroll
+        for (int k = L - 1; k >= 0; --k) {
+            if (c * L + k <= last_local) {
+                f32x4 ao, ro;
+#pragma unroll
+                for (int j = 0; j < kV; ++j) {
+                    double delta, m;
+                    gae_step<TRUNC>((double)r[k][j], (double)v[k][j], vn[j], (uint8_t)(d[k] >> (8 * j)),
+                                    TRUNC ? (uint8_t)(tr[TRUNC ? k : 0] >> (8 * j)) : 0,
+                                    TRUNC ? fv[TRUNC ? k : 0][j] : 0.0f, a.gamma, gl, &delta, &m);
+                    A[j] = delta + m * A[j];
+                    ao[j] = (float)A[j];
+                    ro[j] = (float)(A[j] + (double)v[k][j]);
+                    vn[j] = (double)v[k][j];
+                }
+                if (active) {
+                    const int64_t rb = full ? (row0 + k) * E : (row0 + c * L + k) * E;
+                    const uint32_t off = full ? lo : (uint32_t)e0;
+                    *reinterpret_cast<f32x4*>(a.adv + rb + off) = ao;
+                    *reinterpret_cast<f32x4*>(a.ret + rb + off) = ro;
+                }
+            }
+        }
+        __syncthreads();  // every lane has read carry_s
+        if (c == 0) {
+#pragma unroll
+            for (int j = 0; j < kV; ++j)
+                carry_s[q * kV + j] = sP[cur][0][q * kV + j] * cin[j] + sS[cur][0][q * kV + j];
+        }
     }
 }
 
@@ -287,6 +465,20 @@ __global__ void k_fill_u64(uint64_t* p, uint64_t v, int64_t n) {
 hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
     if (a.T <= 0 || a.E <= 0) return hipSuccess;
     if (a.E > kGaeMaxEnvs) return hipErrorInvalidValue;  // the ABI rejects this first
+    auto al = [](const void* p, uintptr_t m) { return (reinterpret_cast<uintptr_t>(p) & (m - 1)) == 0; };
+    const bool vec = a.E % kV == 0 && al(a.reward, 16) && al(a.value, 16) && al(a.bootstrap, 16) &&
+                     al(a.adv, 16) && al(a.ret, 16) && al(a.done, 4) && al(a.truncated, 4) &&
+                     al(a.final_value, 16);
+    if (vec) {
+        const int64_t vblocks = (a.E + kEnvsV - 1) / kEnvsV;
+        constexpr int L = kGaeVecChunk;
+        const dim3 block(kQuads * (kSuperV / L));
+        if (a.truncated)
+            hipLaunchKernelGGL((k_gae_v4<true, L>), dim3((unsigned)vblocks), block, 0, s, a);
+        else
+            hipLaunchKernelGGL((k_gae_v4<false, L>), dim3((unsigned)vblocks), block, 0, s, a);
+        return hipGetLastError();
+    }
     const int64_t blocks = (a.E + kEnvs - 1) / kEnvs;
     if (a.truncated)
         hipLaunchKernelGGL(k_gae<true>, dim3((unsigned)blocks), dim3(kTmThreads), 0, s, a);

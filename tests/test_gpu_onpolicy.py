@@ -27,7 +27,11 @@ def _gae_gpu(r, v, d, b, gamma, lam):
 @pytest.mark.parametrize("T,E,p_done,with_v,with_b", [
     (1, 1, 0.0, True, True), (2, 3, 0.5, True, False), (37, 19, 0.05, True, True), (64, 16, 0.0, False, False),
     (65, 17, 1.0, True, True), (200, 70, 0.01, True, True), (1000, 5, 0.002, True, True),
-    (2500, 9, 0.003, True, True), (1024, 8, 0.0, True, False), (3073, 3, 0.01, False, True)])
+    (2500, 9, 0.003, True, True), (1024, 8, 0.0, True, False), (3073, 3, 0.01, False, True),
+    # E a multiple of 4 (four environments per lane): a half-used workgroup,
+    # several 2048-step passes with a partial one, an XCD-remapped grid
+    (100, 12, 0.02, True, True), (2500, 12, 0.003, True, True), (4096, 8, 0.001, True, True),
+    (2049, 4, 0.01, True, False), (300, 128, 0.01, True, True), (33, 64, 0.1, False, False)])
 def test_gae_time_major_shapes(T, E, p_done, with_v, with_b):
     print(f"gae T={T} E={E}", flush=True)
     rng = np.random.default_rng(T * 131 + E)
@@ -44,7 +48,7 @@ def test_gae_time_major_shapes(T, E, p_done, with_v, with_b):
 
 @pytest.mark.parametrize("T,E,p_done,p_trunc", [
     (1, 1, 0.0, 1.0), (37, 19, 0.05, 0.05), (200, 70, 0.01, 0.02), (1024, 8, 0.0, 0.01), (2500, 9, 0.003, 0.002),
-    (65, 17, 0.5, 0.5), (3073, 3, 0.0, 0.0)])
+    (65, 17, 0.5, 0.5), (3073, 3, 0.0, 0.0), (300, 128, 0.01, 0.01), (2049, 12, 0.01, 0.01)])
 def test_gae_truncated_shapes(T, E, p_done, p_trunc):
     print(f"gae truncated T={T} E={E}", flush=True)
     rng = np.random.default_rng(T * 137 + E)
@@ -62,6 +66,33 @@ def test_gae_truncated_shapes(T, E, p_done, p_trunc):
         oa, orr = oracle.gae(r, v, d, b, gamma, lam, truncated=tr, final_value=fv)
         assert_gae_close(host(adv), oa)
         assert_gae_close(host(ret), orr)
+
+
+def test_gae_misaligned_rows_take_the_lane_per_environment_kernel():
+    """E a multiple of 4 but rows 4 bytes off a 16-byte boundary: the launcher
+    must not use 16-byte vectors; results still match the oracle."""
+    print("gae misaligned rows", flush=True)
+    T, E = 333, 16
+    rng = np.random.default_rng(7)
+    r = rng.standard_normal((T, E)).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32)
+    d = (rng.random((T, E)) < 0.02).astype(np.uint8)
+    b = rng.standard_normal(E).astype(np.float32)
+
+    def off(a):  # the same values at an address 4 bytes past a 16-byte boundary
+        flat = torch.empty(a.size + 1, dtype=torch.float32, device="cuda")
+        view = flat[1:].view(a.shape)
+        view.copy_(torch.from_numpy(a))
+        assert view.data_ptr() % 16 == 4
+        return view
+
+    adv = torch.full((T * E + 1,), np.nan, dtype=torch.float32, device="cuda")[1:].view(T, E)
+    ret = torch.full((T * E + 1,), np.nan, dtype=torch.float32, device="cuda")[1:].view(T, E)
+    cd.conduit_gae(off(r), off(v), dev(d), dev(b), 0.99, 0.95, adv, ret)
+    assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+    oa, orr = oracle.gae(r, v, d, b, 0.99, 0.95)
+    assert_gae_close(host(adv), oa)
+    assert_gae_close(host(ret), orr)
 
 
 def test_gae_ppo_config_full_size():
