@@ -72,17 +72,48 @@ class Timer:
         return e
 
 
+_DELAY_US_PER_WORK = []
+
+
+def _gpu_delay(us):
+    """Enqueue about `us` microseconds of GPU work (the library's register-only
+    stand-in kernel, one workgroup per compute unit) on torch's current stream."""
+    import torch
+    from paper_2609_24456_amd import conduit as cd
+    if not _DELAY_US_PER_WORK:
+        probe = 200_000
+        cd.conduit_standin(probe)  # loads its code
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        cd.conduit_standin(probe)
+        e1.record()
+        torch.cuda.synchronize()
+        _DELAY_US_PER_WORK.append(max(e0.elapsed_time(e1) * 1e3 / probe, 1e-6))
+    cd.conduit_standin(int(us / _DELAY_US_PER_WORK[0]) + 1)
+
+
 def _b2b_ms(calls, reps=1, warm=2):
     """Milliseconds per call of `calls` (zero-argument callables that enqueue
-    on the library's stream), launched back to back between two events, after
-    `warm` untimed calls (a kernel's first launch loads its code)."""
+    on the library's stream, torch's current stream), launched back to back
+    between two events, after `warm` untimed calls (a kernel's first launch
+    loads its code).  The GPU is paced: a stand-in kernel queued ahead of the
+    first event outlasts the host's enqueue of every timed call, so the events
+    bracket GPU time only, also for calls whose kernels are shorter than their
+    host-side enqueue (Python + ctypes, a few microseconds per call)."""
     import torch
-    for f in calls[:warm]:
+    per_call_us = 15.0
+    for i, f in enumerate(calls[:warm]):
+        t0 = time.perf_counter()
         f()
+        if i > 0:  # the first call may include loading code
+            per_call_us = max(per_call_us, 1.5e6 * (time.perf_counter() - t0))
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     rc = 0
+    _gpu_delay(min(per_call_us * reps * len(calls) + 500.0, 30_000.0))
     e0.record()
     for _ in range(reps):
         for f in calls:

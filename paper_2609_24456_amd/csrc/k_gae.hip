@@ -349,8 +349,8 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
     __shared__ float sV[kPkPad];
     __shared__ float sA[kPkPad];
     __shared__ float sR[kPkPad];
-    __shared__ double sP[kPkThreads];
-    __shared__ double sS[kPkThreads];
+    __shared__ double sP[2][kPkThreads];
+    __shared__ double sS[2][kPkThreads];
     const int c = threadIdx.x;
     const int64_t b = blockIdx.x;
     const int64_t Lmax = a.Lmax;
@@ -362,6 +362,11 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
     const float* val = a.value ? a.value + b * Lmax : nullptr;
     float* adv = a.adv + b * Lmax;
     float* ret = a.ret + b * Lmax;
+    // 16-byte vectors for the value loads and the output stores when the rows
+    // allow them (uniform)
+    auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+    const bool vec_in = val && al16(val);
+    const bool vec_out = al16(adv) && al16(ret);
     const double R = (double)a.last_reward[b];
     const double gl = a.gamma * a.lambda;
     double carry = 0.0;    // A at the start of the later segment
@@ -370,7 +375,30 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
     for (int64_t sg = segs - 1; sg >= 0; --sg) {
         const int64_t base = sg * kPkSeg;
         const int seg_len = (int)(Lmax - base < kPkSeg ? Lmax - base : kPkSeg);
-        for (int t = c; t < seg_len; t += kPkThreads) sV[lpad(t)] = val ? val[base + t] : 0.0f;
+        if (vec_in) {
+            // every lane's 4 vectors are loaded before the first LDS write
+            constexpr int kVecs = kPkSeg / (4 * kPkThreads);
+            f32x4 q[kVecs];
+#pragma unroll
+            for (int j = 0; j < kVecs; ++j) {
+                const int t = (j * kPkThreads + c) * 4;
+                if (t + 3 < seg_len) {
+                    q[j] = *reinterpret_cast<const f32x4*>(val + base + t);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) q[j][i] = t + i < seg_len ? val[base + t + i] : 0.0f;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kVecs; ++j) {
+                const int t = (j * kPkThreads + c) * 4;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (t + i < seg_len) sV[lpad(t + i)] = q[j][i];
+            }
+        } else {
+            for (int t = c; t < seg_len; t += kPkThreads) sV[lpad(t)] = val ? val[base + t] : 0.0f;
+        }
         __syncthreads();
         // this lane's chunk [t0, t1) of the segment, live part [t0, u1)
         const int t0 = c * kPkChunk;
@@ -397,26 +425,25 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
                 }
             }
         }
-        sP[c] = P;
-        sS[c] = S;
+        // suffix scan over the lanes' chunks, ping-pong buffers: round r reads
+        // what round r - 1 wrote and writes the other buffer, one barrier each
+        int cur = 0;
+        sP[cur][c] = P;
+        sS[cur][c] = S;
         __syncthreads();
         for (int off = 1; off < kPkThreads; off <<= 1) {
-            const bool has = c + off < kPkThreads;
-            double p2 = 1.0, s2 = 0.0;
-            if (has) {
-                p2 = sP[c + off];
-                s2 = sS[c + off];
-            }
-            __syncthreads();
-            if (has) {
+            if (c + off < kPkThreads) {
+                const double p2 = sP[cur][c + off];
+                const double s2 = sS[cur][c + off];
                 S = S + P * s2;
                 P = P * p2;
-                sP[c] = P;
-                sS[c] = S;
             }
+            sP[cur ^ 1][c] = P;
+            sS[cur ^ 1][c] = S;
+            cur ^= 1;
             __syncthreads();
         }
-        double A = c + 1 < kPkThreads ? sP[c + 1] * carry + sS[c + 1] : carry;
+        double A = c + 1 < kPkThreads ? sP[cur][c + 1] * carry + sS[cur][c + 1] : carry;
         {
             double v_next = v_end;
 #pragma unroll
@@ -440,11 +467,34 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
             }
         }
         __syncthreads();
-        for (int t = c; t < seg_len; t += kPkThreads) {
-            adv[base + t] = sA[lpad(t)];
-            ret[base + t] = sR[lpad(t)];
+        if (vec_out) {
+            constexpr int kVecs = kPkSeg / (4 * kPkThreads);
+#pragma unroll
+            for (int j = 0; j < kVecs; ++j) {
+                const int t = (j * kPkThreads + c) * 4;
+                if (t + 3 < seg_len) {
+                    f32x4 oa, orr;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        oa[i] = sA[lpad(t + i)];
+                        orr[i] = sR[lpad(t + i)];
+                    }
+                    *reinterpret_cast<f32x4*>(adv + base + t) = oa;
+                    *reinterpret_cast<f32x4*>(ret + base + t) = orr;
+                } else {
+                    for (int i = 0; i < 4 && t + i < seg_len; ++i) {
+                        adv[base + t + i] = sA[lpad(t + i)];
+                        ret[base + t + i] = sR[lpad(t + i)];
+                    }
+                }
+            }
+        } else {
+            for (int t = c; t < seg_len; t += kPkThreads) {
+                adv[base + t] = sA[lpad(t)];
+                ret[base + t] = sR[lpad(t)];
+            }
         }
-        carry = sP[0] * carry + sS[0];
+        carry = sP[cur][0] * carry + sS[cur][0];
         v_after = (double)sV[lpad(0)];
         __syncthreads();  // LDS is rewritten by the next segment
     }
