@@ -5,14 +5,19 @@
 // Sec. 2.2).
 //
 // Two kinds of workgroup share the grid:
-//   * sampler workgroups (the head of the grid, four samples each, one per
-//     wavefront) run tree_descend (descend.h), write the indices and error
-//     flags, and park each sampled leaf in the weight array;
-//   * gather workgroups (W per sample, two work items each; W = 2 for a stack
-//     of four frames) run the same descent for their sample themselves -- a
-//     few KB of redundant tree reads -- so the frame loads never wait for
-//     another workgroup or for the index to make a round trip through memory.
-//     The first of a sample's W writes its scalar columns.
+//   * gather workgroups (the head of the grid, W per sample, two work items
+//     each; W = 2 for a stack of four frames) run tree_descend (descend.h) for
+//     their sample themselves -- a few KB of redundant tree reads -- so the
+//     frame loads never wait for another workgroup or for the index to make a
+//     round trip through memory.  The first of a sample's W writes its scalar
+//     columns.
+//   * sampler workgroups (the tail of the grid, four samples each, one per
+//     wavefront) run the same descent, write the indices and error flags, and
+//     park each sampled leaf in the weight array.
+// A compute unit holds at most 1,024 resident lanes here, so 1,024 workgroups
+// of 256 lanes fill the GPU: the DQN batch's 1,024 gather workgroups take the
+// first round and the 128 sampler workgroups start as the first gathers
+// retire; their weights are still done long before the last frame store.
 //
 // Importance weights need the smallest sampled leaf of the whole batch (or,
 // normalised buffer-wide, of the whole buffer: then each sampler workgroup
@@ -104,11 +109,12 @@ __global__ __launch_bounds__(kThreads) void k_sample_gather(SampleArgs sa, Gathe
                                                             int32_t wgs, int32_t sampler_wgs) {
     __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
     __shared__ int64_t s_slot;
-    if ((int32_t)blockIdx.x < sampler_wgs) {
-        sampler_wg<PRE>(sa, dv, blockIdx.x);
+    const int64_t gather_wgs = (int64_t)gridDim.x - sampler_wgs;
+    if ((int64_t)blockIdx.x >= gather_wgs) {
+        sampler_wg<PRE>(sa, dv, (int64_t)blockIdx.x - gather_wgs);
         return;
     }
-    const int64_t g = (int64_t)blockIdx.x - sampler_wgs;
+    const int64_t g = blockIdx.x;
     const int64_t b = g / wgs;
     const int part = (int)(g - b * wgs);
     if (threadIdx.x < kWave) {
