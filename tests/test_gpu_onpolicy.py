@@ -31,7 +31,9 @@ def _gae_gpu(r, v, d, b, gamma, lam):
     # E a multiple of 4 (four environments per lane): a half-used workgroup,
     # several 2048-step passes with a partial one, an XCD-remapped grid
     (100, 12, 0.02, True, True), (2500, 12, 0.003, True, True), (4096, 8, 0.001, True, True),
-    (2049, 4, 0.01, True, False), (300, 128, 0.01, True, True), (33, 64, 0.1, False, False)])
+    (2049, 4, 0.01, True, False), (300, 128, 0.01, True, True), (33, 64, 0.1, False, False),
+    # the most environments the ABI takes (2^19), on both kernels
+    (3, 1 << 19, 0.2, True, True), (2, (1 << 19) - 1, 0.2, True, True)])
 def test_gae_time_major_shapes(T, E, p_done, with_v, with_b):
     print(f"gae T={T} E={E}", flush=True)
     rng = np.random.default_rng(T * 131 + E)

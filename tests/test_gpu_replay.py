@@ -458,6 +458,42 @@ def test_zero_priorities_and_batch_larger_than_size():
     buf.close()
 
 
+@pytest.mark.parametrize("B", [(1 << 20) - 1, 1 << 20])
+def test_largest_batch_sample_and_fused_gather(B):
+    """The largest batch the ABI takes (2^20) and one below it: the stratified
+    targets' multiply-shift division by B at its widest, through the separate
+    sampler and through the fused sampler + gather (2^20 gathered rows)."""
+    print(f"largest batch B={B}", flush=True)
+    rng = np.random.default_rng(B)
+    cap, n = 5003, 6000  # wraps
+    obs = rng.integers(0, 256, size=(n, 8), dtype=np.uint8)
+    reward = rng.standard_normal(n).astype(np.float32)
+    prio = synth.quantise_priority(rng.lognormal(0, 2, n))
+    prio[rng.random(n) < 0.05] = 0  # zero leaves are never sampled
+    buf = _mk(cap, (8,), torch.uint8, action_bytes=0)
+    store = np.zeros((cap, 8), np.uint8)
+    orc = oracle.Replay(cap, (8,), np.uint8, act_bytes=0, obs_storage=store)
+    for a in range(0, n, 3000):
+        b = min(n, a + 3000)
+        buf.ingest(dev(obs[a:b]), reward=dev(reward[a:b]), prio=dev(prio[a:b]))
+        orc.ingest(b - a, obs=obs[a:b], reward=reward[a:b], prio=prio[a:b])
+    uu = synth.uniforms(rng, B)
+    o_idx, o_w = orc.sample(uu)
+    idx, w = buf.sample(dev(uu))
+    assert np.array_equal(host(idx), o_idx)
+    assert_weights_close(host(w), o_w)
+    out = torch.empty((B, 1, 8), dtype=torch.uint8, device="cuda")
+    rew = torch.empty(B, dtype=torch.float32, device="cuda")
+    idx2, w2 = buf.sample_gather(dev(uu), cd.transform(cd.XF_NONE), obs=out, reward=rew)
+    assert np.array_equal(host(idx2), o_idx)
+    assert_weights_close(host(w2), o_w)
+    o_obs, _, o_rew, _ = orc.gather(o_idx, oracle.XF_NONE)
+    assert np.array_equal(host(out).reshape(-1), o_obs.reshape(-1))
+    assert np.array_equal(host(rew), o_rew)
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
+
+
 @pytest.mark.parametrize("given_prio", [False, True])
 def test_update_ingest_one_call_edge_cases(given_prio):
     # updates with duplicates and slots the same call's ingest evicts, on a
