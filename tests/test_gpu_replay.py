@@ -423,6 +423,38 @@ def test_tree_shapes_sample_and_update(cap):
     buf.close()
 
 
+@pytest.mark.slow
+def test_depth_five_tree():
+    """64^4 + 1 slots, every one ingested: a depth-5 tree (level sizes 262,145,
+    4,097, 65, 2, 1), sampled and updated against the oracle."""
+    cap = (1 << 24) + 1
+    print(f"depth-5 tree cap={cap}", flush=True)
+    rng = np.random.default_rng(5)
+    buf = _mk(cap, (4,), torch.uint8, action_bytes=0)
+    orc = oracle.Replay(cap, (4,), np.uint8, act_bytes=0, keep_obs=False)
+    assert buf.info().tree_depth == 5
+    chunk = 1 << 22
+    for a in range(0, cap, chunk):
+        b = min(cap, a + chunk)
+        p = synth.quantise_priority(rng.lognormal(0, 1, b - a))
+        buf.ingest(torch.zeros((b - a, 4), dtype=torch.uint8, device="cuda"), prio=dev(p))
+        orc.ingest(b - a, prio=p)
+    for it in range(3):
+        uu = synth.uniforms(rng, 1000)
+        idx, w = buf.sample(dev(uu))
+        o_idx, o_w = orc.sample(uu)
+        assert np.array_equal(host(idx), o_idx), it
+        assert_weights_close(host(w), o_w)
+        upd_idx = rng.integers(0, cap, size=5000)
+        upd_p = rng.integers(0, 1 << 32, size=5000, dtype=np.uint64).astype(np.uint32)
+        buf.update(dev(upd_idx), dev(upd_p))
+        orc.update(upd_idx, upd_p)
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    assert np.array_equal(read_col(buf, cd.COL_LEAVES, cap * 4, np.uint32), orc.leaf)
+    assert tree_consistent(buf, cap) == orc.total_priority()
+    buf.close()
+
+
 def test_duplicate_heavy_updates_last_writer_wins():
     print("updates: 256 and 3000 updates over 64 slots", flush=True)
     rng = np.random.default_rng(9)
