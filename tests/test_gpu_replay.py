@@ -526,22 +526,27 @@ def test_largest_batch_sample_and_fused_gather(B):
     buf.close()
 
 
-@pytest.mark.parametrize("given_prio", [False, True])
-def test_update_ingest_one_call_edge_cases(given_prio):
+@pytest.mark.parametrize("given_prio,long_lists,big_ingest",
+                         [(False, False, False), (True, False, False), (False, True, False), (False, False, True)])
+def test_update_ingest_one_call_edge_cases(given_prio, long_lists, big_ingest):
     # updates with duplicates and slots the same call's ingest evicts, on a
-    # wrapped ring, with and without caller-given priorities on the new rows
-    print(f"update + ingest edge cases, given priorities={given_prio}", flush=True)
+    # wrapped ring, with and without caller-given priorities on the new rows.
+    # Long update lists run several 1,024-entry chunks in the update workgroup
+    # and several passes of the raised maximum in the one launch; ingests of
+    # more than 4,096 rows take the call's two-launch path.
+    print(f"update + ingest edge cases, given priorities={given_prio}, long lists={long_lists}, "
+          f"big ingest={big_ingest}", flush=True)
     rng = np.random.default_rng(91)
-    cap = 300
+    cap = 12000 if big_ingest else 300
     buf = _mk(cap, (4,), torch.uint8, action_bytes=0)
     orc = oracle.Replay(cap, (4,), np.uint8, act_bytes=0)
     pos = 0
     for rnd in range(12):
-        n = int(rng.integers(1, 200))
+        n = int(rng.integers(4097, 6000)) if big_ingest else int(rng.integers(1, 200))
         rows = rng.integers(0, 256, (n, 4), dtype=np.uint8)
         p_new = synth.quantise_priority(rng.lognormal(0, 2, n)) if given_prio else None
         if orc.size:
-            k = int(rng.integers(1, 400))
+            k = int(rng.integers(4097, 6000)) if long_lists else int(rng.integers(1, 400))
             # half of the updates hit the slots this ingest is about to evict
             evict = (orc.head + rng.integers(0, n, k)) % cap
             idx = np.where(rng.random(k) < 0.5, evict, rng.integers(0, orc.size, k)).astype(np.int64)
