@@ -813,8 +813,11 @@ conduit_status conduit_nstep(conduit_buffer* b, const int64_t* idx, int64_t batc
     a.valid = valid;
     a.err = err_words(b->err_slot);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = launch_nstep(a, s);
-    if (e == hipSuccess && next_obs) e = launch_gather(ga, s);
+    hipError_t e = next_obs ? launch_nstep_gather(a, ga, s) : hipErrorNotSupported;
+    if (e == hipErrorNotSupported) {  // the targets, then the stacks: one launch each
+        e = launch_nstep(a, s);
+        if (e == hipSuccess && next_obs) e = launch_gather(ga, s);
+    }
     if (e != hipSuccess) return hip_fail(e, "nstep launch");
     return CONDUIT_OK;
 }

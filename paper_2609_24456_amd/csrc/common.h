@@ -492,6 +492,10 @@ struct NstepArgs {
 };
 
 hipError_t launch_nstep(const NstepArgs& a, hipStream_t s);
+// the targets and the bootstrap stacks of rows of a few work items in one
+// launch (ga.idx unused: each sample's slot comes from its window);
+// hipErrorNotSupported for other shapes
+hipError_t launch_nstep_gather(const NstepArgs& na, const GatherArgs& ga, hipStream_t s);
 
 struct GaePackedArgs {
     const float* last_reward;

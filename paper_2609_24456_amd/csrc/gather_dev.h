@@ -255,5 +255,79 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
 }
 
 
+// The row's scalar columns, one column word per lane: every load before any
+// store (the row's slot is known, so this is one memory round trip).
+__device__ __forceinline__ void row_scalars(const GatherArgs& a, int64_t b, int64_t i) {
+    const bool ok = i >= 0 && i < a.limit;
+    const int64_t s = ok ? i : 0;
+    const bool words = (a.action_bytes & 3) == 0;
+    const int na = a.out_action && a.action_bytes > 0 ? (words ? a.action_bytes >> 2 : a.action_bytes) : 0;
+    for (int t = threadIdx.x; t < na + 2; t += kThreads) {
+        if (t < na) {
+            if (words) {
+                const uint32_t v = reinterpret_cast<const uint32_t*>(a.action + s * a.action_bytes)[t];
+                reinterpret_cast<uint32_t*>(a.out_action + b * a.action_bytes)[t] = ok ? v : 0u;
+            } else {
+                const uint8_t v = a.action[s * a.action_bytes + t];
+                a.out_action[b * a.action_bytes + t] = ok ? v : (uint8_t)0;
+            }
+        } else if (t == na) {
+            if (a.out_reward) {
+                const float v = a.reward[s];
+                a.out_reward[b] = ok ? v : 0.0f;
+            }
+        } else {
+            if (a.out_done) {
+                const uint8_t v = a.done[s];
+                a.out_done[b] = ok ? v : (uint8_t)0;
+            }
+        }
+    }
+}
+
+// rows of at most this many work items take the fused kernels (a sample's
+// workgroups find its slot themselves and gather two items each)
+constexpr int64_t kFusedMaxItemsPerRow = 8;
+
+// The work items of row b (the slot i, or out of range for a zero row) that
+// workgroup `part` of the row's `wgs` owns, two per workgroup when the row has
+// more than two, double-buffered: the next item's loads are issued before the
+// current item's stores.  The row's first workgroup also writes its scalar
+// columns.
+template <int XF>
+__device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int part, int64_t wgs, int32_t bpf,
+                                           int64_t i, const uint16_t* lut) {
+    const bool owner = part == 0;
+    const int64_t per_row = (int64_t)bpf * a.stack;
+    const int64_t per_wg = (per_row + wgs - 1) / wgs;
+    const int64_t it0 = b * per_row + part * per_wg;
+    int64_t it_end = it0 + per_wg;
+    if (it_end > (b + 1) * per_row) it_end = (b + 1) * per_row;
+    if (it0 >= it_end) {
+        if (owner) row_scalars(a, b, i);
+        return;
+    }
+    typename UnitOf<XF>::T va[kUnroll], vb[kUnroll];
+    int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
+    uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
+    Item ta = decode(a, it0, bpf, i), tb;
+    issue<XF>(a, ta, i, va, sia, sja, eia, eja);
+    if (owner) row_scalars(a, b, i);
+    for (int64_t it = it0; it < it_end; it += 2) {
+        const bool has_b = it + 1 < it_end;  // uniform
+        if (has_b) {
+            tb = decode(a, it + 1, bpf, i);
+            issue<XF>(a, tb, i, vb, sib, sjb, eib, ejb);
+        }
+        finish<XF, true, false>(a, ta, va, sia, sja, eia, eja, lut);
+        if (!has_b) break;
+        if (it + 2 < it_end) {
+            ta = decode(a, it + 2, bpf, i);
+            issue<XF>(a, ta, i, va, sia, sja, eia, eja);
+        }
+        finish<XF, true, false>(a, tb, vb, sib, sjb, eib, ejb, lut);
+    }
+}
+
 }  // namespace
 }  // namespace conduit

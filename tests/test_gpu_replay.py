@@ -77,7 +77,44 @@ def _check_nstep(buf, orc, idx_d, o_idx, n, gamma, xf_kind, row_shape, obs_kind=
         want, _, _, _ = orc.gather(o_n[boot], oracle.XF_U8_F32 if xf_kind == cd.XF_U8_F32 else oracle.XF_NONE)
         assert np.array_equal(g[boot], want.reshape(int(boot.sum()), -1).view(np.uint8))
     assert not g[~boot].any()
+    # the targets alone (no stacks requested) take the one-wavefront-per-sample kernel
+    nxt2 = torch.empty_like(nxt)
+    ret2 = torch.empty_like(ret)
+    disc2 = torch.empty_like(disc)
+    val2 = torch.empty_like(val)
+    cd.conduit_nstep(buf.handle, idx_d, n, gamma, nxt2, ret2, disc2, val2)
+    assert np.array_equal(host(nxt2), o_n)
+    assert np.array_equal(host(val2), o_v)
+    assert np.array_equal(host(ret2), host(ret))
+    assert np.array_equal(host(disc2), o_d)
     return o_v
+
+
+@pytest.mark.parametrize("n", [1, 3])
+def test_nstep_rows_of_many_items(n):
+    """Bootstrap stacks of rows too large for the one-launch kernel (3x84x84
+    u8 frames, stack of 4: 12 work items per row) take two launches."""
+    print(f"n-step with 3x84x84 stacks, n={n}", flush=True)
+    rng = np.random.default_rng(40 + n)
+    cap, total, K, shape = 300, 420, 4, (3, 84, 84)
+    row = int(np.prod(shape))
+    done = (rng.random(total) < 0.04).astype(np.uint8)
+    episode, step = synth.episodes_from_done(done)
+    obs = rng.integers(0, 256, size=(total, row), dtype=np.uint8)
+    reward = rng.standard_normal(total).astype(np.float32)
+    buf = _mk(cap, shape, torch.uint8, frame_stack=K, action_bytes=0)
+    store = np.zeros((cap, row), np.uint8)
+    orc = oracle.Replay(cap, shape, np.uint8, act_bytes=0, frame_stack=K, obs_storage=store)
+    for a in range(0, total, 140):
+        b = min(total, a + 140)
+        buf.ingest(dev(obs[a:b].reshape((b - a,) + shape)), reward=dev(reward[a:b]), done=dev(done[a:b]),
+                   episode_id=dev(episode[a:b]), step=dev(step[a:b]))
+        orc.ingest(b - a, obs=obs[a:b], reward=reward[a:b], done=done[a:b], episode=episode[a:b], step=step[a:b])
+    o_idx = rng.integers(0, cap, 97).astype(np.int64)
+    valid = _check_nstep(buf, orc, dev(o_idx), o_idx, n, 0.97, cd.XF_U8_F32, shape)
+    assert valid.any()
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
 
 
 def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH,
