@@ -94,7 +94,7 @@ __global__ __launch_bounds__(kThreads) void k_sample_gather(SampleArgs sa, Gathe
         build_lut(a, lut, kWave, kThreads - kWave);
     }
     __syncthreads();
-    gather_row<XF>(a, b, part, wgs, bpf, s_slot, lut);
+    gather_row<XF, true>(a, b, part, wgs, bpf, s_slot, lut);
 }
 
 template <int XF>
