@@ -66,7 +66,7 @@ __device__ __forceinline__ uint16_t bf16_rne(float f) {
 // store: one memory round trip after the index instead of one per column.
 constexpr int kScalarWords = 8;  // action words held in registers per pass
 
-__device__ void gather_scalars(const GatherArgs& a, int64_t block) {
+__device__ inline void gather_scalars(const GatherArgs& a, int64_t block) {
     const int64_t b = block * kThreads + threadIdx.x;
     if (b >= a.n) return;
     const int64_t i = a.idx[b];

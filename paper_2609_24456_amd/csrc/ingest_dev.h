@@ -61,7 +61,7 @@ __device__ void copy_dense(const IngestArgs& a, int64_t block, int tid) {
     }
 }
 
-__device__ void copy_ragged(const IngestArgs& a, int64_t j, int tid) {
+__device__ inline void copy_ragged(const IngestArgs& a, int64_t j, int tid) {
     int64_t slot = a.head + j;
     if (slot >= a.capacity) slot -= a.capacity;
     int64_t len = a.src_offsets[j + 1] - a.src_offsets[j];

@@ -42,7 +42,7 @@ __device__ __forceinline__ bool tail_block(const GatherArgs& a, int64_t tail) {
 // in flight.
 
 template <int XF, bool NT>
-__global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t bpf, int64_t n_items, int32_t tail) {
+__global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t bpf, int32_t tail) {
     __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
     if (tail_block(a, tail)) return;
     const int64_t it = (int64_t)blockIdx.x - tail;
@@ -215,7 +215,7 @@ hipError_t launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t tail_blo
     } else {
         // large batches: one workgroup per item
         hipLaunchKernelGGL((k_gather_rows<XF, true>), dim3((unsigned)(n_items + tail_blocks)), dim3(kThreads), 0, s,
-                           a, (int32_t)bpf, n_items, (int32_t)tail_blocks);
+                           a, (int32_t)bpf, (int32_t)tail_blocks);
     }
     return hipGetLastError();
 }
