@@ -37,6 +37,13 @@
  *     kernel has finished returns CONDUIT_ESTATE until the flag is cleared.
  *     conduit_sync_check() waits for a stream and reports the flag.
  *   - conduit_last_error() returns a thread-local message for the last failure.
+ *   - The delivery and on-policy calls (conduit_sample, conduit_gather_transform,
+ *     conduit_sample_gather, conduit_update_priorities, conduit_nstep, the GAE
+ *     calls, conduit_minibatch_gather) only enqueue kernels: no allocation,
+ *     memset or synchronisation, so they may be captured into a HIP graph and
+ *     replayed; a replay uses the arguments and the ring state (size, total)
+ *     of the capture.  The ingest calls advance the ring's host-side head when
+ *     they are enqueued, so a captured ingest would replay into the same slots.
  */
 #ifndef CONDUIT_H
 #define CONDUIT_H
