@@ -3,17 +3,22 @@
 Headline workload (the configuration the metric is quoted on): DQN replay of
 1,000,000 single 84x84 uint8 frames, frame stack 4, batch 512, proportional
 prioritisation alpha 0.6 / beta 0.4.  One step = ingest 512 new frames + sample
-512 + gather/transform 512 -> [512, 4, 84, 84] fp32 + priority update 512, with
-sampling and gathering through the fused conduit_sample_gather call (the step
-through separate conduit_sample / conduit_gather_transform calls is reported
-beside it).
-Inputs (frames of the steps, uniforms, new priorities) are resident in HBM
-before the timed region.
+512 + gather/transform 512 -> [512, 4, 84, 84] fp32 + priority update 512, as
+two calls per step: conduit_update_ingest (the previous step's priority update
+with this step's ingest) and conduit_sample_gather (sampling, IS weights and
+the gather in one launch).  The same steps with a separate update call and
+through separate conduit_sample / conduit_gather_transform calls are reported
+beside it.  Inputs (frames of the steps, uniforms, new priorities) are resident
+in HBM before the timed region.
 
 Prints ONE JSON line.  Besides the headline it carries the roofline of the
 dominant kernel, the oracle timed on the host cores (cpu_baseline), per-kernel
-times of the step, and the other workloads' rows (PPO GAE + minibatch gather,
-large-payload bf16 gather, token packing + packed GAE, tiny replay latency).
+times of the step, and the other workloads' rows (DQN ingest and n-step
+targets, PPO rollout ingest + GAE + minibatch gather, large-payload bf16
+gather, token packing + packed GAE, tiny replay latency, the synthetic stress
+transitions, the scheduling model against measured schedules, placement).
+The rows are timed GPU-paced (a stand-in kernel queued ahead of the first
+event), so each brackets GPU time only.
 """
 import argparse
 import ctypes as C
