@@ -83,7 +83,7 @@ const char* kErrText[kErrKinds] = {
     "sample from a tree whose total priority is 0",
     "sequence length outside [0, max_len]",
     "permutation entry outside [0, n_src)",
-    "",
+    "GAE segment never published by its workgroup (GAE calls overlapping on one GPU?)",
     "sum-tree descent found no child",
     "",
 };
@@ -831,7 +831,7 @@ conduit_status conduit_gae(const float* rewards, const float* values, const uint
     if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
     conduit_status st = standalone_flags();
     if (st != CONDUIT_OK) return st;
-    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, nullptr, nullptr};
+    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, nullptr, nullptr, err_words(0)};
     hipError_t e = launch_gae(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "gae launch");
     return CONDUIT_OK;
@@ -849,7 +849,8 @@ conduit_status conduit_gae_truncated(const float* rewards, const float* values, 
     if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
     conduit_status st = standalone_flags();
     if (st != CONDUIT_OK) return st;
-    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, truncated, final_values};
+    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, truncated, final_values,
+              err_words(0)};
     hipError_t e = launch_gae(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "gae launch");
     return CONDUIT_OK;

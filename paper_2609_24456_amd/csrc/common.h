@@ -22,7 +22,7 @@ enum ErrKind : int {
     ERR_EMPTY_TREE = 2,     // sample with a zero root
     ERR_SEQ_LENGTH = 3,     // ragged sequence longer than the slot / bad GAE length
     ERR_PERM_INDEX = 4,     // minibatch permutation entry outside [0, n_src)
-    // 5: unused
+    ERR_GAE_WAIT = 5,       // split GAE: a later segment never published (overlapping calls)
     ERR_DESCENT = 6,        // tree descent found no child (never expected)
     kErrKinds = 8,
 };
@@ -59,9 +59,10 @@ __device__ __forceinline__ void flag_error(uint32_t* err, int kind) {
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
-// DPP controls: shift right within a row of 16 lanes, and broadcast of lane 15
-// (31) of a row into the next row (rows 1 and 3; rows 2 and 3)
-constexpr int kDppRowShr = 0x110, kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+// DPP controls: shift right (lane i reads lane i - n) and left (lane i reads
+// lane i + n) within a row of 16 lanes, and broadcast of lane 15 (31) of a row
+// into the next row (rows 1 and 3; rows 2 and 3)
+constexpr int kDppRowShr = 0x110, kDppRowShl = 0x100, kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
 
 // x moved by one DPP control; lanes with no source, or in rows the row mask
 // leaves out, read `id`
@@ -470,6 +471,7 @@ struct GaeArgs {
     float* ret;
     const uint8_t* truncated;   // NULL: no truncation bootstrap
     const float* final_value;   // read where truncated (and not done)
+    uint32_t* err;              // sticky error words
 };
 
 hipError_t launch_gae(const GaeArgs& a, hipStream_t s);

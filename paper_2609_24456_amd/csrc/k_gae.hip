@@ -18,6 +18,8 @@
 // chunks per pass, lanes fastest over environments so every load instruction of
 // a wavefront reads eight 32-byte runs.  Padded sequences
 // [B, Lmax] (k_gae_packed): one workgroup per sequence, 256 chunks along t.
+#include <atomic>
+
 #include "common.h"
 
 namespace conduit {
@@ -332,6 +334,542 @@ __global__ __launch_bounds__(kQuads * (kSuperV / L)) void k_gae_v4(GaeArgs a) {
     }
 }
 
+#ifndef CONDUIT_GAE_SPLIT_MAX_ENVS
+#define CONDUIT_GAE_SPLIT_MAX_ENVS 4096
+#endif
+#ifndef CONDUIT_GAE_SPLIT_MIN_TILES
+#define CONDUIT_GAE_SPLIT_MIN_TILES 256
+#endif
+constexpr int64_t kGaeSplitMaxEnvs = CONDUIT_GAE_SPLIT_MAX_ENVS;    // from E / 8 = 512 workgroups on, one pass each
+constexpr int64_t kGaeSplitMinTiles = CONDUIT_GAE_SPLIT_MIN_TILES;  // one tile per compute unit before shorter chunks
+
+// ---------------------------------------------------------------------------
+// Time-major GAE split along T.  With few environments the kernels above run
+// on E / 8 workgroups, each walking all T steps of its 8 columns, and every
+// compute unit pulls whole 128-byte lines for 32-byte runs.  The split path
+// cuts [T, E] into tiles of 32 environments (one 128-byte line of every float
+// row) by Ts = 32 L steps, so every compute unit of the GPU takes a share, and
+// joins the segments with the same affine composition as the chunks:
+//   1. k_gae_seg_fold: tile (g, s >= 1) folds its segment into (P, S) per
+//      environment, A_{row0(s)} = P A_{row0(s+1)} + S, and parks the pair as
+//      four 32-bit words in rows row0(s-1) .. row0(s-1)+3 of ret (segment s-1
+//      is a full segment; segment 0's map is never needed);
+//   2. k_gae_seg_carry: per group of 32 environments, a suffix scan over the
+//      parked maps gives A at the start of every segment s >= 1, i.e. the carry
+//      of segment s-1, written as two words into rows row0(s-1), row0(s-1)+1 of
+//      adv (A_T = 0 seeds it);
+//   3. k_gae_seg_replay: tile (g, s) folds its chunks again, scans them, takes
+//      its carry (0 for the last segment) and replays, writing adv and ret.
+// Launches are ordered by the stream, each launch reads what the one before
+// wrote, and a tile overwrites the parked words of its own segment only after
+// every lane of the tile has read its carry, so no launch needs anything but
+// the caller's arrays.
+constexpr int kSegQuads = 8;                         // environment quads per tile
+constexpr int kSegEnvs = kSegQuads * kV;             // 32 environments: one line per row
+constexpr int kSegChunks = 32;                       // chunk lanes per tile
+constexpr int kSegThreads = kSegQuads * kSegChunks;  // 256
+constexpr int kSegWaves = kSegThreads / kWave;       // 4
+constexpr int kChunksPerWave = kWave / kSegQuads;    // 8
+
+// Affine maps of four environments: A_start = P * A_end + S.
+struct Map4 {
+    double P[kV], S[kV];
+};
+
+__device__ __forceinline__ Map4 map_identity() {
+    Map4 m;
+#pragma unroll
+    for (int j = 0; j < kV; ++j) {
+        m.P[j] = 1.0;
+        m.S[j] = 0.0;
+    }
+    return m;
+}
+
+// f then g in time (f covers the earlier steps): A_start(f) = P_f (P_g A + S_g) + S_f
+__device__ __forceinline__ Map4 map_compose(const Map4& f, const Map4& g) {
+    Map4 r;
+#pragma unroll
+    for (int j = 0; j < kV; ++j) {
+        r.S[j] = f.S[j] + f.P[j] * g.S[j];
+        r.P[j] = f.P[j] * g.P[j];
+    }
+    return r;
+}
+
+// Lane layout of a tile: wavefront w holds chunks 8w .. 8w + 7 of all 8 quads,
+// lane = quad * 8 + chunk % 8.  A quad's chunks of one wavefront are 8
+// neighbouring lanes (a DPP row holds two quads), and every load instruction
+// still reads 8 rows of 8 quads: 8 whole 128-byte lines.
+__device__ __forceinline__ void seg_lane(int* q, int* c) {
+    const int lane = (int)threadIdx.x % kWave;
+    *q = lane / kChunksPerWave;
+    *c = (int)(threadIdx.x / kWave) * kChunksPerWave + lane % kChunksPerWave;
+}
+
+// the maps of the lane N places up in the same DPP row (register moves only)
+template <int N>
+__device__ __forceinline__ Map4 map_from_lane_up(const Map4& m) {
+    Map4 r;
+#pragma unroll
+    for (int j = 0; j < kV; ++j) {
+        r.P[j] = __longlong_as_double(
+            (long long)dpp_u64<kDppRowShl + N, 0xf, 0xf>((uint64_t)__double_as_longlong(m.P[j])));
+        r.S[j] = __longlong_as_double(
+            (long long)dpp_u64<kDppRowShl + N, 0xf, 0xf>((uint64_t)__double_as_longlong(m.S[j])));
+    }
+    return r;
+}
+
+// Suffix composition over the 32 chunks of a tile (lanes as in seg_lane).
+// Returns, for chunk c, incl = map(c) o ... o map(31) and excl = map(c + 1) o
+// ... o map(31) (the identity for chunk 31).  Hillis-Steele over the 8 lanes of
+// a quad with DPP row shifts, one exchange of the wavefront totals through LDS
+// and one barrier.
+__device__ __forceinline__ void tile_suffix(const Map4& own, int c, int q, Map4* incl, Map4* excl) {
+    __shared__ double sWP[kSegWaves][kSegQuads][kV];
+    __shared__ double sWS[kSegWaves][kSegQuads][kV];
+    const int cw = c % kChunksPerWave;
+    Map4 in = own;
+    {
+        const Map4 nx = map_from_lane_up<1>(in);
+        if (cw + 1 < kChunksPerWave) in = map_compose(in, nx);
+    }
+    {
+        const Map4 nx = map_from_lane_up<2>(in);
+        if (cw + 2 < kChunksPerWave) in = map_compose(in, nx);
+    }
+    {
+        const Map4 nx = map_from_lane_up<4>(in);
+        if (cw + 4 < kChunksPerWave) in = map_compose(in, nx);
+    }
+    Map4 ex = map_from_lane_up<1>(in);
+    if (cw == kChunksPerWave - 1) ex = map_identity();
+    const int w = c / kChunksPerWave;
+    if (cw == 0) {
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            sWP[w][q][j] = in.P[j];
+            sWS[w][q][j] = in.S[j];
+        }
+    }
+    __syncthreads();
+    Map4 later = map_identity();  // wavefronts w + 1 .. 3, in time order
+#pragma unroll
+    for (int v = kSegWaves - 1; v > 0; --v) {
+        if (v > w) {
+            Map4 t;
+#pragma unroll
+            for (int j = 0; j < kV; ++j) {
+                t.P[j] = sWP[v][q][j];
+                t.S[j] = sWS[v][q][j];
+            }
+            later = map_compose(t, later);
+        }
+    }
+    *incl = map_compose(in, later);
+    *excl = map_compose(ex, later);
+}
+
+// Tile coordinates: workgroups are dealt round-robin to the 8 XCDs; the ones on
+// one XCD take consecutive tiles, i.e. neighbouring environment groups of one
+// segment, which share the lines of the done rows.
+__device__ __forceinline__ int64_t tile_of_block() {
+    const int64_t nb = gridDim.x;
+    return nb % 8 == 0 ? (int64_t)(blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : (int64_t)blockIdx.x;
+}
+
+// Loads and folds one lane's chunk: L steps from row t0 of the quad at column
+// e0 (steps at or past T are skipped; their loads re-read row T - 1).
+template <bool TRUNC, int L>
+struct SegChunk {
+    f32x4 r[L], v[L];
+    uint32_t d[L];
+    uint32_t tr[TRUNC ? L : 1];
+    f32x4 fv[TRUNC ? L : 1];
+    f32x4 ve;
+
+    __device__ __forceinline__ void load(const GaeArgs& a, int64_t t0, int64_t e0) {
+        const int64_t E = a.E, T = a.T;
+#pragma unroll
+        for (int k = 0; k < L; ++k) {
+            const int64_t t = t0 + k < T ? t0 + k : T - 1;
+            const int64_t o = t * E + e0;
+            r[k] = *reinterpret_cast<const f32x4*>(a.reward + o);
+            v[k] = a.value ? *reinterpret_cast<const f32x4*>(a.value + o) : (f32x4)(0.0f);
+            d[k] = *reinterpret_cast<const uint32_t*>(a.done + o);
+            if constexpr (TRUNC) {
+                tr[TRUNC ? k : 0] = *reinterpret_cast<const uint32_t*>(a.truncated + o);
+                fv[TRUNC ? k : 0] = *reinterpret_cast<const f32x4*>(a.final_value + o);
+            }
+        }
+        const int64_t t1 = t0 + L;
+        if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4*>(a.bootstrap + e0) : (f32x4)(0.0f);
+        else ve = a.value ? *reinterpret_cast<const f32x4*>(a.value + t1 * E + e0) : (f32x4)(0.0f);
+    }
+
+    __device__ __forceinline__ void step(const GaeArgs& a, double gl, int k, int j, double vn, double* delta,
+                                         double* m) const {
+        gae_step<TRUNC>((double)r[k][j], (double)v[k][j], vn, (uint8_t)(d[k] >> (8 * j)),
+                        TRUNC ? (uint8_t)(tr[TRUNC ? k : 0] >> (8 * j)) : 0, TRUNC ? fv[TRUNC ? k : 0][j] : 0.0f,
+                        a.gamma, gl, delta, m);
+    }
+
+    // A_start = P A_end + S over the chunk's live steps
+    __device__ __forceinline__ Map4 fold(const GaeArgs& a, double gl, int64_t t0) const {
+        Map4 m = map_identity();
+        double vn[kV];
+#pragma unroll
+        for (int j = 0; j < kV; ++j) vn[j] = (double)ve[j];
+#pragma unroll
+        for (int k = L - 1; k >= 0; --k) {
+            if (t0 + k < a.T) {
+#pragma unroll
+                for (int j = 0; j < kV; ++j) {
+                    double delta, mk;
+                    step(a, gl, k, j, vn[j], &delta, &mk);
+                    m.S[j] = delta + mk * m.S[j];
+                    m.P[j] = mk * m.P[j];
+                    vn[j] = (double)v[k][j];
+                }
+            }
+        }
+        return m;
+    }
+};
+
+// The 32-bit words of a double, low word first.
+__device__ __forceinline__ uint32_t dlo(double x) { return (uint32_t)__double_as_longlong(x); }
+__device__ __forceinline__ uint32_t dhi(double x) { return (uint32_t)((uint64_t)__double_as_longlong(x) >> 32); }
+__device__ __forceinline__ double dword2(uint32_t lo, uint32_t hi) {
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool TRUNC, int L>
+__global__ __launch_bounds__(kSegThreads) void k_gae_seg_fold(GaeArgs a, int32_t groups) {
+    constexpr int64_t Ts = (int64_t)kSegChunks * L;
+    int q, c;
+    seg_lane(&q, &c);
+    const int64_t tile = tile_of_block();
+    const int64_t g = tile % groups, s = 1 + tile / groups;
+    const int64_t E = a.E;
+    const int64_t e_raw = g * kSegEnvs + q * kV;
+    const bool active = e_raw < E;
+    const int64_t e0 = active ? e_raw : E - kV;
+    const int64_t t0 = s * Ts + (int64_t)c * L;
+    SegChunk<TRUNC, L> ch;
+    ch.load(a, t0, e0);
+    const Map4 own = ch.fold(a, a.gamma * a.lambda, t0);
+    Map4 incl, excl;
+    tile_suffix(own, c, q, &incl, &excl);
+    if (c == 0 && active) {  // the segment's map, parked in segment s - 1
+        u32x4* dst = reinterpret_cast<u32x4*>(a.ret + (s - 1) * Ts * E + e0);
+        const int64_t rs = E / kV;  // row stride in 16-byte vectors
+        u32x4 w0, w1, w2, w3;
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            w0[j] = dlo(incl.P[j]);
+            w1[j] = dhi(incl.P[j]);
+            w2[j] = dlo(incl.S[j]);
+            w3[j] = dhi(incl.S[j]);
+        }
+        dst[0] = w0;
+        dst[rs] = w1;
+        dst[2 * rs] = w2;
+        dst[3 * rs] = w3;
+    }
+}
+
+// One workgroup per group of 32 environments; lanes as in seg_lane, chunk = segment, 32
+// segments per pass, passes from the end with the carried A.
+__global__ __launch_bounds__(kSegThreads) void k_gae_seg_carry(float* adv, const float* ret, int64_t E, int64_t Ts,
+                                                              int64_t S) {
+    __shared__ double s_carry[kSegQuads][kV];
+    int q, c;
+    seg_lane(&q, &c);
+    const int64_t g = blockIdx.x;
+    const int64_t e_raw = g * kSegEnvs + q * kV;
+    const bool active = e_raw < E;
+    const int64_t e0 = active ? e_raw : E - kV;
+    const int64_t rs = E / kV;
+    double carry[kV];
+#pragma unroll
+    for (int j = 0; j < kV; ++j) carry[j] = 0.0;  // A_T = 0
+    // segments 1 .. S-1 in passes of 32 from the end: pass p covers
+    // hi - 31 .. hi, chunk c takes segment hi - 31 + c (chunks below 1 idle)
+    for (int64_t hi = S - 1; hi >= 1; hi -= kSegChunks) {
+        const int64_t seg = hi - (kSegChunks - 1) + c;
+        const bool live = seg >= 1;
+        const int64_t sr = live ? seg : hi;  // idle lanes read a valid map
+        const u32x4* src = reinterpret_cast<const u32x4*>(ret + (sr - 1) * Ts * E + e0);
+        const u32x4 w0 = src[0], w1 = src[rs], w2 = src[2 * rs], w3 = src[3 * rs];
+        Map4 own;
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            own.P[j] = live ? dword2(w0[j], w1[j]) : 1.0;
+            own.S[j] = live ? dword2(w2[j], w3[j]) : 0.0;
+        }
+        Map4 incl, excl;
+        tile_suffix(own, c, q, &incl, &excl);
+        double A[kV];
+#pragma unroll
+        for (int j = 0; j < kV; ++j) A[j] = incl.P[j] * carry[j] + incl.S[j];  // A at row0(seg)
+        if (live && active) {
+            u32x4* dst = reinterpret_cast<u32x4*>(adv + (seg - 1) * Ts * E + e0);
+            u32x4 lo, hw;
+#pragma unroll
+            for (int j = 0; j < kV; ++j) {
+                lo[j] = dlo(A[j]);
+                hw[j] = dhi(A[j]);
+            }
+            dst[0] = lo;
+            dst[rs] = hw;
+        }
+        if (hi - kSegChunks < 1) break;  // uniform
+        // the next pass starts from A at row0(hi - 31), held by chunk c = 0
+        if (c == 0) {
+#pragma unroll
+            for (int j = 0; j < kV; ++j) s_carry[q][j] = A[j];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kV; ++j) carry[j] = s_carry[q][j];
+        __syncthreads();  // s_carry and the scan's LDS are rewritten by the next pass
+    }
+}
+
+template <bool TRUNC, int L>
+__global__ __launch_bounds__(kSegThreads) void k_gae_seg_replay(GaeArgs a, int32_t groups, int64_t S) {
+    constexpr int64_t Ts = (int64_t)kSegChunks * L;
+    int q, c;
+    seg_lane(&q, &c);
+    const int64_t tile = tile_of_block();
+    const int64_t g = tile % groups, s = tile / groups;
+    const int64_t E = a.E, T = a.T;
+    const int64_t e_raw = g * kSegEnvs + q * kV;
+    const bool active = e_raw < E;
+    const int64_t e0 = active ? e_raw : E - kV;
+    const int64_t rs = E / kV;
+    const int64_t row0 = s * Ts;
+    const int64_t t0 = row0 + (int64_t)c * L;
+    // the carry first: rows row0, row0 + 1 of adv are rewritten below
+    u32x4 clo = (u32x4)(0u), chi = (u32x4)(0u);
+    if (s + 1 < S) {
+        const u32x4* src = reinterpret_cast<const u32x4*>(a.adv + row0 * E + e0);
+        clo = src[0];
+        chi = src[rs];
+    }
+    SegChunk<TRUNC, L> ch;
+    ch.load(a, t0, e0);
+    const double gl = a.gamma * a.lambda;
+    const Map4 own = ch.fold(a, gl, t0);
+    double cin[kV];
+#pragma unroll
+    for (int j = 0; j < kV; ++j) cin[j] = dword2(clo[j], chi[j]);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // every load of this lane has returned
+    Map4 incl, excl;
+    tile_suffix(own, c, q, &incl, &excl);  // its barrier orders the carry reads before the stores
+    double A[kV], vn[kV];
+#pragma unroll
+    for (int j = 0; j < kV; ++j) {
+        A[j] = excl.P[j] * cin[j] + excl.S[j];  // A at the end of this chunk
+        vn[j] = (double)ch.ve[j];
+    }
+#pragma unroll
+    for (int k = L - 1; k >= 0; --k) {
+        if (t0 + k < T) {
+            f32x4 ao, ro;
+#pragma unroll
+            for (int j = 0; j < kV; ++j) {
+                double delta, m;
+                ch.step(a, gl, k, j, vn[j], &delta, &m);
+                A[j] = delta + m * A[j];
+                ao[j] = (float)A[j];
+                ro[j] = (float)(A[j] + (double)ch.v[k][j]);
+                vn[j] = (double)ch.v[k][j];
+            }
+            if (active) {
+                const int64_t o = (t0 + k) * E + e0;
+                *reinterpret_cast<f32x4*>(a.adv + o) = ao;
+                *reinterpret_cast<f32x4*>(a.ret + o) = ro;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Time-major GAE split along T in one launch (decoupled look-back).  The tiles
+// are those of the three-launch path, dealt in block order with the later
+// segments first: a workgroup only ever waits for workgroups with smaller
+// block indices, which the dispatcher has started before it, and those publish
+// their segment's map without waiting for anyone.  A tile
+//   1. folds its chunks and scans them (as k_gae_seg_replay);
+//   2. publishes its segment's map (P, S), or, for the last segment, A at its
+//      first step (A_T = 0), and raises its flag;
+//   3. looks back over the later segments of its environment group in windows
+//      of 32 (one per chunk lane): it waits for every flag of the window, takes
+//      A where a segment has published it (the constant map P = 0, S = A) and
+//      (P, S) otherwise, composes the window, and stops at the first window
+//      that holds a published A or reaches the end of the rollout;
+//   4. publishes A at its own first step when the rollout is longer than one
+//      window (so that look-backs of earlier tiles stop early), then replays its
+//      chunks from the carry.
+// Maps and flags live in a small per-GPU table (static device memory, no
+// allocation).  A flag holds the call's epoch next to its state, and every
+// call takes a new epoch on the host, so nothing an earlier call left in the
+// table is ever taken for this call's; a call enqueued under stream capture,
+// whose epoch its graph replays repeat, first clears the flags with a
+// one-workgroup kernel.  Calls that overlap on one GPU share the table and
+// race; a wait that outlasts its bound gives up, flags ERR_GAE_WAIT and lets
+// the kernel finish.  Every published value is written with agent-scope atomic
+// stores and acknowledged before the flag is raised; readers use agent-scope
+// atomic loads.
+constexpr int kLookMaxTiles = 4096;
+constexpr int kLookSpin = 1 << 15;  // polls of one flag before a wait gives up (tens of ms)
+constexpr uint64_t kFlagMap = 1, kFlagA = 2;
+
+__device__ uint64_t g_look_flag[kLookMaxTiles];              // epoch << 2 | state
+__device__ uint64_t g_look_map[kLookMaxTiles][2][kSegEnvs];  // P, S of the segment (fp64 bits)
+__device__ uint64_t g_look_a[kLookMaxTiles][kSegEnvs];       // A at the segment's first step
+
+__global__ __launch_bounds__(kSegThreads) void k_gae_look_clear(int32_t tiles) {
+    for (int i = threadIdx.x; i < tiles; i += kSegThreads)
+        __hip_atomic_store(&g_look_flag[i], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void put_f64(uint64_t* p, double x) {
+    __hip_atomic_store(p, (uint64_t)__double_as_longlong(x), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double get_f64(uint64_t* p) {
+    return __longlong_as_double((long long)__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+
+template <bool TRUNC, int L>
+__global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, int32_t groups, int32_t S, uint64_t epoch) {
+    constexpr int64_t Ts = (int64_t)kSegChunks * L;
+    __shared__ double s_cin[kSegQuads][kV];
+    int q, c;
+    seg_lane(&q, &c);
+    const int64_t s = S - 1 - (int64_t)(blockIdx.x / (uint32_t)groups);  // later segments first
+    const int64_t g = blockIdx.x % (uint32_t)groups;
+    const int64_t me = s * groups + g;  // table row of this tile
+    const int64_t E = a.E, T = a.T;
+    const int64_t e_raw = g * kSegEnvs + q * kV;
+    const bool active = e_raw < E;
+    const int64_t e0 = active ? e_raw : E - kV;
+    const int64_t t0 = s * Ts + (int64_t)c * L;
+    const double gl = a.gamma * a.lambda;
+    SegChunk<TRUNC, L> ch;
+    ch.load(a, t0, e0);
+    const Map4 own = ch.fold(a, gl, t0);
+    Map4 incl, excl;
+    tile_suffix(own, c, q, &incl, &excl);  // incl of chunk 0: the segment's map
+    const bool last = s == S - 1;
+    if (c == 0) {  // lanes 0..7 of wavefront 0, one per quad
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            if (last) {
+                put_f64(&g_look_a[me][q * kV + j], incl.S[j]);
+            } else {
+                put_f64(&g_look_map[me][0][q * kV + j], incl.P[j]);
+                put_f64(&g_look_map[me][1][q * kV + j], incl.S[j]);
+            }
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // acknowledged device-wide
+        if (q == 0)
+            __hip_atomic_store(&g_look_flag[me], epoch << 2 | (last ? kFlagA : kFlagMap), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (!last) {  // uniform
+        Map4 acc = map_identity();  // the windows so far, in time order (chunk-0 lanes)
+        for (int64_t w0 = s + 1;; w0 += kSegChunks) {
+            const int64_t sj = w0 + c;
+            Map4 m = map_identity();
+            int stop = 0;
+            if (sj < S) {
+                const int64_t j = sj * groups + g;
+                uint64_t f = 0;
+                for (int it = 0; it < kLookSpin; ++it) {
+                    const uint64_t w = __hip_atomic_load(&g_look_flag[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    f = (w >> 2) == epoch ? (w & 3) : 0;
+                    if (f) break;
+                    __builtin_amdgcn_s_sleep(2);
+                }
+                if (f == kFlagMap) {
+#pragma unroll
+                    for (int jj = 0; jj < kV; ++jj) {
+                        m.P[jj] = get_f64(&g_look_map[j][0][q * kV + jj]);
+                        m.S[jj] = get_f64(&g_look_map[j][1][q * kV + jj]);
+                    }
+                } else {
+                    // A published (or the wait gave up: flagged, A taken as 0)
+#pragma unroll
+                    for (int jj = 0; jj < kV; ++jj) {
+                        m.P[jj] = 0.0;
+                        m.S[jj] = f == kFlagA ? get_f64(&g_look_a[j][q * kV + jj]) : 0.0;
+                    }
+                    if (f != kFlagA && q == 0) flag_error(a.err, ERR_GAE_WAIT);
+                    stop = 1;
+                }
+            } else {
+                stop = 1;  // past the last step: A_T = 0
+            }
+            __syncthreads();  // the scan's LDS is free again
+            Map4 wi, we;
+            tile_suffix(m, c, q, &wi, &we);
+            acc = map_compose(acc, wi);
+            if (__syncthreads_or(stop)) break;
+        }
+        // A at the end of this segment is acc applied to 0 (a constant map ends
+        // every window chain); A at its first step goes to the table when some
+        // look-back window does not reach the end of the rollout
+        if (c == 0) {
+#pragma unroll
+            for (int j = 0; j < kV; ++j) s_cin[q][j] = acc.S[j];
+            if (S > kSegChunks + 1) {
+#pragma unroll
+                for (int j = 0; j < kV; ++j) put_f64(&g_look_a[me][q * kV + j], incl.P[j] * acc.S[j] + incl.S[j]);
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                if (q == 0)
+                    __hip_atomic_store(&g_look_flag[me], epoch << 2 | kFlagA, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+    } else if (c == 0) {
+#pragma unroll
+        for (int j = 0; j < kV; ++j) s_cin[q][j] = 0.0;  // A_T = 0
+    }
+    __syncthreads();
+    double A[kV], vn[kV];
+#pragma unroll
+    for (int j = 0; j < kV; ++j) {
+        A[j] = excl.P[j] * s_cin[q][j] + excl.S[j];  // A at the end of this chunk
+        vn[j] = (double)ch.ve[j];
+    }
+#pragma unroll
+    for (int k = L - 1; k >= 0; --k) {
+        if (t0 + k < T) {
+            f32x4 ao, ro;
+#pragma unroll
+            for (int j = 0; j < kV; ++j) {
+                double delta, m;
+                ch.step(a, gl, k, j, vn[j], &delta, &m);
+                A[j] = delta + m * A[j];
+                ao[j] = (float)A[j];
+                ro[j] = (float)(A[j] + (double)ch.v[k][j]);
+                vn[j] = (double)ch.v[k][j];
+            }
+            if (active) {
+                const int64_t o = (t0 + k) * E + e0;
+                *reinterpret_cast<f32x4*>(a.adv + o) = ao;
+                *reinterpret_cast<f32x4*>(a.ret + o) = ro;
+            }
+        }
+    }
+}
+
 constexpr int kPkThreads = 256;
 constexpr int kPkChunk = 16;                      // elements per lane and segment
 constexpr int kPkSeg = kPkThreads * kPkChunk;     // 4096 elements per pass
@@ -512,6 +1050,59 @@ __global__ void k_fill_u64(uint64_t* p, uint64_t v, int64_t n) {
 
 }  // namespace
 
+template <bool TRUNC, int L>
+hipError_t launch_gae_split_t(const GaeArgs& a, int64_t groups, hipStream_t s) {
+    constexpr int64_t Ts = (int64_t)kSegChunks * L;
+    const int64_t S = (a.T + Ts - 1) / Ts;
+    const dim3 block(kSegThreads);
+    hipLaunchKernelGGL((k_gae_seg_fold<TRUNC, L>), dim3((unsigned)(groups * (S - 1))), block, 0, s, a,
+                       (int32_t)groups);
+    hipLaunchKernelGGL(k_gae_seg_carry, dim3((unsigned)groups), block, 0, s, a.adv, a.ret, a.E, Ts, S);
+    hipLaunchKernelGGL((k_gae_seg_replay<TRUNC, L>), dim3((unsigned)(groups * S)), block, 0, s, a, (int32_t)groups,
+                       S);
+    return hipGetLastError();
+}
+
+template <bool TRUNC>
+hipError_t launch_gae_split_l(const GaeArgs& a, int64_t groups, int L, hipStream_t s) {
+    switch (L) {
+        case 8: return launch_gae_split_t<TRUNC, 8>(a, groups, s);
+        case 4: return launch_gae_split_t<TRUNC, 4>(a, groups, s);
+        default: return launch_gae_split_t<TRUNC, 2>(a, groups, s);
+    }
+}
+
+hipError_t launch_gae_split(const GaeArgs& a, int64_t groups, int L, hipStream_t s) {
+    return a.truncated ? launch_gae_split_l<true>(a, groups, L, s) : launch_gae_split_l<false>(a, groups, L, s);
+}
+
+template <bool TRUNC>
+hipError_t launch_gae_look_l(const GaeArgs& a, int32_t groups, int32_t S, int L, uint64_t ep, hipStream_t s) {
+    const dim3 grid((unsigned)(groups * S)), block(kSegThreads);
+    switch (L) {
+        case 8: hipLaunchKernelGGL((k_gae_look<TRUNC, 8>), grid, block, 0, s, a, groups, S, ep); break;
+        case 4: hipLaunchKernelGGL((k_gae_look<TRUNC, 4>), grid, block, 0, s, a, groups, S, ep); break;
+        default: hipLaunchKernelGGL((k_gae_look<TRUNC, 2>), grid, block, 0, s, a, groups, S, ep); break;
+    }
+    return hipGetLastError();
+}
+
+std::atomic<uint64_t> g_look_epoch{0};  // epochs of the look-back table, 1, 2, ... (62 bits)
+
+hipError_t launch_gae_look(const GaeArgs& a, int32_t groups, int32_t S, int L, hipStream_t s) {
+    const uint64_t ep = (g_look_epoch.fetch_add(1) + 1) & ((1ull << 62) - 1);
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(s, &cap);
+    if (e != hipSuccess) return e;
+    if (cap != hipStreamCaptureStatusNone) {  // replays repeat the epoch: clear the flags first
+        hipLaunchKernelGGL(k_gae_look_clear, dim3(1), dim3(kSegThreads), 0, s, groups * S);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return a.truncated ? launch_gae_look_l<true>(a, groups, S, L, ep, s)
+                       : launch_gae_look_l<false>(a, groups, S, L, ep, s);
+}
+
 hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
     if (a.T <= 0 || a.E <= 0) return hipSuccess;
     if (a.E > kGaeMaxEnvs) return hipErrorInvalidValue;  // the ABI rejects this first
@@ -519,6 +1110,24 @@ hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
     const bool vec = a.E % kV == 0 && al(a.reward, 16) && al(a.value, 16) && al(a.bootstrap, 16) &&
                      al(a.adv, 16) && al(a.ret, 16) && al(a.done, 4) && al(a.truncated, 4) &&
                      al(a.final_value, 16);
+    if (vec && a.E < kGaeSplitMaxEnvs) {
+        // split along T: the largest chunk length that still gives every compute
+        // unit tiles, and at least two segments
+        const int64_t groups = (a.E + kSegEnvs - 1) / kSegEnvs;
+        int L = 0;
+        for (int cand : {8, 4, 2}) {
+            const int64_t segs = (a.T + (int64_t)kSegChunks * cand - 1) / ((int64_t)kSegChunks * cand);
+            if (segs >= 2 && (groups * segs >= kGaeSplitMinTiles || cand == 2)) {
+                L = cand;
+                break;
+            }
+        }
+        if (L) {
+            const int64_t segs = (a.T + (int64_t)kSegChunks * L - 1) / ((int64_t)kSegChunks * L);
+            if (groups * segs <= kLookMaxTiles) return launch_gae_look(a, (int32_t)groups, (int32_t)segs, L, s);
+            return launch_gae_split(a, groups, L, s);
+        }
+    }
     if (vec) {
         const int64_t vblocks = (a.E + kEnvsV - 1) / kEnvsV;
         constexpr int L = kGaeVecChunk;

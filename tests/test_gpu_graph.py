@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import synth
-from gpu_util import assert_weights_close, dev, host
+from gpu_util import assert_gae_close, assert_weights_close, dev, host
 
 pytestmark = pytest.mark.gpu
 
@@ -89,3 +89,56 @@ def test_captured_sample_gather_and_update_replays():
     buf.read(cd.COL_LEAVES, leaves)
     assert np.array_equal(host(leaves).view(np.uint32), orc.leaf)
     buf.close()
+
+
+def test_captured_gae_replays():
+    """Time-major GAE on the one-launch split path (table clear + look-back
+    kernel) captured once and replayed with new rollouts, with eager GAE calls
+    of other shapes between the replays."""
+    print("graph: capture gae [2048, 256], 4 replays", flush=True)
+    T, E = 2048, 256
+    rng = np.random.default_rng(5)
+    r_s = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    v_s = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    d_s = torch.empty((T, E), dtype=torch.uint8, device="cuda")
+    b_s = torch.empty(E, dtype=torch.float32, device="cuda")
+    adv = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    ret = torch.empty((T, E), dtype=torch.float32, device="cuda")
+
+    def draw():
+        return (rng.standard_normal((T, E)).astype(np.float32), rng.standard_normal((T, E)).astype(np.float32),
+                (rng.random((T, E)) < 0.01).astype(np.uint8), rng.standard_normal(E).astype(np.float32))
+
+    def gae():
+        cd.conduit_gae(r_s, v_s, d_s, b_s, 0.99, 0.95, adv, ret)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        gae()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        gae()
+    torch.cuda.synchronize()
+    for k in range(4):
+        r, v, d, b = draw()
+        for dst, src in ((r_s, r), (v_s, v), (d_s, d), (b_s, b)):
+            dst.copy_(dev(src))
+        adv.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        oa, orr = oracle.gae(r, v, d, b, 0.99, 0.95)
+        assert_gae_close(host(adv), oa)
+        assert_gae_close(host(ret), orr)
+        # eager calls between replays: more tiles, then fewer
+        for T2, E2 in ((3000, 1000), (300, 8)):
+            r2 = rng.standard_normal((T2, E2)).astype(np.float32)
+            d2 = np.zeros((T2, E2), np.uint8)
+            a2 = torch.empty((T2, E2), dtype=torch.float32, device="cuda")
+            x2 = torch.empty((T2, E2), dtype=torch.float32, device="cuda")
+            cd.conduit_gae(dev(r2), None, dev(d2), None, 0.9, 0.8, a2, x2)
+            oa2, _ = oracle.gae(r2, None, d2, None, 0.9, 0.8)
+            assert_gae_close(host(a2), oa2)
+    assert cd.conduit_sync_check() == cd.OK, cd.last_error()

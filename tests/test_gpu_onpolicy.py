@@ -28,8 +28,8 @@ def _gae_gpu(r, v, d, b, gamma, lam):
     (1, 1, 0.0, True, True), (2, 3, 0.5, True, False), (37, 19, 0.05, True, True), (64, 16, 0.0, False, False),
     (65, 17, 1.0, True, True), (200, 70, 0.01, True, True), (1000, 5, 0.002, True, True),
     (2500, 9, 0.003, True, True), (1024, 8, 0.0, True, False), (3073, 3, 0.01, False, True),
-    # E a multiple of 4 (four environments per lane): a half-used workgroup,
-    # several 2048-step passes with a partial one, an XCD-remapped grid
+    # E a multiple of 4: four environments per lane, split along T where T > 64
+    # (see SPLIT_CASES below), one pass of all T steps for T <= 64
     (100, 12, 0.02, True, True), (2500, 12, 0.003, True, True), (4096, 8, 0.001, True, True),
     (2049, 4, 0.01, True, False), (300, 128, 0.01, True, True), (33, 64, 0.1, False, False),
     # the most environments the ABI takes (2^19), on both kernels
@@ -68,6 +68,97 @@ def test_gae_truncated_shapes(T, E, p_done, p_trunc):
         oa, orr = oracle.gae(r, v, d, b, gamma, lam, truncated=tr, final_value=fv)
         assert_gae_close(host(adv), oa)
         assert_gae_close(host(ret), orr)
+
+
+# Which kernels a shape takes (E a multiple of 4 with aligned rows): fewer than
+# 4,096 environments and more than 64 steps split the rollout along T into
+# tiles of 32 environments by 32 L steps (L = 8, 4 or 2, the longest that still
+# gives 256 tiles); up to 4,096 tiles run in one launch with a look-back over
+# the later segments ("look"), more in three launches ("split").  Otherwise one
+# workgroup walks all T steps of 8 environments ("one").
+SPLIT_CASES = [
+    # (T, E, p_done, expected path, expected chunk length)
+    (65, 4, 0.05, "look", 2),         # two segments, the last one a single step
+    (129, 36, 0.02, "look", 2),       # a partial environment group (36 = 32 + 4)
+    (2048, 256, 0.001, "look", 2),    # 32 segments of 64 steps: one look-back window
+    (40000, 4, 0.0005, "look", 4),    # 313 segments: look-backs chained over windows
+    (16000, 100, 0.001, "look", 4),   # 125 segments x 4 groups (last one 4 envs)
+    (65573, 4, 0.0005, "look", 8),    # 257 segments of 256 steps, ragged end
+    (2100, 1000, 0.003, "look", 8),   # 9 segments, 32 groups (last one 8 envs)
+    (1100, 4052, 0.003, "look", 8),   # 5 segments, 127 groups (last one 20 envs)
+    (3000, 4092, 0.01, "look", 8),    # the widest split
+    (1048576, 4, 0.0001, "look", 8),  # 4,096 tiles: the most one launch takes
+    (1100000, 4, 0.0001, "split", 8),  # 4,297 tiles: three launches, 135 carry passes
+    (600000, 36, 0.0002, "split", 8),  # 4,688 tiles, a partial group
+]
+
+def _time_major_path(T, E):
+    """(path, chunk length) the launcher picks for an aligned [T, E] rollout."""
+    if E % 4 or E >= 4096:
+        return "one", 0
+    groups = -(-E // 32)
+    for L in (8, 4, 2):
+        segs = -(-T // (32 * L))
+        if segs >= 2 and (groups * segs >= 256 or L == 2):
+            return ("look" if groups * segs <= 4096 else "split"), L
+    return "one", 0
+
+
+@pytest.mark.parametrize("T,E,p_done,path,L", SPLIT_CASES)
+def test_gae_split_along_t(T, E, p_done, path, L):
+    print(f"gae split T={T} E={E} {path} L={L}", flush=True)
+    assert _time_major_path(T, E) == (path, L)
+    rng = np.random.default_rng(T * 7 + E)
+    r = rng.standard_normal((T, E)).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32)
+    d = (rng.random((T, E)) < p_done).astype(np.uint8)
+    b = rng.standard_normal(E).astype(np.float32)
+    for gamma, lam in [(0.99, 0.95), (1.0, 1.0)]:
+        ga, gr = _gae_gpu(r, v, d, b, gamma, lam)
+        oa, orr = oracle.gae(r, v, d, b, gamma, lam)
+        assert_gae_close(ga, oa)
+        assert_gae_close(gr, orr)
+    # no values, no bootstrap, every step done: delta = r and A = r exactly
+    ones = np.ones((T, E), np.uint8)
+    ga, gr = _gae_gpu(r, None, ones, None, 0.99, 0.95)
+    assert np.array_equal(ga, r) and np.array_equal(gr, r)
+
+
+@pytest.mark.parametrize("T,E", [(2100, 1000), (1100, 4052), (700, 36), (1100000, 4)])
+def test_gae_truncated_split_along_t(T, E):
+    print(f"gae truncated split T={T} E={E}", flush=True)
+    assert _time_major_path(T, E)[0] != "one"
+    rng = np.random.default_rng(T * 11 + E)
+    r = rng.standard_normal((T, E)).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32)
+    d = (rng.random((T, E)) < 0.004).astype(np.uint8)
+    tr = (rng.random((T, E)) < 0.004).astype(np.uint8)
+    fv = rng.standard_normal((T, E)).astype(np.float32)
+    b = rng.standard_normal(E).astype(np.float32)
+    adv = torch.full((T, E), np.nan, dtype=torch.float32, device="cuda")
+    ret = torch.full((T, E), np.nan, dtype=torch.float32, device="cuda")
+    cd.conduit_gae_truncated(dev(r), dev(v), dev(d), dev(tr), dev(fv), dev(b), 0.99, 0.95, adv, ret)
+    assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+    oa, orr = oracle.gae(r, v, d, b, 0.99, 0.95, truncated=tr, final_value=fv)
+    assert_gae_close(host(adv), oa)
+    assert_gae_close(host(ret), orr)
+
+
+@pytest.mark.parametrize("T,E", [(2100, 4096), (4097, 4100)])
+def test_gae_single_pass_kernel_several_passes(T, E):
+    """4,096 environments or more keep one workgroup per 8 environments walking
+    2,048-step passes (a partial last pass here)."""
+    print(f"gae single-pass T={T} E={E}", flush=True)
+    assert _time_major_path(T, E)[0] == "one"
+    rng = np.random.default_rng(T + E)
+    r = rng.standard_normal((T, E)).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32)
+    d = (rng.random((T, E)) < 0.002).astype(np.uint8)
+    b = rng.standard_normal(E).astype(np.float32)
+    ga, gr = _gae_gpu(r, v, d, b, 0.99, 0.95)
+    oa, orr = oracle.gae(r, v, d, b, 0.99, 0.95)
+    assert_gae_close(ga, oa)
+    assert_gae_close(gr, orr)
 
 
 def test_gae_misaligned_rows_take_the_lane_per_environment_kernel():
