@@ -793,7 +793,10 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, int32_t gro
                 uint64_t f = 0;
                 for (int it = 0; it < kLookSpin; ++it) {
                     const uint64_t w = __hip_atomic_load(&g_look_flag[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    f = (w >> 2) == epoch ? (w & 3) : 0;
+                    // the 8 quads of a segment take quad 0's reading (lane
+                    // chunk % 8), so they agree on where their chains end
+                    f = (uint64_t)__shfl((int)((w >> 2) == epoch ? (w & 3) : 0), (int)(threadIdx.x % kChunksPerWave),
+                                         kWave);
                     if (f) break;
                     __builtin_amdgcn_s_sleep(2);
                 }
