@@ -822,6 +822,26 @@ conduit_status conduit_nstep(conduit_buffer* b, const int64_t* idx, int64_t batc
     return CONDUIT_OK;
 }
 
+// true if [a, a + na) and [b, b + nb) share a byte (NULL ranges share none)
+static bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+    if (!a || !b) return false;
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+// GAE outputs (adv, ret: T*E floats) may overlap neither each other nor any input
+static bool gae_outputs_overlap(const float* rewards, const float* values, const uint8_t* dones,
+                                const uint8_t* truncated, const float* final_values, const float* bootstrap,
+                                int64_t T, int64_t E, const float* adv, const float* ret) {
+    const int64_t nf = T * E * 4, nb = T * E;
+    for (const float* o : {adv, ret}) {
+        if (overlaps(o, nf, rewards, nf) || overlaps(o, nf, values, nf) || overlaps(o, nf, dones, nb) ||
+            overlaps(o, nf, truncated, nb) || overlaps(o, nf, final_values, nf) || overlaps(o, nf, bootstrap, E * 4))
+            return true;
+    }
+    return overlaps(adv, nf, ret, nf);
+}
+
 conduit_status conduit_gae(const float* rewards, const float* values, const uint8_t* dones, const float* bootstrap,
                            int64_t T, int64_t E, double gamma, double lambda, float* adv, float* ret, void* stream) {
     if (T < 0 || E < 0) return fail(CONDUIT_EINVAL, "T and E must be >= 0");
@@ -829,6 +849,8 @@ conduit_status conduit_gae(const float* rewards, const float* values, const uint
     if (T == 0 || E == 0) return CONDUIT_OK;
     if (!rewards || !dones || !adv || !ret) return fail(CONDUIT_EINVAL, "rewards, dones, adv and ret must not be NULL");
     if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
+    if (gae_outputs_overlap(rewards, values, dones, nullptr, nullptr, bootstrap, T, E, adv, ret))
+        return fail(CONDUIT_EINVAL, "adv and ret must overlap neither each other nor the inputs");
     conduit_status st = standalone_flags();
     if (st != CONDUIT_OK) return st;
     GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, nullptr, nullptr, err_words(0)};
@@ -847,6 +869,8 @@ conduit_status conduit_gae_truncated(const float* rewards, const float* values, 
     if (!rewards || !dones || !truncated || !final_values || !adv || !ret)
         return fail(CONDUIT_EINVAL, "rewards, dones, truncated, final_values, adv and ret must not be NULL");
     if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
+    if (gae_outputs_overlap(rewards, values, dones, truncated, final_values, bootstrap, T, E, adv, ret))
+        return fail(CONDUIT_EINVAL, "adv and ret must overlap neither each other nor the inputs");
     conduit_status st = standalone_flags();
     if (st != CONDUIT_OK) return st;
     GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, truncated, final_values,

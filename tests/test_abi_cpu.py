@@ -96,6 +96,17 @@ def test_standalone_calls_validate_on_host():
     assert L.conduit_gae(P, None, P, None, -1, 4, 0.99, 0.95, P, P, None) == cd.EINVAL
     assert L.conduit_gae(P, None, P, None, 4, 4, float("nan"), 0.95, P, P, None) == cd.EINVAL
     assert L.conduit_gae(None, None, None, None, 0, 4, 0.99, 0.95, None, None, None) == cd.OK  # empty
+    # [4, 4] rollouts: 64-byte float arrays, 16-byte flag arrays; outputs that
+    # overlap each other or an input by one element are refused
+    R, D, A, B, F, U = (C.c_void_p(k << 20) for k in range(1, 7))
+    at = lambda p, off: C.c_void_p(p.value + off)  # noqa: E731
+    assert L.conduit_gae(R, None, D, None, 4, 4, 0.99, 0.95, A, at(A, 60), None) == cd.EINVAL
+    assert L.conduit_gae(R, None, D, None, 4, 4, 0.99, 0.95, at(R, 60), B, None) == cd.EINVAL
+    assert L.conduit_gae(R, None, D, None, 4, 4, 0.99, 0.95, A, at(D, 15), None) == cd.EINVAL
+    assert L.conduit_gae(R, A, D, None, 4, 4, 0.99, 0.95, at(A, -60), B, None) == cd.EINVAL
+    assert "overlap" in cd.last_error()
+    assert L.conduit_gae_truncated(R, None, D, U, F, None, 4, 4, 0.99, 0.95, at(F, 48), B, None) == cd.EINVAL
+    assert L.conduit_gae_truncated(R, None, D, U, F, None, 4, 4, 0.99, 0.95, A, at(U, 15), None) == cd.EINVAL
     assert L.conduit_gae_packed(None, None, None, 2, 8, 1.0, 0.95, None, None, None) == cd.EINVAL
     assert L.conduit_gae_packed(None, None, None, 0, 8, 1.0, 0.95, None, None, None) == cd.OK
     xf = cd.transform(cd.XF_NONE)
