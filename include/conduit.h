@@ -373,14 +373,15 @@ conduit_status conduit_nstep(conduit_buffer* buf, const int64_t* idx, int64_t ba
  * dones uint8 [T,E]; bootstrap float [E] or NULL (0); adv, ret float [T,E]
  * outputs, which must not overlap the inputs.  Arithmetic in fp64 inside, fp32
  * out.
- * Rollouts with fewer than 4,096 environments (E a multiple of 4, 16-byte
- * aligned float rows) are split along T across workgroups: segments publish
- * their affine maps in a small per-GPU table (static device memory, no
- * allocation) and each segment composes the later ones.  Calls that overlap in
- * time on one GPU share that table and race (their results are undefined;
- * later calls are unaffected): order such calls with a stream or events.
- * Larger splits (more than 4,096 tiles of 32 environments) run as three
- * launches that keep their intermediate maps in adv and ret instead.
+ * Rollouts of more than 64 steps (E a multiple of 4, 16-byte aligned float
+ * rows) are split along T across workgroups, in tiles of 32 environments: up
+ * to 4,096 tiles publish their segments' affine maps in a small per-GPU table
+ * (static device memory, no allocation) and each composes the later ones.
+ * Calls that overlap in time on one GPU share that table and race (their
+ * results are undefined; later calls are unaffected): order such calls with a
+ * stream or events.  With more tiles, rollouts of fewer than 4,096
+ * environments run three launches that keep their intermediate maps in adv and
+ * ret instead, and wider ones one workgroup per 8 environments.
  * Errors: EINVAL (T, E < 0, E > 2^19, NULL required pointers), ESTATE (also
  * when a split call found a segment that never published: overlapping calls).
  */

@@ -340,8 +340,9 @@ __global__ __launch_bounds__(kQuads * (kSuperV / L)) void k_gae_v4(GaeArgs a) {
 #ifndef CONDUIT_GAE_SPLIT_MIN_TILES
 #define CONDUIT_GAE_SPLIT_MIN_TILES 256
 #endif
-constexpr int64_t kGaeSplitMaxEnvs = CONDUIT_GAE_SPLIT_MAX_ENVS;    // from E / 8 = 512 workgroups on, one pass each
+constexpr int64_t kGaeSplitMaxEnvs = CONDUIT_GAE_SPLIT_MAX_ENVS;    // three-launch split below this many envs
 constexpr int64_t kGaeSplitMinTiles = CONDUIT_GAE_SPLIT_MIN_TILES;  // one tile per compute unit before shorter chunks
+constexpr int64_t kGaeSplitManyTiles = 1024;                         // from here on, chunks of 4 steps
 
 // ---------------------------------------------------------------------------
 // Time-major GAE split along T.  With few environments the kernels above run
@@ -1113,22 +1114,28 @@ hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
     const bool vec = a.E % kV == 0 && al(a.reward, 16) && al(a.value, 16) && al(a.bootstrap, 16) &&
                      al(a.adv, 16) && al(a.ret, 16) && al(a.done, 4) && al(a.truncated, 4) &&
                      al(a.final_value, 16);
-    if (vec && a.E < kGaeSplitMaxEnvs) {
-        // split along T: the largest chunk length that still gives every compute
-        // unit tiles, and at least two segments
+    if (vec) {
+        // split along T: the longest chunk that still gives every compute unit a
+        // tile, at least two segments; chunks of 4 steps where that still gives
+        // 1,024 to 4,096 tiles (a tile of 8-step chunks holds 288 registers per
+        // lane, one workgroup per compute unit, too few in flight for large
+        // rollouts)
         const int64_t groups = (a.E + kSegEnvs - 1) / kSegEnvs;
+        auto segs_of = [&](int L) { return (a.T + (int64_t)kSegChunks * L - 1) / ((int64_t)kSegChunks * L); };
         int L = 0;
         for (int cand : {8, 4, 2}) {
-            const int64_t segs = (a.T + (int64_t)kSegChunks * cand - 1) / ((int64_t)kSegChunks * cand);
-            if (segs >= 2 && (groups * segs >= kGaeSplitMinTiles || cand == 2)) {
+            if (segs_of(cand) >= 2 && (groups * segs_of(cand) >= kGaeSplitMinTiles || cand == 2)) {
                 L = cand;
                 break;
             }
         }
+        if (L == 8 && groups * segs_of(4) >= kGaeSplitManyTiles && groups * segs_of(4) <= kLookMaxTiles) L = 4;
         if (L) {
-            const int64_t segs = (a.T + (int64_t)kSegChunks * L - 1) / ((int64_t)kSegChunks * L);
+            const int64_t segs = segs_of(L);
             if (groups * segs <= kLookMaxTiles) return launch_gae_look(a, (int32_t)groups, (int32_t)segs, L, s);
-            return launch_gae_split(a, groups, L, s);
+            // beyond the table: three launches for narrow rollouts; wide ones keep
+            // one workgroup per 8 environments, which already fills the GPU
+            if (a.E < kGaeSplitMaxEnvs) return launch_gae_split(a, groups, L, s);
         }
     }
     if (vec) {

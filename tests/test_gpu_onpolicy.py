@@ -70,12 +70,13 @@ def test_gae_truncated_shapes(T, E, p_done, p_trunc):
         assert_gae_close(host(ret), orr)
 
 
-# Which kernels a shape takes (E a multiple of 4 with aligned rows): fewer than
-# 4,096 environments and more than 64 steps split the rollout along T into
-# tiles of 32 environments by 32 L steps (L = 8, 4 or 2, the longest that still
-# gives 256 tiles); up to 4,096 tiles run in one launch with a look-back over
-# the later segments ("look"), more in three launches ("split").  Otherwise one
-# workgroup walks all T steps of 8 environments ("one").
+# Which kernels a shape takes (E a multiple of 4 with aligned rows, T > 64): the
+# rollout is split along T into tiles of 32 environments by 32 L steps, L the
+# longest of 8, 4, 2 that still gives 256 tiles (4 when 8 would fit but 4 gives
+# 1,024 to 4,096 tiles); up to 4,096 tiles run in one launch with a look-back
+# over the later segments ("look"); more run in three launches below 4,096
+# environments ("split") and otherwise, like T <= 64, as one workgroup walking
+# all T steps of 8 environments ("one").
 SPLIT_CASES = [
     # (T, E, p_done, expected path, expected chunk length)
     (65, 4, 0.05, "look", 2),         # two segments, the last one a single step
@@ -85,22 +86,37 @@ SPLIT_CASES = [
     (16000, 100, 0.001, "look", 4),   # 125 segments x 4 groups (last one 4 envs)
     (65573, 4, 0.0005, "look", 8),    # 257 segments of 256 steps, ragged end
     (2100, 1000, 0.003, "look", 8),   # 9 segments, 32 groups (last one 8 envs)
-    (1100, 4052, 0.003, "look", 8),   # 5 segments, 127 groups (last one 20 envs)
-    (3000, 4092, 0.01, "look", 8),    # the widest split
+    (1100, 4052, 0.003, "look", 4),   # 9 segments, 127 groups (last one 20 envs)
+    (3000, 4092, 0.01, "look", 4),    # 3,072 tiles
+    (2100, 4096, 0.002, "look", 4),   # 4,096 environments and up split too
+    (4097, 4100, 0.002, "look", 8),   # 2,193 tiles (chunks of 4 would need 4,257)
     (1048576, 4, 0.0001, "look", 8),  # 4,096 tiles: the most one launch takes
     (1100000, 4, 0.0001, "split", 8),  # 4,297 tiles: three launches, 135 carry passes
     (600000, 36, 0.0002, "split", 8),  # 4,688 tiles, a partial group
 ]
 
+
 def _time_major_path(T, E):
     """(path, chunk length) the launcher picks for an aligned [T, E] rollout."""
-    if E % 4 or E >= 4096:
+    if E % 4:
         return "one", 0
     groups = -(-E // 32)
-    for L in (8, 4, 2):
-        segs = -(-T // (32 * L))
-        if segs >= 2 and (groups * segs >= 256 or L == 2):
-            return ("look" if groups * segs <= 4096 else "split"), L
+
+    def segs(L):
+        return -(-T // (32 * L))
+
+    L = 0
+    for c in (8, 4, 2):
+        if segs(c) >= 2 and (groups * segs(c) >= 256 or c == 2):
+            L = c
+            break
+    if L == 8 and 1024 <= groups * segs(4) <= 4096:
+        L = 4
+    if L:
+        if groups * segs(L) <= 4096:
+            return "look", L
+        if E < 4096:
+            return "split", L
     return "one", 0
 
 
@@ -144,10 +160,11 @@ def test_gae_truncated_split_along_t(T, E):
     assert_gae_close(host(ret), orr)
 
 
-@pytest.mark.parametrize("T,E", [(2100, 4096), (4097, 4100)])
+@pytest.mark.parametrize("T,E", [(65, 131072), pytest.param(2049, 65536, marks=pytest.mark.slow)])
 def test_gae_single_pass_kernel_several_passes(T, E):
-    """4,096 environments or more keep one workgroup per 8 environments walking
-    2,048-step passes (a partial last pass here)."""
+    """Wide rollouts beyond the look-back table keep one workgroup per 8
+    environments walking 2,048-step passes (two passes, the last of one step,
+    in the slow case)."""
     print(f"gae single-pass T={T} E={E}", flush=True)
     assert _time_major_path(T, E)[0] == "one"
     rng = np.random.default_rng(T + E)
