@@ -887,18 +887,45 @@ __device__ __forceinline__ int lpad(int t) { return t + (t >> 4); }
 // segments of 4096 elements from the end with a carry.  Values are staged into
 // LDS with coalesced loads, each lane owns a contiguous chunk of 16 for the scan,
 // and advantages/returns are staged back and written coalesced.
+// A double moved by one DPP control; lanes with no source keep `id`.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_f64(double x, double id) {
+    const uint64_t b = (uint64_t)__double_as_longlong(x), o = (uint64_t)__double_as_longlong(id);
+    const uint32_t lo =
+        (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)o, (int)(uint32_t)b, CTRL, ROWS, 0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(o >> 32), (int)(uint32_t)(b >> 32),
+                                                              CTRL, ROWS, 0xf, false);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// One step of a wavefront prefix scan of affine maps whose lanes run backwards
+// in time: the source lane (lower) covers later steps than this one.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void later_scan_step(double& P, double& S) {
+    const double p2 = dpp_f64<CTRL, ROWS>(P, 1.0);
+    const double s2 = dpp_f64<CTRL, ROWS>(S, 0.0);
+    S = S + P * s2;
+    P = P * p2;
+}
+
+constexpr int kDppWaveShr1 = 0x138;  // lane i reads lane i - 1 across the whole wavefront
+
 __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
     __shared__ float sV[kPkPad];
     __shared__ float sA[kPkPad];
     __shared__ float sR[kPkPad];
-    __shared__ double sP[2][kPkThreads];
-    __shared__ double sS[2][kPkThreads];
-    const int c = threadIdx.x;
+    __shared__ double sWP[kPkThreads / kWave];
+    __shared__ double sWS[kPkThreads / kWave];
+    const int tid = threadIdx.x;
+    // chunks run backwards inside a wavefront (lane 0 holds its last chunk), so
+    // the suffix composition over the chunks is a prefix scan over the lanes
+    const int wv = tid / kWave, lane = tid % kWave;
+    const int c = wv * kWave + (kWave - 1 - lane);
     const int64_t b = blockIdx.x;
     const int64_t Lmax = a.Lmax;
     int64_t L = a.length[b];
     if (L < 0 || L > Lmax) {
-        if (c == 0) flag_error(a.err, ERR_SEQ_LENGTH);
+        if (tid == 0) flag_error(a.err, ERR_SEQ_LENGTH);
         L = L < 0 ? 0 : Lmax;
     }
     const float* val = a.value ? a.value + b * Lmax : nullptr;
@@ -923,7 +950,7 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
             f32x4 q[kVecs];
 #pragma unroll
             for (int j = 0; j < kVecs; ++j) {
-                const int t = (j * kPkThreads + c) * 4;
+                const int t = (j * kPkThreads + tid) * 4;
                 if (t + 3 < seg_len) {
                     q[j] = *reinterpret_cast<const f32x4*>(val + base + t);
                 } else {
@@ -933,13 +960,13 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
             }
 #pragma unroll
             for (int j = 0; j < kVecs; ++j) {
-                const int t = (j * kPkThreads + c) * 4;
+                const int t = (j * kPkThreads + tid) * 4;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     if (t + i < seg_len) sV[lpad(t + i)] = q[j][i];
             }
         } else {
-            for (int t = c; t < seg_len; t += kPkThreads) sV[lpad(t)] = val ? val[base + t] : 0.0f;
+            for (int t = tid; t < seg_len; t += kPkThreads) sV[lpad(t)] = val ? val[base + t] : 0.0f;
         }
         __syncthreads();
         // this lane's chunk [t0, t1) of the segment, live part [t0, u1)
@@ -967,25 +994,35 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
                 }
             }
         }
-        // suffix scan over the lanes' chunks, ping-pong buffers: round r reads
-        // what round r - 1 wrote and writes the other buffer, one barrier each
-        int cur = 0;
-        sP[cur][c] = P;
-        sS[cur][c] = S;
-        __syncthreads();
-        for (int off = 1; off < kPkThreads; off <<= 1) {
-            if (c + off < kPkThreads) {
-                const double p2 = sP[cur][c + off];
-                const double s2 = sS[cur][c + off];
-                S = S + P * s2;
-                P = P * p2;
-            }
-            sP[cur ^ 1][c] = P;
-            sS[cur ^ 1][c] = S;
-            cur ^= 1;
-            __syncthreads();
+        // suffix composition over the chunks: a DPP prefix scan inside each
+        // wavefront (shifts by 1, 2, 4, 8 in a row, then the row broadcasts),
+        // the wavefront totals through LDS, one barrier
+        double iP = P, iS = S;  // chunks c .. the wavefront's last
+        later_scan_step<kDppRowShr + 1, 0xf>(iP, iS);
+        later_scan_step<kDppRowShr + 2, 0xf>(iP, iS);
+        later_scan_step<kDppRowShr + 4, 0xf>(iP, iS);
+        later_scan_step<kDppRowShr + 8, 0xf>(iP, iS);
+        later_scan_step<kDppRowBcast15, 0xa>(iP, iS);
+        later_scan_step<kDppRowBcast31, 0xc>(iP, iS);
+        const double eP = dpp_f64<kDppWaveShr1, 0xf>(iP, 1.0);  // chunks c + 1 .. the last
+        const double eS = dpp_f64<kDppWaveShr1, 0xf>(iS, 0.0);
+        if (lane == kWave - 1) {
+            sWP[wv] = iP;
+            sWS[wv] = iS;
         }
-        double A = c + 1 < kPkThreads ? sP[cur][c + 1] * carry + sS[cur][c + 1] : carry;
+        __syncthreads();
+        double lP = 1.0, lS = 0.0;  // the later wavefronts' chunks
+        double tP = 1.0, tS = 0.0;  // the whole segment
+#pragma unroll
+        for (int w = kPkThreads / kWave - 1; w >= 0; --w) {
+            tS = sWS[w] + sWP[w] * tS;
+            tP = sWP[w] * tP;
+            if (w == wv + 1) {
+                lP = tP;
+                lS = tS;
+            }
+        }
+        double A = eP * (lP * carry + lS) + eS;  // A at the end of this chunk
         {
             double v_next = v_end;
 #pragma unroll
@@ -1013,7 +1050,7 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
             constexpr int kVecs = kPkSeg / (4 * kPkThreads);
 #pragma unroll
             for (int j = 0; j < kVecs; ++j) {
-                const int t = (j * kPkThreads + c) * 4;
+                const int t = (j * kPkThreads + tid) * 4;
                 if (t + 3 < seg_len) {
                     f32x4 oa, orr;
 #pragma unroll
@@ -1031,12 +1068,12 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
                 }
             }
         } else {
-            for (int t = c; t < seg_len; t += kPkThreads) {
+            for (int t = tid; t < seg_len; t += kPkThreads) {
                 adv[base + t] = sA[lpad(t)];
                 ret[base + t] = sR[lpad(t)];
             }
         }
-        carry = sP[cur][0] * carry + sS[cur][0];
+        carry = tP * carry + tS;
         v_after = (double)sV[lpad(0)];
         __syncthreads();  // LDS is rewritten by the next segment
     }
