@@ -373,8 +373,9 @@ conduit_status conduit_nstep(conduit_buffer* buf, const int64_t* idx, int64_t ba
  * dones uint8 [T,E]; bootstrap float [E] or NULL (0); adv, ret float [T,E]
  * outputs, which must not overlap the inputs.  Arithmetic in fp64 inside, fp32
  * out.
- * Rollouts of more than 64 steps (E a multiple of 4, 16-byte aligned float
- * rows) are split along T across workgroups, in tiles of 32 environments: up
+ * With E a multiple of 4 and 16-byte aligned float rows, a workgroup takes 32
+ * environments of a rollout of at most 64 steps on its own; longer rollouts
+ * are split along T across workgroups, in tiles of 32 environments: up
  * to 4,096 tiles publish their segments' affine maps in a small per-GPU table
  * (static device memory, no allocation) and each composes the later ones.
  * Calls that overlap in time on one GPU share that table and race (their

@@ -717,6 +717,8 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_replay(GaeArgs a, int32
 //   4. publishes A at its own first step when the rollout is longer than one
 //      window (so that look-backs of earlier tiles stop early), then replays its
 //      chunks from the carry.
+// A rollout of one segment (at most 64 steps) skips steps 2 to 4: each tile
+// folds, scans and replays its 32 environments alone.
 // Maps and flags live in a small per-GPU table (static device memory, no
 // allocation).  A flag holds the call's epoch next to its state, and every
 // call takes a new epoch on the host, so nothing an earlier call left in the
@@ -768,7 +770,7 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, int32_t gro
     Map4 incl, excl;
     tile_suffix(own, c, q, &incl, &excl);  // incl of chunk 0: the segment's map
     const bool last = s == S - 1;
-    if (c == 0) {  // lanes 0..7 of wavefront 0, one per quad
+    if (c == 0 && S > 1) {  // lanes 0..7 of wavefront 0, one per quad; one segment publishes nothing
 #pragma unroll
         for (int j = 0; j < kV; ++j) {
             if (last) {
@@ -1135,7 +1137,7 @@ hipError_t launch_gae_look(const GaeArgs& a, int32_t groups, int32_t S, int L, h
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
     hipError_t e = hipStreamIsCapturing(s, &cap);
     if (e != hipSuccess) return e;
-    if (cap != hipStreamCaptureStatusNone) {  // replays repeat the epoch: clear the flags first
+    if (S > 1 && cap != hipStreamCaptureStatusNone) {  // replays repeat the epoch: clear the flags first
         hipLaunchKernelGGL(k_gae_look_clear, dim3(1), dim3(kSegThreads), 0, s, groups * S);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -1158,6 +1160,9 @@ hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
         // lane, one workgroup per compute unit, too few in flight for large
         // rollouts)
         const int64_t groups = (a.E + kSegEnvs - 1) / kSegEnvs;
+        // a rollout of at most 64 steps is one segment of 2-step chunks: no
+        // table and no waiting, so any number of tiles
+        if (a.T <= (int64_t)kSegChunks * 2) return launch_gae_look(a, (int32_t)groups, 1, 2, s);
         auto segs_of = [&](int L) { return (a.T + (int64_t)kSegChunks * L - 1) / ((int64_t)kSegChunks * L); };
         int L = 0;
         for (int cand : {8, 4, 2}) {

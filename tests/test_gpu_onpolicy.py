@@ -70,15 +70,20 @@ def test_gae_truncated_shapes(T, E, p_done, p_trunc):
         assert_gae_close(host(ret), orr)
 
 
-# Which kernels a shape takes (E a multiple of 4 with aligned rows, T > 64): the
-# rollout is split along T into tiles of 32 environments by 32 L steps, L the
+# Which kernels a shape takes (E a multiple of 4 with aligned rows): a rollout of
+# at most 64 steps is one tile per 32 environments ("short"); a longer one is
+# split along T into tiles of 32 environments by 32 L steps, L the
 # longest of 8, 4, 2 that still gives 256 tiles (4 when 8 would fit but 4 gives
 # 1,024 to 4,096 tiles); up to 4,096 tiles run in one launch with a look-back
 # over the later segments ("look"); more run in three launches below 4,096
-# environments ("split") and otherwise, like T <= 64, as one workgroup walking
-# all T steps of 8 environments ("one").
+# environments ("split") and otherwise as one workgroup walking all T steps of
+# 8 environments ("one").
 SPLIT_CASES = [
     # (T, E, p_done, expected path, expected chunk length)
+    (1, 4, 0.5, "short", 2),          # one step
+    (16, 4100, 0.02, "short", 2),     # 129 groups, the last one 4 envs
+    (64, 65536, 0.01, "short", 2),    # 2,048 tiles, every chunk full
+    (33, 131072, 0.01, "short", 2),   # 4,096 tiles and beyond: no table is used
     (65, 4, 0.05, "look", 2),         # two segments, the last one a single step
     (129, 36, 0.02, "look", 2),       # a partial environment group (36 = 32 + 4)
     (2048, 256, 0.001, "look", 2),    # 32 segments of 64 steps: one look-back window
@@ -101,6 +106,8 @@ def _time_major_path(T, E):
     if E % 4:
         return "one", 0
     groups = -(-E // 32)
+    if T <= 64:
+        return "short", 2
 
     def segs(L):
         return -(-T // (32 * L))
