@@ -410,6 +410,20 @@ conduit_status conduit_gae_truncated(const float* rewards, const float* values, 
                                      void* stream);
 
 /*
+ * The kernels conduit_gae and conduit_gae_truncated take for a rollout of T
+ * steps and E environments whose rows are all 16-byte aligned (aligned != 0)
+ * or not, as chosen by the call itself: *path = 0 one workgroup per 8
+ * environments walks all T steps, one environment per lane; 1 the same with
+ * four environments per lane (E % 4 == 0, aligned); 2 one tile of 32
+ * environments per workgroup (T <= 64); 3 split along T, one launch with a
+ * look-back over the later segments' maps (up to 4,096 tiles); 4 split along
+ * T in three launches.  *chunk = steps per lane of a tile (2, 4 or 8; 0 for
+ * paths 0 and 1).  Host only, nothing is enqueued.  Errors: EINVAL (T, E < 0,
+ * NULL outputs).
+ */
+conduit_status conduit_gae_plan(int64_t T, int64_t E, int32_t aligned, int32_t* path, int32_t* chunk);
+
+/*
  * GAE over B right-padded sequences of up to Lmax elements (LLM post-training
  * shape; the paper's Verl mapping puts advantage computation in ingestion,
  * App. A / Table "Verl map"): sequence b of length L = lengths[b] receives the

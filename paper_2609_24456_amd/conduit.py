@@ -129,6 +129,7 @@ SIGNATURES = {
     "conduit_update_ingest": (ST, [P, P, P, I64, P, P]),
     "conduit_nstep": (ST, [P, P, I64, I32_, F64, P, P, P, P, P, P, P]),
     "conduit_gae_truncated": (ST, [P, P, P, P, P, P, I64, I64, F64, F64, P, P, P]),
+    "conduit_gae_plan": (ST, [I64, I64, I32_, P, P]),
     "conduit_gae_packed": (ST, [P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_minibatch_gather": (ST, [P, I64, I64, P, I64, P, P, P, P, I32_, P]),
     "conduit_buffer_get_info": (ST, [P, P]),
@@ -332,6 +333,17 @@ def conduit_gae(rewards, values, dones, bootstrap, gamma, lam, adv, ret, stream=
                              _ptr(dones, torch.uint8, "dones"), _ptr(bootstrap, torch.float32, "bootstrap"), T, E,
                              float(gamma), float(lam), _ptr(adv, torch.float32, "adv"),
                              _ptr(ret, torch.float32, "ret"), _stream(stream)))
+
+
+GAE_PATHS = ("one", "one_v4", "short", "look", "split")
+
+
+def gae_plan(T, E, aligned=True):
+    """(path, chunk) conduit_gae takes for a [T, E] rollout: path one of
+    GAE_PATHS (conduit_gae_plan's *path), chunk the tile's steps per lane."""
+    path, chunk = C.c_int32(), C.c_int32()
+    _check(lib().conduit_gae_plan(int(T), int(E), 1 if aligned else 0, C.byref(path), C.byref(chunk)))
+    return GAE_PATHS[path.value], chunk.value
 
 
 def conduit_gae_truncated(rewards, values, dones, truncated, final_values, bootstrap, gamma, lam, adv, ret,

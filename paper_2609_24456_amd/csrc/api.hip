@@ -7,6 +7,7 @@
 #include <string>
 
 #include "common.h"
+#include "gae_plan.h"
 
 using namespace conduit;
 
@@ -877,6 +878,15 @@ conduit_status conduit_gae_truncated(const float* rewards, const float* values, 
               err_words(0)};
     hipError_t e = launch_gae(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "gae launch");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_gae_plan(int64_t T, int64_t E, int32_t aligned, int32_t* path, int32_t* chunk) {
+    if (T < 0 || E < 0) return fail(CONDUIT_EINVAL, "T and E must be >= 0");
+    if (!path || !chunk) return fail(CONDUIT_EINVAL, "path and chunk must not be NULL");
+    const GaePlan p = plan_gae(T, E, aligned != 0 && E % 4 == 0);
+    *path = p.path;
+    *chunk = p.chunk;
     return CONDUIT_OK;
 }
 

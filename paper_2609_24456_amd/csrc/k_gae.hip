@@ -21,6 +21,7 @@
 #include <atomic>
 
 #include "common.h"
+#include "gae_plan.h"
 
 namespace conduit {
 
@@ -1146,6 +1147,36 @@ hipError_t launch_gae_look(const GaeArgs& a, int32_t groups, int32_t S, int L, h
                        : launch_gae_look_l<false>(a, groups, S, L, ep, s);
 }
 
+GaePlan plan_gae(int64_t T, int64_t E, bool vec) {
+    GaePlan p{vec ? GAE_ONE_PASS_V4 : GAE_ONE_PASS, 0, 0, 0};
+    if (!vec || T <= 0 || E <= 0) return p;
+    // split along T: the longest chunk that still gives every compute unit a
+    // tile, at least two segments; chunks of 4 steps where that still gives
+    // 1,024 to 4,096 tiles (a tile of 8-step chunks holds 288 registers per
+    // lane, one workgroup per compute unit, too few in flight for large
+    // rollouts)
+    const int64_t groups = (E + kSegEnvs - 1) / kSegEnvs;
+    // a rollout of at most 64 steps is one segment of 2-step chunks: no table
+    // and no waiting, so any number of tiles
+    if (T <= (int64_t)kSegChunks * 2) return GaePlan{GAE_SHORT, 2, groups, 1};
+    auto segs_of = [&](int L) { return (T + (int64_t)kSegChunks * L - 1) / ((int64_t)kSegChunks * L); };
+    int L = 0;
+    for (int cand : {8, 4, 2}) {
+        if (segs_of(cand) >= 2 && (groups * segs_of(cand) >= kGaeSplitMinTiles || cand == 2)) {
+            L = cand;
+            break;
+        }
+    }
+    if (L == 8 && groups * segs_of(4) >= kGaeSplitManyTiles && groups * segs_of(4) <= kLookMaxTiles) L = 4;
+    if (!L) return p;
+    const int64_t segs = segs_of(L);
+    if (groups * segs <= kLookMaxTiles) return GaePlan{GAE_LOOK_BACK, L, groups, segs};
+    // beyond the table: three launches for narrow rollouts; wide ones keep one
+    // workgroup per 8 environments, which already fills the GPU
+    if (E < kGaeSplitMaxEnvs) return GaePlan{GAE_THREE_LAUNCHES, L, groups, segs};
+    return p;
+}
+
 hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
     if (a.T <= 0 || a.E <= 0) return hipSuccess;
     if (a.E > kGaeMaxEnvs) return hipErrorInvalidValue;  // the ABI rejects this first
@@ -1153,49 +1184,30 @@ hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
     const bool vec = a.E % kV == 0 && al(a.reward, 16) && al(a.value, 16) && al(a.bootstrap, 16) &&
                      al(a.adv, 16) && al(a.ret, 16) && al(a.done, 4) && al(a.truncated, 4) &&
                      al(a.final_value, 16);
-    if (vec) {
-        // split along T: the longest chunk that still gives every compute unit a
-        // tile, at least two segments; chunks of 4 steps where that still gives
-        // 1,024 to 4,096 tiles (a tile of 8-step chunks holds 288 registers per
-        // lane, one workgroup per compute unit, too few in flight for large
-        // rollouts)
-        const int64_t groups = (a.E + kSegEnvs - 1) / kSegEnvs;
-        // a rollout of at most 64 steps is one segment of 2-step chunks: no
-        // table and no waiting, so any number of tiles
-        if (a.T <= (int64_t)kSegChunks * 2) return launch_gae_look(a, (int32_t)groups, 1, 2, s);
-        auto segs_of = [&](int L) { return (a.T + (int64_t)kSegChunks * L - 1) / ((int64_t)kSegChunks * L); };
-        int L = 0;
-        for (int cand : {8, 4, 2}) {
-            if (segs_of(cand) >= 2 && (groups * segs_of(cand) >= kGaeSplitMinTiles || cand == 2)) {
-                L = cand;
-                break;
-            }
+    const GaePlan p = plan_gae(a.T, a.E, vec);
+    switch (p.path) {
+        case GAE_SHORT:
+        case GAE_LOOK_BACK: return launch_gae_look(a, (int32_t)p.groups, (int32_t)p.segments, p.chunk, s);
+        case GAE_THREE_LAUNCHES: return launch_gae_split(a, p.groups, p.chunk, s);
+        case GAE_ONE_PASS_V4: {
+            const int64_t vblocks = (a.E + kEnvsV - 1) / kEnvsV;
+            constexpr int L = kGaeVecChunk;
+            const dim3 block(kQuads * (kSuperV / L));
+            if (a.truncated)
+                hipLaunchKernelGGL((k_gae_v4<true, L>), dim3((unsigned)vblocks), block, 0, s, a);
+            else
+                hipLaunchKernelGGL((k_gae_v4<false, L>), dim3((unsigned)vblocks), block, 0, s, a);
+            return hipGetLastError();
         }
-        if (L == 8 && groups * segs_of(4) >= kGaeSplitManyTiles && groups * segs_of(4) <= kLookMaxTiles) L = 4;
-        if (L) {
-            const int64_t segs = segs_of(L);
-            if (groups * segs <= kLookMaxTiles) return launch_gae_look(a, (int32_t)groups, (int32_t)segs, L, s);
-            // beyond the table: three launches for narrow rollouts; wide ones keep
-            // one workgroup per 8 environments, which already fills the GPU
-            if (a.E < kGaeSplitMaxEnvs) return launch_gae_split(a, groups, L, s);
+        default: {
+            const int64_t blocks = (a.E + kEnvs - 1) / kEnvs;
+            if (a.truncated)
+                hipLaunchKernelGGL(k_gae<true>, dim3((unsigned)blocks), dim3(kTmThreads), 0, s, a);
+            else
+                hipLaunchKernelGGL(k_gae<false>, dim3((unsigned)blocks), dim3(kTmThreads), 0, s, a);
+            return hipGetLastError();
         }
     }
-    if (vec) {
-        const int64_t vblocks = (a.E + kEnvsV - 1) / kEnvsV;
-        constexpr int L = kGaeVecChunk;
-        const dim3 block(kQuads * (kSuperV / L));
-        if (a.truncated)
-            hipLaunchKernelGGL((k_gae_v4<true, L>), dim3((unsigned)vblocks), block, 0, s, a);
-        else
-            hipLaunchKernelGGL((k_gae_v4<false, L>), dim3((unsigned)vblocks), block, 0, s, a);
-        return hipGetLastError();
-    }
-    const int64_t blocks = (a.E + kEnvs - 1) / kEnvs;
-    if (a.truncated)
-        hipLaunchKernelGGL(k_gae<true>, dim3((unsigned)blocks), dim3(kTmThreads), 0, s, a);
-    else
-        hipLaunchKernelGGL(k_gae<false>, dim3((unsigned)blocks), dim3(kTmThreads), 0, s, a);
-    return hipGetLastError();
 }
 
 hipError_t launch_gae_packed(const GaePackedArgs& a, hipStream_t s) {

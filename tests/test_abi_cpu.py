@@ -145,3 +145,38 @@ def test_struct_layouts_match_header(tmp_path):
         assert int(got[cname]) == C.sizeof(py), cname
         for field, _ in py._fields_:
             assert int(got[f"{cname}.{field}"]) == getattr(py, field).offset, (cname, field)
+
+
+# (T, E, aligned) -> (path, chunk) that conduit_gae_plan reports (the GPU tests
+# run these shapes and assert the same plan)
+GAE_PLANS = [
+    ((2048, 256, True), ("look", 2)),       # the PPO rollout: 8 groups x 32 segments
+    ((2048, 1024, True), ("look", 8)),      # 256 tiles of 8-step chunks
+    ((2048, 4096, True), ("look", 4)),      # 8-step chunks would give 1,152 tiles
+    ((4097, 4100, True), ("look", 8)),      # 4-step chunks would need 4,257 tiles
+    ((40000, 4, True), ("look", 4)),
+    ((65, 4, True), ("look", 2)),           # two segments
+    ((64, 4, True), ("short", 2)),          # one segment
+    ((1, 4, True), ("short", 2)),
+    ((33, 131072, True), ("short", 2)),     # any number of tiles
+    ((1048576, 4, True), ("look", 8)),      # 4,096 tiles: the table's size
+    ((1100000, 4, True), ("split", 8)),     # 4,297 tiles, fewer than 4,096 envs
+    ((65, 131072, True), ("one_v4", 0)),    # 8,192 tiles, 4,096 envs or more
+    ((2049, 65536, True), ("one_v4", 0)),
+    ((2048, 256, False), ("one", 0)),       # rows off a 16-byte boundary
+    ((2048, 255, True), ("one", 0)),        # E not a multiple of 4
+    ((0, 4, True), ("one_v4", 0)),          # empty rollouts enqueue nothing
+]
+
+
+@pytest.mark.parametrize("shape,plan", GAE_PLANS)
+def test_gae_plan_on_the_host(shape, plan):
+    T, E, aligned = shape
+    assert cd.gae_plan(T, E, aligned) == plan
+
+
+def test_gae_plan_validates():
+    L = cd.lib()
+    x = C.c_int32()
+    assert L.conduit_gae_plan(-1, 4, 1, C.byref(x), C.byref(x)) == cd.EINVAL
+    assert L.conduit_gae_plan(4, 4, 1, None, C.byref(x)) == cd.EINVAL

@@ -77,7 +77,9 @@ def test_gae_truncated_shapes(T, E, p_done, p_trunc):
 # 1,024 to 4,096 tiles); up to 4,096 tiles run in one launch with a look-back
 # over the later segments ("look"); more run in three launches below 4,096
 # environments ("split") and otherwise as one workgroup walking all T steps of
-# 8 environments ("one").
+# 8 environments ("one_v4"; "one" for E not a multiple of 4 or unaligned rows).
+# conduit_gae_plan reports the choice; tests/test_abi_cpu.py checks it on the
+# host.
 SPLIT_CASES = [
     # (T, E, p_done, expected path, expected chunk length)
     (1, 4, 0.5, "short", 2),          # one step
@@ -102,29 +104,8 @@ SPLIT_CASES = [
 
 
 def _time_major_path(T, E):
-    """(path, chunk length) the launcher picks for an aligned [T, E] rollout."""
-    if E % 4:
-        return "one", 0
-    groups = -(-E // 32)
-    if T <= 64:
-        return "short", 2
-
-    def segs(L):
-        return -(-T // (32 * L))
-
-    L = 0
-    for c in (8, 4, 2):
-        if segs(c) >= 2 and (groups * segs(c) >= 256 or c == 2):
-            L = c
-            break
-    if L == 8 and 1024 <= groups * segs(4) <= 4096:
-        L = 4
-    if L:
-        if groups * segs(L) <= 4096:
-            return "look", L
-        if E < 4096:
-            return "split", L
-    return "one", 0
+    """(path, chunk length) the library picks for an aligned [T, E] rollout."""
+    return cd.gae_plan(T, E, aligned=True)
 
 
 @pytest.mark.parametrize("T,E,p_done,path,L", SPLIT_CASES)
@@ -173,7 +154,7 @@ def test_gae_single_pass_kernel_several_passes(T, E):
     environments walking 2,048-step passes (two passes, the last of one step,
     in the slow case)."""
     print(f"gae single-pass T={T} E={E}", flush=True)
-    assert _time_major_path(T, E)[0] == "one"
+    assert _time_major_path(T, E)[0] == "one_v4"
     rng = np.random.default_rng(T + E)
     r = rng.standard_normal((T, E)).astype(np.float32)
     v = rng.standard_normal((T, E)).astype(np.float32)
