@@ -3,21 +3,25 @@
 //
 // The recursion A_t = delta_t + a_t A_{t+1}, a_t = gamma*lambda*(1 - d_t), is
 // affine in A_{t+1}, so a chunk of consecutive steps composes into one map
-// A_start = P * A_end + S.  Each kernel runs three phases inside one workgroup:
-//   1. every lane folds its chunk of steps into (P, S) (reverse order);
-//   2. a Hillis-Steele suffix scan over the chunks in LDS composes the maps, so
-//      chunk c learns A at its end, A_{t1(c)} = A_start(c + 1);
-//   3. every lane replays its chunk from that carry and writes A_t and
-//      R_t = A_t + V_t.
-// All arithmetic is fp64; outputs are rounded to fp32 once.
-//
-// Time-major rollouts [T, E]: a workgroup owns 8 environments and walks the
-// rollout in passes of 2048 steps.  k_gae_v4 (E a multiple of 4, aligned rows)
-// gives each lane 4 environments as 16-byte vectors and 16 steps, 128 chunks
-// per pass; k_gae (any E) gives each lane one environment and 32 steps, 64
-// chunks per pass, lanes fastest over environments so every load instruction of
-// a wavefront reads eight 32-byte runs.  Padded sequences
-// [B, Lmax] (k_gae_packed): one workgroup per sequence, 256 chunks along t.
+// A_start = P * A_end + S, and so does any run of chunks.  Every kernel
+//   1. folds each lane's chunk of steps into (P, S) (reverse order);
+//   2. composes the chunks' maps with a suffix scan, so chunk c learns A at its
+//      end, A_{t1(c)} = A_start(c + 1);
+//   3. replays each chunk from that carry and writes A_t and R_t = A_t + V_t.
+// All arithmetic is fp64; outputs are rounded to fp32 once.  plan_gae picks
+// the kernels of a time-major call:
+//   * tiles of 32 environments x 32 chunks (E a multiple of 4, aligned rows):
+//     a rollout of at most 64 steps is one tile per workgroup
+//     (k_gae_look with one segment); a longer one is split along T into
+//     segments whose maps are joined by a decoupled look-back in one launch
+//     (k_gae_look), or, beyond its table, by three launches (k_gae_seg_*);
+//   * otherwise a workgroup owns 8 environments and walks the rollout in
+//     passes of 2048 steps: k_gae_v4 gives each lane 4 environments as 16-byte
+//     vectors and 16 steps (128 chunks per pass); k_gae (any E, any alignment)
+//     one environment and 32 steps (64 chunks per pass), lanes fastest over
+//     environments so every load instruction reads eight 32-byte runs.
+// Padded sequences [B, Lmax] (k_gae_packed): one workgroup per sequence, 256
+// chunks along t, scanned with DPP inside each wavefront.
 #include <atomic>
 
 #include "common.h"
