@@ -444,7 +444,8 @@ def bench_ppo(reps=3):
         "rollout_ingest": {"bytes": ing_bytes, "ms": ing_ms, "GBps": ing_bytes / ing_ms / 1e6,
                            "frac": ing_bytes / ing_ms / 1e6 / PEAK_HBM_GBPS},
         "gae_2048x256": {"bytes": gae_bytes, "us": gae_ms * 1e3, "GBps": gae_bytes / gae_ms / 1e6,
-                         "frac": gae_bytes / gae_ms / 1e6 / PEAK_HBM_GBPS},
+                         "frac": gae_bytes / gae_ms / 1e6 / PEAK_HBM_GBPS,
+                         "kernels": "%s, %d-step chunks (conduit_gae_plan)" % cd.gae_plan(T, E)},
         "minibatch_gather_16384": {"bytes": mb_bytes, "us": mb_ms * 1e3, "GBps": mb_bytes / mb_ms / 1e6,
                                    "frac": mb_bytes / mb_ms / 1e6 / PEAK_HBM_GBPS},
         "epoch_32_minibatches_ms": mb_ms * 32,
