@@ -91,12 +91,14 @@ def test_captured_sample_gather_and_update_replays():
     buf.close()
 
 
-def test_captured_gae_replays():
-    """Time-major GAE on the one-launch split path (table clear + look-back
-    kernel) captured once and replayed with new rollouts, with eager GAE calls
-    of other shapes between the replays."""
-    print("graph: capture gae [2048, 256], 4 replays", flush=True)
-    T, E = 2048, 256
+@pytest.mark.parametrize("T,E,path", [(2048, 256, "look"), (40, 4096, "short"), (1100000, 4, "split")])
+def test_captured_gae_replays(T, E, path):
+    """Time-major GAE captured once and replayed with new rollouts, with eager
+    GAE calls of other shapes between the replays: the one-launch split (its
+    capture records the table clear before the look-back kernel), the short
+    tile path and the three-launch split."""
+    print(f"graph: capture gae [{T}, {E}] ({path}), 4 replays", flush=True)
+    assert cd.gae_plan(T, E)[0] == path
     rng = np.random.default_rng(5)
     r_s = torch.empty((T, E), dtype=torch.float32, device="cuda")
     v_s = torch.empty((T, E), dtype=torch.float32, device="cuda")
