@@ -11,14 +11,17 @@ through separate conduit_sample / conduit_gather_transform calls are reported
 beside it.  Inputs (frames of the steps, uniforms, new priorities) are resident
 in HBM before the timed region.
 
-Prints ONE JSON line.  Besides the headline it carries the roofline of the
-dominant kernel, the oracle timed on the host cores (cpu_baseline), per-kernel
-times of the step, and the other workloads' rows (DQN ingest and n-step
+Prints ONE JSON line on stdout, the last line and compact: the headline, the
+roofline of the dominant kernel, the oracle timed on the host cores
+(cpu_baseline: one pinned core, median of 5 reps, and every allowed core with
+one instance each; timed in forked children before this process touches the
+GPU) and a few figures of each other workload's row (DQN ingest and n-step
 targets, PPO rollout ingest + GAE + minibatch gather, large-payload bf16
 gather, token packing + packed GAE, tiny replay latency, the synthetic stress
 transitions, the scheduling model against measured schedules, placement).
-The rows are timed GPU-paced (a stand-in kernel queued ahead of the first
-event), so each brackets GPU time only.
+Each row's full record goes to stderr as a line 'bench.detail {...}' (and to
+--detail-out).  The rows are timed GPU-paced (a stand-in kernel queued ahead
+of the first event), so each brackets GPU time only.
 """
 import argparse
 import ctypes as C
@@ -46,7 +49,8 @@ def parse():
     p.add_argument("--calibrate-copy", action="store_true", help="run a plain 1 GiB device copy (counter scale)")
     p.add_argument("--sources-sha", action="store_true",
                    help="print the hash of the fused kernel's sources (for the counter summary)")
-    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--cpu-rep-seconds", type=float, default=2.0, help="seconds per timed rep of the oracle")
+    p.add_argument("--detail-out", default="", help="also append the per-row JSON records to this file")
     return p.parse_args()
 
 
@@ -1117,19 +1121,32 @@ def bench_tiny(iters=100):
 
 
 # ----------------------------------------------------------------------------
-# CPU baseline: the oracle on the host cores
+# CPU baseline: the oracle on the host cores, timed before the GPU is touched
 # ----------------------------------------------------------------------------
-def cpu_baseline(seconds):
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_dqn_state(n_iter_max):
+    """The oracle's DQN replay at the headline's capacity: every observation
+    page resident (real DRAM traffic), metadata and priorities prefilled with
+    1.05M transitions, and the inputs of n_iter_max steps generated up front."""
     import numpy as np
     import oracle
     import synth
     Cap, B, K, prefill = 1_000_000, 512, 4, 1_050_000
-    n_iter_max = 400
     cfg = synth.DQN(prefill + n_iter_max * B)
     row = 84 * 84
     store = np.empty((Cap, row), np.uint8)
     tile = cfg.frames(0, 4096).reshape(4096, row).numpy()
-    for a in range(0, Cap, 4096):  # every page resident (real DRAM traffic)
+    for a in range(0, Cap, 4096):
         b = min(Cap, a + 4096)
         store[a:b] = tile[:b - a]
     orc = oracle.Replay(Cap, (84, 84), np.uint8, act_bytes=4, frame_stack=K, obs_storage=store)
@@ -1139,25 +1156,118 @@ def cpu_baseline(seconds):
                    episode=cfg.episode[a:b], step=cfg.step[a:b], prio=cfg.prio[a:b])
     u, prio = cfg.draws(n_iter_max, B)
     frames = cfg.frames(prefill, 8 * B).reshape(8 * B, row).numpy()
-    done_iters = 0
+    cols = {k: np.ascontiguousarray(getattr(cfg, k)[prefill:prefill + n_iter_max * B])
+            for k in ("action", "reward", "done", "episode", "step")}
+    return orc, frames, cols, u, prio
+
+
+def _oracle_steps(state, first, n):
+    """Seconds for n oracle DQN steps (ingest 512, sample 512 with IS weights,
+    gather 512 -> [512,4,84,84] fp32, update 512) starting at step `first`."""
+    import oracle
+    orc, frames, cols, u, prio = state
+    B = 512
     t0 = time.perf_counter()
-    while done_iters < n_iter_max:
-        i = done_iters
-        a = prefill + i * B
-        orc.ingest(B, obs=frames[(i % 8) * B:(i % 8 + 1) * B], action=cfg.action[a:a + B],
-                   reward=cfg.reward[a:a + B], done=cfg.done[a:a + B], episode=cfg.episode[a:a + B],
-                   step=cfg.step[a:a + B])
-        idx, w = orc.sample(u[i])
+    for i in range(first, first + n):
+        a = i * B
+        orc.ingest(B, obs=frames[(i % 8) * B:(i % 8 + 1) * B], action=cols["action"][a:a + B],
+                   reward=cols["reward"][a:a + B], done=cols["done"][a:a + B], episode=cols["episode"][a:a + B],
+                   step=cols["step"][a:a + B])
+        idx, _w = orc.sample(u[i])
         orc.gather(idx, oracle.XF_U8_F32)
         orc.update(idx, prio[i])
-        done_iters += 1
-        if time.perf_counter() - t0 > seconds and done_iters >= 3:
-            break
-    el = time.perf_counter() - t0
-    return {"value": done_iters * B / el, "unit": "sampled transitions/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done_iters} DQN steps (ingest 512 + sample 512 + gather 512 -> fp32 + update 512) on the "
-                      f"1M-slot replay (metadata prefilled with 1.05M transitions), single-threaded C oracle, "
-                      f"{el:.1f} s", "seconds": el}
+    return time.perf_counter() - t0
+
+
+def _in_child(core, fn):
+    """Run fn() in a forked child pinned to `core`; returns its result (a
+    JSON-serialisable value).  The parent has not touched the GPU."""
+    r, w = os.pipe()
+    pid = os.fork()
+    if pid == 0:  # child: pinned, runs the oracle only, reports, exits
+        os.close(r)
+        code = 0
+        try:
+            os.sched_setaffinity(0, {core})
+            msg = json.dumps({"ok": fn()})
+        except BaseException as e:  # noqa: BLE001 - reported to the parent
+            msg = json.dumps({"error": repr(e)})
+            code = 1
+        with os.fdopen(w, "w") as f:
+            f.write(msg)
+        os._exit(code)
+    os.close(w)
+    return pid, r
+
+
+def _collect(pid, r):
+    with os.fdopen(r) as f:
+        msg = f.read()
+    os.waitpid(pid, 0)
+    rec = json.loads(msg) if msg else {"error": "no result"}
+    if "error" in rec:
+        raise RuntimeError(f"oracle worker failed: {rec['error']}")
+    return rec["ok"]
+
+
+def cpu_baseline(rep_seconds=2.0, reps=5, all_core_seconds=3.0, max_workers=16):
+    """The oracle (single-threaded C, never tuned for speed) on the DQN step at
+    the headline's capacity, timed in forked children before this process
+    touches the GPU: one child pinned to one core runs a few warm-up steps and
+    then `reps` reps of ~rep_seconds (the median is reported); then one independent
+    oracle instance per core (up to max_workers cores, each pinned) runs
+    concurrently for ~all_core_seconds, and the aggregate rate is reported
+    beside it.  Data generation is outside every timed region."""
+    import statistics
+    B = 512
+    cores = sorted(os.sched_getaffinity(0))
+    probe_steps = 3  # the warm-up, which also sizes the reps
+    n_iter_max = 1200
+    t_setup = time.perf_counter()
+    state = _oracle_dqn_state(n_iter_max)
+    setup_s = time.perf_counter() - t_setup
+
+    def single():
+        warm = _oracle_steps(state, 0, probe_steps)
+        n = max(3, int(rep_seconds / (warm / probe_steps)))
+        n = min(n, (n_iter_max - probe_steps) // reps)
+        times = []
+        first = probe_steps
+        for _ in range(reps):
+            times.append(_oracle_steps(state, first, n))
+            first += n
+        return {"steps_per_rep": n, "rep_s": times}
+
+    pid, r = _in_child(cores[0], single)
+    one = _collect(pid, r)
+    med = statistics.median(one["rep_s"])
+    per_step_s = med / one["steps_per_rep"]
+    value = B / per_step_s
+    # all cores: independent instances (copy-on-write copies of one state)
+    workers = cores[:max_workers]
+    n_all = max(2, min(int(all_core_seconds / per_step_s), n_iter_max - 1))
+
+    def many():
+        return _oracle_steps(state, 1, n_all)
+
+    kids = [_in_child(c, many) for c in workers]
+    t_all = [_collect(p, fd) for p, fd in kids]
+    value_all = len(workers) * n_all * B / max(t_all)
+    del state
+    import gc
+    gc.collect()
+    return {
+        "value": value, "unit": "sampled transitions/s", "cores": 1, "kind": "oracle",
+        "sample": f"median of {reps} reps x {one['steps_per_rep']} DQN steps (ingest 512 + sample 512 + gather "
+                  f"512 -> [512,4,84,84] fp32 + update 512) on the 1M-slot replay (1.05M prefill), after a "
+                  f"{probe_steps}-step warm-up; single-threaded C oracle pinned to core {cores[0]}",
+        "rep_s": one["rep_s"], "steps_per_rep": one["steps_per_rep"],
+        "all_cores": {"value": value_all, "cores": len(workers), "steps_per_worker": n_all,
+                      "worker_s_max": max(t_all),
+                      "how": "one independent oracle instance per core, each pinned, run concurrently"},
+        "nproc": os.cpu_count(), "cores_allowed": len(cores), "cpu_model": _cpu_model(),
+        "setup_s": setup_s,
+    }
 
 
 def calibrate_copy():
@@ -1207,14 +1317,63 @@ ROWS = {"tiny": lambda: bench_tiny(), "ppo": lambda: bench_ppo(), "large": lambd
         "schedule_onpolicy": lambda: bench_schedule_onpolicy(), "placement": lambda: bench_placement()}
 
 
+def _row_summary(name, r):
+    """A few figures of an extra row for the headline line (its full record
+    goes to stderr and, with --detail-out, to a file)."""
+    try:
+        if name == "tiny":
+            return {"us_per_iteration": r["us_per_iteration"], "sampled_per_s": r["sampled_per_s"]}
+        if name == "ppo":
+            return {"rollout_ingest_frac": r["rollout_ingest"]["frac"], "gae_us": r["gae_2048x256"]["us"],
+                    "minibatch_us": r["minibatch_gather_16384"]["us"],
+                    "minibatch_frac": r["minibatch_gather_16384"]["frac"]}
+        if name == "large":
+            return {"gather_bf16_us": r["gather_bf16_1024"]["us"], "gather_bf16_frac": r["gather_bf16_1024"]["frac"],
+                    "iteration_us": r["iteration_us"]}
+        if name == "tokens":
+            return {"pack_us": r["pack_256x4096"]["us"], "gae_packed_us": r["gae_packed_256x4096"]["us"],
+                    "iteration_us": r["iteration_us"]}
+        if name == "stress":
+            return {k: round(v["iteration_us"], 2) for k, v in r.items()}
+        if name in ("schedule", "schedule_onpolicy"):
+            return {"model_us": r["model_choice"]["measured_us"], "best_us": r["measured_best"]["measured_us"],
+                    "sequential_us": r["sequential"]["measured_us"], "spearman": r["spearman_pred_vs_measured"]}
+        if name == "placement":
+            t = r["dqn_step_by_tier"]
+            return {"hbm_step_us": t["hbm"]["step_us"], "pinned_step_us": t["host_pinned"]["step_us"],
+                    "ranking_holds": t["model_ranking_holds"]}
+    except (KeyError, TypeError):
+        pass
+    return None
+
+
+def _emit_detail(rec, path):
+    """Per-row detail: one JSON line on stderr, and appended to `path`."""
+    line = json.dumps(rec)
+    print("bench.detail " + line, file=sys.stderr, flush=True)
+    if path:
+        with open(path, "a") as f:
+            f.write(line + "\n")
+
+
 def main():
     args = parse()
     if args.sources_sha:
         print(kernel_sources_sha())
         return
     if args.gpus != 1:
-        print(f"bench.py: the experience path runs on one GPU; --gpus {args.gpus} is not supported", flush=True)
+        print(f"bench.py: the experience path runs on one GPU; --gpus {args.gpus} is not supported "
+              "(one process, one GPU; no collectives)", flush=True)
         sys.exit(2)
+    if args.detail_out:
+        os.makedirs(os.path.dirname(os.path.abspath(args.detail_out)), exist_ok=True)
+        open(args.detail_out, "w").close()
+    # the oracle first, in forked children, before anything touches the GPU
+    cb = None
+    if not args.no_cpu_baseline:
+        print("bench.py: CPU baseline (oracle, before GPU initialisation) ...", file=sys.stderr, flush=True)
+        cb = cpu_baseline(rep_seconds=args.cpu_rep_seconds)
+        _emit_detail({"cpu_baseline": cb}, args.detail_out)
     import torch
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
     from paper_2609_24456_amd import conduit as cd
@@ -1230,6 +1389,7 @@ def main():
     g_gbps = d["gather_bytes"] / g_ms / 1e6
     f_ms = d["fused_b2b_ms"]
     achieved = d["fused_bytes"] / f_ms / 1e6
+    _emit_detail({"dqn": d}, args.detail_out)
     out = {
         "metric": METRIC,
         "value": value,
@@ -1243,44 +1403,42 @@ def main():
         "vs_baseline": None,
         "dtype": "u8->f32",
         "data": "synthetic",
-        "config": {"workload": "dqn-1M-replay: capacity 1,000,000 single 84x84 u8 frames, frame stack 4, "
-                               "batch 512, PER alpha 0.6 beta 0.4; step = ingest 512 + sample 512 + "
-                               "gather 512 -> [512,4,84,84] fp32 + priority update 512",
+        "config": {"workload": "dqn-1M-replay: 1,000,000 slots of 84x84 u8, stack 4, batch 512, PER a=0.6 b=0.4; "
+                               "step = ingest 512 + sample 512 + gather -> [512,4,84,84] f32 + update 512",
                    "capacity": 1_000_000, "batch": 512, "frame_stack": 4},
-        "step_calls": "conduit_update_ingest (the previous step's priority update, then this step's ingest) "
-                      "+ conduit_sample_gather",
-        "ms_per_step_separate_update": d["separate_ms"] / args.steps,
-        "ms_per_step_unfused": d["unfused_ms"] / args.steps,
-        "update_ingest_call_us": d["update_ingest_call"]["mean_us"],
-        "roofline": {"bound": "hbm", "kernel": "k_sample_gather<U8_F32> (one launch: 512 tree descents, "
-                                               "IS weights, frame-stack gather 512 x 4 frames -> fp32; the "
-                                               "dominant kernel of the step)",
+        "roofline": {"bound": "hbm", "kernel": "k_sample_gather<U8_F32> (descent + IS weights + gather, one launch)",
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": _traffic_from_profile(),
-                     "algorithmic_bytes_per_launch": d["fused_bytes"], "avg_launch_us": f_ms * 1e3,
-                     "timing": "HIP events around back-to-back launches over the timed steps' uniforms"},
+                     "algorithmic_bytes": d["fused_bytes"], "avg_launch_us": f_ms * 1e3,
+                     "timing": "HIP events, back-to-back launches over the timed steps' uniforms"},
         "gather_GBps": g_gbps,
         "gather_frac_of_peak": g_gbps / PEAK_HBM_GBPS,
-        "gather_kernel": "k_gather_pipe<U8_F32>: conduit_gather_transform alone over the timed steps' "
-                         "batches, back to back",
         "gather_avg_launch_us": g_ms * 1e3,
-        "kernels_us_in_step": {k: v["mean_us"] for k, v in d["kernels"].items()},
-        "host_enqueue_us_per_step": d["host_enqueue_s"] * 1e6 / args.steps,
-        "rows": {"dqn_ingest_32768": d["ingest_big"], "dqn_nstep3": d["nstep3"]},
+        "ms_per_step_separate_update": d["separate_ms"] / args.steps,
+        "ms_per_step_unfused": d["unfused_ms"] / args.steps,
+        "kernels_us_in_step": {k.split(" ")[0]: round(v["mean_us"], 3) for k, v in d["kernels"].items()},
+        "rows": {"dqn_ingest_32768_frac": d["ingest_big"]["GBps"] / PEAK_HBM_GBPS,
+                 "dqn_nstep3_us": d["nstep3"]["us"]},
     }
     if not args.no_rows:
         only = set(x for x in args.only.split(",") if x) or set(ROWS)
         for name in ("tiny", "ppo", "large", "tokens", "stress", "schedule", "schedule_onpolicy", "placement"):
             if name in only:
                 print(f"bench.py: row {name} ...", file=sys.stderr, flush=True)
-                out["rows"][name] = ROWS[name]()
+                r = ROWS[name]()
+                _emit_detail({"row": name, "result": r}, args.detail_out)
+                out["rows"][name] = _row_summary(name, r)
                 torch.cuda.empty_cache()
-    if not args.no_cpu_baseline:
-        print("bench.py: CPU baseline (oracle) ...", file=sys.stderr, flush=True)
-        cb = cpu_baseline(args.cpu_seconds)
-        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+    if cb is not None:
+        out["cpu_baseline"] = {"value": cb["value"], "unit": cb["unit"], "cores": cb["cores"], "kind": cb["kind"],
+                               "sample": cb["sample"], "nproc": cb["nproc"], "cpu_model": cb["cpu_model"],
+                               "all_cores": {k: cb["all_cores"][k] for k in ("value", "cores")}}
         out["gpu_over_cpu"] = value / cb["value"]
-    print(json.dumps(out), flush=True)
+        out["gpu_over_cpu_all_cores"] = value / cb["all_cores"]["value"]
+    out["detail"] = "per-row records: stderr lines 'bench.detail {...}'" + (
+        f" and {args.detail_out}" if args.detail_out else "")
+    # the headline: the last stdout line, compact
+    print(json.dumps(out, separators=(",", ":")), flush=True)
 
 
 if __name__ == "__main__":

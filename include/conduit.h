@@ -476,6 +476,19 @@ typedef struct {
 /* Host-side state of the buffer; no device synchronisation. */
 conduit_status conduit_buffer_get_info(const conduit_buffer* buf, conduit_buffer_info* info);
 
+/*
+ * Ring state of the buffer (Sec. 2.2 off-policy ingestion keeps the indices
+ * and metadata of the stored transitions): *size stored transitions, *head the
+ * next slot to write, *total transitions ever ingested (each output may be
+ * NULL).  Synchronous: waits for all work enqueued on the buffer's device
+ * (hipDeviceSynchronize), so the device-side columns and tree then hold exactly
+ * these transitions.  The outputs are written in every case; the return is
+ * ESTATE (with the description in conduit_last_error) if a kernel flagged
+ * bad device-side input since the flag was last cleared.
+ * Errors: EINVAL (NULL buffer), EDEVICE, ESTATE.
+ */
+conduit_status conduit_buffer_stats(conduit_buffer* buf, int64_t* size, int64_t* head, uint64_t* total);
+
 typedef enum {
     CONDUIT_COL_OBS = 0,      /* [capacity, row_bytes] bytes */
     CONDUIT_COL_ACTION = 1,   /* [capacity, action_bytes] */

@@ -133,6 +133,7 @@ SIGNATURES = {
     "conduit_gae_packed": (ST, [P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_minibatch_gather": (ST, [P, I64, I64, P, I64, P, P, P, P, I32_, P]),
     "conduit_buffer_get_info": (ST, [P, P]),
+    "conduit_buffer_stats": (ST, [P, P, P, P]),
     "conduit_buffer_read": (ST, [P, I32_, I32_, I64, I64, P, P]),
     "conduit_sync_check": (ST, [P, P]),
     "conduit_clear_error": (None, [P]),
@@ -462,6 +463,13 @@ def conduit_buffer_get_info(handle):
     return info
 
 
+def conduit_buffer_stats(handle):
+    """(size, head, total) after waiting for the buffer's device."""
+    size, head, total = C.c_int64(), C.c_int64(), C.c_uint64()
+    _check(lib().conduit_buffer_stats(handle, C.byref(size), C.byref(head), C.byref(total)))
+    return size.value, head.value, total.value
+
+
 def conduit_buffer_read(handle, col, dst, offset=0, level=0, stream=None):
     _check(lib().conduit_buffer_read(handle, col, level, int(offset), dst.numel() * dst.element_size(),
                                      _ptr(dst, None, "dst"), _stream(stream)))
@@ -508,6 +516,9 @@ class ReplayBuffer:
 
     def info(self):
         return conduit_buffer_get_info(self.handle)
+
+    def stats(self):
+        return conduit_buffer_stats(self.handle)
 
     def ingest(self, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None, offsets=None,
                aux=None, n=None, stream=None):

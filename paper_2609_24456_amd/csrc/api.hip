@@ -446,6 +446,19 @@ conduit_status conduit_buffer_get_info(const conduit_buffer* b, conduit_buffer_i
     return CONDUIT_OK;
 }
 
+conduit_status conduit_buffer_stats(conduit_buffer* b, int64_t* size, int64_t* head, uint64_t* total) {
+    if (!b) return fail(CONDUIT_EINVAL, "NULL buffer");
+    DeviceGuard g(b->device);
+    // every call enqueued on the buffer's device has finished: the ring state
+    // below is then the one the device-side columns hold
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "device synchronise");
+    if (size) *size = b->size;
+    if (head) *head = b->head;
+    if (total) *total = (uint64_t)b->total;
+    return check_flags(b->err_slot);
+}
+
 // Validated kernel arguments of an ingest (n > 0) at the buffer's current head.
 static conduit_status ingest_args(conduit_buffer* b, const conduit_transitions* t, IngestArgs* out) {
     const conduit_buffer_opts& o = b->opts;

@@ -19,11 +19,24 @@ def _declared_functions():
     return sorted(set(re.findall(r"\b(conduit_[a-z_]+)\s*\(", text)))
 
 
+# the calls the experience path's boundary is stated in: buffer lifecycle,
+# ingestion, the priority callback, sampling, gather/transform, the two GAE
+# forms, the minibatch shuffle-gather, the ring-state query and the error text
+BOUNDARY = ["conduit_buffer_create", "conduit_buffer_required_bytes", "conduit_buffer_destroy", "conduit_ingest",
+            "conduit_update_priorities", "conduit_sample", "conduit_gather_transform", "conduit_gae",
+            "conduit_gae_packed", "conduit_minibatch_gather", "conduit_buffer_stats", "conduit_last_error"]
+
+
 def test_header_declares_the_boundary():
     names = _declared_functions()
-    for required in ["conduit_buffer_create", "conduit_ingest", "conduit_update_priorities", "conduit_sample",
-                     "conduit_gather_transform", "conduit_gae", "conduit_gae_packed", "conduit_minibatch_gather"]:
-        assert required in names
+    for required in BOUNDARY:
+        assert required in names, required
+
+
+def test_library_exports_the_boundary():
+    L = cd.lib()
+    for name in BOUNDARY:
+        assert hasattr(L, name), name
 
 
 def test_library_exports_every_declared_symbol():
@@ -86,6 +99,7 @@ def test_null_arguments_rejected():
     assert L.conduit_gather_transform(None, None, 1, None, None, None) == cd.EINVAL
     assert L.conduit_buffer_get_info(None, None) == cd.EINVAL
     assert L.conduit_buffer_read(None, 0, 0, 0, 0, None, None) == cd.EINVAL
+    assert L.conduit_buffer_stats(None, None, None, None) == cd.EINVAL
     L.conduit_buffer_destroy(None)  # no-op
 
 

@@ -672,3 +672,25 @@ def test_empty_calls_are_noops():
     assert buf.sync_check() == cd.OK
     assert buf.info().size == 0
     buf.close()
+
+
+def test_buffer_stats_ring_state_matches_oracle():
+    """conduit_buffer_stats waits for the device and reports size, head and
+    total; they equal the oracle's ring state across a wrap, and the device's
+    step column holds exactly `size` written slots."""
+    print("buffer stats: capacity 100, ingests of 64, 64, 100, 7", flush=True)
+    cap = 100
+    buf = _mk(cap, (4,), torch.uint8)
+    orc = oracle.Replay(cap, (4,), np.uint8)
+    rng = np.random.default_rng(7)
+    assert buf.stats() == (0, 0, 0)
+    for n in (64, 64, 100, 7):
+        obs = rng.integers(0, 256, (n, 4), dtype=np.uint8)
+        buf.ingest(dev(obs))
+        orc.ingest(n, obs=obs)
+        size, head, total = buf.stats()
+        assert (size, head, total) == (orc.size, orc.head, orc.total)
+        assert (size, head, total) == (buf.info().size, buf.info().head, buf.info().total)
+        steps = read_col(buf, cd.COL_STEP, cap * 4, np.int32)
+        assert int((steps >= 0).sum()) == size
+    buf.close()
