@@ -3,13 +3,13 @@
  *
  * The experience path is the per-iteration work between actors and learners
  * that the Conduit paper calls experience ingestion and experience delivery
- * (Sec. 2.2, "Experience Path Responsibilities"; Sec. 4, "Experience Data
- * Plane"):
- *   - off-policy ingestion inserts transitions into a persistent replay dataset
- *     and maintains the indices and metadata used for sampling and eviction;
- *   - off-policy delivery samples from that dataset, materialises the chosen
- *     transitions and applies batch/layout transforms (stacking, reshaping);
- *   - on-policy ingestion computes returns/advantages over trajectories;
+ * (Sec. 2.2, the responsibilities of the experience path; Sec. 4, the
+ * experience data plane):
+ *   - off-policy ingestion adds transitions to a long-lived replay store and
+ *     keeps the per-slot bookkeeping that sampling and eviction need;
+ *   - off-policy delivery draws from that store, builds the learner batch and
+ *     changes its layout (stacking, reshaping);
+ *   - on-policy ingestion derives returns and advantages over trajectories;
  *   - on-policy delivery partitions a rollout into shuffled minibatches;
  *   - replay priorities are updated through algorithm callbacks (App. C,
  *     Invariant 2), and staging never changes contents (App. C, Invariant 1).
@@ -137,8 +137,8 @@ size_t conduit_buffer_required_bytes(int64_t capacity, const int64_t* obs_shape,
                                      conduit_dtype obs_dtype, const conduit_buffer_opts* opts);
 
 /*
- * Create the persistent replay dataset of Sec. 2.2 ("inserts transitions into a
- * persistent replay dataset and maintains indices and metadata"): an HBM ring
+ * Create the replay dataset that off-policy ingestion writes into and keeps
+ * indexed (Sec. 2.2): an HBM ring
  * of `capacity` slots, each holding one observation of shape obs_shape[0..ndim)
  * and type obs_dtype (row-major), an action, a reward, a done flag, an episode
  * id and a step index, and (prioritized) a quantised priority leaf of a 64-ary
@@ -173,7 +173,10 @@ typedef struct {
     /* dense: device [n, row] observations, row = prod(obs_shape) * dtype size.
      * ragged: device concatenated elements of the n sequences. */
     const void* obs;
-    const int64_t* offsets;      /* ragged: device [n+1] element offsets, offsets[0] = 0 */
+    const int64_t* offsets;      /* ragged: device [n+1] element offsets, non-decreasing */
+    int64_t src_elems;           /* ragged: elements obs (and aux) hold; a row whose offsets
+                                    decrease or leave [0, src_elems] is stored empty and
+                                    flagged (CONDUIT_ESTATE later).  Ignored for dense rows. */
     const void* aux;             /* ragged, aux_elem_bytes > 0: device concatenated aux elements */
     const void* action;          /* device [n, action_bytes] or NULL (zeros) */
     const float* reward;         /* device [n] or NULL (zeros) */
@@ -189,13 +192,15 @@ typedef struct {
  * oldest transitions once the ring is full.  Then head = (head + n) mod capacity,
  * size = min(size + n, capacity).  With priorities, slot j's leaf becomes
  * L(prio[j]) and the running maximum absorbs prio[j]; without them, every new
- * transition gets L(running maximum) ("new transitions at maximal priority",
- * Schaul et al.).  L(p) = floor(2^F * p^alpha) computed exactly in integers,
+ * transition gets L(running maximum) (new transitions enter at the largest
+ * priority seen so far, as in Schaul et al.).  L(p) = floor(2^F * p^alpha) computed exactly in integers,
  * F = min(31, floor(32 (1 - alpha))) (see conduit_update_priorities).  The sum
  * tree is brought up to date before any later call in stream order.
  * Ragged rows longer than max_len are flagged (CONDUIT_ESTATE later) and stored
- * truncated.  Observation pointers must be 4-byte aligned.
- * Errors: EINVAL (n < 0 or n > capacity, missing required pointer), ESTATE.
+ * truncated; rows with offsets outside [0, src_elems] are flagged and stored
+ * empty.  Observation pointers must be 4-byte aligned.
+ * Errors: EINVAL (n < 0 or n > capacity, missing required pointer, ragged
+ * src_elems < 0), ESTATE.
  */
 conduit_status conduit_ingest(conduit_buffer* buf, const conduit_transitions* t, void* stream);
 
@@ -234,8 +239,8 @@ conduit_status conduit_update_priorities(conduit_buffer* buf, const int64_t* idx
 conduit_status conduit_update_ingest(conduit_buffer* buf, const int64_t* idx, const uint32_t* prio, int64_t n_update,
                                      const conduit_transitions* t, void* stream);
 /* ---------------------------------------------------------------------------
- * Sampling (Sec. 2.2 off-policy delivery: "samples from a persistent replay
- * dataset"; proportional prioritised replay)
+ * Sampling (Sec. 2.2 off-policy delivery draws from the replay dataset;
+ * proportional prioritised replay)
  * ------------------------------------------------------------------------- */
 /*
  * Draw `batch` slots by stratified inverse-CDF sampling over the sum tree.
@@ -259,9 +264,9 @@ conduit_status conduit_sample(conduit_buffer* buf, int64_t batch, const uint64_t
                               float* is_w_out, void* stream);
 
 /* ---------------------------------------------------------------------------
- * Gather / transform (Sec. 2.2 off-policy delivery: "materializes the selected
- * transitions, and performs batch/layout transformations"; processing
- * operators concat/stack, reshape, batching, padding/packing)
+ * Gather / transform (Sec. 2.2 off-policy delivery builds the learner batch
+ * from the drawn transitions and changes its layout; the processing operators
+ * it lists are concat/stack, reshape, batching and padding/packing)
  * ------------------------------------------------------------------------- */
 typedef enum {
     CONDUIT_XF_NONE = 0,        /* copy observation bytes unchanged */
@@ -359,8 +364,8 @@ conduit_status conduit_nstep(conduit_buffer* buf, const int64_t* idx, int64_t ba
                              const conduit_transform* xf, void* next_obs, void* stream);
 
 /* ---------------------------------------------------------------------------
- * Returns / advantages (Sec. 2.2 on-policy ingestion "computing
- * returns/advantages"; GAE as used by PPO, Schulman et al.)
+ * Returns / advantages (Sec. 2.2: on-policy ingestion derives returns and
+ * advantages; GAE as used by PPO, Schulman et al.)
  * ------------------------------------------------------------------------- */
 /*
  * Generalised advantage estimation over a time-major rollout of T steps and E
@@ -391,8 +396,8 @@ conduit_status conduit_gae(const float* rewards, const float* values, const uint
                            float* adv, float* ret, void* stream);
 
 /*
- * GAE with truncation bootstrap (on-policy ingestion's "boundary detection,
- * padding/truncation ... computing returns/advantages", Sec. 2.2): as
+ * GAE with truncation bootstrap (on-policy ingestion also finds episode
+ * boundaries and handles truncation before deriving advantages, Sec. 2.2): as
  * conduit_gae, and a step may also end by truncation (a time limit: the
  * episode would have continued).  Either end cuts the recursion; a truncated
  * step that did not also terminate bootstraps from final_values, the critic's
@@ -426,7 +431,7 @@ conduit_status conduit_gae_plan(int64_t T, int64_t E, int32_t aligned, int32_t* 
 /*
  * GAE over B right-padded sequences of up to Lmax elements (LLM post-training
  * shape; the paper's Verl mapping puts advantage computation in ingestion,
- * App. A / Table "Verl map"): sequence b of length L = lengths[b] receives the
+ * App. A, the table mapping Verl's stages): sequence b of length L = lengths[b] receives the
  * scalar last_reward[b] on element L-1, which also ends it; all other rewards
  * are 0.  values: device float [B, Lmax] or NULL (0).  adv, ret: device float
  * [B, Lmax]; positions t >= L are written as 0.  fp64 inside.
@@ -438,8 +443,8 @@ conduit_status conduit_gae_packed(const float* last_reward, const int32_t* lengt
                                   float* ret, void* stream);
 
 /* ---------------------------------------------------------------------------
- * Minibatch shuffle-gather (Sec. 2.2 on-policy delivery: "partitioning
- * trajectories into mini-batches and ... shuffling"; App. C Invariant 2)
+ * Minibatch shuffle-gather (Sec. 2.2: on-policy delivery splits trajectories
+ * into shuffled minibatches; App. C Invariant 2)
  * ------------------------------------------------------------------------- */
 /*
  * out row m = transform(src row perm[m]) for m = 0..n-1, plus up to 8 scalar
@@ -471,9 +476,17 @@ typedef struct {
     int32_t tree_depth;       /* root level (leaves are level 0) */
     int64_t tree_nodes[8];    /* nodes per level 0..tree_depth (level 0 = capacity) */
     int64_t arena_bytes;
+    /* the options the buffer was created with */
+    int32_t obs_dtype;        /* conduit_dtype */
+    int32_t prioritized;
+    int32_t frame_stack;
+    int32_t action_bytes;
+    int32_t ragged;
+    int32_t aux_elem_bytes;
+    int64_t max_len;          /* ragged: elements per slot (0 for dense buffers) */
 } conduit_buffer_info;
 
-/* Host-side state of the buffer; no device synchronisation. */
+/* Host-side state and geometry of the buffer; no device synchronisation. */
 conduit_status conduit_buffer_get_info(const conduit_buffer* buf, conduit_buffer_info* info);
 
 /*

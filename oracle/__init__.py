@@ -22,7 +22,8 @@ _LIB = None
 def lib():
     global _LIB
     if _LIB is None:
-        if not os.path.exists(_build.LIB):
+        # (re)build when the library is missing or older than its source
+        if not os.path.exists(_build.LIB) or os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC):
             _build.build()
         _LIB = C.CDLL(_build.LIB)
         _declare(_LIB)

@@ -7,11 +7,11 @@
  * two share no code (no headers, helpers, tables or constants).
  *
  * What is computed, and where it comes from:
- *   - The paper (Sec. 2.2, "Experience Path Responsibilities") names the operations:
- *     off-policy ingestion inserts transitions into a persistent replay dataset and
- *     keeps indices and metadata for sampling and eviction; off-policy delivery
- *     samples, materialises the chosen transitions and reshapes/concatenates them;
- *     on-policy ingestion computes returns/advantages; on-policy delivery partitions
+ *   - The paper (Sec. 2.2, the responsibilities of the experience path) names the operations:
+ *     off-policy ingestion adds transitions to a long-lived replay store and keeps
+ *     the per-slot bookkeeping that sampling and eviction need; off-policy
+ *     delivery draws from it, builds the batch and changes its layout; on-policy
+ *     ingestion derives returns and advantages; on-policy delivery partitions
  *     a rollout into shuffled minibatches; processing operators include
  *     concat/stack, reshape, sampling, shuffling, batching and padding/packing of
  *     variable-length sequences.  Tuples carry episode IDs (Sec. 2.1).

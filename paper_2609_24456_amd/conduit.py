@@ -40,7 +40,8 @@ class BufferOpts(C.Structure):
 
 
 class Transitions(C.Structure):
-    _fields_ = [("n", C.c_int64), ("obs", C.c_void_p), ("offsets", C.c_void_p), ("aux", C.c_void_p),
+    _fields_ = [("n", C.c_int64), ("obs", C.c_void_p), ("offsets", C.c_void_p), ("src_elems", C.c_int64),
+                ("aux", C.c_void_p),
                 ("action", C.c_void_p), ("reward", C.c_void_p), ("done", C.c_void_p),
                 ("episode_id", C.c_void_p), ("step", C.c_void_p), ("prio", C.c_void_p)]
 
@@ -106,7 +107,9 @@ class PlaceProfile(C.Structure):
 class BufferInfo(C.Structure):
     _fields_ = [("capacity", C.c_int64), ("row_bytes", C.c_int64), ("head", C.c_int64), ("size", C.c_int64),
                 ("total", C.c_int64), ("tree_depth", C.c_int32), ("tree_nodes", C.c_int64 * 8),
-                ("arena_bytes", C.c_int64)]
+                ("arena_bytes", C.c_int64), ("obs_dtype", C.c_int32), ("prioritized", C.c_int32),
+                ("frame_stack", C.c_int32), ("action_bytes", C.c_int32), ("ragged", C.c_int32),
+                ("aux_elem_bytes", C.c_int32), ("max_len", C.c_int64)]
 
 
 # every symbol include/conduit.h declares, with its ctypes signature
@@ -182,18 +185,73 @@ def _stream(stream):
     return C.c_void_p(int(stream))
 
 
-def _ptr(t, dtype=None, name="tensor"):
+_ELEM4_INT = (torch.int32, torch.uint32)
+_ELEM8_INT = (torch.int64, torch.uint64)
+
+
+def _ptr(t, dtype=None, name="tensor", nbytes=None, numel=None):
+    """Device address of a contiguous tensor, after checking (in this order)
+    its type, dtype (one dtype or a tuple of accepted dtypes), that it holds at
+    least `nbytes` bytes / `numel` elements, contiguity and device.  Each
+    failure raises before anything reaches the library, so a shape or dtype
+    slip never becomes an out-of-bounds device access."""
     if t is None:
         return None
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch tensor")
-    if not t.is_cuda:
-        raise ValueError(f"{name} must be on a HIP device")
+    if dtype is not None:
+        ok = t.dtype in dtype if isinstance(dtype, tuple) else t.dtype == dtype
+        if not ok:
+            raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if nbytes is not None and t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes, the call touches {nbytes}")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, the call touches {numel}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
-    if dtype is not None and t.dtype != dtype:
-        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not _on_device(t):
+        raise ValueError(f"{name} must be on a HIP device")
     return t.data_ptr()
+
+
+def _on_device(t):
+    return t.is_cuda
+
+
+def _info(handle):
+    """The buffer's host-side geometry (conduit_buffer_get_info: no device work)."""
+    info = BufferInfo()
+    _check(lib().conduit_buffer_get_info(handle, C.byref(info)))
+    return info
+
+
+_OUT_ELEM = {XF_NONE: 1, XF_U8_F32: 4, XF_U8_BF16_NORM: 2}
+
+
+def _out_row_bytes(info, xf):
+    """Bytes of one gathered sample's observation output (dense buffers)."""
+    if xf.kind not in _OUT_ELEM:
+        raise ValueError("dense buffers gather with NONE, U8_F32 or U8_BF16_NORM")
+    return info.frame_stack * info.row_bytes * _OUT_ELEM[xf.kind]
+
+
+def _batch_ptrs(info, n, xf, obs, action, reward, done, mask, aux, length):
+    """A LearnerBatch for n samples of the buffer described by `info`, every
+    output checked against the bytes the gather writes."""
+    out = LearnerBatch()
+    if info.ragged:
+        L = info.max_len
+        out.obs = _ptr(obs, _ELEM4_INT + (torch.float32,), "obs", nbytes=n * L * 4)
+        out.mask = _ptr(mask, (torch.uint8, torch.bool), "mask", nbytes=n * L)
+        out.aux = _ptr(aux, None, "aux", nbytes=n * L * 4)
+        out.length = _ptr(length, torch.int32, "length", numel=n)
+    else:
+        out.obs = _ptr(obs, None, "obs", nbytes=n * _out_row_bytes(info, xf))
+        out.mask, out.aux, out.length = None, None, None
+    out.action = _ptr(action, None, "action", nbytes=n * info.action_bytes)
+    out.reward = _ptr(reward, torch.float32, "reward", numel=n)
+    out.done = _ptr(done, (torch.uint8, torch.bool), "done", numel=n)
+    return out
 
 
 def transform(kind=XF_NONE, mean=None, std=None, pad_id=0):
@@ -241,99 +299,108 @@ def conduit_buffer_destroy(handle):
     lib().conduit_buffer_destroy(handle)
 
 
-def _transitions(n, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None, offsets=None,
-                 aux=None):
+def _transitions(info, n, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None,
+                 offsets=None, aux=None):
+    n = int(n)
+    if n < 0:
+        raise ValueError("n must be >= 0")
     t = Transitions()
-    t.n = int(n)
-    t.obs = _ptr(obs, None, "obs")
-    t.offsets = _ptr(offsets, torch.int64, "offsets")
-    t.aux = _ptr(aux, None, "aux")
-    t.action = _ptr(action, None, "action")
-    t.reward = _ptr(reward, torch.float32, "reward")
-    t.done = _ptr(done, torch.uint8, "done")
-    t.episode_id = _ptr(episode_id, None, "episode_id")  # uint32 ids (int32 view accepted)
-    t.step = _ptr(step, torch.int32, "step")
-    t.prio = _ptr(prio, None, "prio")
+    t.n = n
+    if info.ragged:
+        t.obs = _ptr(obs, _ELEM4_INT + (torch.float32,), "obs")
+        t.offsets = _ptr(offsets, torch.int64, "offsets", numel=n + 1)
+        t.aux = _ptr(aux, None, "aux")
+        if aux is not None and aux.element_size() != 4:
+            raise TypeError("aux must hold 4-byte elements")
+        # the kernel keeps every offset within the elements obs (and aux) hold
+        t.src_elems = min(obs.numel(), aux.numel()) if aux is not None else obs.numel()
+    else:
+        t.obs = _ptr(obs, None, "obs", nbytes=n * info.row_bytes)
+        t.offsets, t.aux, t.src_elems = None, None, 0
+    t.action = _ptr(action, None, "action", nbytes=n * info.action_bytes)
+    t.reward = _ptr(reward, torch.float32, "reward", numel=n)
+    t.done = _ptr(done, (torch.uint8, torch.bool), "done", numel=n)
+    t.episode_id = _ptr(episode_id, _ELEM4_INT, "episode_id", numel=n)  # uint32 ids (int32 view accepted)
+    t.step = _ptr(step, torch.int32, "step", numel=n)
+    t.prio = _ptr(prio, _ELEM4_INT, "prio", numel=n)
     return t
 
 
 def conduit_ingest(handle, n, obs, action=None, reward=None, done=None, episode_id=None, step=None, prio=None,
                    offsets=None, aux=None, stream=None):
-    t = _transitions(n, obs, action, reward, done, episode_id, step, prio, offsets, aux)
+    t = _transitions(_info(handle), n, obs, action, reward, done, episode_id, step, prio, offsets, aux)
     _check(lib().conduit_ingest(handle, C.byref(t), _stream(stream)))
 
 
 def conduit_update_ingest(handle, idx, upd_prio, n, obs, action=None, reward=None, done=None, episode_id=None,
                           step=None, prio=None, offsets=None, aux=None, stream=None):
     """The priority update (idx, upd_prio), then the ingest of n rows, in one call."""
-    t = _transitions(n, obs, action, reward, done, episode_id, step, prio, offsets, aux)
+    t = _transitions(_info(handle), n, obs, action, reward, done, episode_id, step, prio, offsets, aux)
     k = idx.numel() if idx is not None else 0
-    _check(lib().conduit_update_ingest(handle, _ptr(idx, torch.int64, "idx"), _ptr(upd_prio, None, "upd_prio"), k,
-                                       C.byref(t), _stream(stream)))
+    _check(lib().conduit_update_ingest(handle, _ptr(idx, torch.int64, "idx"),
+                                       _ptr(upd_prio, _ELEM4_INT, "upd_prio", numel=k), k, C.byref(t),
+                                       _stream(stream)))
 
 
 def conduit_update_priorities(handle, idx, prio, stream=None):
     n = idx.numel()
     if prio.numel() != n:
         raise ValueError("idx and prio must have the same length")
-    _check(lib().conduit_update_priorities(handle, _ptr(idx, torch.int64, "idx"), _ptr(prio, None, "prio"), n,
+    _check(lib().conduit_update_priorities(handle, _ptr(idx, torch.int64, "idx"), _ptr(prio, _ELEM4_INT, "prio"), n,
                                            _stream(stream)))
 
 
 def conduit_sample(handle, batch, uniforms, idx_out, is_w_out=None, stream=None):
-    if uniforms.numel() < batch or idx_out.numel() < batch or (is_w_out is not None and is_w_out.numel() < batch):
-        raise ValueError("uniforms/outputs smaller than batch")
-    _check(lib().conduit_sample(handle, batch, _ptr(uniforms, None, "uniforms"), _ptr(idx_out, torch.int64, "idx_out"),
-                                _ptr(is_w_out, torch.float32, "is_w_out"), _stream(stream)))
+    _check(lib().conduit_sample(handle, batch, _ptr(uniforms, _ELEM8_INT, "uniforms", numel=batch),
+                                _ptr(idx_out, torch.int64, "idx_out", numel=batch),
+                                _ptr(is_w_out, torch.float32, "is_w_out", numel=batch), _stream(stream)))
 
 
 def conduit_gather_transform(handle, idx, xf, obs=None, action=None, reward=None, done=None, mask=None, aux=None,
                              length=None, stream=None):
-    out = LearnerBatch()
-    out.obs = _ptr(obs, None, "obs")
-    out.action = _ptr(action, None, "action")
-    out.reward = _ptr(reward, torch.float32, "reward")
-    out.done = _ptr(done, torch.uint8, "done")
-    out.mask = _ptr(mask, None, "mask")
-    out.aux = _ptr(aux, None, "aux")
-    out.length = _ptr(length, torch.int32, "length")
-    _check(lib().conduit_gather_transform(handle, _ptr(idx, torch.int64, "idx"), idx.numel(), C.byref(xf),
-                                          C.byref(out), _stream(stream)))
+    n = idx.numel()
+    out = _batch_ptrs(_info(handle), n, xf, obs, action, reward, done, mask, aux, length)
+    _check(lib().conduit_gather_transform(handle, _ptr(idx, torch.int64, "idx"), n, C.byref(xf), C.byref(out),
+                                          _stream(stream)))
 
 
 def conduit_sample_gather(handle, batch, uniforms, idx_out, is_w_out, xf, obs=None, action=None, reward=None,
                           done=None, mask=None, aux=None, length=None, stream=None):
-    if uniforms.numel() < batch or idx_out.numel() < batch or (is_w_out is not None and is_w_out.numel() < batch):
-        raise ValueError("uniforms/outputs smaller than batch")
-    out = LearnerBatch()
-    out.obs = _ptr(obs, None, "obs")
-    out.action = _ptr(action, None, "action")
-    out.reward = _ptr(reward, torch.float32, "reward")
-    out.done = _ptr(done, torch.uint8, "done")
-    out.mask = _ptr(mask, None, "mask")
-    out.aux = _ptr(aux, None, "aux")
-    out.length = _ptr(length, torch.int32, "length")
-    _check(lib().conduit_sample_gather(handle, batch, _ptr(uniforms, None, "uniforms"),
-                                       _ptr(idx_out, torch.int64, "idx_out"), _ptr(is_w_out, torch.float32, "is_w_out"),
+    out = _batch_ptrs(_info(handle), batch, xf, obs, action, reward, done, mask, aux, length)
+    _check(lib().conduit_sample_gather(handle, batch, _ptr(uniforms, _ELEM8_INT, "uniforms", numel=batch),
+                                       _ptr(idx_out, torch.int64, "idx_out", numel=batch),
+                                       _ptr(is_w_out, torch.float32, "is_w_out", numel=batch),
                                        C.byref(xf), C.byref(out), _stream(stream)))
 
 
 def conduit_nstep(handle, idx, n, gamma, next_idx, ret, discount, valid, xf=None, next_obs=None, stream=None):
     """n-step return targets (and bootstrap-state stacks) of sampled slots."""
     B = idx.numel()
+    info = _info(handle)
+    nbytes = B * _out_row_bytes(info, xf) if (next_obs is not None and xf is not None and not info.ragged) else None
     _check(lib().conduit_nstep(handle, _ptr(idx, torch.int64, "idx"), B, int(n), float(gamma),
-                               _ptr(next_idx, torch.int64, "next_idx"), _ptr(ret, torch.float32, "ret"),
-                               _ptr(discount, torch.float32, "discount"), _ptr(valid, torch.uint8, "valid"),
+                               _ptr(next_idx, torch.int64, "next_idx", numel=B),
+                               _ptr(ret, torch.float32, "ret", numel=B),
+                               _ptr(discount, torch.float32, "discount", numel=B),
+                               _ptr(valid, (torch.uint8, torch.bool), "valid", numel=B),
                                C.byref(xf) if xf is not None else None,
-                               next_obs.data_ptr() if next_obs is not None else None, _stream(stream)))
+                               _ptr(next_obs, None, "next_obs", nbytes=nbytes), _stream(stream)))
+
+
+def _rollout_shape(rewards):
+    if not isinstance(rewards, torch.Tensor) or rewards.dim() != 2:
+        raise ValueError("rewards must be a [T, E] tensor")
+    return rewards.shape
 
 
 def conduit_gae(rewards, values, dones, bootstrap, gamma, lam, adv, ret, stream=None):
-    T, E = rewards.shape
-    _check(lib().conduit_gae(_ptr(rewards, torch.float32, "rewards"), _ptr(values, torch.float32, "values"),
-                             _ptr(dones, torch.uint8, "dones"), _ptr(bootstrap, torch.float32, "bootstrap"), T, E,
-                             float(gamma), float(lam), _ptr(adv, torch.float32, "adv"),
-                             _ptr(ret, torch.float32, "ret"), _stream(stream)))
+    T, E = _rollout_shape(rewards)
+    N = T * E
+    _check(lib().conduit_gae(_ptr(rewards, torch.float32, "rewards"), _ptr(values, torch.float32, "values", numel=N),
+                             _ptr(dones, (torch.uint8, torch.bool), "dones", numel=N),
+                             _ptr(bootstrap, torch.float32, "bootstrap", numel=E), T, E, float(gamma), float(lam),
+                             _ptr(adv, torch.float32, "adv", numel=N), _ptr(ret, torch.float32, "ret", numel=N),
+                             _stream(stream)))
 
 
 GAE_PATHS = ("one", "one_v4", "short", "look", "split")
@@ -349,21 +416,26 @@ def gae_plan(T, E, aligned=True):
 
 def conduit_gae_truncated(rewards, values, dones, truncated, final_values, bootstrap, gamma, lam, adv, ret,
                           stream=None):
-    T, E = rewards.shape
-    _check(lib().conduit_gae_truncated(_ptr(rewards, torch.float32, "rewards"), _ptr(values, torch.float32, "values"),
-                                       _ptr(dones, torch.uint8, "dones"), _ptr(truncated, torch.uint8, "truncated"),
-                                       _ptr(final_values, torch.float32, "final_values"),
-                                       _ptr(bootstrap, torch.float32, "bootstrap"), T, E, float(gamma), float(lam),
-                                       _ptr(adv, torch.float32, "adv"), _ptr(ret, torch.float32, "ret"),
-                                       _stream(stream)))
+    T, E = _rollout_shape(rewards)
+    N = T * E
+    u8 = (torch.uint8, torch.bool)
+    _check(lib().conduit_gae_truncated(_ptr(rewards, torch.float32, "rewards"),
+                                       _ptr(values, torch.float32, "values", numel=N),
+                                       _ptr(dones, u8, "dones", numel=N), _ptr(truncated, u8, "truncated", numel=N),
+                                       _ptr(final_values, torch.float32, "final_values", numel=N),
+                                       _ptr(bootstrap, torch.float32, "bootstrap", numel=E), T, E, float(gamma),
+                                       float(lam), _ptr(adv, torch.float32, "adv", numel=N),
+                                       _ptr(ret, torch.float32, "ret", numel=N), _stream(stream)))
 
 
 def conduit_gae_packed(last_reward, lengths, values, Lmax, gamma, lam, adv, ret, stream=None):
     B = last_reward.numel()
+    N = B * int(Lmax)
     _check(lib().conduit_gae_packed(_ptr(last_reward, torch.float32, "last_reward"),
-                                    _ptr(lengths, torch.int32, "lengths"), _ptr(values, torch.float32, "values"), B,
-                                    int(Lmax), float(gamma), float(lam), _ptr(adv, torch.float32, "adv"),
-                                    _ptr(ret, torch.float32, "ret"), _stream(stream)))
+                                    _ptr(lengths, torch.int32, "lengths", numel=B),
+                                    _ptr(values, torch.float32, "values", numel=N), B, int(Lmax), float(gamma),
+                                    float(lam), _ptr(adv, torch.float32, "adv", numel=N),
+                                    _ptr(ret, torch.float32, "ret", numel=N), _stream(stream)))
 
 
 def conduit_schedule(t_rollout, t_update, g_ing, t_ing, g_del, t_del, t_sync_ing=0.0, t_sync_del=0.0,
@@ -449,18 +521,21 @@ def conduit_sync_cost_us(s1, s2, hops=200):
 
 def conduit_minibatch_gather(src, row_bytes, n_src, perm, xf, out, cols=(), cols_out=(), stream=None):
     ncols = len(cols)
-    ca = (C.c_void_p * max(1, ncols))(*[_ptr(c, torch.float32, "col") for c in cols])
-    co = (C.c_void_p * max(1, ncols))(*[_ptr(c, torch.float32, "col_out") for c in cols_out])
-    _check(lib().conduit_minibatch_gather(_ptr(src, None, "src"), int(row_bytes), int(n_src),
-                                          _ptr(perm, torch.int64, "perm"), perm.numel(), C.byref(xf),
-                                          _ptr(out, None, "out"), ca if ncols else None, co if ncols else None,
-                                          ncols, _stream(stream)))
+    if len(cols_out) != ncols:
+        raise ValueError("cols and cols_out must have the same length")
+    if xf.kind not in _OUT_ELEM:
+        raise ValueError("the minibatch gather takes NONE, U8_F32 or U8_BF16_NORM")
+    n, row_bytes, n_src = perm.numel(), int(row_bytes), int(n_src)
+    ca = (C.c_void_p * max(1, ncols))(*[_ptr(c, torch.float32, "col", numel=n_src) for c in cols])
+    co = (C.c_void_p * max(1, ncols))(*[_ptr(c, torch.float32, "col_out", numel=n) for c in cols_out])
+    _check(lib().conduit_minibatch_gather(_ptr(src, None, "src", nbytes=n_src * row_bytes), row_bytes, n_src,
+                                          _ptr(perm, torch.int64, "perm"), n, C.byref(xf),
+                                          _ptr(out, None, "out", nbytes=n * row_bytes * _OUT_ELEM[xf.kind]),
+                                          ca if ncols else None, co if ncols else None, ncols, _stream(stream)))
 
 
 def conduit_buffer_get_info(handle):
-    info = BufferInfo()
-    _check(lib().conduit_buffer_get_info(handle, C.byref(info)))
-    return info
+    return _info(handle)
 
 
 def conduit_buffer_stats(handle):

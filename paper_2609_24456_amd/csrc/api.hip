@@ -86,7 +86,7 @@ const char* kErrText[kErrKinds] = {
     "permutation entry outside [0, n_src)",
     "GAE segment never published by its workgroup (GAE calls overlapping on one GPU?)",
     "sum-tree descent found no child",
-    "",
+    "ragged ingest offsets decreasing or outside [0, src_elems]",
 };
 
 // Returns ESTATE if any flag of `slot` is set (no synchronisation).
@@ -443,6 +443,13 @@ conduit_status conduit_buffer_get_info(const conduit_buffer* b, conduit_buffer_i
     info->tree_depth = b->opts.prioritized ? b->layout.depth : 0;
     for (int l = 0; l <= b->layout.depth && l < 8; ++l) info->tree_nodes[l] = b->layout.nodes[l];
     info->arena_bytes = (int64_t)b->layout.total;
+    info->obs_dtype = (int32_t)b->obs_dtype;
+    info->prioritized = b->opts.prioritized;
+    info->frame_stack = b->opts.frame_stack;
+    info->action_bytes = b->opts.action_bytes;
+    info->ragged = b->opts.ragged;
+    info->aux_elem_bytes = b->opts.aux_elem_bytes;
+    info->max_len = b->layout.max_len;
     return CONDUIT_OK;
 }
 
@@ -465,6 +472,7 @@ static conduit_status ingest_args(conduit_buffer* b, const conduit_transitions* 
     if (!t->obs) return fail(CONDUIT_EINVAL, "obs must not be NULL");
     if (reinterpret_cast<uintptr_t>(t->obs) % 4) return fail(CONDUIT_EINVAL, "obs must be 4-byte aligned");
     if (o.ragged && !t->offsets) return fail(CONDUIT_EINVAL, "ragged ingest needs offsets");
+    if (o.ragged && t->src_elems < 0) return fail(CONDUIT_EINVAL, "ragged ingest needs src_elems >= 0");
     if (o.ragged && t->aux && reinterpret_cast<uintptr_t>(t->aux) % 4) return fail(CONDUIT_EINVAL, "aux must be 4-byte aligned");
     if (o.frame_stack > 1 && (!t->episode_id || !t->step))
         return fail(CONDUIT_EINVAL, "frame-stacking buffers need episode_id and step");
@@ -486,6 +494,7 @@ static conduit_status ingest_args(conduit_buffer* b, const conduit_transitions* 
     a.prioritized = o.prioritized;
     a.src_obs = static_cast<const uint8_t*>(t->obs);
     a.src_offsets = t->offsets;
+    a.src_elems = o.ragged ? t->src_elems : 0;
     a.src_aux = static_cast<const uint8_t*>(t->aux);
     a.src_action = static_cast<const uint8_t*>(t->action);
     a.src_reward = t->reward;

@@ -24,6 +24,7 @@ enum ErrKind : int {
     ERR_PERM_INDEX = 4,     // minibatch permutation entry outside [0, n_src)
     ERR_GAE_WAIT = 5,       // split GAE: a later segment never published (overlapping calls)
     ERR_DESCENT = 6,        // tree descent found no child (never expected)
+    ERR_OFFSETS = 7,        // ragged ingest offsets decreasing or outside [0, src_elems]
     kErrKinds = 8,
 };
 
@@ -285,6 +286,7 @@ struct IngestArgs {
     // source
     const uint8_t* src_obs;
     const int64_t* src_offsets;
+    int64_t src_elems;       // ragged: elements the source obs (and aux) hold
     const uint8_t* src_aux;
     const uint8_t* src_action;
     const float* src_reward;

@@ -1,6 +1,6 @@
 // Stratified inverse-CDF descent of the 64-ary integer sum tree by one
 // wavefront (proportional prioritised replay, Schaul et al.; the paper's
-// off-policy delivery samples from the persistent replay dataset, Sec. 2.2).
+// off-policy delivery draws from the replay store, Sec. 2.2).
 // Shared by the sampler kernel and the fused sampler + gather.
 #pragma once
 #include "common.h"

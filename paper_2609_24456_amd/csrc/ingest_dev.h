@@ -61,13 +61,23 @@ __device__ void copy_dense(const IngestArgs& a, int64_t block, int tid) {
     }
 }
 
+// Source span [*off, *off + *len) of ragged row j.  Offsets that decrease or
+// leave [0, src_elems] give an empty span (ok = false: the metadata lane of the
+// row flags it), so no element outside the source is ever read.
+__device__ __forceinline__ bool ragged_span(const IngestArgs& a, int64_t j, int64_t* off, int64_t* len) {
+    const int64_t b = a.src_offsets[j], e = a.src_offsets[j + 1];
+    const bool ok = 0 <= b && b <= e && e <= a.src_elems;
+    *off = ok ? b : 0;
+    *len = ok ? e - b : 0;
+    return ok;
+}
+
 __device__ inline void copy_ragged(const IngestArgs& a, int64_t j, int tid) {
     int64_t slot = a.head + j;
     if (slot >= a.capacity) slot -= a.capacity;
-    int64_t len = a.src_offsets[j + 1] - a.src_offsets[j];
-    if (len < 0) len = 0;
+    int64_t off, len;
+    ragged_span(a, j, &off, &len);
     if (len > a.max_len) len = a.max_len;  // flagged by the meta lane of row j
-    const int64_t off = a.src_offsets[j];
     if (len == 0) return;
     const uint32_t* __restrict__ s = reinterpret_cast<const uint32_t*>(a.src_obs) + off;
     uint32_t* __restrict__ d = reinterpret_cast<uint32_t*>(a.obs + slot * a.row_bytes);
@@ -207,7 +217,8 @@ __device__ __forceinline__ void ingest_meta(const IngestArgs& a, int64_t block, 
     const uint8_t dn = a.src_done ? a.src_done[jj] : (uint8_t)0;
     const uint32_t ep = a.src_episode ? a.src_episode[jj] : 0u;
     const int32_t st = a.src_step ? a.src_step[jj] : 0;
-    const int64_t len = a.length ? a.src_offsets[jj + 1] - a.src_offsets[jj] : 0;
+    int64_t len = 0, off_unused;
+    const bool span_ok = a.length ? ragged_span(a, jj, &off_unused, &len) : true;
     const bool act_words = a.src_action && (a.action_bytes & 3) == 0;
     const int words = act_words ? a.action_bytes >> 2 : 0;
     uint32_t w[kActWords];
@@ -236,9 +247,10 @@ __device__ __forceinline__ void ingest_meta(const IngestArgs& a, int64_t block, 
         a.step[slot] = st;
         if (a.length) {
             int64_t l = len;
-            if (l < 0 || l > a.max_len) {
+            if (!span_ok) flag_error(a.err, ERR_OFFSETS);
+            if (l > a.max_len) {
                 flag_error(a.err, ERR_SEQ_LENGTH);
-                l = l < 0 ? 0 : a.max_len;
+                l = a.max_len;
             }
             a.length[slot] = (int32_t)l;
         }

@@ -1,5 +1,5 @@
-// Generalised advantage estimation (on-policy ingestion "computing
-// returns/advantages", paper Sec. 2.2; GAE as used by PPO, Schulman et al.).
+// Generalised advantage estimation (on-policy ingestion derives returns and
+// advantages, paper Sec. 2.2; GAE as used by PPO, Schulman et al.).
 //
 // The recursion A_t = delta_t + a_t A_{t+1}, a_t = gamma*lambda*(1 - d_t), is
 // affine in A_{t+1}, so a chunk of consecutive steps composes into one map

@@ -1,7 +1,7 @@
 // Gather / transform: materialise the learner batch (off-policy delivery
-// "materializes the selected transitions, and performs batch/layout
-// transformations", paper Sec. 2.2; concat/stack, reshape, batching and
-// padding/packing are the processing operators it lists).  The same kernels
+// builds it from the drawn transitions and changes its layout, paper Sec. 2.2;
+// concat/stack, reshape, batching and padding/packing are the processing
+// operators it lists).  The same kernels
 // serve the on-policy minibatch shuffle-gather (K = 1, rows of a rollout).
 //
 // Two shapes over the work items of gather_dev.h: four persistent workgroups

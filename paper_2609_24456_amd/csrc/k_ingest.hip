@@ -1,8 +1,8 @@
 // Ring-buffer ingest: copy n transitions into slots (head + j) mod capacity and
 // bring the priority sum tree up to date, in one launch.
 //
-// Off-policy ingestion inserts transitions into a persistent replay dataset and
-// keeps the indices and metadata needed for sampling and eviction (paper
+// Off-policy ingestion adds transitions to the long-lived replay store and
+// keeps the per-slot bookkeeping that sampling and eviction need (paper
 // Sec. 2.2); new transitions enter with the running maximum priority unless the
 // caller gives one (proportional prioritised replay, Schaul et al.).
 //

@@ -1,6 +1,6 @@
 // Stratified inverse-CDF sampling over the 64-ary integer sum tree, with
-// importance weights (off-policy delivery "samples from a persistent replay
-// dataset", paper Sec. 2.2; proportional prioritised replay, Schaul et al.).
+// importance weights (off-policy delivery draws from the replay dataset, paper
+// Sec. 2.2; proportional prioritised replay, Schaul et al.).
 //
 // k_sample: one wavefront per sample runs tree_descend (descend.h): the exact
 // stratified target, then one coalesced 64-child load, wavefront prefix scan

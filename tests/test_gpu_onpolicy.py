@@ -301,36 +301,3 @@ def test_minibatch_transforms_and_bad_perm():
     o = host(out)
     assert np.all(o[5] == 0) and np.all(o[6] == 0)
     assert np.array_equal(o[7:], src_h[bad[7:]])
-
-
-@pytest.mark.slow
-def test_ppo_full_size_minibatch_sampled_rows():
-    print("ppo: full rollout 2048 x 256 x 3x84x84 (11.1 GB), GAE, minibatches 0 and 31", flush=True)
-    cfg = synth.PPO()
-    T, E = cfg.T, cfg.E
-    row = 3 * 84 * 84
-    buf = _ppo_rollout_buffer(cfg, steps_per_call=64)
-    src = torch.empty(0, dtype=torch.uint8, device="cuda")
-    # gather straight from the buffer's observation column: one minibatch of 16384 rows
-    ga, gr = _gae_gpu(cfg.reward, cfg.value, cfg.done, cfg.bootstrap, cfg.gamma, cfg.lam)
-    oa, orr = oracle.gae(cfg.reward, cfg.value, cfg.done, cfg.bootstrap, cfg.gamma, cfg.lam)
-    assert_gae_close(ga, oa)
-    A, R = dev(ga.reshape(-1)), dev(gr.reshape(-1))
-    src = _obs_column_tensor(buf, T * E, row)
-    buf.close()
-    mb = 16384
-    check = np.random.default_rng(0).choice(mb, 48, replace=False)
-    for m in [0, 31]:
-        rows = cfg.perm[m * mb:(m + 1) * mb]
-        out = torch.empty((mb, 3, 84, 84), dtype=torch.float32, device="cuda")
-        a_out = torch.empty(mb, dtype=torch.float32, device="cuda")
-        r_out = torch.empty(mb, dtype=torch.float32, device="cuda")
-        cd.conduit_minibatch_gather(src, row, T * E, dev(rows), cd.transform(cd.XF_U8_F32), out, cols=[A, R],
-                                    cols_out=[a_out, r_out])
-        assert cd.conduit_sync_check() == cd.OK, cd.last_error()
-        sel = rows[check]
-        want = oracle.rows(cfg.obs_rows(sel).numpy(), np.arange(len(sel)), oracle.XF_U8_F32)
-        assert np.array_equal(host(out[check]).view(np.uint32), want.view(np.uint32))
-        assert_gae_close(host(a_out), oa.reshape(-1)[rows])
-        assert_gae_close(host(r_out), orr.reshape(-1)[rows])
-        del out

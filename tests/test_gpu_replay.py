@@ -694,3 +694,29 @@ def test_buffer_stats_ring_state_matches_oracle():
         steps = read_col(buf, cd.COL_STEP, cap * 4, np.int32)
         assert int((steps >= 0).sum()) == size
     buf.close()
+
+
+def test_ragged_offsets_outside_the_source_are_flagged():
+    """Ragged ingest rows whose offsets decrease or leave the source's elements
+    are stored empty and flagged; a good row beside them is stored intact."""
+    print("ragged ingest: offsets [0, 5, 3, 200] over 100 source elements", flush=True)
+    buf = _mk(8, (16,), torch.int32, ragged=True, aux_elem_bytes=4)
+    tok = np.arange(100, dtype=np.int32) + 1000
+    lp = -np.arange(100, dtype=np.float32)
+    off = np.array([0, 5, 3, 200], np.int64)
+    buf.ingest(dev(tok), offsets=dev(off), aux=dev(lp))
+    assert buf.sync_check() == cd.ESTATE
+    assert "offsets" in cd.last_error()
+    buf.clear_error()
+    length = read_col(buf, cd.COL_LENGTH, 8 * 4, np.int32)
+    assert list(length[:3]) == [5, 0, 0]
+    seq = read_col(buf, cd.COL_OBS, 8 * 16 * 4, np.int32).reshape(8, 16)
+    assert np.array_equal(seq[0, :5], tok[:5])
+    aux = read_col(buf, cd.COL_AUX, 8 * 16 * 4, np.float32).reshape(8, 16)
+    assert np.array_equal(aux[0, :5], lp[:5])
+    # the same rows with offsets inside the source: no flag
+    buf.ingest(dev(tok), offsets=dev(np.array([0, 5, 9, 25], np.int64)), aux=dev(lp))
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    length = read_col(buf, cd.COL_LENGTH, 8 * 4, np.int32)
+    assert list(length[3:6]) == [5, 4, 16]
+    buf.close()
