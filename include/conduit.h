@@ -396,6 +396,28 @@ conduit_status conduit_gae(const float* rewards, const float* values, const uint
                            float* adv, float* ret, void* stream);
 
 /*
+ * conduit_gae for callers that cannot allocate memory: code recorded under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, kernels and results as conduit_gae, and it calls no allocating
+ * routine on any call, the first included: its scratch memory (the look-back
+ * table of the split path and its own sticky error words) is the per-GPU
+ * static table conduit_gae uses too, 3.2 MB of device memory that each GPU
+ * holds until the process ends; its address is looked up once per GPU, on the
+ * first call made with that GPU current.  Limit: a rollout whose split path
+ * needs more than 4,096 tiles of the table is rejected with EINVAL (the plan
+ * of conduit_gae_plan never asks for more: wider rollouts take kernels that
+ * need no table).  Calls that overlap in time on one GPU, of either function,
+ * share the table and race.  Device-side errors of this call are recorded in
+ * the table, not in pinned host memory, and are reported by
+ * conduit_sync_check(NULL, stream) and cleared by conduit_clear_error(NULL);
+ * the call itself cannot see them (it never reads device memory).
+ * Errors: EINVAL, EDEVICE.
+ */
+conduit_status conduit_gae_noalloc(const float* rewards, const float* values, const uint8_t* dones,
+                                   const float* bootstrap, int64_t T, int64_t E, double gamma, double lambda,
+                                   float* adv, float* ret, void* stream);
+
+/*
  * GAE with truncation bootstrap (on-policy ingestion also finds episode
  * boundaries and handles truncation before deriving advantages, Sec. 2.2): as
  * conduit_gae, and a step may also end by truncation (a time limit: the
@@ -527,12 +549,14 @@ conduit_status conduit_buffer_read(const conduit_buffer* buf, conduit_column col
 /*
  * Wait for `stream`, then report the sticky device-side error flag of `buf`
  * (NULL: the flag shared by the stand-alone calls conduit_gae,
- * conduit_gae_packed and conduit_minibatch_gather).  Returns OK or ESTATE (with
+ * conduit_gae_packed and conduit_minibatch_gather, and then the words
+ * conduit_gae_noalloc keeps in the current GPU's static table).  Returns OK or ESTATE (with
  * a description in conduit_last_error), or EDEVICE.
  */
 conduit_status conduit_sync_check(const conduit_buffer* buf, void* stream);
 
-/* Clear the sticky device-side error flag of `buf` (NULL: the stand-alone flag). */
+/* Clear the sticky device-side error flag of `buf` (NULL: the stand-alone flag,
+ * and conduit_gae_noalloc's words on the current GPU, a synchronous copy). */
 void conduit_clear_error(conduit_buffer* buf);
 
 /* Thread-local description of the last failed call ("" if none). */

@@ -129,6 +129,7 @@ SIGNATURES = {
     "conduit_gather_transform": (ST, [P, P, I64, P, P, P]),
     "conduit_sample_gather": (ST, [P, I64, P, P, P, P, P, P]),
     "conduit_gae": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
+    "conduit_gae_noalloc": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_update_ingest": (ST, [P, P, P, I64, P, P]),
     "conduit_nstep": (ST, [P, P, I64, I32_, F64, P, P, P, P, P, P, P]),
     "conduit_gae_truncated": (ST, [P, P, P, P, P, P, I64, I64, F64, F64, P, P, P]),

@@ -882,6 +882,32 @@ conduit_status conduit_gae(const float* rewards, const float* values, const uint
     return CONDUIT_OK;
 }
 
+conduit_status conduit_gae_noalloc(const float* rewards, const float* values, const uint8_t* dones,
+                                   const float* bootstrap, int64_t T, int64_t E, double gamma, double lambda,
+                                   float* adv, float* ret, void* stream) {
+    if (T < 0 || E < 0) return fail(CONDUIT_EINVAL, "T and E must be >= 0");
+    if (E > kGaeMaxEnvs) return fail(CONDUIT_EINVAL, "E must be at most 2^19 environments");
+    if (T == 0 || E == 0) return CONDUIT_OK;
+    if (!rewards || !dones || !adv || !ret) return fail(CONDUIT_EINVAL, "rewards, dones, adv and ret must not be NULL");
+    if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
+    if (gae_outputs_overlap(rewards, values, dones, nullptr, nullptr, bootstrap, T, E, adv, ret))
+        return fail(CONDUIT_EINVAL, "adv and ret must overlap neither each other nor the inputs");
+    // the look-back path holds at most kLookMaxTiles tiles in the static table
+    auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+    const bool vec = E % 4 == 0 && al(rewards) && al(values) && al(bootstrap) && al(adv) && al(ret) &&
+                     (reinterpret_cast<uintptr_t>(dones) & 3) == 0;
+    const GaePlan p = plan_gae(T, E, vec);
+    if (p.path == GAE_LOOK_BACK && p.groups * p.segments > kLookMaxTiles)
+        return fail(CONDUIT_EINVAL, "rollout needs more look-back tiles than the static table holds (4,096)");
+    uint32_t* err = nullptr;
+    hipError_t e = gae_noalloc_err_words(&err);
+    if (e != hipSuccess) return hip_fail(e, "look-back table address (hipGetSymbolAddress)");
+    GaeArgs a{rewards, values, dones, bootstrap, T, E, gamma, lambda, adv, ret, nullptr, nullptr, err};
+    e = launch_gae(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "gae launch");
+    return CONDUIT_OK;
+}
+
 conduit_status conduit_gae_truncated(const float* rewards, const float* values, const uint8_t* dones,
                                      const uint8_t* truncated, const float* final_values, const float* bootstrap,
                                      int64_t T, int64_t E, double gamma, double lambda, float* adv, float* ret,
@@ -1013,14 +1039,29 @@ conduit_status conduit_sync_check(const conduit_buffer* b, void* stream) {
         DeviceGuard g(b->device);
         hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
         if (e != hipSuccess) return hip_fail(e, "stream synchronise");
-    } else {
-        hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
-        if (e != hipSuccess) return hip_fail(e, "stream synchronise");
+        return check_flags(slot);
     }
-    return check_flags(slot);
+    hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "stream synchronise");
+    conduit_status st = check_flags(0);
+    if (st != CONDUIT_OK) return st;
+    // the allocation-free GAE call's words, in the current GPU's static table
+    uint32_t w[kErrKinds];
+    e = gae_noalloc_read_errors(w);
+    if (e != hipSuccess) return hip_fail(e, "reading the static error words");
+    std::string msg;
+    for (int k = 0; k < kErrKinds; ++k) {
+        if (w[k]) {
+            if (!msg.empty()) msg += "; ";
+            msg += kErrText[k];
+        }
+    }
+    if (msg.empty()) return CONDUIT_OK;
+    return fail(CONDUIT_ESTATE, "device-side error flagged earlier (conduit_gae_noalloc): " + msg);
 }
 
 void conduit_clear_error(conduit_buffer* b) {
+    if (!b) (void)gae_noalloc_clear_errors();
     std::lock_guard<std::mutex> lk(g_err_mu);
     if (!g_err_host) return;
     const int slot = b ? b->err_slot : 0;

@@ -478,6 +478,13 @@ struct GaeArgs {
 
 hipError_t launch_gae(const GaeArgs& a, hipStream_t s);
 
+// The allocation-free GAE call keeps its sticky error words in the current
+// GPU's look-back table (k_gae.hip): their device address (set-up on first
+// use), and a synchronous read / clear of them.
+hipError_t gae_noalloc_err_words(uint32_t** err);
+hipError_t gae_noalloc_read_errors(uint32_t* host_words);
+hipError_t gae_noalloc_clear_errors();
+
 // n-step return targets of sampled slots (k_nstep.hip)
 struct NstepArgs {
     const int64_t* idx;

@@ -23,4 +23,7 @@ struct GaePlan {
 // `vec`: E % 4 == 0 and every row 16-byte aligned.
 GaePlan plan_gae(int64_t T, int64_t E, bool vec);
 
+// Tiles the per-GPU look-back table holds (the look-back path's limit).
+constexpr int64_t kLookMaxTiles = 4096;
+
 }  // namespace conduit

@@ -24,6 +24,8 @@
 // chunks along t, scanned with DPP inside each wavefront.
 #include <atomic>
 
+#include <mutex>
+
 #include "common.h"
 #include "gae_plan.h"
 
@@ -734,17 +736,27 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_replay(GaeArgs a, int32
 // the kernel finish.  Every published value is written with agent-scope atomic
 // stores and acknowledged before the flag is raised; readers use agent-scope
 // atomic loads.
-constexpr int kLookMaxTiles = 4096;
 constexpr int kLookSpin = 1 << 15;  // polls of one flag before a wait gives up (tens of ms)
 constexpr uint64_t kFlagMap = 1, kFlagA = 2;
 
-__device__ uint64_t g_look_flag[kLookMaxTiles];              // epoch << 2 | state
-__device__ uint64_t g_look_map[kLookMaxTiles][2][kSegEnvs];  // P, S of the segment (fp64 bits)
-__device__ uint64_t g_look_a[kLookMaxTiles][kSegEnvs];       // A at the segment's first step
+// The per-GPU look-back table, plus the sticky error words of the
+// allocation-free call (conduit_gae_noalloc).
+struct LookTable {
+    uint64_t flag[kLookMaxTiles];              // epoch << 2 | state
+    uint64_t map[kLookMaxTiles][2][kSegEnvs];  // P, S of the segment (fp64 bits)
+    uint64_t a[kLookMaxTiles][kSegEnvs];       // A at the segment's first step
+    uint32_t err[kErrKinds];
+};
 
-__global__ __launch_bounds__(kSegThreads) void k_gae_look_clear(int32_t tiles) {
+// Its storage: static device memory, zero when the code object loads, never
+// allocated, held by each GPU until the process ends (3.2 MB).  In host code
+// the name below is only a host-side stand-in: every host use goes through the
+// device address hipGetSymbolAddress returns for the current GPU (gae_table).
+static __device__ __align__(256) uint8_t scratch[sizeof(LookTable)];
+
+__global__ __launch_bounds__(kSegThreads) void k_gae_look_clear(LookTable* tab, int32_t tiles) {
     for (int i = threadIdx.x; i < tiles; i += kSegThreads)
-        __hip_atomic_store(&g_look_flag[i], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&tab->flag[i], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void put_f64(uint64_t* p, double x) {
@@ -755,7 +767,8 @@ __device__ __forceinline__ double get_f64(uint64_t* p) {
 }
 
 template <bool TRUNC, int L>
-__global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, int32_t groups, int32_t S, uint64_t epoch) {
+__global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, LookTable* tab, int32_t groups, int32_t S,
+                                                           uint64_t epoch) {
     constexpr int64_t Ts = (int64_t)kSegChunks * L;
     __shared__ double s_cin[kSegQuads][kV];
     int q, c;
@@ -779,15 +792,15 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, int32_t gro
 #pragma unroll
         for (int j = 0; j < kV; ++j) {
             if (last) {
-                put_f64(&g_look_a[me][q * kV + j], incl.S[j]);
+                put_f64(&tab->a[me][q * kV + j], incl.S[j]);
             } else {
-                put_f64(&g_look_map[me][0][q * kV + j], incl.P[j]);
-                put_f64(&g_look_map[me][1][q * kV + j], incl.S[j]);
+                put_f64(&tab->map[me][0][q * kV + j], incl.P[j]);
+                put_f64(&tab->map[me][1][q * kV + j], incl.S[j]);
             }
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // acknowledged device-wide
         if (q == 0)
-            __hip_atomic_store(&g_look_flag[me], epoch << 2 | (last ? kFlagA : kFlagMap), __ATOMIC_RELAXED,
+            __hip_atomic_store(&tab->flag[me], epoch << 2 | (last ? kFlagA : kFlagMap), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
     }
     if (!last) {  // uniform
@@ -800,7 +813,7 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, int32_t gro
                 const int64_t j = sj * groups + g;
                 uint64_t f = 0;
                 for (int it = 0; it < kLookSpin; ++it) {
-                    const uint64_t w = __hip_atomic_load(&g_look_flag[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const uint64_t w = __hip_atomic_load(&tab->flag[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     // the 8 quads of a segment take quad 0's reading (lane
                     // chunk % 8), so they agree on where their chains end
                     f = (uint64_t)__shfl((int)((w >> 2) == epoch ? (w & 3) : 0), (int)(threadIdx.x % kChunksPerWave),
@@ -811,15 +824,15 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, int32_t gro
                 if (f == kFlagMap) {
 #pragma unroll
                     for (int jj = 0; jj < kV; ++jj) {
-                        m.P[jj] = get_f64(&g_look_map[j][0][q * kV + jj]);
-                        m.S[jj] = get_f64(&g_look_map[j][1][q * kV + jj]);
+                        m.P[jj] = get_f64(&tab->map[j][0][q * kV + jj]);
+                        m.S[jj] = get_f64(&tab->map[j][1][q * kV + jj]);
                     }
                 } else {
                     // A published (or the wait gave up: flagged, A taken as 0)
 #pragma unroll
                     for (int jj = 0; jj < kV; ++jj) {
                         m.P[jj] = 0.0;
-                        m.S[jj] = f == kFlagA ? get_f64(&g_look_a[j][q * kV + jj]) : 0.0;
+                        m.S[jj] = f == kFlagA ? get_f64(&tab->a[j][q * kV + jj]) : 0.0;
                     }
                     if (f != kFlagA && q == 0) flag_error(a.err, ERR_GAE_WAIT);
                     stop = 1;
@@ -841,10 +854,10 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, int32_t gro
             for (int j = 0; j < kV; ++j) s_cin[q][j] = acc.S[j];
             if (S > kSegChunks + 1) {
 #pragma unroll
-                for (int j = 0; j < kV; ++j) put_f64(&g_look_a[me][q * kV + j], incl.P[j] * acc.S[j] + incl.S[j]);
+                for (int j = 0; j < kV; ++j) put_f64(&tab->a[me][q * kV + j], incl.P[j] * acc.S[j] + incl.S[j]);
                 asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                 if (q == 0)
-                    __hip_atomic_store(&g_look_flag[me], epoch << 2 | kFlagA, __ATOMIC_RELAXED,
+                    __hip_atomic_store(&tab->flag[me], epoch << 2 | kFlagA, __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_AGENT);
             }
         }
@@ -1125,30 +1138,96 @@ hipError_t launch_gae_split(const GaeArgs& a, int64_t groups, int L, hipStream_t
 }
 
 template <bool TRUNC>
-hipError_t launch_gae_look_l(const GaeArgs& a, int32_t groups, int32_t S, int L, uint64_t ep, hipStream_t s) {
+hipError_t launch_gae_look_l(const GaeArgs& a, LookTable* tab, int32_t groups, int32_t S, int L, uint64_t ep,
+                             hipStream_t s) {
     const dim3 grid((unsigned)(groups * S)), block(kSegThreads);
     switch (L) {
-        case 8: hipLaunchKernelGGL((k_gae_look<TRUNC, 8>), grid, block, 0, s, a, groups, S, ep); break;
-        case 4: hipLaunchKernelGGL((k_gae_look<TRUNC, 4>), grid, block, 0, s, a, groups, S, ep); break;
-        default: hipLaunchKernelGGL((k_gae_look<TRUNC, 2>), grid, block, 0, s, a, groups, S, ep); break;
+        case 8: hipLaunchKernelGGL((k_gae_look<TRUNC, 8>), grid, block, 0, s, a, tab, groups, S, ep); break;
+        case 4: hipLaunchKernelGGL((k_gae_look<TRUNC, 4>), grid, block, 0, s, a, tab, groups, S, ep); break;
+        default: hipLaunchKernelGGL((k_gae_look<TRUNC, 2>), grid, block, 0, s, a, tab, groups, S, ep); break;
     }
     return hipGetLastError();
 }
 
 std::atomic<uint64_t> g_look_epoch{0};  // epochs of the look-back table, 1, 2, ... (62 bits)
 
+// Device address of the current GPU's table, found once per GPU (with that GPU
+// current) and kept for the process.
+constexpr int kMaxGpus = 64;
+static std::mutex g_table_mu;
+static LookTable* g_table[kMaxGpus] = {};
+
+static hipError_t gae_table(LookTable** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxGpus) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_table_mu);
+    if (!g_table[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_table[dev] = static_cast<LookTable*>(p);
+    }
+    *out = g_table[dev];
+    return hipSuccess;
+}
+
 hipError_t launch_gae_look(const GaeArgs& a, int32_t groups, int32_t S, int L, hipStream_t s) {
+    // one segment (the short path) uses no table; split rollouts at most the
+    // table's tiles (the plan never asks for more)
+    if (S > 1 && (int64_t)groups * S > kLookMaxTiles) return hipErrorInvalidValue;
+    LookTable* tab = nullptr;
+    hipError_t e = gae_table(&tab);
+    if (e != hipSuccess) return e;
     const uint64_t ep = (g_look_epoch.fetch_add(1) + 1) & ((1ull << 62) - 1);
     hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-    hipError_t e = hipStreamIsCapturing(s, &cap);
+    e = hipStreamIsCapturing(s, &cap);
     if (e != hipSuccess) return e;
     if (S > 1 && cap != hipStreamCaptureStatusNone) {  // replays repeat the epoch: clear the flags first
-        hipLaunchKernelGGL(k_gae_look_clear, dim3(1), dim3(kSegThreads), 0, s, groups * S);
+        hipLaunchKernelGGL(k_gae_look_clear, dim3(1), dim3(kSegThreads), 0, s, tab, groups * S);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    return a.truncated ? launch_gae_look_l<true>(a, groups, S, L, ep, s)
-                       : launch_gae_look_l<false>(a, groups, S, L, ep, s);
+    return a.truncated ? launch_gae_look_l<true>(a, tab, groups, S, L, ep, s)
+                       : launch_gae_look_l<false>(a, tab, groups, S, L, ep, s);
+}
+
+hipError_t gae_noalloc_err_words(uint32_t** err) {
+    LookTable* tab = nullptr;
+    hipError_t e = gae_table(&tab);
+    if (e == hipSuccess) *err = tab->err;
+    return e;
+}
+
+hipError_t gae_noalloc_read_errors(uint32_t* host_words) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    LookTable* tab = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_table_mu);
+        tab = dev >= 0 && dev < kMaxGpus ? g_table[dev] : nullptr;
+    }
+    if (!tab) {  // no allocation-free call on this GPU yet: nothing flagged
+        for (int k = 0; k < kErrKinds; ++k) host_words[k] = 0;
+        return hipSuccess;
+    }
+    return hipMemcpy(host_words, tab->err, sizeof(uint32_t) * kErrKinds, hipMemcpyDeviceToHost);
+}
+
+hipError_t gae_noalloc_clear_errors() {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    LookTable* tab = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_table_mu);
+        tab = dev >= 0 && dev < kMaxGpus ? g_table[dev] : nullptr;
+    }
+    if (!tab) return hipSuccess;
+    const uint32_t zero[kErrKinds] = {};
+    return hipMemcpy(tab->err, zero, sizeof(zero), hipMemcpyHostToDevice);
 }
 
 GaePlan plan_gae(int64_t T, int64_t E, bool vec) {
