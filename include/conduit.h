@@ -670,11 +670,12 @@ typedef struct conduit_sched_mode {
  * overlap_ing, overlap_del, i_ing, i_del (each ascending, the last fastest);
  * the first of equal minima wins.  If `all` is not NULL it receives every
  * mode in that order (4 * n_ing * n_del entries, caller-owned).
- * On-policy, App. E's fractional case applies on all of (0, 1]: a rollout
- * must be ingested, and a batch delivered, within its own iteration, so only
- * the part of the operator that is not its last invocation can hide; at g = 1
- * nothing does (the g >= 1 case of App. E describes off-policy batching
- * across iterations).
+ * On-policy, App. E's fractional case applies on all of (0, 1]: App. C
+ * Invariant 2 allows on-policy pipelining only within an iteration, so a
+ * rollout must be ingested, and a batch delivered, within its own iteration
+ * and only the part of the operator that is not its last invocation can hide;
+ * at g = 1 nothing does (the g >= 1 case of App. E describes off-policy
+ * batching across iterations).
  * Errors: EINVAL (NULL costs/best, n_ing or n_del < 1, NULL arrays, a
  * granularity <= 0, or > 1 on-policy, a negative or non-finite time).
  */

@@ -22,7 +22,8 @@ import itertools
 def gamma(g, on_policy=False):
     """App. E: the overlappable fraction of the per-unit cost.  Off-policy
     batches (g >= 1) can hide all of it, fractions only 1 - g.  Reading: on
-    policy every g is a fraction of the current iteration (g <= 1), so the
+    policy every g is a fraction of the current iteration (g <= 1; App. C
+    Invariant 2 allows pipelining only within the iteration), so the
     fractional case is taken up to g = 1."""
     if g >= 1 and not on_policy:
         return 1.0

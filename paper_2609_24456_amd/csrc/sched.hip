@@ -11,8 +11,9 @@ namespace {
 
 // gamma(g) of App. E: an overlapped off-policy batch (g >= 1) can hide its whole
 // per-unit cost; a pipelined fraction only the part not yet exposed.  On-policy
-// every granularity is a fraction of the current iteration's work (g <= 1),
-// so the fractional case holds up to g = 1, which hides nothing.
+// every granularity is a fraction of the current iteration's work (g <= 1):
+// App. C Invariant 2 allows pipelining only within the iteration, so the
+// fractional case holds up to g = 1, whose single invocation hides nothing.
 double overlappable(double g, bool on_policy) { return !on_policy && g >= 1.0 ? 1.0 : 1.0 - g; }
 
 // exposed latency of one path: neighbour stage (rollout or update) plus the

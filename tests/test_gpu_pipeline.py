@@ -218,3 +218,95 @@ def test_onpolicy_loop_rejects_bad_configurations():
         cd.conduit_run_onpolicy(buf.handle, lp, None, None)
     assert e.value.status == cd.EINVAL
     buf.close()
+
+
+def _standin_us_per_work(stream):
+    L = cd.lib()
+    s = C.c_void_p(stream.cuda_stream)
+    L.conduit_standin(100_000, s)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        e0.record()
+        L.conduit_standin(400_000, s)
+        e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / 400_000
+
+
+def test_onpolicy_whole_rollout_ingestion_overlaps_nothing_on_the_executor():
+    """The reading that an on-policy ingestion of the whole rollout (g = 1)
+    hides nothing when overlapped, measured on the executor rather than taken
+    from the model.  App. C Invariant 2 lets on-policy training pipeline only
+    within its own iteration: the g = 1 ingestion is one invocation that needs
+    the rollout's last slice and must end before that iteration's delivery, so
+    there is no rollout left to run beside it.  Taken at g >= 1, App. E would
+    instead predict that overlap hides min(T_rollout, T_ing(1)).  On a rollout
+    whose ingestion costs over 50 us, the overlapped mode must not come out
+    faster than the inline one by half of that cost."""
+    print("onpolicy: g = 1 ingestion inline vs overlapped, 64 envs x 256 steps of 3x84x84", flush=True)
+    L = cd.lib()
+    T, E, M, iters = 256, 64, 8, 3
+    shape = (3, 84, 84)
+    row = int(np.prod(shape))
+    U = T * E
+    rng = np.random.default_rng(31)
+    obs = torch.randint(0, 256, (iters, U, row), dtype=torch.uint8, device="cuda")
+    d = {k: dev(v) for k, v in dict(
+        rew=rng.standard_normal((iters, U)).astype(np.float32), val=rng.standard_normal((iters, U)).astype(np.float32),
+        done=(rng.random((iters, U)) < 0.01).astype(np.uint8), boot=rng.standard_normal((iters, E)).astype(np.float32),
+        perm=np.stack([rng.permutation(U) for _ in range(iters)]).astype(np.int64)).items()}
+    buf = cd.ReplayBuffer(U, shape, torch.uint8, prioritized=False, action_bytes=0)
+    adv = torch.empty(U, dtype=torch.float32, device="cuda")
+    ret = torch.empty(U, dtype=torch.float32, device="cuda")
+    out = torch.empty((iters, U, row), dtype=torch.float32, device="cuda")
+    out_adv = torch.empty((iters, U), dtype=torch.float32, device="cuda")
+    out_ret = torch.empty((iters, U), dtype=torch.float32, device="cuda")
+    xf = cd.transform(cd.XF_U8_F32)
+    comp, exp = torch.cuda.Stream(), torch.cuda.Stream()
+    upw = _standin_us_per_work(comp)
+    work = (int(600.0 / upw), int(800.0 / upw))  # rollout 600 us, update 800 us per iteration
+
+    def loop(overlap_ing):
+        lp = cd.OnpolicyLoop()
+        lp.overlap_ing, lp.ing_slices, lp.overlap_del, lp.minibatches = overlap_ing, M, 0, M
+        lp.iters, lp.steps, lp.envs = iters, T, E
+        lp.rollout_work, lp.update_work = work
+        lp.obs, lp.reward, lp.value, lp.done = obs.data_ptr(), d["rew"].data_ptr(), d["val"].data_ptr(), \
+            d["done"].data_ptr()
+        lp.bootstrap, lp.gamma, lp.lam, lp.perm = d["boot"].data_ptr(), 0.99, 0.95, d["perm"].data_ptr()
+        lp.xf = C.pointer(xf)
+        lp.adv, lp.ret = adv.data_ptr(), ret.data_ptr()
+        lp.out_obs, lp.out_adv, lp.out_ret = out.data_ptr(), out_adv.data_ptr(), out_ret.data_ptr()
+        # the GPU starts behind a stand-in, so the loop's events time the GPU
+        # and not the host's enqueue
+        L.conduit_standin(int(iters * 3000.0 / upw), C.c_void_p(comp.cuda_stream))
+        ms, log = cd.conduit_run_onpolicy(buf.handle, lp, comp, exp)
+        assert [op for op in log if op[0] == cd.OP_INGEST] == [(cd.OP_INGEST, i, 0, M) for i in range(iters)]
+        return ms * 1e3 / iters
+
+    # the cost of the g = 1 ingestion: all U rows in one call, alone
+    tr = cd.Transitions()
+    tr.n, tr.obs = U, obs[0].data_ptr()
+    tr.reward, tr.done = d["rew"][0].data_ptr(), d["done"][0].data_ptr()
+    s = C.c_void_p(comp.cuda_stream)
+    assert L.conduit_ingest(buf.handle, C.byref(tr), s) == 0
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(comp):
+        e0.record()
+        for _ in range(4):
+            assert L.conduit_ingest(buf.handle, C.byref(tr), s) == 0
+        e1.record()
+    torch.cuda.synchronize()
+    t_ing1 = e0.elapsed_time(e1) * 1e3 / 4
+    assert buf.info().head == 0  # every ingest filled the ring exactly
+    loop(0)  # warm-up
+    inline = min(loop(0) for _ in range(2))
+    overlapped = min(loop(1) for _ in range(2))
+    print(f"T_ing(1) = {t_ing1:.1f} us; iteration inline {inline:.1f} us, overlapped {overlapped:.1f} us",
+          flush=True)
+    assert t_ing1 > 50.0
+    assert overlapped - inline > -0.5 * t_ing1, (inline, overlapped, t_ing1)
+    assert buf.sync_check() == cd.OK and cd.conduit_sync_check() == cd.OK, cd.last_error()
+    buf.close()

@@ -87,8 +87,12 @@ def test_mode_count_order_and_ties():
 
 
 def test_on_policy_whole_rollout_overlap_hides_nothing():
-    # on-policy the g = 1 ingestion is the iteration's last invocation: overlap
-    # only adds the synchronisation (off-policy the same g hides fully)
+    # on-policy the g = 1 ingestion is the iteration's last invocation (App. C
+    # Invariant 2: pipelining only within the iteration), so overlap only adds
+    # the synchronisation (off-policy the same g hides fully).  This states the
+    # model's reading; what pins it is the measurement on the executor,
+    # test_onpolicy_whole_rollout_ingestion_overlaps_nothing_on_the_executor
+    # (GPU), and the limit below.
     on = osch.modes(100.0, 200.0, [1.0], [40.0], [1.0], [30.0], 3.0, 4.0, on_policy=True)
     off = osch.modes(100.0, 200.0, [1.0], [40.0], [1.0], [30.0], 3.0, 4.0)
     seq_on = next(m for m in on if m["overlap_ing"] == 0 and m["overlap_del"] == 0)
@@ -97,6 +101,20 @@ def test_on_policy_whole_rollout_overlap_hides_nothing():
     assert ov_on["t_del_path"] == pytest.approx(seq_on["t_del_path"] + 4.0)
     ov_off = next(m for m in off if m["overlap_ing"] == 1 and m["overlap_del"] == 1)
     assert ov_off["t_ing_path"] == pytest.approx(100.0 + 3.0)
+
+
+def test_on_policy_whole_rollout_is_the_limit_of_the_fractional_case():
+    # App. E's fractional case hides (1 - g) min(stage, per-unit cost); the
+    # on-policy value at g = 1 is the limit of that expression as g -> 1 from
+    # below, computed here from the formula the paper prints for 0 < g < 1
+    t_roll, t_ing1, sync = 100.0, 40.0, 3.0
+    at_one = osch.modes(t_roll, 200.0, [1.0], [t_ing1], [1.0], [30.0], sync, 4.0, on_policy=True)
+    ov = next(m for m in at_one if m["overlap_ing"] == 1 and m["overlap_del"] == 0)
+    for k in (10, 20, 40):
+        g = 1.0 - 2.0 ** -k
+        per_unit = t_ing1 / 1.0  # T(g) / g with T(g) = g * T(1): the per-unit cost of a linear operator
+        limit = t_roll + per_unit + sync - (1.0 - g) * min(t_roll, per_unit)
+        assert ov["t_ing_path"] == pytest.approx(limit, abs=t_roll * 2.0 ** -k * 2)
 
 
 @pytest.mark.parametrize("M", [2, 4, 8])
