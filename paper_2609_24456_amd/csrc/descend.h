@@ -57,23 +57,31 @@ struct Descent {
 // level below the root's children -- at most PRE groups of 64 entries, one
 // group per child of the root -- is loaded in that same round trip and the
 // descent selects the group in registers, saving one round trip (the launcher
-// picks PRE from the tree's shape).  All lanes return the same result.
-template <int PRE>
+// picks PRE from the tree's shape).  The tree's depth is a template parameter
+// (the launcher dispatches on it): every level pointer is then read from the
+// kernel arguments at a constant offset, all at kernel start, where a depth
+// known only at run time made each level's pointer a dependent load in front
+// of that level's nodes (about 0.5 us of a DQN batch's descent).  All lanes
+// return the same result.
+template <int PRE, int DEPTH>
 __device__ __forceinline__ Descent tree_descend(const TreeView& tr, const uint64_t* uniforms, int64_t k, const DivB& dv) {
+    static_assert(DEPTH >= 1 && DEPTH <= kMaxLevels, "tree depth");
+    static_assert(PRE == 0 || DEPTH >= 2, "the prefetched level lies two below the root");
+    constexpr int top = DEPTH;
     const int lane = lane_id();
-    const int top = tr.depth;
     const uint64_t Q = tr.level[top][0];
     const uint64_t u = uniforms[k];
     uint64_t v = top == 1 ? (uint64_t)tr.leaves[lane] : tr.level[top - 1][lane];
     uint64_t pre[PRE > 0 ? PRE : 1];
     if constexpr (PRE > 0) {
-        // top >= 2 and 1 <= nodes[top - 1] <= PRE (launcher); groups past the
-        // last re-read group 0 so that every load is unconditional
+        // 1 <= nodes[top - 1] <= PRE (launcher); groups past the last re-read
+        // group 0 so that every load is unconditional
         const int groups = (int)tr.nodes[top - 1];
 #pragma unroll
         for (int g = 0; g < PRE; ++g) {
             const int64_t c = (int64_t)(g < groups ? g : 0) * kFanout + lane;
-            pre[g] = top == 2 ? (uint64_t)tr.leaves[c] : tr.level[top - 2][c];
+            if constexpr (top == 2) pre[g] = (uint64_t)tr.leaves[c];
+            else pre[g] = tr.level[top - 2][c];
         }
     }
     Descent r{-1, 0u, false};
@@ -84,6 +92,7 @@ __device__ __forceinline__ Descent tree_descend(const TreeView& tr, const uint64
     const uint64_t qh = div_b(dv, h), rh = h - qh * dv.d;
     uint64_t t = kk * qQ + qh + div_b(dv, kk * rQ + rh);
     uint64_t node = 0;
+#pragma unroll
     for (int l = top; l >= 1; --l) {
         if (l != top) {
             if (PRE > 0 && l == top - 1) {
@@ -105,6 +114,30 @@ __device__ __forceinline__ Descent tree_descend(const TreeView& tr, const uint64
     }
     r.slot = (int64_t)node;
     return r;
+}
+
+// Depths a capacity of at most 2^31 - 1 slots gives a 64-ary tree.
+constexpr int kMaxDescentDepth = 6;
+
+// Calls f.template operator()<PRE, DEPTH>() for the tree's prefetch width and
+// depth (compile-time values for tree_descend).
+template <typename F>
+hipError_t with_descent_shape(const TreeView& tr, int pre, F&& f) {
+    switch (tr.depth) {
+        case 1: return f.template operator()<0, 1>();
+#define CONDUIT_DEPTH_CASE(D)                                        \
+        case D:                                                      \
+            if (pre == 4) return f.template operator()<4, D>();      \
+            if (pre == 16) return f.template operator()<16, D>();    \
+            return f.template operator()<0, D>();
+        CONDUIT_DEPTH_CASE(2)
+        CONDUIT_DEPTH_CASE(3)
+        CONDUIT_DEPTH_CASE(4)
+        CONDUIT_DEPTH_CASE(5)
+        CONDUIT_DEPTH_CASE(6)
+#undef CONDUIT_DEPTH_CASE
+        default: return hipErrorInvalidValue;
+    }
 }
 
 // The PRE of tree_descend for a tree: how many groups of the level under the

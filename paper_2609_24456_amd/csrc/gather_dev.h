@@ -149,11 +149,11 @@ __device__ __forceinline__ Item decode(const GatherArgs& a, int64_t it, int bpf,
 template <int XF, bool NT = false>
 __device__ __forceinline__ void issue(const GatherArgs& a, const Item& t, int64_t i,
                                       typename UnitOf<XF>::T (&v)[kUnroll], int32_t& si, int32_t& sj, uint32_t& ei,
-                                      uint32_t& ej) {
+                                      uint32_t& ej, int tid) {
     typedef typename UnitOf<XF>::T U;
     const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
     const U* __restrict__ src = reinterpret_cast<const U*>(a.src + t.j * a.row_bytes);
-    const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + threadIdx.x;
+    const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + tid;
 #pragma unroll
     for (int r = 0; r < kUnroll; ++r) {
         const int64_t u = u0 + (int64_t)r * kThreads;
@@ -172,10 +172,11 @@ __device__ __forceinline__ void issue(const GatherArgs& a, const Item& t, int64_
 
 template <int XF, bool NT, bool PIN>
 __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const typename UnitOf<XF>::T (&v)[kUnroll],
-                                       int32_t si, int32_t sj, uint32_t ei, uint32_t ej, const uint16_t* lut) {
+                                       int32_t si, int32_t sj, uint32_t ei, uint32_t ej, const uint16_t* lut,
+                                       int tid) {
     const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
     const bool valid = t.d == 0 ? t.ok : (t.ok & (t.d <= si) & (ei == ej) & (sj == si - t.d));
-    const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + threadIdx.x;
+    const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + tid;
     const int64_t out_unit0 = (t.b * a.stack + t.k) * units;
     // Every conversion first, branch-free (an invalid frame is zeroed by a
     // select), then the stores.  With PIN the empty asm statements keep the
@@ -261,14 +262,15 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
 }
 
 
-// The row's scalar columns, one column word per lane: every load before any
-// store (the row's slot is known, so this is one memory round trip).
-__device__ __forceinline__ void row_scalars(const GatherArgs& a, int64_t b, int64_t i) {
+// The row's scalar columns, one column word per lane (tid of a 256-lane group):
+// every load before any store (the row's slot is known, so this is one memory
+// round trip).
+__device__ __forceinline__ void row_scalars(const GatherArgs& a, int64_t b, int64_t i, int tid) {
     const bool ok = i >= 0 && i < a.limit;
     const int64_t s = ok ? i : 0;
     const bool words = (a.action_bytes & 3) == 0;
     const int na = a.out_action && a.action_bytes > 0 ? (words ? a.action_bytes >> 2 : a.action_bytes) : 0;
-    for (int t = threadIdx.x; t < na + 2; t += kThreads) {
+    for (int t = tid; t < na + 2; t += kThreads) {
         if (t < na) {
             if (words) {
                 const uint32_t v = reinterpret_cast<const uint32_t*>(a.action + s * a.action_bytes)[t];
@@ -292,17 +294,17 @@ __device__ __forceinline__ void row_scalars(const GatherArgs& a, int64_t b, int6
 }
 
 // rows of at most this many work items take the fused kernels (a sample's
-// workgroups find its slot themselves and gather two items each)
+// workgroup finds its slot itself and its two 256-lane halves share the items)
 constexpr int64_t kFusedMaxItemsPerRow = 8;
 
 // The work items of row b (the slot i, or out of range for a zero row) that
-// workgroup `part` of the row's `wgs` owns, two per workgroup when the row has
-// more than two, double-buffered: the next item's loads are issued before the
-// current item's stores.  The row's first workgroup also writes its scalar
-// columns.
+// 256-lane group `part` of the row's `wgs` owns (tid: the lane in the group),
+// two per group when the row has more than two, double-buffered: the next
+// item's loads are issued before the current item's stores.  The row's first
+// group also writes its scalar columns.
 template <int XF, bool NT_LOADS = false>
 __device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int part, int64_t wgs, int32_t bpf,
-                                           int64_t i, const uint16_t* lut) {
+                                           int64_t i, const uint16_t* lut, int tid) {
     const bool owner = part == 0;
     const int64_t per_row = (int64_t)bpf * a.stack;
     const int64_t per_wg = (per_row + wgs - 1) / wgs;
@@ -310,28 +312,28 @@ __device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int p
     int64_t it_end = it0 + per_wg;
     if (it_end > (b + 1) * per_row) it_end = (b + 1) * per_row;
     if (it0 >= it_end) {
-        if (owner) row_scalars(a, b, i);
+        if (owner) row_scalars(a, b, i, tid);
         return;
     }
     typename UnitOf<XF>::T va[kUnroll], vb[kUnroll];
     int32_t sia = 0, sja = 0, sib = 0, sjb = 0;
     uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
     Item ta = decode(a, it0, bpf, i), tb;
-    issue<XF, NT_LOADS>(a, ta, i, va, sia, sja, eia, eja);
-    if (owner) row_scalars(a, b, i);
+    issue<XF, NT_LOADS>(a, ta, i, va, sia, sja, eia, eja, tid);
+    if (owner) row_scalars(a, b, i, tid);
     for (int64_t it = it0; it < it_end; it += 2) {
         const bool has_b = it + 1 < it_end;  // uniform
         if (has_b) {
             tb = decode(a, it + 1, bpf, i);
-            issue<XF, NT_LOADS>(a, tb, i, vb, sib, sjb, eib, ejb);
+            issue<XF, NT_LOADS>(a, tb, i, vb, sib, sjb, eib, ejb, tid);
         }
-        finish<XF, true, false>(a, ta, va, sia, sja, eia, eja, lut);
+        finish<XF, true, false>(a, ta, va, sia, sja, eia, eja, lut, tid);
         if (!has_b) break;
         if (it + 2 < it_end) {
             ta = decode(a, it + 2, bpf, i);
-            issue<XF, NT_LOADS>(a, ta, i, va, sia, sja, eia, eja);
+            issue<XF, NT_LOADS>(a, ta, i, va, sia, sja, eia, eja, tid);
         }
-        finish<XF, true, false>(a, tb, vb, sib, sjb, eib, ejb, lut);
+        finish<XF, true, false>(a, tb, vb, sib, sjb, eib, ejb, lut, tid);
     }
 }
 

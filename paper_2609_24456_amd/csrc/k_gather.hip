@@ -56,8 +56,8 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
     typename UnitOf<XF>::T v[kUnroll];
     int32_t si = 0, sj = 0;
     uint32_t ei = 0, ej = 0;
-    issue<XF>(a, t, i, v, si, sj, ei, ej);
-    finish<XF, NT, true>(a, t, v, si, sj, ei, ej, lut);
+    issue<XF>(a, t, i, v, si, sj, ei, ej, threadIdx.x);
+    finish<XF, NT, true>(a, t, v, si, sj, ei, ej, lut, threadIdx.x);
 }
 
 // Persistent workgroups walk the items with a stride of the grid.  Two register
@@ -86,22 +86,22 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
     uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
     Item ta = decode(a, it, bpf, i0), tb;
     if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_index(a);
-    issue<XF>(a, ta, i0, va, sia, sja, eia, eja);
+    issue<XF>(a, ta, i0, va, sia, sja, eia, eja, threadIdx.x);
     while (true) {
         tb = decode(a, clampi(itn), bpf, i1);
-        issue<XF>(a, tb, i1, vb, sib, sjb, eib, ejb);
+        issue<XF>(a, tb, i1, vb, sib, sjb, eib, ejb, threadIdx.x);
         int64_t itnn = itn + G;
         int64_t i2 = a.idx[clampi(itnn) / per_row];
-        finish<XF, NT, false>(a, ta, va, sia, sja, eia, eja, lut);
+        finish<XF, NT, false>(a, ta, va, sia, sja, eia, eja, lut, threadIdx.x);
         if (itn >= n_items) break;
         if (!tb.ok && threadIdx.x == 0 && tb.part == 0 && tb.k == a.stack - 1) flag_index(a);
         itn = itnn;
         i1 = i2;
         ta = decode(a, clampi(itn), bpf, i1);
-        issue<XF>(a, ta, i1, va, sia, sja, eia, eja);
+        issue<XF>(a, ta, i1, va, sia, sja, eia, eja, threadIdx.x);
         itnn = itn + G;
         i2 = a.idx[clampi(itnn) / per_row];
-        finish<XF, NT, false>(a, tb, vb, sib, sjb, eib, ejb, lut);
+        finish<XF, NT, false>(a, tb, vb, sib, sjb, eib, ejb, lut, threadIdx.x);
         if (itn >= n_items) break;
         if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_index(a);
         itn = itnn;

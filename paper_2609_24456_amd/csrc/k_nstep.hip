@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kThreads) void k_nstep_gather(NstepArgs na, GatherA
         build_lut(a, lut, kWave, kThreads - kWave);
     }
     __syncthreads();
-    gather_row<XF>(a, b, part, wgs, bpf, s_slot, lut);
+    gather_row<XF>(a, b, part, wgs, bpf, s_slot, lut, threadIdx.x);
 }
 
 template <int XF>

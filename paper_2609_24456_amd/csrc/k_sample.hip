@@ -22,11 +22,11 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * kWave;
 
-template <int PRE>
+template <int PRE, int DEPTH>
 __global__ __launch_bounds__(kThreads) void k_sample(SampleArgs a, DivB dv) {
     const int64_t k = (int64_t)blockIdx.x * kWaves + threadIdx.x / kWave;
     if (k < a.batch) {  // wave-uniform
-        const Descent d = tree_descend<PRE>(a.tree, a.uniforms, k, dv);
+        const Descent d = tree_descend<PRE, DEPTH>(a.tree, a.uniforms, k, dv);
         if (lane_id() == 0) {
             a.idx_out[k] = d.slot;
             // the sampled leaf is parked in the weight slot for the weights block
@@ -43,19 +43,23 @@ constexpr int kWThreads = 1024;
 
 __global__ __launch_bounds__(kWThreads) void k_is_weights(WeightsArgs a) { is_weights_block<kWThreads>(a); }
 
+// the sampler grid for a tree of PRE prefetched groups and depth DEPTH
+struct DescendLaunch {
+    const SampleArgs& a;
+    DivB dv;
+    hipStream_t s;
+    template <int PRE, int DEPTH>
+    hipError_t operator()() const {
+        const int64_t blocks = (a.batch + kWaves - 1) / kWaves;
+        hipLaunchKernelGGL((k_sample<PRE, DEPTH>), dim3((unsigned)blocks), dim3(kThreads), 0, s, a, dv);
+        return hipGetLastError();
+    }
+};
+
 }  // namespace
 
 hipError_t launch_descend(const SampleArgs& a, hipStream_t s) {
-    const int64_t blocks = (a.batch + kWaves - 1) / kWaves;
-    const DivB dv = make_divb((uint64_t)a.batch);
-    const int pre = descend_prefetch(a.tree);
-    if (pre == 4)
-        hipLaunchKernelGGL(k_sample<4>, dim3((unsigned)blocks), dim3(kThreads), 0, s, a, dv);
-    else if (pre == 16)
-        hipLaunchKernelGGL(k_sample<16>, dim3((unsigned)blocks), dim3(kThreads), 0, s, a, dv);
-    else
-        hipLaunchKernelGGL(k_sample<0>, dim3((unsigned)blocks), dim3(kThreads), 0, s, a, dv);
-    return hipGetLastError();
+    return with_descent_shape(a.tree, descend_prefetch(a.tree), DescendLaunch{a, make_divb((uint64_t)a.batch), s});
 }
 
 hipError_t launch_sample(const SampleArgs& a, hipStream_t s) {
