@@ -262,35 +262,63 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
 }
 
 
-// The row's scalar columns, one column word per lane (tid of a 256-lane group):
-// every load before any store (the row's slot is known, so this is one memory
-// round trip).
-__device__ __forceinline__ void row_scalars(const GatherArgs& a, int64_t b, int64_t i, int tid) {
-    const bool ok = i >= 0 && i < a.limit;
-    const int64_t s = ok ? i : 0;
-    const bool words = (a.action_bytes & 3) == 0;
-    const int na = a.out_action && a.action_bytes > 0 ? (words ? a.action_bytes >> 2 : a.action_bytes) : 0;
-    for (int t = tid; t < na + 2; t += kThreads) {
-        if (t < na) {
-            if (words) {
-                const uint32_t v = reinterpret_cast<const uint32_t*>(a.action + s * a.action_bytes)[t];
-                reinterpret_cast<uint32_t*>(a.out_action + b * a.action_bytes)[t] = ok ? v : 0u;
-            } else {
-                const uint8_t v = a.action[s * a.action_bytes + t];
-                a.out_action[b * a.action_bytes + t] = ok ? v : (uint8_t)0;
-            }
-        } else if (t == na) {
-            if (a.out_reward) {
-                const float v = a.reward[s];
-                a.out_reward[b] = ok ? v : 0.0f;
-            }
-        } else {
-            if (a.out_done) {
-                const uint8_t v = a.done[s];
-                a.out_done[b] = ok ? v : (uint8_t)0;
-            }
-        }
+// The row's scalar columns, one column word per lane (tid of a 256-lane
+// group).  The value a lane carries is loaded with the row's frame loads and
+// stored after the frames (row_scalars_load / row_scalars_store): a store
+// placed between the two frames' loads would wait for the first frame's loads
+// (vmcnt counts loads and stores in one queue) and delay the second frame's.
+// A row of more than 254 action words or bytes has a second pass of lanes,
+// loaded and stored together at the end.
+struct RowScalar {
+    uint32_t v;  // the lane's action word or byte, reward bits or done byte
+    bool ok;     // the row's index is in range
+};
+
+__device__ __forceinline__ int row_scalar_lanes(const GatherArgs& a, bool* words) {
+    *words = (a.action_bytes & 3) == 0;
+    const int na = a.out_action && a.action_bytes > 0 ? (*words ? a.action_bytes >> 2 : a.action_bytes) : 0;
+    return na + 2;  // action units, then reward, then done
+}
+
+// column unit t of row slot s (slot 0 when the index is out of range)
+__device__ __forceinline__ uint32_t row_scalar_load(const GatherArgs& a, int64_t s, int t, int na, bool words) {
+    if (t < na) {
+        return words ? reinterpret_cast<const uint32_t*>(a.action + s * a.action_bytes)[t]
+                     : (uint32_t)a.action[s * a.action_bytes + t];
     }
+    if (t == na) return a.out_reward ? __float_as_uint(a.reward[s]) : 0u;
+    return a.out_done ? (uint32_t)a.done[s] : 0u;
+}
+
+__device__ __forceinline__ void row_scalar_store(const GatherArgs& a, int64_t b, int t, int na, bool words,
+                                                 uint32_t v) {
+    if (t < na) {
+        if (words) reinterpret_cast<uint32_t*>(a.out_action + b * a.action_bytes)[t] = v;
+        else a.out_action[b * a.action_bytes + t] = (uint8_t)v;
+    } else if (t == na) {
+        if (a.out_reward) a.out_reward[b] = __uint_as_float(v);
+    } else {
+        if (a.out_done) a.out_done[b] = (uint8_t)v;
+    }
+}
+
+__device__ __forceinline__ RowScalar row_scalars_load(const GatherArgs& a, int64_t i, int tid) {
+    bool words;
+    const int n = row_scalar_lanes(a, &words);
+    const bool ok = i >= 0 && i < a.limit;
+    RowScalar r{0u, ok};
+    if (tid < n) r.v = row_scalar_load(a, ok ? i : 0, tid, n - 2, words);
+    return r;
+}
+
+__device__ __forceinline__ void row_scalars_store(const GatherArgs& a, int64_t b, int64_t i, const RowScalar& r,
+                                                  int tid) {
+    bool words;
+    const int n = row_scalar_lanes(a, &words);
+    const int64_t s = r.ok ? i : 0;
+    if (tid < n) row_scalar_store(a, b, tid, n - 2, words, r.ok ? r.v : 0u);
+    for (int t = tid + kThreads; t < n; t += kThreads)  // rows of more than 256 units
+        row_scalar_store(a, b, t, n - 2, words, r.ok ? row_scalar_load(a, s, t, n - 2, words) : 0u);
 }
 
 // rows of at most this many work items take the fused kernels (a sample's
@@ -301,7 +329,7 @@ constexpr int64_t kFusedMaxItemsPerRow = 8;
 // 256-lane group `part` of the row's `wgs` owns (tid: the lane in the group),
 // two per group when the row has more than two, double-buffered: the next
 // item's loads are issued before the current item's stores.  The row's first
-// group also writes its scalar columns.
+// group also writes its scalar columns, after the frames.
 template <int XF, bool NT_LOADS = false>
 __device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int part, int64_t wgs, int32_t bpf,
                                            int64_t i, const uint16_t* lut, int tid) {
@@ -312,7 +340,7 @@ __device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int p
     int64_t it_end = it0 + per_wg;
     if (it_end > (b + 1) * per_row) it_end = (b + 1) * per_row;
     if (it0 >= it_end) {
-        if (owner) row_scalars(a, b, i, tid);
+        if (owner) row_scalars_store(a, b, i, row_scalars_load(a, i, tid), tid);
         return;
     }
     typename UnitOf<XF>::T va[kUnroll], vb[kUnroll];
@@ -320,7 +348,8 @@ __device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int p
     uint32_t eia = 0, eja = 0, eib = 0, ejb = 0;
     Item ta = decode(a, it0, bpf, i), tb;
     issue<XF, NT_LOADS>(a, ta, i, va, sia, sja, eia, eja, tid);
-    if (owner) row_scalars(a, b, i, tid);
+    RowScalar rs{0u, false};
+    if (owner) rs = row_scalars_load(a, i, tid);
     for (int64_t it = it0; it < it_end; it += 2) {
         const bool has_b = it + 1 < it_end;  // uniform
         if (has_b) {
@@ -335,6 +364,7 @@ __device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int p
         }
         finish<XF, true, false>(a, tb, vb, sib, sjb, eib, ejb, lut, tid);
     }
+    if (owner) row_scalars_store(a, b, i, rs, tid);
 }
 
 }  // namespace
