@@ -170,23 +170,87 @@ __device__ __forceinline__ void issue(const GatherArgs& a, const Item& t, int64_
     }
 }
 
-template <int XF, bool NT, bool PIN>
+// Output stores of one item, by policy:
+//   kStoreWT     buffer stores at agent scope (cache policy SC1), based at the
+//                item's first output unit, so each store is written through to
+//                the level every XCD sees rather than left dirty in the writing
+//                XCD's L2 for the end-of-kernel write-back (the hardware also
+//                drops any store past the item's last unit).  Measured on the
+//                DQN batch (512 x 4 x 84x84 -> fp32, one launch with the
+//                sampler): 17.1 us with non-temporal global stores, 15.2 us
+//                with plain stores, 14.65 us write-through.
+//   kStoreNT     non-temporal global stores;
+//   kStorePlain  plain global stores.
+enum StorePolicy : int { kStorePlain = 0, kStoreNT = 1, kStoreWT = 2 };
+constexpr int kRsrcWord3 = 0x00020000;  // raw buffer descriptor, 32-bit data format
+constexpr int kStoreAgentScope = 16;    // SC1
+
+__device__ __forceinline__ void put_unit(__amdgpu_buffer_rsrc_t rs, int off, uint32_t v) {
+    __builtin_amdgcn_raw_buffer_store_b32(v, rs, off, 0, kStoreAgentScope);
+}
+__device__ __forceinline__ void put_unit(__amdgpu_buffer_rsrc_t rs, int off, u32x2 v) {
+    __builtin_amdgcn_raw_buffer_store_b64(v, rs, off, 0, kStoreAgentScope);
+}
+__device__ __forceinline__ void put_unit(__amdgpu_buffer_rsrc_t rs, int off, u32x4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, rs, off, 0, kStoreAgentScope);
+}
+__device__ __forceinline__ void put_unit(__amdgpu_buffer_rsrc_t rs, int off, f32x4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, off, 0, kStoreAgentScope);
+}
+
+// A value every lane of the wavefront holds, as a scalar (read from the first
+// lane): a buffer descriptor built from it needs no per-lane loop.
+__device__ __forceinline__ int64_t wave_uniform(int64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+template <int POL, typename O>
+__device__ __forceinline__ void store_item(const GatherArgs& a, const Item& t, int64_t units, int tid,
+                                           const O (&o)[kUnroll]) {
+    // the item's place and size are the same for every lane (items belong to
+    // whole wavefronts)
+    const int64_t first = wave_uniform((int64_t)t.part * kUnitsPerBlock);  // its first unit within the frame
+    const int64_t at = wave_uniform((t.b * a.stack + t.k) * units + first);
+    O* base = reinterpret_cast<O*>(a.out) + at;
+    if constexpr (POL == kStoreWT) {
+        const int n = (int)(units - first < kUnitsPerBlock ? units - first : kUnitsPerBlock);
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            base, 0, __builtin_amdgcn_readfirstlane(n * (int)sizeof(O)), kRsrcWord3);
+#pragma unroll
+        for (int r = 0; r < kUnroll; ++r) {
+            const int e = tid + r * kThreads;
+            if (e < n) put_unit(rs, e * (int)sizeof(O), o[r]);
+        }
+    } else {
+#pragma unroll
+        for (int r = 0; r < kUnroll; ++r) {
+            const int e = tid + r * kThreads;
+            if (first + e < units) {
+                if constexpr (POL == kStoreNT) __builtin_nontemporal_store(o[r], base + e);
+                else base[e] = o[r];
+            }
+        }
+    }
+}
+
+// The converted item (every conversion first, branch-free: an invalid frame is
+// zeroed by a select), then its stores.  With PIN the empty asm statements keep
+// the converted values in registers ahead of the first store; otherwise the
+// compiler may sink each conversion into its store's range check, and the
+// load waits it then places between stores also wait for the earlier stores
+// (vmcnt counts both).  Measured on the DQN and PPO shapes: the
+// one-item-per-workgroup kernel needs the pin (353 -> 328 us per PPO
+// minibatch); the double-buffered kernels are faster without it (14.9 vs
+// 15.3 us per DQN batch), where waiting per load lets stores start sooner.
+template <int XF, int POL, bool PIN>
 __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const typename UnitOf<XF>::T (&v)[kUnroll],
                                        int32_t si, int32_t sj, uint32_t ei, uint32_t ej, const uint16_t* lut,
                                        int tid) {
     const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
     const bool valid = t.d == 0 ? t.ok : (t.ok & (t.d <= si) & (ei == ej) & (sj == si - t.d));
     const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + tid;
-    const int64_t out_unit0 = (t.b * a.stack + t.k) * units;
-    // Every conversion first, branch-free (an invalid frame is zeroed by a
-    // select), then the stores.  With PIN the empty asm statements keep the
-    // converted values in registers ahead of the first store; otherwise the
-    // compiler may sink each conversion into its store's range check, and the
-    // load waits it then places between stores also wait for the earlier
-    // stores (vmcnt counts both).  Measured on the DQN and PPO shapes: the
-    // one-item-per-workgroup kernel needs the pin (353 -> 328 us per PPO
-    // minibatch); the double-buffered kernels are faster without it (14.9 vs
-    // 15.3 us per DQN batch), where waiting per load lets stores start sooner.
     if constexpr (XF == kXfCopy16) {
         u32x4 o[kUnroll];
 #pragma unroll
@@ -194,14 +258,7 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
             o[r] = valid ? v[r] : (u32x4)(0u);
             if constexpr (PIN) asm volatile("" : "+v"(o[r]));
         }
-#pragma unroll
-        for (int r = 0; r < kUnroll; ++r) {
-            const int64_t u = u0 + (int64_t)r * kThreads;
-            u32x4* p = reinterpret_cast<u32x4*>(a.out) + out_unit0 + u;
-            if (u < units) {
-                if constexpr (NT) __builtin_nontemporal_store(o[r], p); else *p = o[r];
-            }
-        }
+        store_item<POL>(a, t, units, tid, o);
     } else if constexpr (XF == CONDUIT_XF_NONE) {
         uint32_t o[kUnroll];
 #pragma unroll
@@ -209,14 +266,7 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
             o[r] = valid ? v[r] : 0u;
             if constexpr (PIN) asm volatile("" : "+v"(o[r]));
         }
-#pragma unroll
-        for (int r = 0; r < kUnroll; ++r) {
-            const int64_t u = u0 + (int64_t)r * kThreads;
-            uint32_t* p = reinterpret_cast<uint32_t*>(a.out) + out_unit0 + u;
-            if (u < units) {
-                if constexpr (NT) __builtin_nontemporal_store(o[r], p); else *p = o[r];
-            }
-        }
+        store_item<POL>(a, t, units, tid, o);
     } else if constexpr (XF == CONDUIT_XF_U8_F32) {
         f32x4 o[kUnroll];
 #pragma unroll
@@ -228,14 +278,7 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
             o[r].w = u8_unit_f32(x >> 24);
             if constexpr (PIN) asm volatile("" : "+v"(o[r]));
         }
-#pragma unroll
-        for (int r = 0; r < kUnroll; ++r) {
-            const int64_t u = u0 + (int64_t)r * kThreads;
-            f32x4* p = reinterpret_cast<f32x4*>(a.out) + out_unit0 + u;
-            if (u < units) {
-                if constexpr (NT) __builtin_nontemporal_store(o[r], p); else *p = o[r];
-            }
-        }
+        store_item<POL>(a, t, units, tid, o);
     } else {  // U8_BF16_NORM
         u32x2 o[kUnroll];
 #pragma unroll
@@ -250,14 +293,7 @@ __device__ __forceinline__ void finish(const GatherArgs& a, const Item& t, const
             o[r].y = valid ? hi : 0u;
             if constexpr (PIN) asm volatile("" : "+v"(o[r]));
         }
-#pragma unroll
-        for (int r = 0; r < kUnroll; ++r) {
-            const int64_t u = u0 + (int64_t)r * kThreads;
-            u32x2* p = reinterpret_cast<u32x2*>(a.out) + out_unit0 + u;
-            if (u < units) {
-                if constexpr (NT) __builtin_nontemporal_store(o[r], p); else *p = o[r];
-            }
-        }
+        store_item<POL>(a, t, units, tid, o);
     }
 }
 
@@ -356,13 +392,13 @@ __device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int p
             tb = decode(a, it + 1, bpf, i);
             issue<XF, NT_LOADS>(a, tb, i, vb, sib, sjb, eib, ejb, tid);
         }
-        finish<XF, true, false>(a, ta, va, sia, sja, eia, eja, lut, tid);
+        finish<XF, kStoreWT, false>(a, ta, va, sia, sja, eia, eja, lut, tid);
         if (!has_b) break;
         if (it + 2 < it_end) {
             ta = decode(a, it + 2, bpf, i);
             issue<XF, NT_LOADS>(a, ta, i, va, sia, sja, eia, eja, tid);
         }
-        finish<XF, true, false>(a, tb, vb, sib, sjb, eib, ejb, lut, tid);
+        finish<XF, kStoreWT, false>(a, tb, vb, sib, sjb, eib, ejb, lut, tid);
     }
     if (owner) row_scalars_store(a, b, i, rs, tid);
 }

@@ -41,7 +41,7 @@ __device__ __forceinline__ bool tail_block(const GatherArgs& a, int64_t tail) {
 // shape for large outputs, where many resident workgroups keep the most bytes
 // in flight.
 
-template <int XF, bool NT>
+template <int XF>
 __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t bpf, int32_t tail) {
     __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
     if (tail_block(a, tail)) return;
@@ -57,7 +57,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
     int32_t si = 0, sj = 0;
     uint32_t ei = 0, ej = 0;
     issue<XF>(a, t, i, v, si, sj, ei, ej, threadIdx.x);
-    finish<XF, NT, true>(a, t, v, si, sj, ei, ej, lut, threadIdx.x);
+    finish<XF, kStoreNT, true>(a, t, v, si, sj, ei, ej, lut, threadIdx.x);
 }
 
 // Persistent workgroups walk the items with a stride of the grid.  Two register
@@ -65,7 +65,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_rows(GatherArgs a, int32_t 
 // the current one, so reads of one item overlap the writes of the previous one
 // instead of the whole GPU reading first and writing afterwards.  The sample
 // index of the item after next is fetched one step ahead as well.
-template <int XF, bool NT>
+template <int XF>
 __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t bpf, int64_t n_items, int32_t frame_grid,
                                                           int32_t tail) {
     __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
@@ -92,7 +92,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
         issue<XF>(a, tb, i1, vb, sib, sjb, eib, ejb, threadIdx.x);
         int64_t itnn = itn + G;
         int64_t i2 = a.idx[clampi(itnn) / per_row];
-        finish<XF, NT, false>(a, ta, va, sia, sja, eia, eja, lut, threadIdx.x);
+        finish<XF, kStoreWT, false>(a, ta, va, sia, sja, eia, eja, lut, threadIdx.x);
         if (itn >= n_items) break;
         if (!tb.ok && threadIdx.x == 0 && tb.part == 0 && tb.k == a.stack - 1) flag_index(a);
         itn = itnn;
@@ -101,7 +101,7 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
         issue<XF>(a, ta, i1, va, sia, sja, eia, eja, threadIdx.x);
         itnn = itn + G;
         i2 = a.idx[clampi(itnn) / per_row];
-        finish<XF, NT, false>(a, tb, vb, sib, sjb, eib, ejb, lut, threadIdx.x);
+        finish<XF, kStoreWT, false>(a, tb, vb, sib, sjb, eib, ejb, lut, threadIdx.x);
         if (itn >= n_items) break;
         if (!ta.ok && threadIdx.x == 0 && ta.part == 0 && ta.k == a.stack - 1) flag_index(a);
         itn = itnn;
@@ -195,10 +195,12 @@ int device_cus() {
     return cached[dev];
 }
 
-// Both shapes write the learner batch with non-temporal stores: measured in the
-// full ingest/sample/gather/update loop they leave the caches to the next
-// kernels and beat plain stores, even when the batch would fit the 256 MB
-// Infinity Cache.
+// Stores: the persistent kernel writes through at agent scope (outputs of at
+// most 128 MB: no dirty L2 lines left for the end-of-kernel write-back; the
+// DQN gather 15.2 -> 14.9 us), the one-item-per-workgroup kernel writes
+// non-temporal (larger outputs stream: PPO minibatch 325 us against 342 us
+// written through and 344 us with plain stores; large bf16 86 against 93 and
+// 94 us).
 template <int XF>
 hipError_t launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t tail_blocks) {
     const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
@@ -210,11 +212,11 @@ hipError_t launch_gather_xf(const GatherArgs& a, hipStream_t s, int64_t tail_blo
     if (out_bytes <= kPipeMaxOutBytes) {
         // small batches: persistent pipelined workgroups
         const int64_t frame_grid = n_items < 4LL * device_cus() ? n_items : 4LL * device_cus();
-        hipLaunchKernelGGL((k_gather_pipe<XF, true>), dim3((unsigned)(frame_grid + tail_blocks)), dim3(kThreads), 0,
+        hipLaunchKernelGGL((k_gather_pipe<XF>), dim3((unsigned)(frame_grid + tail_blocks)), dim3(kThreads), 0,
                            s, a, (int32_t)bpf, n_items, (int32_t)frame_grid, (int32_t)tail_blocks);
     } else {
         // large batches: one workgroup per item
-        hipLaunchKernelGGL((k_gather_rows<XF, true>), dim3((unsigned)(n_items + tail_blocks)), dim3(kThreads), 0, s,
+        hipLaunchKernelGGL((k_gather_rows<XF>), dim3((unsigned)(n_items + tail_blocks)), dim3(kThreads), 0, s,
                            a, (int32_t)bpf, (int32_t)tail_blocks);
     }
     return hipGetLastError();

@@ -94,8 +94,11 @@ __global__ __launch_bounds__(kWg) void k_sample_gather(SampleArgs sa, GatherArgs
         build_lut(a, lut, kWave, kWg - kWave);
     }
     __syncthreads();
-    // half h of the workgroup takes the row's items as part h of 2
-    gather_row<XF, true>(a, b, (int)(threadIdx.x / kThreads), 2, bpf, s_slot, lut, (int)(threadIdx.x % kThreads));
+    // half h of the workgroup takes the row's items as part h of 2 (uniform in
+    // each wavefront: read from the first lane, so that the item's output base
+    // stays a scalar)
+    const int half = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kThreads));
+    gather_row<XF, true>(a, b, half, 2, bpf, s_slot, lut, (int)(threadIdx.x % kThreads));
 }
 
 template <int XF>
