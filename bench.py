@@ -748,7 +748,7 @@ def bench_schedule(d=10000, t_stage_us=(100.0, 150.0), iters=64, gs=(1, 2, 4, 8)
                 r |= L.conduit_update_priorities(h, idx[j * B:].data_ptr(), p_d[j * B:].data_ptr(), B, stream)
             return r
         t_del.append(_b2b_ms([one] * 10) * 1e3)
-    comp, exp = torch.cuda.Stream(), torch.cuda.Stream()
+    comp, exp, co_run = _co_running_streams()
     t_hop, t_sync = cd.conduit_sync_cost_us(comp, exp, 200)
     best, modes = cd.conduit_schedule(t_roll, t_upd, list(gs), t_ing, list(gs), t_del, t_sync, t_sync)
     best_hop, _ = cd.conduit_schedule(t_roll, t_upd, list(gs), t_ing, list(gs), t_del, t_hop, t_hop)
@@ -770,6 +770,7 @@ def bench_schedule(d=10000, t_stage_us=(100.0, 150.0), iters=64, gs=(1, 2, 4, 8)
                     f"register-only compute stand-in (one workgroup per CU) for rollout and update",
         "profiled_us": {"t_rollout": t_roll, "t_update": t_upd, "t_sync": t_sync, "t_hop_unmet": t_hop,
                         "t_ing": dict(zip(map(str, gs), t_ing)), "t_del": dict(zip(map(str, gs), t_del))},
+        "streams_co_run_us": co_run,
     }
     out.update(_schedule_report(modes, best, measured, name, seq, t_roll + t_upd))
     out["model_choice_with_unmet_hop_as_t_sync"] = name(best_hop)
@@ -783,6 +784,54 @@ def _head_start(stream, us):
     import torch
     with torch.cuda.stream(stream):
         _gpu_delay(us)
+
+
+def _co_run_us(a, b, us=300.0):
+    """GPU time of about `us` of stand-in work on stream `a` alone, and of the
+    same work on `a` and on `b` at once (one workgroup per CU each, so two
+    streams that run concurrently take about as long as one): shows whether
+    the two streams of an overlapped schedule really overlap."""
+    import torch
+    from paper_2609_24456_amd import conduit as cd
+    _gpu_delay(1.0)  # calibrates the stand-in's rate
+    work = max(1, int(us / _DELAY_US_PER_WORK[0]))
+    cd.conduit_standin(work, a)
+    cd.conduit_standin(work, b)
+    torch.cuda.synchronize()
+
+    def run(both):
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record(a)
+        b.wait_event(e0)
+        cd.conduit_standin(work, a)
+        if both:
+            cd.conduit_standin(work, b)
+        e1.record(b)
+        a.wait_event(e1)
+        e2.record(a)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e2) * 1e3
+
+    return {"alone_us": min(run(False) for _ in range(3)), "both_us": min(run(True) for _ in range(3))}
+
+
+def _co_running_streams(tries=8):
+    """Two torch streams measured to run concurrently.  HIP serves every
+    stream of a process from a few hardware queues (4 here), shared among
+    all streams, torch's pool of 32 included, so two streams can land on one
+    queue and run one after the other, and an overlapped schedule on them
+    then hides nothing.  The first stream is kept; candidates for the second
+    are drawn from the pool until one co-runs with it (both stand-ins
+    together within 1.3x of one alone)."""
+    import torch
+    comp = torch.cuda.Stream()
+    for k in range(1, tries + 1):
+        exp = torch.cuda.Stream()
+        co = _co_run_us(comp, exp)
+        co["candidates_tried"] = k
+        if co["both_us"] < 1.3 * co["alone_us"]:
+            break
+    return comp, exp, co
 
 
 def _schedule_report(modes, best, measured, name, seq, stages):
@@ -908,7 +957,7 @@ def bench_schedule_onpolicy(T=256, E=64, M=8, iters=8, t_stage_us=(600.0, 800.0)
                 out.data_ptr() + o * row * 4, cols, co, 2, stream))
     _b2b_ms(calls)
     t_del = [_b2b_ms(calls) * 1e3]
-    comp, exp = torch.cuda.Stream(), torch.cuda.Stream()
+    comp, exp, co_run = _co_running_streams()
     t_hop, t_sync = cd.conduit_sync_cost_us(comp, exp, 200)
     best, modes = cd.conduit_schedule(t_roll, t_upd, g_ing, t_ing, g_del, t_del, t_sync, t_sync, on_policy=True)
     cd.conduit_run_onpolicy(buf.handle, loop_struct((0, M, 0), work), comp, exp)  # warm-up
@@ -931,6 +980,7 @@ def bench_schedule_onpolicy(T=256, E=64, M=8, iters=8, t_stage_us=(600.0, 800.0)
         "profiled_us": {"t_rollout": t_roll, "t_update": t_upd, "t_sync": t_sync, "t_hop_unmet": t_hop,
                         "t_gae": t_gae, "t_ing": {f"{j}/{M}": t for j, t in zip(range(1, M + 1), t_ing)},
                         "t_del": {f"1/{M}": t_del[0]}},
+        "streams_co_run_us": co_run,
     }
     out_d.update(_schedule_report(modes, best, measured, name, seq, t_roll + t_upd))
     return out_d

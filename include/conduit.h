@@ -741,6 +741,11 @@ conduit_status conduit_sync_cost_us(void* s1, void* s2, int32_t hops, double* ho
  *                    1: they run on the experience stream, the next group's
  *                    delivery issued during the learner's update (prefetch,
  *                    so it samples before this iteration's new priorities).
+ * Overlap hides work only if the two streams run concurrently.  HIP serves
+ * all of a process's streams from a few hardware queues, and two streams on
+ * one queue run one after the other: the loop is still correct then, but an
+ * overlapped mode only adds its synchronisation.  The caller picks the pair
+ * (e.g. by timing stand-in work on both at once against one alone).
  * Whatever the mode, the experience operators keep one fixed program order
  * (an operator issued on the other stream than its predecessor waits for the
  * predecessor's event), so the data produced does not depend on timing
