@@ -166,7 +166,7 @@ def test_sampling_frequencies_chi_square():
     r = _filled_replay(prio, alpha=(3, 5))
     leaves = np.array([oracle.leaf(int(p)) for p in prio], np.float64)
     counts = np.zeros(64)
-    batches, B = 4096, 64
+    batches, B = 1 << 16, 64  # 2^22 draws
     for _ in range(batches):
         idx, _ = r.sample(rng.integers(0, 1 << 64, size=B, dtype=np.uint64))
         counts += np.bincount(idx, minlength=64)
@@ -174,7 +174,7 @@ def test_sampling_frequencies_chi_square():
     stat = float(((counts - expect) ** 2 / expect).sum())
     assert stat < chi2.isf(1e-6, df=63), stat
     # leaves follow p^alpha, not p: the same counts are far from p-proportional
-    wrong = batches * B * prio / prio.sum()
+    wrong = batches * B * prio.astype(np.float64) / float(prio.sum())
     assert float(((counts - wrong) ** 2 / wrong).sum()) > chi2.isf(1e-6, df=63)
 
 
