@@ -378,9 +378,11 @@ conduit_status conduit_nstep(conduit_buffer* buf, const int64_t* idx, int64_t ba
  * dones uint8 [T,E]; bootstrap float [E] or NULL (0); adv, ret float [T,E]
  * outputs, which must not overlap the inputs.  Arithmetic in fp64 inside, fp32
  * out.
- * With E a multiple of 4 and 16-byte aligned float rows, a workgroup takes 32
- * environments of a rollout of at most 64 steps on its own; longer rollouts
- * are split along T across workgroups, in tiles of 32 environments: up
+ * A workgroup takes 32 environments of a rollout of at most 64 steps on its
+ * own; longer rollouts are split along T across workgroups, in tiles of 32
+ * environments (any E and any 4-byte aligned rows; 16-byte aligned rows with
+ * E a multiple of 4 take aligned vector accesses, the others 16-byte accesses
+ * at 4-byte alignment): up
  * to 4,096 tiles publish their segments' affine maps in a small per-GPU table
  * (static device memory, no allocation) and each composes the later ones.
  * Calls that overlap in time on one GPU share that table and race (their
@@ -444,7 +446,9 @@ conduit_status conduit_gae_truncated(const float* rewards, const float* values, 
  * four environments per lane (E % 4 == 0, aligned); 2 one tile of 32
  * environments per workgroup (T <= 64); 3 split along T, one launch with a
  * look-back over the later segments' maps (up to 4,096 tiles); 4 split along
- * T in three launches.  *chunk = steps per lane of a tile (2, 4 or 8; 0 for
+ * T in three launches.  Paths 2-4 take any E and either alignment; paths 0
+ * and 1 serve only rollouts that need more than 4,096 tiles and have at least
+ * 4,096 environments.  *chunk = steps per lane of a tile (2, 4 or 8; 0 for
  * paths 0 and 1).  Host only, nothing is enqueued.  Errors: EINVAL (T, E < 0,
  * NULL outputs).
  */

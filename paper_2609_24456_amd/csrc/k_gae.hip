@@ -10,16 +10,19 @@
 //   3. replays each chunk from that carry and writes A_t and R_t = A_t + V_t.
 // All arithmetic is fp64; outputs are rounded to fp32 once.  plan_gae picks
 // the kernels of a time-major call:
-//   * tiles of 32 environments x 32 chunks (E a multiple of 4, aligned rows):
-//     a rollout of at most 64 steps is one tile per workgroup
-//     (k_gae_look with one segment); a longer one is split along T into
-//     segments whose maps are joined by a decoupled look-back in one launch
-//     (k_gae_look), or, beyond its table, by three launches (k_gae_seg_*);
-//   * otherwise a workgroup owns 8 environments and walks the rollout in
-//     passes of 2048 steps: k_gae_v4 gives each lane 4 environments as 16-byte
-//     vectors and 16 steps (128 chunks per pass); k_gae (any E, any alignment)
-//     one environment and 32 steps (64 chunks per pass), lanes fastest over
-//     environments so every load instruction reads eight 32-byte runs.
+//   * tiles of 32 environments x 32 chunks: a rollout of at most 64 steps is
+//     one tile per workgroup (k_gae_look with one segment); a longer one is
+//     split along T into segments whose maps are joined by a decoupled
+//     look-back in one launch (k_gae_look), or, beyond its table, by three
+//     launches (k_gae_seg_*).  With E a multiple of 4 and aligned rows a lane
+//     moves its 4 environments as 16-byte vectors, otherwise one by one (any
+//     E, any alignment: the V4 template parameter);
+//   * wide rollouts beyond the table: a workgroup owns 8 environments and
+//     walks the rollout in passes of 2048 steps: k_gae_v4 gives each lane 4
+//     environments as 16-byte vectors and 16 steps (128 chunks per pass); k_gae
+//     (any E, any alignment) one environment and 32 steps (64 chunks per
+//     pass), lanes fastest over environments so every load instruction reads
+//     eight 32-byte runs.
 // Padded sequences [B, Lmax] (k_gae_packed): one workgroup per sequence, 256
 // chunks along t, scanned with DPP inside each wavefront.
 #include <atomic>
@@ -487,9 +490,35 @@ __device__ __forceinline__ int64_t tile_of_block() {
     return nb % 8 == 0 ? (int64_t)(blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : (int64_t)blockIdx.x;
 }
 
+// 16-byte vectors at 4-byte aligned addresses
+typedef float f32x4u __attribute__((ext_vector_type(4), aligned(4)));
+typedef uint32_t u32x4u __attribute__((ext_vector_type(4), aligned(4)));
+
+// element j of the result is element min(j + sh, 3) of x (sh in 0..3)
+__device__ __forceinline__ f32x4 shift_down(const f32x4& x, int sh) {
+    f32x4 y;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int i = j + sh;
+        y[j] = i <= 1 ? (i == 0 ? x[0] : x[1]) : (i == 2 ? x[2] : x[3]);
+    }
+    return y;
+}
+
+// four consecutive bytes at any address, byte k in bits 8k .. 8k + 7
+__device__ __forceinline__ uint32_t bytes4(const uint8_t* p) {
+    return (uint32_t)p[0] | (uint32_t)p[1] << 8 | (uint32_t)p[2] << 16 | (uint32_t)p[3] << 24;
+}
+
 // Loads and folds one lane's chunk: L steps from row t0 of the quad at column
-// e0 (steps at or past T are skipped; their loads re-read row T - 1).
-template <bool TRUNC, int L>
+// e0 (steps at or past T are skipped; their loads re-read row T - 1).  V4: the
+// quad's four environments are one 16-byte aligned vector of every float row
+// (E % 4 == 0, aligned rows; an inactive quad passes e0 = E - 4).  Otherwise
+// (any E, any alignment; e0 is the quad's first column) every quad loads 16
+// bytes per float row at 4-byte alignment, a quad reaching past E the row's
+// last four columns, shifted down into place; with E < 4 each environment is
+// loaded on its own.
+template <bool TRUNC, int L, bool V4>
 struct SegChunk {
     f32x4 r[L], v[L];
     uint32_t d[L];
@@ -499,21 +528,89 @@ struct SegChunk {
 
     __device__ __forceinline__ void load(const GaeArgs& a, int64_t t0, int64_t e0) {
         const int64_t E = a.E, T = a.T;
+        if constexpr (V4) {
 #pragma unroll
-        for (int k = 0; k < L; ++k) {
-            const int64_t t = t0 + k < T ? t0 + k : T - 1;
-            const int64_t o = t * E + e0;
-            r[k] = *reinterpret_cast<const f32x4*>(a.reward + o);
-            v[k] = a.value ? *reinterpret_cast<const f32x4*>(a.value + o) : (f32x4)(0.0f);
-            d[k] = *reinterpret_cast<const uint32_t*>(a.done + o);
-            if constexpr (TRUNC) {
-                tr[TRUNC ? k : 0] = *reinterpret_cast<const uint32_t*>(a.truncated + o);
-                fv[TRUNC ? k : 0] = *reinterpret_cast<const f32x4*>(a.final_value + o);
+            for (int k = 0; k < L; ++k) {
+                const int64_t t = t0 + k < T ? t0 + k : T - 1;
+                const int64_t o = t * E + e0;
+                r[k] = *reinterpret_cast<const f32x4*>(a.reward + o);
+                v[k] = a.value ? *reinterpret_cast<const f32x4*>(a.value + o) : (f32x4)(0.0f);
+                d[k] = *reinterpret_cast<const uint32_t*>(a.done + o);
+                if constexpr (TRUNC) {
+                    tr[TRUNC ? k : 0] = *reinterpret_cast<const uint32_t*>(a.truncated + o);
+                    fv[TRUNC ? k : 0] = *reinterpret_cast<const f32x4*>(a.final_value + o);
+                }
+            }
+            const int64_t t1 = t0 + L;
+            if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4*>(a.bootstrap + e0) : (f32x4)(0.0f);
+            else ve = a.value ? *reinterpret_cast<const f32x4*>(a.value + t1 * E + e0) : (f32x4)(0.0f);
+        } else if (E >= kV) {
+            // 16 bytes per float row at a 4-byte aligned address (dword
+            // alignment is all a multi-dword load needs).  A quad reaching past
+            // E loads the row's last four columns instead and shifts them down
+            // (environment j of the quad is loaded column eb + j + sh; columns
+            // past E take column E - 1), so every lane runs the same loads.
+            const int64_t eb = e0 + kV <= E ? e0 : E - kV;
+            const int sh = (int)(e0 - eb < kV ? e0 - eb : kV - 1);
+#pragma unroll
+            for (int k = 0; k < L; ++k) {
+                const int64_t t = t0 + k < T ? t0 + k : T - 1;
+                const int64_t o = t * E + eb;
+                r[k] = *reinterpret_cast<const f32x4u*>(a.reward + o);
+                v[k] = a.value ? *reinterpret_cast<const f32x4u*>(a.value + o) : (f32x4)(0.0f);
+                d[k] = bytes4(a.done + o);
+                if constexpr (TRUNC) {
+                    tr[TRUNC ? k : 0] = bytes4(a.truncated + o);
+                    fv[TRUNC ? k : 0] = *reinterpret_cast<const f32x4u*>(a.final_value + o);
+                }
+            }
+            const int64_t t1 = t0 + L;
+            if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4u*>(a.bootstrap + eb) : (f32x4)(0.0f);
+            else ve = a.value ? *reinterpret_cast<const f32x4u*>(a.value + t1 * E + eb) : (f32x4)(0.0f);
+            if (sh) {
+#pragma unroll
+                for (int k = 0; k < L; ++k) {
+                    r[k] = shift_down(r[k], sh);
+                    v[k] = shift_down(v[k], sh);
+                    d[k] >>= 8 * sh;
+                    if constexpr (TRUNC) {
+                        tr[TRUNC ? k : 0] >>= 8 * sh;
+                        fv[TRUNC ? k : 0] = shift_down(fv[TRUNC ? k : 0], sh);
+                    }
+                }
+                ve = shift_down(ve, sh);
+            }
+        } else {
+            // fewer than four environments: each on its own, columns past E
+            // re-reading column E - 1
+            int64_t ec[kV];
+#pragma unroll
+            for (int j = 0; j < kV; ++j) ec[j] = e0 + j < E ? e0 + j : E - 1;
+#pragma unroll
+            for (int k = 0; k < L; ++k) {
+                const int64_t t = t0 + k < T ? t0 + k : T - 1;
+                const int64_t row = t * E;
+                d[k] = 0u;
+                if constexpr (TRUNC) tr[TRUNC ? k : 0] = 0u;
+#pragma unroll
+                for (int j = 0; j < kV; ++j) {
+                    const int64_t o = row + ec[j];
+                    r[k][j] = a.reward[o];
+                    v[k][j] = a.value ? a.value[o] : 0.0f;
+                    d[k] |= (uint32_t)a.done[o] << (8 * j);
+                    if constexpr (TRUNC) {
+                        tr[TRUNC ? k : 0] |= (uint32_t)a.truncated[o] << (8 * j);
+                        fv[TRUNC ? k : 0][j] = a.final_value[o];
+                    }
+                }
+            }
+            const int64_t t1 = t0 + L;
+#pragma unroll
+            for (int j = 0; j < kV; ++j) {
+                if (t1 >= T) ve[j] = a.bootstrap ? a.bootstrap[ec[j]] : 0.0f;
+                else ve[j] = a.value ? a.value[t1 * E + ec[j]] : 0.0f;
             }
         }
-        const int64_t t1 = t0 + L;
-        if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4*>(a.bootstrap + e0) : (f32x4)(0.0f);
-        else ve = a.value ? *reinterpret_cast<const f32x4*>(a.value + t1 * E + e0) : (f32x4)(0.0f);
     }
 
     __device__ __forceinline__ void step(const GaeArgs& a, double gl, int k, int j, double vn, double* delta,
@@ -555,7 +652,59 @@ __device__ __forceinline__ double dword2(uint32_t lo, uint32_t hi) {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <bool TRUNC, int L>
+// One row of a tile's quad in a float array [T, E] (or its 32-bit words).  V4:
+// one 16-byte aligned access at column e0 (stores only for active quads).
+// Otherwise a quad inside [0, E) takes one 16-byte access at 4-byte alignment,
+// and the quad reaching past E one access per environment: stores skip columns
+// at or past E, loads re-read column E - 1 there.
+template <bool V4>
+__device__ __forceinline__ void put_quad(float* p, int64_t row, int64_t E, int64_t e0, bool active, const f32x4& x) {
+    if constexpr (V4) {
+        if (active) *reinterpret_cast<f32x4*>(p + row * E + e0) = x;
+    } else if (e0 + kV <= E) {
+        *reinterpret_cast<f32x4u*>(p + row * E + e0) = x;
+    } else {
+#pragma unroll
+        for (int j = 0; j < kV; ++j)
+            if (e0 + j < E) p[row * E + e0 + j] = x[j];
+    }
+}
+
+template <bool V4>
+__device__ __forceinline__ void put_words(float* p, int64_t row, int64_t E, int64_t e0, bool active, const u32x4& w) {
+    if constexpr (V4) {
+        if (active) *reinterpret_cast<u32x4*>(p + row * E + e0) = w;
+    } else if (e0 + kV <= E) {
+        *reinterpret_cast<u32x4u*>(p + row * E + e0) = w;
+    } else {
+#pragma unroll
+        for (int j = 0; j < kV; ++j)
+            if (e0 + j < E) reinterpret_cast<uint32_t*>(p)[row * E + e0 + j] = w[j];
+    }
+}
+
+template <bool V4>
+__device__ __forceinline__ u32x4 get_words(const float* p, int64_t row, int64_t E, int64_t e0) {
+    if constexpr (V4) {
+        return *reinterpret_cast<const u32x4*>(p + row * E + e0);
+    } else if (e0 + kV <= E) {
+        return *reinterpret_cast<const u32x4u*>(p + row * E + e0);
+    } else {
+        u32x4 w;
+#pragma unroll
+        for (int j = 0; j < kV; ++j) w[j] = reinterpret_cast<const uint32_t*>(p)[row * E + (e0 + j < E ? e0 + j : E - 1)];
+        return w;
+    }
+}
+
+// A tile quad's first column: V4 passes an inactive quad E - 4 (every access
+// stays inside the row); the per-environment accesses clamp or skip on their own.
+template <bool V4>
+__device__ __forceinline__ int64_t quad_base(int64_t e_raw, int64_t E) {
+    return V4 ? (e_raw < E ? e_raw : E - kV) : e_raw;
+}
+
+template <bool TRUNC, int L, bool V4>
 __global__ __launch_bounds__(kSegThreads) void k_gae_seg_fold(GaeArgs a, int32_t groups) {
     constexpr int64_t Ts = (int64_t)kSegChunks * L;
     int q, c;
@@ -565,16 +714,14 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_fold(GaeArgs a, int32_t
     const int64_t E = a.E;
     const int64_t e_raw = g * kSegEnvs + q * kV;
     const bool active = e_raw < E;
-    const int64_t e0 = active ? e_raw : E - kV;
+    const int64_t e0 = quad_base<V4>(e_raw, E);
     const int64_t t0 = s * Ts + (int64_t)c * L;
-    SegChunk<TRUNC, L> ch;
+    SegChunk<TRUNC, L, V4> ch;
     ch.load(a, t0, e0);
     const Map4 own = ch.fold(a, a.gamma * a.lambda, t0);
     Map4 incl, excl;
     tile_suffix(own, c, q, &incl, &excl);
-    if (c == 0 && active) {  // the segment's map, parked in segment s - 1
-        u32x4* dst = reinterpret_cast<u32x4*>(a.ret + (s - 1) * Ts * E + e0);
-        const int64_t rs = E / kV;  // row stride in 16-byte vectors
+    if (c == 0 && active) {  // the segment's map, parked in rows row0(s - 1) + 0..3
         u32x4 w0, w1, w2, w3;
 #pragma unroll
         for (int j = 0; j < kV; ++j) {
@@ -583,15 +730,17 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_fold(GaeArgs a, int32_t
             w2[j] = dlo(incl.S[j]);
             w3[j] = dhi(incl.S[j]);
         }
-        dst[0] = w0;
-        dst[rs] = w1;
-        dst[2 * rs] = w2;
-        dst[3 * rs] = w3;
+        const int64_t r0 = (s - 1) * Ts;
+        put_words<V4>(a.ret, r0, E, e0, true, w0);
+        put_words<V4>(a.ret, r0 + 1, E, e0, true, w1);
+        put_words<V4>(a.ret, r0 + 2, E, e0, true, w2);
+        put_words<V4>(a.ret, r0 + 3, E, e0, true, w3);
     }
 }
 
 // One workgroup per group of 32 environments; lanes as in seg_lane, chunk = segment, 32
 // segments per pass, passes from the end with the carried A.
+template <bool V4>
 __global__ __launch_bounds__(kSegThreads) void k_gae_seg_carry(float* adv, const float* ret, int64_t E, int64_t Ts,
                                                               int64_t S) {
     __shared__ double s_carry[kSegQuads][kV];
@@ -600,8 +749,7 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_carry(float* adv, const
     const int64_t g = blockIdx.x;
     const int64_t e_raw = g * kSegEnvs + q * kV;
     const bool active = e_raw < E;
-    const int64_t e0 = active ? e_raw : E - kV;
-    const int64_t rs = E / kV;
+    const int64_t e0 = quad_base<V4>(e_raw, E);
     double carry[kV];
 #pragma unroll
     for (int j = 0; j < kV; ++j) carry[j] = 0.0;  // A_T = 0
@@ -611,8 +759,9 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_carry(float* adv, const
         const int64_t seg = hi - (kSegChunks - 1) + c;
         const bool live = seg >= 1;
         const int64_t sr = live ? seg : hi;  // idle lanes read a valid map
-        const u32x4* src = reinterpret_cast<const u32x4*>(ret + (sr - 1) * Ts * E + e0);
-        const u32x4 w0 = src[0], w1 = src[rs], w2 = src[2 * rs], w3 = src[3 * rs];
+        const int64_t r0 = (sr - 1) * Ts;
+        const u32x4 w0 = get_words<V4>(ret, r0, E, e0), w1 = get_words<V4>(ret, r0 + 1, E, e0);
+        const u32x4 w2 = get_words<V4>(ret, r0 + 2, E, e0), w3 = get_words<V4>(ret, r0 + 3, E, e0);
         Map4 own;
 #pragma unroll
         for (int j = 0; j < kV; ++j) {
@@ -625,15 +774,14 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_carry(float* adv, const
 #pragma unroll
         for (int j = 0; j < kV; ++j) A[j] = incl.P[j] * carry[j] + incl.S[j];  // A at row0(seg)
         if (live && active) {
-            u32x4* dst = reinterpret_cast<u32x4*>(adv + (seg - 1) * Ts * E + e0);
             u32x4 lo, hw;
 #pragma unroll
             for (int j = 0; j < kV; ++j) {
                 lo[j] = dlo(A[j]);
                 hw[j] = dhi(A[j]);
             }
-            dst[0] = lo;
-            dst[rs] = hw;
+            put_words<V4>(adv, (seg - 1) * Ts, E, e0, true, lo);
+            put_words<V4>(adv, (seg - 1) * Ts + 1, E, e0, true, hw);
         }
         if (hi - kSegChunks < 1) break;  // uniform
         // the next pass starts from A at row0(hi - 31), held by chunk c = 0
@@ -648,7 +796,7 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_carry(float* adv, const
     }
 }
 
-template <bool TRUNC, int L>
+template <bool TRUNC, int L, bool V4>
 __global__ __launch_bounds__(kSegThreads) void k_gae_seg_replay(GaeArgs a, int32_t groups, int64_t S) {
     constexpr int64_t Ts = (int64_t)kSegChunks * L;
     int q, c;
@@ -658,18 +806,16 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_replay(GaeArgs a, int32
     const int64_t E = a.E, T = a.T;
     const int64_t e_raw = g * kSegEnvs + q * kV;
     const bool active = e_raw < E;
-    const int64_t e0 = active ? e_raw : E - kV;
-    const int64_t rs = E / kV;
+    const int64_t e0 = quad_base<V4>(e_raw, E);
     const int64_t row0 = s * Ts;
     const int64_t t0 = row0 + (int64_t)c * L;
     // the carry first: rows row0, row0 + 1 of adv are rewritten below
     u32x4 clo = (u32x4)(0u), chi = (u32x4)(0u);
     if (s + 1 < S) {
-        const u32x4* src = reinterpret_cast<const u32x4*>(a.adv + row0 * E + e0);
-        clo = src[0];
-        chi = src[rs];
+        clo = get_words<V4>(a.adv, row0, E, e0);
+        chi = get_words<V4>(a.adv, row0 + 1, E, e0);
     }
-    SegChunk<TRUNC, L> ch;
+    SegChunk<TRUNC, L, V4> ch;
     ch.load(a, t0, e0);
     const double gl = a.gamma * a.lambda;
     const Map4 own = ch.fold(a, gl, t0);
@@ -698,11 +844,8 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_replay(GaeArgs a, int32
                 ro[j] = (float)(A[j] + (double)ch.v[k][j]);
                 vn[j] = (double)ch.v[k][j];
             }
-            if (active) {
-                const int64_t o = (t0 + k) * E + e0;
-                *reinterpret_cast<f32x4*>(a.adv + o) = ao;
-                *reinterpret_cast<f32x4*>(a.ret + o) = ro;
-            }
+            put_quad<V4>(a.adv, t0 + k, E, e0, active, ao);
+            put_quad<V4>(a.ret, t0 + k, E, e0, active, ro);
         }
     }
 }
@@ -766,7 +909,7 @@ __device__ __forceinline__ double get_f64(uint64_t* p) {
     return __longlong_as_double((long long)__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
 }
 
-template <bool TRUNC, int L>
+template <bool TRUNC, int L, bool V4>
 __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, LookTable* tab, int32_t groups, int32_t S,
                                                            uint64_t epoch) {
     constexpr int64_t Ts = (int64_t)kSegChunks * L;
@@ -779,10 +922,10 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, LookTable* 
     const int64_t E = a.E, T = a.T;
     const int64_t e_raw = g * kSegEnvs + q * kV;
     const bool active = e_raw < E;
-    const int64_t e0 = active ? e_raw : E - kV;
+    const int64_t e0 = quad_base<V4>(e_raw, E);
     const int64_t t0 = s * Ts + (int64_t)c * L;
     const double gl = a.gamma * a.lambda;
-    SegChunk<TRUNC, L> ch;
+    SegChunk<TRUNC, L, V4> ch;
     ch.load(a, t0, e0);
     const Map4 own = ch.fold(a, gl, t0);
     Map4 incl, excl;
@@ -885,11 +1028,8 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, LookTable* 
                 ro[j] = (float)(A[j] + (double)ch.v[k][j]);
                 vn[j] = (double)ch.v[k][j];
             }
-            if (active) {
-                const int64_t o = (t0 + k) * E + e0;
-                *reinterpret_cast<f32x4*>(a.adv + o) = ao;
-                *reinterpret_cast<f32x4*>(a.ret + o) = ro;
-            }
+            put_quad<V4>(a.adv, t0 + k, E, e0, active, ao);
+            put_quad<V4>(a.ret, t0 + k, E, e0, active, ro);
         }
     }
 }
@@ -1111,40 +1251,44 @@ __global__ void k_fill_u64(uint64_t* p, uint64_t v, int64_t n) {
 
 }  // namespace
 
-template <bool TRUNC, int L>
+template <bool TRUNC, int L, bool V4>
 hipError_t launch_gae_split_t(const GaeArgs& a, int64_t groups, hipStream_t s) {
     constexpr int64_t Ts = (int64_t)kSegChunks * L;
     const int64_t S = (a.T + Ts - 1) / Ts;
     const dim3 block(kSegThreads);
-    hipLaunchKernelGGL((k_gae_seg_fold<TRUNC, L>), dim3((unsigned)(groups * (S - 1))), block, 0, s, a,
+    hipLaunchKernelGGL((k_gae_seg_fold<TRUNC, L, V4>), dim3((unsigned)(groups * (S - 1))), block, 0, s, a,
                        (int32_t)groups);
-    hipLaunchKernelGGL(k_gae_seg_carry, dim3((unsigned)groups), block, 0, s, a.adv, a.ret, a.E, Ts, S);
-    hipLaunchKernelGGL((k_gae_seg_replay<TRUNC, L>), dim3((unsigned)(groups * S)), block, 0, s, a, (int32_t)groups,
-                       S);
+    hipLaunchKernelGGL(k_gae_seg_carry<V4>, dim3((unsigned)groups), block, 0, s, a.adv, a.ret, a.E, Ts, S);
+    hipLaunchKernelGGL((k_gae_seg_replay<TRUNC, L, V4>), dim3((unsigned)(groups * S)), block, 0, s, a,
+                       (int32_t)groups, S);
     return hipGetLastError();
 }
 
-template <bool TRUNC>
+template <bool TRUNC, bool V4>
 hipError_t launch_gae_split_l(const GaeArgs& a, int64_t groups, int L, hipStream_t s) {
     switch (L) {
-        case 8: return launch_gae_split_t<TRUNC, 8>(a, groups, s);
-        case 4: return launch_gae_split_t<TRUNC, 4>(a, groups, s);
-        default: return launch_gae_split_t<TRUNC, 2>(a, groups, s);
+        case 8: return launch_gae_split_t<TRUNC, 8, V4>(a, groups, s);
+        case 4: return launch_gae_split_t<TRUNC, 4, V4>(a, groups, s);
+        default: return launch_gae_split_t<TRUNC, 2, V4>(a, groups, s);
     }
 }
 
-hipError_t launch_gae_split(const GaeArgs& a, int64_t groups, int L, hipStream_t s) {
-    return a.truncated ? launch_gae_split_l<true>(a, groups, L, s) : launch_gae_split_l<false>(a, groups, L, s);
+hipError_t launch_gae_split(const GaeArgs& a, int64_t groups, int L, bool v4, hipStream_t s) {
+    if (v4)
+        return a.truncated ? launch_gae_split_l<true, true>(a, groups, L, s)
+                           : launch_gae_split_l<false, true>(a, groups, L, s);
+    return a.truncated ? launch_gae_split_l<true, false>(a, groups, L, s)
+                       : launch_gae_split_l<false, false>(a, groups, L, s);
 }
 
-template <bool TRUNC>
+template <bool TRUNC, bool V4>
 hipError_t launch_gae_look_l(const GaeArgs& a, LookTable* tab, int32_t groups, int32_t S, int L, uint64_t ep,
                              hipStream_t s) {
     const dim3 grid((unsigned)(groups * S)), block(kSegThreads);
     switch (L) {
-        case 8: hipLaunchKernelGGL((k_gae_look<TRUNC, 8>), grid, block, 0, s, a, tab, groups, S, ep); break;
-        case 4: hipLaunchKernelGGL((k_gae_look<TRUNC, 4>), grid, block, 0, s, a, tab, groups, S, ep); break;
-        default: hipLaunchKernelGGL((k_gae_look<TRUNC, 2>), grid, block, 0, s, a, tab, groups, S, ep); break;
+        case 8: hipLaunchKernelGGL((k_gae_look<TRUNC, 8, V4>), grid, block, 0, s, a, tab, groups, S, ep); break;
+        case 4: hipLaunchKernelGGL((k_gae_look<TRUNC, 4, V4>), grid, block, 0, s, a, tab, groups, S, ep); break;
+        default: hipLaunchKernelGGL((k_gae_look<TRUNC, 2, V4>), grid, block, 0, s, a, tab, groups, S, ep); break;
     }
     return hipGetLastError();
 }
@@ -1173,7 +1317,7 @@ static hipError_t gae_table(LookTable** out) {
     return hipSuccess;
 }
 
-hipError_t launch_gae_look(const GaeArgs& a, int32_t groups, int32_t S, int L, hipStream_t s) {
+hipError_t launch_gae_look(const GaeArgs& a, int32_t groups, int32_t S, int L, bool v4, hipStream_t s) {
     // one segment (the short path) uses no table; split rollouts at most the
     // table's tiles (the plan never asks for more)
     if (S > 1 && (int64_t)groups * S > kLookMaxTiles) return hipErrorInvalidValue;
@@ -1189,8 +1333,11 @@ hipError_t launch_gae_look(const GaeArgs& a, int32_t groups, int32_t S, int L, h
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    return a.truncated ? launch_gae_look_l<true>(a, tab, groups, S, L, ep, s)
-                       : launch_gae_look_l<false>(a, tab, groups, S, L, ep, s);
+    if (v4)
+        return a.truncated ? launch_gae_look_l<true, true>(a, tab, groups, S, L, ep, s)
+                           : launch_gae_look_l<false, true>(a, tab, groups, S, L, ep, s);
+    return a.truncated ? launch_gae_look_l<true, false>(a, tab, groups, S, L, ep, s)
+                       : launch_gae_look_l<false, false>(a, tab, groups, S, L, ep, s);
 }
 
 hipError_t gae_noalloc_err_words(uint32_t** err) {
@@ -1232,7 +1379,7 @@ hipError_t gae_noalloc_clear_errors() {
 
 GaePlan plan_gae(int64_t T, int64_t E, bool vec) {
     GaePlan p{vec ? GAE_ONE_PASS_V4 : GAE_ONE_PASS, 0, 0, 0};
-    if (!vec || T <= 0 || E <= 0) return p;
+    if (T <= 0 || E <= 0) return p;
     // split along T: the longest chunk that still gives every compute unit a
     // tile, at least two segments; chunks of 4 steps where that still gives
     // 1,024 to 4,096 tiles (a tile of 8-step chunks holds 288 registers per
@@ -1270,8 +1417,8 @@ hipError_t launch_gae(const GaeArgs& a, hipStream_t s) {
     const GaePlan p = plan_gae(a.T, a.E, vec);
     switch (p.path) {
         case GAE_SHORT:
-        case GAE_LOOK_BACK: return launch_gae_look(a, (int32_t)p.groups, (int32_t)p.segments, p.chunk, s);
-        case GAE_THREE_LAUNCHES: return launch_gae_split(a, p.groups, p.chunk, s);
+        case GAE_LOOK_BACK: return launch_gae_look(a, (int32_t)p.groups, (int32_t)p.segments, p.chunk, vec, s);
+        case GAE_THREE_LAUNCHES: return launch_gae_split(a, p.groups, p.chunk, vec, s);
         case GAE_ONE_PASS_V4: {
             const int64_t vblocks = (a.E + kEnvsV - 1) / kEnvsV;
             constexpr int L = kGaeVecChunk;

@@ -177,8 +177,12 @@ GAE_PLANS = [
     ((1100000, 4, True), ("split", 8)),     # 4,297 tiles, fewer than 4,096 envs
     ((65, 131072, True), ("one_v4", 0)),    # 8,192 tiles, 4,096 envs or more
     ((2049, 65536, True), ("one_v4", 0)),
-    ((2048, 256, False), ("one", 0)),       # rows off a 16-byte boundary
-    ((2048, 255, True), ("one", 0)),        # E not a multiple of 4
+    ((2048, 256, False), ("look", 2)),      # rows off a 16-byte boundary: per-element tiles
+    ((2048, 255, True), ("look", 2)),       # E not a multiple of 4: per-element tiles
+    ((64, 4099, True), ("short", 2)),
+    ((1100000, 3, True), ("split", 8)),     # 4,297 tiles of one partial group
+    ((65, 131071, True), ("one", 0)),       # 8,192 tiles, 4,096 envs or more, E % 4 != 0
+    ((65, 131072, False), ("one", 0)),
     ((0, 4, True), ("one_v4", 0)),          # empty rollouts enqueue nothing
 ]
 

@@ -28,8 +28,8 @@ def _gae_gpu(r, v, d, b, gamma, lam):
     (1, 1, 0.0, True, True), (2, 3, 0.5, True, False), (37, 19, 0.05, True, True), (64, 16, 0.0, False, False),
     (65, 17, 1.0, True, True), (200, 70, 0.01, True, True), (1000, 5, 0.002, True, True),
     (2500, 9, 0.003, True, True), (1024, 8, 0.0, True, False), (3073, 3, 0.01, False, True),
-    # E a multiple of 4: four environments per lane, split along T where T > 64
-    # (see SPLIT_CASES below), one pass of all T steps for T <= 64
+    # E a multiple of 4 or not: one tile per 32 environments for T <= 64, split
+    # along T beyond (see SPLIT_CASES below)
     (100, 12, 0.02, True, True), (2500, 12, 0.003, True, True), (4096, 8, 0.001, True, True),
     (2049, 4, 0.01, True, False), (300, 128, 0.01, True, True), (33, 64, 0.1, False, False),
     # the most environments the ABI takes (2^19), on both kernels
@@ -78,6 +78,7 @@ def test_gae_truncated_shapes(T, E, p_done, p_trunc):
 # over the later segments ("look"); more run in three launches below 4,096
 # environments ("split") and otherwise as one workgroup walking all T steps of
 # 8 environments ("one_v4"; "one" for E not a multiple of 4 or unaligned rows).
+# The tiles take any E and rows off a 16-byte boundary (SPLIT_CASES_ANY_E).
 # conduit_gae_plan reports the choice; tests/test_abi_cpu.py checks it on the
 # host.
 SPLIT_CASES = [
@@ -128,7 +129,44 @@ def test_gae_split_along_t(T, E, p_done, path, L):
     assert np.array_equal(ga, r) and np.array_equal(gr, r)
 
 
-@pytest.mark.parametrize("T,E", [(2100, 1000), (1100, 4052), (700, 36), (1100000, 4), (40, 4100), (64, 36)])
+# E not a multiple of 4: the same tiles, each lane loading and storing its
+# four environments one by one (columns past E skipped on store, clamped on load)
+SPLIT_CASES_ANY_E = [
+    # (T, E, p_done, expected path, expected chunk length)
+    (1, 3, 0.5, "short", 2),           # fewer environments than a quad
+    (16, 4101, 0.02, "short", 2),      # 129 groups, the last one 5 envs (a partial quad)
+    (64, 131071, 0.01, "short", 2),    # 4,096 tiles
+    (65, 5, 0.05, "look", 2),          # two segments, one partial quad
+    (129, 37, 0.02, "look", 2),        # a partial group and a partial quad
+    (2048, 255, 0.001, "look", 2),     # the PPO rollout with one environment fewer
+    (40000, 6, 0.0005, "look", 4),     # chained look-back windows
+    (2100, 1001, 0.003, "look", 8),
+    (3000, 4091, 0.01, "look", 4),     # 3,072 tiles
+    (1100000, 3, 0.0001, "split", 8),  # three launches, one partial quad
+    (600000, 37, 0.0002, "split", 8),  # three launches, a partial group and quad
+]
+
+
+@pytest.mark.parametrize("T,E,p_done,path,L", SPLIT_CASES_ANY_E)
+def test_gae_split_along_t_any_e(T, E, p_done, path, L):
+    print(f"gae split any E T={T} E={E} {path} L={L}", flush=True)
+    assert _time_major_path(T, E) == (path, L)
+    rng = np.random.default_rng(T * 13 + E)
+    r = rng.standard_normal((T, E)).astype(np.float32)
+    v = rng.standard_normal((T, E)).astype(np.float32)
+    d = (rng.random((T, E)) < p_done).astype(np.uint8)
+    b = rng.standard_normal(E).astype(np.float32)
+    for gamma, lam in [(0.99, 0.95), (1.0, 1.0)]:
+        ga, gr = _gae_gpu(r, v, d, b, gamma, lam)
+        oa, orr = oracle.gae(r, v, d, b, gamma, lam)
+        assert_gae_close(ga, oa)
+        assert_gae_close(gr, orr)
+    ga, gr = _gae_gpu(r, None, np.ones((T, E), np.uint8), None, 0.99, 0.95)
+    assert np.array_equal(ga, r) and np.array_equal(gr, r)
+
+
+@pytest.mark.parametrize("T,E", [(2100, 1000), (1100, 4052), (700, 36), (1100000, 4), (40, 4100), (64, 36),
+                                 (2100, 1001), (700, 37), (1100000, 3), (40, 4101)])
 def test_gae_truncated_split_along_t(T, E):
     print(f"gae truncated split T={T} E={E}", flush=True)
     assert _time_major_path(T, E)[0] in ("short", "look", "split")
@@ -148,13 +186,15 @@ def test_gae_truncated_split_along_t(T, E):
     assert_gae_close(host(ret), orr)
 
 
-@pytest.mark.parametrize("T,E", [(65, 131072), pytest.param(2049, 65536, marks=pytest.mark.slow)])
-def test_gae_single_pass_kernel_several_passes(T, E):
+@pytest.mark.parametrize("T,E,path", [(65, 131072, "one_v4"), (65, 131071, "one"), (2100, 16383, "one"),
+                                      pytest.param(2049, 65536, "one_v4", marks=pytest.mark.slow)])
+def test_gae_single_pass_kernel_several_passes(T, E, path):
     """Wide rollouts beyond the look-back table keep one workgroup per 8
     environments walking 2,048-step passes (two passes, the last of one step,
-    in the slow case)."""
+    in the slow case and at T = 2,100); four environments per lane where E is
+    a multiple of 4, one otherwise."""
     print(f"gae single-pass T={T} E={E}", flush=True)
-    assert _time_major_path(T, E)[0] == "one_v4"
+    assert _time_major_path(T, E)[0] == path
     rng = np.random.default_rng(T + E)
     r = rng.standard_normal((T, E)).astype(np.float32)
     v = rng.standard_normal((T, E)).astype(np.float32)
@@ -166,11 +206,15 @@ def test_gae_single_pass_kernel_several_passes(T, E):
     assert_gae_close(gr, orr)
 
 
-def test_gae_misaligned_rows_take_the_lane_per_environment_kernel():
+@pytest.mark.parametrize("T,E,path", [(333, 16, "look"), (40, 16, "short"), (1100000, 4, "split"),
+                                      (65, 131072, "one")])
+def test_gae_misaligned_rows_take_per_element_access(T, E, path):
     """E a multiple of 4 but rows 4 bytes off a 16-byte boundary: the launcher
-    must not use 16-byte vectors; results still match the oracle."""
-    print("gae misaligned rows", flush=True)
-    T, E = 333, 16
+    must not use 16-byte vectors (tiles load and store each environment on its
+    own, the wide one-pass kernel takes one environment per lane); results
+    still match the oracle."""
+    print(f"gae misaligned rows T={T} E={E}", flush=True)
+    assert cd.gae_plan(T, E, aligned=False)[0] == path
     rng = np.random.default_rng(7)
     r = rng.standard_normal((T, E)).astype(np.float32)
     v = rng.standard_normal((T, E)).astype(np.float32)
