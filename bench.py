@@ -366,11 +366,27 @@ def bench_dqn(steps, warmup):
     _b2b_ms(ns_calls[:5])
     nstep_ms = _b2b_ms(ns_calls)
     boot = int(nval.sum().item())
+    # delivery with n-step targets and bootstrap stacks: one call
+    # (conduit_sample_gather_nstep, one launch that reads every frame of the
+    # two stacks once) against conduit_sample_gather + conduit_nstep
+    sgn = L.conduit_sample_gather_nstep
+    one_calls = [lambda i=i: sgn(h, B, pu[i], pi[i], pw[i], xfr, lbr, n_step, gam, nxt.data_ptr(), nret.data_ptr(),
+                                 ndisc.data_ptr(), nval.data_ptr(), next_out.data_ptr(), stream)
+                 for i in range(warmup, warmup + steps)]
+    two_calls = [lambda i=i: sgat(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream) | nst(h, pi[i], B, n_step, gam, *ns_args)
+                 for i in range(warmup, warmup + steps)]
+    _b2b_ms(one_calls[:5])
+    _b2b_ms(two_calls[:5])
+    deliver_nstep_one_ms = _b2b_ms(one_calls)
+    deliver_nstep_two_ms = _b2b_ms(two_calls)
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
     return {
         "nstep3": {"us": nstep_ms * 1e3, "n": n_step, "gamma": gam, "valid_in_last_batch": boot,
                    "call": "conduit_nstep: targets plus the bootstrap frame stacks [512,4,84,84] fp32"},
+        "deliver_nstep3": {"one_call_us": deliver_nstep_one_ms * 1e3, "two_calls_us": deliver_nstep_two_ms * 1e3,
+                           "call": "conduit_sample_gather_nstep (sample 512, [512,4,84,84] fp32 batch, n = 3 "
+                                   "targets and bootstrap stacks) against conduit_sample_gather + conduit_nstep"},
         "B": B, "steps": steps, "warmup": warmup, "total_ms": total_ms, "host_enqueue_s": host_enqueue_s,
         "gather_b2b_ms": gather_b2b_ms, "fused_b2b_ms": fused_b2b_ms, "unfused_ms": unfused_ms,
         "separate_ms": separate_ms, "update_ingest_call": ui_stats,
@@ -1474,7 +1490,9 @@ def main():
         "ms_per_step_unfused": d["unfused_ms"] / args.steps,
         "kernels_us_in_step": {k.split(" ")[0]: round(v["mean_us"], 3) for k, v in d["kernels"].items()},
         "rows": {"dqn_ingest_32768_frac": d["ingest_big"]["GBps"] / PEAK_HBM_GBPS,
-                 "dqn_nstep3_us": d["nstep3"]["us"]},
+                 "dqn_nstep3_us": d["nstep3"]["us"],
+                 "dqn_deliver_nstep3_us": {"one_call": d["deliver_nstep3"]["one_call_us"],
+                                           "two_calls": d["deliver_nstep3"]["two_calls_us"]}},
     }
     if not args.no_rows:
         only = set(x for x in args.only.split(",") if x) or set(ROWS)

@@ -38,7 +38,8 @@
  *     conduit_sync_check() waits for a stream and reports the flag.
  *   - conduit_last_error() returns a thread-local message for the last failure.
  *   - The delivery and on-policy calls (conduit_sample, conduit_gather_transform,
- *     conduit_sample_gather, conduit_update_priorities, conduit_nstep, the GAE
+ *     conduit_sample_gather, conduit_sample_gather_nstep,
+ *     conduit_update_priorities, conduit_nstep, the GAE
  *     calls, conduit_minibatch_gather) only enqueue kernels: no allocation,
  *     memset or synchronisation, so they may be captured into a HIP graph and
  *     replayed; a replay uses the arguments and the ring state (size, total)
@@ -362,6 +363,27 @@ conduit_status conduit_sample_gather(conduit_buffer* buf, int64_t batch, const u
 conduit_status conduit_nstep(conduit_buffer* buf, const int64_t* idx, int64_t batch, int32_t n, double gamma,
                              int64_t* next_idx, float* ret, float* discount, uint8_t* valid,
                              const conduit_transform* xf, void* next_obs, void* stream);
+
+/*
+ * Fused off-policy delivery with n-step targets (Sec. 2.2: delivery samples,
+ * then materialises training-ready transitions; the n-step target as in
+ * conduit_nstep): exactly conduit_sample_gather(buf, batch, uniforms, idx_out,
+ * is_w_out, xf, out) followed by conduit_nstep(buf, idx_out, batch, n, gamma,
+ * next_idx, ret, discount, valid, xf, next_obs), with the same outputs,
+ * layouts and errors as the two calls (next_obs may be NULL: targets only).
+ * Dense buffers whose state stack and bootstrap stack together need at most
+ * 16 gather work items of 7,168 bytes (e.g. 84x84 frames, a stack of 4, any
+ * n) take one launch: each sample's workgroup descends the tree, evaluates
+ * the window from the slot it found and reads every frame of the two stacks
+ * once (K + min(n, K) frames instead of 2K), storing each into the stacks it
+ * belongs to.  Other buffers take the two calls.  Calls on one buffer must
+ * not overlap (as for every call on a buffer).
+ */
+conduit_status conduit_sample_gather_nstep(conduit_buffer* buf, int64_t batch, const uint64_t* uniforms,
+                                           int64_t* idx_out, float* is_w_out, const conduit_transform* xf,
+                                           const conduit_learner_batch* out, int32_t n, double gamma,
+                                           int64_t* next_idx, float* ret, float* discount, uint8_t* valid,
+                                           void* next_obs, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Returns / advantages (Sec. 2.2: on-policy ingestion derives returns and

@@ -128,6 +128,7 @@ SIGNATURES = {
     "conduit_sample": (ST, [P, I64, P, P, P, P]),
     "conduit_gather_transform": (ST, [P, P, I64, P, P, P]),
     "conduit_sample_gather": (ST, [P, I64, P, P, P, P, P, P]),
+    "conduit_sample_gather_nstep": (ST, [P, I64, P, P, P, P, P, I32_, F64, P, P, P, P, P, P]),
     "conduit_gae": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_gae_noalloc": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_update_ingest": (ST, [P, P, P, I64, P, P]),
@@ -372,6 +373,22 @@ def conduit_sample_gather(handle, batch, uniforms, idx_out, is_w_out, xf, obs=No
                                        _ptr(idx_out, torch.int64, "idx_out", numel=batch),
                                        _ptr(is_w_out, torch.float32, "is_w_out", numel=batch),
                                        C.byref(xf), C.byref(out), _stream(stream)))
+
+
+def conduit_sample_gather_nstep(handle, batch, uniforms, idx_out, is_w_out, xf, n, gamma, next_idx, ret, discount,
+                                valid, next_obs=None, obs=None, action=None, reward=None, done=None, stream=None):
+    """conduit_sample_gather then conduit_nstep on the sampled slots, in one
+    launch where the buffer's rows allow it."""
+    info = _info(handle)
+    out = _batch_ptrs(info, batch, xf, obs, action, reward, done, None, None, None)
+    nbytes = batch * _out_row_bytes(info, xf) if (next_obs is not None and not info.ragged) else None
+    _check(lib().conduit_sample_gather_nstep(
+        handle, batch, _ptr(uniforms, _ELEM8_INT, "uniforms", numel=batch),
+        _ptr(idx_out, torch.int64, "idx_out", numel=batch), _ptr(is_w_out, torch.float32, "is_w_out", numel=batch),
+        C.byref(xf), C.byref(out), int(n), float(gamma), _ptr(next_idx, torch.int64, "next_idx", numel=batch),
+        _ptr(ret, torch.float32, "ret", numel=batch), _ptr(discount, torch.float32, "discount", numel=batch),
+        _ptr(valid, (torch.uint8, torch.bool), "valid", numel=batch), _ptr(next_obs, None, "next_obs", nbytes=nbytes),
+        _stream(stream)))
 
 
 def conduit_nstep(handle, idx, n, gamma, next_idx, ret, discount, valid, xf=None, next_obs=None, stream=None):
@@ -628,6 +645,22 @@ class ReplayBuffer:
 
     def gather(self, idx, xf, **outs):
         conduit_gather_transform(self.handle, idx, xf, stream=outs.pop("stream", None), **outs)
+
+    def sample_gather_nstep(self, uniforms, xf, n, gamma, next_obs=None, **outs):
+        """(idx, w, next_idx, ret, discount, valid) of one fused delivery with
+        n-step targets; the batch and the bootstrap stacks go to the given
+        outputs."""
+        B = uniforms.numel()
+        dev = uniforms.device
+        idx = torch.empty(B, dtype=torch.int64, device=dev)
+        w = torch.empty(B, dtype=torch.float32, device=dev)
+        nxt = torch.empty(B, dtype=torch.int64, device=dev)
+        ret = torch.empty(B, dtype=torch.float32, device=dev)
+        disc = torch.empty(B, dtype=torch.float32, device=dev)
+        val = torch.empty(B, dtype=torch.uint8, device=dev)
+        conduit_sample_gather_nstep(self.handle, B, uniforms, idx, w, xf, n, gamma, nxt, ret, disc, val,
+                                    next_obs=next_obs, stream=outs.pop("stream", None), **outs)
+        return idx, w, nxt, ret, disc, val
 
     def read(self, col, dst, offset=0, level=0, stream=None):
         conduit_buffer_read(self.handle, col, dst, offset, level, stream)

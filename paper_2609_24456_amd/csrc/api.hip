@@ -845,6 +845,72 @@ conduit_status conduit_nstep(conduit_buffer* b, const int64_t* idx, int64_t batc
     return CONDUIT_OK;
 }
 
+conduit_status conduit_sample_gather_nstep(conduit_buffer* b, int64_t batch, const uint64_t* uniforms,
+                                           int64_t* idx_out, float* is_w_out, const conduit_transform* xf,
+                                           const conduit_learner_batch* out, int32_t n, double gamma,
+                                           int64_t* next_idx, float* ret, float* discount, uint8_t* valid,
+                                           void* next_obs, void* stream) {
+    if (!b || !xf || !out) return fail(CONDUIT_EINVAL, "NULL buffer, transform or output");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (!b->opts.prioritized) return fail(CONDUIT_EINVAL, "buffer was created without priorities");
+    if (batch < 1 || batch > (1LL << 20)) return fail(CONDUIT_EINVAL, "batch must be in [1, 2^20]");
+    if (!uniforms || !idx_out) return fail(CONDUIT_EINVAL, "uniforms and idx_out must not be NULL");
+    if (n < 1 || n > 63) return fail(CONDUIT_EINVAL, "n must be in [1, 63]");
+    if (!(gamma == gamma)) return fail(CONDUIT_EINVAL, "gamma must be a number");
+    if (!next_idx || !ret || !discount || !valid) return fail(CONDUIT_EINVAL, "NULL n-step output");
+    if (next_obs && b->opts.ragged) return fail(CONDUIT_EINVAL, "next-state stacks need a dense buffer");
+    if (b->size == 0) return fail(CONDUIT_EEMPTY, "sample from an empty buffer");
+    GatherArgs ga{};
+    PackArgs pa{};
+    st = prepare_gather(b, idx_out, batch, xf, out, &ga, &pa);
+    if (st != CONDUIT_OK) return st;
+    if (next_obs) {  // the bootstrap stacks are laid out as a gather's obs output
+        conduit_learner_batch nb{};
+        nb.obs = next_obs;
+        GatherArgs gn{};
+        PackArgs pn{};
+        st = prepare_gather(b, next_idx, batch, xf, &nb, &gn, &pn);
+        if (st != CONDUIT_OK) return st;
+    }
+    if (!b->opts.ragged) {
+        DeviceGuard g(b->device);
+        SampleArgs sa{};
+        sa.tree = b->tree;
+        sa.uniforms = uniforms;
+        sa.idx_out = idx_out;
+        sa.w_out = is_w_out;
+        sa.batch = batch;
+        sa.beta = b->opts.beta;
+        sa.state = b->state;
+        sa.err = err_words(b->err_slot);
+        set_leaf_min(b, &sa);
+        NstepArgs na{};
+        na.idx = idx_out;
+        na.batch = batch;
+        na.n = n;
+        na.gamma = gamma;
+        na.capacity = b->capacity;
+        na.size = b->size;
+        na.total = b->total;
+        na.reward = b->reward;
+        na.done = b->done;
+        na.episode = b->episode;
+        na.next_idx = next_idx;
+        na.ret = ret;
+        na.discount = discount;
+        na.valid = valid;
+        na.err = err_words(b->err_slot);
+        const hipError_t e = launch_sample_gather_nstep(sa, ga, na, next_obs, static_cast<hipStream_t>(stream));
+        if (e == hipSuccess) return CONDUIT_OK;
+        if (e != hipErrorNotSupported) return hip_fail(e, "sample_gather_nstep launch");
+    }
+    // other shapes: the two calls
+    st = conduit_sample_gather(b, batch, uniforms, idx_out, is_w_out, xf, out, stream);
+    if (st != CONDUIT_OK) return st;
+    return conduit_nstep(b, idx_out, batch, n, gamma, next_idx, ret, discount, valid, xf, next_obs, stream);
+}
+
 // true if [a, a + na) and [b, b + nb) share a byte (NULL ranges share none)
 static bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
     if (!a || !b) return false;

@@ -507,6 +507,12 @@ hipError_t launch_nstep(const NstepArgs& a, hipStream_t s);
 // launch (ga.idx unused: each sample's slot comes from its window);
 // hipErrorNotSupported for other shapes
 hipError_t launch_nstep_gather(const NstepArgs& na, const GatherArgs& ga, hipStream_t s);
+// sample + gather + n-step targets (+ the bootstrap stacks into next_out if not
+// NULL) in one launch, for dense rows whose state and bootstrap stacks need at
+// most 16 work items (na.idx unused: slots come from the descent);
+// hipErrorNotSupported for other shapes
+hipError_t launch_sample_gather_nstep(const SampleArgs& sa, const GatherArgs& ga, const NstepArgs& na,
+                                      void* next_out, hipStream_t s);
 
 struct GaePackedArgs {
     const float* last_reward;

@@ -206,14 +206,16 @@ __device__ __forceinline__ int64_t wave_uniform(int64_t x) {
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
+// The units of part `part` of output frame `frame` (frames of `units` units
+// each, counted from `out`).
 template <int POL, typename O>
-__device__ __forceinline__ void store_item(const GatherArgs& a, const Item& t, int64_t units, int tid,
-                                           const O (&o)[kUnroll]) {
+__device__ __forceinline__ void store_at(void* out, int64_t frame, int part, int64_t units, int tid,
+                                         const O (&o)[kUnroll]) {
     // the item's place and size are the same for every lane (items belong to
     // whole wavefronts)
-    const int64_t first = wave_uniform((int64_t)t.part * kUnitsPerBlock);  // its first unit within the frame
-    const int64_t at = wave_uniform((t.b * a.stack + t.k) * units + first);
-    O* base = reinterpret_cast<O*>(a.out) + at;
+    const int64_t first = wave_uniform((int64_t)part * kUnitsPerBlock);  // its first unit within the frame
+    const int64_t at = wave_uniform(frame * units + first);
+    O* base = reinterpret_cast<O*>(out) + at;
     if constexpr (POL == kStoreWT) {
         const int n = (int)(units - first < kUnitsPerBlock ? units - first : kUnitsPerBlock);
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
@@ -233,6 +235,12 @@ __device__ __forceinline__ void store_item(const GatherArgs& a, const Item& t, i
             }
         }
     }
+}
+
+template <int POL, typename O>
+__device__ __forceinline__ void store_item(const GatherArgs& a, const Item& t, int64_t units, int tid,
+                                           const O (&o)[kUnroll]) {
+    store_at<POL>(a.out, t.b * a.stack + t.k, t.part, units, tid, o);
 }
 
 // The converted item (every conversion first, branch-free: an invalid frame is
@@ -360,6 +368,8 @@ __device__ __forceinline__ void row_scalars_store(const GatherArgs& a, int64_t b
 // rows of at most this many work items take the fused kernels (a sample's
 // workgroup finds its slot itself and its two 256-lane halves share the items)
 constexpr int64_t kFusedMaxItemsPerRow = 8;
+// ... and with the n-step bootstrap stack, the union of the two stacks' frames
+constexpr int64_t kFusedNstepMaxItemsPerRow = 16;
 
 // The work items of row b (the slot i, or out of range for a zero row) that
 // 256-lane group `part` of the row's `wgs` owns (tid: the lane in the group),
@@ -402,6 +412,209 @@ __device__ __forceinline__ void gather_row(const GatherArgs& a, int64_t b, int p
     }
     if (owner) row_scalars_store(a, b, i, rs, tid);
 }
+
+
+// ---------------------------------------------------------------------------
+// A sample's state stack and its n-step bootstrap stack from one read of each
+// frame they need.  With the sample at stream position p (slot i) and the
+// bootstrap state at p + n (slot jn), the state stack holds positions
+// p - K + 1 .. p and the bootstrap stack p + n - K + 1 .. p + n; the first K
+// positions and the S = min(n, K) newest of the bootstrap stack cover both:
+// U = K + S frames, frame u at position p + off(u),
+//   off(u) = u - (K - 1)              for u < K (state frame u),
+//            n - S + 1 + (u - K)      for u >= K,
+// bootstrap frame u - n (u < K) or u - S (u >= K) where that is >= 0.  Each
+// frame is converted once and stored into each stack it belongs to, zero
+// where its stack's episode/step check fails (as the gather checks it for
+// that stack's own newest slot) and in every frame of a row without a
+// bootstrap state.
+
+// the converted units of an item, as stored
+template <int XF> struct OutUnit { typedef uint32_t T; };
+template <> struct OutUnit<kXfCopy16> { typedef u32x4 T; };
+template <> struct OutUnit<CONDUIT_XF_U8_F32> { typedef f32x4 T; };
+template <> struct OutUnit<CONDUIT_XF_U8_BF16_NORM> { typedef u32x2 T; };
+
+template <int XF>
+__device__ __forceinline__ void convert_units(const GatherArgs& a, int part, const typename UnitOf<XF>::T (&v)[kUnroll],
+                                              const uint16_t* lut, int tid, typename OutUnit<XF>::T (&o)[kUnroll]) {
+    if constexpr (XF == kXfCopy16 || XF == CONDUIT_XF_NONE) {
+#pragma unroll
+        for (int r = 0; r < kUnroll; ++r) o[r] = v[r];
+    } else if constexpr (XF == CONDUIT_XF_U8_F32) {
+#pragma unroll
+        for (int r = 0; r < kUnroll; ++r) {
+            const uint32_t x = v[r];
+            o[r].x = u8_unit_f32(x & 255u);
+            o[r].y = u8_unit_f32((x >> 8) & 255u);
+            o[r].z = u8_unit_f32((x >> 16) & 255u);
+            o[r].w = u8_unit_f32(x >> 24);
+        }
+    } else {  // U8_BF16_NORM
+        const int64_t units = a.row_bytes >> 2;
+        const int64_t u0 = (int64_t)part * kUnitsPerBlock + tid;
+#pragma unroll
+        for (int r = 0; r < kUnroll; ++r) {
+            const int64_t u = u0 + (int64_t)r * kThreads;
+            const uint32_t uu = (uint32_t)(u < units ? u : units - 1);  // keeps the plane index in range
+            const uint16_t* tb = lut + (uu / (uint32_t)a.plane_units) * 256;
+            const uint32_t x = v[r];
+            o[r].x = (uint32_t)tb[x & 255u] | ((uint32_t)tb[(x >> 8) & 255u] << 16);
+            o[r].y = (uint32_t)tb[(x >> 16) & 255u] | ((uint32_t)tb[x >> 24] << 16);
+        }
+    }
+}
+
+template <typename O>
+__device__ __forceinline__ O zero_unit() {
+    return O{};
+}
+
+// The row: its sample's slot and bootstrap slot with their episode/step.
+struct UnionRow {
+    int64_t b, i, jn;
+    int K, n, S;
+    bool ok;          // i in [0, limit)
+    int32_t si, sn;   // step of slot i, of slot jn
+    uint32_t ei, en;  // episode of slot i, of slot jn
+};
+
+// The row of slot i; its bootstrap slot, if any, is the one n positions on,
+// (i + n) mod capacity, whose episode/step are loaded here already.  r.jn is
+// -1 until the caller sets it (the n-step window decides whether that slot is
+// the bootstrap state).
+__device__ __forceinline__ UnionRow union_row(const GatherArgs& a, int64_t b, int64_t i, int n, bool with_next) {
+    UnionRow r;
+    r.b = b;
+    r.i = i;
+    r.jn = -1;
+    r.K = a.stack;
+    r.n = n;
+    r.S = with_next ? (n < a.stack ? n : a.stack) : 0;
+    r.ok = i >= 0 && i < a.limit;
+    r.si = r.sn = 0;
+    r.ei = r.en = 0;
+    if (a.stack > 1) {  // kernel argument: uniform
+        const int64_t ii = r.ok ? i : 0;
+        const int64_t jc = r.ok ? (i + n) % a.capacity : 0;
+        r.si = a.step[ii];
+        r.ei = a.episode[ii];
+        r.sn = a.step[jc];
+        r.en = a.episode[jc];
+    }
+    return r;
+}
+
+struct UnionItem {
+    int u, part;
+    int64_t src;  // the slot read
+};
+
+__device__ __forceinline__ UnionItem union_item(const GatherArgs& a, const UnionRow& r, int64_t it, int32_t bpf) {
+    UnionItem t;
+    t.u = (int)(it / bpf);
+    t.part = (int)(it - (int64_t)t.u * bpf);
+    const int64_t off = t.u < r.K ? (int64_t)t.u - (r.K - 1) : (int64_t)(r.n - r.S + 1 + (t.u - r.K));
+    int64_t j = 0;
+    if (r.ok) {
+        j = (r.i + off) % a.capacity;
+        if (j < 0) j += a.capacity;
+    }
+    t.src = j;
+    return t;
+}
+
+template <int XF>
+__device__ __forceinline__ void union_issue(const GatherArgs& a, const UnionItem& t, typename UnitOf<XF>::T (&v)[kUnroll],
+                                            int32_t& sj, uint32_t& ej, int tid) {
+    typedef typename UnitOf<XF>::T U;
+    const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
+    const U* __restrict__ src = reinterpret_cast<const U*>(a.src + t.src * a.row_bytes);
+    const int64_t u0 = (int64_t)t.part * kUnitsPerBlock + tid;
+#pragma unroll
+    for (int r = 0; r < kUnroll; ++r) {
+        const int64_t u = u0 + (int64_t)r * kThreads;
+        v[r] = src[u < units ? u : units - 1];
+    }
+    if (a.stack > 1) {  // kernel argument: uniform
+        sj = a.step[t.src];
+        ej = a.episode[t.src];
+    }
+}
+
+// convert once, store into the state stack and / or the bootstrap stack
+template <int XF>
+__device__ __forceinline__ void union_finish(const GatherArgs& a, const UnionRow& r, const UnionItem& t,
+                                             const typename UnitOf<XF>::T (&v)[kUnroll], int32_t sj, uint32_t ej,
+                                             void* next_out, const uint16_t* lut, int tid) {
+    typedef typename OutUnit<XF>::T O;
+    const int64_t units = a.row_bytes >> UnitOf<XF>::kShift;
+    O o[kUnroll], z[kUnroll];
+    convert_units<XF>(a, t.part, v, lut, tid, o);
+    if (t.u < r.K) {  // uniform: frame u of the state stack
+        const int d = r.K - 1 - t.u;
+        const bool valid = d == 0 ? r.ok : (r.ok & (d <= r.si) & (r.ei == ej) & (sj == r.si - d));
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) z[k] = valid ? o[k] : zero_unit<O>();
+        store_at<kStoreWT>(a.out, r.b * r.K + t.u, t.part, units, tid, z);
+    }
+    const int kn = t.u < r.K ? t.u - r.n : t.u - r.S;
+    if (r.S > 0 && kn >= 0) {  // uniform: frame kn of the bootstrap stack
+        const int d = r.K - 1 - kn;
+        const bool valid = r.jn >= 0 && (d == 0 || ((d <= r.sn) & (r.en == ej) & (sj == r.sn - d)));
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) z[k] = valid ? o[k] : zero_unit<O>();
+        store_at<kStoreWT>(next_out, r.b * r.K + kn, t.part, units, tid, z);
+    }
+}
+
+// The union's work items that 256-lane group `part` of `parts` owns (tid: the
+// lane in the group): items part, part + parts, ... (the frames stored twice,
+// held by both stacks, spread over the groups), double-buffered as in
+// gather_row.  start() issues the first item's loads, which need only the
+// sample's slot; run() needs the bootstrap slot too (r.jn) and finishes the
+// items.  The first group also writes the state row's scalar columns, after
+// the frames.
+template <int XF>
+struct UnionGather {
+    typename UnitOf<XF>::T va[kUnroll], vb[kUnroll];
+    int32_t sja, sjb;
+    uint32_t eja, ejb;
+    UnionItem ta, tb;
+    RowScalar rs;
+
+    __device__ __forceinline__ void start(const GatherArgs& a, const UnionRow& r, int part, int32_t bpf, int tid) {
+        const int64_t items = (int64_t)(r.K + r.S) * bpf;
+        sja = sjb = 0;
+        eja = ejb = 0;
+        rs = RowScalar{0u, false};
+        if (part == 0) rs = row_scalars_load(a, r.i, tid);
+        if (part < items) {
+            ta = union_item(a, r, part, bpf);
+            union_issue<XF>(a, ta, va, sja, eja, tid);
+        }
+    }
+
+    __device__ __forceinline__ void run(const GatherArgs& a, const UnionRow& r, int part, int parts, int32_t bpf,
+                                        void* next_out, const uint16_t* lut, int tid) {
+        const int64_t items = (int64_t)(r.K + r.S) * bpf;
+        for (int64_t it = part; it < items; it += 2 * parts) {
+            const bool has_b = it + parts < items;  // uniform
+            if (has_b) {
+                tb = union_item(a, r, it + parts, bpf);
+                union_issue<XF>(a, tb, vb, sjb, ejb, tid);
+            }
+            union_finish<XF>(a, r, ta, va, sja, eja, next_out, lut, tid);
+            if (!has_b) break;
+            if (it + 2 * parts < items) {
+                ta = union_item(a, r, it + 2 * parts, bpf);
+                union_issue<XF>(a, ta, va, sja, eja, tid);
+            }
+            union_finish<XF>(a, r, tb, vb, sjb, ejb, next_out, lut, tid);
+        }
+        if (part == 0) row_scalars_store(a, r.b, r.i, rs, tid);
+    }
+};
 
 }  // namespace
 }  // namespace conduit

@@ -12,6 +12,7 @@
 // With the bootstrap frame stacks requested, k_nstep_gather evaluates the
 // windows inside the gather's own workgroups (one launch); otherwise k_nstep.
 #include "gather_dev.h"
+#include "nstep_dev.h"
 
 namespace conduit {
 
@@ -20,66 +21,9 @@ namespace {
 constexpr int kNstepWaves = 4;
 constexpr int kNstepThreads = kNstepWaves * kWave;
 
-// The window of sample b by one whole wavefront.  Returns the slot of the
-// bootstrap state (position p + n), or -1 when the sample has none (its episode
-// ended inside the window, the window is invalid, or the index is out of
-// range).  With `write`, lane 0 stores the sample's targets and flags a bad
-// index.
+// The window of sample b, at the slot its index names.
 __device__ __forceinline__ int64_t nstep_window(const NstepArgs& a, int64_t b, bool write) {
-    const int lane = lane_id();
-    const int64_t i = a.idx[b];
-    const bool ok = i >= 0 && i < a.size;  // wave-uniform
-    if (!ok) {
-        if (write && lane == 0) {
-            flag_error(a.err, ERR_GATHER_INDEX);
-            a.next_idx[b] = -1;
-            a.ret[b] = 0.0f;
-            a.discount[b] = 0.0f;
-            a.valid[b] = 0;
-        }
-        return -1;
-    }
-    // the stream position slot i holds: the newest q = i (mod capacity) below total
-    const int64_t p = i + ((a.total - 1 - i) / a.capacity) * a.capacity;
-    const int64_t q = p + lane;
-    const bool stored = lane <= a.n && q < a.total;
-    const int64_t s = stored ? q % a.capacity : i;  // clamped: every load is in range
-    const float r = a.reward[s];
-    const uint8_t d = a.done[s];
-    const uint32_t e = a.episode[s];
-    const uint32_t e0 = __builtin_amdgcn_readlane(e, 0);
-    const bool same = stored && e == e0;  // position p + lane continues the episode
-    const uint64_t gap = __ballot(lane < a.n && !same);
-    const uint64_t term = __ballot(lane < a.n && same && d != 0);
-    const uint64_t cont = __ballot(same);
-    const int first_gap = gap ? __ffsll((unsigned long long)gap) - 1 : 64;
-    const int first_term = term ? __ffsll((unsigned long long)term) - 1 : 64;
-    int m = 0;            // transitions summed
-    bool valid = false, bootstrap = false;
-    if (first_term < first_gap) {  // the episode ends inside the window
-        valid = true;
-        m = first_term + 1;
-    } else if (first_gap >= a.n && ((cont >> a.n) & 1ull)) {  // n transitions, state at p+n stored
-        valid = true;
-        bootstrap = true;
-        m = a.n;
-    }
-    const int64_t next = bootstrap ? (p + a.n) % a.capacity : -1;
-    if (write) {
-        double R = 0.0, g = 1.0;
-        for (int k = 0; k < m; ++k) {  // uniform trip count
-            const float rk = __shfl(r, k, kWave);
-            R += g * (double)rk;
-            g *= a.gamma;
-        }
-        if (lane == 0) {
-            a.next_idx[b] = next;
-            a.ret[b] = valid ? (float)R : 0.0f;
-            a.discount[b] = bootstrap ? (float)g : 0.0f;
-            a.valid[b] = valid ? 1 : 0;
-        }
-    }
-    return next;
+    return nstep_window_at(a, b, a.idx[b], write);
 }
 
 __global__ __launch_bounds__(kNstepThreads) void k_nstep(NstepArgs a) {

@@ -34,6 +34,7 @@
 // off the frame workgroups.
 #include "descend.h"
 #include "gather_dev.h"
+#include "nstep_dev.h"
 
 namespace conduit {
 
@@ -124,6 +125,81 @@ hipError_t launch_xf(const SampleArgs& sa, const GatherArgs& ga, hipStream_t s, 
                               FusedLaunch<XF>{sa, ga, make_divb((uint64_t)sa.batch), bpf, s});
 }
 
+// The fused sampler + gather with n-step targets: each gather workgroup's
+// first wavefront descends for its sample and issues the loads of the
+// sample's n-step window from the slot it found; once every wavefront knows
+// the slot, the two halves issue the loads of their first frames of the union
+// of the state stack and the bootstrap stack (UnionGather) while the first
+// wavefront evaluates the window (lane 0 writes the targets), and after a
+// second barrier, with the bootstrap slot known, they convert and store every
+// frame once into the stacks it belongs to.  Sampler workgroups as in
+// k_sample_gather.
+constexpr int kNstepWgsPerSample = 1;  // 512-lane workgroups per sample (2: 34.8 against 31.0 us per DQN batch, n = 3; past one residency round)
+
+template <int XF, int PRE, int DEPTH>
+__global__ __launch_bounds__(kWg) void k_sample_gather_nstep(SampleArgs sa, GatherArgs a, NstepArgs na,
+                                                             void* next_out, DivB dv, int32_t bpf,
+                                                             int32_t sampler_wgs) {
+    __shared__ uint16_t lut[(XF == CONDUIT_XF_U8_BF16_NORM) ? 4 * 256 : 1];
+    __shared__ int64_t s_slot, s_next;
+    const int64_t gather_wgs = (int64_t)gridDim.x - sampler_wgs;
+    if ((int64_t)blockIdx.x >= gather_wgs) {
+        sampler_wg<PRE, DEPTH>(sa, dv, (int64_t)blockIdx.x - gather_wgs);
+        return;
+    }
+    const int64_t b = blockIdx.x / kNstepWgsPerSample;
+    const int sub = (int)(blockIdx.x % kNstepWgsPerSample);
+    WindowLoads win;
+    if (threadIdx.x < kWave) {
+        const Descent d = tree_descend<PRE, DEPTH>(sa.tree, sa.uniforms, b, dv);
+        const int64_t slot = __builtin_amdgcn_readfirstlane((uint32_t)d.slot) |
+                             ((int64_t)__builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)d.slot >> 32)) << 32);
+        win = nstep_window_load(na, slot);  // in flight across the barrier
+        if (threadIdx.x == 0) s_slot = slot;
+    } else if constexpr (XF == CONDUIT_XF_U8_BF16_NORM) {
+        build_lut(a, lut, kWave, kWg - kWave);
+    }
+    __syncthreads();  // the slot is known
+    UnionRow r = union_row(a, b, s_slot, na.n, next_out != nullptr);
+    const int half = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kThreads));
+    const int part = sub * 2 + half, tid = (int)(threadIdx.x % kThreads);
+    UnionGather<XF> g;
+    g.start(a, r, part, bpf, tid);  // the first frames' loads, while the window is evaluated
+    if (threadIdx.x < kWave) {
+        const int64_t next = nstep_window_finish(na, b, win, sub == 0);
+        if (threadIdx.x == 0) s_next = next;
+    }
+    __syncthreads();  // the bootstrap slot is known
+    r.jn = r.S > 0 ? s_next : -1;
+    g.run(a, r, part, 2 * kNstepWgsPerSample, bpf, next_out, lut, tid);
+}
+
+template <int XF>
+struct FusedNstepLaunch {
+    const SampleArgs& sa;
+    const GatherArgs& ga;
+    const NstepArgs& na;
+    void* next_out;
+    DivB dv;
+    int64_t bpf;
+    hipStream_t s;
+    template <int PRE, int DEPTH>
+    hipError_t operator()() const {
+        const int64_t sampler_wgs = (sa.batch + kSamplesPerSamplerWg - 1) / kSamplesPerSamplerWg;
+        const dim3 grid((unsigned)(sampler_wgs + sa.batch * kNstepWgsPerSample)), block(kWg);
+        hipLaunchKernelGGL((k_sample_gather_nstep<XF, PRE, DEPTH>), grid, block, 0, s, sa, ga, na, next_out, dv,
+                           (int32_t)bpf, (int32_t)sampler_wgs);
+        return hipGetLastError();
+    }
+};
+
+template <int XF>
+hipError_t launch_nstep_xf(const SampleArgs& sa, const GatherArgs& ga, const NstepArgs& na, void* next_out,
+                           hipStream_t s, int64_t bpf) {
+    return with_descent_shape(sa.tree, descend_prefetch(sa.tree),
+                              FusedNstepLaunch<XF>{sa, ga, na, next_out, make_divb((uint64_t)sa.batch), bpf, s});
+}
+
 }  // namespace
 
 hipError_t launch_sample_gather(const SampleArgs& sa, const GatherArgs& ga, hipStream_t s) {
@@ -137,6 +213,24 @@ hipError_t launch_sample_gather(const SampleArgs& sa, const GatherArgs& ga, hipS
         case CONDUIT_XF_NONE: return launch_xf<CONDUIT_XF_NONE>(sa, ga, s, bpf);
         case CONDUIT_XF_U8_F32: return launch_xf<CONDUIT_XF_U8_F32>(sa, ga, s, bpf);
         case CONDUIT_XF_U8_BF16_NORM: return launch_xf<CONDUIT_XF_U8_BF16_NORM>(sa, ga, s, bpf);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_sample_gather_nstep(const SampleArgs& sa, const GatherArgs& ga, const NstepArgs& na,
+                                      void* next_out, hipStream_t s) {
+    const bool c16 = copy16(ga);
+    const int64_t units = ga.row_bytes >> (c16 ? 4 : 2);
+    const int64_t bpf = ga.out && units > 0 ? (units + kUnitsPerBlock - 1) / kUnitsPerBlock : 0;
+    const int64_t frames = ga.stack + (next_out ? (na.n < ga.stack ? na.n : ga.stack) : 0);
+    if (sa.batch <= 0 || na.batch != sa.batch || ga.ncols != 0 || bpf < 1 ||
+        bpf * frames > kFusedNstepMaxItemsPerRow)
+        return hipErrorNotSupported;
+    if (c16) return launch_nstep_xf<kXfCopy16>(sa, ga, na, next_out, s, bpf);
+    switch (ga.xform) {
+        case CONDUIT_XF_NONE: return launch_nstep_xf<CONDUIT_XF_NONE>(sa, ga, na, next_out, s, bpf);
+        case CONDUIT_XF_U8_F32: return launch_nstep_xf<CONDUIT_XF_U8_F32>(sa, ga, na, next_out, s, bpf);
+        case CONDUIT_XF_U8_BF16_NORM: return launch_nstep_xf<CONDUIT_XF_U8_BF16_NORM>(sa, ga, na, next_out, s, bpf);
         default: return hipErrorInvalidValue;
     }
 }

@@ -90,6 +90,25 @@ def _check_nstep(buf, orc, idx_d, o_idx, n, gamma, xf_kind, row_shape, obs_kind=
     return o_v
 
 
+def _assert_nstep_outputs(orc, o_idx, n, gamma, xf_kind, nxt, ret, disc, val, nobs):
+    """n-step outputs of one delivery against the oracle (bootstrap stacks:
+    zero rows where there is none); returns the oracle's targets."""
+    B = len(o_idx)
+    o_n, o_r, o_d, o_v = orc.nstep(o_idx, n, gamma)
+    assert np.array_equal(host(nxt), o_n)
+    assert np.array_equal(host(val), o_v)
+    np.testing.assert_allclose(host(ret), o_r, rtol=1e-6, atol=1e-6)
+    assert np.array_equal(host(disc), o_d)
+    if nobs is not None:
+        g = host(nobs).reshape(B, -1).view(np.uint8)
+        boot = o_n >= 0
+        if boot.any():
+            want, _, _, _ = orc.gather(o_n[boot], oracle.XF_U8_F32 if xf_kind == cd.XF_U8_F32 else oracle.XF_NONE)
+            assert np.array_equal(g[boot], want.reshape(int(boot.sum()), -1).view(np.uint8))
+        assert not g[~boot].any()
+    return o_n, o_r, o_d, o_v
+
+
 @pytest.mark.parametrize("n", [1, 3])
 def test_nstep_rows_of_many_items(n):
     """Bootstrap stacks of rows too large for the one-launch kernel (3x84x84
@@ -113,12 +132,25 @@ def test_nstep_rows_of_many_items(n):
     o_idx = rng.integers(0, cap, 97).astype(np.int64)
     valid = _check_nstep(buf, orc, dev(o_idx), o_idx, n, 0.97, cd.XF_U8_F32, shape)
     assert valid.any()
+    # the fused call on these rows (more work items than one launch takes):
+    # the two calls it stands for
+    u = rng.integers(0, 1 << 63, size=64, dtype=np.int64)
+    obs_o = torch.empty((64, K) + shape, dtype=torch.float32, device="cuda")
+    nobs = torch.full((64, K) + shape, 7.0, dtype=torch.float32, device="cuda")
+    idx, w, nxt, ret, disc, val = buf.sample_gather_nstep(dev(u), cd.transform(cd.XF_U8_F32), n, 0.97,
+                                                          next_obs=nobs, obs=obs_o)
+    o_idx2, o_w2 = orc.sample(u.view(np.uint64))
+    assert np.array_equal(host(idx), o_idx2)
+    assert_weights_close(host(w), o_w2)
+    o_obs = orc.gather(o_idx2, oracle.XF_U8_F32)[0]
+    assert np.array_equal(host(obs_o).view(np.uint32).reshape(64, -1), o_obs.view(np.uint32).reshape(64, -1))
+    _assert_nstep_outputs(orc, o_idx2, n, 0.97, cd.XF_U8_F32, nxt, ret, disc, val, nobs)
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
 
 
 def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH,
-              nstep=None, update_ingest=False):
+              nstep=None, update_ingest=False, fused_nstep=None):
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
@@ -151,7 +183,12 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
         ingest(pos, pos + n_in, pending)
         pending = None
         pos += n_in
-        if fused:
+        if fused_nstep is not None:
+            nobs_f = torch.full((B, 1, 8), 7.0, dtype=torch.float32, device="cuda")
+            idx, w, f_nxt, f_ret, f_disc, f_val = buf.sample_gather_nstep(
+                dev(u[it]), xf, fused_nstep[0], fused_nstep[1], next_obs=nobs_f, obs=obs_out, action=act_out,
+                reward=rew_out, done=done_out)
+        elif fused:
             idx, w = buf.sample_gather(dev(u[it]), xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
         else:
             idx, w = buf.sample(dev(u[it]))
@@ -159,6 +196,9 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
         o_idx, o_w = orc.sample(u[it])
         if nstep is not None:
             _check_nstep(buf, orc, idx, o_idx, nstep[0], nstep[1], cd.XF_NONE, (8,), torch.float32)
+        if fused_nstep is not None:
+            _assert_nstep_outputs(orc, o_idx, fused_nstep[0], fused_nstep[1], cd.XF_NONE, f_nxt, f_ret, f_disc,
+                                  f_val, nobs_f)
         o_obs, o_act, o_rew, o_done = orc.gather(o_idx)
         if update_ingest and it + 1 < iters:  # applied with the next ingest
             pending = (idx.clone(), prio[it], o_idx)
@@ -208,6 +248,13 @@ def test_tiny_config_update_ingest_one_call(fused):
     _run_tiny(prefill=20000, iters=30, seed_shift=12, fused=fused, update_ingest=True)
 
 
+@pytest.mark.parametrize("n,gamma", [(1, 0.99), (5, 0.99), (63, 0.9)])
+def test_tiny_config_sample_gather_nstep_one_launch(n, gamma):
+    print(f"tiny config: sample + gather + {n}-step in one call", flush=True)
+    _run_tiny(prefill=0, iters=20, seed_shift=13, fused_nstep=(n, gamma))
+    _run_tiny(prefill=20000, iters=10, seed_shift=14, fused_nstep=(n, gamma), weight_norm=cd.WNORM_BUFFER)
+
+
 @pytest.mark.parametrize("n,gamma", [(1, 0.99), (3, 0.99), (63, 0.9)])
 def test_tiny_config_nstep_targets(n, gamma):
     print(f"tiny config: {n}-step targets", flush=True)
@@ -235,10 +282,12 @@ def test_tiny_config_payload_in_pinned_host_memory(fused):
 # configuration 1 (DQN, frame stack 4, u8 -> fp32/255) at reduced capacity
 # ----------------------------------------------------------------------------
 def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False,
-            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH, nstep=None, update_ingest=False):
+            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH, nstep=None, update_ingest=False, fused_nstep=None):
     """Drive GPU buffer and oracle through the same DQN stream; the oracle keeps
     metadata only and its observation rows are regenerated for the slots a
-    gather reads."""
+    gather reads.  fused_nstep = (n, gamma): every delivery goes through
+    conduit_sample_gather_nstep (batch, targets and bootstrap stacks in one
+    call), checked against the oracle and, bit for bit, against conduit_nstep."""
     n_total = prefill + iters * batch
     cfg = synth.DQN(n_total)
     if short_episodes:  # many episode starts: exercises the zero fill
@@ -279,7 +328,12 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
         ingest(pos, pos + batch, with_prio=False, pending=pending)
         pending = None
         pos += batch
-        if fused:
+        if fused_nstep is not None:
+            nobs_f = torch.full((batch, K, 84, 84), 7.0, dtype=torch.float32, device="cuda")
+            idx, w, f_nxt, f_ret, f_disc, f_val = buf.sample_gather_nstep(
+                dev(u[it]), xf, fused_nstep[0], fused_nstep[1], next_obs=nobs_f, obs=obs_out, action=act_out,
+                reward=rew_out, done=done_out)
+        elif fused:
             idx, w = buf.sample_gather(dev(u[it]), xf, obs=obs_out, action=act_out, reward=rew_out, done=done_out)
         else:
             idx, w = buf.sample(dev(u[it]))
@@ -293,8 +347,9 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
         assert_weights_close(host(w), o_w)
         rows = np.arange(batch) if check_rows is None else check_rows
         sel = o_idx[rows]
-        if nstep is not None:  # the bootstrap stacks need their frames too
-            o_next = orc.nstep(o_idx, nstep[0], nstep[1])[0]
+        ns = nstep if nstep is not None else fused_nstep
+        if ns is not None:  # the bootstrap stacks need their frames too
+            o_next = orc.nstep(o_idx, ns[0], ns[1])[0]
             sel_all = np.concatenate([sel, o_next[o_next >= 0]])
         else:
             sel_all = sel
@@ -310,6 +365,16 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
         assert np.array_equal(host(done_out)[rows], o_done), it
         if nstep is not None:
             _check_nstep(buf, orc, idx, o_idx, nstep[0], nstep[1], cd.XF_U8_F32, (84, 84))
+        if fused_nstep is not None:
+            fn, fg = fused_nstep
+            _assert_nstep_outputs(orc, o_idx, fn, fg, cd.XF_U8_F32, f_nxt, f_ret, f_disc, f_val, nobs_f)
+            # bit for bit what conduit_nstep writes for the same indices
+            t_nxt, t_ret = torch.empty_like(f_nxt), torch.empty_like(f_ret)
+            t_disc, t_val = torch.empty_like(f_disc), torch.empty_like(f_val)
+            t_obs = torch.empty_like(nobs_f)
+            cd.conduit_nstep(buf.handle, idx, fn, fg, t_nxt, t_ret, t_disc, t_val, xf, t_obs)
+            for x, y in [(f_nxt, t_nxt), (f_ret, t_ret), (f_disc, t_disc), (f_val, t_val), (nobs_f, t_obs)]:
+                assert np.array_equal(host(x).view(np.uint8), host(y).view(np.uint8)), it
         orc.update(o_idx, prio[it])
     assert buf.sync_check() == cd.OK, cd.last_error()
     leaves = read_col(buf, cd.COL_LEAVES, cap * 4, np.uint32)
@@ -352,6 +417,13 @@ def test_dqn_nstep_targets_and_next_stacks(n, short):
     print(f"dqn: {n}-step targets and bootstrap stacks, short episodes={short}", flush=True)
     run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused=True,
             nstep=(n, 0.99))
+
+
+@pytest.mark.parametrize("n,short", [(1, True), (3, False), (4, True), (7, True)])
+def test_dqn_sample_gather_nstep_one_launch(n, short):
+    # n < K: the stacks share K - n frames (K + n read); n >= K: disjoint (2K read)
+    print(f"dqn: sample + gather + {n}-step in one call, short episodes={short}", flush=True)
+    run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused_nstep=(n, 0.99))
 
 
 @pytest.mark.parametrize("fused", [False, True])
