@@ -526,8 +526,14 @@ struct SegChunk {
     f32x4 fv[TRUNC ? L : 1];
     f32x4 ve;
 
-    __device__ __forceinline__ void load(const GaeArgs& a, int64_t t0, int64_t e0) {
+    // c: the lane's chunk in the tile.  The value after the chunk's last step
+    // (ve) is the next chunk's first value, which the next lane of the DPP row
+    // loads anyway; the lane loads it itself only in a wavefront's last chunk
+    // (c % 8 == 7) and past the rollout's end (the bootstrap).
+    __device__ __forceinline__ void load(const GaeArgs& a, int64_t t0, int64_t e0, int c) {
         const int64_t E = a.E, T = a.T;
+        const bool own = c % kChunksPerWave == kChunksPerWave - 1 || t0 + L >= T;
+        ve = (f32x4)(0.0f);
         if constexpr (V4) {
 #pragma unroll
             for (int k = 0; k < L; ++k) {
@@ -542,8 +548,10 @@ struct SegChunk {
                 }
             }
             const int64_t t1 = t0 + L;
-            if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4*>(a.bootstrap + e0) : (f32x4)(0.0f);
-            else ve = a.value ? *reinterpret_cast<const f32x4*>(a.value + t1 * E + e0) : (f32x4)(0.0f);
+            if (own) {
+                if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4*>(a.bootstrap + e0) : (f32x4)(0.0f);
+                else ve = a.value ? *reinterpret_cast<const f32x4*>(a.value + t1 * E + e0) : (f32x4)(0.0f);
+            }
         } else if (E >= kV) {
             // 16 bytes per float row at a 4-byte aligned address (dword
             // alignment is all a multi-dword load needs).  A quad reaching past
@@ -565,8 +573,10 @@ struct SegChunk {
                 }
             }
             const int64_t t1 = t0 + L;
-            if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4u*>(a.bootstrap + eb) : (f32x4)(0.0f);
-            else ve = a.value ? *reinterpret_cast<const f32x4u*>(a.value + t1 * E + eb) : (f32x4)(0.0f);
+            if (own) {
+                if (t1 >= T) ve = a.bootstrap ? *reinterpret_cast<const f32x4u*>(a.bootstrap + eb) : (f32x4)(0.0f);
+                else ve = a.value ? *reinterpret_cast<const f32x4u*>(a.value + t1 * E + eb) : (f32x4)(0.0f);
+            }
             if (sh) {
 #pragma unroll
                 for (int k = 0; k < L; ++k) {
@@ -605,12 +615,22 @@ struct SegChunk {
                 }
             }
             const int64_t t1 = t0 + L;
+            if (own) {
 #pragma unroll
-            for (int j = 0; j < kV; ++j) {
-                if (t1 >= T) ve[j] = a.bootstrap ? a.bootstrap[ec[j]] : 0.0f;
-                else ve[j] = a.value ? a.value[t1 * E + ec[j]] : 0.0f;
+                for (int j = 0; j < kV; ++j) {
+                    if (t1 >= T) ve[j] = a.bootstrap ? a.bootstrap[ec[j]] : 0.0f;
+                    else ve[j] = a.value ? a.value[t1 * E + ec[j]] : 0.0f;
+                }
             }
         }
+        // the other lanes: the next lane's first value (row_shl:1 moves lane
+        // i + 1 into lane i; every lane runs it, the loads above are in place)
+        f32x4 up;
+#pragma unroll
+        for (int j = 0; j < kV; ++j)
+            up[j] = __uint_as_float((uint32_t)__builtin_amdgcn_update_dpp(0, (int)__float_as_uint(v[0][j]),
+                                                                          kDppRowShl + 1, 0xf, 0xf, true));
+        if (!own) ve = up;
     }
 
     __device__ __forceinline__ void step(const GaeArgs& a, double gl, int k, int j, double vn, double* delta,
@@ -717,7 +737,7 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_fold(GaeArgs a, int32_t
     const int64_t e0 = quad_base<V4>(e_raw, E);
     const int64_t t0 = s * Ts + (int64_t)c * L;
     SegChunk<TRUNC, L, V4> ch;
-    ch.load(a, t0, e0);
+    ch.load(a, t0, e0, c);
     const Map4 own = ch.fold(a, a.gamma * a.lambda, t0);
     Map4 incl, excl;
     tile_suffix(own, c, q, &incl, &excl);
@@ -816,7 +836,7 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_seg_replay(GaeArgs a, int32
         chi = get_words<V4>(a.adv, row0 + 1, E, e0);
     }
     SegChunk<TRUNC, L, V4> ch;
-    ch.load(a, t0, e0);
+    ch.load(a, t0, e0, c);
     const double gl = a.gamma * a.lambda;
     const Map4 own = ch.fold(a, gl, t0);
     double cin[kV];
@@ -926,7 +946,7 @@ __global__ __launch_bounds__(kSegThreads) void k_gae_look(GaeArgs a, LookTable* 
     const int64_t t0 = s * Ts + (int64_t)c * L;
     const double gl = a.gamma * a.lambda;
     SegChunk<TRUNC, L, V4> ch;
-    ch.load(a, t0, e0);
+    ch.load(a, t0, e0, c);
     const Map4 own = ch.fold(a, gl, t0);
     Map4 incl, excl;
     tile_suffix(own, c, q, &incl, &excl);  // incl of chunk 0: the segment's map
