@@ -447,6 +447,12 @@ def test_dqn_full_capacity(fused):
     run_dqn(cap=1_000_000, prefill=1_050_000, iters=3, batch=512, chunk=4096, fused=fused)
 
 
+@pytest.mark.slow
+def test_dqn_full_capacity_nstep_one_launch():
+    print("dqn: full size cap 1M, batch + 3-step targets + bootstrap stacks in one call", flush=True)
+    run_dqn(cap=1_000_000, prefill=1_050_000, iters=2, batch=512, chunk=4096, fused_nstep=(3, 0.99))
+
+
 # ----------------------------------------------------------------------------
 # fused sample + gather: every transform, stacked and single frames, odd sizes
 # ----------------------------------------------------------------------------
