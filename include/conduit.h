@@ -87,7 +87,7 @@ typedef struct {
     /* importance-sampling exponent beta >= 0.  Default 0.4. */
     double beta;
     /* observations per sample returned by gather (frame stacking), 1..16.
-     * K > 1 needs episode_id and step on every ingest.  Default 1. */
+     * Default 1. */
     int32_t frame_stack;
     /* bytes of one action (any layout; copied verbatim), 0..256.  Default 4. */
     int32_t action_bytes;
@@ -182,9 +182,14 @@ typedef struct {
     const void* action;          /* device [n, action_bytes] or NULL (zeros) */
     const float* reward;         /* device [n] or NULL (zeros) */
     const uint8_t* done;         /* device [n] or NULL (zeros) */
-    const uint32_t* episode_id;  /* device [n] or NULL; required when frame_stack > 1 */
-    const int32_t* step;         /* device [n] step index within the episode (>= 0) or NULL;
-                                    required when frame_stack > 1 */
+    /* device [n] episode ids and step indices within the episode (>= 0).  NULL:
+     * derived from done as one stream (the transitions of every ingest follow
+     * the buffer's last stored transition): a transition continues its
+     * predecessor's episode one step on, unless the predecessor's done ended
+     * it, when it starts the next episode id at step 0; the first transition
+     * ever is episode 0, step 0.  Deriving costs one more small launch. */
+    const uint32_t* episode_id;
+    const int32_t* step;
     const uint32_t* prio;        /* device [n] priorities or NULL: the running maximum */
 } conduit_transitions;
 

@@ -171,7 +171,11 @@ uint64_t orc_total_priority(const orc_replay* r) { return r->tree[1]; }
 
 /*
  * Insert n transitions at slots (head + j) mod capacity, overwriting the oldest
- * ones once the ring is full (eviction).  episode/step may be NULL (not kept).
+ * ones once the ring is full (eviction).  episode/step NULL: derived from done
+ * as one stream (tuples carry an episode ID, Sec. 2.1; the reading for callers
+ * that give none): a transition continues its predecessor's episode one step
+ * on, unless the predecessor was done, when it starts the next episode at step
+ * 0; the first transition ever is episode 0, step 0.
  * prio NULL: every new transition gets the running maximum priority.
  * Ragged datasets take concatenated sequences: row j spans elements
  * [offsets[j], offsets[j+1]) of obs and aux.
@@ -207,10 +211,18 @@ int32_t orc_ingest(orc_replay* r, int64_t n, const uint8_t* obs, const int64_t* 
         }
         if (r->ragged) r->length[s] = (int32_t)(offsets[j + 1] - offsets[j]);
         if (action) memcpy(r->action + s * r->act_bytes, action + j * r->act_bytes, (size_t)r->act_bytes);
+        /* the predecessor (stream position total + j - 1) sits in the slot before s */
+        uint32_t ep_d = 0;
+        int32_t st_d = 0;
+        if (r->total + j > 0) {
+            int64_t ps = (s + r->capacity - 1) % r->capacity;
+            ep_d = r->episode[ps] + (r->done[ps] ? 1u : 0u);
+            st_d = r->done[ps] ? 0 : r->step[ps] + 1;
+        }
         r->reward[s] = reward ? reward[j] : 0.0f;
         r->done[s] = done ? done[j] : 0;
-        r->episode[s] = episode ? episode[j] : 0;
-        r->step[s] = step ? step[j] : 0;
+        r->episode[s] = episode ? episode[j] : ep_d;
+        r->step[s] = step ? step[j] : st_d;
         r->position[s] = r->total + j;
         uint32_t p = prio ? prio[j] : fill_prio;
         tree_set(r, s, orc_leaf(p, r->alpha_num, r->alpha_den));

@@ -474,8 +474,6 @@ static conduit_status ingest_args(conduit_buffer* b, const conduit_transitions* 
     if (o.ragged && !t->offsets) return fail(CONDUIT_EINVAL, "ragged ingest needs offsets");
     if (o.ragged && t->src_elems < 0) return fail(CONDUIT_EINVAL, "ragged ingest needs src_elems >= 0");
     if (o.ragged && t->aux && reinterpret_cast<uintptr_t>(t->aux) % 4) return fail(CONDUIT_EINVAL, "aux must be 4-byte aligned");
-    if (o.frame_stack > 1 && (!t->episode_id || !t->step))
-        return fail(CONDUIT_EINVAL, "frame-stacking buffers need episode_id and step");
     IngestArgs a{};
     a.obs = b->obs;
     a.aux = b->aux;
@@ -504,6 +502,8 @@ static conduit_status ingest_args(conduit_buffer* b, const conduit_transitions* 
     a.src_prio = o.prioritized ? t->prio : nullptr;
     a.n = t->n;
     a.head = b->head;
+    a.total = b->total;
+    a.derive = (t->episode_id ? 0 : kDeriveEpisode) | (t->step ? 0 : kDeriveStep);
     a.tree = b->tree;
     a.state = b->state;
     a.err = err_words(b->err_slot);
@@ -545,7 +545,8 @@ conduit_status conduit_ingest(conduit_buffer* b, const conduit_transitions* t, v
     st = ingest_args(b, t, &a);
     if (st != CONDUIT_OK) return st;
     DeviceGuard g(b->device);
-    hipError_t e = launch_ingest(a, static_cast<hipStream_t>(stream));
+    hipError_t e = launch_derive_meta(a, static_cast<hipStream_t>(stream));
+    if (e == hipSuccess) e = launch_ingest(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "ingest launch");
     advance_ring(b, t->n);
     return CONDUIT_OK;
@@ -592,12 +593,15 @@ conduit_status conduit_update_ingest(conduit_buffer* b, const int64_t* idx, cons
     }
     DeviceGuard g(b->device);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = hipSuccess;
-    if (n_update > 0 && t->n > 0 && !b->opts.ragged && t->n <= kFusedIngestMaxRows) {
-        e = launch_update_ingest(u, a, s);
-    } else {  // the same two operations, one launch each
-        if (n_update > 0) e = launch_update(u, s);
-        if (e == hipSuccess && t->n > 0) e = launch_ingest(a, s);
+    // derived episode/step columns first: the update does not read them
+    hipError_t e = t->n > 0 ? launch_derive_meta(a, s) : hipSuccess;
+    if (e == hipSuccess) {
+        if (n_update > 0 && t->n > 0 && !b->opts.ragged && t->n <= kFusedIngestMaxRows) {
+            e = launch_update_ingest(u, a, s);
+        } else {  // the same two operations, one launch each
+            if (n_update > 0) e = launch_update(u, s);
+            if (e == hipSuccess && t->n > 0) e = launch_ingest(a, s);
+        }
     }
     if (e != hipSuccess) return hip_fail(e, "update + ingest launch");
     advance_ring(b, t->n);

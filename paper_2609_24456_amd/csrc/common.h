@@ -298,10 +298,17 @@ struct IngestArgs {
     int64_t head;
     TreeView tree;
     DeviceState* state;
+    int64_t total;           // stream position of row 0 (transitions ingested before)
+    int32_t derive;          // kDeriveEpisode | kDeriveStep: columns the caller left NULL,
+                             // derived from done and written into the ring before the ingest
     uint32_t* err;
 };
 
+constexpr int32_t kDeriveEpisode = 1, kDeriveStep = 2;
 hipError_t launch_ingest(const IngestArgs& a, hipStream_t s);
+// the derived episode / step columns of an ingest (a.derive != 0), written into
+// the ring at the rows' slots; enqueue before the ingest itself
+hipError_t launch_derive_meta(const IngestArgs& a, hipStream_t s);
 
 struct UpdateArgs {
     TreeView tree;

@@ -243,8 +243,8 @@ __device__ __forceinline__ void ingest_meta(const IngestArgs& a, int64_t block, 
         }
         a.reward[slot] = rew;
         a.done[slot] = dn;
-        a.episode[slot] = ep;
-        a.step[slot] = st;
+        if (!(a.derive & kDeriveEpisode)) a.episode[slot] = ep;  // else written by the derive pass
+        if (!(a.derive & kDeriveStep)) a.step[slot] = st;
         if (a.length) {
             int64_t l = len;
             if (!span_ok) flag_error(a.err, ERR_OFFSETS);

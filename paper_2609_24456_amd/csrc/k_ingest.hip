@@ -40,7 +40,85 @@ __global__ __launch_bounds__(kIngestThreads) void k_ingest(IngestArgs a, int64_t
     }
 }
 
+// Episode id and step of the rows of a single stream, from their done flags
+// (the caller gave none): transition t + 1 continues t's episode one step on,
+// unless t ended it (done), when t + 1 starts the next episode at step 0; the
+// first transition ever is episode 0, step 0.  So for row j, with the
+// previous transition (position total - 1, in the slot before head) as row -1:
+//   episode(j) = episode(-1) + #{done among rows -1 .. j-1}
+//   step(j)    = j - start(j),  start(j) = 1 + the last row k < j with done,
+//                or, without one, -(step(-1) + 1) (the episode continues).
+// One workgroup: each lane counts the dones of its contiguous share of rows,
+// the lanes' counts and last done rows are scanned in LDS, then every lane
+// walks its share again writing both columns into the ring.
+constexpr int kDeriveThreads = 1024;
+
+__global__ __launch_bounds__(kDeriveThreads) void k_derive_meta(IngestArgs a) {
+    __shared__ int64_t s_cnt[2][kDeriveThreads];
+    __shared__ int64_t s_last[2][kDeriveThreads];
+    __shared__ uint32_t s_ep0;
+    __shared__ int64_t s_start0;
+    const int tid = threadIdx.x;
+    const int64_t per = (a.n + kDeriveThreads - 1) / kDeriveThreads;
+    const int64_t lo = (int64_t)tid * per < a.n ? (int64_t)tid * per : a.n;
+    const int64_t hi = lo + per < a.n ? lo + per : a.n;
+    if (tid == 0) {  // row -1: read before any slot is rewritten (the barriers below)
+        uint32_t ep0 = 0;
+        int64_t start0 = 0;
+        if (a.total > 0) {
+            const int64_t ps = (a.head + a.capacity - 1) % a.capacity;
+            const bool pd = a.done[ps] != 0;
+            ep0 = a.episode[ps] + (pd ? 1u : 0u);
+            start0 = pd ? 0 : -((int64_t)a.step[ps] + 1);
+        }
+        s_ep0 = ep0;
+        s_start0 = start0;
+    }
+    int64_t cnt = 0, last = -1;
+    if (a.src_done) {
+        for (int64_t j = lo; j < hi; ++j) {
+            if (a.src_done[j]) {
+                ++cnt;
+                last = j;
+            }
+        }
+    }
+    // inclusive scans over the lanes (sum of counts, max of last done rows),
+    // ping-ponging between two LDS rows
+    int cur = 0;
+    s_cnt[0][tid] = cnt;
+    s_last[0][tid] = last;
+    __syncthreads();
+    for (int d = 1; d < kDeriveThreads; d <<= 1) {
+        const int64_t c = s_cnt[cur][tid] + (tid >= d ? s_cnt[cur][tid - d] : 0);
+        const int64_t l0 = s_last[cur][tid], l1 = tid >= d ? s_last[cur][tid - d] : -1;
+        s_cnt[cur ^ 1][tid] = c;
+        s_last[cur ^ 1][tid] = l0 > l1 ? l0 : l1;
+        cur ^= 1;
+        __syncthreads();
+    }
+    const int64_t excl_cnt = tid > 0 ? s_cnt[cur][tid - 1] : 0;
+    const int64_t excl_last = tid > 0 ? s_last[cur][tid - 1] : -1;
+    uint32_t ep = s_ep0 + (uint32_t)excl_cnt;
+    int64_t start = excl_last >= 0 ? excl_last + 1 : s_start0;
+    for (int64_t j = lo; j < hi; ++j) {
+        const int64_t slot = (a.head + j) % a.capacity;
+        if (a.derive & kDeriveEpisode) a.episode[slot] = ep;
+        if (a.derive & kDeriveStep) a.step[slot] = (int32_t)(j - start);
+        if (a.src_done && a.src_done[j]) {
+            ++ep;
+            start = j + 1;
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_derive_meta(const IngestArgs& a, hipStream_t s) {
+    if (a.n <= 0 || !a.derive) return hipSuccess;
+    hipLaunchKernelGGL(k_derive_meta, dim3(1), dim3(kDeriveThreads), 0, s, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_ingest(const IngestArgs& a, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;

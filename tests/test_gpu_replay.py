@@ -150,7 +150,7 @@ def test_nstep_rows_of_many_items(n):
 
 
 def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH,
-              nstep=None, update_ingest=False, fused_nstep=None):
+              nstep=None, update_ingest=False, fused_nstep=None, derive_meta=False):
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
@@ -160,15 +160,16 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
     def ingest(a, b, pending=None):
         """ingest rows [a, b); `pending` (idx, prio) is a priority update that
         precedes it, applied through the one-call update + ingest"""
-        cols = dict(action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]), done=dev(cfg.done[a:b]),
-                    episode_id=dev(cfg.episode[a:b]), step=dev(cfg.step[a:b]))
+        meta = dict(episode_id=None, step=None) if derive_meta else dict(episode_id=dev(cfg.episode[a:b]),
+                                                                          step=dev(cfg.step[a:b]))
+        cols = dict(action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]), done=dev(cfg.done[a:b]), **meta)
         if pending is not None:
             buf.update_ingest(pending[0], dev(pending[1]), dev(cfg.obs[a:b]), **cols)
             orc.update(pending[2], pending[1])
         else:
             buf.ingest(dev(cfg.obs[a:b]), **cols)
         orc.ingest(b - a, obs=cfg.obs[a:b], action=cfg.action[a:b], reward=cfg.reward[a:b], done=cfg.done[a:b],
-                   episode=cfg.episode[a:b], step=cfg.step[a:b])
+                   episode=None if derive_meta else cfg.episode[a:b], step=None if derive_meta else cfg.step[a:b])
 
     for a in range(0, prefill, C // 2):
         ingest(a, min(prefill, a + C // 2))
@@ -222,6 +223,10 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
     written = orc.position >= 0
     got = read_col(buf, cd.COL_OBS, C * 32, np.uint8).reshape(C, 32)
     assert np.array_equal(got[written], orc.obs[written])
+    ep = read_col(buf, cd.COL_EPISODE, C * 4, np.uint32)
+    st = read_col(buf, cd.COL_STEP, C * 4, np.int32)
+    assert np.array_equal(ep[written], orc.episode[written])
+    assert np.array_equal(st[written], orc.step[written])
     buf.close()
 
 
@@ -246,6 +251,34 @@ def test_tiny_config_update_ingest_one_call(fused):
     print(f"tiny config: update + ingest in one call, fused sample={fused}", flush=True)
     _run_tiny(prefill=0, iters=60, seed_shift=11, fused=fused, update_ingest=True)
     _run_tiny(prefill=20000, iters=30, seed_shift=12, fused=fused, update_ingest=True)
+
+
+def test_derived_episodes_whole_ring_ingests():
+    # ingests of the whole ring (the predecessor's slot is rewritten by the
+    # same call) and of single rows, against the oracle after every call
+    print("derived episodes: whole-ring and single-row ingests", flush=True)
+    rng = np.random.default_rng(77)
+    cap = 100
+    buf = _mk(cap, (4,), torch.float32, action_bytes=0)
+    orc = oracle.Replay(cap, (4,), np.float32, act_bytes=0)
+    for n in [30, 100, 7, 100, 1, 1, 99, 100]:
+        obs = rng.standard_normal((n, 4)).astype(np.float32)
+        done = (rng.random(n) < 0.2).astype(np.uint8)
+        buf.ingest(dev(obs), done=dev(done))
+        orc.ingest(n, obs=obs, done=done)
+        held = orc.position >= 0
+        ep = read_col(buf, cd.COL_EPISODE, cap * 4, np.uint32)
+        st = read_col(buf, cd.COL_STEP, cap * 4, np.int32)
+        assert np.array_equal(ep[held], orc.episode[held]), n
+        assert np.array_equal(st[held], orc.step[held]), n
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
+
+
+def test_tiny_config_episodes_derived_from_done():
+    print("tiny config: episode ids and steps derived from done", flush=True)
+    _run_tiny(prefill=0, iters=30, seed_shift=15, derive_meta=True, nstep=(5, 0.99))
+    _run_tiny(prefill=20000, iters=20, seed_shift=16, derive_meta=True, update_ingest=True, fused=True)
 
 
 @pytest.mark.parametrize("n,gamma", [(1, 0.99), (5, 0.99), (63, 0.9)])
@@ -282,7 +315,8 @@ def test_tiny_config_payload_in_pinned_host_memory(fused):
 # configuration 1 (DQN, frame stack 4, u8 -> fp32/255) at reduced capacity
 # ----------------------------------------------------------------------------
 def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False,
-            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH, nstep=None, update_ingest=False, fused_nstep=None):
+            placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH, nstep=None, update_ingest=False, fused_nstep=None,
+            derive_meta=False):
     """Drive GPU buffer and oracle through the same DQN stream; the oracle keeps
     metadata only and its observation rows are regenerated for the slots a
     gather reads.  fused_nstep = (n, gamma): every delivery goes through
@@ -306,14 +340,17 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
 
     def ingest(a, b, with_prio, pending=None):
         p = cfg.prio[a:b] if with_prio else None
+        meta = dict(episode_id=None, step=None) if derive_meta else dict(episode_id=dev(cfg.episode[a:b]),
+                                                                          step=dev(cfg.step[a:b]))
         cols = dict(action=dev(cfg.action[a:b]), reward=dev(cfg.reward[a:b]), done=dev(cfg.done[a:b]),
-                    episode_id=dev(cfg.episode[a:b]), step=dev(cfg.step[a:b]), prio=dev(p) if p is not None else None)
+                    prio=dev(p) if p is not None else None, **meta)
         if pending is not None:  # the previous iteration's update, in the same call
             buf.update_ingest(pending[0], pending[1], cfg.frames(a, b - a, "cuda"), **cols)
         else:
             buf.ingest(cfg.frames(a, b - a, "cuda"), **cols)
         orc.ingest(b - a, obs=None, action=cfg.action[a:b], reward=cfg.reward[a:b], done=cfg.done[a:b],
-                   episode=cfg.episode[a:b], step=cfg.step[a:b], prio=p)
+                   episode=None if derive_meta else cfg.episode[a:b], step=None if derive_meta else cfg.step[a:b],
+                   prio=p)
 
     for a in range(0, prefill, chunk):
         ingest(a, min(prefill, a + chunk), with_prio=True)
@@ -424,6 +461,15 @@ def test_dqn_sample_gather_nstep_one_launch(n, short):
     # n < K: the stacks share K - n frames (K + n read); n >= K: disjoint (2K read)
     print(f"dqn: sample + gather + {n}-step in one call, short episodes={short}", flush=True)
     run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=short, fused_nstep=(n, 0.99))
+
+
+@pytest.mark.parametrize("update_ingest", [False, True])
+def test_dqn_episodes_derived_from_done(update_ingest):
+    # no episode ids or steps given: the library derives them from done as one
+    # stream, like the oracle; frame stacks and n-step windows follow them
+    print(f"dqn: episode ids and steps derived from done, update+ingest={update_ingest}", flush=True)
+    run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=True, fused=True,
+            update_ingest=update_ingest, derive_meta=True, nstep=(3, 0.99))
 
 
 @pytest.mark.parametrize("fused", [False, True])

@@ -100,6 +100,55 @@ def _filled_replay(leaves_prio, alpha=(1, 1), beta=0.4):
     return r
 
 
+def test_derived_episodes_hand_example():
+    # a stream of 7 transitions in two ingests into a 5-slot ring, no episode
+    # ids or steps given; done at positions 1, 5 and 6.  Position p continues
+    # p-1's episode one step on unless p-1 was done:
+    #   position: 0  1  2  3  4  5  6
+    #   done:     0  1  0  0  0  1  1
+    #   episode:  0  0  1  1  1  1  2
+    #   step:     0  1  0  1  2  3  0
+    # the ring then holds positions 5, 6, 2, 3, 4 in slots 0..4
+    r = oracle.Replay(5, (1,), np.uint8)
+    r.ingest(3, obs=np.zeros((3, 1), np.uint8), done=np.array([0, 1, 0], np.uint8))
+    r.ingest(4, obs=np.zeros((4, 1), np.uint8), done=np.array([0, 0, 1, 1], np.uint8))
+    assert list(r.position) == [5, 6, 2, 3, 4]
+    assert list(r.episode) == [1, 2, 1, 1, 1]
+    assert list(r.step) == [3, 0, 0, 1, 2]
+
+
+def test_derived_episodes_match_the_actor_bookkeeping():
+    # any split of one stream into ingests, wrapping rings included, stores the
+    # episode ids and steps an actor would have attached to the whole stream
+    # (the generator's own bookkeeping, written independently)
+    rng = np.random.default_rng(41)
+    for trial in range(40):
+        total = int(rng.integers(1, 400))
+        cap = int(rng.integers(1, 120))
+        done = (rng.random(total) < rng.choice([0.0, 0.05, 0.3, 1.0])).astype(np.uint8)
+        ep, st = synth.episodes_from_done(done)
+        r = oracle.Replay(cap, (1,), np.uint8)
+        a = 0
+        while a < total:
+            b = min(total, a + int(rng.integers(1, cap + 1)))
+            r.ingest(b - a, obs=np.zeros((b - a, 1), np.uint8), done=done[a:b])
+            a = b
+        held = r.position >= 0
+        assert np.array_equal(r.episode[held], ep[r.position[held]]), trial
+        assert np.array_equal(r.step[held], st[r.position[held]]), trial
+
+
+def test_derived_episodes_continue_given_ones():
+    # ids given by one ingest, derived by the next: the stream continues from
+    # the last given transition (episode 7, step 41, not done)
+    r = oracle.Replay(8, (1,), np.uint8)
+    r.ingest(2, obs=np.zeros((2, 1), np.uint8), done=np.array([0, 0], np.uint8),
+             episode=np.array([7, 7], np.uint32), step=np.array([40, 41], np.int32))
+    r.ingest(3, obs=np.zeros((3, 1), np.uint8), done=np.array([1, 0, 0], np.uint8))
+    assert list(r.episode[:5]) == [7, 7, 7, 8, 8]
+    assert list(r.step[:5]) == [40, 41, 42, 0, 1]
+
+
 def test_sample_matches_linear_scan():
     rng = np.random.default_rng(11)
     for trial in range(200):
