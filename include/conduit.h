@@ -110,6 +110,13 @@ typedef struct {
      * could receive, that of the smallest non-zero leaf of the buffer (the
      * sampler workgroups reduce the leaves in the same launches). */
     int32_t weight_norm;
+    /* 1: the buffer holds one stream of transitions, and an ingest that gives
+     * no episode_id (or no step) derives them from done (see
+     * conduit_transitions), with one more small launch.  0 (default): such an
+     * ingest stores episode 0 and step 0 (rollouts of several environments
+     * interleaved, whose ids nothing reads), and frame-stacking buffers need
+     * both arrays on every ingest. */
+    int32_t single_stream;
 } conduit_buffer_opts;
 
 #define CONDUIT_WNORM_BATCH 0
@@ -182,12 +189,13 @@ typedef struct {
     const void* action;          /* device [n, action_bytes] or NULL (zeros) */
     const float* reward;         /* device [n] or NULL (zeros) */
     const uint8_t* done;         /* device [n] or NULL (zeros) */
-    /* device [n] episode ids and step indices within the episode (>= 0).  NULL:
-     * derived from done as one stream (the transitions of every ingest follow
-     * the buffer's last stored transition): a transition continues its
-     * predecessor's episode one step on, unless the predecessor's done ended
-     * it, when it starts the next episode id at step 0; the first transition
-     * ever is episode 0, step 0.  Deriving costs one more small launch. */
+    /* device [n] episode ids and step indices within the episode (>= 0).  NULL
+     * in a single_stream buffer: derived from done as one stream (the
+     * transitions of every ingest follow the buffer's last stored transition):
+     * a transition continues its predecessor's episode one step on, unless the
+     * predecessor's done ended it, when it starts the next episode id at step
+     * 0; the first transition ever is episode 0, step 0.  NULL otherwise: 0
+     * (not allowed when frame_stack > 1). */
     const uint32_t* episode_id;
     const int32_t* step;
     const uint32_t* prio;        /* device [n] priorities or NULL: the running maximum */

@@ -41,7 +41,7 @@ class _Replay(C.Structure):
     _fields_ = [
         ("capacity", I64), ("row_bytes", I64), ("elem_bytes", I64), ("aux_elem_bytes", I64),
         ("act_bytes", I64), ("alpha_num", I32), ("alpha_den", I32), ("beta", F64),
-        ("frame_stack", I32), ("ragged", I32), ("tree_leaves", I64),
+        ("frame_stack", I32), ("ragged", I32), ("single_stream", I32), ("tree_leaves", I64),
         ("obs", P), ("aux", P), ("action", P), ("reward", P), ("done", P), ("episode", P),
         ("step", P), ("position", P), ("length", P), ("leaf", P), ("tree", P),
         ("head", I64), ("size", I64), ("total", I64), ("max_prio", U32),
@@ -135,7 +135,7 @@ class Replay:
 
     def __init__(self, capacity, obs_shape, obs_dtype=np.uint8, act_bytes=4, alpha=(3, 5),
                  beta=0.4, frame_stack=1, ragged=False, aux_dtype=None, keep_obs=True,
-                 obs_storage=None, buffer_norm=False):
+                 obs_storage=None, buffer_norm=False, single_stream=False):
         obs_dtype = np.dtype(obs_dtype)
         self.buffer_norm = bool(buffer_norm)
         self.capacity = int(capacity)
@@ -177,6 +177,7 @@ class Replay:
         s.beta = beta
         s.frame_stack = frame_stack
         s.ragged = 1 if ragged else 0
+        s.single_stream = 1 if single_stream else 0
         s.tree_leaves = tl
         s.obs = _ptr(self.obs) if self.obs is not None else None
         s.aux = _ptr(self.aux) if self.aux is not None else None

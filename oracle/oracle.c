@@ -128,6 +128,7 @@ typedef struct {
     double beta;
     int32_t frame_stack;     /* K >= 1 observations per sample */
     int32_t ragged;          /* observations are variable-length sequences */
+    int32_t single_stream;   /* 1: episode/step left NULL are derived from done */
     int64_t tree_leaves;     /* power of two >= capacity */
     /* storage */
     uint8_t* obs;            /* capacity*row_bytes, or NULL: observations not kept */
@@ -171,11 +172,12 @@ uint64_t orc_total_priority(const orc_replay* r) { return r->tree[1]; }
 
 /*
  * Insert n transitions at slots (head + j) mod capacity, overwriting the oldest
- * ones once the ring is full (eviction).  episode/step NULL: derived from done
- * as one stream (tuples carry an episode ID, Sec. 2.1; the reading for callers
- * that give none): a transition continues its predecessor's episode one step
- * on, unless the predecessor was done, when it starts the next episode at step
- * 0; the first transition ever is episode 0, step 0.
+ * ones once the ring is full (eviction).  episode/step NULL: with
+ * single_stream, derived from done as one stream (tuples carry an episode ID,
+ * Sec. 2.1; the reading for callers that give none): a transition continues
+ * its predecessor's episode one step on, unless the predecessor was done, when
+ * it starts the next episode at step 0; the first transition ever is episode
+ * 0, step 0.  Without single_stream they are stored as 0.
  * prio NULL: every new transition gets the running maximum priority.
  * Ragged datasets take concatenated sequences: row j spans elements
  * [offsets[j], offsets[j+1]) of obs and aux.
@@ -221,8 +223,8 @@ int32_t orc_ingest(orc_replay* r, int64_t n, const uint8_t* obs, const int64_t* 
         }
         r->reward[s] = reward ? reward[j] : 0.0f;
         r->done[s] = done ? done[j] : 0;
-        r->episode[s] = episode ? episode[j] : ep_d;
-        r->step[s] = step ? step[j] : st_d;
+        r->episode[s] = episode ? episode[j] : r->single_stream ? ep_d : 0;
+        r->step[s] = step ? step[j] : r->single_stream ? st_d : 0;
         r->position[s] = r->total + j;
         uint32_t p = prio ? prio[j] : fill_prio;
         tree_set(r, s, orc_leaf(p, r->alpha_num, r->alpha_den));

@@ -36,7 +36,7 @@ class BufferOpts(C.Structure):
     _fields_ = [("prioritized", C.c_int32), ("alpha_num", C.c_int32), ("alpha_den", C.c_int32),
                 ("beta", C.c_double), ("frame_stack", C.c_int32), ("action_bytes", C.c_int32),
                 ("ragged", C.c_int32), ("aux_elem_bytes", C.c_int32), ("payload_placement", C.c_int32),
-                ("weight_norm", C.c_int32)]
+                ("weight_norm", C.c_int32), ("single_stream", C.c_int32)]
 
 
 class Transitions(C.Structure):
@@ -585,11 +585,11 @@ class ReplayBuffer:
 
     def __init__(self, capacity, obs_shape, obs_dtype=torch.uint8, prioritized=True, alpha=(3, 5), beta=0.4,
                  frame_stack=1, action_bytes=4, ragged=False, aux_elem_bytes=0, arena=None, placement=PLACE_HBM,
-                 weight_norm=0):
+                 weight_norm=0, single_stream=False):
         self.opts = default_opts(prioritized=int(prioritized), alpha_num=alpha[0], alpha_den=alpha[1], beta=beta,
                                  frame_stack=frame_stack, action_bytes=action_bytes, ragged=int(ragged),
                                  aux_elem_bytes=aux_elem_bytes, payload_placement=int(placement),
-                                 weight_norm=int(weight_norm))
+                                 weight_norm=int(weight_norm), single_stream=int(bool(single_stream)))
         self.capacity = capacity
         self.obs_shape = tuple(obs_shape)
         self.obs_dtype = obs_dtype

@@ -193,6 +193,7 @@ conduit_status make_layout(int64_t capacity, const int64_t* shape, int32_t ndim,
         return fail(CONDUIT_EINVAL, "unknown payload placement");
     if (o.weight_norm != CONDUIT_WNORM_BATCH && o.weight_norm != CONDUIT_WNORM_BUFFER)
         return fail(CONDUIT_EINVAL, "weight_norm must be CONDUIT_WNORM_BATCH or CONDUIT_WNORM_BUFFER");
+    if (o.single_stream != 0 && o.single_stream != 1) return fail(CONDUIT_EINVAL, "single_stream must be 0 or 1");
     // tree shape
     L->nodes[0] = capacity;
     int d = 0;
@@ -286,6 +287,7 @@ void conduit_buffer_opts_default(conduit_buffer_opts* o) {
     o->aux_elem_bytes = 0;
     o->payload_placement = CONDUIT_PLACE_HBM;
     o->weight_norm = CONDUIT_WNORM_BATCH;
+    o->single_stream = 0;
 }
 
 const char* conduit_last_error(void) { return g_last_error.c_str(); }
@@ -474,6 +476,8 @@ static conduit_status ingest_args(conduit_buffer* b, const conduit_transitions* 
     if (o.ragged && !t->offsets) return fail(CONDUIT_EINVAL, "ragged ingest needs offsets");
     if (o.ragged && t->src_elems < 0) return fail(CONDUIT_EINVAL, "ragged ingest needs src_elems >= 0");
     if (o.ragged && t->aux && reinterpret_cast<uintptr_t>(t->aux) % 4) return fail(CONDUIT_EINVAL, "aux must be 4-byte aligned");
+    if (o.frame_stack > 1 && !o.single_stream && (!t->episode_id || !t->step))
+        return fail(CONDUIT_EINVAL, "frame-stacking buffers need episode_id and step (or the single_stream option)");
     IngestArgs a{};
     a.obs = b->obs;
     a.aux = b->aux;
@@ -503,7 +507,7 @@ static conduit_status ingest_args(conduit_buffer* b, const conduit_transitions* 
     a.n = t->n;
     a.head = b->head;
     a.total = b->total;
-    a.derive = (t->episode_id ? 0 : kDeriveEpisode) | (t->step ? 0 : kDeriveStep);
+    a.derive = o.single_stream ? (t->episode_id ? 0 : kDeriveEpisode) | (t->step ? 0 : kDeriveStep) : 0;
     a.tree = b->tree;
     a.state = b->state;
     a.err = err_words(b->err_slot);

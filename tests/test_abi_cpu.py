@@ -198,3 +198,13 @@ def test_gae_plan_validates():
     x = C.c_int32()
     assert L.conduit_gae_plan(-1, 4, 1, C.byref(x), C.byref(x)) == cd.EINVAL
     assert L.conduit_gae_plan(4, 4, 1, None, C.byref(x)) == cd.EINVAL
+
+
+def test_single_stream_option():
+    o = cd.default_opts()
+    assert o.single_stream == 0
+    shape = (C.c_int64 * 1)(8)
+    o.single_stream = 2
+    assert cd.lib().conduit_buffer_required_bytes(16, shape, 1, cd.F32, C.byref(o)) == 0
+    o.single_stream = 1
+    assert cd.lib().conduit_buffer_required_bytes(16, shape, 1, cd.F32, C.byref(o)) > 0

@@ -154,8 +154,10 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
-    buf = _mk(C, (8,), torch.float32, action_bytes=4, placement=placement, weight_norm=weight_norm)
-    orc = oracle.Replay(C, (8,), np.float32, act_bytes=4, buffer_norm=weight_norm == cd.WNORM_BUFFER)
+    buf = _mk(C, (8,), torch.float32, action_bytes=4, placement=placement, weight_norm=weight_norm,
+              single_stream=derive_meta)
+    orc = oracle.Replay(C, (8,), np.float32, act_bytes=4, buffer_norm=weight_norm == cd.WNORM_BUFFER,
+                        single_stream=derive_meta)
 
     def ingest(a, b, pending=None):
         """ingest rows [a, b); `pending` (idx, prio) is a priority update that
@@ -259,8 +261,8 @@ def test_derived_episodes_whole_ring_ingests():
     print("derived episodes: whole-ring and single-row ingests", flush=True)
     rng = np.random.default_rng(77)
     cap = 100
-    buf = _mk(cap, (4,), torch.float32, action_bytes=0)
-    orc = oracle.Replay(cap, (4,), np.float32, act_bytes=0)
+    buf = _mk(cap, (4,), torch.float32, action_bytes=0, single_stream=True)
+    orc = oracle.Replay(cap, (4,), np.float32, act_bytes=0, single_stream=True)
     for n in [30, 100, 7, 100, 1, 1, 99, 100]:
         obs = rng.standard_normal((n, 4)).astype(np.float32)
         done = (rng.random(n) < 0.2).astype(np.uint8)
@@ -333,10 +335,10 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
     u, prio = cfg.draws(iters, batch)
     K = 4
     buf = _mk(cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4, placement=placement,
-              weight_norm=weight_norm)
+              weight_norm=weight_norm, single_stream=derive_meta)
     obs_store = np.zeros((cap, 84 * 84), np.uint8)  # untouched pages stay unallocated
     orc = oracle.Replay(cap, (84, 84), np.uint8, act_bytes=4, frame_stack=K, obs_storage=obs_store,
-                        buffer_norm=weight_norm == cd.WNORM_BUFFER)
+                        buffer_norm=weight_norm == cd.WNORM_BUFFER, single_stream=derive_meta)
 
     def ingest(a, b, with_prio, pending=None):
         p = cfg.prio[a:b] if with_prio else None
@@ -465,8 +467,9 @@ def test_dqn_sample_gather_nstep_one_launch(n, short):
 
 @pytest.mark.parametrize("update_ingest", [False, True])
 def test_dqn_episodes_derived_from_done(update_ingest):
-    # no episode ids or steps given: the library derives them from done as one
-    # stream, like the oracle; frame stacks and n-step windows follow them
+    # no episode ids or steps given to a single-stream buffer: the library
+    # derives them from done, like the oracle; frame stacks and n-step windows
+    # follow them
     print(f"dqn: episode ids and steps derived from done, update+ingest={update_ingest}", flush=True)
     run_dqn(cap=3000, prefill=3500, iters=3, batch=512, chunk=700, short_episodes=True, fused=True,
             update_ingest=update_ingest, derive_meta=True, nstep=(3, 0.99))

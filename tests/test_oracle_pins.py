@@ -109,7 +109,7 @@ def test_derived_episodes_hand_example():
     #   episode:  0  0  1  1  1  1  2
     #   step:     0  1  0  1  2  3  0
     # the ring then holds positions 5, 6, 2, 3, 4 in slots 0..4
-    r = oracle.Replay(5, (1,), np.uint8)
+    r = oracle.Replay(5, (1,), np.uint8, single_stream=True)
     r.ingest(3, obs=np.zeros((3, 1), np.uint8), done=np.array([0, 1, 0], np.uint8))
     r.ingest(4, obs=np.zeros((4, 1), np.uint8), done=np.array([0, 0, 1, 1], np.uint8))
     assert list(r.position) == [5, 6, 2, 3, 4]
@@ -127,7 +127,7 @@ def test_derived_episodes_match_the_actor_bookkeeping():
         cap = int(rng.integers(1, 120))
         done = (rng.random(total) < rng.choice([0.0, 0.05, 0.3, 1.0])).astype(np.uint8)
         ep, st = synth.episodes_from_done(done)
-        r = oracle.Replay(cap, (1,), np.uint8)
+        r = oracle.Replay(cap, (1,), np.uint8, single_stream=True)
         a = 0
         while a < total:
             b = min(total, a + int(rng.integers(1, cap + 1)))
@@ -141,12 +141,16 @@ def test_derived_episodes_match_the_actor_bookkeeping():
 def test_derived_episodes_continue_given_ones():
     # ids given by one ingest, derived by the next: the stream continues from
     # the last given transition (episode 7, step 41, not done)
-    r = oracle.Replay(8, (1,), np.uint8)
+    r = oracle.Replay(8, (1,), np.uint8, single_stream=True)
     r.ingest(2, obs=np.zeros((2, 1), np.uint8), done=np.array([0, 0], np.uint8),
              episode=np.array([7, 7], np.uint32), step=np.array([40, 41], np.int32))
     r.ingest(3, obs=np.zeros((3, 1), np.uint8), done=np.array([1, 0, 0], np.uint8))
     assert list(r.episode[:5]) == [7, 7, 7, 8, 8]
     assert list(r.step[:5]) == [40, 41, 42, 0, 1]
+    # without the single-stream option, omitted ids are stored as 0
+    r = oracle.Replay(8, (1,), np.uint8)
+    r.ingest(3, obs=np.zeros((3, 1), np.uint8), done=np.array([1, 0, 1], np.uint8))
+    assert list(r.episode[:3]) == [0, 0, 0] and list(r.step[:3]) == [0, 0, 0]
 
 
 def test_sample_matches_linear_scan():
