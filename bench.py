@@ -1375,10 +1375,10 @@ def _traffic_from_profile():
         return None
     rec = {}
     with open(path) as f:
-        for line in f:
+        for line in f:  # the file's first block is the fused kernel's; later blocks are context
             if "=" in line and not line.lstrip().startswith("#"):
                 k, v = line.split("=", 1)
-                rec[k.strip()] = v.strip()
+                rec.setdefault(k.strip(), v.strip())
     if rec.get("kernel_sources_sha256_16") != kernel_sources_sha():
         return None
     return float(rec["hbm_bytes_per_launch"])
