@@ -90,7 +90,10 @@ def _check_nstep(buf, orc, idx_d, o_idx, n, gamma, xf_kind, row_shape, obs_kind=
     return o_v
 
 
-def _assert_nstep_outputs(orc, o_idx, n, gamma, xf_kind, nxt, ret, disc, val, nobs):
+_ORC_XF = {cd.XF_NONE: oracle.XF_NONE, cd.XF_U8_F32: oracle.XF_U8_F32, cd.XF_U8_BF16_NORM: oracle.XF_U8_BF16_NORM}
+
+
+def _assert_nstep_outputs(orc, o_idx, n, gamma, xf_kind, nxt, ret, disc, val, nobs, mean=None, std=None):
     """n-step outputs of one delivery against the oracle (bootstrap stacks:
     zero rows where there is none); returns the oracle's targets."""
     B = len(o_idx)
@@ -100,13 +103,66 @@ def _assert_nstep_outputs(orc, o_idx, n, gamma, xf_kind, nxt, ret, disc, val, no
     np.testing.assert_allclose(host(ret), o_r, rtol=1e-6, atol=1e-6)
     assert np.array_equal(host(disc), o_d)
     if nobs is not None:
-        g = host(nobs).reshape(B, -1).view(np.uint8)
+        g = host(nobs.view(torch.uint8)).reshape(B, -1)
         boot = o_n >= 0
         if boot.any():
-            want, _, _, _ = orc.gather(o_n[boot], oracle.XF_U8_F32 if xf_kind == cd.XF_U8_F32 else oracle.XF_NONE)
+            want, _, _, _ = orc.gather(o_n[boot], _ORC_XF[xf_kind], mean, std)
             assert np.array_equal(g[boot], want.reshape(int(boot.sum()), -1).view(np.uint8))
         assert not g[~boot].any()
     return o_n, o_r, o_d, o_v
+
+
+@pytest.mark.parametrize("kind,B,n", [("u8_f32", 1, 1), ("u8_f32", 77, 2), ("bf16", 513, 3), ("bf16", 64, 6),
+                                      ("none", 300, 4), ("none", 33, 9)])
+def test_sample_gather_nstep_transforms_and_batches(kind, B, n):
+    """The one-launch delivery with n-step targets on every pixel transform
+    (the bf16 table per channel included), odd batches and n below, at and
+    above the stack, on a wrapped ring of 3x16x16 frames (one work item per
+    frame, stack of 4)."""
+    print(f"sample + gather + n-step: {kind}, B={B}, n={n}", flush=True)
+    rng = np.random.default_rng(B * 7 + n)
+    cap, total, K, shape = 700, 1000, 4, (3, 16, 16)
+    row = int(np.prod(shape))
+    done = (rng.random(total) < 0.05).astype(np.uint8)
+    episode, step = synth.episodes_from_done(done)
+    obs = rng.integers(0, 256, size=(total, row), dtype=np.uint8)
+    reward = rng.standard_normal(total).astype(np.float32)
+    action = rng.integers(0, 256, size=(total, 4), dtype=np.uint8)
+    prio = rng.integers(1, 10 ** 6, size=total).astype(np.uint32)
+    buf = _mk(cap, shape, torch.uint8, frame_stack=K, action_bytes=4)
+    orc = oracle.Replay(cap, shape, np.uint8, act_bytes=4, frame_stack=K)
+    for a in range(0, total, 250):
+        b = min(total, a + 250)
+        buf.ingest(dev(obs[a:b].reshape((b - a,) + shape)), action=dev(action[a:b]), reward=dev(reward[a:b]),
+                   done=dev(done[a:b]), episode_id=dev(episode[a:b]), step=dev(step[a:b]), prio=dev(prio[a:b]))
+        orc.ingest(b - a, obs=obs[a:b], action=action[a:b], reward=reward[a:b], done=done[a:b],
+                   episode=episode[a:b], step=step[a:b], prio=prio[a:b])
+    mean = std = None
+    if kind == "bf16":
+        mean, std = np.array([0.485, 0.456, 0.406], np.float32), np.array([0.229, 0.224, 0.225], np.float32)
+    xk = {"u8_f32": cd.XF_U8_F32, "bf16": cd.XF_U8_BF16_NORM, "none": cd.XF_NONE}[kind]
+    odt = {"u8_f32": torch.float32, "bf16": torch.bfloat16, "none": torch.uint8}[kind]
+    xf = cd.transform(xk, mean, std)
+    obs_o = torch.full((B, K) + shape, 7, dtype=odt, device="cuda")
+    nobs = torch.full((B, K) + shape, 7, dtype=odt, device="cuda")
+    act_o = torch.full((B, 4), 7, dtype=torch.uint8, device="cuda")
+    rew_o = torch.full((B,), 7.0, dtype=torch.float32, device="cuda")
+    done_o = torch.full((B,), 7, dtype=torch.uint8, device="cuda")
+    u = rng.integers(0, 1 << 63, size=B, dtype=np.int64)
+    idx, w, nxt, ret, disc, val = buf.sample_gather_nstep(dev(u), xf, n, 0.97, next_obs=nobs, obs=obs_o,
+                                                          action=act_o, reward=rew_o, done=done_o)
+    o_idx, o_w = orc.sample(u.view(np.uint64))
+    assert np.array_equal(host(idx), o_idx)
+    assert_weights_close(host(w), o_w)
+    o_obs, o_act, o_rew, o_done = orc.gather(o_idx, _ORC_XF[xk], mean, std)
+    assert np.array_equal(host(obs_o.view(torch.uint8)).reshape(B, -1), o_obs.reshape(B, -1).view(np.uint8))
+    assert np.array_equal(host(act_o), o_act)
+    assert np.array_equal(host(rew_o), o_rew)
+    assert np.array_equal(host(done_o), o_done)
+    o_n = _assert_nstep_outputs(orc, o_idx, n, 0.97, xk, nxt, ret, disc, val, nobs, mean, std)[0]
+    assert (o_n >= 0).any()
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    buf.close()
 
 
 @pytest.mark.parametrize("n", [1, 3])
