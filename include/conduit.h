@@ -340,10 +340,11 @@ conduit_status conduit_gather_transform(conduit_buffer* buf, const int64_t* idx,
  * conduit_gather_transform(buf, idx_out, batch, xf, out), with the same
  * outputs, arguments and errors as the two calls.  Dense buffers whose rows
  * are at most 8 gather work items of 7,168 bytes (e.g. a stack of four 84x84
- * frames) take one launch: the workgroups that gather a sample descend the
- * tree for it themselves, and the importance weights are computed inside the
- * same launch.  Other buffers take two launches: the sampler, then the gather
- * (or packing) launch with one extra workgroup for the weights.  The call uses
+ * frames), and ragged buffers, take one launch: the workgroups that gather (or
+ * pack) a sample descend the tree for it themselves, and the importance
+ * weights are computed inside the same launch.  Other dense buffers take two
+ * launches: the sampler, then the gather launch with one extra workgroup for
+ * the weights.  The call uses
  * a word of the buffer's device state between its launches' workgroups, so
  * calls on one buffer must not overlap (as for every call on a buffer).
  */

@@ -787,8 +787,8 @@ conduit_status conduit_sample_gather(conduit_buffer* b, int64_t batch, const uin
     sa.err = err_words(b->err_slot);
     set_leaf_min(b, &sa);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // dense rows of a few work items: one fused launch
-    hipError_t e = b->opts.ragged ? hipErrorNotSupported : launch_sample_gather(sa, ga, s);
+    // dense rows of a few work items, and ragged rows: one fused launch
+    hipError_t e = b->opts.ragged ? launch_sample_pack(sa, pa, s) : launch_sample_gather(sa, ga, s);
     if (e == hipErrorNotSupported) {
         // otherwise the sampler parks the sampled leaves in is_w_out, and the
         // gather (or packing) launch carries one more workgroup that turns them

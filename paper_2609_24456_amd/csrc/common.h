@@ -465,6 +465,9 @@ struct PackArgs {
 };
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+// sample + pack in one launch (ragged buffers); hipErrorNotSupported if the
+// batch and the pack arguments disagree
+hipError_t launch_sample_pack(const SampleArgs& sa, const PackArgs& pa, hipStream_t s);
 
 // time-major GAE addresses a slab of the rollout with 32-bit offsets
 constexpr int64_t kGaeMaxEnvs = 1ll << 19;

@@ -111,74 +111,13 @@ __global__ __launch_bounds__(kThreads) void k_gather_pipe(GatherArgs a, int32_t 
 
 // ragged token packing: one workgroup per sample; each lane handles up to 4
 // quads (16 elements) per pass, all loads issued before the stores
-constexpr int kPackQuads = 4;
-
 __global__ __launch_bounds__(kThreads) void k_pack(PackArgs a) {
     const int64_t b = blockIdx.x;
     if (b >= a.n) {  // the weights workgroup
         is_weights_block<kThreads>(a.weights);
         return;
     }
-    const int64_t i = a.idx[b];
-    const bool ok = i >= 0 && i < a.size;
-    if (!ok && threadIdx.x == 0) flag_error(a.err, ERR_GATHER_INDEX);
-    // the row's scalar columns are loaded now, with its length, and stored last
-    const int64_t si = ok ? i : 0;
-    const float rew = a.out_reward ? a.reward[si] : 0.0f;
-    const uint8_t dn = a.out_done ? a.done[si] : (uint8_t)0;
-    const bool act = a.out_action && (int)threadIdx.x < a.action_bytes;
-    const uint8_t ab = act ? a.action[si * a.action_bytes + threadIdx.x] : (uint8_t)0;
-    int64_t L = ok ? a.length[i] : 0;
-    if (L < 0) L = 0;
-    if (L > a.max_len) L = a.max_len;
-    const int32_t* __restrict__ seq = reinterpret_cast<const int32_t*>(a.seq) + (ok ? i : 0) * a.max_len;
-    const float* __restrict__ aux = a.aux ? reinterpret_cast<const float*>(a.aux) + (ok ? i : 0) * a.max_len : nullptr;
-    const int64_t quads = a.max_len >> 2;
-    for (int64_t q0 = threadIdx.x; q0 < quads; q0 += kThreads * kPackQuads) {
-        int4 tok[kPackQuads];
-        f32x4 lp[kPackQuads];
-        uint32_t m[kPackQuads];
-#pragma unroll
-        for (int r = 0; r < kPackQuads; ++r) {
-            const int64_t q = q0 + (int64_t)r * kThreads;
-            const int64_t t = q * 4;
-            if (q < quads && t + 3 < L) {
-                tok[r] = *reinterpret_cast<const int4*>(seq + t);
-                lp[r] = aux ? *reinterpret_cast<const f32x4*>(aux + t) : (f32x4)(0.0f);
-                m[r] = 0x01010101u;
-            } else {
-                tok[r].x = t + 0 < L ? seq[t + 0] : a.pad_id;
-                tok[r].y = t + 1 < L ? seq[t + 1] : a.pad_id;
-                tok[r].z = t + 2 < L ? seq[t + 2] : a.pad_id;
-                tok[r].w = t + 3 < L ? seq[t + 3] : a.pad_id;
-                lp[r].x = (aux && t + 0 < L) ? aux[t + 0] : 0.0f;
-                lp[r].y = (aux && t + 1 < L) ? aux[t + 1] : 0.0f;
-                lp[r].z = (aux && t + 2 < L) ? aux[t + 2] : 0.0f;
-                lp[r].w = (aux && t + 3 < L) ? aux[t + 3] : 0.0f;
-                m[r] = (t + 0 < L ? 0x1u : 0u) | (t + 1 < L ? 0x100u : 0u) | (t + 2 < L ? 0x10000u : 0u) |
-                       (t + 3 < L ? 0x1000000u : 0u);
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < kPackQuads; ++r) {
-            const int64_t q = q0 + (int64_t)r * kThreads;
-            if (q >= quads) continue;
-            const int64_t o = b * a.max_len + q * 4;
-            *reinterpret_cast<int4*>(reinterpret_cast<int32_t*>(a.out_seq) + o) = tok[r];
-            if (a.out_aux) *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out_aux) + o) = lp[r];
-            if (a.out_mask) *reinterpret_cast<uint32_t*>(a.out_mask + o) = m[r];
-        }
-    }
-    if (threadIdx.x == 0) {
-        if (a.out_length) a.out_length[b] = (int32_t)L;
-        if (a.out_reward) a.out_reward[b] = ok ? rew : 0.0f;
-        if (a.out_done) a.out_done[b] = ok ? dn : (uint8_t)0;
-    }
-    if (act) a.out_action[b * a.action_bytes + threadIdx.x] = ok ? ab : (uint8_t)0;
-    if (a.out_action) {  // actions longer than one byte per lane
-        for (int c = (int)threadIdx.x + kThreads; c < a.action_bytes; c += kThreads)
-            a.out_action[b * a.action_bytes + c] = ok ? a.action[si * a.action_bytes + c] : (uint8_t)0;
-    }
+    pack_row(a, b, a.idx[b]);
 }
 
 }  // namespace

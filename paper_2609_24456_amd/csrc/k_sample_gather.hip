@@ -1,8 +1,9 @@
 // Fused sampler + gather for dense buffers whose rows are a few work items
-// (the frame-stack DQN shape): one launch delivers indices, importance weights
-// and the learner batch (proportional prioritised replay, Schaul et al.; the
-// paper's off-policy delivery samples and then materialises the batch,
-// Sec. 2.2).
+// (the frame-stack DQN shape), and fused sampler + token packing for ragged
+// buffers (k_sample_pack, at the end): one launch delivers indices,
+// importance weights and the learner batch (proportional prioritised replay,
+// Schaul et al.; the paper's off-policy delivery samples and then materialises
+// the batch, Sec. 2.2).
 //
 // Two kinds of 512-lane workgroup share the grid:
 //   * gather workgroups (the head of the grid, one per sample): wavefront 0
@@ -43,10 +44,12 @@ namespace {
 constexpr int kWg = 2 * kThreads;  // two 256-lane halves
 constexpr int kSamplesPerSamplerWg = kWg / kWave;
 
-template <int PRE, int DEPTH>
+// A sampler workgroup of NT lanes: NT / 64 samples, one per wavefront.
+template <int NT, int PRE, int DEPTH>
 __device__ void sampler_wg(const SampleArgs& sa, const DivB& dv, int64_t wg) {
+    constexpr int64_t kPer = NT / kWave;
     __shared__ uint32_t s_last;
-    const int64_t k = wg * kSamplesPerSamplerWg + threadIdx.x / kWave;
+    const int64_t k = wg * kPer + threadIdx.x / kWave;
     if (k < sa.batch) {  // wave-uniform
         const Descent d = tree_descend<PRE, DEPTH>(sa.tree, sa.uniforms, k, dv);
         if (lane_id() == 0) {
@@ -61,18 +64,18 @@ __device__ void sampler_wg(const SampleArgs& sa, const DivB& dv, int64_t wg) {
     if (!sa.w_out) return;  // kernel argument: uniform
     // buffer-wide normalisation: this workgroup's share of the leaf minimum,
     // folded in before the ticket like the parked leaves
-    if (sa.leaf_min) fold_leaf_min<kWg>(sa, wg, (sa.batch + kSamplesPerSamplerWg - 1) / kSamplesPerSamplerWg);
+    if (sa.leaf_min) fold_leaf_min<NT>(sa, wg, (sa.batch + kPer - 1) / kPer);
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_waitcnt(0);  // this wavefront's parked leaves are acknowledged
     __syncthreads();                // ... and every wavefront's
     if (threadIdx.x == 0) {
-        const uint32_t tickets = (uint32_t)((sa.batch + kSamplesPerSamplerWg - 1) / kSamplesPerSamplerWg);
+        const uint32_t tickets = (uint32_t)((sa.batch + kPer - 1) / kPer);
         const uint32_t t = __hip_atomic_fetch_add(&sa.state->ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         s_last = t == tickets - 1;
     }
     __syncthreads();
     if (s_last) {  // every leaf of the batch is parked and visible
-        is_weights_block<kWg, true>(WeightsArgs{sa.w_out, sa.batch, sa.beta, sa.leaf_min});
+        is_weights_block<NT, true>(WeightsArgs{sa.w_out, sa.batch, sa.beta, sa.leaf_min});
         if (threadIdx.x == 0) __hip_atomic_store(&sa.state->ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
@@ -84,7 +87,7 @@ __global__ __launch_bounds__(kWg) void k_sample_gather(SampleArgs sa, GatherArgs
     __shared__ int64_t s_slot;
     const int64_t gather_wgs = (int64_t)gridDim.x - sampler_wgs;
     if ((int64_t)blockIdx.x >= gather_wgs) {
-        sampler_wg<PRE, DEPTH>(sa, dv, (int64_t)blockIdx.x - gather_wgs);
+        sampler_wg<kWg, PRE, DEPTH>(sa, dv, (int64_t)blockIdx.x - gather_wgs);
         return;
     }
     const int64_t b = blockIdx.x;
@@ -144,7 +147,7 @@ __global__ __launch_bounds__(kWg) void k_sample_gather_nstep(SampleArgs sa, Gath
     __shared__ int64_t s_slot, s_next;
     const int64_t gather_wgs = (int64_t)gridDim.x - sampler_wgs;
     if ((int64_t)blockIdx.x >= gather_wgs) {
-        sampler_wg<PRE, DEPTH>(sa, dv, (int64_t)blockIdx.x - gather_wgs);
+        sampler_wg<kWg, PRE, DEPTH>(sa, dv, (int64_t)blockIdx.x - gather_wgs);
         return;
     }
     const int64_t b = blockIdx.x / kNstepWgsPerSample;
@@ -200,6 +203,44 @@ hipError_t launch_nstep_xf(const SampleArgs& sa, const GatherArgs& ga, const Nst
                               FusedNstepLaunch<XF>{sa, ga, na, next_out, make_divb((uint64_t)sa.batch), bpf, s});
 }
 
+// Sampler + token packing in one launch (ragged buffers): one pack workgroup
+// of 256 lanes per sample at the head of the grid, whose first wavefront
+// descends for the sample before the workgroup packs the row (pack_row), and
+// sampler workgroups of 256 lanes (four samples each) at the tail for the
+// indices and the importance weights, as in k_sample_gather.
+constexpr int kPackWg = kThreads;
+
+template <int PRE, int DEPTH>
+__global__ __launch_bounds__(kPackWg) void k_sample_pack(SampleArgs sa, PackArgs pa, DivB dv, int32_t sampler_wgs) {
+    __shared__ int64_t s_slot;
+    const int64_t pack_wgs = (int64_t)gridDim.x - sampler_wgs;
+    if ((int64_t)blockIdx.x >= pack_wgs) {
+        sampler_wg<kPackWg, PRE, DEPTH>(sa, dv, (int64_t)blockIdx.x - pack_wgs);
+        return;
+    }
+    const int64_t b = blockIdx.x;
+    if (threadIdx.x < kWave) {
+        const Descent d = tree_descend<PRE, DEPTH>(sa.tree, sa.uniforms, b, dv);
+        if (threadIdx.x == 0) s_slot = d.slot;
+    }
+    __syncthreads();
+    pack_row(pa, b, s_slot);
+}
+
+struct PackLaunch {
+    const SampleArgs& sa;
+    const PackArgs& pa;
+    DivB dv;
+    hipStream_t s;
+    template <int PRE, int DEPTH>
+    hipError_t operator()() const {
+        const int64_t sampler_wgs = (sa.batch + kPackWg / kWave - 1) / (kPackWg / kWave);
+        const dim3 grid((unsigned)(sampler_wgs + sa.batch)), block(kPackWg);
+        hipLaunchKernelGGL((k_sample_pack<PRE, DEPTH>), grid, block, 0, s, sa, pa, dv, (int32_t)sampler_wgs);
+        return hipGetLastError();
+    }
+};
+
 }  // namespace
 
 hipError_t launch_sample_gather(const SampleArgs& sa, const GatherArgs& ga, hipStream_t s) {
@@ -233,6 +274,11 @@ hipError_t launch_sample_gather_nstep(const SampleArgs& sa, const GatherArgs& ga
         case CONDUIT_XF_U8_BF16_NORM: return launch_nstep_xf<CONDUIT_XF_U8_BF16_NORM>(sa, ga, na, next_out, s, bpf);
         default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_sample_pack(const SampleArgs& sa, const PackArgs& pa, hipStream_t s) {
+    if (sa.batch <= 0 || pa.n != sa.batch) return hipErrorNotSupported;
+    return with_descent_shape(sa.tree, descend_prefetch(sa.tree), PackLaunch{sa, pa, make_divb((uint64_t)sa.batch), s});
 }
 
 }  // namespace conduit

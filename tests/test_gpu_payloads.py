@@ -99,7 +99,7 @@ def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values,
     ret = torch.empty((batch, max_len), dtype=torch.float32, device="cuda")
     rng = np.random.default_rng(4)
     for it in range(iters):
-        if fused:  # ragged: sampler then packing kernel behind one call
+        if fused:  # ragged: the sampler + packing kernel, one launch
             idx, w = buf.sample_gather(dev(u[it]), xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
         else:
             idx, w = buf.sample(dev(u[it]))
@@ -161,10 +161,11 @@ def test_tokens_long_rows_segmented_gae():
 
 
 @pytest.mark.slow
-def test_tokens_full_size():
-    print("tokens: cap 65536 x 4096, batch 256, 2 iterations", flush=True)
+@pytest.mark.parametrize("fused", [False, True])
+def test_tokens_full_size(fused):
+    print(f"tokens: cap 65536 x 4096, batch 256, 2 iterations, fused={fused}", flush=True)
     run_tokens(cap=65536, max_len=4096, min_len=512, prefill=65536, iters=2, batch=256, chunk=4096,
-               with_values=False)
+               with_values=False, fused=fused)
 
 
 def run_stress(cap, d, prefill, iters, batch, chunk, check_rows):
