@@ -580,6 +580,15 @@ def bench_tokens(iters=10):
         it_calls.append(gae)
         it_calls.append(lambda i=i: L.conduit_update_priorities(h, pi[i], pp[i], B, stream))
     iter_ms = _b2b_ms(it_calls) * 3
+    # the same iterations with the packed rows' GAE inside the delivery launch
+    # (conduit_sample_pack_gae)
+    spg = L.conduit_sample_pack_gae
+    one_calls = []
+    for i in range(iters):
+        one_calls.append(lambda i=i: spg(h, B, pu[i], pi[i], pw[i], xfr, lbr, None, cfg.gamma, cfg.lam,
+                                         adv.data_ptr(), ret.data_ptr(), stream))
+        one_calls.append(lambda i=i: L.conduit_update_priorities(h, pi[i], pp[i], B, stream))
+    iter_one_ms = _b2b_ms(one_calls) * 2
     mean_len = float(length.float().mean())
     pack_ms = _b2b_ms([lambda i=i: L.conduit_gather_transform(h, pi[i], B, xfr, lbr, stream) for i in range(iters)])
     gae_ms = _b2b_ms([gae] * iters)
@@ -593,6 +602,7 @@ def bench_tokens(iters=10):
         "gae_packed_256x4096": {"bytes": gbytes, "us": gae_ms * 1e3, "GBps": gbytes / gae_ms / 1e6,
                                 "frac": gbytes / gae_ms / 1e6 / PEAK_HBM_GBPS},
         "iteration_us": iter_ms * 1e3,
+        "iteration_one_launch_gae_us": iter_one_ms * 1e3,
         "timing": "back-to-back launches between two events, arguments prepared up front",
     }
 
@@ -1404,7 +1414,7 @@ def _row_summary(name, r):
                     "iteration_us": r["iteration_us"]}
         if name == "tokens":
             return {"pack_us": r["pack_256x4096"]["us"], "gae_packed_us": r["gae_packed_256x4096"]["us"],
-                    "iteration_us": r["iteration_us"]}
+                    "iteration_us": r["iteration_us"], "iteration_one_launch_gae_us": r["iteration_one_launch_gae_us"]}
         if name == "stress":
             return {k: round(v["iteration_us"], 2) for k, v in r.items()}
         if name in ("schedule", "schedule_onpolicy"):

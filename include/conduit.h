@@ -38,7 +38,7 @@
  *     conduit_sync_check() waits for a stream and reports the flag.
  *   - conduit_last_error() returns a thread-local message for the last failure.
  *   - The delivery and on-policy calls (conduit_sample, conduit_gather_transform,
- *     conduit_sample_gather, conduit_sample_gather_nstep,
+ *     conduit_sample_gather, conduit_sample_gather_nstep, conduit_sample_pack_gae,
  *     conduit_update_priorities, conduit_nstep, the GAE
  *     calls, conduit_minibatch_gather) only enqueue kernels: no allocation,
  *     memset or synchronisation, so they may be captured into a HIP graph and
@@ -398,6 +398,24 @@ conduit_status conduit_sample_gather_nstep(conduit_buffer* buf, int64_t batch, c
                                            const conduit_learner_batch* out, int32_t n, double gamma,
                                            int64_t* next_idx, float* ret, float* discount, uint8_t* valid,
                                            void* next_obs, void* stream);
+
+/*
+ * Token delivery with advantages in one launch (Sec. 2.2: delivery samples and
+ * pads sequences into a batch; on-policy-style advantage computation over the
+ * packed rows, as for GRPO-shaped token workloads): exactly
+ * conduit_sample_gather(buf, batch, uniforms, idx_out, is_w_out, xf, out)
+ * on a ragged buffer followed by conduit_gae_packed(out->reward, out->length,
+ * values, batch, max_len, gamma, lambda, adv, ret), with the same outputs,
+ * layouts and errors as the two calls.  Each sample's workgroup descends the
+ * tree, packs its row and runs the row's GAE from the length and reward it has
+ * just written.  out->reward and out->length must not be NULL (the GAE reads
+ * them); values is NULL (V = 0) or a device [batch, max_len] array.  Errors:
+ * EINVAL (a dense buffer, NULL outputs, bad transform), EEMPTY, ESTATE.
+ */
+conduit_status conduit_sample_pack_gae(conduit_buffer* buf, int64_t batch, const uint64_t* uniforms,
+                                      int64_t* idx_out, float* is_w_out, const conduit_transform* xf,
+                                      const conduit_learner_batch* out, const float* values, double gamma,
+                                      double lambda, float* adv, float* ret, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Returns / advantages (Sec. 2.2: on-policy ingestion derives returns and

@@ -129,6 +129,7 @@ SIGNATURES = {
     "conduit_gather_transform": (ST, [P, P, I64, P, P, P]),
     "conduit_sample_gather": (ST, [P, I64, P, P, P, P, P, P]),
     "conduit_sample_gather_nstep": (ST, [P, I64, P, P, P, P, P, I32_, F64, P, P, P, P, P, P]),
+    "conduit_sample_pack_gae": (ST, [P, I64, P, P, P, P, P, P, F64, F64, P, P, P]),
     "conduit_gae": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_gae_noalloc": (ST, [P, P, P, P, I64, I64, F64, F64, P, P, P]),
     "conduit_update_ingest": (ST, [P, P, P, I64, P, P]),
@@ -391,6 +392,21 @@ def conduit_sample_gather_nstep(handle, batch, uniforms, idx_out, is_w_out, xf, 
         _stream(stream)))
 
 
+def conduit_sample_pack_gae(handle, batch, uniforms, idx_out, is_w_out, xf, values, gamma, lam, adv, ret, obs=None,
+                            action=None, reward=None, done=None, mask=None, aux=None, length=None, stream=None):
+    """conduit_sample_gather on a ragged buffer, then conduit_gae_packed over the
+    packed rows, in one launch."""
+    info = _info(handle)
+    out = _batch_ptrs(info, batch, xf, obs, action, reward, done, mask, aux, length)
+    L = info.max_len
+    _check(lib().conduit_sample_pack_gae(
+        handle, batch, _ptr(uniforms, _ELEM8_INT, "uniforms", numel=batch),
+        _ptr(idx_out, torch.int64, "idx_out", numel=batch), _ptr(is_w_out, torch.float32, "is_w_out", numel=batch),
+        C.byref(xf), C.byref(out), _ptr(values, torch.float32, "values", numel=batch * L), float(gamma), float(lam),
+        _ptr(adv, torch.float32, "adv", numel=batch * L), _ptr(ret, torch.float32, "ret", numel=batch * L),
+        _stream(stream)))
+
+
 def conduit_nstep(handle, idx, n, gamma, next_idx, ret, discount, valid, xf=None, next_obs=None, stream=None):
     """n-step return targets (and bootstrap-state stacks) of sampled slots."""
     B = idx.numel()
@@ -645,6 +661,17 @@ class ReplayBuffer:
 
     def gather(self, idx, xf, **outs):
         conduit_gather_transform(self.handle, idx, xf, stream=outs.pop("stream", None), **outs)
+
+    def sample_pack_gae(self, uniforms, xf, gamma, lam, adv, ret, values=None, **outs):
+        """(idx, w) of one token delivery whose packed rows' GAE goes to adv
+        and ret in the same launch."""
+        B = uniforms.numel()
+        dev = uniforms.device
+        idx = torch.empty(B, dtype=torch.int64, device=dev)
+        w = torch.empty(B, dtype=torch.float32, device=dev)
+        conduit_sample_pack_gae(self.handle, B, uniforms, idx, w, xf, values, gamma, lam, adv, ret,
+                                stream=outs.pop("stream", None), **outs)
+        return idx, w
 
     def sample_gather_nstep(self, uniforms, xf, n, gamma, next_obs=None, **outs):
         """(idx, w, next_idx, ret, discount, valid) of one fused delivery with

@@ -788,7 +788,7 @@ conduit_status conduit_sample_gather(conduit_buffer* b, int64_t batch, const uin
     set_leaf_min(b, &sa);
     hipStream_t s = static_cast<hipStream_t>(stream);
     // dense rows of a few work items, and ragged rows: one fused launch
-    hipError_t e = b->opts.ragged ? launch_sample_pack(sa, pa, s) : launch_sample_gather(sa, ga, s);
+    hipError_t e = b->opts.ragged ? launch_sample_pack(sa, pa, nullptr, s) : launch_sample_gather(sa, ga, s);
     if (e == hipErrorNotSupported) {
         // otherwise the sampler parks the sampled leaves in is_w_out, and the
         // gather (or packing) launch carries one more workgroup that turns them
@@ -917,6 +917,43 @@ conduit_status conduit_sample_gather_nstep(conduit_buffer* b, int64_t batch, con
     st = conduit_sample_gather(b, batch, uniforms, idx_out, is_w_out, xf, out, stream);
     if (st != CONDUIT_OK) return st;
     return conduit_nstep(b, idx_out, batch, n, gamma, next_idx, ret, discount, valid, xf, next_obs, stream);
+}
+
+conduit_status conduit_sample_pack_gae(conduit_buffer* b, int64_t batch, const uint64_t* uniforms, int64_t* idx_out,
+                                      float* is_w_out, const conduit_transform* xf, const conduit_learner_batch* out,
+                                      const float* values, double gamma, double lambda, float* adv, float* ret,
+                                      void* stream) {
+    if (!b || !xf || !out) return fail(CONDUIT_EINVAL, "NULL buffer, transform or output");
+    conduit_status st = check_flags(b->err_slot);
+    if (st != CONDUIT_OK) return st;
+    if (!b->opts.prioritized) return fail(CONDUIT_EINVAL, "buffer was created without priorities");
+    if (!b->opts.ragged) return fail(CONDUIT_EINVAL, "packing needs a ragged buffer");
+    if (batch < 1 || batch > (1LL << 20)) return fail(CONDUIT_EINVAL, "batch must be in [1, 2^20]");
+    if (!uniforms || !idx_out) return fail(CONDUIT_EINVAL, "uniforms and idx_out must not be NULL");
+    if (!out->reward || !out->length) return fail(CONDUIT_EINVAL, "the GAE reads the packed rewards and lengths");
+    if (!adv || !ret) return fail(CONDUIT_EINVAL, "adv and ret must not be NULL");
+    if (!(gamma == gamma) || !(lambda == lambda)) return fail(CONDUIT_EINVAL, "gamma/lambda must be numbers");
+    if (b->size == 0) return fail(CONDUIT_EEMPTY, "sample from an empty buffer");
+    GatherArgs ga_unused{};
+    PackArgs pa{};
+    st = prepare_gather(b, idx_out, batch, xf, out, &ga_unused, &pa);
+    if (st != CONDUIT_OK) return st;
+    DeviceGuard g(b->device);
+    SampleArgs sa{};
+    sa.tree = b->tree;
+    sa.uniforms = uniforms;
+    sa.idx_out = idx_out;
+    sa.w_out = is_w_out;
+    sa.batch = batch;
+    sa.beta = b->opts.beta;
+    sa.state = b->state;
+    sa.err = err_words(b->err_slot);
+    set_leaf_min(b, &sa);
+    const GaePackedArgs gp{out->reward, out->length, values, batch, b->layout.max_len, gamma, lambda,
+                           adv, ret, err_words(b->err_slot)};
+    const hipError_t e = launch_sample_pack(sa, pa, &gp, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "sample_pack_gae launch");
+    return CONDUIT_OK;
 }
 
 // true if [a, a + na) and [b, b + nb) share a byte (NULL ranges share none)

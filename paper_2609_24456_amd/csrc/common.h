@@ -465,9 +465,6 @@ struct PackArgs {
 };
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
-// sample + pack in one launch (ragged buffers); hipErrorNotSupported if the
-// batch and the pack arguments disagree
-hipError_t launch_sample_pack(const SampleArgs& sa, const PackArgs& pa, hipStream_t s);
 
 // time-major GAE addresses a slab of the rollout with 32-bit offsets
 constexpr int64_t kGaeMaxEnvs = 1ll << 19;
@@ -536,6 +533,10 @@ struct GaePackedArgs {
 };
 
 hipError_t launch_gae_packed(const GaePackedArgs& a, hipStream_t s);
+// sample + pack in one launch (ragged buffers), and with ga the GAE of every
+// packed row in the same launch; hipErrorNotSupported if the batch and the
+// other arguments disagree
+hipError_t launch_sample_pack(const SampleArgs& sa, const PackArgs& pa, const GaePackedArgs* ga, hipStream_t s);
 
 hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t n, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int64_t n, hipStream_t s);

@@ -621,7 +621,13 @@ struct UnionGather {
 // with an error flag), by one workgroup of kThreads lanes.
 constexpr int kPackQuads = 4;
 
-__device__ void pack_row(const PackArgs& a, int64_t b, int64_t i) {
+// what pack_row wrote for the row: its length and reward columns
+struct PackedRow {
+    int64_t L;
+    float R;
+};
+
+__device__ PackedRow pack_row(const PackArgs& a, int64_t b, int64_t i) {
     const bool ok = i >= 0 && i < a.size;
     if (!ok && threadIdx.x == 0) flag_error(a.err, ERR_GATHER_INDEX);
     // the row's scalar columns are loaded now, with its length, and stored last
@@ -681,6 +687,7 @@ __device__ void pack_row(const PackArgs& a, int64_t b, int64_t i) {
         for (int c = (int)threadIdx.x + kThreads; c < a.action_bytes; c += kThreads)
             a.out_action[b * a.action_bytes + c] = ok ? a.action[si * a.action_bytes + c] : (uint8_t)0;
     }
+    return PackedRow{L, ok ? rew : 0.0f};
 }
 
 }  // namespace

@@ -34,6 +34,7 @@
 // back the L2 under the frame stores) is needed, and the ticket latency stays
 // off the frame workgroups.
 #include "descend.h"
+#include "gae_packed_dev.h"
 #include "gather_dev.h"
 #include "nstep_dev.h"
 
@@ -210,8 +211,14 @@ hipError_t launch_nstep_xf(const SampleArgs& sa, const GatherArgs& ga, const Nst
 // indices and the importance weights, as in k_sample_gather.
 constexpr int kPackWg = kThreads;
 
-template <int PRE, int DEPTH>
-__global__ __launch_bounds__(kPackWg) void k_sample_pack(SampleArgs sa, PackArgs pa, DivB dv, int32_t sampler_wgs) {
+// With GAE, each pack workgroup then runs the GAE of its packed row from the
+// length and reward it has just written (gae_packed_row), as
+// conduit_gae_packed would over the packed batch.
+static_assert(kPackWg == kPkThreads, "the packed GAE takes the pack workgroup as it is");
+
+template <int PRE, int DEPTH, bool GAE>
+__global__ __launch_bounds__(kPackWg) void k_sample_pack(SampleArgs sa, PackArgs pa, GaePackedArgs ga, DivB dv,
+                                                         int32_t sampler_wgs) {
     __shared__ int64_t s_slot;
     const int64_t pack_wgs = (int64_t)gridDim.x - sampler_wgs;
     if ((int64_t)blockIdx.x >= pack_wgs) {
@@ -224,19 +231,26 @@ __global__ __launch_bounds__(kPackWg) void k_sample_pack(SampleArgs sa, PackArgs
         if (threadIdx.x == 0) s_slot = d.slot;
     }
     __syncthreads();
-    pack_row(pa, b, s_slot);
+    const PackedRow row = pack_row(pa, b, s_slot);
+    if constexpr (GAE) gae_packed_row(ga, b, row.L, (double)row.R);
 }
 
 struct PackLaunch {
     const SampleArgs& sa;
     const PackArgs& pa;
+    const GaePackedArgs* ga;  // NULL: no GAE
     DivB dv;
     hipStream_t s;
     template <int PRE, int DEPTH>
     hipError_t operator()() const {
         const int64_t sampler_wgs = (sa.batch + kPackWg / kWave - 1) / (kPackWg / kWave);
         const dim3 grid((unsigned)(sampler_wgs + sa.batch)), block(kPackWg);
-        hipLaunchKernelGGL((k_sample_pack<PRE, DEPTH>), grid, block, 0, s, sa, pa, dv, (int32_t)sampler_wgs);
+        if (ga)
+            hipLaunchKernelGGL((k_sample_pack<PRE, DEPTH, true>), grid, block, 0, s, sa, pa, *ga, dv,
+                               (int32_t)sampler_wgs);
+        else
+            hipLaunchKernelGGL((k_sample_pack<PRE, DEPTH, false>), grid, block, 0, s, sa, pa, GaePackedArgs{}, dv,
+                               (int32_t)sampler_wgs);
         return hipGetLastError();
     }
 };
@@ -276,9 +290,10 @@ hipError_t launch_sample_gather_nstep(const SampleArgs& sa, const GatherArgs& ga
     }
 }
 
-hipError_t launch_sample_pack(const SampleArgs& sa, const PackArgs& pa, hipStream_t s) {
-    if (sa.batch <= 0 || pa.n != sa.batch) return hipErrorNotSupported;
-    return with_descent_shape(sa.tree, descend_prefetch(sa.tree), PackLaunch{sa, pa, make_divb((uint64_t)sa.batch), s});
+hipError_t launch_sample_pack(const SampleArgs& sa, const PackArgs& pa, const GaePackedArgs* ga, hipStream_t s) {
+    if (sa.batch <= 0 || pa.n != sa.batch || (ga && ga->B != sa.batch)) return hipErrorNotSupported;
+    return with_descent_shape(sa.tree, descend_prefetch(sa.tree),
+                              PackLaunch{sa, pa, ga, make_divb((uint64_t)sa.batch), s});
 }
 
 }  // namespace conduit

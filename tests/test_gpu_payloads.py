@@ -70,7 +70,7 @@ def test_large_payload_full_size():
 
 
 def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values, fused=False, placement=cd.PLACE_HBM,
-               weight_norm=cd.WNORM_BATCH):
+               weight_norm=cd.WNORM_BATCH, with_gae=False):
     cfg = synth.Tokens(prefill, max_len=max_len, min_len=min_len)
     u, prio = cfg.draws(iters, batch)
     buf = cd.ReplayBuffer(cap, (max_len,), torch.int32, action_bytes=4, ragged=True, aux_elem_bytes=4,
@@ -99,14 +99,21 @@ def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values,
     ret = torch.empty((batch, max_len), dtype=torch.float32, device="cuda")
     rng = np.random.default_rng(4)
     for it in range(iters):
-        if fused:  # ragged: the sampler + packing kernel, one launch
-            idx, w = buf.sample_gather(dev(u[it]), xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
-        else:
-            idx, w = buf.sample(dev(u[it]))
-            buf.gather(idx, xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
         vals = rng.standard_normal((batch, max_len)).astype(np.float32) if with_values else None
-        cd.conduit_gae_packed(rew, length, dev(vals) if vals is not None else None, max_len, cfg.gamma, cfg.lam,
-                              adv, ret)
+        if with_gae:  # sampler + packing + GAE of the packed rows, one launch
+            adv.fill_(float("nan"))
+            ret.fill_(float("nan"))
+            idx, w = buf.sample_pack_gae(dev(u[it]), xf, cfg.gamma, cfg.lam, adv, ret,
+                                         values=dev(vals) if vals is not None else None, obs=seq, mask=mask,
+                                         aux=lp_out, length=length, reward=rew)
+        else:
+            if fused:  # ragged: the sampler + packing kernel, one launch
+                idx, w = buf.sample_gather(dev(u[it]), xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
+            else:
+                idx, w = buf.sample(dev(u[it]))
+                buf.gather(idx, xf, obs=seq, mask=mask, aux=lp_out, length=length, reward=rew)
+            cd.conduit_gae_packed(rew, length, dev(vals) if vals is not None else None, max_len, cfg.gamma, cfg.lam,
+                                  adv, ret)
         buf.update(idx, dev(prio[it]))
         o_idx, o_w = orc.sample(u[it])
         assert np.array_equal(host(idx), o_idx), it
@@ -155,17 +162,28 @@ def test_tokens_payload_in_pinned_host_memory(fused):
                fused=fused, placement=cd.PLACE_HOST_PINNED)
 
 
-def test_tokens_long_rows_segmented_gae():
-    print("tokens: max_len 8192 (two GAE segments), batch 16", flush=True)
-    run_tokens(cap=40, max_len=8192, min_len=3000, prefill=50, iters=2, batch=16, chunk=25, with_values=True)
+@pytest.mark.parametrize("with_gae", [False, True])
+def test_tokens_long_rows_segmented_gae(with_gae):
+    print(f"tokens: max_len 8192 (two GAE segments), batch 16, one-launch GAE={with_gae}", flush=True)
+    run_tokens(cap=40, max_len=8192, min_len=3000, prefill=50, iters=2, batch=16, chunk=25, with_values=True,
+               with_gae=with_gae)
+
+
+@pytest.mark.parametrize("with_values,weight_norm", [(True, cd.WNORM_BATCH), (False, cd.WNORM_BUFFER)])
+def test_tokens_sample_pack_gae_one_launch(with_values, weight_norm):
+    print(f"tokens: sample + pack + GAE in one launch, values={with_values}, weight_norm={weight_norm}", flush=True)
+    run_tokens(cap=300, max_len=256, min_len=8, prefill=400, iters=3, batch=64, chunk=128, with_values=with_values,
+               weight_norm=weight_norm, with_gae=True)
+    run_tokens(cap=300, max_len=300, min_len=1, prefill=330, iters=2, batch=77, chunk=100, with_values=with_values,
+               weight_norm=weight_norm, with_gae=True)
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("fused", [False, True])
-def test_tokens_full_size(fused):
-    print(f"tokens: cap 65536 x 4096, batch 256, 2 iterations, fused={fused}", flush=True)
+@pytest.mark.parametrize("fused,with_gae", [(False, False), (True, False), (True, True)])
+def test_tokens_full_size(fused, with_gae):
+    print(f"tokens: cap 65536 x 4096, batch 256, 2 iterations, fused={fused}, one-launch GAE={with_gae}", flush=True)
     run_tokens(cap=65536, max_len=4096, min_len=512, prefill=65536, iters=2, batch=256, chunk=4096,
-               with_values=False, fused=fused)
+               with_values=False, fused=fused, with_gae=with_gae)
 
 
 def run_stress(cap, d, prefill, iters, batch, chunk, check_rows):
