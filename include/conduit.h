@@ -604,6 +604,89 @@ typedef enum {
 conduit_status conduit_buffer_read(const conduit_buffer* buf, conduit_column col, int32_t level, int64_t offset,
                                    int64_t nbytes, void* dst, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Checkpoint / resume of a buffer.  The paper's buffers are long-lived state
+ * (Sec. 2.2: the off-policy buffer keeps the stored transitions with their
+ * indices and metadata, and the priority structure over them); these calls
+ * turn that state into one byte image and back, so that a run can stop and
+ * resume with the same buffer contents, ring position and priorities.
+ *
+ * Image layout (native byte order, little-endian on this platform): a
+ * conduit_ckpt_header, then the sections the header lists, each starting at a
+ * multiple of 256 bytes, in this order, each present only if the buffer holds
+ * the column: OBS, ACTION, REWARD, DONE, EPISODE, STEP, LENGTH, AUX, LEAVES,
+ * MAX_PRIO (layouts as in conduit_column; whole columns, all `capacity` slots).
+ * The sum tree above the leaves is not stored: it is a function of the leaves
+ * (integer sums), and restoring recomputes it exactly.
+ * ------------------------------------------------------------------------- */
+#define CONDUIT_CKPT_MAGIC "CNDTCKPT"
+#define CONDUIT_CKPT_VERSION 1u
+#define CONDUIT_CKPT_MAX_SECTIONS 10
+
+typedef struct {
+    int32_t column;    /* conduit_column */
+    int32_t reserved;  /* 0 */
+    int64_t offset;    /* bytes from the start of the image, a multiple of 256 */
+    int64_t bytes;     /* section length in bytes */
+} conduit_ckpt_section;
+
+typedef struct {
+    char magic[8];             /* CONDUIT_CKPT_MAGIC, without its terminating NUL */
+    uint32_t version;          /* CONDUIT_CKPT_VERSION */
+    uint32_t n_sections;
+    uint64_t image_bytes;      /* whole image: header, sections and the padding between them */
+    int64_t capacity;
+    int64_t row_bytes;         /* observation bytes per slot */
+    int64_t max_len;           /* ragged slot length in elements, 0 otherwise */
+    int32_t obs_dtype;         /* conduit_dtype */
+    int32_t prioritized;
+    int32_t alpha_num, alpha_den;
+    int32_t action_bytes;
+    int32_t ragged;
+    int32_t aux_elem_bytes;
+    int32_t reserved;          /* 0 */
+    int64_t head, size;        /* ring state: next slot to write, stored transitions */
+    uint64_t total;            /* transitions ever ingested */
+    conduit_ckpt_section section[CONDUIT_CKPT_MAX_SECTIONS];
+} conduit_ckpt_header;
+
+/* Size in bytes of the checkpoint image of `buf` (*bytes).  Errors: EINVAL (NULL argument). */
+conduit_status conduit_buffer_checkpoint_bytes(const conduit_buffer* buf, uint64_t* bytes);
+
+/*
+ * Write the checkpoint image of `buf` to `dst` (device memory, pinned or
+ * pageable host memory; `dst_bytes` its size, at least
+ * conduit_buffer_checkpoint_bytes).  The copies are ordered after the work
+ * already enqueued on `stream`, and the call waits for them: on return the
+ * image is complete and `buf` may change again.  Work on other streams that
+ * writes the buffer must be ordered before this call by the caller.
+ * The caller owns `dst`.
+ * Errors: EINVAL (NULL argument, dst_bytes too small), EDEVICE.
+ */
+conduit_status conduit_buffer_checkpoint(const conduit_buffer* buf, void* dst, uint64_t dst_bytes, void* stream);
+
+/*
+ * Replace the whole state of `buf` with the image at `src` (device or host
+ * memory, `src_bytes` long), made by conduit_buffer_checkpoint from a buffer
+ * of the same capacity, observation bytes and dtype, prioritisation, alpha,
+ * action bytes and ragged layout (max_len, aux_elem_bytes).  Options that only
+ * steer later calls (beta, weight normalisation, frame stack, payload
+ * placement, single_stream) may differ: an image taken from an HBM buffer
+ * restores into a host-placed one.  The columns and the ring state (head,
+ * size, total) become the image's, the sum tree is recomputed from the leaves,
+ * and the running maximum priority is the image's.  Ordered after the work on
+ * `stream`; the call waits for its copies and kernels, so `src` may be freed
+ * on return.  The header is checked (magic, version, the layout fields above,
+ * the section table against this buffer's columns, a ring state reachable by
+ * ingestion: size = min(total, capacity) and head = total mod capacity); the
+ * column contents are taken as they are.  On an error nothing of `buf` has
+ * been changed, except on EDEVICE during the copies, after which the buffer's
+ * contents are undefined (restore again).
+ * Errors: EINVAL (NULL argument, src_bytes too small, a header that does not
+ * describe an image of this buffer), EDEVICE.
+ */
+conduit_status conduit_buffer_restore(conduit_buffer* buf, const void* src, uint64_t src_bytes, void* stream);
+
 /*
  * Wait for `stream`, then report the sticky device-side error flag of `buf`
  * (NULL: the flag shared by the stand-alone calls conduit_gae,

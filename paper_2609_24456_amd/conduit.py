@@ -112,6 +112,24 @@ class BufferInfo(C.Structure):
                 ("aux_elem_bytes", C.c_int32), ("max_len", C.c_int64)]
 
 
+CKPT_MAGIC = b"CNDTCKPT"
+CKPT_MAX_SECTIONS = 10
+
+
+class CkptSection(C.Structure):
+    _fields_ = [("column", C.c_int32), ("reserved", C.c_int32), ("offset", C.c_int64), ("bytes", C.c_int64)]
+
+
+class CkptHeader(C.Structure):
+    _fields_ = [("magic", C.c_char * 8), ("version", C.c_uint32), ("n_sections", C.c_uint32),
+                ("image_bytes", C.c_uint64), ("capacity", C.c_int64), ("row_bytes", C.c_int64),
+                ("max_len", C.c_int64), ("obs_dtype", C.c_int32), ("prioritized", C.c_int32),
+                ("alpha_num", C.c_int32), ("alpha_den", C.c_int32), ("action_bytes", C.c_int32),
+                ("ragged", C.c_int32), ("aux_elem_bytes", C.c_int32), ("reserved", C.c_int32),
+                ("head", C.c_int64), ("size", C.c_int64), ("total", C.c_uint64),
+                ("section", CkptSection * CKPT_MAX_SECTIONS)]
+
+
 # every symbol include/conduit.h declares, with its ctypes signature
 P = C.c_void_p
 I64 = C.c_int64
@@ -141,6 +159,9 @@ SIGNATURES = {
     "conduit_buffer_get_info": (ST, [P, P]),
     "conduit_buffer_stats": (ST, [P, P, P, P]),
     "conduit_buffer_read": (ST, [P, I32_, I32_, I64, I64, P, P]),
+    "conduit_buffer_checkpoint_bytes": (ST, [P, P]),
+    "conduit_buffer_checkpoint": (ST, [P, P, C.c_uint64, P]),
+    "conduit_buffer_restore": (ST, [P, P, C.c_uint64, P]),
     "conduit_sync_check": (ST, [P, P]),
     "conduit_clear_error": (None, [P]),
     "conduit_last_error": (C.c_char_p, []),
@@ -584,6 +605,42 @@ def conduit_buffer_read(handle, col, dst, offset=0, level=0, stream=None):
                                      _ptr(dst, None, "dst"), _stream(stream)))
 
 
+def conduit_buffer_checkpoint_bytes(handle):
+    n = C.c_uint64()
+    _check(lib().conduit_buffer_checkpoint_bytes(handle, C.byref(n)))
+    return n.value
+
+
+def _image_ptr(t, name, nbytes=None):
+    """Address of a contiguous uint8 image tensor, on the device or in host memory."""
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.uint8:
+        raise TypeError(f"{name} must be a torch.uint8 tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if nbytes is not None and t.numel() < nbytes:
+        raise ValueError(f"{name} holds {t.numel()} bytes, the image needs {nbytes}")
+    return t.data_ptr()
+
+
+def conduit_buffer_checkpoint(handle, dst, stream=None):
+    """Write the buffer's checkpoint image into `dst` (uint8 tensor, device or host memory)."""
+    n = conduit_buffer_checkpoint_bytes(handle)
+    _check(lib().conduit_buffer_checkpoint(handle, _image_ptr(dst, "dst", n), dst.numel(), _stream(stream)))
+
+
+def conduit_buffer_restore(handle, src, stream=None):
+    """Replace the buffer's state with the checkpoint image in `src` (uint8 tensor)."""
+    _check(lib().conduit_buffer_restore(handle, _image_ptr(src, "src"), src.numel(), _stream(stream)))
+
+
+def ckpt_header(image):
+    """The header of a checkpoint image held in host memory (a uint8 tensor or bytes)."""
+    raw = bytes(image[:C.sizeof(CkptHeader)].numpy()) if isinstance(image, torch.Tensor) else bytes(image[:C.sizeof(CkptHeader)])
+    if len(raw) < C.sizeof(CkptHeader) or raw[:8] != CKPT_MAGIC:
+        raise ValueError("not a checkpoint image")
+    return CkptHeader.from_buffer_copy(raw)
+
+
 def conduit_sync_check(handle=None, stream=None):
     return lib().conduit_sync_check(handle, _stream(stream))
 
@@ -691,6 +748,28 @@ class ReplayBuffer:
 
     def read(self, col, dst, offset=0, level=0, stream=None):
         conduit_buffer_read(self.handle, col, dst, offset, level, stream)
+
+    def checkpoint(self, dst=None, pin=True, stream=None):
+        """The buffer's checkpoint image: written into `dst` if given, else into a
+        new host tensor (pinned unless pin=False).  Returns the image tensor."""
+        if dst is None:
+            n = conduit_buffer_checkpoint_bytes(self.handle)
+            dst = torch.empty(n, dtype=torch.uint8, pin_memory=pin)
+        conduit_buffer_checkpoint(self.handle, dst, stream)
+        return dst
+
+    def restore(self, src, stream=None):
+        conduit_buffer_restore(self.handle, src, stream)
+
+    def save(self, path, stream=None):
+        """Checkpoint image written to a file."""
+        img = self.checkpoint(pin=False, stream=stream)
+        img.numpy().tofile(path)
+
+    def load(self, path, stream=None):
+        """State restored from a file written by save()."""
+        img = torch.from_file(path, shared=False, size=os.path.getsize(path), dtype=torch.uint8)
+        self.restore(img, stream)
 
     def sync_check(self, stream=None):
         return conduit_sync_check(self.handle, stream)

@@ -273,6 +273,82 @@ BufferGeometry conduit::buffer_geometry(const conduit_buffer* b) {
     return g;
 }
 
+// Device (or mapped host) address and size in bytes of one column; a column
+// the buffer does not hold has size 0.
+static conduit_status column_span(const conduit_buffer* b, conduit_column col, int32_t level, uint8_t** base,
+                                  int64_t* bytes) {
+    const Layout& L = b->layout;
+    const int64_t C = b->capacity;
+    uint8_t* p = nullptr;
+    int64_t n = 0;
+    switch (col) {
+        case CONDUIT_COL_OBS: p = b->obs; n = C * L.row_bytes; break;
+        case CONDUIT_COL_ACTION: p = b->action; n = b->action ? C * b->opts.action_bytes : 0; break;
+        case CONDUIT_COL_REWARD: p = reinterpret_cast<uint8_t*>(b->reward); n = C * 4; break;
+        case CONDUIT_COL_DONE: p = b->done; n = C; break;
+        case CONDUIT_COL_EPISODE: p = reinterpret_cast<uint8_t*>(b->episode); n = C * 4; break;
+        case CONDUIT_COL_STEP: p = reinterpret_cast<uint8_t*>(b->step); n = C * 4; break;
+        case CONDUIT_COL_LENGTH: p = reinterpret_cast<uint8_t*>(b->length); n = b->length ? C * 4 : 0; break;
+        case CONDUIT_COL_AUX: p = b->aux; n = b->aux ? C * L.max_len * b->opts.aux_elem_bytes : 0; break;
+        case CONDUIT_COL_LEAVES:
+            p = reinterpret_cast<uint8_t*>(b->tree.leaves);
+            n = b->opts.prioritized ? C * 4 : 0;
+            break;
+        case CONDUIT_COL_TREE:
+            if (!b->opts.prioritized || level < 1 || level > L.depth) return fail(CONDUIT_EINVAL, "no such tree level");
+            p = reinterpret_cast<uint8_t*>(b->tree.level[level]);
+            n = L.nodes[level] * 8;
+            break;
+        case CONDUIT_COL_MAX_PRIO: p = reinterpret_cast<uint8_t*>(&b->state->max_prio); n = 4; break;
+        default: return fail(CONDUIT_EINVAL, "unknown column");
+    }
+    *base = p;
+    *bytes = p ? n : 0;
+    return CONDUIT_OK;
+}
+
+// The checkpoint header of `b`: layout fields, ring state and the section
+// table (sections in column order, each at a multiple of 256 bytes).
+static_assert(sizeof(conduit_ckpt_section) == 24 && sizeof(conduit_ckpt_header) == 344,
+              "checkpoint header layout is part of the image format");
+
+static void ckpt_header(const conduit_buffer* b, conduit_ckpt_header* h) {
+    std::memset(h, 0, sizeof(*h));
+    std::memcpy(h->magic, CONDUIT_CKPT_MAGIC, sizeof(h->magic));
+    h->version = CONDUIT_CKPT_VERSION;
+    h->capacity = b->capacity;
+    h->row_bytes = b->layout.row_bytes;
+    h->max_len = b->layout.max_len;
+    h->obs_dtype = (int32_t)b->obs_dtype;
+    h->prioritized = b->opts.prioritized;
+    h->alpha_num = b->opts.alpha_num;
+    h->alpha_den = b->opts.alpha_den;
+    h->action_bytes = b->opts.action_bytes;
+    h->ragged = b->opts.ragged;
+    h->aux_elem_bytes = b->opts.aux_elem_bytes;
+    h->head = b->head;
+    h->size = b->size;
+    h->total = (uint64_t)b->total;
+    static const conduit_column order[] = {CONDUIT_COL_OBS,     CONDUIT_COL_ACTION, CONDUIT_COL_REWARD,
+                                           CONDUIT_COL_DONE,    CONDUIT_COL_EPISODE, CONDUIT_COL_STEP,
+                                           CONDUIT_COL_LENGTH,  CONDUIT_COL_AUX,    CONDUIT_COL_LEAVES,
+                                           CONDUIT_COL_MAX_PRIO};
+    static_assert(sizeof(order) / sizeof(order[0]) == CONDUIT_CKPT_MAX_SECTIONS, "one section per stored column");
+    size_t off = align_up(sizeof(*h));
+    for (conduit_column c : order) {
+        uint8_t* base = nullptr;
+        int64_t n = 0;
+        (void)column_span(b, c, 0, &base, &n);
+        if (n == 0) continue;
+        conduit_ckpt_section& sec = h->section[h->n_sections++];
+        sec.column = (int32_t)c;
+        sec.offset = (int64_t)off;
+        sec.bytes = n;
+        off = align_up(off + (size_t)n);
+    }
+    h->image_bytes = off;
+}
+
 extern "C" {
 
 void conduit_buffer_opts_default(conduit_buffer_opts* o) {
@@ -1109,37 +1185,93 @@ conduit_status conduit_minibatch_gather(const void* src, int64_t row_bytes, int6
 conduit_status conduit_buffer_read(const conduit_buffer* b, conduit_column col, int32_t level, int64_t offset,
                                    int64_t nbytes, void* dst, void* stream) {
     if (!b || !dst) return fail(CONDUIT_EINVAL, "NULL buffer or destination");
-    const Layout& L = b->layout;
-    const int64_t C = b->capacity;
-    const uint8_t* base = nullptr;
+    uint8_t* base = nullptr;
     int64_t bytes = 0;
-    switch (col) {
-        case CONDUIT_COL_OBS: base = b->obs; bytes = C * L.row_bytes; break;
-        case CONDUIT_COL_ACTION: base = b->action; bytes = C * b->opts.action_bytes; break;
-        case CONDUIT_COL_REWARD: base = reinterpret_cast<const uint8_t*>(b->reward); bytes = C * 4; break;
-        case CONDUIT_COL_DONE: base = b->done; bytes = C; break;
-        case CONDUIT_COL_EPISODE: base = reinterpret_cast<const uint8_t*>(b->episode); bytes = C * 4; break;
-        case CONDUIT_COL_STEP: base = reinterpret_cast<const uint8_t*>(b->step); bytes = C * 4; break;
-        case CONDUIT_COL_LENGTH: base = reinterpret_cast<const uint8_t*>(b->length); bytes = b->length ? C * 4 : 0; break;
-        case CONDUIT_COL_AUX: base = b->aux; bytes = b->aux ? C * L.max_len * b->opts.aux_elem_bytes : 0; break;
-        case CONDUIT_COL_LEAVES:
-            base = reinterpret_cast<const uint8_t*>(b->tree.leaves);
-            bytes = b->opts.prioritized ? C * 4 : 0;
-            break;
-        case CONDUIT_COL_TREE:
-            if (!b->opts.prioritized || level < 1 || level > L.depth) return fail(CONDUIT_EINVAL, "no such tree level");
-            base = reinterpret_cast<const uint8_t*>(b->tree.level[level]);
-            bytes = L.nodes[level] * 8;
-            break;
-        case CONDUIT_COL_MAX_PRIO: base = reinterpret_cast<const uint8_t*>(&b->state->max_prio); bytes = 4; break;
-        default: return fail(CONDUIT_EINVAL, "unknown column");
-    }
+    conduit_status st = column_span(b, col, level, &base, &bytes);
+    if (st != CONDUIT_OK) return st;
     if (!base || offset < 0 || nbytes < 0 || offset + nbytes > bytes) return fail(CONDUIT_EINVAL, "range outside the column");
     if (nbytes == 0) return CONDUIT_OK;
     DeviceGuard g(b->device);
     hipError_t e = hipMemcpyAsync(dst, base + offset, (size_t)nbytes, hipMemcpyDefault,
                                   static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "column copy");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_buffer_checkpoint_bytes(const conduit_buffer* b, uint64_t* bytes) {
+    if (!b || !bytes) return fail(CONDUIT_EINVAL, "NULL buffer or size pointer");
+    conduit_ckpt_header h;
+    ckpt_header(b, &h);
+    *bytes = h.image_bytes;
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_buffer_checkpoint(const conduit_buffer* b, void* dst, uint64_t dst_bytes, void* stream) {
+    if (!b || !dst) return fail(CONDUIT_EINVAL, "NULL buffer or destination");
+    conduit_ckpt_header h;
+    ckpt_header(b, &h);
+    if (dst_bytes < h.image_bytes) return fail(CONDUIT_EINVAL, "destination smaller than the checkpoint image");
+    DeviceGuard g(b->device);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint8_t* out = static_cast<uint8_t*>(dst);
+    hipError_t e = hipMemcpyAsync(out, &h, sizeof(h), hipMemcpyDefault, s);
+    for (uint32_t k = 0; k < h.n_sections && e == hipSuccess; ++k) {
+        uint8_t* base = nullptr;
+        int64_t n = 0;
+        (void)column_span(b, (conduit_column)h.section[k].column, 0, &base, &n);
+        e = hipMemcpyAsync(out + h.section[k].offset, base, (size_t)n, hipMemcpyDefault, s);
+    }
+    // the header copy reads this frame's `h`: wait before returning
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "checkpoint copy");
+    return CONDUIT_OK;
+}
+
+conduit_status conduit_buffer_restore(conduit_buffer* b, const void* src, uint64_t src_bytes, void* stream) {
+    if (!b || !src) return fail(CONDUIT_EINVAL, "NULL buffer or source");
+    conduit_ckpt_header h;
+    if (src_bytes < sizeof(h)) return fail(CONDUIT_EINVAL, "source smaller than a checkpoint header");
+    DeviceGuard g(b->device);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(&h, src, sizeof(h), hipMemcpyDefault, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "checkpoint header copy");
+    conduit_ckpt_header want;
+    ckpt_header(b, &want);
+    if (std::memcmp(h.magic, want.magic, sizeof(h.magic)) != 0) return fail(CONDUIT_EINVAL, "not a checkpoint image");
+    if (h.version != want.version) return fail(CONDUIT_EINVAL, "unsupported checkpoint version");
+    if (h.capacity != want.capacity || h.row_bytes != want.row_bytes || h.max_len != want.max_len ||
+        h.obs_dtype != want.obs_dtype || h.prioritized != want.prioritized || h.alpha_num != want.alpha_num ||
+        h.alpha_den != want.alpha_den || h.action_bytes != want.action_bytes || h.ragged != want.ragged ||
+        h.aux_elem_bytes != want.aux_elem_bytes)
+        return fail(CONDUIT_EINVAL, "checkpoint of a buffer with another layout (capacity, observation, "
+                                    "prioritisation, alpha, action or ragged options differ)");
+    if (h.image_bytes != want.image_bytes || h.n_sections != want.n_sections)
+        return fail(CONDUIT_EINVAL, "checkpoint section table does not match this buffer");
+    for (uint32_t k = 0; k < h.n_sections; ++k) {
+        const conduit_ckpt_section& a = h.section[k];
+        const conduit_ckpt_section& w = want.section[k];
+        if (a.column != w.column || a.offset != w.offset || a.bytes != w.bytes)
+            return fail(CONDUIT_EINVAL, "checkpoint section table does not match this buffer");
+    }
+    if (src_bytes < h.image_bytes) return fail(CONDUIT_EINVAL, "source smaller than the checkpoint image");
+    const int64_t C = b->capacity;
+    if (h.total > (uint64_t)INT64_MAX || h.size != ((int64_t)h.total < C ? (int64_t)h.total : C) ||
+        h.head != (int64_t)(h.total % (uint64_t)C))
+        return fail(CONDUIT_EINVAL, "checkpoint ring state is not one that ingestion reaches");
+    const uint8_t* in = static_cast<const uint8_t*>(src);
+    for (uint32_t k = 0; k < h.n_sections && e == hipSuccess; ++k) {
+        uint8_t* base = nullptr;
+        int64_t n = 0;
+        (void)column_span(b, (conduit_column)h.section[k].column, 0, &base, &n);
+        e = hipMemcpyAsync(base, in + h.section[k].offset, (size_t)n, hipMemcpyDefault, s);
+    }
+    if (e == hipSuccess && b->opts.prioritized) e = launch_tree_rebuild(b->tree, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "checkpoint restore");
+    b->head = h.head;
+    b->size = h.size;
+    b->total = (int64_t)h.total;
     return CONDUIT_OK;
 }
 

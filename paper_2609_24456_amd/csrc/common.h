@@ -321,6 +321,8 @@ struct UpdateArgs {
 };
 
 hipError_t launch_update(const UpdateArgs& a, hipStream_t s);
+// every tree level recomputed from the leaves, level 1 first
+hipError_t launch_tree_rebuild(const TreeView& t, hipStream_t s);
 // the update, then a dense ingest, in one launch (k_update_ingest.hip)
 hipError_t launch_update_ingest(const UpdateArgs& u, const IngestArgs& a, hipStream_t s);
 

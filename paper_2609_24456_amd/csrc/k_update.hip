@@ -39,7 +39,36 @@ __global__ __launch_bounds__(kUpdateThreads) void k_update(UpdateArgs a) {
     if (lane_id() == 0 && wm > 0) atomicMax(&a.state->max_prio, wm);
 }
 
+// One tree level recomputed from the level below it (level 1 from the
+// leaves): one wavefront per node, lane j loading child 64 * node + j, the
+// wavefront's integer sum stored by lane 0.  Every level is zero-padded to a
+// multiple of 64 entries and nodes(l) = ceil(nodes(l - 1) / 64), so every
+// child index is inside the padded level.
+constexpr int kRebuildThreads = 256;
+
+__global__ __launch_bounds__(kRebuildThreads) void k_tree_level(const uint32_t* leaves, const uint64_t* below,
+                                                                uint64_t* out, int64_t nodes) {
+    const int64_t node = ((int64_t)blockIdx.x * kRebuildThreads + threadIdx.x) / kWave;
+    if (node >= nodes) return;  // whole wavefronts leave together
+    const int64_t c = node * kWave + lane_id();
+    const uint64_t x = leaves ? (uint64_t)leaves[c] : below[c];
+    const uint64_t sum = readlane_u64(wave_inclusive_scan_u64(x), kWave - 1);
+    if (lane_id() == 0) out[node] = sum;
+}
+
 }  // namespace
+
+hipError_t launch_tree_rebuild(const TreeView& t, hipStream_t s) {
+    for (int l = 1; l <= t.depth; ++l) {
+        const int64_t threads = t.nodes[l] * kWave;
+        const int64_t grid = (threads + kRebuildThreads - 1) / kRebuildThreads;
+        hipLaunchKernelGGL(k_tree_level, dim3((unsigned)grid), dim3(kRebuildThreads), 0, s, l == 1 ? t.leaves : nullptr,
+                           l == 1 ? nullptr : t.level[l - 1], t.level[l], t.nodes[l]);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
 
 hipError_t launch_update(const UpdateArgs& a, hipStream_t s) {
     if (a.n <= 0) return hipSuccess;

@@ -61,3 +61,58 @@ def tree_consistent(buf, cap):
     assert len(below) == 1
     assert int(below[0]) == int(leaves.sum(dtype=np.uint64))
     return int(below[0])
+
+
+def buffer_columns(buf):
+    """Every column of a buffer as host bytes, keyed by (column, level), with
+    the ring state under "ring"."""
+    from paper_2609_24456_amd import conduit as cd
+    info = buf.info()
+    C = info.capacity
+    cols = {(cd.COL_OBS, 0): C * info.row_bytes, (cd.COL_REWARD, 0): C * 4, (cd.COL_DONE, 0): C,
+            (cd.COL_EPISODE, 0): C * 4, (cd.COL_STEP, 0): C * 4, (cd.COL_MAX_PRIO, 0): 4}
+    if info.action_bytes:
+        cols[(cd.COL_ACTION, 0)] = C * info.action_bytes
+    if info.ragged:
+        cols[(cd.COL_LENGTH, 0)] = C * 4
+        if info.aux_elem_bytes:
+            cols[(cd.COL_AUX, 0)] = C * info.max_len * info.aux_elem_bytes
+    if info.prioritized:
+        cols[(cd.COL_LEAVES, 0)] = C * 4
+        for level in range(1, info.tree_depth + 1):
+            cols[(cd.COL_TREE, level)] = info.tree_nodes[level] * 8
+    out = {k: read_col(buf, k[0], n, np.uint8, level=k[1]) for k, n in cols.items()}
+    out["ring"] = (info.head, info.size, info.total)
+    return out
+
+
+def image_tensor(buf, via):
+    """A tensor to hold the buffer's checkpoint image: in HBM, pinned or pageable host memory."""
+    from paper_2609_24456_amd import conduit as cd
+    n = cd.conduit_buffer_checkpoint_bytes(buf.handle)
+    if via == "device":
+        return torch.empty(n, dtype=torch.uint8, device="cuda")
+    return torch.empty(n, dtype=torch.uint8, pin_memory=(via == "pinned"))
+
+
+def swap_through_checkpoint(buf, via, make, tmp_dir=None):
+    """Checkpoint `buf` (into HBM, pinned or pageable host memory, or a file),
+    restore the image into a new buffer from make(), check that every column,
+    tree level and the ring state came across, close `buf` and return the new
+    buffer."""
+    import os
+    before = buffer_columns(buf)
+    fresh = make()
+    if via == "file":
+        path = os.path.join(tmp_dir, "replay.ckpt")
+        buf.save(path)
+        fresh.load(path)
+    else:
+        img = buf.checkpoint(dst=image_tensor(buf, via))
+        fresh.restore(img)
+    after = buffer_columns(fresh)
+    assert before.keys() == after.keys()
+    for k in before:
+        assert np.array_equal(before[k], after[k]), k
+    buf.close()
+    return fresh

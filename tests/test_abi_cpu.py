@@ -100,6 +100,9 @@ def test_null_arguments_rejected():
     assert L.conduit_buffer_get_info(None, None) == cd.EINVAL
     assert L.conduit_buffer_read(None, 0, 0, 0, 0, None, None) == cd.EINVAL
     assert L.conduit_buffer_stats(None, None, None, None) == cd.EINVAL
+    assert L.conduit_buffer_checkpoint_bytes(None, None) == cd.EINVAL
+    assert L.conduit_buffer_checkpoint(None, None, 0, None) == cd.EINVAL
+    assert L.conduit_buffer_restore(None, None, 0, None) == cd.EINVAL
     L.conduit_buffer_destroy(None)  # no-op
 
 
@@ -142,7 +145,8 @@ def test_struct_layouts_match_header(tmp_path):
                "conduit_transform": cd.Transform, "conduit_learner_batch": cd.LearnerBatch,
                "conduit_buffer_info": cd.BufferInfo, "conduit_sched_costs": cd.SchedCosts,
                "conduit_sched_mode": cd.SchedMode, "conduit_offpolicy_loop": cd.OffpolicyLoop,
-               "conduit_onpolicy_loop": cd.OnpolicyLoop, "conduit_place_profile": cd.PlaceProfile}
+               "conduit_onpolicy_loop": cd.OnpolicyLoop, "conduit_place_profile": cd.PlaceProfile,
+               "conduit_ckpt_section": cd.CkptSection, "conduit_ckpt_header": cd.CkptHeader}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "conduit.h"', "int main(void) {"]
     for cname, py in structs.items():
         lines.append(f'printf("{cname} %zu\\n", sizeof({cname}));')

@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import synth
-from gpu_util import assert_weights_close, dev, host, read_col, tree_consistent
+from gpu_util import assert_weights_close, dev, host, read_col, swap_through_checkpoint, tree_consistent
 
 pytestmark = pytest.mark.gpu
 
@@ -206,12 +206,16 @@ def test_nstep_rows_of_many_items(n):
 
 
 def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH,
-              nstep=None, update_ingest=False, fused_nstep=None, derive_meta=False):
+              nstep=None, update_ingest=False, fused_nstep=None, derive_meta=False, resume=None):
+    """resume = (iteration, via, placement, tmp_dir): before that iteration the
+    buffer is checkpointed (into HBM, pinned or pageable host memory, or a
+    file), restored into a new buffer with the given payload placement, and the
+    run goes on with the new buffer against the same, uninterrupted oracle."""
     cfg = synth.Tiny(n=prefill + synth.Tiny.ingest_n * iters, seed=synth.data_seed(0) + seed_shift)
     u, prio = cfg.draws(iters=iters)
     C, n_in, B = cfg.capacity, cfg.ingest_n, cfg.batch
-    buf = _mk(C, (8,), torch.float32, action_bytes=4, placement=placement, weight_norm=weight_norm,
-              single_stream=derive_meta)
+    mk_kw = dict(action_bytes=4, placement=placement, weight_norm=weight_norm, single_stream=derive_meta)
+    buf = _mk(C, (8,), torch.float32, **mk_kw)
     orc = oracle.Replay(C, (8,), np.float32, act_bytes=4, buffer_norm=weight_norm == cd.WNORM_BUFFER,
                         single_stream=derive_meta)
 
@@ -239,6 +243,14 @@ def _run_tiny(prefill, iters, seed_shift=0, fused=False, placement=cd.PLACE_HBM,
     xf = cd.transform(cd.XF_NONE)
     pending = None
     for it in range(iters):
+        if resume is not None and it == resume[0]:
+            if pending is not None:  # the pending update goes in before the checkpoint
+                buf.update(pending[0], dev(pending[1]))
+                orc.update(pending[2], pending[1])
+                pending = None
+            buf = swap_through_checkpoint(buf, resume[1], lambda: _mk(C, (8,), torch.float32,
+                                                                       **{**mk_kw, "placement": resume[2]}),
+                                          resume[3])
         ingest(pos, pos + n_in, pending)
         pending = None
         pos += n_in
@@ -374,12 +386,14 @@ def test_tiny_config_payload_in_pinned_host_memory(fused):
 # ----------------------------------------------------------------------------
 def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=None, fused=False,
             placement=cd.PLACE_HBM, weight_norm=cd.WNORM_BATCH, nstep=None, update_ingest=False, fused_nstep=None,
-            derive_meta=False):
+            derive_meta=False, resume=None):
     """Drive GPU buffer and oracle through the same DQN stream; the oracle keeps
     metadata only and its observation rows are regenerated for the slots a
     gather reads.  fused_nstep = (n, gamma): every delivery goes through
     conduit_sample_gather_nstep (batch, targets and bootstrap stacks in one
-    call), checked against the oracle and, bit for bit, against conduit_nstep."""
+    call), checked against the oracle and, bit for bit, against conduit_nstep.
+    resume = (iteration, via, placement, tmp_dir): the buffer goes through a
+    checkpoint and a restore into a new buffer before that iteration."""
     n_total = prefill + iters * batch
     cfg = synth.DQN(n_total)
     if short_episodes:  # many episode starts: exercises the zero fill
@@ -390,8 +404,9 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
         cfg.drift = rng.integers(1, 4, int(cfg.episode.max()) + 1).astype(np.int64)
     u, prio = cfg.draws(iters, batch)
     K = 4
-    buf = _mk(cap, (84, 84), torch.uint8, frame_stack=K, action_bytes=4, placement=placement,
-              weight_norm=weight_norm, single_stream=derive_meta)
+    mk_kw = dict(frame_stack=K, action_bytes=4, placement=placement, weight_norm=weight_norm,
+                 single_stream=derive_meta)
+    buf = _mk(cap, (84, 84), torch.uint8, **mk_kw)
     obs_store = np.zeros((cap, 84 * 84), np.uint8)  # untouched pages stay unallocated
     orc = oracle.Replay(cap, (84, 84), np.uint8, act_bytes=4, frame_stack=K, obs_storage=obs_store,
                         buffer_norm=weight_norm == cd.WNORM_BUFFER, single_stream=derive_meta)
@@ -420,6 +435,13 @@ def run_dqn(cap, prefill, iters, batch, chunk, short_episodes=False, check_rows=
     xf = cd.transform(cd.XF_U8_F32)
     pending = None
     for it in range(iters):
+        if resume is not None and it == resume[0]:
+            if pending is not None:  # the pending update goes in before the checkpoint
+                buf.update(pending[0], pending[1])
+                pending = None
+            buf = swap_through_checkpoint(buf, resume[1], lambda: _mk(cap, (84, 84), torch.uint8,
+                                                                       **{**mk_kw, "placement": resume[2]}),
+                                          resume[3])
         ingest(pos, pos + batch, with_prio=False, pending=pending)
         pending = None
         pos += batch
