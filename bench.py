@@ -381,6 +381,10 @@ def bench_dqn(steps, warmup):
     deliver_nstep_two_ms = _b2b_ms(two_calls)
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
+    # references for the batch's read/write mix over B x K frames laid out
+    # contiguously (no sampling, no gather): the library's streaming expand
+    # (conduit_expand_reference) and torch's elementwise u8 -> fp32 scale
+    ref_bytes, ref_ms, torch_ms = _expand_references(B * K * row, next_out.view(-1), steps, stream)
     return {
         "nstep3": {"us": nstep_ms * 1e3, "n": n_step, "gamma": gam, "valid_in_last_batch": boot,
                    "call": "conduit_nstep: targets plus the bootstrap frame stacks [512,4,84,84] fp32"},
@@ -395,12 +399,39 @@ def bench_dqn(steps, warmup):
         "ingest_big": {"frames": 32768, "ms": ingest_big_ms,
                        "GBps": 32768 * ingest_bytes_per_frame / ingest_big_ms / 1e6},
         "ingest_bytes_per_frame": ingest_bytes_per_frame,
+        "expand_reference": _expand_record(ref_bytes, ref_ms, torch_ms, "the batch's 512 x 4 frames"),
     }
 
 
 # ----------------------------------------------------------------------------
 # other rows
 # ----------------------------------------------------------------------------
+def _expand_references(n, out_f32, calls, stream):
+    """(bytes, ms, torch ms) of u8 -> fp32 over n contiguous bytes into
+    out_f32: conduit_expand_reference (a streaming kernel with the gathers'
+    1:4 read/write mix and none of their indexing) and torch.mul(u8, 1/255)."""
+    import torch
+    from paper_2609_24456_amd import conduit as cd
+    L = cd.lib()
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = out_f32[:n]
+    ref = lambda: L.conduit_expand_reference(src.data_ptr(), dst.data_ptr(), n, stream)  # noqa: E731
+    tch = lambda: torch.mul(src, 1.0 / 255.0, out=dst) is None  # noqa: E731  (a status of 0)
+    _b2b_ms([ref] * 3)
+    ref_ms = _b2b_ms([ref] * calls)
+    _b2b_ms([tch] * 3)
+    torch_ms = _b2b_ms([tch] * calls)
+    return 5 * n, ref_ms, torch_ms
+
+
+def _expand_record(nbytes, ref_ms, torch_ms, what):
+    return {"bytes": nbytes, "us": ref_ms * 1e3, "GBps": nbytes / ref_ms / 1e6,
+            "frac": nbytes / ref_ms / 1e6 / PEAK_HBM_GBPS,
+            "torch_us": torch_ms * 1e3, "torch_frac": nbytes / torch_ms / 1e6 / PEAK_HBM_GBPS,
+            "what": "u8 -> fp32 /255 over " + what + " laid out contiguously (the same 1:4 read/write mix, no "
+                    "indexing): conduit_expand_reference, and torch.mul(u8, 1/255, out=fp32) beside it"}
+
+
 def bench_ppo(reps=3):
     """PPO rollout [2048 x 256] of 3x84x84 u8: rollout ingest (32 calls of 64
     steps), GAE over [T, E], and the 32 minibatch gathers of one epoch; each
@@ -460,6 +491,9 @@ def bench_ppo(reps=3):
     assert cd.conduit_sync_check() == cd.OK, cd.last_error()
     mb_bytes = mb * (row + row * 4 + 8 + 2 * 4 + 2 * 4)
     ing_bytes = N * (2 * row + 2 * (4 + 1) + 2 * (4 + 4))
+    # references for the read/write mix over the same bytes laid out
+    # contiguously (no index, no scattered rows)
+    ex_bytes, ex_ms, ex_torch_ms = _expand_references(mb * row, out.view(-1), 10, stream)
     return {
         "rollout_ingest": {"bytes": ing_bytes, "ms": ing_ms, "GBps": ing_bytes / ing_ms / 1e6,
                            "frac": ing_bytes / ing_ms / 1e6 / PEAK_HBM_GBPS},
@@ -469,6 +503,8 @@ def bench_ppo(reps=3):
         "minibatch_gather_16384": {"bytes": mb_bytes, "us": mb_ms * 1e3, "GBps": mb_bytes / mb_ms / 1e6,
                                    "frac": mb_bytes / mb_ms / 1e6 / PEAK_HBM_GBPS},
         "epoch_32_minibatches_ms": mb_ms * 32,
+        "expand_reference": _expand_record(ex_bytes, ex_ms, ex_torch_ms, "one minibatch's 16,384 frames"),
+        "minibatch_over_expand_reference": (mb_bytes / mb_ms) / (ex_bytes / ex_ms),
         "timing": "back-to-back launches between two events, arguments prepared up front",
     }
 
@@ -1408,7 +1444,9 @@ def _row_summary(name, r):
         if name == "ppo":
             return {"rollout_ingest_frac": r["rollout_ingest"]["frac"], "gae_us": r["gae_2048x256"]["us"],
                     "minibatch_us": r["minibatch_gather_16384"]["us"],
-                    "minibatch_frac": r["minibatch_gather_16384"]["frac"]}
+                    "minibatch_frac": r["minibatch_gather_16384"]["frac"],
+                    "expand_reference_frac": r["expand_reference"]["frac"],
+                    "torch_expand_frac": r["expand_reference"]["torch_frac"]}
         if name == "large":
             return {"gather_bf16_us": r["gather_bf16_1024"]["us"], "gather_bf16_frac": r["gather_bf16_1024"]["frac"],
                     "iteration_us": r["iteration_us"]}
@@ -1496,6 +1534,8 @@ def main():
         "gather_GBps": g_gbps,
         "gather_frac_of_peak": g_gbps / PEAK_HBM_GBPS,
         "gather_avg_launch_us": g_ms * 1e3,
+        "expand_reference_frac": d["expand_reference"]["frac"],
+        "torch_expand_frac": d["expand_reference"]["torch_frac"],
         "ms_per_step_separate_update": d["separate_ms"] / args.steps,
         "ms_per_step_unfused": d["unfused_ms"] / args.steps,
         "kernels_us_in_step": {k.split(" ")[0]: round(v["mean_us"], 3) for k, v in d["kernels"].items()},

@@ -847,6 +847,20 @@ conduit_status conduit_sched_candidates(int32_t on_policy, int32_t minibatches, 
 conduit_status conduit_standin(int64_t work, void* stream);
 
 /*
+ * Measurement reference, not a step of the path: dst[i] = src[i] / 255
+ * (correctly rounded fp32) for i < n over contiguous memory, in one streaming
+ * launch with coalesced 256-byte loads and 1 KB non-temporal stores.  It moves
+ * the byte mix of the u8 -> fp32 gathers (one byte read, four written per
+ * element; Sec. 2.2 delivery's batch/layout transformation) without their
+ * indexing, so its rate at a gather's size is the practical ceiling that
+ * gather's fraction of the HBM peak is read against.  src: device, n bytes,
+ * 4-byte aligned; dst: device, 4n bytes, 16-byte aligned, not overlapping src.
+ * Errors: EINVAL (n < 0 or not a multiple of 4, NULL or misaligned pointers,
+ * overlap), EDEVICE.
+ */
+conduit_status conduit_expand_reference(const uint8_t* src, float* dst, int64_t n, void* stream);
+
+/*
  * Profiles the synchronisation cost of overlap (Sec. 6.2 T_sync) between two
  * streams of one GPU, in microseconds per dependency (each >= 0):
  *   *hop_us: a dependency the waiting stream reaches before it is met --

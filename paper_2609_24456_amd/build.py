@@ -10,7 +10,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libconduit.so")
 SOURCES = ["api.hip", "k_ingest.hip", "k_update.hip", "k_sample.hip", "k_gather.hip", "k_sample_gather.hip",
-           "k_gae.hip", "sched.hip", "loop.hip", "place.hip", "k_nstep.hip", "k_update_ingest.hip"]
+           "k_gae.hip", "sched.hip", "loop.hip", "place.hip", "k_nstep.hip", "k_update_ingest.hip",
+           "k_reference.hip"]
 ARCH = os.environ.get("CONDUIT_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",

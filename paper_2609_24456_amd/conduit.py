@@ -168,6 +168,7 @@ SIGNATURES = {
     "conduit_version": (C.c_char_p, []),
     "conduit_schedule": (ST, [P, P, P]),
     "conduit_standin": (ST, [I64, P]),
+    "conduit_expand_reference": (ST, [P, P, I64, P]),
     "conduit_sync_cost_us": (ST, [P, P, I32_, P, P]),
     "conduit_sched_candidates": (ST, [I32_, I32_, I32_, I32_, P, I32_, P, P, I32_, P]),
     "conduit_run_onpolicy": (ST, [P, P, P, P, P, P, P]),
@@ -564,6 +565,13 @@ def conduit_place(profile, actor_on_gpu, capacity, sample_bytes, candidates=(0, 
 
 def conduit_standin(work, stream=None):
     _check(lib().conduit_standin(int(work), _stream(stream)))
+
+
+def conduit_expand_reference(src, dst, stream=None):
+    """dst = src / 255 over contiguous memory (the gathers' read/write mix without their indexing)."""
+    n = src.numel()
+    _check(lib().conduit_expand_reference(_ptr(src, torch.uint8, "src"),
+                                          _ptr(dst, torch.float32, "dst", numel=n), n, _stream(stream)))
 
 
 def conduit_sync_cost_us(s1, s2, hops=200):

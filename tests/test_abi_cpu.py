@@ -212,3 +212,16 @@ def test_single_stream_option():
     assert cd.lib().conduit_buffer_required_bytes(16, shape, 1, cd.F32, C.byref(o)) == 0
     o.single_stream = 1
     assert cd.lib().conduit_buffer_required_bytes(16, shape, 1, cd.F32, C.byref(o)) > 0
+
+
+def test_expand_reference_validates_on_host():
+    L = cd.lib()
+    P, Q = C.c_void_p(1 << 20), C.c_void_p(16 << 20)  # never dereferenced: validation fails first
+    assert L.conduit_expand_reference(None, None, 0, None) == cd.OK  # empty
+    assert L.conduit_expand_reference(P, Q, -4, None) == cd.EINVAL
+    assert L.conduit_expand_reference(P, Q, 6, None) == cd.EINVAL
+    assert L.conduit_expand_reference(None, Q, 8, None) == cd.EINVAL
+    assert L.conduit_expand_reference(P, C.c_void_p(Q.value + 4), 8, None) == cd.EINVAL  # dst not 16-byte aligned
+    assert L.conduit_expand_reference(C.c_void_p(P.value + 2), Q, 8, None) == cd.EINVAL  # src not 4-byte aligned
+    assert L.conduit_expand_reference(P, C.c_void_p(P.value + 16), 64, None) == cd.EINVAL
+    assert "overlap" in cd.last_error()
