@@ -380,6 +380,7 @@ def bench_dqn(steps, warmup):
     deliver_nstep_one_ms = _b2b_ms(one_calls)
     deliver_nstep_two_ms = _b2b_ms(two_calls)
     assert buf.sync_check() == cd.OK, cd.last_error()
+    ckpt = _checkpoint_times(buf)
     buf.close()
     # references for the batch's read/write mix over B x K frames laid out
     # contiguously (no sampling, no gather): the library's streaming expand
@@ -400,12 +401,42 @@ def bench_dqn(steps, warmup):
                        "GBps": 32768 * ingest_bytes_per_frame / ingest_big_ms / 1e6},
         "ingest_bytes_per_frame": ingest_bytes_per_frame,
         "expand_reference": _expand_record(ref_bytes, ref_ms, torch_ms, "the batch's 512 x 4 frames"),
+        "checkpoint": ckpt,
     }
 
 
 # ----------------------------------------------------------------------------
 # other rows
 # ----------------------------------------------------------------------------
+def _checkpoint_times(buf):
+    """Wall time of a checkpoint of the whole buffer into HBM and into pinned
+    host memory, and of restoring it from HBM (the copies plus the tree
+    rebuild); each call waits for its own copies.  The image is restored into
+    the buffer it came from, so the state does not change."""
+    import torch
+    from paper_2609_24456_amd import conduit as cd
+    n = cd.conduit_buffer_checkpoint_bytes(buf.handle)
+    out = {"image_bytes": n}
+    img = torch.empty(n, dtype=torch.uint8, device="cuda")
+    for name, fn in (("checkpoint_hbm", lambda: buf.checkpoint(dst=img)), ("restore_hbm", lambda: buf.restore(img))):
+        fn()  # first call: page-in, code load
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn()
+        dt = time.perf_counter() - t0
+        out[name] = {"ms": dt * 1e3, "GBps": n / dt / 1e9}
+    del img
+    host = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    buf.checkpoint(dst=host)
+    t0 = time.perf_counter()
+    buf.checkpoint(dst=host)
+    dt = time.perf_counter() - t0
+    out["checkpoint_pinned_host"] = {"ms": dt * 1e3, "GBps": n / dt / 1e9}
+    del host
+    assert buf.sync_check() == cd.OK, cd.last_error()
+    return out
+
+
 def _expand_references(n, out_f32, calls, stream):
     """(bytes, ms, torch ms) of u8 -> fp32 over n contiguous bytes into
     out_f32: conduit_expand_reference (a streaming kernel with the gathers'
@@ -1376,9 +1407,8 @@ def cpu_baseline(rep_seconds=2.0, reps=5, all_core_seconds=3.0, max_workers=16):
     gc.collect()
     return {
         "value": value, "unit": "sampled transitions/s", "cores": 1, "kind": "oracle",
-        "sample": f"median of {reps} reps x {one['steps_per_rep']} DQN steps (ingest 512 + sample 512 + gather "
-                  f"512 -> [512,4,84,84] fp32 + update 512) on the 1M-slot replay (1.05M prefill), after a "
-                  f"{probe_steps}-step warm-up; single-threaded C oracle pinned to core {cores[0]}",
+        "sample": f"median of {reps} reps x {one['steps_per_rep']} DQN steps (the same step) on the 1M-slot "
+                  f"replay (1.05M prefill) after {probe_steps} warm-up steps; one-thread C oracle on core {cores[0]}",
         "rep_s": one["rep_s"], "steps_per_rep": one["steps_per_rep"],
         "all_cores": {"value": value_all, "cores": len(workers), "steps_per_worker": n_all,
                       "worker_s_max": max(t_all),
@@ -1530,7 +1560,7 @@ def main():
                      "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBPS,
                      "traffic": _traffic_from_profile(),
                      "algorithmic_bytes": d["fused_bytes"], "avg_launch_us": f_ms * 1e3,
-                     "timing": "HIP events, back-to-back launches over the timed steps' uniforms"},
+                     "timing": "HIP events around back-to-back launches"},
         "gather_GBps": g_gbps,
         "gather_frac_of_peak": g_gbps / PEAK_HBM_GBPS,
         "gather_avg_launch_us": g_ms * 1e3,
@@ -1542,7 +1572,9 @@ def main():
         "rows": {"dqn_ingest_32768_frac": d["ingest_big"]["GBps"] / PEAK_HBM_GBPS,
                  "dqn_nstep3_us": d["nstep3"]["us"],
                  "dqn_deliver_nstep3_us": {"one_call": d["deliver_nstep3"]["one_call_us"],
-                                           "two_calls": d["deliver_nstep3"]["two_calls_us"]}},
+                                           "two_calls": d["deliver_nstep3"]["two_calls_us"]},
+                 "dqn_checkpoint_GBps": {k: round(v["GBps"], 1) for k, v in d["checkpoint"].items()
+                                         if isinstance(v, dict)}},
     }
     if not args.no_rows:
         only = set(x for x in args.only.split(",") if x) or set(ROWS)
