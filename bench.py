@@ -659,6 +659,11 @@ def bench_tokens(iters=10):
     mean_len = float(length.float().mean())
     pack_ms = _b2b_ms([lambda i=i: L.conduit_gather_transform(h, pi[i], B, xfr, lbr, stream) for i in range(iters)])
     gae_ms = _b2b_ms([gae] * iters)
+    # the two delivery launches alone: sampler + pack, and sampler + pack + GAE
+    sp_ms = _b2b_ms([lambda i=i: L.conduit_sample_gather(h, B, pu[i], pi[i], pw[i], xfr, lbr, stream)
+                     for i in range(iters)])
+    spg_ms = _b2b_ms([lambda i=i: spg(h, B, pu[i], pi[i], pw[i], xfr, lbr, None, cfg.gamma, cfg.lam, adv.data_ptr(),
+                                      ret.data_ptr(), stream) for i in range(iters)])
     assert buf.sync_check() == cd.OK, cd.last_error()
     buf.close()
     pbytes = int(B * mean_len * 8 + B * Lmax * (4 + 1 + 4) + B * (8 + 4 + 4 + 4 + 4))
@@ -670,6 +675,8 @@ def bench_tokens(iters=10):
                                 "frac": gbytes / gae_ms / 1e6 / PEAK_HBM_GBPS},
         "iteration_us": iter_ms * 1e3,
         "iteration_one_launch_gae_us": iter_one_ms * 1e3,
+        "sample_pack_us": sp_ms * 1e3,
+        "sample_pack_gae_us": spg_ms * 1e3,
         "timing": "back-to-back launches between two events, arguments prepared up front",
     }
 

@@ -1,6 +1,6 @@
 // Generalised advantage estimation over packed (right-padded) sequences, one
-// workgroup of 256 lanes per sequence: shared by the packed GAE kernel and the
-// fused sampler + packing + GAE kernel.
+// workgroup per sequence: shared by the packed GAE kernel (512 lanes) and the
+// fused sampler + packing + GAE kernel (its pack workgroup as it is).
 #pragma once
 #include "common.h"
 
@@ -12,13 +12,16 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kRsrcRaw32 = 0x00020000;  // raw buffer descriptor, 32-bit data format
 constexpr int kAgentScopeStore = 16;    // cache policy SC1: written through at agent scope
 
-constexpr int kPkThreads = 256;
-constexpr int kPkChunk = 16;                      // elements per lane and segment
-constexpr int kPkSeg = kPkThreads * kPkChunk;     // 4096 elements per pass
+// Lanes of the stand-alone packed GAE kernel.  A sequence of 4,096 elements
+// as 512 lanes x 8 (against 256 x 16): [256, 4096] 6.9 -> 5.5 us, [1024, 4096]
+// 13.2 -> 11.8 us, [256, 1024] 6.0 -> 4.7 us; 1,024 lanes x 4 gains at 256
+// rows (5.9 us) but loses at 1,024 (18.7 us).
+constexpr int kPkThreads = 512;
+constexpr int kPkSeg = 4096;                      // elements per pass
 constexpr int kPkPad = kPkSeg + kPkSeg / 16 + 1;  // padded LDS row
 
 // padded LDS index: one spare word every 16, so lanes reading their own
-// contiguous chunk of 16 hit distinct banks
+// contiguous chunk of up to 16 hit distinct banks
 __device__ __forceinline__ int lpad(int t) { return t + (t >> 4); }
 
 // GAE over right-padded sequences, one workgroup per sequence, walked in
@@ -49,13 +52,17 @@ __device__ __forceinline__ void later_scan_step(double& P, double& S) {
 constexpr int kDppWaveShr1 = 0x138;  // lane i reads lane i - 1 across the whole wavefront
 
 // GAE of packed row b, of L live elements (0 <= L <= Lmax) with reward R on
-// the last one, by one workgroup of kPkThreads lanes.
+// the last one, by one workgroup of NT lanes (each lane a chunk of 4096 / NT
+// consecutive elements per pass).
+template <int NT>
 __device__ void gae_packed_row(const GaePackedArgs& a, int64_t b, int64_t L, double R) {
+    static_assert(NT % kWave == 0 && kPkSeg % (4 * NT) == 0 && kPkSeg / NT <= 16, "lanes per sequence");
+    constexpr int kPkChunk = kPkSeg / NT;  // elements per lane and pass
     __shared__ float sV[kPkPad];
     __shared__ float sA[kPkPad];
     __shared__ float sR[kPkPad];
-    __shared__ double sWP[kPkThreads / kWave];
-    __shared__ double sWS[kPkThreads / kWave];
+    __shared__ double sWP[NT / kWave];
+    __shared__ double sWS[NT / kWave];
     const int tid = threadIdx.x;
     // chunks run backwards inside a wavefront (lane 0 holds its last chunk), so
     // the suffix composition over the chunks is a prefix scan over the lanes
@@ -79,11 +86,11 @@ __device__ void gae_packed_row(const GaePackedArgs& a, int64_t b, int64_t L, dou
         const int seg_len = (int)(Lmax - base < kPkSeg ? Lmax - base : kPkSeg);
         if (vec_in) {
             // every lane's 4 vectors are loaded before the first LDS write
-            constexpr int kVecs = kPkSeg / (4 * kPkThreads);
+            constexpr int kVecs = kPkSeg / (4 * NT);
             f32x4 q[kVecs];
 #pragma unroll
             for (int j = 0; j < kVecs; ++j) {
-                const int t = (j * kPkThreads + tid) * 4;
+                const int t = (j * NT + tid) * 4;
                 if (t + 3 < seg_len) {
                     q[j] = *reinterpret_cast<const f32x4*>(val + base + t);
                 } else {
@@ -93,13 +100,13 @@ __device__ void gae_packed_row(const GaePackedArgs& a, int64_t b, int64_t L, dou
             }
 #pragma unroll
             for (int j = 0; j < kVecs; ++j) {
-                const int t = (j * kPkThreads + tid) * 4;
+                const int t = (j * NT + tid) * 4;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     if (t + i < seg_len) sV[lpad(t + i)] = q[j][i];
             }
         } else {
-            for (int t = tid; t < seg_len; t += kPkThreads) sV[lpad(t)] = val ? val[base + t] : 0.0f;
+            for (int t = tid; t < seg_len; t += NT) sV[lpad(t)] = val ? val[base + t] : 0.0f;
         }
         __syncthreads();
         // this lane's chunk [t0, t1) of the segment, live part [t0, u1)
@@ -147,7 +154,7 @@ __device__ void gae_packed_row(const GaePackedArgs& a, int64_t b, int64_t L, dou
         double lP = 1.0, lS = 0.0;  // the later wavefronts' chunks
         double tP = 1.0, tS = 0.0;  // the whole segment
 #pragma unroll
-        for (int w = kPkThreads / kWave - 1; w >= 0; --w) {
+        for (int w = NT / kWave - 1; w >= 0; --w) {
             tS = sWS[w] + sWP[w] * tS;
             tP = sWP[w] * tP;
             if (w == wv + 1) {
@@ -180,7 +187,7 @@ __device__ void gae_packed_row(const GaePackedArgs& a, int64_t b, int64_t L, dou
         }
         __syncthreads();
         if (vec_out) {
-            constexpr int kVecs = kPkSeg / (4 * kPkThreads);
+            constexpr int kVecs = kPkSeg / (4 * NT);
             // write-through buffer stores at agent scope over this segment (the
             // rows leave no dirty lines for the end-of-kernel write-back: 7.95
             // -> 7.26 us for [256, 4096], the tokens iteration 22.7 -> 22.0 us)
@@ -189,7 +196,7 @@ __device__ void gae_packed_row(const GaePackedArgs& a, int64_t b, int64_t L, dou
             const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(ret + base, 0, nb, kRsrcRaw32);
 #pragma unroll
             for (int j = 0; j < kVecs; ++j) {
-                const int t = (j * kPkThreads + tid) * 4;
+                const int t = (j * NT + tid) * 4;
                 if (t + 3 < seg_len) {
                     f32x4 oa, orr;
 #pragma unroll
@@ -207,7 +214,7 @@ __device__ void gae_packed_row(const GaePackedArgs& a, int64_t b, int64_t L, dou
                 }
             }
         } else {
-            for (int t = tid; t < seg_len; t += kPkThreads) {
+            for (int t = tid; t < seg_len; t += NT) {
                 adv[base + t] = sA[lpad(t)];
                 ret[base + t] = sR[lpad(t)];
             }

@@ -627,6 +627,7 @@ struct PackedRow {
     float R;
 };
 
+template <int NT>
 __device__ PackedRow pack_row(const PackArgs& a, int64_t b, int64_t i) {
     const bool ok = i >= 0 && i < a.size;
     if (!ok && threadIdx.x == 0) flag_error(a.err, ERR_GATHER_INDEX);
@@ -642,13 +643,13 @@ __device__ PackedRow pack_row(const PackArgs& a, int64_t b, int64_t i) {
     const int32_t* __restrict__ seq = reinterpret_cast<const int32_t*>(a.seq) + (ok ? i : 0) * a.max_len;
     const float* __restrict__ aux = a.aux ? reinterpret_cast<const float*>(a.aux) + (ok ? i : 0) * a.max_len : nullptr;
     const int64_t quads = a.max_len >> 2;
-    for (int64_t q0 = threadIdx.x; q0 < quads; q0 += kThreads * kPackQuads) {
+    for (int64_t q0 = threadIdx.x; q0 < quads; q0 += NT * kPackQuads) {
         int4 tok[kPackQuads];
         f32x4 lp[kPackQuads];
         uint32_t m[kPackQuads];
 #pragma unroll
         for (int r = 0; r < kPackQuads; ++r) {
-            const int64_t q = q0 + (int64_t)r * kThreads;
+            const int64_t q = q0 + (int64_t)r * NT;
             const int64_t t = q * 4;
             if (q < quads && t + 3 < L) {
                 tok[r] = *reinterpret_cast<const int4*>(seq + t);
@@ -669,7 +670,7 @@ __device__ PackedRow pack_row(const PackArgs& a, int64_t b, int64_t i) {
         }
 #pragma unroll
         for (int r = 0; r < kPackQuads; ++r) {
-            const int64_t q = q0 + (int64_t)r * kThreads;
+            const int64_t q = q0 + (int64_t)r * NT;
             if (q >= quads) continue;
             const int64_t o = b * a.max_len + q * 4;
             *reinterpret_cast<int4*>(reinterpret_cast<int32_t*>(a.out_seq) + o) = tok[r];
@@ -684,7 +685,7 @@ __device__ PackedRow pack_row(const PackArgs& a, int64_t b, int64_t i) {
     }
     if (act) a.out_action[b * a.action_bytes + threadIdx.x] = ok ? ab : (uint8_t)0;
     if (a.out_action) {  // actions longer than one byte per lane
-        for (int c = (int)threadIdx.x + kThreads; c < a.action_bytes; c += kThreads)
+        for (int c = (int)threadIdx.x + NT; c < a.action_bytes; c += NT)
             a.out_action[b * a.action_bytes + c] = ok ? a.action[si * a.action_bytes + c] : (uint8_t)0;
     }
     return PackedRow{L, ok ? rew : 0.0f};

@@ -23,7 +23,7 @@
 //     (any E, any alignment) one environment and 32 steps (64 chunks per
 //     pass), lanes fastest over environments so every load instruction reads
 //     eight 32-byte runs.
-// Padded sequences [B, Lmax] (k_gae_packed): one workgroup per sequence, 256
+// Padded sequences [B, Lmax] (k_gae_packed): one workgroup per sequence, 512
 // chunks along t, scanned with DPP inside each wavefront.
 #include <atomic>
 
@@ -1077,7 +1077,7 @@ __global__ __launch_bounds__(kPkThreads) void k_gae_packed(GaePackedArgs a) {
         if (threadIdx.x == 0) flag_error(a.err, ERR_SEQ_LENGTH);
         L = L < 0 ? 0 : a.Lmax;
     }
-    gae_packed_row(a, b, L, (double)a.last_reward[b]);
+    gae_packed_row<kPkThreads>(a, b, L, (double)a.last_reward[b]);
 }
 
 __global__ void k_fill_u32(uint32_t* p, uint32_t v, int64_t n) {

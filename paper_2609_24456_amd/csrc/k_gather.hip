@@ -117,7 +117,7 @@ __global__ __launch_bounds__(kThreads) void k_pack(PackArgs a) {
         is_weights_block<kThreads>(a.weights);
         return;
     }
-    pack_row(a, b, a.idx[b]);
+    pack_row<kThreads>(a, b, a.idx[b]);
 }
 
 }  // namespace

@@ -205,24 +205,30 @@ hipError_t launch_nstep_xf(const SampleArgs& sa, const GatherArgs& ga, const Nst
 }
 
 // Sampler + token packing in one launch (ragged buffers): one pack workgroup
-// of 256 lanes per sample at the head of the grid, whose first wavefront
-// descends for the sample before the workgroup packs the row (pack_row), and
-// sampler workgroups of 256 lanes (four samples each) at the tail for the
-// indices and the importance weights, as in k_sample_gather.
-constexpr int kPackWg = kThreads;
-
+// per sample at the head of the grid, whose first wavefront descends for the
+// sample before the workgroup packs the row (pack_row), and sampler workgroups
+// of the same width (one sample per wavefront) at the tail for the indices and
+// the importance weights, as in k_sample_gather.
+//
 // With GAE, each pack workgroup then runs the GAE of its packed row from the
 // length and reward it has just written (gae_packed_row), as
 // conduit_gae_packed would over the packed batch.
-static_assert(kPackWg == kPkThreads, "the packed GAE takes the pack workgroup as it is");
+//
+// Widths, measured on [256, 4096] token batches: the pack alone takes 256
+// lanes (7.4 us; 7.8-8.3 us with 512), the pack + GAE 512 lanes (10.3 us
+// against 12.1 us with 256: the row's recursion is 8 steps per lane instead
+// of 16).
+template <bool GAE>
+constexpr int pack_wg() { return GAE ? 512 : kThreads; }
 
 template <int PRE, int DEPTH, bool GAE>
-__global__ __launch_bounds__(kPackWg) void k_sample_pack(SampleArgs sa, PackArgs pa, GaePackedArgs ga, DivB dv,
-                                                         int32_t sampler_wgs) {
+__global__ __launch_bounds__(pack_wg<GAE>()) void k_sample_pack(SampleArgs sa, PackArgs pa, GaePackedArgs ga,
+                                                                DivB dv, int32_t sampler_wgs) {
+    constexpr int NT = pack_wg<GAE>();
     __shared__ int64_t s_slot;
     const int64_t pack_wgs = (int64_t)gridDim.x - sampler_wgs;
     if ((int64_t)blockIdx.x >= pack_wgs) {
-        sampler_wg<kPackWg, PRE, DEPTH>(sa, dv, (int64_t)blockIdx.x - pack_wgs);
+        sampler_wg<NT, PRE, DEPTH>(sa, dv, (int64_t)blockIdx.x - pack_wgs);
         return;
     }
     const int64_t b = blockIdx.x;
@@ -231,8 +237,8 @@ __global__ __launch_bounds__(kPackWg) void k_sample_pack(SampleArgs sa, PackArgs
         if (threadIdx.x == 0) s_slot = d.slot;
     }
     __syncthreads();
-    const PackedRow row = pack_row(pa, b, s_slot);
-    if constexpr (GAE) gae_packed_row(ga, b, row.L, (double)row.R);
+    const PackedRow row = pack_row<NT>(pa, b, s_slot);
+    if constexpr (GAE) gae_packed_row<NT>(ga, b, row.L, (double)row.R);
 }
 
 struct PackLaunch {
@@ -241,17 +247,18 @@ struct PackLaunch {
     const GaePackedArgs* ga;  // NULL: no GAE
     DivB dv;
     hipStream_t s;
+    template <bool GAE, int PRE, int DEPTH>
+    hipError_t launch() const {
+        constexpr int NT = pack_wg<GAE>();
+        const int64_t sampler_wgs = (sa.batch + NT / kWave - 1) / (NT / kWave);
+        const dim3 grid((unsigned)(sampler_wgs + sa.batch)), block(NT);
+        hipLaunchKernelGGL((k_sample_pack<PRE, DEPTH, GAE>), grid, block, 0, s, sa, pa, ga ? *ga : GaePackedArgs{},
+                           dv, (int32_t)sampler_wgs);
+        return hipGetLastError();
+    }
     template <int PRE, int DEPTH>
     hipError_t operator()() const {
-        const int64_t sampler_wgs = (sa.batch + kPackWg / kWave - 1) / (kPackWg / kWave);
-        const dim3 grid((unsigned)(sampler_wgs + sa.batch)), block(kPackWg);
-        if (ga)
-            hipLaunchKernelGGL((k_sample_pack<PRE, DEPTH, true>), grid, block, 0, s, sa, pa, *ga, dv,
-                               (int32_t)sampler_wgs);
-        else
-            hipLaunchKernelGGL((k_sample_pack<PRE, DEPTH, false>), grid, block, 0, s, sa, pa, GaePackedArgs{}, dv,
-                               (int32_t)sampler_wgs);
-        return hipGetLastError();
+        return ga ? launch<true, PRE, DEPTH>() : launch<false, PRE, DEPTH>();
     }
 };
 
