@@ -235,3 +235,11 @@ def test_restore_rejects_images_of_other_buffers():
     assert st == cd.EINVAL
     a.close()
     target.close()
+
+
+@pytest.mark.slow
+def test_dqn_full_capacity_resumes_from_checkpoint(tmp_path):
+    print("checkpoint: dqn full size (1M slots, 7.08 GB image in HBM), resumed after the first iteration",
+          flush=True)
+    run_dqn(cap=1_000_000, prefill=1_050_000, iters=3, batch=512, chunk=4096, fused=True,
+            resume=(1, "device", cd.PLACE_HBM, str(tmp_path)))
