@@ -250,7 +250,10 @@ def bench_dqn(steps, warmup):
     assert rc == 0, cd.last_error()
     torch.cuda.synchronize()
     # timed pass: each step applies the previous step's update with its own
-    # ingest, so K steps hold K ingests, K samples + gathers and K updates
+    # ingest, so K steps hold K ingests, K samples + gathers and K updates.  A
+    # stand-in kernel queued ahead of the first event keeps the GPU busy while
+    # the host enqueues the first steps, so the events bracket GPU time only
+    _gpu_delay(1000.0)
     e_start = tm.ev()
     h0 = time.perf_counter()
     rc = 0
@@ -266,6 +269,7 @@ def bench_dqn(steps, warmup):
     p1 = warmup + steps
     rc |= step(p1)  # one untimed step first
     torch.cuda.synchronize()
+    _gpu_delay(1000.0)
     s_start = tm.ev()
     for i in range(p1 + 1, p1 + 1 + steps):
         rc |= step(i)
@@ -277,6 +281,7 @@ def bench_dqn(steps, warmup):
     p2 = p1 + 1 + steps
     rc |= step_unfused(p2)
     torch.cuda.synchronize()
+    _gpu_delay(1000.0)
     u_start = tm.ev()
     for i in range(p2 + 1, p2 + 1 + steps):
         rc |= step_unfused(i)
