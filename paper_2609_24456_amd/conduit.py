@@ -642,8 +642,9 @@ def conduit_buffer_restore(handle, src, stream=None):
 
 
 def ckpt_header(image):
-    """The header of a checkpoint image held in host memory (a uint8 tensor or bytes)."""
-    raw = bytes(image[:C.sizeof(CkptHeader)].numpy()) if isinstance(image, torch.Tensor) else bytes(image[:C.sizeof(CkptHeader)])
+    """The header of a checkpoint image (a uint8 tensor on the device or the host, or bytes)."""
+    n = C.sizeof(CkptHeader)
+    raw = bytes(image[:n].cpu().numpy()) if isinstance(image, torch.Tensor) else bytes(image[:n])
     if len(raw) < C.sizeof(CkptHeader) or raw[:8] != CKPT_MAGIC:
         raise ValueError("not a checkpoint image")
     return CkptHeader.from_buffer_copy(raw)

@@ -177,3 +177,22 @@ def test_minibatch_checks(host_tensors):
                                     cols=[z(50, dtype=torch.float32)], cols_out=[z(9, dtype=torch.float32)])
     with pytest.raises(ValueError, match="NONE, U8_F32"):
         cd.conduit_minibatch_gather(z(50, 64), 64, 50, perm, cd.transform(cd.XF_TOKENS_PAD), z(10, 64))
+
+
+def test_checkpoint_header_parser():
+    """ckpt_header reads a header from bytes or a host tensor and refuses
+    anything without the magic (the library writes the header; this is the
+    binding's reader only)."""
+    h = cd.CkptHeader()
+    h.magic = cd.CKPT_MAGIC
+    h.version, h.capacity, h.head, h.size, h.total, h.n_sections = 1, 1000, 500, 1000, 1500, 2
+    h.section[1].column, h.section[1].offset, h.section[1].bytes = cd.COL_MAX_PRIO, 1024, 4
+    raw = bytes(h) + bytes(64)
+    for img in (raw, torch.frombuffer(bytearray(raw), dtype=torch.uint8)):
+        g = cd.ckpt_header(img)
+        assert (g.capacity, g.head, g.size, g.total, g.n_sections) == (1000, 500, 1000, 1500, 2)
+        assert (g.section[1].column, g.section[1].offset, g.section[1].bytes) == (cd.COL_MAX_PRIO, 1024, 4)
+    with pytest.raises(ValueError):
+        cd.ckpt_header(b"CNDTCKP")  # shorter than a header
+    with pytest.raises(ValueError):
+        cd.ckpt_header(b"X" + raw[1:])
