@@ -64,12 +64,18 @@ typedef int32_t conduit_status;
 #define CONDUIT_EDEVICE (-4) /* a HIP runtime call failed (text in conduit_last_error) */
 #define CONDUIT_ESTATE (-5)  /* a kernel flagged bad device-side input earlier */
 
-typedef enum {
+/* Enumerations cross the ABI as int32_t (a C enum's width is the compiler's
+ * choice, and a value outside an enum's range is undefined in C++): every
+ * entry point checks the value and returns EINVAL for an unknown one. */
+
+/* observation element type */
+typedef int32_t conduit_dtype;
+enum {
     CONDUIT_U8 = 0,
     CONDUIT_I32 = 1,
     CONDUIT_F32 = 2,
     CONDUIT_BF16 = 3,
-} conduit_dtype;
+};
 
 typedef struct conduit_buffer conduit_buffer;
 
@@ -282,12 +288,14 @@ conduit_status conduit_sample(conduit_buffer* buf, int64_t batch, const uint64_t
  * from the drawn transitions and changes its layout; the processing operators
  * it lists are concat/stack, reshape, batching and padding/packing)
  * ------------------------------------------------------------------------- */
-typedef enum {
+/* transform of a gathered row */
+typedef int32_t conduit_xform_kind;
+enum {
     CONDUIT_XF_NONE = 0,        /* copy observation bytes unchanged */
     CONDUIT_XF_U8_F32 = 1,      /* uint8 x -> float x/255 (the float nearest to x/255) */
     CONDUIT_XF_U8_BF16_NORM = 2,/* uint8 x -> bf16(((x/255) - mean_c) / std_c), c = plane */
     CONDUIT_XF_TOKENS_PAD = 3,  /* ragged: right-pad sequences to max_len with pad_id */
-} conduit_xform_kind;
+};
 
 typedef struct {
     conduit_xform_kind kind;
@@ -582,7 +590,9 @@ conduit_status conduit_buffer_get_info(const conduit_buffer* buf, conduit_buffer
  */
 conduit_status conduit_buffer_stats(conduit_buffer* buf, int64_t* size, int64_t* head, uint64_t* total);
 
-typedef enum {
+/* a column of a buffer (conduit_buffer_read, checkpoint sections) */
+typedef int32_t conduit_column;
+enum {
     CONDUIT_COL_OBS = 0,      /* [capacity, row_bytes] bytes */
     CONDUIT_COL_ACTION = 1,   /* [capacity, action_bytes] */
     CONDUIT_COL_REWARD = 2,   /* float [capacity] */
@@ -594,7 +604,7 @@ typedef enum {
     CONDUIT_COL_LEAVES = 8,   /* uint32 [tree_nodes[0]] quantised priorities */
     CONDUIT_COL_TREE = 9,     /* uint64 [tree_nodes[level]] sums, level 1..tree_depth */
     CONDUIT_COL_MAX_PRIO = 10,/* uint32 [1] running maximum priority */
-} conduit_column;
+};
 
 /*
  * Copy `nbytes` bytes starting `offset` bytes into a column (level selects the
