@@ -20,5 +20,24 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_sanitized(out_dir: str) -> str:
+    """The oracle with AddressSanitizer + UndefinedBehaviorSanitizer (same
+    floating-point flags), into out_dir/_liboracle_san.so."""
+    os.makedirs(out_dir, exist_ok=True)
+    out = os.path.join(out_dir, "_liboracle_san.so")
+    cmd = ["gcc", "-O1", "-g", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",
+           "-fsanitize=address,undefined", "-fno-sanitize-recover=all", "-fno-omit-frame-pointer",
+           "-Wall", "-Wextra", "-Wno-unused-parameter", SRC, "-o", out, "-lm"]
+    subprocess.run(cmd, check=True)
+    return out
+
+
+def sanitizer_runtimes() -> str:
+    """The gcc ASan and UBSan runtimes, as an LD_PRELOAD list."""
+    libs = [subprocess.run(["gcc", f"-print-file-name={n}"], capture_output=True, text=True).stdout.strip()
+            for n in ("libasan.so", "libubsan.so")]
+    return ":".join(libs)
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
