@@ -18,6 +18,7 @@ from gpu_util import buffer_columns, dev, host, image_tensor, swap_through_check
 pytestmark = pytest.mark.gpu
 
 from paper_2609_24456_amd import conduit as cd  # noqa: E402
+from test_gpu_payloads import run_tokens  # noqa: E402
 from test_gpu_replay import _run_tiny, run_dqn  # noqa: E402
 
 
@@ -44,6 +45,15 @@ def test_dqn_run_resumes_from_checkpoint(short, update_ingest, via, tmp_path):
           flush=True)
     run_dqn(cap=4096, prefill=5000, iters=4, batch=512, chunk=1024, short_episodes=short, fused=True,
             update_ingest=update_ingest, resume=(2, via, cd.PLACE_HBM, str(tmp_path)))
+
+
+@pytest.mark.parametrize("fused,with_gae,via,placement", [(True, False, "file", cd.PLACE_HBM),
+                                                          (False, True, "pinned", cd.PLACE_HOST_PINNED)])
+def test_tokens_run_resumes_from_checkpoint(fused, with_gae, via, placement, tmp_path):
+    print(f"checkpoint: tokens cap 300 (wrapped), resumed via {via}, fused={fused}, with_gae={with_gae}",
+          flush=True)
+    run_tokens(cap=300, max_len=256, min_len=8, prefill=400, iters=3, batch=64, chunk=128, with_values=True,
+               fused=fused, with_gae=with_gae, resume=(1, via, placement, str(tmp_path)))
 
 
 def _filled(cap, obs_shape, dtype, seed, n, **kw):

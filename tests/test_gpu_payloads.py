@@ -7,7 +7,7 @@ import torch
 
 import oracle
 import synth
-from gpu_util import assert_gae_close, assert_weights_close, dev, host, read_col, tree_consistent
+from gpu_util import assert_gae_close, assert_weights_close, dev, host, read_col, swap_through_checkpoint, tree_consistent
 
 pytestmark = pytest.mark.gpu
 
@@ -70,7 +70,9 @@ def test_large_payload_full_size():
 
 
 def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values, fused=False, placement=cd.PLACE_HBM,
-               weight_norm=cd.WNORM_BATCH, with_gae=False):
+               weight_norm=cd.WNORM_BATCH, with_gae=False, resume=None):
+    """resume = (iteration, via, placement, tmp_dir): before that iteration the
+    buffer goes through a checkpoint and a restore into a new buffer."""
     cfg = synth.Tokens(prefill, max_len=max_len, min_len=min_len)
     u, prio = cfg.draws(iters, batch)
     buf = cd.ReplayBuffer(cap, (max_len,), torch.int32, action_bytes=4, ragged=True, aux_elem_bytes=4,
@@ -99,6 +101,11 @@ def run_tokens(cap, max_len, min_len, prefill, iters, batch, chunk, with_values,
     ret = torch.empty((batch, max_len), dtype=torch.float32, device="cuda")
     rng = np.random.default_rng(4)
     for it in range(iters):
+        if resume is not None and it == resume[0]:
+            buf = swap_through_checkpoint(
+                buf, resume[1], lambda: cd.ReplayBuffer(cap, (max_len,), torch.int32, action_bytes=4, ragged=True,
+                                                        aux_elem_bytes=4, placement=resume[2],
+                                                        weight_norm=weight_norm), resume[3])
         vals = rng.standard_normal((batch, max_len)).astype(np.float32) if with_values else None
         if with_gae:  # sampler + packing + GAE of the packed rows, one launch
             adv.fill_(float("nan"))
