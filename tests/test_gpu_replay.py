@@ -575,6 +575,16 @@ def test_dqn_full_capacity(fused):
 
 
 @pytest.mark.slow
+def test_dqn_many_fused_steps():
+    # 150 steps through the one-launch update + ingest and the fused sampler +
+    # gather, each checked against the oracle: the sampler's ticket hand-off
+    # over 150 launches of 64 sampler workgroups
+    print("dqn: cap 8192, short episodes, 150 fused steps with update + ingest in one call", flush=True)
+    run_dqn(cap=8192, prefill=9000, iters=150, batch=512, chunk=1024, short_episodes=True, fused=True,
+            update_ingest=True)
+
+
+@pytest.mark.slow
 def test_dqn_full_capacity_nstep_one_launch():
     print("dqn: full size cap 1M, batch + 3-step targets + bootstrap stacks in one call", flush=True)
     run_dqn(cap=1_000_000, prefill=1_050_000, iters=2, batch=512, chunk=4096, fused_nstep=(3, 0.99))
