@@ -78,3 +78,25 @@ def test_gae_is_bit_identical_across_calls(T, E):
     for a, c in res[1:]:
         assert np.array_equal(a.view(np.uint32), res[0][0].view(np.uint32))
         assert np.array_equal(c.view(np.uint32), res[0][1].view(np.uint32))
+
+
+def test_split_gae_over_many_calls():
+    # the look-back table is reused by every call (a new epoch each time): 300
+    # calls in a row, each equal bit for bit to the first
+    print("determinism: GAE [2048, 256], 300 calls back to back", flush=True)
+    T, E = 2048, 256
+    rng = np.random.default_rng(9)
+    r = dev(rng.standard_normal((T, E)).astype(np.float32))
+    v = dev(rng.standard_normal((T, E)).astype(np.float32))
+    d = dev((rng.random((T, E)) < 0.01).astype(np.uint8))
+    b = dev(rng.standard_normal(E).astype(np.float32))
+    adv0, ret0 = torch.empty((T, E), device="cuda"), torch.empty((T, E), device="cuda")
+    cd.conduit_gae(r, v, d, b, 0.99, 0.95, adv0, ret0)
+    adv, ret = torch.empty_like(adv0), torch.empty_like(ret0)
+    bad = 0
+    for _ in range(300):
+        cd.conduit_gae(r, v, d, b, 0.99, 0.95, adv, ret)
+        bad += int(not torch.equal(adv.view(torch.int32), adv0.view(torch.int32)))
+        bad += int(not torch.equal(ret.view(torch.int32), ret0.view(torch.int32)))
+    assert cd.conduit_sync_check() == cd.OK, cd.last_error()
+    assert bad == 0
