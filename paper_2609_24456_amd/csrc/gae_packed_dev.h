@@ -51,11 +51,74 @@ __device__ __forceinline__ void later_scan_step(double& P, double& S) {
 
 constexpr int kDppWaveShr1 = 0x138;  // lane i reads lane i - 1 across the whole wavefront
 
+// g^e (e >= 0) by binary exponentiation in fp64
+__device__ __forceinline__ double pow_int(double g, int64_t e) {
+    double r = 1.0;
+    for (; e; e >>= 1, g *= g)
+        if (e & 1) r *= g;
+    return r;
+}
+
+// A packed row without values (V = 0): the only non-zero TD residual is the
+// last live element's reward R, so A_t = R (gamma lambda)^(L-1-t) for t < L,
+// 0 beyond, and R_t = A_t.  Each lane takes 16-byte vectors of the row: the
+// vector's last live element from the closed form, the ones before it by the
+// recursion's own step A_t = gamma lambda A_{t+1}.  No element waits for
+// another lane: no scan, no barrier, no LDS.
+template <int NT>
+__device__ void gae_packed_row_novalue(const GaePackedArgs& a, int64_t b, int64_t L, double R) {
+    const int64_t Lmax = a.Lmax;
+    float* adv = a.adv + b * Lmax;
+    float* ret = a.ret + b * Lmax;
+    const double gl = a.gamma * a.lambda;
+    // the values of elements [t, t + 4): o[i] for t + i
+    auto quad = [&](int64_t t, f32x4& o) {
+        const int64_t hi = (t + 3 < L - 1 ? t + 3 : L - 1);  // last live element of the quad
+        double A = hi >= t ? R * pow_int(gl, L - 1 - hi) : 0.0;
+#pragma unroll
+        for (int i = 3; i >= 0; --i) {
+            if (t + i > hi) {
+                o[i] = 0.0f;
+            } else {
+                if (t + i < hi) A = gl * A;
+                o[i] = (float)A;
+            }
+        }
+    };
+    const bool vec = ((reinterpret_cast<uintptr_t>(adv) | reinterpret_cast<uintptr_t>(ret)) & 15) == 0 &&
+                     (Lmax & 3) == 0 && Lmax * 4 <= 0x7fffffffll;  // uniform
+    if (vec) {
+        const int nb = __builtin_amdgcn_readfirstlane((int)(Lmax * 4));
+        const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(adv, 0, nb, kRsrcRaw32);
+        const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(ret, 0, nb, kRsrcRaw32);
+        for (int64_t t = (int64_t)threadIdx.x * 4; t < Lmax; t += (int64_t)NT * 4) {
+            f32x4 o;
+            quad(t, o);
+            // write-through at agent scope, as the scanned path stores its rows
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), ra, (int)(t * 4), 0, kAgentScopeStore);
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, o), rr, (int)(t * 4), 0, kAgentScopeStore);
+        }
+    } else {
+        for (int64_t t = (int64_t)threadIdx.x * 4; t < Lmax; t += (int64_t)NT * 4) {
+            f32x4 o;
+            quad(t, o);
+            for (int i = 0; i < 4 && t + i < Lmax; ++i) {
+                adv[t + i] = o[i];
+                ret[t + i] = o[i];
+            }
+        }
+    }
+}
+
 // GAE of packed row b, of L live elements (0 <= L <= Lmax) with reward R on
 // the last one, by one workgroup of NT lanes (each lane a chunk of 4096 / NT
 // consecutive elements per pass).
 template <int NT>
 __device__ void gae_packed_row(const GaePackedArgs& a, int64_t b, int64_t L, double R) {
+    if (!a.value) {  // kernel argument: uniform
+        gae_packed_row_novalue<NT>(a, b, L, R);
+        return;
+    }
     static_assert(NT % kWave == 0 && kPkSeg % (4 * NT) == 0 && kPkSeg / NT <= 16, "lanes per sequence");
     constexpr int kPkChunk = kPkSeg / NT;  // elements per lane and pass
     __shared__ float sV[kPkPad];
