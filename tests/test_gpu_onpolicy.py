@@ -249,7 +249,9 @@ def test_gae_ppo_config_full_size():
 @pytest.mark.parametrize("B,Lmax,with_v", [(1, 4, False), (5, 8, True), (33, 260, True), (256, 4096, False),
                                            (64, 4096, True), (7, 4097, True), (5, 9000, True), (3, 12288, False),
                                            # rows off a 16-byte boundary and short vector tails
-                                           (9, 6, True), (6, 1001, True), (4, 4099, True)])
+                                           (9, 6, True), (6, 1001, True), (4, 4099, True),
+                                           # the same without values (the closed form's scalar stores)
+                                           (9, 6, False), (6, 1001, False), (4, 4099, False)])
 def test_gae_packed(B, Lmax, with_v):
     print(f"gae packed B={B} Lmax={Lmax}", flush=True)
     rng = np.random.default_rng(B * 7 + Lmax)
