@@ -602,15 +602,18 @@ def test_gae_termination_wins_over_truncation_and_none_is_plain_gae():
         assert np.array_equal(x[0], plain[0]) and np.array_equal(x[1], plain[1])
 
 
-def test_gae_packed_closed_form_and_padding():
+@pytest.mark.parametrize("gamma", [1.0, 0.99])
+def test_gae_packed_closed_form_and_padding(gamma):
+    # without values the only non-zero TD residual is the last element's
+    # reward: A_t = R (gamma lambda)^(L-1-t), zero in the padding
     rng = np.random.default_rng(59)
     B, Lmax, lam = 6, 50, 0.95
     length = np.array([1, 50, 7, 0, 33, 2], np.int32)
     R = rng.standard_normal(B).astype(np.float32)
-    adv, ret = oracle.gae_packed(R, length, None, Lmax, 1.0, lam)
+    adv, ret = oracle.gae_packed(R, length, None, Lmax, gamma, lam)
     for b in range(B):
         for t in range(Lmax):
-            want = lam ** (length[b] - 1 - t) * float(R[b]) if t < length[b] else 0.0
+            want = (gamma * lam) ** (length[b] - 1 - t) * float(R[b]) if t < length[b] else 0.0
             assert adv[b, t] == pytest.approx(want, rel=1e-6, abs=1e-7)
             assert ret[b, t] == adv[b, t]
 
