@@ -262,7 +262,8 @@ def test_gae_packed(B, Lmax, with_v):
         length[2] = 0
     R = rng.standard_normal(B).astype(np.float32)
     v = rng.standard_normal((B, Lmax)).astype(np.float32) if with_v else None
-    for gamma, lam in [(1.0, 0.95), (0.99, 0.9)]:
+    # gamma lambda = 0 (the degenerate cases): only the last live element keeps a non-zero advantage without values
+    for gamma, lam in [(1.0, 0.95), (0.99, 0.9), (0.0, 0.95), (0.99, 0.0)]:
         adv = torch.full((B, Lmax), np.nan, dtype=torch.float32, device="cuda")
         ret = torch.full((B, Lmax), np.nan, dtype=torch.float32, device="cuda")
         cd.conduit_gae_packed(dev(R), dev(length), dev(v) if v is not None else None, Lmax, gamma, lam, adv, ret)
